@@ -1,0 +1,215 @@
+"""CPU oracle of the ActKV compression step -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, the package smoke check and the benchmark's CPU-baseline leg may import
+this module.  It wraps ``actkv_oracle.c`` (plain C, fp64, OpenMP over independent
+(request, KV head) pairs) through ctypes.  It shares no code with the HIP library; its
+inputs are host numpy arrays (bf16 carried as uint16 bit patterns).
+
+The functions take a ``problem`` object with the attributes of a synthetic workload
+(``seq_lens``, ``q_lens``, ``budgets``, ``q``, ``kv``, ``block_table``, ``free_pages``,
+``num_q_heads``, ``num_kv_heads``, ``head_dim``, ``page_size``, ``sm_scale``,
+``pool_window``, ``causal``); any object with those attributes works.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "actkv_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+AGG = {"sum": 0, "max_mean": 1}
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, no fast-math, OpenMP)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
+                        "-o", tmp, _SRC, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [("num_reqs", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("num_pages", ctypes.c_int64),
+                ("bt_stride", ctypes.c_int32),
+                ("seq_lens", ctypes.c_void_p), ("q_lens", ctypes.c_void_p),
+                ("budgets", ctypes.c_void_p), ("sm_scale", ctypes.c_double),
+                ("pool_window", ctypes.c_int32), ("causal", ctypes.c_int32),
+                ("agg", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.POINTER(_Problem)
+        vp, i64 = ctypes.c_void_p, ctypes.c_int64
+        lib.actkv_oracle_slot.argtypes = [vp, ctypes.c_int32, i64]
+        lib.actkv_oracle_slot.restype = i64
+        lib.actkv_oracle_lse.argtypes = [P, vp, vp, vp, vp]
+        lib.actkv_oracle_scores.argtypes = [P, vp, vp, vp, vp, vp]
+        lib.actkv_oracle_pool.argtypes = [P, vp, vp]
+        lib.actkv_oracle_select.argtypes = [P, vp, vp]
+        lib.actkv_oracle_totals.argtypes = [P, ctypes.POINTER(i64), ctypes.POINTER(i64),
+                                            ctypes.POINTER(i64)]
+        lib.actkv_oracle_compact.argtypes = [P, vp, vp, vp, vp, i64, vp, vp]
+        for f in ("actkv_oracle_lse", "actkv_oracle_scores", "actkv_oracle_pool",
+                  "actkv_oracle_select", "actkv_oracle_totals", "actkv_oracle_compact"):
+            getattr(lib, f).restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+class _Bound:
+    """Keeps the numpy arrays referenced by the C struct alive."""
+
+    def __init__(self, pb, agg="sum", budgets=None, pool_window=None, causal=None,
+                 sm_scale=None):
+        self.seq = np.ascontiguousarray(pb.seq_lens, dtype=np.int32)
+        self.ql = np.ascontiguousarray(pb.q_lens, dtype=np.int32)
+        self.bud = np.ascontiguousarray(pb.budgets if budgets is None else budgets,
+                                        dtype=np.int32)
+        bt = np.asarray(pb.block_table)
+        self.st = _Problem(
+            num_reqs=self.seq.shape[0], num_q_heads=pb.num_q_heads,
+            num_kv_heads=pb.num_kv_heads, head_dim=pb.head_dim, page_size=pb.page_size,
+            num_pages=int(np.asarray(pb.kv).shape[1]), bt_stride=int(bt.shape[1]),
+            seq_lens=self.seq.ctypes.data, q_lens=self.ql.ctypes.data,
+            budgets=self.bud.ctypes.data,
+            sm_scale=float(pb.sm_scale if sm_scale is None else sm_scale),
+            pool_window=int(pb.pool_window if pool_window is None else pool_window),
+            causal=int(pb.causal if causal is None else causal), agg=AGG[agg])
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.st)
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise ValueError(f"oracle {what} rejected its arguments (rc={rc})")
+
+
+def slot(bt_row, page_size: int, t: int) -> int:
+    """Flat physical slot of logical token t (Sec. 2.5 block-table mapping)."""
+    row = np.ascontiguousarray(bt_row, dtype=np.int32)
+    return int(_load().actkv_oracle_slot(row.ctypes.data, page_size, t))
+
+
+def num_scores(pb) -> int:
+    return int(np.sum(np.asarray(pb.seq_lens, dtype=np.int64)) * pb.num_kv_heads)
+
+
+def lse(pb, **kw) -> np.ndarray:
+    """fp64 log-sum-exp of every action-query row, [sum n, Hq]."""
+    b = _Bound(pb, **kw)
+    out = np.zeros((int(b.ql.sum()), pb.num_q_heads), dtype=np.float64)
+    q = np.ascontiguousarray(pb.q, dtype=np.uint16)
+    kv = np.ascontiguousarray(pb.kv, dtype=np.uint16)
+    bt = np.ascontiguousarray(pb.block_table, dtype=np.int32)
+    _check(_load().actkv_oracle_lse(b.ref, q.ctypes.data, kv.ctypes.data, bt.ctypes.data,
+                                    out.ctypes.data), "lse")
+    return out
+
+
+def scores(pb, lse_in: Optional[np.ndarray] = None, agg: str = "sum", **kw) -> np.ndarray:
+    """Raw per-entry scores (float32, one fp64 sum rounded once), ragged [sum_r Hkv*L_r]."""
+    b = _Bound(pb, agg=agg, **kw)
+    out = np.zeros(num_scores(pb), dtype=np.float32)
+    q = np.ascontiguousarray(pb.q, dtype=np.uint16)
+    kv = np.ascontiguousarray(pb.kv, dtype=np.uint16)
+    bt = np.ascontiguousarray(pb.block_table, dtype=np.int32)
+    li = None if lse_in is None else np.ascontiguousarray(lse_in, dtype=np.float32)
+    _check(_load().actkv_oracle_scores(b.ref, q.ctypes.data, kv.ctypes.data, bt.ctypes.data,
+                                       _ptr(li), out.ctypes.data), "scores")
+    return out
+
+
+def pool(pb, raw: np.ndarray, **kw) -> np.ndarray:
+    b = _Bound(pb, **kw)
+    raw = np.ascontiguousarray(raw, dtype=np.float32)
+    out = np.zeros_like(raw)
+    _check(_load().actkv_oracle_pool(b.ref, raw.ctypes.data, out.ctypes.data), "pool")
+    return out
+
+
+def totals(pb, **kw):
+    """(entries kept, fresh pages needed, pages freed) of one step."""
+    b = _Bound(pb, **kw)
+    a, c, d = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(_load().actkv_oracle_totals(b.ref, ctypes.byref(a), ctypes.byref(c),
+                                       ctypes.byref(d)), "totals")
+    return a.value, c.value, d.value
+
+
+def select(pb, pooled: np.ndarray, **kw) -> np.ndarray:
+    """Kept token indices, ascending per (request, KV head), concatenated in (r, h) order."""
+    b = _Bound(pb, **kw)
+    nk, _, _ = totals(pb, **kw)
+    pooled = np.ascontiguousarray(pooled, dtype=np.float32)
+    out = np.zeros(max(nk, 1), dtype=np.int32)
+    _check(_load().actkv_oracle_select(b.ref, pooled.ctypes.data, out.ctypes.data), "select")
+    return out[:nk]
+
+
+def compact(pb, kept: np.ndarray, kv: Optional[np.ndarray] = None,
+            block_table: Optional[np.ndarray] = None, free_pages: Optional[np.ndarray] = None,
+            **kw):
+    """Fresh-page compaction on copies of the inputs.
+
+    Returns (kv', block_table', freed_pages, new_lens).
+    """
+    b = _Bound(pb, **kw)
+    _, need, nfreed = totals(pb, **kw)
+    kv2 = np.array(pb.kv if kv is None else kv, dtype=np.uint16, copy=True, order="C")
+    bt2 = np.array(pb.block_table if block_table is None else block_table, dtype=np.int32,
+                   copy=True, order="C")
+    fp = np.ascontiguousarray(pb.free_pages if free_pages is None else free_pages,
+                              dtype=np.int32)
+    kept = np.ascontiguousarray(kept, dtype=np.int32)
+    freed = np.zeros(max(nfreed, 1), dtype=np.int32)
+    new_lens = np.zeros(b.bud.shape[0], dtype=np.int32)
+    rc = _load().actkv_oracle_compact(b.ref, kv2.ctypes.data, bt2.ctypes.data,
+                                      kept.ctypes.data if kept.size else None,
+                                      fp.ctypes.data if fp.size else None, fp.shape[0],
+                                      freed.ctypes.data, new_lens.ctypes.data)
+    if rc == -2:
+        raise ValueError("oracle compact: free list shorter than the fresh pages needed")
+    _check(rc, "compact")
+    return kv2, bt2, freed[:nfreed], new_lens
+
+
+def step(pb, lse_in: Optional[np.ndarray] = None, agg: str = "sum", **kw) -> dict:
+    """The whole compression step on copies of the inputs; returns every intermediate."""
+    raw = scores(pb, lse_in=lse_in, agg=agg, **kw)
+    pooled = pool(pb, raw, **kw)
+    kept = select(pb, pooled, **kw)
+    kv2, bt2, freed, new_lens = compact(pb, kept, **kw)
+    return dict(raw=raw, pooled=pooled, kept=kept, kv=kv2, block_table=bt2, freed=freed,
+                new_lens=new_lens)
+
+
+def num_threads() -> int:
+    """Threads the OpenMP oracle will use (OMP_NUM_THREADS, else the CPU count)."""
+    v = os.environ.get("OMP_NUM_THREADS")
+    if v and v.isdigit() and int(v) > 0:
+        return int(v)
+    return len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()

@@ -1,0 +1,376 @@
+/*
+ * actkv_oracle.c -- plain, slow CPU oracle of the ActKV compression step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path links, loads or calls this file;
+ * only the tests, the package's smoke check and the benchmark's CPU-baseline leg do.  It
+ * shares no source, header, table or helper with the HIP library: it has its own problem
+ * struct, its own bf16 decoding and its own paged addressing.
+ *
+ * What it computes (ActKV, "Efficient LLM Agents through Action-Guided KV Cache
+ * Management"):
+ *   scores   -- for every cached entry t of request r and KV head h, the softmax attention
+ *               that the action-region queries give it (Sec. 2.3 attention definition;
+ *               Sec. 7.1 log-sum-exp and the recovery identity A = exp(s - LSE); Alg. 3).
+ *               Aggregation over the query heads of a GQA group and over the action
+ *               queries is a SUM, or (Alg. 3 / Sec. 7.1 prose) a max over the group followed
+ *               by a mean over the queries.
+ *   pool     -- an optional centred 1-D max-pool over token positions (not in the paper;
+ *               window 1 means none).
+ *   select   -- TopK(score, k = budget) per (request, KV head) (Alg. 1, step 5), ties to
+ *               the lower token index, emitted in ascending token order.
+ *   compact  -- the survivors' K/V rows are written, in ascending token order, into fresh
+ *               pages taken from a free list; the block table row is rewritten and the old
+ *               pages are returned (the freed-block return of Sec. 7.2; the paper's own
+ *               compaction is in place, Alg. 4 -- this oracle follows the fresh-page form).
+ *
+ * Every floating-point quantity is carried in double (fp64).  The raw per-entry score is
+ * rounded once to float at the end; pooling and selection then act on those float values,
+ * which is also the precision the selection is decided in on the GPU.
+ *
+ * Readings where the paper is silent (each also listed in the design notes):
+ *   - logits are sm_scale * q.k (the paper writes q.k^T with no scale);
+ *   - action query j of a request with L cached tokens and n action queries sits at
+ *     position L - n + j and, when causal, sees keys t <= L - n + j (itself included);
+ *     non-causal queries see all L keys;
+ *   - MAX_MEAN with n == 0 queries gives 0.
+ *
+ * Paged layout (Sec. 2.5): kv is [2][num_pages][page_size][Hkv][D] bf16, K at [0], V at
+ * [1]; logical token t of a request lives in physical block bt[t / page_size], slot
+ * t % page_size, so its flat slot index is bt[t / page_size] * page_size + t % page_size.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { ORACLE_AGG_SUM = 0, ORACLE_AGG_MAX_MEAN = 1 };
+
+typedef struct oracle_problem {
+  int32_t num_reqs, num_q_heads, num_kv_heads, head_dim, page_size;
+  int64_t num_pages;
+  int32_t bt_stride;
+  const int32_t* seq_lens;   /* [R] */
+  const int32_t* q_lens;     /* [R] */
+  const int32_t* budgets;    /* [R * Hkv] */
+  double sm_scale;
+  int32_t pool_window;       /* odd >= 1 */
+  int32_t causal;
+  int32_t agg;
+} oracle_problem;
+
+/* bf16 bit pattern -> value: the 16 bits are the high half of an IEEE float. */
+static double bf16_value(uint16_t bits) {
+  uint32_t u = (uint32_t)bits << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+/* Sec. 2.5 worked example: bt = [17, 9], page_size 2, tokens 0..2 -> slots 34, 35, 18. */
+int64_t actkv_oracle_slot(const int32_t* bt_row, int32_t page_size, int64_t t) {
+  return (int64_t)bt_row[t / page_size] * page_size + t % page_size;
+}
+
+static const uint16_t* kv_row(const oracle_problem* p, const uint16_t* kv, int which,
+                              int64_t slot, int h) {
+  int64_t plane = p->num_pages * (int64_t)p->page_size;
+  return kv + (((int64_t)which * plane + slot) * p->num_kv_heads + h) * p->head_dim;
+}
+
+static uint16_t* kv_row_mut(const oracle_problem* p, uint16_t* kv, int which, int64_t slot,
+                            int h) {
+  int64_t plane = p->num_pages * (int64_t)p->page_size;
+  return kv + (((int64_t)which * plane + slot) * p->num_kv_heads + h) * p->head_dim;
+}
+
+static int64_t q_offset(const oracle_problem* p, int r) {
+  int64_t off = 0;
+  for (int i = 0; i < r; ++i) off += p->q_lens[i];
+  return off;
+}
+
+static int64_t score_offset(const oracle_problem* p, int r) {
+  int64_t off = 0;
+  for (int i = 0; i < r; ++i) off += (int64_t)p->num_kv_heads * p->seq_lens[i];
+  return off;
+}
+
+static int64_t kept_offset(const oracle_problem* p, int r, int h) {
+  int64_t off = 0;
+  for (int i = 0; i < r * p->num_kv_heads + h; ++i) {
+    int64_t L = p->seq_lens[i / p->num_kv_heads];
+    int64_t b = p->budgets[i];
+    off += b < 0 ? 0 : (b > L ? L : b);
+  }
+  return off;
+}
+
+/* Position of action query j (see the readings above); keys t <= position are visible. */
+static int64_t last_visible_key(const oracle_problem* p, int r, int j) {
+  int64_t L = p->seq_lens[r], n = p->q_lens[r];
+  return p->causal ? L - n + j : L - 1;
+}
+
+/* s[t] = sm_scale * q . k_t for t = 0..last (Sec. 2.3: q_i K^T, Sec. 7.1: s_ij). */
+static void logits_row(const oracle_problem* p, const uint16_t* q_row, const uint16_t* kv,
+                       const int32_t* bt_row, int h, int64_t last, double* s) {
+  for (int64_t t = 0; t <= last; ++t) {
+    const uint16_t* k = kv_row(p, kv, 0, actkv_oracle_slot(bt_row, p->page_size, t), h);
+    double dot = 0.0;
+    for (int d = 0; d < p->head_dim; ++d) dot += bf16_value(q_row[d]) * bf16_value(k[d]);
+    s[t] = p->sm_scale * dot;
+  }
+}
+
+/* LSE = log sum_t exp(s_t) (Sec. 7.1), evaluated as m + log sum exp(s_t - m). */
+static double log_sum_exp(const double* s, int64_t count) {
+  double m = -INFINITY;
+  for (int64_t t = 0; t < count; ++t) m = s[t] > m ? s[t] : m;
+  if (count == 0) return -INFINITY;
+  double acc = 0.0;
+  for (int64_t t = 0; t < count; ++t) acc += exp(s[t] - m);
+  return m + log(acc);
+}
+
+static int check_problem(const oracle_problem* p) {
+  if (!p || p->num_reqs < 0 || p->num_kv_heads <= 0 || p->num_q_heads <= 0 ||
+      p->num_q_heads % p->num_kv_heads || p->head_dim <= 0 || p->page_size <= 0)
+    return -1;
+  for (int r = 0; r < p->num_reqs; ++r) {
+    if (p->seq_lens[r] < 0 || p->q_lens[r] < 0) return -1;
+    if (p->causal && p->q_lens[r] > p->seq_lens[r]) return -1;
+    if ((p->seq_lens[r] + p->page_size - 1) / p->page_size > p->bt_stride) return -1;
+  }
+  return 0;
+}
+
+/* lse_out[(q_offset(r) + j) * Hq + g] = log sum_{t visible to j} exp(s_t)   (Sec. 7.1). */
+int actkv_oracle_lse(const oracle_problem* p, const uint16_t* q, const uint16_t* kv,
+                     const int32_t* bt, double* lse_out) {
+  if (check_problem(p)) return -1;
+  const int Hq = p->num_q_heads, G = p->num_q_heads / p->num_kv_heads, D = p->head_dim;
+  for (int r = 0; r < p->num_reqs; ++r) {
+    const int64_t qoff = q_offset(p, r);
+    const int n = p->q_lens[r];
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int row = 0; row < n * Hq; ++row) {
+      const int j = row / Hq, g = row % Hq;
+      const int64_t last = last_visible_key(p, r, j);
+      double* s = (double*)malloc(sizeof(double) * (size_t)(last + 1 > 0 ? last + 1 : 1));
+      logits_row(p, q + ((qoff + j) * Hq + g) * D, kv, bt + (int64_t)r * p->bt_stride, g / G,
+                 last, s);
+      lse_out[(qoff + j) * Hq + g] = log_sum_exp(s, last + 1);
+      free(s);
+    }
+  }
+  return 0;
+}
+
+/*
+ * raw_out[score_offset(r) + h * L_r + t]:
+ *   SUM:      sum_{g in group(h)} sum_{j : t visible} exp(s_{j,g,t} - LSE_{j,g})
+ *   MAX_MEAN: (1/n) sum_{j : t visible} max_{g in group(h)} exp(s_{j,g,t} - LSE_{j,g})
+ * LSE is taken from lse_in (float, [sum n][Hq]) when given -- the recovery of Sec. 7.1 --
+ * and otherwise computed here from its definition.  Each value is rounded to float once.
+ */
+int actkv_oracle_scores(const oracle_problem* p, const uint16_t* q, const uint16_t* kv,
+                        const int32_t* bt, const float* lse_in, float* raw_out) {
+  if (check_problem(p)) return -1;
+  const int Hq = p->num_q_heads, Hkv = p->num_kv_heads, G = Hq / Hkv, D = p->head_dim;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int rh = 0; rh < p->num_reqs * Hkv; ++rh) {
+    const int r = rh / Hkv, h = rh % Hkv;
+    const int64_t L = p->seq_lens[r], qoff = q_offset(p, r), soff = score_offset(p, r);
+    const int n = p->q_lens[r];
+    {
+      double* acc = (double*)calloc((size_t)(L > 0 ? L : 1), sizeof(double));
+      double* s = (double*)malloc(sizeof(double) * (size_t)(L > 0 ? L : 1));
+      double* mx = (double*)malloc(sizeof(double) * (size_t)(L > 0 ? L : 1));
+      for (int j = 0; j < n; ++j) {
+        const int64_t last = last_visible_key(p, r, j);
+        for (int64_t t = 0; t <= last; ++t) mx[t] = 0.0;
+        for (int gi = 0; gi < G; ++gi) {
+          const int g = h * G + gi;
+          logits_row(p, q + ((qoff + j) * Hq + g) * D, kv, bt + (int64_t)r * p->bt_stride, h,
+                     last, s);
+          const double lse = lse_in ? (double)lse_in[(qoff + j) * Hq + g]
+                                    : log_sum_exp(s, last + 1);
+          for (int64_t t = 0; t <= last; ++t) {
+            const double a = exp(s[t] - lse);   /* A_{j,t} = exp(s - LSE), Sec. 7.1 */
+            if (p->agg == ORACLE_AGG_SUM) acc[t] += a;
+            else mx[t] = a > mx[t] ? a : mx[t];
+          }
+        }
+        if (p->agg == ORACLE_AGG_MAX_MEAN)
+          for (int64_t t = 0; t <= last; ++t) acc[t] += mx[t];
+      }
+      for (int64_t t = 0; t < L; ++t) {
+        double v = acc[t];
+        if (p->agg == ORACLE_AGG_MAX_MEAN) v = n > 0 ? v / n : 0.0;
+        raw_out[soff + h * L + t] = (float)v;
+      }
+      free(acc);
+      free(s);
+      free(mx);
+    }
+  }
+  return 0;
+}
+
+/* pooled[t] = max raw[u] over |u - t| <= w/2, 0 <= u < L, per (request, KV head). */
+int actkv_oracle_pool(const oracle_problem* p, const float* raw, float* pooled) {
+  if (check_problem(p) || p->pool_window < 1 || p->pool_window % 2 == 0) return -1;
+  const int half = p->pool_window / 2;
+  for (int r = 0; r < p->num_reqs; ++r) {
+    const int64_t L = p->seq_lens[r], soff = score_offset(p, r);
+    for (int h = 0; h < p->num_kv_heads; ++h) {
+      const float* in = raw + soff + h * L;
+      float* out = pooled + soff + h * L;
+      for (int64_t t = 0; t < L; ++t) {
+        float m = in[t];
+        for (int64_t u = t - half; u <= t + half; ++u)
+          if (u >= 0 && u < L && in[u] > m) m = in[u];
+        out[t] = m;
+      }
+    }
+  }
+  return 0;
+}
+
+typedef struct { float v; int32_t t; } scored_entry;
+
+/* Descending score, then ascending token index: the order TopK keeps. */
+static int by_score_then_index(const void* a, const void* b) {
+  const scored_entry* x = (const scored_entry*)a;
+  const scored_entry* y = (const scored_entry*)b;
+  if (x->v > y->v) return -1;
+  if (x->v < y->v) return 1;
+  return (x->t > y->t) - (x->t < y->t);
+}
+
+static int ascending_int(const void* a, const void* b) {
+  int32_t x = *(const int32_t*)a, y = *(const int32_t*)b;
+  return (x > y) - (x < y);
+}
+
+/* kept[kept_offset(r,h) ...] = the min(max(B,0), L) best entries of (r,h), ascending. */
+int actkv_oracle_select(const oracle_problem* p, const float* pooled, int32_t* kept) {
+  if (check_problem(p)) return -1;
+  for (int r = 0; r < p->num_reqs; ++r) {
+    const int64_t L = p->seq_lens[r], soff = score_offset(p, r);
+    for (int h = 0; h < p->num_kv_heads; ++h) {
+      int64_t k = p->budgets[r * p->num_kv_heads + h];
+      if (k < 0) return -1;
+      if (k > L) k = L;
+      scored_entry* e = (scored_entry*)malloc(sizeof(scored_entry) * (size_t)(L > 0 ? L : 1));
+      for (int64_t t = 0; t < L; ++t) {
+        float v = pooled[soff + h * L + t];
+        e[t].v = v == 0.0f ? 0.0f : v;   /* -0 and +0 compare equal; keep one spelling */
+        e[t].t = (int32_t)t;
+      }
+      qsort(e, (size_t)L, sizeof(scored_entry), by_score_then_index);
+      int32_t* out = kept + kept_offset(p, r, h);
+      for (int64_t i = 0; i < k; ++i) out[i] = e[i].t;
+      qsort(out, (size_t)k, sizeof(int32_t), ascending_int);
+      free(e);
+    }
+  }
+  return 0;
+}
+
+/* Host-side totals of one step: entries kept, fresh pages needed, pages freed. */
+int actkv_oracle_totals(const oracle_problem* p, int64_t* num_kept, int64_t* fresh_needed,
+                        int64_t* pages_freed) {
+  if (check_problem(p)) return -1;
+  int64_t nk = 0, fresh = 0, freed = 0;
+  for (int r = 0; r < p->num_reqs; ++r) {
+    const int64_t L = p->seq_lens[r];
+    int64_t kmax = 0, bmin = INT64_MAX;
+    for (int h = 0; h < p->num_kv_heads; ++h) {
+      int64_t b = p->budgets[r * p->num_kv_heads + h];
+      if (b < 0) return -1;
+      int64_t k = b > L ? L : b;
+      nk += k;
+      kmax = k > kmax ? k : kmax;
+      bmin = b < bmin ? b : bmin;
+    }
+    if (bmin >= L) continue;   /* every head keeps everything: request left untouched */
+    fresh += (kmax + p->page_size - 1) / p->page_size;
+    freed += (L + p->page_size - 1) / p->page_size;
+  }
+  *num_kept = nk;
+  *fresh_needed = fresh;
+  *pages_freed = freed;
+  return 0;
+}
+
+/*
+ * Fresh-page compaction.  Requests in order; a request whose every head keeps all its
+ * entries is skipped (block table row, pages and lengths untouched).  Otherwise, with
+ * X = ceil(max_h k_h / page_size) and Y = ceil(L / page_size):
+ *   fresh    = free_pages[off .. off + X), off advancing over the requests in order;
+ *   for each head h and j < k_h the K and V rows of token kept[j] are copied bit for bit
+ *   to page fresh[j / page_size], slot j % page_size;
+ *   freed_out gets the old bt[r, 0 .. Y) (request order);
+ *   bt[r, 0 .. X) = fresh, bt[r, X .. Y) = -1;  new_lens[r, h] = k_h.
+ * Slots of fresh pages at or beyond k_h (for head h) are not written.
+ */
+int actkv_oracle_compact(const oracle_problem* p, uint16_t* kv, int32_t* bt,
+                         const int32_t* kept, const int32_t* free_pages, int64_t num_free,
+                         int32_t* freed_out, int32_t* new_lens) {
+  if (check_problem(p)) return -1;
+  int64_t nk, need, nfreed;
+  if (actkv_oracle_totals(p, &nk, &need, &nfreed)) return -1;
+  if (need > num_free) return -2;
+  const int Hkv = p->num_kv_heads, D = p->head_dim, BS = p->page_size;
+  int64_t fresh_off = 0, freed_off = 0;
+  for (int r = 0; r < p->num_reqs; ++r) {
+    const int64_t L = p->seq_lens[r];
+    int32_t* row = bt + (int64_t)r * p->bt_stride;
+    int64_t kmax = 0, bmin = INT64_MAX;
+    for (int h = 0; h < Hkv; ++h) {
+      int64_t b = p->budgets[r * Hkv + h];
+      int64_t k = b > L ? L : b;
+      kmax = k > kmax ? k : kmax;
+      bmin = b < bmin ? b : bmin;
+    }
+    if (bmin >= L) {
+      for (int h = 0; h < Hkv; ++h) new_lens[r * Hkv + h] = (int32_t)L;
+      continue;
+    }
+    const int64_t X = (kmax + BS - 1) / BS, Y = (L + BS - 1) / BS;
+    const int32_t* fresh = free_pages + fresh_off;
+    int32_t* old_pages = freed_out + freed_off;
+    for (int64_t i = 0; i < Y; ++i) old_pages[i] = row[i];
+    for (int h = 0; h < Hkv; ++h) {
+      int64_t b = p->budgets[r * Hkv + h];
+      int64_t k = b > L ? L : b;
+      const int32_t* idx = kept + kept_offset(p, r, h);
+      for (int64_t j = 0; j < k; ++j) {
+        const int64_t src = actkv_oracle_slot(old_pages, BS, idx[j]);
+        const int64_t dst = (int64_t)fresh[j / BS] * BS + j % BS;
+        for (int which = 0; which < 2; ++which)
+          memcpy(kv_row_mut(p, kv, which, dst, h), kv_row(p, kv, which, src, h),
+                 sizeof(uint16_t) * (size_t)D);
+      }
+      new_lens[r * Hkv + h] = (int32_t)k;
+    }
+    for (int64_t i = 0; i < Y; ++i) row[i] = i < X ? fresh[i] : -1;
+    fresh_off += X;
+    freed_off += Y;
+  }
+  return 0;
+}
+
+/* The whole step: scores -> pool -> select -> compact, each as defined above. */
+int actkv_oracle_step(const oracle_problem* p, const uint16_t* q, uint16_t* kv, int32_t* bt,
+                      const float* lse_in, const int32_t* free_pages, int64_t num_free,
+                      float* raw_out, float* pooled_out, int32_t* kept_out,
+                      int32_t* freed_out, int32_t* new_lens) {
+  int rc = actkv_oracle_scores(p, q, kv, bt, lse_in, raw_out);
+  if (!rc) rc = actkv_oracle_pool(p, raw_out, pooled_out);
+  if (!rc) rc = actkv_oracle_select(p, pooled_out, kept_out);
+  if (!rc) rc = actkv_oracle_compact(p, kv, bt, kept_out, free_pages, num_free, freed_out,
+                                     new_lens);
+  return rc;
+}

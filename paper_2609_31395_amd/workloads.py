@@ -1,0 +1,261 @@
+"""Seeded synthetic inputs for the ActKV compression step (score -> select -> compact).
+
+This module only *draws* inputs: Gaussian Q/K/V rounded to bf16, planted spike keys,
+a shuffled physical page pool with its block table and free list, per-(request, KV head)
+budgets and the scoring flags.  None of the method's arithmetic (logits, softmax, scores,
+pooling, selection, compaction) lives here, so the CPU oracle and the HIP path can both
+consume these arrays without sharing any of that code.
+
+The paper's evaluation runs agent traces from ALFWorld, HotpotQA-Web and WebShop on
+Qwen3 / GPT-OSS models (Sec. 8.1).  None of those traces or weights are used: the
+workloads below are synthetic stand-ins with the head shapes of Qwen3-30B
+(32 query heads, 4 KV heads, head_dim 128, 16-token pages), the trace lengths the paper
+reports (about 35K tokens for a 25-iteration WebShop task, Sec. 1; mean FullKV lengths
+8K-33K, Sec. 8.1) and the page-pool layout of Sec. 2.5.
+
+Recipe (all draws from numpy PCG64, one child stream per request via SeedSequence.spawn):
+  * Q, K, V ~ N(0, 1) in float32, rounded to bf16 (round-to-nearest-even).
+  * Spike keys: per (request, KV head) ``round(spike_frac * L)`` distinct token indices;
+    their K row (before rounding) gets ``+ 3 * mean`` where ``mean`` is the average of that
+    request's bf16 action queries over the G query heads that share the KV head.
+  * Pages: the pool holds ``pool_factor`` times the pages in use (or a fixed count), is
+    shuffled by a seeded permutation; each request takes its pages in logical order from
+    the permutation, the rest form the free list.
+  * Budgets: a fixed count, a fraction of L, or a Dirichlet(alpha) split of a fraction of
+    ``Hkv * L`` across the KV heads of a request (floor; never above L).
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+PAGE_SIZE = 16
+
+
+@dataclass(frozen=True)
+class WorkloadConfig:
+    name: str
+    num_reqs: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    seq_len: Tuple[int, int]      # inclusive range; lo == hi for a fixed length
+    q_len: Tuple[int, int]        # inclusive range of action queries per request
+    budget: Tuple                 # ("fixed", B) | ("frac", f) | ("dirichlet", alpha, f)
+    pool_window: int
+    spike_frac: float
+    seed: int
+    pool_factor: float = 2.0
+    fixed_pool_pages: Optional[int] = None
+    causal: bool = True
+    description: str = ""
+
+
+CONFIGS: Dict[str, WorkloadConfig] = {
+    "tiny": WorkloadConfig(
+        "tiny", 1, 8, 2, 64, (2048, 2048), (16, 16), ("fixed", 512), 5, 0.02, 1001,
+        fixed_pool_pages=256,
+        description="1 request, 8q/2kv heads, d=64, 2048 tokens in 128 of 256 shuffled "
+                    "pages, 16 action queries, 2% spikes, pool 5, budget 512 per KV head"),
+    "single35k": WorkloadConfig(
+        "single35k", 1, 32, 4, 128, (35000, 35000), (64, 64), ("frac", 0.25), 7, 0.01, 1002,
+        description="1 request, Qwen3-30B heads (32q/4kv, d=128), 35,000 tokens, "
+                    "64 action queries, 1% spikes, pool 7, budget 25% per KV head"),
+    "batched": WorkloadConfig(
+        "batched", 32, 32, 4, 128, (8000, 40000), (32, 128), ("frac", 0.25), 7, 0.01, 1003,
+        description="32 requests, Qwen3-30B heads, L ~ U[8000, 40000], 32-128 action "
+                    "queries, 1% spikes, pool 7, budget 25% per KV head"),
+    "adaptive": WorkloadConfig(
+        "adaptive", 32, 32, 4, 128, (8000, 40000), (32, 128), ("dirichlet", 0.5, 0.25), 7,
+        0.01, 1004,
+        description="as 'batched' with per-(request, KV head) budgets from a "
+                    "Dirichlet(0.5) split of 25% of Hkv*L"),
+    "batch32x35k": WorkloadConfig(
+        "batch32x35k", 32, 32, 4, 128, (35000, 35000), (64, 64), ("frac", 0.25), 7, 0.01, 1006,
+        description="32 requests x 35,000 tokens, Qwen3-30B heads (32q/4kv, d=128), "
+                    "64 action queries each, 1% spikes, pool 7, budget 25% per KV head"),
+}
+
+
+@dataclass
+class Problem:
+    """Host-side (numpy) inputs of one compression step over one layer."""
+    cfg_name: str
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    page_size: int
+    seq_lens: np.ndarray          # int32 [R]
+    q_lens: np.ndarray            # int32 [R]
+    budgets: np.ndarray           # int32 [R * Hkv]
+    q: np.ndarray                 # uint16 (bf16 bits) [sum n, Hq, D]
+    kv: np.ndarray                # uint16 (bf16 bits) [2, P, page_size, Hkv, D]
+    block_table: np.ndarray       # int32 [R, bt_stride], -1 past each request's pages
+    free_pages: np.ndarray        # int32 [num_free]
+    sm_scale: float               # float32 value
+    pool_window: int
+    causal: bool
+    k_dense: List[np.ndarray] = field(default_factory=list)   # per request uint16 [L, Hkv, D]
+    v_dense: List[np.ndarray] = field(default_factory=list)
+    spikes: List[List[np.ndarray]] = field(default_factory=list)  # [r][h] -> token indices
+
+    @property
+    def num_reqs(self) -> int:
+        return int(self.seq_lens.shape[0])
+
+    @property
+    def num_pages(self) -> int:
+        return int(self.kv.shape[1])
+
+    @property
+    def bt_stride(self) -> int:
+        return int(self.block_table.shape[1])
+
+    @property
+    def cu_q(self) -> np.ndarray:
+        return np.concatenate([[0], np.cumsum(self.q_lens, dtype=np.int64)])
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bit pattern (uint16), round to nearest even (finite inputs)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_to_f32(b: np.ndarray) -> np.ndarray:
+    """bf16 bit pattern (uint16) -> float32 (exact)."""
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _draw_lengths(rng, cfg: WorkloadConfig):
+    lo, hi = cfg.seq_len
+    L = rng.integers(lo, hi + 1, size=cfg.num_reqs).astype(np.int32)
+    qlo, qhi = cfg.q_len
+    n = rng.integers(qlo, qhi + 1, size=cfg.num_reqs).astype(np.int32)
+    return L, n
+
+
+def _draw_budgets(rng, cfg: WorkloadConfig, L: np.ndarray) -> np.ndarray:
+    R, H = cfg.num_reqs, cfg.num_kv_heads
+    kind = cfg.budget[0]
+    if kind == "fixed":
+        b = np.full((R, H), cfg.budget[1], dtype=np.int64)
+    elif kind == "frac":
+        b = np.repeat(np.floor(cfg.budget[1] * L.astype(np.float64))[:, None], H, axis=1)
+    elif kind == "dirichlet":
+        alpha, frac = cfg.budget[1], cfg.budget[2]
+        w = rng.dirichlet(np.full(H, alpha), size=R)
+        b = np.floor(w * H * frac * L.astype(np.float64)[:, None])
+        b = np.minimum(b, L[:, None])
+    else:
+        raise ValueError(kind)
+    return b.astype(np.int32).reshape(-1)
+
+
+def make_problem(name: str, *, seed: Optional[int] = None, overrides: Optional[dict] = None,
+                 keep_dense: bool = True) -> Problem:
+    """Draw the inputs of workload ``name`` (see CONFIGS), optionally overriding fields."""
+    cfg = CONFIGS[name]
+    if overrides:
+        cfg = WorkloadConfig(**{**cfg.__dict__, **overrides})
+    return make_problem_from_config(cfg, seed=seed, keep_dense=keep_dense)
+
+
+def make_problem_from_config(cfg: WorkloadConfig, *, seed: Optional[int] = None,
+                             keep_dense: bool = True) -> Problem:
+    ss = np.random.SeedSequence(cfg.seed if seed is None else seed)
+    meta_ss, page_ss, budget_ss, *req_ss = ss.spawn(3 + cfg.num_reqs)
+    if cfg.num_q_heads % cfg.num_kv_heads:
+        raise ValueError("num_q_heads must be a multiple of num_kv_heads")
+    L, n = _draw_lengths(np.random.Generator(np.random.PCG64(meta_ss)), cfg)
+    budgets = _draw_budgets(np.random.Generator(np.random.PCG64(budget_ss)), cfg, L)
+    used = int(((L.astype(np.int64) + PAGE_SIZE - 1) // PAGE_SIZE).sum())
+    P = cfg.fixed_pool_pages if cfg.fixed_pool_pages is not None else \
+        max(used + 1, int(math.ceil(cfg.pool_factor * used)))
+    perm = np.random.Generator(np.random.PCG64(page_ss)).permutation(P).astype(np.int32)
+    return _assemble(cfg.name, L, n, budgets, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim,
+                     cfg.spike_frac, perm, req_ss, cfg.pool_window, cfg.causal, keep_dense)
+
+
+def make_custom(*, seq_lens, q_lens, num_q_heads, num_kv_heads, head_dim, budgets,
+                pool_window=1, spike_frac=0.0, seed=0, pool_factor=2.0, causal=True,
+                identity_pages=False, extra_pool_pages=0) -> Problem:
+    """Small hand-shaped problems for tests: explicit lengths and budgets.
+
+    ``budgets`` is an int, or an array of R*Hkv ints.  With ``identity_pages`` the pages of
+    the requests are laid out contiguously in logical order (no shuffle).
+    """
+    seq_lens = np.asarray(seq_lens, dtype=np.int32).reshape(-1)
+    q_lens = np.asarray(q_lens, dtype=np.int32).reshape(-1)
+    R = seq_lens.shape[0]
+    ss = np.random.SeedSequence(seed)
+    page_ss, *req_ss = ss.spawn(1 + R)
+    b = np.asarray(budgets, dtype=np.int64)
+    b = np.full(R * num_kv_heads, int(b)) if b.ndim == 0 else b.reshape(-1)
+    used = int(((seq_lens.astype(np.int64) + PAGE_SIZE - 1) // PAGE_SIZE).sum())
+    P = max(used + 1, int(math.ceil(pool_factor * used))) + extra_pool_pages
+    if identity_pages:
+        perm = np.arange(P, dtype=np.int32)
+    else:
+        perm = np.random.Generator(np.random.PCG64(page_ss)).permutation(P).astype(np.int32)
+    return _assemble("custom", seq_lens, q_lens, b.astype(np.int32), num_q_heads, num_kv_heads,
+                     head_dim, spike_frac, perm, req_ss, pool_window, causal, True)
+
+
+def _assemble(name, L, n, budgets, Hq, Hkv, D, spike_frac, perm, req_ss, pool_window, causal,
+              keep_dense) -> Problem:
+    """Draw Q/K/V per request, plant spikes, and scatter K/V into the shuffled page pool."""
+    BS = PAGE_SIZE
+    R = int(L.shape[0])
+    G = Hq // Hkv
+    Y = (L.astype(np.int64) + BS - 1) // BS
+    used = int(Y.sum())
+    P = int(perm.shape[0])
+    if P < used:
+        raise ValueError("page pool smaller than the pages in use")
+    bt_stride = int(max(1, Y.max(initial=0)))
+    block_table = np.full((R, bt_stride), -1, dtype=np.int32)
+    kv = np.zeros((2, P, BS, Hkv, D), dtype=np.uint16)
+    q_all = np.empty((int(n.sum()), Hq, D), dtype=np.uint16)
+    k_dense, v_dense, spikes = [], [], []
+    off_page, off_q = 0, 0
+    for r in range(R):
+        rng = np.random.Generator(np.random.PCG64(req_ss[r]))
+        Lr, nr, Yr = int(L[r]), int(n[r]), int(Y[r])
+        q = bf16_bits(rng.standard_normal((nr, Hq, D), dtype=np.float32))
+        k = rng.standard_normal((Lr, Hkv, D), dtype=np.float32)
+        v = rng.standard_normal((Lr, Hkv, D), dtype=np.float32)
+        qf = bf16_to_f32(q).astype(np.float64)
+        sp_r = []
+        for h in range(Hkv):
+            cnt = int(round(spike_frac * Lr))
+            idx = np.sort(rng.choice(Lr, size=cnt, replace=False)) if cnt > 0 else \
+                np.zeros(0, dtype=np.int64)
+            if cnt > 0 and nr > 0:
+                mean = qf[:, h * G:(h + 1) * G, :].reshape(-1, D).mean(axis=0)
+                k[idx, h, :] += (3.0 * mean).astype(np.float32)
+            sp_r.append(idx.astype(np.int32))
+        kb, vb = bf16_bits(k), bf16_bits(v)
+        pages = perm[off_page:off_page + Yr]
+        block_table[r, :Yr] = pages
+        pad = Yr * BS - Lr
+        if Yr:
+            zpad = np.zeros((pad, Hkv, D), np.uint16)
+            kv[0, pages] = np.concatenate([kb, zpad]).reshape(Yr, BS, Hkv, D)
+            kv[1, pages] = np.concatenate([vb, zpad]).reshape(Yr, BS, Hkv, D)
+        q_all[off_q:off_q + nr] = q
+        off_page += Yr
+        off_q += nr
+        if keep_dense:
+            k_dense.append(kb)
+            v_dense.append(vb)
+        spikes.append(sp_r)
+    free_pages = perm[used:].copy()
+    sm_scale = float(np.float32(1.0) / np.sqrt(np.float32(D)))
+    return Problem(name, Hq, Hkv, D, BS, L.astype(np.int32), n.astype(np.int32),
+                   budgets.astype(np.int32), q_all, kv, block_table, free_pages, sm_scale,
+                   int(pool_window), bool(causal), k_dense, v_dense, spikes)
