@@ -1,0 +1,181 @@
+/*
+ * actkv.h -- C ABI of libactkv, the MI355X (gfx950) library for the compression step of
+ * ActKV's action-oriented KV-cache eviction ("ActKV: Efficient LLM Agents through
+ * Action-Guided KV Cache Management").
+ *
+ * The step standardises compression into three primitives (Sec. 3.3):
+ *     AttnScore <- CalAttn(target queries, K cache)          actkv_score
+ *     KeepMask  <- Eviction(AttnScore, Budget)               actkv_select
+ *     KVCache   <- Compaction(KVCache, KeepMask)             actkv_compact
+ * and actkv_step runs all three back to back on one stream.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers are DEVICE pointers unless the name ends in _h (host memory).
+ *  - bf16 tensors are passed as void* and hold IEEE bfloat16 values.
+ *  - The paged cache (Sec. 2.5) is bf16 kv_cache[2][num_pages][page_size][num_kv_heads]
+ *    [head_dim]: index 0 holds K, index 1 holds V.  Logical token t of request r lives in
+ *    physical page block_table[r * bt_stride + t / page_size], slot t % page_size.
+ *  - Query head g belongs to KV head g / G, G = num_q_heads / num_kv_heads (GQA groups,
+ *    Alg. 3 input GQAGroup).
+ *  - Action query j of request r (0 <= j < q_lens[r]) is row (sum_{r'<r} q_lens[r'] + j)
+ *    of q; it sits at token position seq_lens[r] - q_lens[r] + j and, when causal, sees
+ *    keys t <= that position.  Non-causal queries see all seq_lens[r] keys.
+ *  - Scores are one fp32 per (request, KV head, token), ragged and concatenated in
+ *    (r, h, t) order: request r's head h segment starts at Hkv * sum_{r'<r} L_r' + h * L_r.
+ *  - Kept indices are int32 token indices, ascending within each (request, KV head),
+ *    concatenated in (r, h) order; segment (r, h) holds k_rh = min(budget_rh, L_r)
+ *    entries.
+ *  - Ownership: the caller owns every buffer, including the workspace whose size
+ *    actkv_query reports.  The library allocates and frees nothing, keeps no pointer after
+ *    a call returns and has no mutable global state: calls are reentrant.
+ *  - Asynchrony: each call validates its arguments on the host, then enqueues kernels on
+ *    `stream` (a hipStream_t; NULL is the default stream) and returns without
+ *    synchronising.  Outputs are valid once the stream reaches that point.
+ *  - Errors: every argument error is detected on the host before anything is enqueued,
+ *    and then nothing is written.  ACTKV_ERR_HIP reports a failed kernel launch.  Faults
+ *    inside kernels surface at the caller's next synchronisation.
+ *  - Undefined behaviour: non-finite q or K, block-table entries outside
+ *    [0, num_pages) for live tokens, device mirrors that disagree with the host mirrors,
+ *    fresh pages that are still live, and buffers that overlap where the text says they
+ *    must not.
+ */
+#ifndef ACTKV_H
+#define ACTKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum actkv_status {
+  ACTKV_OK = 0,
+  ACTKV_ERR_INVALID_ARGUMENT = -1,    /* shapes, lengths, flags or pointers out of contract */
+  ACTKV_ERR_UNSUPPORTED = -2,         /* valid request this build does not handle          */
+  ACTKV_ERR_WORKSPACE_TOO_SMALL = -3, /* workspace_bytes below actkv_query's figure        */
+  ACTKV_ERR_OUT_OF_PAGES = -4,        /* free list shorter than the fresh pages needed     */
+  ACTKV_ERR_HIP = -5                  /* a HIP launch or runtime call failed               */
+} actkv_status;
+
+typedef enum actkv_agg {
+  /* sum over the G query heads of a KV head and over the action queries */
+  ACTKV_AGG_SUM = 0,
+  /* max over the G query heads, mean over the action queries (Alg. 3 steps 4-5 and the
+   * running mean of Sec. 7.1); needs G in {1, 2, 4, 8, 16} */
+  ACTKV_AGG_MAX_MEAN = 1
+} actkv_agg;
+
+/*
+ * One compression step over one layer for a batch of requests (Alg. 3 inputs Q,
+ * PagedKV, BlockTable, LSE, GQAGroup, ActionReq; Alg. 4 inputs SeqUsedK, B, BlockSize;
+ * Alg. 1 input B).  The batch passed in IS the set of requests being compressed.
+ */
+typedef struct actkv_problem {
+  int32_t num_reqs;         /* R >= 0                                                    */
+  int32_t num_q_heads;      /* Hq > 0, a multiple of num_kv_heads                        */
+  int32_t num_kv_heads;     /* Hkv > 0                                                   */
+  int32_t head_dim;         /* D: 64 or 128                                              */
+  int32_t page_size;        /* slots per page: 16                                        */
+  int64_t num_pages;        /* physical pages in kv_cache                                */
+  int32_t bt_stride;        /* block_table row stride (int32 elements), >= every
+                               ceil(seq_lens[r] / page_size)                             */
+  const int32_t* seq_lens_h;  /* host [R]: cached tokens L_r >= 0 (SeqUsedK)             */
+  const int32_t* q_lens_h;    /* host [R]: action queries n_r >= 0 (<= L_r when causal)  */
+  const int32_t* budgets_h;   /* host [R * Hkv]: entries to keep per (r, h), >= 0        */
+  const int32_t* seq_lens_d;  /* device mirror of seq_lens_h                             */
+  const int32_t* q_lens_d;    /* device mirror of q_lens_h                               */
+  const int32_t* budgets_d;   /* device mirror of budgets_h                              */
+  float sm_scale;           /* logits are sm_scale * q.k; 0 selects 1 / sqrt(head_dim)   */
+  int32_t pool_window;      /* odd, 1..63: centred max-pool width over token positions;
+                               1 = no pooling                                            */
+  int32_t causal;           /* 1: causal visibility (see conventions), 0: all keys       */
+  int32_t agg;              /* actkv_agg                                                 */
+} actkv_problem;
+
+/*
+ * Host-only planning: no GPU work, callable without a device.  Reports the workspace
+ * size the other calls need for `p` (the maximum over them, so one workspace serves
+ * every entry point), the number of kept entries sum_{r,h} min(budget, L_r), the fresh
+ * pages compaction pops from the free list (sum over compacted requests of
+ * ceil(max_h k_rh / page_size)) and the pages it returns (sum of ceil(L_r / page_size)
+ * over compacted requests).  A request whose every head has budget >= L_r is left
+ * untouched by compaction.  Any output pointer may be NULL.
+ */
+actkv_status actkv_query(const actkv_problem* p, size_t* workspace_bytes, int64_t* num_kept,
+                         int64_t* fresh_pages_needed, int64_t* pages_freed);
+
+/*
+ * Log-sum-exp of every action-query row (Sec. 7.1: LSE = log sum_j exp(s_ij) over the
+ * keys the query sees), the normaliser a paged-attention backend produces as a
+ * by-product.  q: bf16 [sum n][Hq][D]; lse_out: fp32 [sum n][Hq], natural log.
+ */
+actkv_status actkv_lse(const actkv_problem* p, const void* q, const void* kv_cache,
+                       const int32_t* block_table, float* lse_out, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/*
+ * Recovery-based attention scoring (Sec. 7.1, Alg. 3): for every cached entry t of
+ * request r and KV head h,
+ *   SUM:      scores = sum_{g in group(h)} sum_{j sees t} exp(sm_scale q_jg . k_t - LSE_jg)
+ *   MAX_MEAN: scores = (1/n_r) sum_{j sees t} max_{g in group(h)} exp(...)
+ * lse: fp32 [sum n][Hq] natural-log LSE over the same keys and scale (the paper's input),
+ * or NULL to have the library compute it first (actkv_lse into the workspace).
+ * scores: fp32, ragged (see conventions).
+ */
+actkv_status actkv_score(const actkv_problem* p, const void* q, const void* kv_cache,
+                         const int32_t* block_table, const float* lse, float* scores,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Eviction (Alg. 1 step 5, TopK(score, k = B)): per (request, KV head) the
+ * k_rh = min(budget_rh, L_r) entries with the largest pooled score are kept, ties going
+ * to the lower token index, and written ascending into `kept` ([num_kept] int32).
+ * pooled (nullable): fp32, same layout as scores, receives the max-pooled scores
+ * (pool_window 1 copies them).  scores is not modified.
+ */
+actkv_status actkv_select(const actkv_problem* p, const float* scores, float* pooled,
+                          int32_t* kept, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+/*
+ * Fresh-page compaction (the compaction primitive of Sec. 3.3 with the freed-block
+ * return of Sec. 7.2).  For each request in order that is not left untouched, with
+ * X = ceil(max_h k_rh / page_size) and Y = ceil(L_r / page_size):
+ *   fresh = free_pages[off .. off + X), off advancing over the compacted requests;
+ *   for every head h and j < k_rh, the K and V rows of token kept[j] are copied bit for
+ *   bit to page fresh[j / page_size], slot j % page_size (ascending token order);
+ *   freed_pages receives the old block_table[r, 0..Y) (request order);
+ *   block_table[r, 0..X) = fresh, block_table[r, X..Y) = -1 (rewritten in place);
+ *   new_lens[r * Hkv + h] = k_rh.
+ * Untouched requests keep their row, free nothing and get new_lens = L_r.  Slots of a
+ * fresh page at or beyond k_rh (for head h) are left unwritten.  Only fresh pages are
+ * written; old pages are returned intact.  free_pages must not contain live pages.
+ * num_free < fresh_pages_needed gives ACTKV_ERR_OUT_OF_PAGES.  freed_pages holds
+ * pages_freed entries (see actkv_query); new_lens is int32 [R * Hkv].
+ */
+actkv_status actkv_compact(const actkv_problem* p, void* kv_cache, int32_t* block_table,
+                           const int32_t* kept, const int32_t* free_pages, int64_t num_free,
+                           int32_t* freed_pages, int32_t* new_lens, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+/*
+ * The whole step (Alg. 1 steps 1, 5 and 6): score -> select -> compact on `stream`.
+ * scores, pooled and kept are optional outputs (NULL keeps them in the workspace);
+ * lse may be NULL as in actkv_score.  The other arguments are as above.
+ */
+actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
+                        int32_t* block_table, const float* lse, const int32_t* free_pages,
+                        int64_t num_free, float* scores, float* pooled, int32_t* kept,
+                        int32_t* freed_pages, int32_t* new_lens, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/* Static text for a status code. */
+const char* actkv_status_str(actkv_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ACTKV_H */

@@ -1,0 +1,256 @@
+"""Python binding of libactkv (ctypes): argument marshalling only.
+
+Every function here forwards to the C entry point of the same name in ``libactkv.so``
+(HIP kernels for gfx950); PyTorch only supplies device memory and the current stream.
+The library must be built in-tree (``python -m paper_2609_31395_amd.build``); importing
+this module without it raises, and there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libactkv.so")
+
+STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too small",
+          -4: "out of pages", -5: "HIP error"}
+AGG = {"sum": 0, "max_mean": 1}
+PAGE_SIZE = 16
+
+
+class ActKVError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__(f"{fn} failed: {STATUS.get(code, code)} ({code})")
+        self.code = code
+
+
+class CProblem(ctypes.Structure):
+    _fields_ = [("num_reqs", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("num_pages", ctypes.c_int64),
+                ("bt_stride", ctypes.c_int32),
+                ("seq_lens_h", ctypes.c_void_p), ("q_lens_h", ctypes.c_void_p),
+                ("budgets_h", ctypes.c_void_p), ("seq_lens_d", ctypes.c_void_p),
+                ("q_lens_d", ctypes.c_void_p), ("budgets_d", ctypes.c_void_p),
+                ("sm_scale", ctypes.c_float), ("pool_window", ctypes.c_int32),
+                ("causal", ctypes.c_int32), ("agg", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libactkv.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2609_31395_amd.build`")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER(CProblem)
+    vp, i64, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+    lib.actkv_query.argtypes = [P, ctypes.POINTER(sz), ctypes.POINTER(i64), ctypes.POINTER(i64),
+                                ctypes.POINTER(i64)]
+    lib.actkv_lse.argtypes = [P, vp, vp, vp, vp, vp, sz, vp]
+    lib.actkv_score.argtypes = [P, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.actkv_select.argtypes = [P, vp, vp, vp, vp, sz, vp]
+    lib.actkv_compact.argtypes = [P, vp, vp, vp, vp, i64, vp, vp, vp, sz, vp]
+    lib.actkv_step.argtypes = [P, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, sz, vp]
+    for f in ("actkv_query", "actkv_lse", "actkv_score", "actkv_select", "actkv_compact",
+              "actkv_step"):
+        getattr(lib, f).restype = ctypes.c_int
+    lib.actkv_status_str.argtypes = [ctypes.c_int]
+    lib.actkv_status_str.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+@dataclass
+class Problem:
+    """One compression step's metadata: host arrays plus their device mirrors."""
+    seq_lens: np.ndarray
+    q_lens: np.ndarray
+    budgets: np.ndarray
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    num_pages: int
+    bt_stride: int
+    sm_scale: float = 0.0
+    pool_window: int = 1
+    causal: bool = True
+    agg: str = "sum"
+    seq_lens_d: Optional[torch.Tensor] = None
+    q_lens_d: Optional[torch.Tensor] = None
+    budgets_d: Optional[torch.Tensor] = None
+    page_size: int = PAGE_SIZE
+
+    def __post_init__(self):
+        self.seq_lens = np.ascontiguousarray(self.seq_lens, dtype=np.int32).reshape(-1)
+        self.q_lens = np.ascontiguousarray(self.q_lens, dtype=np.int32).reshape(-1)
+        self.budgets = np.ascontiguousarray(self.budgets, dtype=np.int32).reshape(-1)
+
+    def to_device(self, device="cuda") -> "Problem":
+        self.seq_lens_d = torch.from_numpy(self.seq_lens).to(device)
+        self.q_lens_d = torch.from_numpy(self.q_lens).to(device)
+        self.budgets_d = torch.from_numpy(self.budgets).to(device)
+        return self
+
+    @property
+    def num_reqs(self) -> int:
+        return int(self.seq_lens.shape[0])
+
+    def cstruct(self) -> CProblem:
+        def dptr(t):
+            return None if t is None else t.data_ptr()
+        return CProblem(
+            num_reqs=self.num_reqs, num_q_heads=self.num_q_heads,
+            num_kv_heads=self.num_kv_heads, head_dim=self.head_dim, page_size=self.page_size,
+            num_pages=self.num_pages, bt_stride=self.bt_stride,
+            seq_lens_h=self.seq_lens.ctypes.data, q_lens_h=self.q_lens.ctypes.data,
+            budgets_h=self.budgets.ctypes.data, seq_lens_d=dptr(self.seq_lens_d),
+            q_lens_d=dptr(self.q_lens_d), budgets_d=dptr(self.budgets_d),
+            sm_scale=float(self.sm_scale), pool_window=int(self.pool_window),
+            causal=int(bool(self.causal)), agg=AGG[self.agg])
+
+
+def _check(fn: str, code: int):
+    if code != 0:
+        raise ActKVError(fn, code)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def query(p: Problem) -> dict:
+    """Host-only: workspace bytes, kept entries, fresh pages needed, pages freed."""
+    lib = load_library()
+    c = p.cstruct()
+    ws, nk, fresh, freed = ctypes.c_size_t(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check("actkv_query", lib.actkv_query(ctypes.byref(c), ctypes.byref(ws), ctypes.byref(nk),
+                                          ctypes.byref(fresh), ctypes.byref(freed)))
+    return dict(workspace_bytes=ws.value, num_kept=nk.value, fresh_pages_needed=fresh.value,
+                pages_freed=freed.value)
+
+
+def num_scores(p: Problem) -> int:
+    return int(p.seq_lens.astype(np.int64).sum()) * p.num_kv_heads
+
+
+def workspace(p: Problem, device="cuda") -> torch.Tensor:
+    return torch.empty(max(query(p)["workspace_bytes"], 1), dtype=torch.uint8, device=device)
+
+
+def lse(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch.Tensor,
+        out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+        stream=None) -> torch.Tensor:
+    lib = load_library()
+    dev = kv_cache.device
+    if out is None:
+        out = torch.empty((int(p.q_lens.sum()), p.num_q_heads), dtype=torch.float32, device=dev)
+    ws = workspace(p, dev) if ws is None else ws
+    c = p.cstruct()
+    _check("actkv_lse", lib.actkv_lse(ctypes.byref(c), _ptr(q), _ptr(kv_cache),
+                                      _ptr(block_table), _ptr(out), _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+    return out
+
+
+def score(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch.Tensor,
+          lse: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+          ws: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    lib = load_library()
+    dev = kv_cache.device
+    if out is None:
+        out = torch.empty(num_scores(p), dtype=torch.float32, device=dev)
+    ws = workspace(p, dev) if ws is None else ws
+    c = p.cstruct()
+    _check("actkv_score", lib.actkv_score(ctypes.byref(c), _ptr(q), _ptr(kv_cache),
+                                          _ptr(block_table), _ptr(lse), _ptr(out), _ptr(ws),
+                                          ws.numel(), _stream(stream)))
+    return out
+
+
+def select(p: Problem, scores: torch.Tensor, pooled: Optional[torch.Tensor] = None,
+           kept: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+           stream=None, want_pooled: bool = True):
+    """Returns (kept, pooled); pooled is None when not requested."""
+    lib = load_library()
+    dev = scores.device
+    if kept is None:
+        kept = torch.empty(max(query(p)["num_kept"], 1), dtype=torch.int32, device=dev)
+    if pooled is None and want_pooled:
+        pooled = torch.empty_like(scores)
+    ws = workspace(p, dev) if ws is None else ws
+    c = p.cstruct()
+    _check("actkv_select", lib.actkv_select(ctypes.byref(c), _ptr(scores), _ptr(pooled),
+                                            _ptr(kept), _ptr(ws), ws.numel(), _stream(stream)))
+    return kept[:query(p)["num_kept"]], pooled
+
+
+def compact(p: Problem, kv_cache: torch.Tensor, block_table: torch.Tensor, kept: torch.Tensor,
+            free_pages: torch.Tensor, freed: Optional[torch.Tensor] = None,
+            new_lens: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+            stream=None):
+    """In place on kv_cache / block_table.  Returns (freed_pages, new_lens)."""
+    lib = load_library()
+    dev = kv_cache.device
+    qy = query(p)
+    if freed is None:
+        freed = torch.empty(max(qy["pages_freed"], 1), dtype=torch.int32, device=dev)
+    if new_lens is None:
+        new_lens = torch.empty(p.num_reqs * p.num_kv_heads, dtype=torch.int32, device=dev)
+    ws = workspace(p, dev) if ws is None else ws
+    c = p.cstruct()
+    _check("actkv_compact", lib.actkv_compact(ctypes.byref(c), _ptr(kv_cache), _ptr(block_table),
+                                              _ptr(kept), _ptr(free_pages), free_pages.numel(),
+                                              _ptr(freed), _ptr(new_lens), _ptr(ws), ws.numel(),
+                                              _stream(stream)))
+    return freed[:qy["pages_freed"]], new_lens
+
+
+def step(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch.Tensor,
+         free_pages: torch.Tensor, lse: Optional[torch.Tensor] = None,
+         scores: Optional[torch.Tensor] = None, pooled: Optional[torch.Tensor] = None,
+         kept: Optional[torch.Tensor] = None, freed: Optional[torch.Tensor] = None,
+         new_lens: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+         stream=None, qy: Optional[dict] = None) -> dict:
+    """The whole step, in place on kv_cache / block_table; optional intermediates."""
+    lib = load_library()
+    dev = kv_cache.device
+    qy = query(p) if qy is None else qy
+    if freed is None:
+        freed = torch.empty(max(qy["pages_freed"], 1), dtype=torch.int32, device=dev)
+    if new_lens is None:
+        new_lens = torch.empty(p.num_reqs * p.num_kv_heads, dtype=torch.int32, device=dev)
+    ws = workspace(p, dev) if ws is None else ws
+    c = p.cstruct()
+    _check("actkv_step", lib.actkv_step(ctypes.byref(c), _ptr(q), _ptr(kv_cache),
+                                        _ptr(block_table), _ptr(lse), _ptr(free_pages),
+                                        free_pages.numel(), _ptr(scores), _ptr(pooled),
+                                        _ptr(kept), _ptr(freed), _ptr(new_lens), _ptr(ws),
+                                        ws.numel(), _stream(stream)))
+    return dict(freed=freed[:qy["pages_freed"]], new_lens=new_lens, scores=scores,
+                pooled=pooled, kept=None if kept is None else kept[:qy["num_kept"]])
+
+
+def status_str(code: int) -> str:
+    return load_library().actkv_status_str(code).decode()
+
+
+def default_sm_scale(head_dim: int) -> float:
+    return float(np.float32(1.0) / np.sqrt(np.float32(head_dim)))

@@ -1,0 +1,110 @@
+// Internal definitions shared by the libactkv host code and its HIP kernels.
+// Nothing here is part of the public ABI (include/actkv.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "actkv.h"
+
+namespace actkv {
+
+constexpr int kPageSize = 16;        // slots per page (the only page size built)
+constexpr int kRowsPerChunk = 512;   // query rows (G * n) one scoring pass holds on chip
+constexpr int kKeyTile = 64;         // keys per scoring / LSE pipeline step (4 pages)
+constexpr int kLseKeysPerBlock = 2048;  // keys one LSE workgroup reduces (32 key tiles)
+constexpr int kMaxPoolWindow = 63;
+
+// Per-request plan, written on the device by plan_kernel from the device mirrors.
+struct ReqPlan {
+  int32_t L, n;            // cached tokens, action queries
+  int32_t X, Y;            // fresh pages popped / old pages returned (0 when untouched)
+  int32_t skip;            // every head keeps everything: request left untouched
+  int32_t nchunk;          // query-row chunks of kRowsPerChunk rows (>= 1)
+  int32_t q_off;           // sum of n over earlier requests
+  int32_t fresh_off;       // sum of X over earlier requests
+  int32_t freed_off;       // sum of Y over earlier requests
+  int32_t lse_blocks;      // ceil(L / kLseKeysPerBlock)
+  int64_t seg_off;         // Hkv * sum of L over earlier requests (score offset, head 0)
+  int64_t lse_part_off;    // sum over earlier requests of n * Hq * lse_blocks
+};
+
+// Everything the host derives from the host mirrors before launching anything.
+struct HostPlan {
+  int32_t R = 0, Hq = 0, Hkv = 0, G = 0, D = 0;
+  int32_t max_chunks = 1;
+  int64_t sum_n = 0, sum_L = 0, num_scores = 0;
+  int64_t num_kept = 0, fresh_needed = 0, pages_freed = 0;
+  int64_t num_segments = 0;       // R * max_chunks * Hkv
+  int64_t score_cost = 0;         // total scoring cost units (key tiles x row tiles)
+  int64_t lse_parts = 0;          // sum_r n_r * Hq * lse_blocks_r
+  int64_t max_lse_blocks = 0;     // max_r ceil(L_r / kLseKeysPerBlock)
+};
+
+// Byte offsets of the workspace regions (each 256-byte aligned).
+struct WsLayout {
+  size_t plan = 0;         // ReqPlan[R]
+  size_t kept_off = 0;     // int64[R * Hkv + 1]
+  size_t seg_cost = 0;     // int64[num_segments + 1]
+  size_t lse = 0;          // float[sum_n * Hq]
+  size_t lse_part = 0;     // float2[lse_parts]
+  size_t scores = 0;       // float[num_scores]
+  size_t score_part = 0;   // float[(max_chunks - 1) * num_scores]
+  size_t pooled = 0;       // float[num_scores]
+  size_t kept = 0;         // int32[num_kept]
+  size_t total = 0;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+inline WsLayout ws_layout(const HostPlan& hp) {
+  WsLayout w;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t at = o; o = align256(o + bytes); return at; };
+  w.plan = take(sizeof(ReqPlan) * (size_t)(hp.R > 0 ? hp.R : 1));
+  w.kept_off = take(sizeof(int64_t) * (size_t)(hp.R * hp.Hkv + 1));
+  w.seg_cost = take(sizeof(int64_t) * (size_t)(hp.num_segments + 1));
+  w.lse = take(sizeof(float) * (size_t)(hp.sum_n * hp.Hq));
+  w.lse_part = take(2 * sizeof(float) * (size_t)hp.lse_parts);
+  w.scores = take(sizeof(float) * (size_t)hp.num_scores);
+  w.score_part = take(sizeof(float) * (size_t)(hp.max_chunks - 1) * (size_t)hp.num_scores);
+  w.pooled = take(sizeof(float) * (size_t)hp.num_scores);
+  w.kept = take(sizeof(int32_t) * (size_t)hp.num_kept);
+  w.total = o;
+  return w;
+}
+
+// Common argument block for the device kernels.
+struct DevProblem {
+  int32_t R, Hq, Hkv, G, D;
+  int64_t num_pages;
+  int32_t bt_stride;
+  int32_t max_chunks;
+  int32_t pool_window;
+  int32_t causal;
+  int32_t agg;
+  float sm_scale;
+  const int32_t* seq_lens;
+  const int32_t* q_lens;
+  const int32_t* budgets;
+  ReqPlan* plan;           // workspace
+  int64_t* kept_off;       // workspace [R*Hkv + 1]
+  int64_t* seg_cost;       // workspace [num_segments + 1]
+  int64_t num_segments;
+};
+
+// Kernel launchers (each returns the hipGetLastError() of its launches).
+hipError_t launch_plan(const DevProblem& dp, hipStream_t s);
+hipError_t launch_lse(const DevProblem& dp, const HostPlan& hp, const void* q, const void* kv,
+                      const int32_t* bt, float* lse_out, float2* lse_part, hipStream_t s);
+hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
+                        const void* kv, const int32_t* bt, const float* lse, float* scores,
+                        float* score_part, hipStream_t s);
+hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
+                         float* pooled, int32_t* kept, hipStream_t s);
+hipError_t launch_compact(const DevProblem& dp, const HostPlan& hp, void* kv, int32_t* bt,
+                          const int32_t* kept, const int32_t* free_pages, int32_t* freed,
+                          int32_t* new_lens, hipStream_t s);
+
+}  // namespace actkv

@@ -1,0 +1,276 @@
+// libactkv C ABI: host-side validation, planning and workspace carving, then kernel
+// launches on the caller's stream.  See include/actkv.h for the contract.
+#include <math.h>
+#include <string.h>
+
+#include "actkv.h"
+#include "actkv_internal.h"
+
+using actkv::DevProblem;
+using actkv::HostPlan;
+using actkv::WsLayout;
+
+namespace {
+
+bool valid_pool_window(int32_t w) { return w >= 1 && w <= actkv::kMaxPoolWindow && (w % 2) == 1; }
+
+// Validates `p` and derives the host plan from the host mirrors.  Touches no device memory.
+actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
+  if (!p) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (p->num_reqs < 0 || p->num_q_heads <= 0 || p->num_kv_heads <= 0 || p->head_dim <= 0 ||
+      p->page_size <= 0 || p->num_pages <= 0 || p->bt_stride <= 0)
+    return ACTKV_ERR_INVALID_ARGUMENT;
+  if (p->num_q_heads % p->num_kv_heads) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (!valid_pool_window(p->pool_window)) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (p->causal != 0 && p->causal != 1) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (p->agg != ACTKV_AGG_SUM && p->agg != ACTKV_AGG_MAX_MEAN) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (!isfinite(p->sm_scale) || p->sm_scale < 0.f) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (p->head_dim != 64 && p->head_dim != 128) return ACTKV_ERR_UNSUPPORTED;
+  if (p->page_size != actkv::kPageSize) return ACTKV_ERR_UNSUPPORTED;
+  const int32_t G = p->num_q_heads / p->num_kv_heads;
+  if (p->agg == ACTKV_AGG_MAX_MEAN && !(G == 1 || G == 2 || G == 4 || G == 8 || G == 16))
+    return ACTKV_ERR_UNSUPPORTED;
+  if (p->num_reqs > 0) {
+    if (!p->seq_lens_h || !p->q_lens_h || !p->budgets_h) return ACTKV_ERR_INVALID_ARGUMENT;
+  }
+  hp->R = p->num_reqs;
+  hp->Hq = p->num_q_heads;
+  hp->Hkv = p->num_kv_heads;
+  hp->G = G;
+  hp->D = p->head_dim;
+  const int BS = actkv::kPageSize;
+  int32_t max_chunks = 1;
+  for (int r = 0; r < p->num_reqs; ++r) {
+    const int64_t L = p->seq_lens_h[r], n = p->q_lens_h[r];
+    if (L < 0 || n < 0) return ACTKV_ERR_INVALID_ARGUMENT;
+    if (p->causal && n > L) return ACTKV_ERR_INVALID_ARGUMENT;
+    if ((L + BS - 1) / BS > p->bt_stride) return ACTKV_ERR_INVALID_ARGUMENT;
+    if (n * G > (int64_t)actkv::kRowsPerChunk * 64) return ACTKV_ERR_UNSUPPORTED;
+    const int32_t chunks = n * G > 0 ? (int32_t)((n * G + actkv::kRowsPerChunk - 1) / actkv::kRowsPerChunk) : 1;
+    max_chunks = chunks > max_chunks ? chunks : max_chunks;
+  }
+  hp->max_chunks = max_chunks;
+  for (int r = 0; r < p->num_reqs; ++r) {
+    const int64_t L = p->seq_lens_h[r], n = p->q_lens_h[r];
+    int64_t kmax = 0, bmin = INT64_MAX;
+    for (int h = 0; h < p->num_kv_heads; ++h) {
+      const int64_t b = p->budgets_h[(int64_t)r * p->num_kv_heads + h];
+      if (b < 0) return ACTKV_ERR_INVALID_ARGUMENT;
+      const int64_t k = b < L ? b : L;
+      hp->num_kept += k;
+      kmax = k > kmax ? k : kmax;
+      bmin = b < bmin ? b : bmin;
+    }
+    if (bmin < L) {
+      hp->fresh_needed += (kmax + BS - 1) / BS;
+      hp->pages_freed += (L + BS - 1) / BS;
+    }
+    hp->sum_n += n;
+    hp->sum_L += L;
+    const int64_t ntiles = (L + actkv::kKeyTile - 1) / actkv::kKeyTile;
+    const int64_t M = n * G;
+    const int32_t chunks = M > 0 ? (int32_t)((M + actkv::kRowsPerChunk - 1) / actkv::kRowsPerChunk) : 1;
+    for (int c = 0; c < chunks; ++c) {
+      const int64_t rows = M - (int64_t)c * actkv::kRowsPerChunk;
+      const int64_t rt = rows <= 0 ? 1 : ((rows < actkv::kRowsPerChunk ? rows : actkv::kRowsPerChunk) + 31) / 32;
+      hp->score_cost += ntiles * rt * p->num_kv_heads;
+    }
+    const int64_t lb = (L + actkv::kLseKeysPerBlock - 1) / actkv::kLseKeysPerBlock;
+    hp->lse_parts += n * p->num_q_heads * lb;
+    hp->max_lse_blocks = lb > hp->max_lse_blocks ? lb : hp->max_lse_blocks;
+  }
+  hp->num_scores = hp->sum_L * p->num_kv_heads;
+  hp->num_segments = (int64_t)p->num_reqs * max_chunks * p->num_kv_heads;
+  if (hp->num_scores > INT64_C(1) << 40 || hp->sum_n > INT32_MAX / 2) return ACTKV_ERR_UNSUPPORTED;
+  return ACTKV_OK;
+}
+
+struct Ctx {
+  HostPlan hp;
+  WsLayout ws;
+  DevProblem dp;
+  char* base = nullptr;
+};
+
+// Common prologue of every launching entry point: validate, check the workspace, carve it
+// and fill the device argument block.
+actkv_status prepare(const actkv_problem* p, void* workspace, size_t workspace_bytes, Ctx* cx) {
+  actkv_status st = plan_host(p, &cx->hp);
+  if (st != ACTKV_OK) return st;
+  if (p->num_reqs > 0 && (!p->seq_lens_d || !p->q_lens_d || !p->budgets_d))
+    return ACTKV_ERR_INVALID_ARGUMENT;
+  cx->ws = actkv::ws_layout(cx->hp);
+  if (workspace_bytes < cx->ws.total) return ACTKV_ERR_WORKSPACE_TOO_SMALL;
+  if (!workspace) return ACTKV_ERR_INVALID_ARGUMENT;
+  cx->base = static_cast<char*>(workspace);
+  DevProblem& d = cx->dp;
+  d.R = cx->hp.R;
+  d.Hq = cx->hp.Hq;
+  d.Hkv = cx->hp.Hkv;
+  d.G = cx->hp.G;
+  d.D = cx->hp.D;
+  d.num_pages = p->num_pages;
+  d.bt_stride = p->bt_stride;
+  d.max_chunks = cx->hp.max_chunks;
+  d.pool_window = p->pool_window;
+  d.causal = p->causal;
+  d.agg = p->agg;
+  d.sm_scale = p->sm_scale > 0.f ? p->sm_scale : 1.0f / sqrtf((float)p->head_dim);
+  d.seq_lens = p->seq_lens_d;
+  d.q_lens = p->q_lens_d;
+  d.budgets = p->budgets_d;
+  d.plan = reinterpret_cast<actkv::ReqPlan*>(cx->base + cx->ws.plan);
+  d.kept_off = reinterpret_cast<int64_t*>(cx->base + cx->ws.kept_off);
+  d.seg_cost = reinterpret_cast<int64_t*>(cx->base + cx->ws.seg_cost);
+  d.num_segments = cx->hp.num_segments;
+  return ACTKV_OK;
+}
+
+actkv_status hip_status(hipError_t e) { return e == hipSuccess ? ACTKV_OK : ACTKV_ERR_HIP; }
+
+actkv_status run_lse(const Ctx& cx, const void* q, const void* kv, const int32_t* bt,
+                     float* lse_out, hipStream_t s) {
+  float2* part = reinterpret_cast<float2*>(cx.base + cx.ws.lse_part);
+  return hip_status(actkv::launch_lse(cx.dp, cx.hp, q, kv, bt, lse_out, part, s));
+}
+
+actkv_status run_score(const Ctx& cx, const void* q, const void* kv, const int32_t* bt,
+                       const float* lse, float* scores, hipStream_t s) {
+  if (!lse) {
+    float* lse_ws = reinterpret_cast<float*>(cx.base + cx.ws.lse);
+    actkv_status st = run_lse(cx, q, kv, bt, lse_ws, s);
+    if (st != ACTKV_OK) return st;
+    lse = lse_ws;
+  }
+  float* part = reinterpret_cast<float*>(cx.base + cx.ws.score_part);
+  return hip_status(actkv::launch_score(cx.dp, cx.hp, q, kv, bt, lse, scores, part, s));
+}
+
+}  // namespace
+
+extern "C" {
+
+actkv_status actkv_query(const actkv_problem* p, size_t* workspace_bytes, int64_t* num_kept,
+                         int64_t* fresh_pages_needed, int64_t* pages_freed) {
+  HostPlan hp;
+  actkv_status st = plan_host(p, &hp);
+  if (st != ACTKV_OK) return st;
+  if (workspace_bytes) *workspace_bytes = actkv::ws_layout(hp).total;
+  if (num_kept) *num_kept = hp.num_kept;
+  if (fresh_pages_needed) *fresh_pages_needed = hp.fresh_needed;
+  if (pages_freed) *pages_freed = hp.pages_freed;
+  return ACTKV_OK;
+}
+
+actkv_status actkv_lse(const actkv_problem* p, const void* q, const void* kv_cache,
+                       const int32_t* block_table, float* lse_out, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  Ctx cx;
+  actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
+  if (st != ACTKV_OK) return st;
+  if (cx.hp.sum_n > 0 && (!q || !kv_cache || !block_table || !lse_out))
+    return ACTKV_ERR_INVALID_ARGUMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cx.hp.R == 0) return ACTKV_OK;
+  st = hip_status(actkv::launch_plan(cx.dp, s));
+  if (st != ACTKV_OK) return st;
+  return run_lse(cx, q, kv_cache, block_table, lse_out, s);
+}
+
+actkv_status actkv_score(const actkv_problem* p, const void* q, const void* kv_cache,
+                         const int32_t* block_table, const float* lse, float* scores,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  Ctx cx;
+  actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
+  if (st != ACTKV_OK) return st;
+  if (cx.hp.num_scores > 0 && (!kv_cache || !block_table || !scores)) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.sum_n > 0 && !q) return ACTKV_ERR_INVALID_ARGUMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cx.hp.R == 0) return ACTKV_OK;
+  st = hip_status(actkv::launch_plan(cx.dp, s));
+  if (st != ACTKV_OK) return st;
+  return run_score(cx, q, kv_cache, block_table, lse, scores, s);
+}
+
+actkv_status actkv_select(const actkv_problem* p, const float* scores, float* pooled,
+                          int32_t* kept, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  Ctx cx;
+  actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
+  if (st != ACTKV_OK) return st;
+  if (cx.hp.num_scores > 0 && !scores) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.num_kept > 0 && !kept) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (pooled && scores && pooled == scores) return ACTKV_ERR_INVALID_ARGUMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cx.hp.R == 0) return ACTKV_OK;
+  if (!pooled) pooled = reinterpret_cast<float*>(cx.base + cx.ws.pooled);
+  st = hip_status(actkv::launch_plan(cx.dp, s));
+  if (st != ACTKV_OK) return st;
+  return hip_status(actkv::launch_select(cx.dp, cx.hp, scores, pooled, kept, s));
+}
+
+actkv_status actkv_compact(const actkv_problem* p, void* kv_cache, int32_t* block_table,
+                           const int32_t* kept, const int32_t* free_pages, int64_t num_free,
+                           int32_t* freed_pages, int32_t* new_lens, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  Ctx cx;
+  actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
+  if (st != ACTKV_OK) return st;
+  if (num_free < 0) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.R > 0 && (!block_table || !new_lens)) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.fresh_needed > 0 && (!kv_cache || !kept)) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.pages_freed > 0 && !freed_pages) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (num_free < cx.hp.fresh_needed) return ACTKV_ERR_OUT_OF_PAGES;
+  if (cx.hp.fresh_needed > 0 && !free_pages) return ACTKV_ERR_INVALID_ARGUMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cx.hp.R == 0) return ACTKV_OK;
+  st = hip_status(actkv::launch_plan(cx.dp, s));
+  if (st != ACTKV_OK) return st;
+  return hip_status(actkv::launch_compact(cx.dp, cx.hp, kv_cache, block_table, kept, free_pages,
+                                          freed_pages, new_lens, s));
+}
+
+actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
+                        int32_t* block_table, const float* lse, const int32_t* free_pages,
+                        int64_t num_free, float* scores, float* pooled, int32_t* kept,
+                        int32_t* freed_pages, int32_t* new_lens, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  Ctx cx;
+  actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
+  if (st != ACTKV_OK) return st;
+  if (num_free < 0) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.R > 0 && (!block_table || !new_lens)) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.num_scores > 0 && !kv_cache) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.sum_n > 0 && !q) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.pages_freed > 0 && !freed_pages) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (num_free < cx.hp.fresh_needed) return ACTKV_ERR_OUT_OF_PAGES;
+  if (cx.hp.fresh_needed > 0 && !free_pages) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (scores && pooled && scores == pooled) return ACTKV_ERR_INVALID_ARGUMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cx.hp.R == 0) return ACTKV_OK;
+  if (!scores) scores = reinterpret_cast<float*>(cx.base + cx.ws.scores);
+  if (!pooled) pooled = reinterpret_cast<float*>(cx.base + cx.ws.pooled);
+  if (!kept) kept = reinterpret_cast<int32_t*>(cx.base + cx.ws.kept);
+  st = hip_status(actkv::launch_plan(cx.dp, s));
+  if (st != ACTKV_OK) return st;
+  st = run_score(cx, q, kv_cache, block_table, lse, scores, s);
+  if (st != ACTKV_OK) return st;
+  st = hip_status(actkv::launch_select(cx.dp, cx.hp, scores, pooled, kept, s));
+  if (st != ACTKV_OK) return st;
+  return hip_status(actkv::launch_compact(cx.dp, cx.hp, kv_cache, block_table, kept, free_pages,
+                                          freed_pages, new_lens, s));
+}
+
+const char* actkv_status_str(actkv_status status) {
+  switch (status) {
+    case ACTKV_OK: return "ok";
+    case ACTKV_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case ACTKV_ERR_UNSUPPORTED: return "unsupported";
+    case ACTKV_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case ACTKV_ERR_OUT_OF_PAGES: return "free list shorter than the fresh pages needed";
+    case ACTKV_ERR_HIP: return "HIP launch or runtime error";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

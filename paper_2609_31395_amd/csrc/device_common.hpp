@@ -1,0 +1,100 @@
+// Device helpers for the libactkv kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "actkv_internal.h"
+
+namespace actkv {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// C += A(32x16) * B(16x32), bf16 inputs, fp32 accumulate.  Lane l holds A row l%32 and
+// B column l%32, each with k = 8*(l/32) .. +8; C column l%32, rows 8*(v/4)+4*(l/32)+v%4.
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Inclusive prefix sum over one wave (64 lanes) of a 64-bit value.
+__device__ __forceinline__ int64_t wave_incl_scan_i64(int64_t v) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    int64_t o = __shfl_up(v, d, kWave);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
+// Exclusive prefix sum over the whole block (blockDim.x a multiple of 64, <= 1024).
+// `tmp` is __shared__ int64_t[16 + 1].  Returns the exclusive prefix; *total the sum.
+__device__ __forceinline__ int64_t block_excl_scan_i64(int64_t v, int64_t* tmp, int64_t* total) {
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  const int nw = blockDim.x / kWave;
+  int64_t inc = wave_incl_scan_i64(v);
+  if (lane == kWave - 1) tmp[w] = inc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t acc = 0;
+    for (int i = 0; i < nw; ++i) { int64_t t = tmp[i]; tmp[i] = acc; acc += t; }
+    tmp[16] = acc;
+  }
+  __syncthreads();
+  int64_t ex = tmp[w] + inc - v;
+  *total = tmp[16];
+  __syncthreads();
+  return ex;
+}
+
+// Exclusive prefix count of a per-thread flag across the block, in thread order.
+// `tmp` is __shared__ uint32_t[16 + 1].
+__device__ __forceinline__ uint32_t block_excl_count(bool flag, uint32_t* tmp, uint32_t* total) {
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  const int nw = blockDim.x / kWave;
+  const uint64_t bal = __ballot(flag);
+  const uint32_t below = __popcll(bal & ((lane == 0) ? 0ull : (~0ull >> (kWave - lane))));
+  if (lane == 0) tmp[w] = (uint32_t)__popcll(bal);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t acc = 0;
+    for (int i = 0; i < nw; ++i) { uint32_t t = tmp[i]; tmp[i] = acc; acc += t; }
+    tmp[16] = acc;
+  }
+  __syncthreads();
+  uint32_t ex = tmp[w] + below;
+  *total = tmp[16];
+  __syncthreads();
+  return ex;
+}
+
+// Map a query row of chunk `chunk`, tile `tile`, tile-local row `mm` (0..31) to its action
+// query j and head-in-group g.  For G in {8, 16} the rows of one query are placed so that
+// a single lane of the 32x32 MFMA accumulator holds all G of them (needed by MAX_MEAN);
+// otherwise row m = j * G + g.
+__device__ __forceinline__ void row_to_query(int G, int chunk, int tile, int mm, int* j, int* g) {
+  const int m = chunk * kRowsPerChunk + tile * 32 + mm;
+  if (G == 8 || G == 16) {
+    const int a = mm >> 3, hf = (mm >> 2) & 1, i = mm & 3;
+    const int qbase = (chunk * kRowsPerChunk + tile * 32) / G;
+    if (G == 8) { *j = qbase + 2 * hf + (a >> 1); *g = 4 * (a & 1) + i; }
+    else { *j = qbase + hf; *g = 4 * a + i; }
+  } else {
+    *j = m / G;
+    *g = m % G;
+  }
+}
+
+}  // namespace actkv

@@ -1,0 +1,142 @@
+"""Host-side checks of libactkv that need no GPU: the shared library loads and exports every
+symbol the header declares, the host planning agrees with the oracle's page accounting,
+and every argument error is reported before anything is enqueued."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_31395_amd import actkv
+from paper_2609_31395_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "actkv.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(actkv_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_documented_entry_points():
+    names = declared_functions()
+    for n in ("actkv_query", "actkv_lse", "actkv_score", "actkv_select", "actkv_compact",
+              "actkv_step", "actkv_status_str"):
+        assert n in names
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    lib = actkv.load_library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert actkv.status_str(0) == "ok"
+    assert "workspace" in actkv.status_str(-3)
+
+
+def binding_problem(pb, **kw):
+    return actkv.Problem(seq_lens=pb.seq_lens, q_lens=pb.q_lens, budgets=pb.budgets,
+                         num_q_heads=pb.num_q_heads, num_kv_heads=pb.num_kv_heads,
+                         head_dim=pb.head_dim, num_pages=pb.num_pages, bt_stride=pb.bt_stride,
+                         sm_scale=pb.sm_scale, pool_window=pb.pool_window, causal=pb.causal,
+                         **kw)
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_query_page_accounting_matches_oracle(seed):
+    rng = np.random.default_rng(seed)
+    R, H = int(rng.integers(1, 6)), 2
+    L = rng.integers(0, 300, size=R)
+    budgets = rng.integers(0, 320, size=R * H)
+    if seed == 0:
+        budgets[:H] = L[0] + 5   # one untouched request
+    pb = W.make_custom(seq_lens=L, q_lens=np.minimum(L, 3), num_q_heads=4, num_kv_heads=H,
+                       head_dim=64, budgets=budgets, seed=seed)
+    q = actkv.query(binding_problem(pb))
+    nk, fresh, freed = oracle.totals(pb)
+    assert (q["num_kept"], q["fresh_pages_needed"], q["pages_freed"]) == (nk, fresh, freed)
+    assert q["workspace_bytes"] > 0
+
+
+def _tiny(**over):
+    kw = dict(seq_lens=[40, 17], q_lens=[4, 2], budgets=[8, 8, 8, 8], num_q_heads=4,
+              num_kv_heads=2, head_dim=128, num_pages=64, bt_stride=3, pool_window=3)
+    kw.update(over)
+    return actkv.Problem(**kw)
+
+
+BAD = [
+    (dict(pool_window=4), -1),
+    (dict(pool_window=65), -1),
+    (dict(pool_window=0), -1),
+    (dict(q_lens=[41, 2]), -1),                      # causal query beyond the cache
+    (dict(num_q_heads=3), -1),                       # Hq not a multiple of Hkv
+    (dict(budgets=[8, -1, 8, 8]), -1),
+    (dict(bt_stride=2), -1),                         # row too short for 40 tokens
+    (dict(seq_lens=[-1, 17]), -1),
+    (dict(num_pages=0), -1),
+    (dict(sm_scale=-1.0), -1),
+    (dict(sm_scale=float("nan")), -1),
+    (dict(head_dim=96), -2),
+    (dict(page_size=32), -2),
+    (dict(agg="max_mean", num_q_heads=6, num_kv_heads=2), -2),   # G = 3
+]
+
+
+@pytest.mark.parametrize("over,code", BAD)
+def test_invalid_problems_are_rejected_on_the_host(over, code):
+    with pytest.raises(actkv.ActKVError) as e:
+        actkv.query(_tiny(**over))
+    assert e.value.code == code
+
+
+def test_non_causal_queries_may_outnumber_the_cache():
+    actkv.query(_tiny(q_lens=[41, 2], causal=False))
+
+
+FAKE = 0x10000   # never dereferenced: every call below must fail before any launch
+
+
+def _call_step(p, ws_bytes, num_free=1000, with_mirrors=True):
+    lib = actkv.load_library()
+    if with_mirrors:
+        c = p.cstruct()
+        c.seq_lens_d = c.q_lens_d = c.budgets_d = FAKE
+    else:
+        c = p.cstruct()
+    return lib.actkv_step(ctypes.byref(c), FAKE, FAKE, FAKE, None, FAKE, num_free, None, None,
+                          None, FAKE, FAKE, FAKE, ws_bytes, None)
+
+
+def test_step_reports_small_workspace_before_launching():
+    p = _tiny()
+    need = actkv.query(p)["workspace_bytes"]
+    assert _call_step(p, need - 1) == -3
+
+
+def test_step_reports_short_free_list_before_launching():
+    p = _tiny()
+    q = actkv.query(p)
+    assert q["fresh_pages_needed"] > 0
+    assert _call_step(p, q["workspace_bytes"], num_free=q["fresh_pages_needed"] - 1) == -4
+
+
+def test_step_requires_device_mirrors():
+    p = _tiny()
+    assert _call_step(p, actkv.query(p)["workspace_bytes"], with_mirrors=False) == -1
+
+
+def test_compact_and_select_validate_before_launching():
+    lib = actkv.load_library()
+    p = _tiny()
+    c = p.cstruct()
+    c.seq_lens_d = c.q_lens_d = c.budgets_d = FAKE
+    ws = actkv.query(p)["workspace_bytes"]
+    assert lib.actkv_compact(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, 0, FAKE, FAKE, FAKE, ws,
+                             None) == -4
+    assert lib.actkv_select(ctypes.byref(c), FAKE, FAKE, None, FAKE, ws, None) == -1
+    assert lib.actkv_score(ctypes.byref(c), FAKE, FAKE, FAKE, None, FAKE, FAKE, 16, None) == -3
+    assert lib.actkv_lse(None, FAKE, FAKE, FAKE, FAKE, FAKE, ws, None) == -1
