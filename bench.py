@@ -1,0 +1,262 @@
+#!/usr/bin/env python3
+"""Benchmark of the ActKV compression step (score -> select -> compact) on one MI355X.
+
+One step = one actkv_step call over one layer of a synthetic batch: every cached KV entry
+of every request is scored by the attention of that request's action queries (LSE
+supplied, as a paged-attention decode produces it), the top-B entries per KV head are
+selected and compacted into fresh pages, and the block table is rewritten.
+
+Prints ONE JSON line (rank 0).  Default workload: 32 requests x 35,000 cached tokens with
+Qwen3-30B head shapes (32 query / 4 KV heads, head_dim 128, 16-token pages), 64 action
+queries per request, 25% budget per KV head, pool window 7 -- drawn on the device from a
+seeded generator.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
+METRIC = "KV tokens scored+compacted/s per layer (1 GPU)"
+SCORE_SOURCES = ["paper_2609_31395_amd/csrc/score.hip",
+                 "paper_2609_31395_amd/csrc/device_common.hpp",
+                 "paper_2609_31395_amd/csrc/actkv_internal.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_kernel_batch32x35k_traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="batch32x35k")
+    ap.add_argument("--cpu-sample-reqs", type=int, default=8,
+                    help="requests of the workload the CPU oracle is timed on")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    for rel in SCORE_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def algorithmic_bytes(dp, num_kept: int) -> int:
+    """HBM bytes the step cannot avoid: read K once; read Q and the LSE; write and read
+    each fp32 score once; write and read each kept index once; read and write each kept
+    K and V row once."""
+    D, Hkv, Hq = dp.head_dim, dp.num_kv_heads, dp.num_q_heads
+    sum_L = int(dp.seq_lens.astype(np.int64).sum())
+    sum_n = int(dp.q_lens.astype(np.int64).sum())
+    k_read = sum_L * Hkv * D * 2
+    q_read = sum_n * Hq * D * 2 + sum_n * Hq * 4
+    scores = 2 * 4 * sum_L * Hkv
+    kept = 2 * 4 * num_kept
+    rows = num_kept * D * 2 * 2 * 2
+    return k_read + q_read + scores + kept + rows
+
+
+def score_flops(dp) -> int:
+    """Dense QK^T flops of one scoring pass: 2 * (G n_r) * L_r * D per (request, KV head)."""
+    G = dp.num_q_heads // dp.num_kv_heads
+    return int(sum(2 * G * int(n) * int(L) * dp.head_dim * dp.num_kv_heads
+                   for L, n in zip(dp.seq_lens, dp.q_lens)))
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the compression step shards by request and KV head with no exchange, "
+              "see the design notes.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2609_31395_amd import actkv
+    from paper_2609_31395_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    actkv.load_library()
+    dev = torch.device("cuda:0")
+    t_gen = time.time()
+    dp = W.make_device_problem(args.workload, device=dev)
+    torch.cuda.synchronize()
+    t_gen = time.time() - t_gen
+    log(f"drew {args.workload} on the device in {t_gen:.1f} s")
+    bp = actkv.Problem(seq_lens=dp.seq_lens, q_lens=dp.q_lens, budgets=dp.budgets,
+                       num_q_heads=dp.num_q_heads, num_kv_heads=dp.num_kv_heads,
+                       head_dim=dp.head_dim, num_pages=dp.num_pages, bt_stride=dp.bt_stride,
+                       sm_scale=dp.sm_scale, pool_window=dp.pool_window,
+                       causal=dp.causal).to_device(dev)
+    qy = actkv.query(bp)
+    ws = torch.empty(qy["workspace_bytes"], dtype=torch.uint8, device=dev)
+    bt0 = torch.from_numpy(dp.block_table).to(dev)
+    free = torch.from_numpy(dp.free_pages).to(dev)
+    n_sc = actkv.num_scores(bp)
+    scores = torch.empty(n_sc, dtype=torch.float32, device=dev)
+    pooled = torch.empty(n_sc, dtype=torch.float32, device=dev)
+    kept = torch.empty(max(qy["num_kept"], 1), dtype=torch.int32, device=dev)
+    freed = torch.empty(max(qy["pages_freed"], 1), dtype=torch.int32, device=dev)
+    new_lens = torch.empty(bp.num_reqs * bp.num_kv_heads, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    # The LSE the decode attention would hand over: produced once, outside the timed region.
+    lse = actkv.lse(bp, dp.q, dp.kv, bt0, ws=ws)
+    torch.cuda.synchronize()
+
+    K, Wm = args.steps, args.warmup
+    # every step compacts against a pristine block table: one copy per step, made up front
+    # (a compacted table must never be reused with the original lengths)
+    bts = [bt0.clone() for _ in range(K + max(Wm, 1))]
+
+    def one_step(bt, with_lse=True):
+        actkv.step(bp, dp.q, dp.kv, bt, free, lse=lse if with_lse else None, scores=scores,
+                   pooled=pooled, kept=kept, freed=freed, new_lens=new_lens, ws=ws, qy=qy)
+
+    for i in range(Wm):
+        one_step(bts[i])
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(K):
+        one_step(bts[Wm + i])
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(K)]
+    ms_per_step = ev[0].elapsed_time(ev[K]) / K
+    log(f"timed {K} steps: {ms_per_step * 1e3:.1f} us/step")
+
+    # ---- per-stage durations (same work, the three entry points called one by one, with
+    # events between them on the launch stream)
+    for b in bts:
+        b.copy_(bt0)
+    torch.cuda.synchronize()
+    se = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    for i in range(K):
+        se[i][0].record(stream)
+        actkv.score(bp, dp.q, dp.kv, bts[i], lse=lse, out=scores, ws=ws)
+        se[i][1].record(stream)
+        actkv.select(bp, scores, pooled=pooled, kept=kept, ws=ws)
+        se[i][2].record(stream)
+        actkv.compact(bp, dp.kv, bts[i], kept, free, freed=freed, new_lens=new_lens, ws=ws)
+        se[i][3].record(stream)
+    torch.cuda.synchronize()
+    stage_ms = np.array([[se[i][j].elapsed_time(se[i][j + 1]) for j in range(3)]
+                         for i in range(K)]).mean(axis=0)
+
+    # ---- the step with the LSE pass included (library computes the normaliser)
+    for b in bts:
+        b.copy_(bt0)
+    torch.cuda.synchronize()
+    el = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    one_step(bts[K], with_lse=False)   # warm-up on its own pristine copy
+    torch.cuda.synchronize()
+    el[0].record(stream)
+    for i in range(K):
+        one_step(bts[i], with_lse=False)
+    el[1].record(stream)
+    torch.cuda.synchronize()
+    ms_with_lse = el[0].elapsed_time(el[1]) / K
+    log(f"stages (us) {np.round(stage_ms * 1e3, 1).tolist()}, step with LSE pass "
+        f"{ms_with_lse * 1e3:.1f} us")
+
+    sum_L = int(dp.seq_lens.astype(np.int64).sum())
+    value = sum_L / (ms_per_step * 1e-3)
+    alg_bytes = algorithmic_bytes(dp, qy["num_kept"])
+    flops = score_flops(dp)
+    score_s = stage_ms[0] * 1e-3
+    achieved_tflops = flops / score_s / 1e12
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("source_sha256") == source_digest() and tr.get("workload") == args.workload:
+            traffic = int(tr["hbm_bytes_per_launch"])
+
+    cpu = None
+    if not args.no_cpu_baseline and args.cpu_sample_reqs > 0:
+        import oracle
+        reqs = list(range(min(args.cpu_sample_reqs, dp.num_reqs)))
+        sample = dp.host_subset(reqs)
+        log(f"timing the CPU oracle on {len(reqs)} requests ({oracle.num_threads()} threads)")
+        t1 = time.perf_counter()
+        oracle.step(sample)   # the oracle's own full step (it derives the LSE itself)
+        cpu_s = time.perf_counter() - t1
+        s_tokens = int(sample.seq_lens.astype(np.int64).sum())
+        cpu = {"value": s_tokens / cpu_s, "unit": "tokens/s", "cores": oracle.num_threads(),
+               "kind": "oracle",
+               "sample": f"{len(reqs)} of {dp.num_reqs} requests of {args.workload} "
+                         f"({s_tokens} cached tokens, all stages, fp64), {cpu_s:.1f} s"}
+
+    cfg = W.CONFIGS[args.workload]
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload,
+            "description": cfg.description,
+            "requests": dp.num_reqs,
+            "cached_tokens": sum_L,
+            "q_heads": dp.num_q_heads, "kv_heads": dp.num_kv_heads, "head_dim": dp.head_dim,
+            "page_size": dp.page_size,
+            "action_queries": int(dp.q_lens.sum()),
+            "kept_entries": qy["num_kept"],
+            "pool_window": dp.pool_window,
+            "lse": "supplied (produced once by actkv_lse outside the timed region)",
+            "parallelism": "single GPU",
+        },
+        "step_us": ms_per_step * 1e3,
+        "step_us_p10_p90": [float(np.percentile(step_ms, 10) * 1e3),
+                            float(np.percentile(step_ms, 90) * 1e3)],
+        "hbm_roofline": {"algorithmic_bytes": alg_bytes,
+                         "t_hbm_us": alg_bytes / (HBM_PEAK_GBS * 1e9) * 1e6,
+                         "frac": (alg_bytes / (HBM_PEAK_GBS * 1e9)) / (ms_per_step * 1e-3)},
+        "stages_us": {"score": stage_ms[0] * 1e3, "select": stage_ms[1] * 1e3,
+                      "compact": stage_ms[2] * 1e3},
+        "step_with_lse_pass_us": ms_with_lse * 1e3,
+        "roofline": {
+            "kernel": "score_kernel (actkv_score, LSE supplied)",
+            "bound": "mfma",
+            "achieved": achieved_tflops,
+            "peak": BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved_tflops / BF16_PEAK_TFLOPS,
+            "traffic": traffic,
+        },
+        "cpu_baseline": cpu,
+        "wall_s_timed": wall,
+        "gen_s": t_gen,
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -35,10 +35,12 @@
  *  - Errors: every argument error is detected on the host before anything is enqueued,
  *    and then nothing is written.  ACTKV_ERR_HIP reports a failed kernel launch.  Faults
  *    inside kernels surface at the caller's next synchronisation.
- *  - Undefined behaviour: non-finite q or K, block-table entries outside
- *    [0, num_pages) for live tokens, device mirrors that disagree with the host mirrors,
- *    fresh pages that are still live, and buffers that overlap where the text says they
- *    must not.
+ *  - Unspecified results (never a fault): block-table or free-list entries outside
+ *    [0, num_pages) are not dereferenced -- the keys behind them read as zero and the
+ *    compacted slots they would feed are left unwritten.
+ *  - Undefined behaviour: non-finite q or K, device mirrors that disagree with the host
+ *    mirrors, fresh pages that are still live, and buffers that overlap where the text
+ *    says they must not.
  */
 #ifndef ACTKV_H
 #define ACTKV_H

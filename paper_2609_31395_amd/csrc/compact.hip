@@ -52,7 +52,11 @@ __global__ __launch_bounds__(256) void compact_gather_kernel(DevProblem dp, uint
       const int kh = bh < pl.L ? bh : pl.L;
       if (j >= kh) continue;
       const int t = kept[dp.kept_off[r * Hkv + h] + j];
+      if (t < 0 || t >= pl.L) continue;
       const int64_t src_page = bt_row[t / kPageSize];
+      // pages outside the pool are never dereferenced (the slot is left unwritten)
+      if (src_page < 0 || src_page >= dp.num_pages || dst_page < 0 || dst_page >= dp.num_pages)
+        continue;
       const int64_t src = which * plane + ((src_page * kPageSize + t % kPageSize) * Hkv + h) * (int64_t)D + ch * 8;
       dst[u] = which * plane + ((dst_page * kPageSize + s) * Hkv + h) * (int64_t)D + ch * 8;
       v[u] = *reinterpret_cast<const u32x4*>(kv + src);

@@ -48,15 +48,16 @@ template <int D>
 __device__ __forceinline__ void load_k_tile(u32x4 (&pre)[TileGeom<D>::kLoadsPerThread],
                                             const uint16_t* __restrict__ kv,
                                             const int32_t* __restrict__ bt_row, int L, int h,
-                                            int Hkv, int64_t tile) {
+                                            int Hkv, int64_t num_pages, int64_t tile) {
   using Gm = TileGeom<D>;
 #pragma unroll
   for (int u = 0; u < Gm::kLoadsPerThread; ++u) {
     const int q = threadIdx.x + kThreads * u;
     const int row = q / Gm::kChunksPerRow, ch = q % Gm::kChunksPerRow;
     const int64_t key = tile * kKeyTile + row;
-    if (key < L) {
-      const int64_t page = bt_row[key / kPageSize];
+    const int64_t page = key < L ? (int64_t)bt_row[key / kPageSize] : -1;
+    // a page outside the pool is never dereferenced (its keys read as zero)
+    if (page >= 0 && page < num_pages) {
       const uint16_t* src =
           kv + ((page * kPageSize + key % kPageSize) * Hkv + h) * (int64_t)D + ch * 8;
       pre[u] = *reinterpret_cast<const u32x4*>(src);
@@ -197,7 +198,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(ScoreArgs a) {
     const int mask_from = dp.causal ? L - n : L;  // keys past this may be hidden from rows
 
     u32x4 pre[Gm::kLoadsPerThread];
-    load_k_tile<D>(pre, a.kv, bt_row, L, h, Hkv, i0);
+    load_k_tile<D>(pre, a.kv, bt_row, L, h, Hkv, dp.num_pages, i0);
     store_k_tile<D>(pre, kbuf[0]);
     __syncthreads();
     // beta of this lane's 16 rows per row tile: rows 8*aa + 4*hf + i
@@ -218,7 +219,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(ScoreArgs a) {
     int buf = 0;
     for (int64_t i = i0; i < i1; ++i) {
       const bool has_next = i + 1 < i1;
-      if (has_next) load_k_tile<D>(pre, a.kv, bt_row, L, h, Hkv, i + 1);
+      if (has_next) load_k_tile<D>(pre, a.kv, bt_row, L, h, Hkv, dp.num_pages, i + 1);
       const int64_t key0 = i * kKeyTile;
       const bool needs_mask = key0 + kKeyTile - 1 > mask_from;
 #pragma unroll
@@ -385,13 +386,13 @@ __global__ __launch_bounds__(kThreads, 1) void lse_partial_kernel(DevProblem dp,
   if (t1 > ntiles) t1 = ntiles;
 
   u32x4 pre[Gm::kLoadsPerThread];
-  load_k_tile<D>(pre, kv, bt_row, L, h, Hkv, t0);
+  load_k_tile<D>(pre, kv, bt_row, L, h, Hkv, dp.num_pages, t0);
   store_k_tile<D>(pre, kbuf[0]);
   __syncthreads();
   int buf = 0;
   for (int64_t i = t0; i < t1; ++i) {
     const bool has_next = i + 1 < t1;
-    if (has_next) load_k_tile<D>(pre, kv, bt_row, L, h, Hkv, i + 1);
+    if (has_next) load_k_tile<D>(pre, kv, bt_row, L, h, Hkv, dp.num_pages, i + 1);
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
       bf16x8 kreg[Gm::kSteps];

@@ -259,3 +259,136 @@ def _assemble(name, L, n, budgets, Hq, Hkv, D, spike_frac, perm, req_ss, pool_wi
     return Problem(name, Hq, Hkv, D, BS, L.astype(np.int32), n.astype(np.int32),
                    budgets.astype(np.int32), q_all, kv, block_table, free_pages, sm_scale,
                    int(pool_window), bool(causal), k_dense, v_dense, spikes)
+
+
+# ---------------------------------------------------------------------------------------
+# Device-side drawing for the full-size workloads (hundreds of millions of bf16 values).
+# Same recipe as above, but the Gaussian draws come from a seeded torch generator on the
+# device, so the numbers differ from the numpy path.  Lengths, query counts, budgets and
+# the page permutation still come from numpy exactly as in make_problem.
+# ---------------------------------------------------------------------------------------
+@dataclass
+class DeviceProblem:
+    cfg_name: str
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    page_size: int
+    seq_lens: np.ndarray
+    q_lens: np.ndarray
+    budgets: np.ndarray
+    block_table: np.ndarray       # host copy of the pristine block table
+    free_pages: np.ndarray
+    sm_scale: float
+    pool_window: int
+    causal: bool
+    q: "object"                   # torch int16 (bf16 bits) [sum n, Hq, D] on the device
+    kv: "object"                  # torch int16 (bf16 bits) [2, P, BS, Hkv, D] on the device
+    pages: List[np.ndarray] = field(default_factory=list)   # request r's physical pages
+
+    @property
+    def num_reqs(self) -> int:
+        return int(self.seq_lens.shape[0])
+
+    @property
+    def num_pages(self) -> int:
+        return int(self.kv.shape[1])
+
+    @property
+    def bt_stride(self) -> int:
+        return int(self.block_table.shape[1])
+
+    @property
+    def cu_q(self) -> np.ndarray:
+        return np.concatenate([[0], np.cumsum(self.q_lens, dtype=np.int64)])
+
+    def host_subset(self, reqs: List[int]) -> Problem:
+        """Copy requests `reqs` back to the host as a self-contained Problem (their own
+        compact page pool, same logical content) -- used to run the oracle on a sample."""
+        import torch
+        BS, Hkv, D = self.page_size, self.num_kv_heads, self.head_dim
+        L = self.seq_lens[reqs].astype(np.int32)
+        n = self.q_lens[reqs].astype(np.int32)
+        b = self.budgets.reshape(-1, Hkv)[reqs].reshape(-1).astype(np.int32)
+        Y = (L.astype(np.int64) + BS - 1) // BS
+        used = int(Y.sum())
+        P = max(2 * used, used + 1)
+        kv = np.zeros((2, P, BS, Hkv, D), np.uint16)
+        bt = np.full((len(reqs), int(max(1, Y.max(initial=0)))), -1, np.int32)
+        qs, kd, vd = [], [], []
+        off = 0
+        cu = self.cu_q
+        for i, r in enumerate(reqs):
+            pg = torch.from_numpy(self.pages[r].astype(np.int64)).to(self.kv.device)
+            blk = self.kv.index_select(1, pg).cpu().numpy().view(np.uint16)   # [2, Y, BS, Hkv, D]
+            kv[:, off:off + Y[i]] = blk
+            bt[i, :Y[i]] = np.arange(off, off + Y[i], dtype=np.int32)
+            flat = blk.reshape(2, -1, Hkv, D)[:, :L[i]]
+            kd.append(flat[0].copy())
+            vd.append(flat[1].copy())
+            qs.append(self.q[int(cu[r]):int(cu[r + 1])].cpu().numpy().view(np.uint16))
+            off += int(Y[i])
+        free = np.arange(off, P, dtype=np.int32)
+        q = np.concatenate(qs) if qs else np.zeros((0, self.num_q_heads, D), np.uint16)
+        return Problem(self.cfg_name + f"[{len(reqs)} requests]", self.num_q_heads, Hkv, D, BS,
+                       L, n, b, q, kv, bt, free, self.sm_scale, self.pool_window, self.causal,
+                       kd, vd, [])
+
+
+def make_device_problem(name: str, device="cuda", *, seed: Optional[int] = None,
+                        overrides: Optional[dict] = None) -> DeviceProblem:
+    """Draw workload `name` directly into device memory (torch, seeded)."""
+    import torch
+    cfg = CONFIGS[name]
+    if overrides:
+        cfg = WorkloadConfig(**{**cfg.__dict__, **overrides})
+    base_seed = cfg.seed if seed is None else seed
+    ss = np.random.SeedSequence(base_seed)
+    meta_ss, page_ss, budget_ss, *req_ss = ss.spawn(3 + cfg.num_reqs)
+    R, Hq, Hkv, D, BS = cfg.num_reqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, PAGE_SIZE
+    G = Hq // Hkv
+    L, n = _draw_lengths(np.random.Generator(np.random.PCG64(meta_ss)), cfg)
+    budgets = _draw_budgets(np.random.Generator(np.random.PCG64(budget_ss)), cfg, L)
+    Y = (L.astype(np.int64) + BS - 1) // BS
+    used = int(Y.sum())
+    P = cfg.fixed_pool_pages if cfg.fixed_pool_pages is not None else \
+        max(used + 1, int(math.ceil(cfg.pool_factor * used)))
+    perm = np.random.Generator(np.random.PCG64(page_ss)).permutation(P).astype(np.int32)
+    bt_stride = int(max(1, Y.max(initial=0)))
+    block_table = np.full((R, bt_stride), -1, dtype=np.int32)
+    kv = torch.empty((2, P, BS, Hkv, D), dtype=torch.bfloat16, device=device)
+    q_all = torch.empty((int(n.sum()), Hq, D), dtype=torch.bfloat16, device=device)
+    pages_list = []
+    off_page, off_q = 0, 0
+    for r in range(R):
+        Lr, nr, Yr = int(L[r]), int(n[r]), int(Y[r])
+        gen = torch.Generator(device=device)
+        gen.manual_seed(int(req_ss[r].generate_state(1, dtype=np.uint64)[0] & 0x7FFFFFFFFFFFFFFF))
+        q = torch.randn((nr, Hq, D), generator=gen, device=device).to(torch.bfloat16)
+        k = torch.randn((Yr * BS, Hkv, D), generator=gen, device=device)
+        v = torch.randn((Yr * BS, Hkv, D), generator=gen, device=device)
+        k[Lr:] = 0
+        v[Lr:] = 0
+        cnt = int(round(cfg.spike_frac * Lr))
+        if cnt > 0 and nr > 0:
+            qf = q.float()
+            for h in range(Hkv):
+                mean = qf[:, h * G:(h + 1) * G, :].reshape(-1, D).double().mean(0).float()
+                idx = torch.randperm(Lr, generator=gen, device=device)[:cnt]
+                k[idx, h, :] += 3.0 * mean
+        pages = perm[off_page:off_page + Yr]
+        block_table[r, :Yr] = pages
+        pg = torch.from_numpy(pages.astype(np.int64)).to(device)
+        kv[0].index_copy_(0, pg, k.to(torch.bfloat16).view(Yr, BS, Hkv, D))
+        kv[1].index_copy_(0, pg, v.to(torch.bfloat16).view(Yr, BS, Hkv, D))
+        q_all[off_q:off_q + nr] = q
+        pages_list.append(pages.copy())
+        off_page += Yr
+        off_q += nr
+        del k, v
+    free_pages = perm[used:].copy()
+    sm_scale = float(np.float32(1.0) / np.sqrt(np.float32(D)))
+    return DeviceProblem(cfg.name, Hq, Hkv, D, BS, L.astype(np.int32), n.astype(np.int32),
+                         budgets.astype(np.int32), block_table, free_pages, sm_scale,
+                         cfg.pool_window, cfg.causal, q_all.view(torch.int16),
+                         kv.view(torch.int16), pages_list)
