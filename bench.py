@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--cpu-sample-reqs", type=int, default=8,
                     help="requests of the workload the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-stage", choices=["score", "select", "compact", "lse", "step"],
+                    help="only run one entry point --steps times (for counter collection); "
+                         "prints a short JSON line instead of the benchmark record")
     return ap.parse_args()
 
 
@@ -78,6 +81,32 @@ def score_flops(dp) -> int:
 
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def run_stage(stage, reps, bp, dp, bts, lse, scores, pooled, kept, free, freed, new_lens, ws, qy):
+    """Run one entry point `reps` times on its own (inputs prepared by the full step once)."""
+    import torch
+    from paper_2609_31395_amd import actkv
+    first = bts[0].clone()   # bts are all pristine here; the prep step gets its own copy
+    actkv.step(bp, dp.q, dp.kv, first, free, lse=lse, scores=scores, pooled=pooled, kept=kept,
+               freed=freed, new_lens=new_lens, ws=ws, qy=qy)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(reps):
+        if stage == "score":
+            actkv.score(bp, dp.q, dp.kv, bts[i], lse=lse, out=scores, ws=ws)
+        elif stage == "select":
+            actkv.select(bp, scores, pooled=pooled, kept=kept, ws=ws)
+        elif stage == "compact":
+            actkv.compact(bp, dp.kv, bts[i], kept, free, freed=freed, new_lens=new_lens, ws=ws)
+        elif stage == "lse":
+            actkv.lse(bp, dp.q, dp.kv, bts[i], out=lse, ws=ws)
+        else:
+            actkv.step(bp, dp.q, dp.kv, bts[i], free, lse=lse, scores=scores, pooled=pooled,
+                       kept=kept, freed=freed, new_lens=new_lens, ws=ws, qy=qy)
+    torch.cuda.synchronize()
+    print(json.dumps({"profile_stage": stage, "reps": reps,
+                      "avg_us": (time.perf_counter() - t0) / reps * 1e6}))
 
 
 def main():
@@ -124,6 +153,11 @@ def main():
     # every step compacts against a pristine block table: one copy per step, made up front
     # (a compacted table must never be reused with the original lengths)
     bts = [bt0.clone() for _ in range(K + max(Wm, 1))]
+
+    if args.profile_stage:
+        run_stage(args.profile_stage, K + Wm, bp, dp, bts, lse, scores, pooled, kept, free, freed,
+                  new_lens, ws, qy)
+        return
 
     def one_step(bt, with_lse=True):
         actkv.step(bp, dp.q, dp.kv, bt, free, lse=lse if with_lse else None, scores=scores,

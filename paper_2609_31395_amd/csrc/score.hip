@@ -33,49 +33,102 @@ namespace {
 constexpr int kThreads = 512;   // 8 waves: two per SIMD at one workgroup per CU
 constexpr int kWaves = kThreads / 64;
 constexpr int kTilesPerWave = kRowsPerChunk / 32 / kWaves;   // 2 row tiles of 32 rows
+constexpr int kStages = 4;      // K tiles in flight / resident in LDS
 
+// Geometry of one K tile (kKeyTile keys of one KV head) in LDS.  Rows are not padded;
+// instead the 16-byte chunk c of row r sits in slot c ^ (r % kChunks), which keeps both
+// the direct-to-LDS loads (64 lanes write one contiguous KiB) and the MFMA operand reads
+// (lanes l and l+1 read rows r, r+1 at the same logical chunk) free of bank conflicts.
 template <int D>
 struct TileGeom {
-  static constexpr int kSteps = D / 16;                 // MFMA k-steps per row
-  static constexpr int kChunksPerRow = D / 8;           // 16-byte chunks per K row
-  static constexpr int kLoadsPerThread = kKeyTile * kChunksPerRow / kThreads;
-  static constexpr int kStride = D * 2 + 16;            // padded LDS row (bytes)
-  static constexpr int kTileBytes = kKeyTile * kStride;
+  static constexpr int kSteps = D / 16;                  // MFMA k-steps per row
+  static constexpr int kRowBytes = D * 2;
+  static constexpr int kChunks = D / 8;                  // 16-byte chunks per row
+  static constexpr int kTileBytes = kKeyTile * kRowBytes;
+  static constexpr int kWaveLoads = kTileBytes / 1024;   // one KiB per wave-wide load
+  static constexpr int kLoadsPerWave = kWaveLoads / kWaves;
+  static constexpr int kRowsPerLoad = 1024 / kRowBytes;
+  static_assert(kWaveLoads % kWaves == 0, "tile must split evenly over the waves");
 };
 
-// Global loads of K tile `tile` (keys 64*tile ..) of request r, head h into registers.
-template <int D>
-__device__ __forceinline__ void load_k_tile(u32x4 (&pre)[TileGeom<D>::kLoadsPerThread],
-                                            const uint16_t* __restrict__ kv,
-                                            const int32_t* __restrict__ bt_row, int L, int h,
-                                            int Hkv, int64_t num_pages, int64_t tile) {
-  using Gm = TileGeom<D>;
-#pragma unroll
-  for (int u = 0; u < Gm::kLoadsPerThread; ++u) {
-    const int q = threadIdx.x + kThreads * u;
-    const int row = q / Gm::kChunksPerRow, ch = q % Gm::kChunksPerRow;
-    const int64_t key = tile * kKeyTile + row;
-    const int64_t page = key < L ? (int64_t)bt_row[key / kPageSize] : -1;
-    // a page outside the pool is never dereferenced (its keys read as zero)
-    if (page >= 0 && page < num_pages) {
-      const uint16_t* src =
-          kv + ((page * kPageSize + key % kPageSize) * Hkv + h) * (int64_t)D + ch * 8;
-      pre[u] = *reinterpret_cast<const u32x4*>(src);
-    } else {
-      pre[u] = u32x4{0u, 0u, 0u, 0u};
-    }
-  }
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
+// This wave's share of K tile `tile` (keys 64*tile ..) of request row bt_row, head h,
+// fetched straight into LDS buffer `dst` with 16-byte loads.  Each wave-wide load covers
+// kRowsPerLoad consecutive keys inside one page, so the page id is wave-uniform and comes
+// from a scalar load (a vector load here would force a wait on the whole DMA queue).
+// Keys past L read slots of the request's last page (their results are discarded); a page
+// outside the pool is never dereferenced.
+typedef __attribute__((address_space(3))) char lds_char;
+
+// One wave-wide 16-byte-per-lane load from global memory straight into LDS at byte
+// address lds_addr + 16 * lane (global_load_lds_dwordx4; the LDS base travels in M0, which
+// is saved and restored around it).  Issued from inline assembly so that the compiler does
+// not add its own wait on the whole vector-memory queue before later LDS reads: the
+// pipeline below orders these loads itself (s_waitcnt vmcnt + barrier).
+__device__ __forceinline__ void dma_to_lds16(const void* src, uint32_t lds_addr) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(lds_addr)
+      : "memory");
 }
 
+// Per-lane part of this wave's K-tile loads: wave-load u of wave w covers rows
+// (w*kLoadsPerWave + u) * kRowsPerLoad .. of a tile, always the same slots of a page and the
+// same (swizzled) 16-byte chunk, so the byte offset inside a page is fixed per segment.
 template <int D>
-__device__ __forceinline__ void store_k_tile(const u32x4 (&pre)[TileGeom<D>::kLoadsPerThread],
-                                             char* buf) {
+struct KLoadPlan {
+  uint32_t lane_off[TileGeom<D>::kLoadsPerWave];   // bytes from the page base (K plane)
+  int wl0;                                          // first wave-load index of this wave
+};
+
+template <int D>
+__device__ __forceinline__ KLoadPlan<D> make_k_load_plan(int h, int Hkv) {
+  using Gm = TileGeom<D>;
+  KLoadPlan<D> kp;
+  const int lane = threadIdx.x & 63;
+  kp.wl0 = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) * Gm::kLoadsPerWave;
+#pragma unroll
+  for (int u = 0; u < Gm::kLoadsPerWave; ++u) {
+    const int wl = kp.wl0 + u;
+    const int row = wl * Gm::kRowsPerLoad + lane / Gm::kChunks;
+    const int chunk = (lane % Gm::kChunks) ^ (row % Gm::kChunks);
+    const int slot = (wl * Gm::kRowsPerLoad) % kPageSize + lane / Gm::kChunks;
+    kp.lane_off[u] = (uint32_t)(((slot * Hkv + h) * D + chunk * 8) * 2);
+  }
+  return kp;
+}
+
+// This wave's share of K tile `tile` (keys 64*tile ..) of one request, fetched straight
+// into the LDS buffer at byte address `dst`.  Each wave-wide load covers kRowsPerLoad
+// consecutive keys inside one page, so the page id is wave-uniform and comes from a
+// scalar load.  Keys past L read slots of the request's last page (their results are
+// discarded); a page outside the pool is never dereferenced (page 0 is read instead).
+template <int D>
+__device__ __forceinline__ void issue_k_tile(uint32_t dst, const char* __restrict__ kv_bytes,
+                                             const int32_t* __restrict__ bt_row, int L,
+                                             int64_t page_bytes, int64_t num_pages,
+                                             const KLoadPlan<D>& kp, int64_t tile) {
   using Gm = TileGeom<D>;
 #pragma unroll
-  for (int u = 0; u < Gm::kLoadsPerThread; ++u) {
-    const int q = threadIdx.x + kThreads * u;
-    const int row = q / Gm::kChunksPerRow, ch = q % Gm::kChunksPerRow;
-    *reinterpret_cast<u32x4*>(buf + row * Gm::kStride + ch * 16) = pre[u];
+  for (int u = 0; u < Gm::kLoadsPerWave; ++u) {
+    const int wl = kp.wl0 + u;
+    const int64_t kbase = tile * kKeyTile + wl * Gm::kRowsPerLoad;   // wave-uniform
+    const int64_t kpage = (kbase < L ? kbase : L - 1) / kPageSize;
+    int64_t page = bt_row[kpage];
+    if (page < 0 || page >= num_pages) page = 0;
+    dma_to_lds16(kv_bytes + page * page_bytes + kp.lane_off[u], dst + (uint32_t)(wl * 1024));
   }
 }
 
@@ -86,10 +139,13 @@ __device__ __forceinline__ void read_k_operand(bf16x8 (&kreg)[TileGeom<D>::kStep
                                                const char* buf, int sub) {
   using Gm = TileGeom<D>;
   const int lane = threadIdx.x & 63;
-  const char* row = buf + (sub * 32 + (lane & 31)) * Gm::kStride + (lane >> 5) * 16;
+  const int row = sub * 32 + (lane & 31);
+  const char* base = buf + row * Gm::kRowBytes;
 #pragma unroll
-  for (int ks = 0; ks < Gm::kSteps; ++ks)
-    kreg[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(row + ks * 32));
+  for (int ks = 0; ks < Gm::kSteps; ++ks) {
+    const int slot = (2 * ks + (lane >> 5)) ^ (row % Gm::kChunks);
+    kreg[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(base + slot * 16));
+  }
 }
 
 // Query rows of tile `tile` of chunk c as the MFMA A (or B) operand: lane l holds row
@@ -124,35 +180,173 @@ __device__ __forceinline__ int chunk_row_tiles(int M, int c) {
   return rows <= 0 ? 1 : ceil_div(rows < kRowsPerChunk ? rows : kRowsPerChunk, 32);
 }
 
-struct ScoreArgs {
-  DevProblem dp;
-  const uint16_t* q;
-  const uint16_t* kv;
-  const int32_t* bt;
-  const float* lse;
-  float* scores;
-  float* score_part;
-  int64_t num_scores;
-};
 
 }  // namespace
 
-template <int D, bool kMaxMean>
-__global__ __launch_bounds__(kThreads, 1) void score_kernel(ScoreArgs a) {
+// Everything the key sweep of one segment needs besides the register-resident Q / beta.
+struct SweepCtx {
+  const char* kv_bytes;
+  const int32_t* bt_row;
+  const int32_t* pos_s;    // LDS: causal position of every row of the chunk
+  float* out;              // scores (or chunk partials) of this (request, KV head)
+  int64_t page_bytes, num_pages;
+  int64_t i0, i1;          // key tiles of this workgroup
+  int L, mask_from, G;
+  float alpha, out_scale;
+  uint32_t kl;             // LDS byte address of the K stages
+};
+
+// Sweep key tiles i0 .. i1-1 of one segment with TPW row tiles (of 32 rows) per wave:
+// kStages-1 tiles in flight through the direct-to-LDS pipeline, one barrier per tile, the
+// first key sub-tile's operands of tile i+1 read across the barrier that ends tile i.
+template <int D, bool kMaxMean, int TPW>
+__device__ __forceinline__ void score_sweep(const SweepCtx& cx, const KLoadPlan<D>& kp,
+                                            const bf16x8 (&qreg)[kTilesPerWave][TileGeom<D>::kSteps],
+                                            const float (&beta)[kTilesPerWave][16],
+                                            char (*kbuf)[TileGeom<D>::kTileBytes],
+                                            float (*red)[kWaves][kKeyTile]) {
   using Gm = TileGeom<D>;
-  __shared__ __align__(16) char kbuf[2][Gm::kTileBytes];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, l32 = lane & 31;
+#pragma unroll
+  for (int p = 0; p < kStages - 1; ++p)
+    issue_k_tile<D>(cx.kl + p * Gm::kTileBytes, cx.kv_bytes, cx.bt_row, cx.L, cx.page_bytes,
+                    cx.num_pages, kp, cx.i0 + p < cx.i1 ? cx.i0 + p : cx.i1 - 1);
+  wait_vmcnt<(kStages - 2) * Gm::kLoadsPerWave>();
+  __builtin_amdgcn_s_barrier();
+  bf16x8 ka[Gm::kSteps], kb[Gm::kSteps];
+  read_k_operand<D>(ka, kbuf[0], 0);
+  for (int64_t i = cx.i0; i < cx.i1; ++i) {
+    const int st = (int)((i - cx.i0) % kStages);
+    {
+      const int64_t nt = i + kStages - 1 < cx.i1 ? i + kStages - 1 : cx.i1 - 1;
+      issue_k_tile<D>(cx.kl + ((st + kStages - 1) % kStages) * Gm::kTileBytes, cx.kv_bytes,
+                      cx.bt_row, cx.L, cx.page_bytes, cx.num_pages, kp, nt);
+    }
+    const int64_t key0 = i * kKeyTile;
+    const bool needs_mask = key0 + kKeyTile - 1 > cx.mask_from;
+    float* rd = red[i & 1][w];
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      const bf16x8 (&kr)[Gm::kSteps] = sub == 0 ? ka : kb;
+      f32x16 e[TPW];
+#pragma unroll
+      for (int ti = 0; ti < TPW; ++ti) {
+        e[ti] = mfma32(qreg[ti][0], kr[0], f32x16{});
+#pragma unroll
+        for (int ks = 1; ks < Gm::kSteps; ++ks) e[ti] = mfma32(qreg[ti][ks], kr[ks], e[ti]);
+      }
+      if (sub == 0) read_k_operand<D>(kb, kbuf[st], 1);   // in flight under the epilogue
+#pragma unroll
+      for (int ti = 0; ti < TPW; ++ti) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          e[ti][v] = fast_exp2(__builtin_fmaf(e[ti][v], cx.alpha, -beta[ti][v]));
+      }
+      if (needs_mask) {
+        const int key = (int)(key0 + sub * 32 + l32);
+#pragma unroll
+        for (int ti = 0; ti < TPW; ++ti) {
+          const int32_t* prow = cx.pos_s + (w + kWaves * ti) * 32 + 4 * hf;
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if (key > prow[8 * (v / 4) + (v % 4)]) e[ti][v] = 0.f;
+        }
+      }
+      float acc;
+      if (!kMaxMean) {
+        float a0 = e[0][0], a1 = e[0][1];
+#pragma unroll
+        for (int v = 2; v < 16; v += 2) { a0 += e[0][v]; a1 += e[0][v + 1]; }
+#pragma unroll
+        for (int ti = 1; ti < TPW; ++ti)
+#pragma unroll
+          for (int v = 0; v < 16; v += 2) { a0 += e[ti][v]; a1 += e[ti][v + 1]; }
+        acc = a0 + a1;
+      } else {
+        float a0 = 0.f, a1 = 0.f;
+        const int G = cx.G;
+#pragma unroll
+        for (int ti = 0; ti < TPW; ++ti) {
+          const f32x16& x = e[ti];
+          if (G == 16) {
+            // the lane's 16 rows are one query's whole group
+            float mx = x[0];
+#pragma unroll
+            for (int v = 1; v < 16; ++v) mx = fmaxf(mx, x[v]);
+            a0 += mx;
+          } else if (G == 8) {
+            // registers 0-7 and 8-15 are two queries' groups
+            float m0 = x[0], m1 = x[8];
+#pragma unroll
+            for (int v = 1; v < 8; ++v) { m0 = fmaxf(m0, x[v]); m1 = fmaxf(m1, x[8 + v]); }
+            a0 += m0; a1 += m1;
+          } else {
+            // registers v0..v0+3 are four consecutive rows of the natural order
+#pragma unroll
+            for (int v0 = 0; v0 < 16; v0 += 4) {
+              if (G == 4) {
+                a0 += fmaxf(fmaxf(x[v0], x[v0 + 1]), fmaxf(x[v0 + 2], x[v0 + 3]));
+              } else if (G == 2) {
+                a0 += fmaxf(x[v0], x[v0 + 1]);
+                a1 += fmaxf(x[v0 + 2], x[v0 + 3]);
+              } else {
+                a0 += x[v0] + x[v0 + 2];
+                a1 += x[v0 + 1] + x[v0 + 3];
+              }
+            }
+          }
+        }
+        acc = a0 + a1;
+      }
+      acc += __shfl_xor(acc, 32, 64);   // lanes l and l+32 hold the same key
+      if (hf == 0) rd[sub * 32 + l32] = acc;
+    }
+    // tile i+1 has landed (only later tiles' loads may be outstanding) and every wave's
+    // partial sums of tile i are in LDS
+    wait_vmcnt<(kStages - 2) * Gm::kLoadsPerWave>();
+    wait_lgkmcnt0();
+    __builtin_amdgcn_s_barrier();
+    if (i + 1 < cx.i1) read_k_operand<D>(ka, kbuf[(st + 1) % kStages], 0);
+    // wave w finishes keys 8w .. 8w+7 of tile i (fixed summation order over waves)
+    if (lane < kKeyTile / kWaves) {
+      const int kk = w * (kKeyTile / kWaves) + lane;
+      const int64_t key = key0 + kk;
+      if (key < cx.L) {
+        float v = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < kWaves; ++ww) v += red[i & 1][ww][kk];
+        cx.out[key] = v * cx.out_scale;
+      }
+    }
+  }
+}
+
+template <int D, bool kMaxMean>
+__global__ __launch_bounds__(kThreads, 1) void score_kernel(
+    DevProblem dp, const uint16_t* __restrict__ q_ptr, const uint16_t* __restrict__ kv_ptr,
+    const int32_t* __restrict__ bt_ptr, const float* __restrict__ lse_ptr,
+    float* __restrict__ scores_ptr, float* __restrict__ part_ptr, int64_t num_scores) {
+  using Gm = TileGeom<D>;
+  __shared__ __align__(1024) char kbuf[kStages][Gm::kTileBytes];
   __shared__ __align__(16) float beta_s[kRowsPerChunk];
   __shared__ __align__(16) int32_t pos_s[kRowsPerChunk];
   __shared__ float red[2][kWaves][kKeyTile];
 
-  const DevProblem& dp = a.dp;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hf = lane >> 5, l32 = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hf = lane >> 5;
   const int G = dp.G, Hq = dp.Hq, Hkv = dp.Hkv, C = dp.max_chunks;
-  const float alpha = dp.sm_scale * kLog2e;
   const int64_t nseg = dp.num_segments;
   const int64_t total = dp.seg_cost[nseg];
   const int64_t c0 = total * blockIdx.x / gridDim.x, c1 = total * (blockIdx.x + 1) / gridDim.x;
   if (c0 >= c1) return;
+
+  SweepCtx cx;
+  cx.kv_bytes = reinterpret_cast<const char*>(kv_ptr);
+  cx.pos_s = pos_s;
+  cx.page_bytes = (int64_t)kPageSize * Hkv * D * 2;
+  cx.num_pages = dp.num_pages;
+  cx.G = G;
+  cx.alpha = dp.sm_scale * kLog2e;
+  cx.kl = (uint32_t)(uintptr_t)(lds_char*)&kbuf[0][0];
 
   // first segment: the largest s with seg_cost[s] <= c0 (it is never empty)
   int64_t lo = 0, hi = nseg;
@@ -171,36 +365,37 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(ScoreArgs a) {
     const int L = pl.L, n = pl.n, M = G * n;
     const int RT = chunk_row_tiles(M, c);
     const int64_t ntiles = ceil_div64(L, kKeyTile);
-    const int64_t i0 = first ? (c0 - cs + RT - 1) / RT : 0;
-    int64_t i1 = (c1 - cs + RT - 1) / RT;
-    if (i1 > ntiles) i1 = ntiles;
+    cx.i0 = first ? (c0 - cs + RT - 1) / RT : 0;
+    cx.i1 = (c1 - cs + RT - 1) / RT;
+    if (cx.i1 > ntiles) cx.i1 = ntiles;
     first = false;
-    if (i0 >= i1) continue;
+    if (cx.i0 >= cx.i1) continue;
 
     // ---- segment setup: beta / causal position of every row, Q rows into registers
-    __syncthreads();  // LDS of the previous segment no longer in use
+    wait_vmcnt<0>();   // no load of the previous segment may still land in a K buffer
+    __syncthreads();
     for (int m = tid; m < kRowsPerChunk; m += kThreads) {
       int j, g;
       row_to_query(G, c, m / 32, m % 32, &j, &g);
-      beta_s[m] = j < n ? a.lse[(int64_t)(pl.q_off + j) * Hq + h * G + g] * kLog2e
+      beta_s[m] = j < n ? lse_ptr[(int64_t)(pl.q_off + j) * Hq + h * G + g] * kLog2e
                         : __builtin_inff();
       pos_s[m] = dp.causal ? L - n + j : L - 1;
     }
     bf16x8 qreg[kTilesPerWave][Gm::kSteps];
 #pragma unroll
     for (int ti = 0; ti < kTilesPerWave; ++ti)
-      if (w + kWaves * ti < RT) load_q_tile<D>(qreg[ti], a.q, G, Hq, h, pl.q_off, n, c, w + kWaves * ti);
-    const int32_t* bt_row = a.bt + (int64_t)r * dp.bt_stride;
-    const float out_scale = (kMaxMean && pl.nchunk == 1) ? (n > 0 ? 1.0f / n : 0.0f) : 1.0f;
-    float* out = (c == 0) ? a.scores + pl.seg_off + (int64_t)h * L
-                          : a.score_part + (int64_t)(c - 1) * a.num_scores + pl.seg_off +
-                                (int64_t)h * L;
-    const int mask_from = dp.causal ? L - n : L;  // keys past this may be hidden from rows
-
-    u32x4 pre[Gm::kLoadsPerThread];
-    load_k_tile<D>(pre, a.kv, bt_row, L, h, Hkv, dp.num_pages, i0);
-    store_k_tile<D>(pre, kbuf[0]);
-    __syncthreads();
+      load_q_tile<D>(qreg[ti], q_ptr, G, Hq, h, pl.q_off, n, c, w + kWaves * ti);
+    cx.bt_row = bt_ptr + (int64_t)r * dp.bt_stride;
+    cx.L = L;
+    cx.mask_from = dp.causal ? L - n : L;  // keys past this may be hidden from some rows
+    cx.out_scale = (kMaxMean && pl.nchunk == 1) ? (n > 0 ? 1.0f / n : 0.0f) : 1.0f;
+    cx.out = (c == 0) ? scores_ptr + pl.seg_off + (int64_t)h * L
+                      : part_ptr + (int64_t)(c - 1) * num_scores + pl.seg_off + (int64_t)h * L;
+    const KLoadPlan<D> kp = make_k_load_plan<D>(h, Hkv);
+    // every ordinary load of the setup has landed before the K pipeline starts, so the
+    // sweep needs no compiler-inserted wait on the vector-memory queue
+    wait_vmcnt<0>();
+    __syncthreads();   // beta_s / pos_s visible
     // beta of this lane's 16 rows per row tile: rows 8*aa + 4*hf + i
     float beta[kTilesPerWave][16];
 #pragma unroll
@@ -208,91 +403,19 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(ScoreArgs a) {
       const float* brow = beta_s + (w + kWaves * ti) * 32 + 4 * hf;
 #pragma unroll
       for (int aa = 0; aa < 4; ++aa) {
-        const float4 b4 = (w + kWaves * ti < RT) ? *reinterpret_cast<const float4*>(brow + 8 * aa)
-                                                 : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 b4 = *reinterpret_cast<const float4*>(brow + 8 * aa);
         beta[ti][4 * aa + 0] = b4.x; beta[ti][4 * aa + 1] = b4.y;
         beta[ti][4 * aa + 2] = b4.z; beta[ti][4 * aa + 3] = b4.w;
       }
     }
-
-    // ---- pipelined sweep over key tiles i0 .. i1-1
-    int buf = 0;
-    for (int64_t i = i0; i < i1; ++i) {
-      const bool has_next = i + 1 < i1;
-      if (has_next) load_k_tile<D>(pre, a.kv, bt_row, L, h, Hkv, dp.num_pages, i + 1);
-      const int64_t key0 = i * kKeyTile;
-      const bool needs_mask = key0 + kKeyTile - 1 > mask_from;
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub) {
-        bf16x8 kreg[Gm::kSteps];
-        read_k_operand<D>(kreg, kbuf[buf], sub);
-        const int key = (int)(key0 + sub * 32 + l32);
-        float sacc0 = 0.f, sacc1 = 0.f;
-#pragma unroll
-        for (int ti = 0; ti < kTilesPerWave; ++ti) {
-          const int tile = w + kWaves * ti;
-          if (tile < RT) {
-            f32x16 p = {};
-#pragma unroll
-            for (int ks = 0; ks < Gm::kSteps; ++ks) p = mfma32(qreg[ti][ks], kreg[ks], p);
-#pragma unroll
-            for (int v = 0; v < 16; ++v) p[v] = fast_exp2(__builtin_fmaf(p[v], alpha, -beta[ti][v]));
-            if (needs_mask) {
-              const int32_t* prow = pos_s + tile * 32 + 4 * hf;
-#pragma unroll
-              for (int v = 0; v < 16; ++v)
-                if (key > prow[8 * (v / 4) + (v % 4)]) p[v] = 0.f;
-            }
-            if (!kMaxMean) {
-#pragma unroll
-              for (int v = 0; v < 16; v += 2) { sacc0 += p[v]; sacc1 += p[v + 1]; }
-            } else if (G == 16) {
-              // the lane's 16 rows are one query's whole group
-              float mx = p[0];
-#pragma unroll
-              for (int v = 1; v < 16; ++v) mx = fmaxf(mx, p[v]);
-              sacc0 += mx;
-            } else if (G == 8) {
-              // registers 0-7 and 8-15 are two queries' groups
-              float m0 = p[0], m1 = p[8];
-#pragma unroll
-              for (int v = 1; v < 8; ++v) { m0 = fmaxf(m0, p[v]); m1 = fmaxf(m1, p[8 + v]); }
-              sacc0 += m0; sacc1 += m1;
-            } else {
-              // registers v0..v0+3 are four consecutive rows of the natural order
-#pragma unroll
-              for (int v0 = 0; v0 < 16; v0 += 4) {
-                if (G == 4) {
-                  sacc0 += fmaxf(fmaxf(p[v0], p[v0 + 1]), fmaxf(p[v0 + 2], p[v0 + 3]));
-                } else if (G == 2) {
-                  sacc0 += fmaxf(p[v0], p[v0 + 1]);
-                  sacc1 += fmaxf(p[v0 + 2], p[v0 + 3]);
-                } else {
-                  sacc0 += p[v0] + p[v0 + 2];
-                  sacc1 += p[v0 + 1] + p[v0 + 3];
-                }
-              }
-            }
-          }
-        }
-        float acc = sacc0 + sacc1;
-        acc += __shfl_xor(acc, 32, 64);   // lanes l and l+32 hold the same key
-        if (hf == 0) red[buf][w][sub * 32 + l32] = acc;
-      }
-      if (has_next) store_k_tile<D>(pre, kbuf[buf ^ 1]);
-      __syncthreads();
-      if (tid < kKeyTile) {
-        const int64_t key = key0 + tid;
-        if (key < L) {
-          float v = 0.f;
-#pragma unroll
-          for (int ww = 0; ww < kWaves; ++ww) v += red[buf][ww][tid];
-          out[key] = v * out_scale;
-        }
-      }
-      buf ^= 1;
-    }
+    // rows past the chunk's row tiles are all padding (Q = 0, beta = +inf): skip the
+    // second row tile of every wave when the chunk has at most kWaves row tiles
+    if (RT > kWaves)
+      score_sweep<D, kMaxMean, 2>(cx, kp, qreg, beta, kbuf, red);
+    else
+      score_sweep<D, kMaxMean, 1>(cx, kp, qreg, beta, kbuf, red);
   }
+  wait_vmcnt<0>();   // drain: no LDS write may be outstanding when the workgroup exits
 }
 
 // scores = (scores + sum_{c >= 1} partial_c) * scale, for requests scored in several row
@@ -316,8 +439,8 @@ hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
                         const void* kv, const int32_t* bt, const float* lse, float* scores,
                         float* score_part, hipStream_t s) {
   if (hp.num_scores == 0) return hipSuccess;
-  ScoreArgs a{dp, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(kv), bt, lse,
-              scores, score_part, hp.num_scores};
+  const uint16_t* qq = static_cast<const uint16_t*>(q);
+  const uint16_t* kk = static_cast<const uint16_t*>(kv);
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess) {
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 256;
@@ -326,11 +449,11 @@ hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
   if (grid > hp.score_cost) grid = hp.score_cost > 0 ? hp.score_cost : 1;
   const bool mm = dp.agg == ACTKV_AGG_MAX_MEAN;
   if (dp.D == 128) {
-    if (mm) hipLaunchKernelGGL((score_kernel<128, true>), dim3(grid), dim3(kThreads), 0, s, a);
-    else hipLaunchKernelGGL((score_kernel<128, false>), dim3(grid), dim3(kThreads), 0, s, a);
+    if (mm) hipLaunchKernelGGL((score_kernel<128, true>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, hp.num_scores);
+    else hipLaunchKernelGGL((score_kernel<128, false>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, hp.num_scores);
   } else {
-    if (mm) hipLaunchKernelGGL((score_kernel<64, true>), dim3(grid), dim3(kThreads), 0, s, a);
-    else hipLaunchKernelGGL((score_kernel<64, false>), dim3(grid), dim3(kThreads), 0, s, a);
+    if (mm) hipLaunchKernelGGL((score_kernel<64, true>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, hp.num_scores);
+    else hipLaunchKernelGGL((score_kernel<64, false>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, hp.num_scores);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -350,11 +473,12 @@ hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
 // kernel combines the partials of a row in order.
 // ---------------------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void lse_partial_kernel(DevProblem dp, const uint16_t* q,
-                                                                  const uint16_t* kv,
-                                                                  const int32_t* bt, float2* part) {
+__global__ __launch_bounds__(kThreads, 1) void lse_partial_kernel(
+    DevProblem dp, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kv,
+    const int32_t* __restrict__ bt, float2* __restrict__ part) {
   using Gm = TileGeom<D>;
-  __shared__ __align__(16) char kbuf[2][Gm::kTileBytes];
+  __shared__ __align__(1024) char kbuf[kStages][Gm::kTileBytes];
+  const uint32_t kl = (uint32_t)(uintptr_t)(lds_char*)&kbuf[0][0];
   const int kb = blockIdx.x, ch = blockIdx.y / dp.Hkv, h = blockIdx.y % dp.Hkv, r = blockIdx.z;
   const ReqPlan pl = dp.plan[r];
   if (kb >= pl.lse_blocks || ch >= pl.nchunk) return;
@@ -362,7 +486,14 @@ __global__ __launch_bounds__(kThreads, 1) void lse_partial_kernel(DevProblem dp,
   const int G = dp.G, Hq = dp.Hq, Hkv = dp.Hkv, L = pl.L, n = pl.n, M = G * n;
   const int RT = chunk_row_tiles(M, ch);
   const float alpha = dp.sm_scale * kLog2e;
-
+  const int32_t* bt_row = bt + (int64_t)r * dp.bt_stride;
+  const char* kv_bytes = reinterpret_cast<const char*>(kv);
+  const int64_t page_bytes = (int64_t)kPageSize * Hkv * D * 2;
+  const KLoadPlan<D> kp = make_k_load_plan<D>(h, Hkv);
+  const int64_t t0 = (int64_t)kb * (kLseKeysPerBlock / kKeyTile);
+  int64_t t1 = t0 + kLseKeysPerBlock / kKeyTile;
+  const int64_t ntiles = ceil_div64(L, kKeyTile);
+  if (t1 > ntiles) t1 = ntiles;
   bf16x8 qreg[kTilesPerWave][Gm::kSteps];
   int pos[kTilesPerWave];
   float rm[kTilesPerWave], rs[kTilesPerWave];
@@ -379,24 +510,24 @@ __global__ __launch_bounds__(kThreads, 1) void lse_partial_kernel(DevProblem dp,
       pos[ti] = j < n ? (dp.causal ? L - n + j : L - 1) : -1;
     }
   }
-  const int32_t* bt_row = bt + (int64_t)r * dp.bt_stride;
-  const int64_t t0 = (int64_t)kb * (kLseKeysPerBlock / kKeyTile);
-  int64_t t1 = t0 + kLseKeysPerBlock / kKeyTile;
-  const int64_t ntiles = ceil_div64(L, kKeyTile);
-  if (t1 > ntiles) t1 = ntiles;
-
-  u32x4 pre[Gm::kLoadsPerThread];
-  load_k_tile<D>(pre, kv, bt_row, L, h, Hkv, dp.num_pages, t0);
-  store_k_tile<D>(pre, kbuf[0]);
-  __syncthreads();
-  int buf = 0;
+  wait_vmcnt<0>();   // Q is in registers before the K pipeline starts
+#pragma unroll
+  for (int p = 0; p < kStages - 1; ++p)
+    issue_k_tile<D>(kl + p * Gm::kTileBytes, kv_bytes, bt_row, L, page_bytes, dp.num_pages, kp,
+                    t0 + p < t1 ? t0 + p : t1 - 1);
   for (int64_t i = t0; i < t1; ++i) {
-    const bool has_next = i + 1 < t1;
-    if (has_next) load_k_tile<D>(pre, kv, bt_row, L, h, Hkv, dp.num_pages, i + 1);
+    const int st = (int)((i - t0) % kStages);
+    wait_vmcnt<(kStages - 2) * Gm::kLoadsPerWave>();
+    __builtin_amdgcn_s_barrier();
+    {
+      const int64_t nt = i + kStages - 1 < t1 ? i + kStages - 1 : t1 - 1;
+      issue_k_tile<D>(kl + ((st + kStages - 1) % kStages) * Gm::kTileBytes, kv_bytes, bt_row, L,
+                      page_bytes, dp.num_pages, kp, nt);
+    }
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
       bf16x8 kreg[Gm::kSteps];
-      read_k_operand<D>(kreg, kbuf[buf], sub);
+      read_k_operand<D>(kreg, kbuf[st], sub);
       const int keybase = (int)(i * kKeyTile + sub * 32 + 4 * hf);
 #pragma unroll
       for (int ti = 0; ti < kTilesPerWave; ++ti) {
@@ -421,10 +552,8 @@ __global__ __launch_bounds__(kThreads, 1) void lse_partial_kernel(DevProblem dp,
         }
       }
     }
-    if (has_next) store_k_tile<D>(pre, kbuf[buf ^ 1]);
-    __syncthreads();
-    buf ^= 1;
   }
+  wait_vmcnt<0>();
   // combine the two lanes that share a query row, then write one partial per row
 #pragma unroll
   for (int ti = 0; ti < kTilesPerWave; ++ti) {
