@@ -77,7 +77,7 @@ typedef enum actkv_agg {
 typedef struct actkv_problem {
   int32_t num_reqs;         /* R >= 0                                                    */
   int32_t num_q_heads;      /* Hq > 0, a multiple of num_kv_heads                        */
-  int32_t num_kv_heads;     /* Hkv > 0                                                   */
+  int32_t num_kv_heads;     /* Hkv: 1..64                                                */
   int32_t head_dim;         /* D: 64 or 128                                              */
   int32_t page_size;        /* slots per page: 16                                        */
   int64_t num_pages;        /* physical pages in kv_cache                                */

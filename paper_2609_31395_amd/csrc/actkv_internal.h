@@ -40,6 +40,7 @@ struct HostPlan {
   int64_t score_cost = 0;         // total scoring cost units (key tiles x row tiles)
   int64_t lse_parts = 0;          // sum_r n_r * Hq * lse_blocks_r
   int64_t max_lse_blocks = 0;     // max_r ceil(L_r / kLseKeysPerBlock)
+  int64_t max_L = 0;              // longest request
 };
 
 // Byte offsets of the workspace regions (each 256-byte aligned).

@@ -27,6 +27,7 @@ actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
   if (!isfinite(p->sm_scale) || p->sm_scale < 0.f) return ACTKV_ERR_INVALID_ARGUMENT;
   if (p->head_dim != 64 && p->head_dim != 128) return ACTKV_ERR_UNSUPPORTED;
   if (p->page_size != actkv::kPageSize) return ACTKV_ERR_UNSUPPORTED;
+  if (p->num_kv_heads > 64) return ACTKV_ERR_UNSUPPORTED;
   const int32_t G = p->num_q_heads / p->num_kv_heads;
   if (p->agg == ACTKV_AGG_MAX_MEAN && !(G == 1 || G == 2 || G == 4 || G == 8 || G == 16))
     return ACTKV_ERR_UNSUPPORTED;
@@ -67,6 +68,7 @@ actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
     }
     hp->sum_n += n;
     hp->sum_L += L;
+    hp->max_L = L > hp->max_L ? L : hp->max_L;
     const int64_t ntiles = (L + actkv::kKeyTile - 1) / actkv::kKeyTile;
     const int64_t M = n * G;
     const int32_t chunks = M > 0 ? (int32_t)((M + actkv::kRowsPerChunk - 1) / actkv::kRowsPerChunk) : 1;

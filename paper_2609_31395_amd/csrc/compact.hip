@@ -3,63 +3,93 @@
 // row is then rewritten and the old pages returned (Sec. 7.2: freed blocks go back to the
 // serving system).
 //
-// compact_gather_kernel: one 256-thread workgroup per destination (fresh) page.  It writes
-// the page's K half and V half contiguously ([slot][head][D] rows, 16 bytes per lane, one
-// 256-byte row per 16 lanes) and reads each source row as one contiguous 256-byte run
-// through the OLD block table.  Destination pages are disjoint from every live page, so
-// all copies are independent and need no ordering among themselves.
+// compact_gather_kernel: one 256-thread workgroup per group of destination (fresh) pages.
+// It first resolves every (page, slot, head) to its source slot through the kept indices
+// and the OLD block table (one lookup per thread, into LDS), then streams the rows: each
+// destination page is written contiguously ([slot][head][D] rows, 16 bytes per lane) and
+// each source row is read as one contiguous run.  Destination pages are disjoint from
+// every live page, so all copies are independent and need no ordering among themselves.
 // compact_rewrite_kernel (runs after the gather, same stream): copies the old block-table
 // row into freed_pages and writes the new row, so the gather never races the rewrite.
 #include "device_common.hpp"
 
 namespace actkv {
 
+constexpr int kCompactThreads = 256;
+constexpr int kCompactTable = 1024;   // (page, slot, head) source entries per workgroup
+
+// Fresh pages handled by one workgroup: enough (page, slot, head) rows to give every
+// thread one source lookup, at least one page.
+__host__ __device__ inline int compact_pages_per_wg(int Hkv) {
+  const int p = kCompactThreads / (kPageSize * Hkv);
+  return p < 1 ? 1 : p;
+}
+
 template <int D>
-__global__ __launch_bounds__(256) void compact_gather_kernel(DevProblem dp, uint16_t* kv,
-                                                             const int32_t* __restrict__ bt,
-                                                             const int32_t* __restrict__ kept,
-                                                             const int32_t* __restrict__ free_pages) {
+__global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
+    DevProblem dp, uint16_t* kv, const int32_t* __restrict__ bt, const int32_t* __restrict__ kept,
+    const int32_t* __restrict__ free_pages, int64_t num_fresh) {
   constexpr int CH = D / 8;                 // 16-byte chunks per row
+  __shared__ int64_t src_slot[kCompactTable];   // flat source slot, -1: nothing to copy
+  __shared__ int64_t dst_page[kCompactTable / kPageSize];
   const int Hkv = dp.Hkv;
-  const int64_t f = blockIdx.x;
-  // request owning fresh page f: the largest r with fresh_off[r] <= f
-  int lo = 0, hi = dp.R - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) / 2;
-    if (dp.plan[mid].fresh_off <= f) lo = mid; else hi = mid - 1;
+  const int ppw = compact_pages_per_wg(Hkv);
+  const int64_t f0 = (int64_t)blockIdx.x * ppw;
+  const int npages = (int)(num_fresh - f0 < ppw ? num_fresh - f0 : ppw);
+  const int entries = npages * kPageSize * Hkv;
+
+  // ---- resolve every (page, slot, head) of this workgroup to its source slot once
+  for (int e = threadIdx.x; e < entries; e += kCompactThreads) {
+    const int p = e / (kPageSize * Hkv), s = (e / Hkv) % kPageSize, h = e % Hkv;
+    const int64_t f = f0 + p;
+    // request owning fresh page f: the largest r with fresh_off[r] <= f
+    int lo = 0, hi = dp.R - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) / 2;
+      if (dp.plan[mid].fresh_off <= f) lo = mid; else hi = mid - 1;
+    }
+    const ReqPlan pl = dp.plan[lo];
+    const int j = (int)(f - pl.fresh_off) * kPageSize + s;
+    const int bh = dp.budgets[lo * Hkv + h];
+    const int kh = bh < pl.L ? bh : pl.L;
+    int64_t src = -1;
+    if (j < kh) {
+      const int t = kept[dp.kept_off[lo * Hkv + h] + j];
+      if (t >= 0 && t < pl.L) {
+        const int64_t page = bt[(int64_t)lo * dp.bt_stride + t / kPageSize];
+        // pages outside the pool are never dereferenced (the slot is left unwritten)
+        if (page >= 0 && page < dp.num_pages) src = page * kPageSize + t % kPageSize;
+      }
+    }
+    src_slot[e] = src;
+    if (s == 0 && h == 0) {
+      const int64_t dpg = free_pages[f];
+      dst_page[p] = (dpg >= 0 && dpg < dp.num_pages) ? dpg : -1;
+    }
   }
-  const int r = lo;
-  const ReqPlan pl = dp.plan[r];
-  const int p = (int)(f - pl.fresh_off);
-  const int64_t dst_page = free_pages[f];
-  const int32_t* bt_row = bt + (int64_t)r * dp.bt_stride;
+  __syncthreads();
+
+  // ---- copy: consecutive threads move consecutive 16-byte chunks of the destination pages
+  // (K half, then V half), so every store is part of a contiguous run
   const int64_t plane = dp.num_pages * kPageSize * Hkv * (int64_t)D;   // K -> V offset
-  const int items = 2 * kPageSize * Hkv * CH;
-  constexpr int kBatch = 8;
-  for (int base = 0; base < items; base += 256 * kBatch) {
+  const int rows = 2 * entries;
+  const int items = rows * CH;
+  constexpr int kBatch = 16;
+  for (int base = 0; base < items; base += kCompactThreads * kBatch) {
     u32x4 v[kBatch];
     int64_t dst[kBatch];
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       dst[u] = -1;
-      const int it = base + 256 * u + threadIdx.x;
+      const int it = base + kCompactThreads * u + threadIdx.x;
       if (it >= items) continue;
-      const int which = it / (kPageSize * Hkv * CH);
-      const int rem = it % (kPageSize * Hkv * CH);
-      const int s = rem / (Hkv * CH), h = (rem / CH) % Hkv, ch = rem % CH;
-      const int j = p * kPageSize + s;
-      const int bh = dp.budgets[r * Hkv + h];
-      const int kh = bh < pl.L ? bh : pl.L;
-      if (j >= kh) continue;
-      const int t = kept[dp.kept_off[r * Hkv + h] + j];
-      if (t < 0 || t >= pl.L) continue;
-      const int64_t src_page = bt_row[t / kPageSize];
-      // pages outside the pool are never dereferenced (the slot is left unwritten)
-      if (src_page < 0 || src_page >= dp.num_pages || dst_page < 0 || dst_page >= dp.num_pages)
-        continue;
-      const int64_t src = which * plane + ((src_page * kPageSize + t % kPageSize) * Hkv + h) * (int64_t)D + ch * 8;
-      dst[u] = which * plane + ((dst_page * kPageSize + s) * Hkv + h) * (int64_t)D + ch * 8;
-      v[u] = *reinterpret_cast<const u32x4*>(kv + src);
+      const int row = it / CH, ch = it % CH;
+      const int which = row / entries, e = row % entries;
+      const int p = e / (kPageSize * Hkv), s = (e / Hkv) % kPageSize, h = e % Hkv;
+      const int64_t src = src_slot[e], dpg = dst_page[p];
+      if (src < 0 || dpg < 0) continue;
+      dst[u] = which * plane + ((dpg * kPageSize + s) * Hkv + h) * (int64_t)D + ch * 8;
+      v[u] = *reinterpret_cast<const u32x4*>(kv + which * plane + (src * Hkv + h) * (int64_t)D + ch * 8);
     }
 #pragma unroll
     for (int u = 0; u < kBatch; ++u)
@@ -91,12 +121,14 @@ hipError_t launch_compact(const DevProblem& dp, const HostPlan& hp, void* kv, in
                           int32_t* new_lens, hipStream_t s) {
   if (hp.R == 0) return hipSuccess;
   if (hp.fresh_needed > 0) {
+    const int ppw = compact_pages_per_wg(hp.Hkv);
+    const unsigned grid = (unsigned)((hp.fresh_needed + ppw - 1) / ppw);
     if (dp.D == 128)
-      hipLaunchKernelGGL(compact_gather_kernel<128>, dim3((unsigned)hp.fresh_needed), dim3(256), 0, s,
-                         dp, static_cast<uint16_t*>(kv), bt, kept, free_pages);
+      hipLaunchKernelGGL(compact_gather_kernel<128>, dim3(grid), dim3(kCompactThreads), 0, s, dp,
+                         static_cast<uint16_t*>(kv), bt, kept, free_pages, hp.fresh_needed);
     else
-      hipLaunchKernelGGL(compact_gather_kernel<64>, dim3((unsigned)hp.fresh_needed), dim3(256), 0, s,
-                         dp, static_cast<uint16_t*>(kv), bt, kept, free_pages);
+      hipLaunchKernelGGL(compact_gather_kernel<64>, dim3(grid), dim3(kCompactThreads), 0, s, dp,
+                         static_cast<uint16_t*>(kv), bt, kept, free_pages, hp.fresh_needed);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -30,25 +30,32 @@ namespace actkv {
 
 namespace {
 
-constexpr int kThreads = 512;   // 8 waves: two per SIMD at one workgroup per CU
+// Scoring: 4 waves per workgroup, 4 row tiles (128 query rows) per wave, two workgroups per
+// CU.  The two waves sharing a SIMD belong to different workgroups, so their barriers are
+// independent and one wave's exp2 epilogue runs beside the other's MFMAs.
+constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kTilesPerWave = kRowsPerChunk / 32 / kWaves;   // 2 row tiles of 32 rows
-constexpr int kStages = 4;      // K tiles in flight / resident in LDS
+constexpr int kTilesPerWave = kRowsPerChunk / 32 / kWaves;   // 4 row tiles of 32 rows
+constexpr int kStages = 3;      // K tiles resident in LDS (two in flight)
+// The LSE pass keeps 8 waves x 2 row tiles (its per-row running max/sum stay in registers).
+constexpr int kLseThreads = 512;
+constexpr int kLseWaves = kLseThreads / 64;
+constexpr int kLseTilesPerWave = kRowsPerChunk / 32 / kLseWaves;
 
 // Geometry of one K tile (kKeyTile keys of one KV head) in LDS.  Rows are not padded;
 // instead the 16-byte chunk c of row r sits in slot c ^ (r % kChunks), which keeps both
 // the direct-to-LDS loads (64 lanes write one contiguous KiB) and the MFMA operand reads
 // (lanes l and l+1 read rows r, r+1 at the same logical chunk) free of bank conflicts.
-template <int D>
+template <int D, int W = kWaves>
 struct TileGeom {
   static constexpr int kSteps = D / 16;                  // MFMA k-steps per row
   static constexpr int kRowBytes = D * 2;
   static constexpr int kChunks = D / 8;                  // 16-byte chunks per row
   static constexpr int kTileBytes = kKeyTile * kRowBytes;
   static constexpr int kWaveLoads = kTileBytes / 1024;   // one KiB per wave-wide load
-  static constexpr int kLoadsPerWave = kWaveLoads / kWaves;
+  static constexpr int kLoadsPerWave = kWaveLoads / W;   // W waves share a tile's loads
   static constexpr int kRowsPerLoad = 1024 / kRowBytes;
-  static_assert(kWaveLoads % kWaves == 0, "tile must split evenly over the waves");
+  static_assert(kWaveLoads % W == 0, "tile must split evenly over the waves");
 };
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
@@ -87,16 +94,16 @@ __device__ __forceinline__ void dma_to_lds16(const void* src, uint32_t lds_addr)
 // Per-lane part of this wave's K-tile loads: wave-load u of wave w covers rows
 // (w*kLoadsPerWave + u) * kRowsPerLoad .. of a tile, always the same slots of a page and the
 // same (swizzled) 16-byte chunk, so the byte offset inside a page is fixed per segment.
-template <int D>
+template <int D, int W>
 struct KLoadPlan {
-  uint32_t lane_off[TileGeom<D>::kLoadsPerWave];   // bytes from the page base (K plane)
-  int wl0;                                          // first wave-load index of this wave
+  uint32_t lane_off[TileGeom<D, W>::kLoadsPerWave];   // bytes from the page base (K plane)
+  int wl0;                                             // first wave-load index of this wave
 };
 
-template <int D>
-__device__ __forceinline__ KLoadPlan<D> make_k_load_plan(int h, int Hkv) {
-  using Gm = TileGeom<D>;
-  KLoadPlan<D> kp;
+template <int D, int W>
+__device__ __forceinline__ KLoadPlan<D, W> make_k_load_plan(int h, int Hkv) {
+  using Gm = TileGeom<D, W>;
+  KLoadPlan<D, W> kp;
   const int lane = threadIdx.x & 63;
   kp.wl0 = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) * Gm::kLoadsPerWave;
 #pragma unroll
@@ -110,26 +117,37 @@ __device__ __forceinline__ KLoadPlan<D> make_k_load_plan(int h, int Hkv) {
   return kp;
 }
 
-// This wave's share of K tile `tile` (keys 64*tile ..) of one request, fetched straight
-// into the LDS buffer at byte address `dst`.  Each wave-wide load covers kRowsPerLoad
-// consecutive keys inside one page, so the page id is wave-uniform and comes from a
-// scalar load.  Keys past L read slots of the request's last page (their results are
-// discarded); a page outside the pool is never dereferenced (page 0 is read instead).
-template <int D>
+// Every wave-wide load of one wave within a K tile falls in the same page: the tile's keys
+// 64*tile .. are split over the waves in runs of kRowsPerLoad * kLoadsPerWave = 16 keys
+// (64 keys over 4 waves, or over 8 waves with two loads per page).  page_of() is the
+// wave-uniform page id of that run (keys past L map to the request's last page); it is
+// fetched a tile ahead so that the scalar load never stalls the DMA issue.
+template <int D, int W>
+__device__ __forceinline__ int64_t page_of(const int32_t* __restrict__ bt_row, int L,
+                                           int64_t num_pages, const KLoadPlan<D, W>& kp,
+                                           int64_t tile) {
+  using Gm = TileGeom<D, W>;
+  const int64_t kbase = tile * kKeyTile + kp.wl0 * Gm::kRowsPerLoad;   // wave-uniform
+  int64_t page = bt_row[(kbase < L ? kbase : L - 1) / kPageSize];
+  if (page < 0 || page >= num_pages) page = 0;   // never dereference outside the pool
+  return page;
+}
+
+// This wave's share of a K tile whose keys live in page `page`, fetched straight into the
+// LDS buffer at byte address `dst`.  Keys past L read slots of the request's last page
+// (their results are discarded).
+template <int D, int W>
 __device__ __forceinline__ void issue_k_tile(uint32_t dst, const char* __restrict__ kv_bytes,
-                                             const int32_t* __restrict__ bt_row, int L,
-                                             int64_t page_bytes, int64_t num_pages,
-                                             const KLoadPlan<D>& kp, int64_t tile) {
-  using Gm = TileGeom<D>;
+                                             int64_t page, int64_t page_bytes,
+                                             const KLoadPlan<D, W>& kp) {
+  using Gm = TileGeom<D, W>;
+  static_assert(Gm::kRowsPerLoad * Gm::kLoadsPerWave <= kPageSize &&
+                    kPageSize % (Gm::kRowsPerLoad * Gm::kLoadsPerWave) == 0,
+                "a wave's loads of one tile must stay inside one page");
+  const char* base = kv_bytes + page * page_bytes;
 #pragma unroll
-  for (int u = 0; u < Gm::kLoadsPerWave; ++u) {
-    const int wl = kp.wl0 + u;
-    const int64_t kbase = tile * kKeyTile + wl * Gm::kRowsPerLoad;   // wave-uniform
-    const int64_t kpage = (kbase < L ? kbase : L - 1) / kPageSize;
-    int64_t page = bt_row[kpage];
-    if (page < 0 || page >= num_pages) page = 0;
-    dma_to_lds16(kv_bytes + page * page_bytes + kp.lane_off[u], dst + (uint32_t)(wl * 1024));
-  }
+  for (int u = 0; u < Gm::kLoadsPerWave; ++u)
+    dma_to_lds16(base + kp.lane_off[u], dst + (uint32_t)((kp.wl0 + u) * 1024));
 }
 
 // The 32x32 MFMA operand of key sub-tile `sub` (32 keys) for every k-step: lane l holds key
@@ -183,10 +201,11 @@ __device__ __forceinline__ int chunk_row_tiles(int M, int c) {
 
 }  // namespace
 
-// Everything the key sweep of one segment needs besides the register-resident Q / beta.
+// Everything the key sweep of one segment needs besides the register-resident Q.
 struct SweepCtx {
   const char* kv_bytes;
   const int32_t* bt_row;
+  const float* beta_s;     // LDS: log2(e) * LSE of every row of the chunk (+inf = padding)
   const int32_t* pos_s;    // LDS: causal position of every row of the chunk
   float* out;              // scores (or chunk partials) of this (request, KV head)
   int64_t page_bytes, num_pages;
@@ -197,117 +216,103 @@ struct SweepCtx {
 };
 
 // Sweep key tiles i0 .. i1-1 of one segment with TPW row tiles (of 32 rows) per wave:
-// kStages-1 tiles in flight through the direct-to-LDS pipeline, one barrier per tile, the
-// first key sub-tile's operands of tile i+1 read across the barrier that ends tile i.
+// kStages-1 tiles in flight through the direct-to-LDS pipeline and one barrier per tile.
 template <int D, bool kMaxMean, int TPW>
-__device__ __forceinline__ void score_sweep(const SweepCtx& cx, const KLoadPlan<D>& kp,
+__device__ __forceinline__ void score_sweep(const SweepCtx& cx, const KLoadPlan<D, kWaves>& kp,
                                             const bf16x8 (&qreg)[kTilesPerWave][TileGeom<D>::kSteps],
-                                            const float (&beta)[kTilesPerWave][16],
                                             char (*kbuf)[TileGeom<D>::kTileBytes],
                                             float (*red)[kWaves][kKeyTile]) {
   using Gm = TileGeom<D>;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, l32 = lane & 31;
+  auto clamp_tile = [&](int64_t t) { return t < cx.i1 ? t : cx.i1 - 1; };
 #pragma unroll
   for (int p = 0; p < kStages - 1; ++p)
-    issue_k_tile<D>(cx.kl + p * Gm::kTileBytes, cx.kv_bytes, cx.bt_row, cx.L, cx.page_bytes,
-                    cx.num_pages, kp, cx.i0 + p < cx.i1 ? cx.i0 + p : cx.i1 - 1);
-  wait_vmcnt<(kStages - 2) * Gm::kLoadsPerWave>();
-  __builtin_amdgcn_s_barrier();
-  bf16x8 ka[Gm::kSteps], kb[Gm::kSteps];
-  read_k_operand<D>(ka, kbuf[0], 0);
+    issue_k_tile<D, kWaves>(cx.kl + p * Gm::kTileBytes, cx.kv_bytes,
+                            page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(cx.i0 + p)),
+                            cx.page_bytes, kp);
+  int64_t next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp,
+                                         clamp_tile(cx.i0 + kStages - 1));
   for (int64_t i = cx.i0; i < cx.i1; ++i) {
     const int st = (int)((i - cx.i0) % kStages);
-    {
-      const int64_t nt = i + kStages - 1 < cx.i1 ? i + kStages - 1 : cx.i1 - 1;
-      issue_k_tile<D>(cx.kl + ((st + kStages - 1) % kStages) * Gm::kTileBytes, cx.kv_bytes,
-                      cx.bt_row, cx.L, cx.page_bytes, cx.num_pages, kp, nt);
-    }
+    // tile i has landed once at most the later tiles' loads are outstanding; the barrier
+    // also retires every wave's reads of the stage the next load overwrites
+    wait_vmcnt<(kStages - 2) * Gm::kLoadsPerWave>();
+    __builtin_amdgcn_s_barrier();
+    issue_k_tile<D, kWaves>(cx.kl + ((st + kStages - 1) % kStages) * Gm::kTileBytes, cx.kv_bytes,
+                            next_page, cx.page_bytes, kp);
+    next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(i + kStages));
     const int64_t key0 = i * kKeyTile;
     const bool needs_mask = key0 + kKeyTile - 1 > cx.mask_from;
     float* rd = red[i & 1][w];
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
-      const bf16x8 (&kr)[Gm::kSteps] = sub == 0 ? ka : kb;
-      f32x16 e[TPW];
+      bf16x8 kr[Gm::kSteps];
+      read_k_operand<D>(kr, kbuf[st], sub);
+      const int key = (int)(key0 + sub * 32 + l32);
+      float a0 = 0.f, a1 = 0.f;
 #pragma unroll
       for (int ti = 0; ti < TPW; ++ti) {
-        e[ti] = mfma32(qreg[ti][0], kr[0], f32x16{});
+        f32x16 e = mfma32(qreg[ti][0], kr[0], f32x16{});
 #pragma unroll
-        for (int ks = 1; ks < Gm::kSteps; ++ks) e[ti] = mfma32(qreg[ti][ks], kr[ks], e[ti]);
-      }
-      if (sub == 0) read_k_operand<D>(kb, kbuf[st], 1);   // in flight under the epilogue
+        for (int ks = 1; ks < Gm::kSteps; ++ks) e = mfma32(qreg[ti][ks], kr[ks], e);
+        // beta of this lane's 16 rows: rows 8*aa + 4*hf + i of row tile w + kWaves*ti
+        const float* brow = cx.beta_s + (w + kWaves * ti) * 32 + 4 * hf;
 #pragma unroll
-      for (int ti = 0; ti < TPW; ++ti) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-          e[ti][v] = fast_exp2(__builtin_fmaf(e[ti][v], cx.alpha, -beta[ti][v]));
-      }
-      if (needs_mask) {
-        const int key = (int)(key0 + sub * 32 + l32);
-#pragma unroll
-        for (int ti = 0; ti < TPW; ++ti) {
+        for (int aa = 0; aa < 4; ++aa) {
+          const float4 b4 = *reinterpret_cast<const float4*>(brow + 8 * aa);
+          e[4 * aa + 0] = fast_exp2(__builtin_fmaf(e[4 * aa + 0], cx.alpha, -b4.x));
+          e[4 * aa + 1] = fast_exp2(__builtin_fmaf(e[4 * aa + 1], cx.alpha, -b4.y));
+          e[4 * aa + 2] = fast_exp2(__builtin_fmaf(e[4 * aa + 2], cx.alpha, -b4.z));
+          e[4 * aa + 3] = fast_exp2(__builtin_fmaf(e[4 * aa + 3], cx.alpha, -b4.w));
+        }
+        if (needs_mask) {
           const int32_t* prow = cx.pos_s + (w + kWaves * ti) * 32 + 4 * hf;
 #pragma unroll
           for (int v = 0; v < 16; ++v)
-            if (key > prow[8 * (v / 4) + (v % 4)]) e[ti][v] = 0.f;
+            if (key > prow[8 * (v / 4) + (v % 4)]) e[v] = 0.f;
         }
-      }
-      float acc;
-      if (!kMaxMean) {
-        float a0 = e[0][0], a1 = e[0][1];
+        if (!kMaxMean) {
 #pragma unroll
-        for (int v = 2; v < 16; v += 2) { a0 += e[0][v]; a1 += e[0][v + 1]; }
+          for (int v = 0; v < 16; v += 2) { a0 += e[v]; a1 += e[v + 1]; }
+        } else if (cx.G == 16) {
+          // the lane's 16 rows are one query's whole group
+          float mx = e[0];
 #pragma unroll
-        for (int ti = 1; ti < TPW; ++ti)
+          for (int v = 1; v < 16; ++v) mx = fmaxf(mx, e[v]);
+          a0 += mx;
+        } else if (cx.G == 8) {
+          // registers 0-7 and 8-15 are two queries' groups
+          float m0 = e[0], m1 = e[8];
 #pragma unroll
-          for (int v = 0; v < 16; v += 2) { a0 += e[ti][v]; a1 += e[ti][v + 1]; }
-        acc = a0 + a1;
-      } else {
-        float a0 = 0.f, a1 = 0.f;
-        const int G = cx.G;
+          for (int v = 1; v < 8; ++v) { m0 = fmaxf(m0, e[v]); m1 = fmaxf(m1, e[8 + v]); }
+          a0 += m0; a1 += m1;
+        } else {
+          // registers v0..v0+3 are four consecutive rows of the natural order
 #pragma unroll
-        for (int ti = 0; ti < TPW; ++ti) {
-          const f32x16& x = e[ti];
-          if (G == 16) {
-            // the lane's 16 rows are one query's whole group
-            float mx = x[0];
-#pragma unroll
-            for (int v = 1; v < 16; ++v) mx = fmaxf(mx, x[v]);
-            a0 += mx;
-          } else if (G == 8) {
-            // registers 0-7 and 8-15 are two queries' groups
-            float m0 = x[0], m1 = x[8];
-#pragma unroll
-            for (int v = 1; v < 8; ++v) { m0 = fmaxf(m0, x[v]); m1 = fmaxf(m1, x[8 + v]); }
-            a0 += m0; a1 += m1;
-          } else {
-            // registers v0..v0+3 are four consecutive rows of the natural order
-#pragma unroll
-            for (int v0 = 0; v0 < 16; v0 += 4) {
-              if (G == 4) {
-                a0 += fmaxf(fmaxf(x[v0], x[v0 + 1]), fmaxf(x[v0 + 2], x[v0 + 3]));
-              } else if (G == 2) {
-                a0 += fmaxf(x[v0], x[v0 + 1]);
-                a1 += fmaxf(x[v0 + 2], x[v0 + 3]);
-              } else {
-                a0 += x[v0] + x[v0 + 2];
-                a1 += x[v0 + 1] + x[v0 + 3];
-              }
+          for (int v0 = 0; v0 < 16; v0 += 4) {
+            if (cx.G == 4) {
+              a0 += fmaxf(fmaxf(e[v0], e[v0 + 1]), fmaxf(e[v0 + 2], e[v0 + 3]));
+            } else if (cx.G == 2) {
+              a0 += fmaxf(e[v0], e[v0 + 1]);
+              a1 += fmaxf(e[v0 + 2], e[v0 + 3]);
+            } else {
+              a0 += e[v0] + e[v0 + 2];
+              a1 += e[v0 + 1] + e[v0 + 3];
             }
           }
         }
-        acc = a0 + a1;
+        // one row tile's accumulator at a time: keeps the wave within 256 registers (the
+        // other workgroup's wave on this SIMD supplies the MFMA / VALU overlap)
+        __builtin_amdgcn_sched_barrier(0);
       }
+      float acc = a0 + a1;
       acc += __shfl_xor(acc, 32, 64);   // lanes l and l+32 hold the same key
       if (hf == 0) rd[sub * 32 + l32] = acc;
+      __builtin_amdgcn_sched_barrier(0);
     }
-    // tile i+1 has landed (only later tiles' loads may be outstanding) and every wave's
-    // partial sums of tile i are in LDS
-    wait_vmcnt<(kStages - 2) * Gm::kLoadsPerWave>();
     wait_lgkmcnt0();
     __builtin_amdgcn_s_barrier();
-    if (i + 1 < cx.i1) read_k_operand<D>(ka, kbuf[(st + 1) % kStages], 0);
-    // wave w finishes keys 8w .. 8w+7 of tile i (fixed summation order over waves)
+    // wave w finishes keys 16w .. 16w+15 of tile i (fixed summation order over waves)
     if (lane < kKeyTile / kWaves) {
       const int kk = w * (kKeyTile / kWaves) + lane;
       const int64_t key = key0 + kk;
@@ -322,7 +327,7 @@ __device__ __forceinline__ void score_sweep(const SweepCtx& cx, const KLoadPlan<
 }
 
 template <int D, bool kMaxMean>
-__global__ __launch_bounds__(kThreads, 1) void score_kernel(
+__global__ __launch_bounds__(kThreads, 2) void score_kernel(
     DevProblem dp, const uint16_t* __restrict__ q_ptr, const uint16_t* __restrict__ kv_ptr,
     const int32_t* __restrict__ bt_ptr, const float* __restrict__ lse_ptr,
     float* __restrict__ scores_ptr, float* __restrict__ part_ptr, int64_t num_scores) {
@@ -332,7 +337,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
   __shared__ __align__(16) int32_t pos_s[kRowsPerChunk];
   __shared__ float red[2][kWaves][kKeyTile];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hf = lane >> 5;
+  const int tid = threadIdx.x, w = tid >> 6;
   const int G = dp.G, Hq = dp.Hq, Hkv = dp.Hkv, C = dp.max_chunks;
   const int64_t nseg = dp.num_segments;
   const int64_t total = dp.seg_cost[nseg];
@@ -341,6 +346,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
 
   SweepCtx cx;
   cx.kv_bytes = reinterpret_cast<const char*>(kv_ptr);
+  cx.beta_s = beta_s;
   cx.pos_s = pos_s;
   cx.page_bytes = (int64_t)kPageSize * Hkv * D * 2;
   cx.num_pages = dp.num_pages;
@@ -391,29 +397,18 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
     cx.out_scale = (kMaxMean && pl.nchunk == 1) ? (n > 0 ? 1.0f / n : 0.0f) : 1.0f;
     cx.out = (c == 0) ? scores_ptr + pl.seg_off + (int64_t)h * L
                       : part_ptr + (int64_t)(c - 1) * num_scores + pl.seg_off + (int64_t)h * L;
-    const KLoadPlan<D> kp = make_k_load_plan<D>(h, Hkv);
+    const KLoadPlan<D, kWaves> kp = make_k_load_plan<D, kWaves>(h, Hkv);
     // every ordinary load of the setup has landed before the K pipeline starts, so the
     // sweep needs no compiler-inserted wait on the vector-memory queue
     wait_vmcnt<0>();
     __syncthreads();   // beta_s / pos_s visible
-    // beta of this lane's 16 rows per row tile: rows 8*aa + 4*hf + i
-    float beta[kTilesPerWave][16];
-#pragma unroll
-    for (int ti = 0; ti < kTilesPerWave; ++ti) {
-      const float* brow = beta_s + (w + kWaves * ti) * 32 + 4 * hf;
-#pragma unroll
-      for (int aa = 0; aa < 4; ++aa) {
-        const float4 b4 = *reinterpret_cast<const float4*>(brow + 8 * aa);
-        beta[ti][4 * aa + 0] = b4.x; beta[ti][4 * aa + 1] = b4.y;
-        beta[ti][4 * aa + 2] = b4.z; beta[ti][4 * aa + 3] = b4.w;
-      }
-    }
-    // rows past the chunk's row tiles are all padding (Q = 0, beta = +inf): skip the
-    // second row tile of every wave when the chunk has at most kWaves row tiles
-    if (RT > kWaves)
-      score_sweep<D, kMaxMean, 2>(cx, kp, qreg, beta, kbuf, red);
-    else
-      score_sweep<D, kMaxMean, 1>(cx, kp, qreg, beta, kbuf, red);
+    // row tiles past the chunk's RT are all padding (Q = 0, beta = +inf): each wave runs
+    // only as many of its row tiles as can hold real rows
+    const int tpw = (RT + kWaves - 1) / kWaves;
+    if (tpw >= 4) score_sweep<D, kMaxMean, 4>(cx, kp, qreg, kbuf, red);
+    else if (tpw == 3) score_sweep<D, kMaxMean, 3>(cx, kp, qreg, kbuf, red);
+    else if (tpw == 2) score_sweep<D, kMaxMean, 2>(cx, kp, qreg, kbuf, red);
+    else score_sweep<D, kMaxMean, 1>(cx, kp, qreg, kbuf, red);
   }
   wait_vmcnt<0>();   // drain: no LDS write may be outstanding when the workgroup exits
 }
@@ -445,7 +440,7 @@ hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
   if (hipGetDevice(&dev) == hipSuccess) {
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 256;
   }
-  int64_t grid = (int64_t)cus;   // one 8-wave workgroup per CU
+  int64_t grid = (int64_t)cus * 2;   // two 4-wave workgroups per CU
   if (grid > hp.score_cost) grid = hp.score_cost > 0 ? hp.score_cost : 1;
   const bool mm = dp.agg == ACTKV_AGG_MAX_MEAN;
   if (dp.D == 128) {
@@ -473,10 +468,10 @@ hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
 // kernel combines the partials of a row in order.
 // ---------------------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void lse_partial_kernel(
+__global__ __launch_bounds__(kLseThreads, 1) void lse_partial_kernel(
     DevProblem dp, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kv,
     const int32_t* __restrict__ bt, float2* __restrict__ part) {
-  using Gm = TileGeom<D>;
+  using Gm = TileGeom<D, kLseWaves>;
   __shared__ __align__(1024) char kbuf[kStages][Gm::kTileBytes];
   const uint32_t kl = (uint32_t)(uintptr_t)(lds_char*)&kbuf[0][0];
   const int kb = blockIdx.x, ch = blockIdx.y / dp.Hkv, h = blockIdx.y % dp.Hkv, r = blockIdx.z;
@@ -489,20 +484,20 @@ __global__ __launch_bounds__(kThreads, 1) void lse_partial_kernel(
   const int32_t* bt_row = bt + (int64_t)r * dp.bt_stride;
   const char* kv_bytes = reinterpret_cast<const char*>(kv);
   const int64_t page_bytes = (int64_t)kPageSize * Hkv * D * 2;
-  const KLoadPlan<D> kp = make_k_load_plan<D>(h, Hkv);
+  const KLoadPlan<D, kLseWaves> kp = make_k_load_plan<D, kLseWaves>(h, Hkv);
   const int64_t t0 = (int64_t)kb * (kLseKeysPerBlock / kKeyTile);
   int64_t t1 = t0 + kLseKeysPerBlock / kKeyTile;
   const int64_t ntiles = ceil_div64(L, kKeyTile);
   if (t1 > ntiles) t1 = ntiles;
-  bf16x8 qreg[kTilesPerWave][Gm::kSteps];
-  int pos[kTilesPerWave];
-  float rm[kTilesPerWave], rs[kTilesPerWave];
+  bf16x8 qreg[kLseTilesPerWave][Gm::kSteps];
+  int pos[kLseTilesPerWave];
+  float rm[kLseTilesPerWave], rs[kLseTilesPerWave];
 #pragma unroll
-  for (int ti = 0; ti < kTilesPerWave; ++ti) {
+  for (int ti = 0; ti < kLseTilesPerWave; ++ti) {
     rm[ti] = -__builtin_inff();
     rs[ti] = 0.f;
     pos[ti] = -1;
-    const int tile = w + kWaves * ti;
+    const int tile = w + kLseWaves * ti;
     if (tile < RT) {
       load_q_tile<D>(qreg[ti], q, G, Hq, h, pl.q_off, n, ch, tile);
       int j, g;
@@ -511,27 +506,28 @@ __global__ __launch_bounds__(kThreads, 1) void lse_partial_kernel(
     }
   }
   wait_vmcnt<0>();   // Q is in registers before the K pipeline starts
+  auto clamp_tile = [&](int64_t t) { return t < t1 ? t : t1 - 1; };
 #pragma unroll
   for (int p = 0; p < kStages - 1; ++p)
-    issue_k_tile<D>(kl + p * Gm::kTileBytes, kv_bytes, bt_row, L, page_bytes, dp.num_pages, kp,
-                    t0 + p < t1 ? t0 + p : t1 - 1);
+    issue_k_tile<D, kLseWaves>(kl + p * Gm::kTileBytes, kv_bytes,
+                               page_of<D, kLseWaves>(bt_row, L, dp.num_pages, kp, clamp_tile(t0 + p)),
+                               page_bytes, kp);
+  int64_t next_page = page_of<D, kLseWaves>(bt_row, L, dp.num_pages, kp, clamp_tile(t0 + kStages - 1));
   for (int64_t i = t0; i < t1; ++i) {
     const int st = (int)((i - t0) % kStages);
     wait_vmcnt<(kStages - 2) * Gm::kLoadsPerWave>();
     __builtin_amdgcn_s_barrier();
-    {
-      const int64_t nt = i + kStages - 1 < t1 ? i + kStages - 1 : t1 - 1;
-      issue_k_tile<D>(kl + ((st + kStages - 1) % kStages) * Gm::kTileBytes, kv_bytes, bt_row, L,
-                      page_bytes, dp.num_pages, kp, nt);
-    }
+    issue_k_tile<D, kLseWaves>(kl + ((st + kStages - 1) % kStages) * Gm::kTileBytes, kv_bytes,
+                               next_page, page_bytes, kp);
+    next_page = page_of<D, kLseWaves>(bt_row, L, dp.num_pages, kp, clamp_tile(i + kStages));
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
       bf16x8 kreg[Gm::kSteps];
       read_k_operand<D>(kreg, kbuf[st], sub);
       const int keybase = (int)(i * kKeyTile + sub * 32 + 4 * hf);
 #pragma unroll
-      for (int ti = 0; ti < kTilesPerWave; ++ti) {
-        if (w + kWaves * ti < RT) {
+      for (int ti = 0; ti < kLseTilesPerWave; ++ti) {
+        if (w + kLseWaves * ti < RT) {
           f32x16 x = {};
 #pragma unroll
           for (int ks = 0; ks < Gm::kSteps; ++ks) x = mfma32(kreg[ks], qreg[ti][ks], x);
@@ -556,8 +552,8 @@ __global__ __launch_bounds__(kThreads, 1) void lse_partial_kernel(
   wait_vmcnt<0>();
   // combine the two lanes that share a query row, then write one partial per row
 #pragma unroll
-  for (int ti = 0; ti < kTilesPerWave; ++ti) {
-    const int tile = w + kWaves * ti;
+  for (int ti = 0; ti < kLseTilesPerWave; ++ti) {
+    const int tile = w + kLseWaves * ti;
     const float om = __shfl_xor(rm[ti], 32, 64), os = __shfl_xor(rs[ti], 32, 64);
     const float m = fmaxf(rm[ti], om);
     float sm = 0.f;
@@ -597,11 +593,11 @@ hipError_t launch_lse(const DevProblem& dp, const HostPlan& hp, const void* q, c
   const int64_t max_blocks = hp.max_lse_blocks > 0 ? hp.max_lse_blocks : 1;
   dim3 grid((unsigned)max_blocks, (unsigned)(hp.max_chunks * hp.Hkv), (unsigned)hp.R);
   if (dp.D == 128)
-    hipLaunchKernelGGL(lse_partial_kernel<128>, grid, dim3(kThreads), 0, s, dp,
+    hipLaunchKernelGGL(lse_partial_kernel<128>, grid, dim3(kLseThreads), 0, s, dp,
                        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(kv), bt,
                        lse_part);
   else
-    hipLaunchKernelGGL(lse_partial_kernel<64>, grid, dim3(kThreads), 0, s, dp,
+    hipLaunchKernelGGL(lse_partial_kernel<64>, grid, dim3(kLseThreads), 0, s, dp,
                        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(kv), bt,
                        lse_part);
   hipError_t e = hipGetLastError();
