@@ -215,6 +215,90 @@ struct SweepCtx {
   uint32_t kl;             // LDS byte address of the K stages
 };
 
+// One K tile (64 keys, LDS buffer `buf`) against this wave's TPW row tiles: for each
+// 32-key half, the MFMA chain of a row tile, its exp2 epilogue and its row sum, one row
+// tile at a time; the per-key sums of the wave go to `rd`.
+template <int D, bool kMaxMean, int TPW, bool kMask>
+__device__ __forceinline__ void score_tile(const SweepCtx& cx,
+                                           const bf16x8 (&qreg)[kTilesPerWave][TileGeom<D>::kSteps],
+                                           const char* buf, int64_t key0, float* rd) {
+  using Gm = TileGeom<D>;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, l32 = lane & 31;
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) {
+    bf16x8 kr[Gm::kSteps];
+    read_k_operand<D>(kr, buf, sub);
+    const int key = (int)(key0 + sub * 32 + l32);
+    float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+    for (int ti = 0; ti < TPW; ++ti) {
+      f32x16 e = mfma32(qreg[ti][0], kr[0], f32x16{});
+#pragma unroll
+      for (int ks = 1; ks < Gm::kSteps; ++ks) e = mfma32(qreg[ti][ks], kr[ks], e);
+      // beta of this lane's 16 rows: rows 8*aa + 4*hf + i of row tile w + kWaves*ti
+      const float* brow = cx.beta_s + (w + kWaves * ti) * 32 + 4 * hf;
+      const int32_t* prow = cx.pos_s + (w + kWaves * ti) * 32 + 4 * hf;
+#pragma unroll
+      for (int aa = 0; aa < 4; ++aa) {
+        const float4 b4 = *reinterpret_cast<const float4*>(brow + 8 * aa);
+        float x0 = __builtin_fmaf(e[4 * aa + 0], cx.alpha, -b4.x);
+        float x1 = __builtin_fmaf(e[4 * aa + 1], cx.alpha, -b4.y);
+        float x2 = __builtin_fmaf(e[4 * aa + 2], cx.alpha, -b4.z);
+        float x3 = __builtin_fmaf(e[4 * aa + 3], cx.alpha, -b4.w);
+        if (kMask) {   // exp2(-inf) = 0 for keys after the row's position
+          const int4 p4 = *reinterpret_cast<const int4*>(prow + 8 * aa);
+          const float ninf = -__builtin_inff();
+          x0 = key > p4.x ? ninf : x0;
+          x1 = key > p4.y ? ninf : x1;
+          x2 = key > p4.z ? ninf : x2;
+          x3 = key > p4.w ? ninf : x3;
+        }
+        e[4 * aa + 0] = fast_exp2(x0);
+        e[4 * aa + 1] = fast_exp2(x1);
+        e[4 * aa + 2] = fast_exp2(x2);
+        e[4 * aa + 3] = fast_exp2(x3);
+      }
+      if (!kMaxMean) {
+#pragma unroll
+        for (int v = 0; v < 16; v += 2) { a0 += e[v]; a1 += e[v + 1]; }
+      } else if (cx.G == 16) {
+        // the lane's 16 rows are one query's whole group
+        float mx = e[0];
+#pragma unroll
+        for (int v = 1; v < 16; ++v) mx = fmaxf(mx, e[v]);
+        a0 += mx;
+      } else if (cx.G == 8) {
+        // registers 0-7 and 8-15 are two queries' groups
+        float m0 = e[0], m1 = e[8];
+#pragma unroll
+        for (int v = 1; v < 8; ++v) { m0 = fmaxf(m0, e[v]); m1 = fmaxf(m1, e[8 + v]); }
+        a0 += m0; a1 += m1;
+      } else {
+        // registers v0..v0+3 are four consecutive rows of the natural order
+#pragma unroll
+        for (int v0 = 0; v0 < 16; v0 += 4) {
+          if (cx.G == 4) {
+            a0 += fmaxf(fmaxf(e[v0], e[v0 + 1]), fmaxf(e[v0 + 2], e[v0 + 3]));
+          } else if (cx.G == 2) {
+            a0 += fmaxf(e[v0], e[v0 + 1]);
+            a1 += fmaxf(e[v0 + 2], e[v0 + 3]);
+          } else {
+            a0 += e[v0] + e[v0 + 2];
+            a1 += e[v0 + 1] + e[v0 + 3];
+          }
+        }
+      }
+      // one row tile's accumulator at a time: keeps the wave within 256 registers (the
+      // other workgroup's wave on this SIMD supplies the MFMA / VALU overlap)
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    float acc = a0 + a1;
+    acc += __shfl_xor(acc, 32, 64);   // lanes l and l+32 hold the same key
+    if (hf == 0) rd[sub * 32 + l32] = acc;
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // Sweep key tiles i0 .. i1-1 of one segment with TPW row tiles (of 32 rows) per wave:
 // kStages-1 tiles in flight through the direct-to-LDS pipeline and one barrier per tile.
 template <int D, bool kMaxMean, int TPW>
@@ -223,7 +307,7 @@ __device__ __forceinline__ void score_sweep(const SweepCtx& cx, const KLoadPlan<
                                             char (*kbuf)[TileGeom<D>::kTileBytes],
                                             float (*red)[kWaves][kKeyTile]) {
   using Gm = TileGeom<D>;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, l32 = lane & 31;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   auto clamp_tile = [&](int64_t t) { return t < cx.i1 ? t : cx.i1 - 1; };
 #pragma unroll
   for (int p = 0; p < kStages - 1; ++p)
@@ -242,74 +326,14 @@ __device__ __forceinline__ void score_sweep(const SweepCtx& cx, const KLoadPlan<
                             next_page, cx.page_bytes, kp);
     next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(i + kStages));
     const int64_t key0 = i * kKeyTile;
-    const bool needs_mask = key0 + kKeyTile - 1 > cx.mask_from;
     float* rd = red[i & 1][w];
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      bf16x8 kr[Gm::kSteps];
-      read_k_operand<D>(kr, kbuf[st], sub);
-      const int key = (int)(key0 + sub * 32 + l32);
-      float a0 = 0.f, a1 = 0.f;
-#pragma unroll
-      for (int ti = 0; ti < TPW; ++ti) {
-        f32x16 e = mfma32(qreg[ti][0], kr[0], f32x16{});
-#pragma unroll
-        for (int ks = 1; ks < Gm::kSteps; ++ks) e = mfma32(qreg[ti][ks], kr[ks], e);
-        // beta of this lane's 16 rows: rows 8*aa + 4*hf + i of row tile w + kWaves*ti
-        const float* brow = cx.beta_s + (w + kWaves * ti) * 32 + 4 * hf;
-#pragma unroll
-        for (int aa = 0; aa < 4; ++aa) {
-          const float4 b4 = *reinterpret_cast<const float4*>(brow + 8 * aa);
-          e[4 * aa + 0] = fast_exp2(__builtin_fmaf(e[4 * aa + 0], cx.alpha, -b4.x));
-          e[4 * aa + 1] = fast_exp2(__builtin_fmaf(e[4 * aa + 1], cx.alpha, -b4.y));
-          e[4 * aa + 2] = fast_exp2(__builtin_fmaf(e[4 * aa + 2], cx.alpha, -b4.z));
-          e[4 * aa + 3] = fast_exp2(__builtin_fmaf(e[4 * aa + 3], cx.alpha, -b4.w));
-        }
-        if (needs_mask) {
-          const int32_t* prow = cx.pos_s + (w + kWaves * ti) * 32 + 4 * hf;
-#pragma unroll
-          for (int v = 0; v < 16; ++v)
-            if (key > prow[8 * (v / 4) + (v % 4)]) e[v] = 0.f;
-        }
-        if (!kMaxMean) {
-#pragma unroll
-          for (int v = 0; v < 16; v += 2) { a0 += e[v]; a1 += e[v + 1]; }
-        } else if (cx.G == 16) {
-          // the lane's 16 rows are one query's whole group
-          float mx = e[0];
-#pragma unroll
-          for (int v = 1; v < 16; ++v) mx = fmaxf(mx, e[v]);
-          a0 += mx;
-        } else if (cx.G == 8) {
-          // registers 0-7 and 8-15 are two queries' groups
-          float m0 = e[0], m1 = e[8];
-#pragma unroll
-          for (int v = 1; v < 8; ++v) { m0 = fmaxf(m0, e[v]); m1 = fmaxf(m1, e[8 + v]); }
-          a0 += m0; a1 += m1;
-        } else {
-          // registers v0..v0+3 are four consecutive rows of the natural order
-#pragma unroll
-          for (int v0 = 0; v0 < 16; v0 += 4) {
-            if (cx.G == 4) {
-              a0 += fmaxf(fmaxf(e[v0], e[v0 + 1]), fmaxf(e[v0 + 2], e[v0 + 3]));
-            } else if (cx.G == 2) {
-              a0 += fmaxf(e[v0], e[v0 + 1]);
-              a1 += fmaxf(e[v0 + 2], e[v0 + 3]);
-            } else {
-              a0 += e[v0] + e[v0 + 2];
-              a1 += e[v0 + 1] + e[v0 + 3];
-            }
-          }
-        }
-        // one row tile's accumulator at a time: keeps the wave within 256 registers (the
-        // other workgroup's wave on this SIMD supplies the MFMA / VALU overlap)
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      float acc = a0 + a1;
-      acc += __shfl_xor(acc, 32, 64);   // lanes l and l+32 hold the same key
-      if (hf == 0) rd[sub * 32 + l32] = acc;
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    // tiles that reach past the first action position may hold keys hidden from some rows;
+    // they take a separate, masked copy of the body so that the common body has no branch
+    // (a branch per row tile would keep all of a tile's exp2 results live at once)
+    if (key0 + kKeyTile - 1 > cx.mask_from)
+      score_tile<D, kMaxMean, TPW, true>(cx, qreg, kbuf[st], key0, rd);
+    else
+      score_tile<D, kMaxMean, TPW, false>(cx, qreg, kbuf[st], key0, rd);
     wait_lgkmcnt0();
     __builtin_amdgcn_s_barrier();
     // wave w finishes keys 16w .. 16w+15 of tile i (fixed summation order over waves)
