@@ -4,39 +4,36 @@
 // Shape of the work: per (request r, KV head h) the scores are column sums of
 //   P = exp2(alpha * Q_h K_h^T - beta),  alpha = sm_scale * log2(e),  beta = LSE * log2(e)
 // where Q_h holds the M = G * n action-query rows of the head group and K_h the L cached
-// keys.  Q_h K_h^T is a real dense contraction (M x L x D) and runs on bf16 MFMA
-// (v_mfma_f32_32x32x16_bf16) with fp32 accumulation; the exp2 / add epilogue runs on the
-// VALU.
+// keys.  Q_h K_h^T is a real dense contraction (M x L x D) and runs on bf16 MFMA with fp32
+// accumulation; the exp2 / add epilogue runs on the VALU.
 //
 // Kernel layout (score_kernel):
-//   * 512 threads = 8 waves (two per SIMD, one workgroup per CU).  A workgroup holds up to
-//     512 query rows ("row chunk") of one (r, h) in registers: wave w owns row tiles w and
-//     w+8 (32 rows each) as the MFMA A operand, and the beta of its rows.  Two waves per
-//     SIMD let one wave's exp2 / add epilogue overlap the other's MFMAs.
-//   * Keys stream through LDS in tiles of 64 (4 pages) gathered through the block table
-//     with 16-byte loads (one 256-byte K row per 16 lanes), double-buffered: the global
-//     loads of tile i+1 are in flight while tile i is multiplied.
-//   * Each lane's accumulator column is one key, its 16 registers 16 query rows, so the
-//     sum over rows is in-lane; lanes l and l+32 are combined with one exchange and the
-//     eight waves through LDS in a fixed order (no atomics: deterministic, and independent
-//     of where the pages physically live).
-//   * The grid is persistent: the (segment, key tile) work list is cut into equal-cost
-//     contiguous ranges (cost = key tiles x row tiles), one per workgroup, so ragged
-//     lengths and query counts stay balanced and Q is loaded once per segment per
-//     workgroup.
+//   * One workgroup of 8 waves per CU (two waves per SIMD), persistent: the list of
+//     (segment, 64-key tile) work, segment = (request, row chunk of up to 512 query rows,
+//     KV head), is cut into equal-cost contiguous ranges, one per workgroup, so ragged
+//     lengths and query counts stay balanced and Q is loaded once per segment.
+//   * Each wave holds 4 row tiles of 16 query rows in registers (v_mfma_f32_16x16x32_bf16
+//     A operand) and the beta of its rows.  K tiles (64 keys, 4 pages) are gathered
+//     through the block table straight into LDS (global_load_lds_dwordx4, 16 bytes per
+//     lane, chunk-swizzled rows), kScoreStages - 1 tiles ahead, one barrier per tile.
+//   * The MFMA chains and the exp2 epilogue are software-pipelined inside each wave (see
+//     the sweep below): the VALU works on one 16x16 unit while the matrix core works on
+//     another.
+//   * A lane's accumulator column is one key and 4 query rows, so the row sum is in-lane;
+//     the 4 lane groups and 8 waves are combined through LDS in a fixed order (no
+//     atomics: deterministic, and independent of where the pages physically live).
 #include "device_common.hpp"
 
 namespace actkv {
 
 namespace {
 
-// Scoring: 4 waves per workgroup, 4 row tiles (128 query rows) per wave, two workgroups per
-// CU.  The two waves sharing a SIMD belong to different workgroups, so their barriers are
-// independent and one wave's exp2 epilogue runs beside the other's MFMAs.
-constexpr int kThreads = 256;
+// Scoring: 8 waves per workgroup (two per SIMD), 64 query rows per wave, one workgroup per
+// CU.
+constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
-constexpr int kTilesPerWave = kRowsPerChunk / 32 / kWaves;   // 4 row tiles of 32 rows
-constexpr int kStages = 3;      // K tiles resident in LDS (two in flight)
+constexpr int kScoreStages = 4;   // K tiles resident in LDS for scoring (three in flight)
+constexpr int kStages = 3;        // the same for the LSE pass
 // The LSE pass keeps 8 waves x 2 row tiles (its per-row running max/sum stay in registers).
 constexpr int kLseThreads = 512;
 constexpr int kLseWaves = kLseThreads / 64;
@@ -201,168 +198,359 @@ __device__ __forceinline__ int chunk_row_tiles(int M, int c) {
 
 }  // namespace
 
-// Everything the key sweep of one segment needs besides the register-resident Q.
+// ---- scoring: software-pipelined 16x16x32 MFMA units -----------------------------------
+//
+// A wave owns kRowTilesPerWave row tiles of 16 query rows (the MFMA A operand, held in
+// registers for the whole segment).  Each 64-key tile in LDS is cut into 4 sub-tiles of 16
+// keys (the B operand).  A "unit" is one (sub-tile, row tile) pair: kSteps16 dependent
+// MFMAs into a 16x16 accumulator -- lane l holds key l%16 and rows 4*(l/16) .. +3 -- and
+// then its epilogue: exp2 of the 4 elements, summed (or max-reduced over the GQA group)
+// into the lane's partial for that key.
+//
+// Phase g issues the chain of unit g one MFMA per slot and, between those MFMAs, the
+// epilogue of unit g - 2, whose accumulator was finished a whole phase earlier.  The two
+// are independent, so the VALU works on one unit while the matrix core works on the other.
+// When unit g + 1 starts a new sub-tile its K operand is read from LDS during phase g,
+// each k-step right after the MFMA that last uses the old value.
+
+constexpr int kRowTile = 16;
+constexpr int kRowTilesPerWave = kRowsPerChunk / kRowTile / kWaves;   // 4
+constexpr int kSubTiles = kKeyTile / 16;                              // 4
+static_assert(kRowTilesPerWave == 4 && kSubTiles == 4, "unit bookkeeping below");
+
+template <int D>
+struct Geom16 {
+  static constexpr int kSteps = D / 32;   // k-steps of 32 per head
+};
+
+// Query row at (row tile T = w + kWaves * rt, tile row mm) of row chunk c.  The natural
+// order m = j * G + g is used unless the group max of MAX_MEAN needs a query's G = 8 or 16
+// heads in one lane: then they sit at the same lane position of 2 or 4 of the wave's row
+// tiles (heads 4*(rt % 2) + i, resp. 4*rt + i).
+__device__ __forceinline__ void score_row_query(int G, bool grouped, int c, int T, int mm,
+                                                int* j, int* g) {
+  if (!grouped) {
+    const int m = c * kRowsPerChunk + T * kRowTile + mm;
+    *j = m / G;
+    *g = m % G;
+    return;
+  }
+  const int w = T % kWaves, rt = T / kWaves, a = mm >> 2, i = mm & 3;
+  if (G == 8) {
+    *j = c * (kRowsPerChunk / 8) + (rt >> 1) * (4 * kWaves) + w * 4 + a;
+    *g = 4 * (rt & 1) + i;
+  } else {
+    *j = c * (kRowsPerChunk / 16) + w * 4 + a;
+    *g = 4 * rt + i;
+  }
+}
+
+// Row tiles per wave that can hold real rows of chunk c (the same for every wave).
+__device__ __forceinline__ int chunk_wave_tiles(int G, bool grouped, int n, int c) {
+  if (!grouped) {
+    const int rows = G * n - c * kRowsPerChunk;
+    if (rows <= 0) return 1;
+    const int r = rows < kRowsPerChunk ? rows : kRowsPerChunk;
+    return ceil_div(r, kRowTile * kWaves);
+  }
+  if (G == 8) {
+    const int qn = n - c * (kRowsPerChunk / 8);
+    return qn <= 4 * kWaves ? 2 : 4;
+  }
+  return 4;
+}
+
+// Row tile rt of this wave as the 16x16x32 A operand: lane l holds row l%16 with head-dim
+// elements 32*ks + 8*(l/16) .. +8; rows past n are zero.
+template <int D>
+__device__ __forceinline__ void load_q16(bf16x8 (&qr)[Geom16<D>::kSteps],
+                                         const uint16_t* __restrict__ q, int G, bool grouped,
+                                         int Hq, int h, int q_off, int n, int c, int T) {
+  const int lane = threadIdx.x & 63;
+  int j, g;
+  score_row_query(G, grouped, c, T, lane & 15, &j, &g);
+  if (j < n) {
+    const uint16_t* src = q + ((int64_t)(q_off + j) * Hq + h * G + g) * D + (lane >> 4) * 8;
+#pragma unroll
+    for (int ks = 0; ks < Geom16<D>::kSteps; ++ks)
+      qr[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + ks * 32));
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < Geom16<D>::kSteps; ++ks) qr[ks] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+  }
+}
+
+// LDS offset of this lane's B-operand chunk for k-step ks of sub-tile 0 (sub-tile s is
+// 16 rows further).  Row r = l%16 holds chunk c = 4 ks + l/16 at slot c ^ (r % kChunks):
+//   r * kRowBytes + 16 ((4 ks + q) ^ x)  =  [r * kRowBytes + 16 (q ^ (x & 3))] + [(64 ks) ^ (16 (x & ~3))]
+// with q = l/16, x = r % kChunks: two per-lane values give every k-step.
+struct KRead16 {
+  uint32_t base, xmask;
+};
+
+template <int D>
+__device__ __forceinline__ KRead16 make_k_read16() {
+  using Gm = TileGeom<D>;
+  const int lane = threadIdx.x & 63, r = lane & 15, qd = lane >> 4, x = r % Gm::kChunks;
+  KRead16 rp;
+  rp.base = (uint32_t)(r * Gm::kRowBytes + 16 * (qd ^ (x & 3)));
+  rp.xmask = (uint32_t)(16 * (x & ~3));
+  return rp;
+}
+
+template <int D>
+__device__ __forceinline__ bf16x8 lds_k16(const char* tile_buf, int sub, const KRead16& rp, int ks) {
+  const uint32_t off = rp.base + ((uint32_t)(64 * ks) ^ rp.xmask);
+  return as_bf16x8(*reinterpret_cast<const u32x4*>(tile_buf + sub * 16 * TileGeom<D>::kRowBytes + off));
+}
+
+// Per-wave state carried from phase to phase.
+template <int D>
+struct Pipe16 {
+  f32x4 c1, c2;                       // accumulators of units g-1 and g-2
+  bf16x8 kr[Geom16<D>::kSteps];       // B operand of the next chain
+  float part[4];                      // the lane's partials of the current sub-tile, one per
+                                      // accumulator element (independent add chains)
+  float ex;                           // SUM: the last exp2 result, added one slot later
+  float mx;                           // MAX_MEAN, G = 8 / 16: running group max
+};
+
+// One phase.  kChain: chain of row tile q against st.kr.  kEpi: epilogue of st.c2 for row
+// tile kRt (beta bt, causal positions at prow, key `key`).  kLoad: after the MFMA of
+// k-step ks, st.kr[ks] <- the next unit's operand (sub-tile next_sub of next_buf).
+template <int D, bool kMaxMean, bool kMask, bool kChain, bool kEpi, bool kLoad, int kRt>
+__device__ __forceinline__ void score_phase16(Pipe16<D>& st, const bf16x8 (&q)[Geom16<D>::kSteps],
+                                              const KRead16& rp, const char* next_buf, int next_sub,
+                                              const float (&bt)[4], const int32_t* prow, int key,
+                                              float alpha, int G) {
+  constexpr int S = Geom16<D>::kSteps;
+  constexpr int EPS = 4 / S;   // epilogue elements per MFMA slot
+  f32x4 prev = st.c2;
+  int pt[4] = {0, 0, 0, 0};
+  if (kEpi && kMask) {
+    const int4 p4 = *reinterpret_cast<const int4*>(prow);
+    pt[0] = p4.x; pt[1] = p4.y; pt[2] = p4.z; pt[3] = p4.w;
+  }
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < S; ++ks) {
+    if (kChain) acc = mfma16(q[ks], st.kr[ks], acc);
+    if (kLoad) st.kr[ks] = lds_k16<D>(next_buf, next_sub, rp, ks);
+    if (kEpi) {
+#pragma unroll
+      for (int v = ks * EPS; v < (ks + 1) * EPS; ++v) {
+        float x = __builtin_fmaf(prev[v], alpha, -bt[v]);
+        if (kMask) x = key > pt[v] ? -__builtin_inff() : x;   // exp2(-inf) = 0
+        if (!kMaxMean) {
+          // the previous element's exp2 is added now, off the exp2 latency path
+          st.part[(v + 3) & 3] += st.ex;
+          st.ex = fast_exp2(x);
+        } else {
+          prev[v] = fast_exp2(x);
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (kEpi && kMaxMean) {
+    const float m01 = fmaxf(prev[0], prev[1]), m23 = fmaxf(prev[2], prev[3]);
+    if (G == 1) {
+      st.part[0] += (prev[0] + prev[1]) + (prev[2] + prev[3]);
+    } else if (G == 2) {
+      st.part[0] += m01 + m23;
+    } else if (G == 4) {
+      st.part[0] += fmaxf(m01, m23);
+    } else if (G == 8) {
+      // heads 0-3 in even row tiles, 4-7 in the next one
+      const float m = fmaxf(m01, m23);
+      if (kRt & 1) st.part[0] += fmaxf(st.mx, m); else st.mx = m;
+    } else {
+      // G == 16: heads 4*rt .. 4*rt+3 in row tile rt
+      const float m = fmaxf(m01, m23);
+      st.mx = kRt == 0 ? m : fmaxf(st.mx, m);
+      if (kRt == kRowTilesPerWave - 1) st.part[0] += st.mx;
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  st.c2 = st.c1;
+  if (kChain) st.c1 = acc;
+}
+
+// Everything the key sweep of one segment needs besides the register-resident Q and beta.
 struct SweepCtx {
   const char* kv_bytes;
   const int32_t* bt_row;
-  const float* beta_s;     // LDS: log2(e) * LSE of every row of the chunk (+inf = padding)
   const int32_t* pos_s;    // LDS: causal position of every row of the chunk
   float* out;              // scores (or chunk partials) of this (request, KV head)
+  const char* kbuf;        // LDS: the K stages
   int64_t page_bytes, num_pages;
-  int64_t i0, i1;          // key tiles of this workgroup
+  int i0, i1;              // key tiles of this workgroup
   int L, mask_from, G;
   float alpha, out_scale;
   uint32_t kl;             // LDS byte address of the K stages
 };
 
-// One K tile (64 keys, LDS buffer `buf`) against this wave's TPW row tiles: for each
-// 32-key half, the MFMA chain of a row tile, its exp2 epilogue and its row sum, one row
-// tile at a time; the per-key sums of the wave go to `rd`.
-template <int D, bool kMaxMean, int TPW, bool kMask>
-__device__ __forceinline__ void score_tile(const SweepCtx& cx,
-                                           const bf16x8 (&qreg)[kTilesPerWave][TileGeom<D>::kSteps],
-                                           const char* buf, int64_t key0, float* rd) {
-  using Gm = TileGeom<D>;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hf = lane >> 5, l32 = lane & 31;
-#pragma unroll
-  for (int sub = 0; sub < 2; ++sub) {
-    bf16x8 kr[Gm::kSteps];
-    read_k_operand<D>(kr, buf, sub);
-    const int key = (int)(key0 + sub * 32 + l32);
-    float a0 = 0.f, a1 = 0.f;
-#pragma unroll
-    for (int ti = 0; ti < TPW; ++ti) {
-      f32x16 e = mfma32(qreg[ti][0], kr[0], f32x16{});
-#pragma unroll
-      for (int ks = 1; ks < Gm::kSteps; ++ks) e = mfma32(qreg[ti][ks], kr[ks], e);
-      // beta of this lane's 16 rows: rows 8*aa + 4*hf + i of row tile w + kWaves*ti
-      const float* brow = cx.beta_s + (w + kWaves * ti) * 32 + 4 * hf;
-      const int32_t* prow = cx.pos_s + (w + kWaves * ti) * 32 + 4 * hf;
-#pragma unroll
-      for (int aa = 0; aa < 4; ++aa) {
-        const float4 b4 = *reinterpret_cast<const float4*>(brow + 8 * aa);
-        float x0 = __builtin_fmaf(e[4 * aa + 0], cx.alpha, -b4.x);
-        float x1 = __builtin_fmaf(e[4 * aa + 1], cx.alpha, -b4.y);
-        float x2 = __builtin_fmaf(e[4 * aa + 2], cx.alpha, -b4.z);
-        float x3 = __builtin_fmaf(e[4 * aa + 3], cx.alpha, -b4.w);
-        if (kMask) {   // exp2(-inf) = 0 for keys after the row's position
-          const int4 p4 = *reinterpret_cast<const int4*>(prow + 8 * aa);
-          const float ninf = -__builtin_inff();
-          x0 = key > p4.x ? ninf : x0;
-          x1 = key > p4.y ? ninf : x1;
-          x2 = key > p4.z ? ninf : x2;
-          x3 = key > p4.w ? ninf : x3;
-        }
-        e[4 * aa + 0] = fast_exp2(x0);
-        e[4 * aa + 1] = fast_exp2(x1);
-        e[4 * aa + 2] = fast_exp2(x2);
-        e[4 * aa + 3] = fast_exp2(x3);
-      }
-      if (!kMaxMean) {
-#pragma unroll
-        for (int v = 0; v < 16; v += 2) { a0 += e[v]; a1 += e[v + 1]; }
-      } else if (cx.G == 16) {
-        // the lane's 16 rows are one query's whole group
-        float mx = e[0];
-#pragma unroll
-        for (int v = 1; v < 16; ++v) mx = fmaxf(mx, e[v]);
-        a0 += mx;
-      } else if (cx.G == 8) {
-        // registers 0-7 and 8-15 are two queries' groups
-        float m0 = e[0], m1 = e[8];
-#pragma unroll
-        for (int v = 1; v < 8; ++v) { m0 = fmaxf(m0, e[v]); m1 = fmaxf(m1, e[8 + v]); }
-        a0 += m0; a1 += m1;
-      } else {
-        // registers v0..v0+3 are four consecutive rows of the natural order
-#pragma unroll
-        for (int v0 = 0; v0 < 16; v0 += 4) {
-          if (cx.G == 4) {
-            a0 += fmaxf(fmaxf(e[v0], e[v0 + 1]), fmaxf(e[v0 + 2], e[v0 + 3]));
-          } else if (cx.G == 2) {
-            a0 += fmaxf(e[v0], e[v0 + 1]);
-            a1 += fmaxf(e[v0 + 2], e[v0 + 3]);
-          } else {
-            a0 += e[v0] + e[v0 + 2];
-            a1 += e[v0 + 1] + e[v0 + 3];
-          }
-        }
-      }
-      // one row tile's accumulator at a time: keeps the wave within 256 registers (the
-      // other workgroup's wave on this SIMD supplies the MFMA / VALU overlap)
-      __builtin_amdgcn_sched_barrier(0);
+// Per-key partials of one tile: wave w, lane group q = l/16, key k at
+// red[w][q * kRedGrp + k].  The padded strides keep both the writes (64 lanes: 4 groups x
+// 16 keys) and the finishing reads (8 waves x 8 keys) on 64 distinct banks.
+constexpr int kRedGrp = kKeyTile + 16;     // 80 floats: group stride = 16 banks apart
+constexpr int kRedRow = 4 * kRedGrp + 8;   // 328 floats: wave stride = 8 banks apart
+typedef float RedTile[kWaves][kRedRow];
+constexpr int kRedBufs = 4;   // a tile's partials are read one tile later
+
+// Sum of the 32 partials of each key of tile t in a fixed order; wave w finishes keys
+// 8w .. 8w+7.  Lane l takes key 8w + l/8 and the four partials of wave l%8, then the
+// eight lanes of a key are summed pairwise (xor 1, 2, 4).
+__device__ __forceinline__ float dpp_xor1(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float dpp_xor2(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float swz_xor4(float v) {
+  // ds_swizzle bit mode: and 0x1f, or 0, xor 4 (within 32-lane halves)
+  return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x101F));
+}
+
+__device__ __forceinline__ void finish_tile(const SweepCtx& cx, const RedTile& red, int t) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int kk = w * (kKeyTile / kWaves) + (lane >> 3), ww = lane & 7;
+  const float* rr = red[ww] + kk;
+  float v = (rr[0] + rr[kRedGrp]) + (rr[2 * kRedGrp] + rr[3 * kRedGrp]);
+  v += dpp_xor1(v);
+  v += dpp_xor2(v);
+  v += swz_xor4(v);
+  const int key = t * kKeyTile + kk;
+  if (ww == 0 && key < cx.L) cx.out[key] = v * cx.out_scale;
+}
+
+// Phases P = 2 .. U+1 of tile i, U = 4 * NRT units per tile: the chain of unit P (of tile
+// i, or of tile i+1 once P >= U) and the epilogue of unit P - 2 of tile i.
+// kMask: tile i holds keys hidden from some rows.  kLast: no tile follows.
+template <int D, bool kMaxMean, int NRT, bool kMask, bool kLast, int P>
+__device__ __forceinline__ void tile_phases16(const SweepCtx& cx, const KLoadPlan<D, kWaves>& kp,
+                                              const KRead16& rp, Pipe16<D>& st,
+                                              const bf16x8 (&qreg)[kRowTilesPerWave][Geom16<D>::kSteps],
+                                              const float (&beta)[kRowTilesPerWave][4],
+                                              RedTile* red, int i, int64_t& next_page) {
+  constexpr int U = kSubTiles * NRT;
+  if constexpr (P <= U + 1) {
+    using Gm = TileGeom<D>;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    static_assert((kScoreStages & (kScoreStages - 1)) == 0, "stage index uses a mask");
+    const int st_i = (i - cx.i0) & (kScoreStages - 1), st_n = (i + 1 - cx.i0) & (kScoreStages - 1);
+    const char* buf_i = cx.kbuf + st_i * Gm::kTileBytes;
+    const char* buf_n = cx.kbuf + st_n * Gm::kTileBytes;
+    if constexpr (P == U - 1) {
+      // tile i + 1 is read from this phase on: this wave's loads of it have landed, this
+      // wave's LDS traffic of tile i is retired, then the barrier
+      wait_vmcnt<(kScoreStages - 2) * Gm::kLoadsPerWave>();
+      wait_lgkmcnt0();
+      __builtin_amdgcn_s_barrier();
+      // no wave reads tile i any more: refill its stage with tile i + kScoreStages
+      issue_k_tile<D, kWaves>(cx.kl + st_i * Gm::kTileBytes, cx.kv_bytes, next_page,
+                              cx.page_bytes, kp);
+      const int nt = i + kScoreStages + 1;
+      next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, nt < cx.i1 ? nt : cx.i1 - 1);
+      if (i > cx.i0) finish_tile(cx, red[(i - 1) & (kRedBufs - 1)], i - 1);
     }
-    float acc = a0 + a1;
-    acc += __shfl_xor(acc, 32, 64);   // lanes l and l+32 hold the same key
-    if (hf == 0) rd[sub * 32 + l32] = acc;
-    __builtin_amdgcn_sched_barrier(0);
+    // epilogue: unit P - 2 of tile i
+    constexpr int eu = P - 2, es = eu / NRT, er = eu % NRT;
+    const int32_t* prow = cx.pos_s + (w + kWaves * er) * kRowTile + 4 * (lane >> 4);
+    const int key = i * kKeyTile + es * 16 + (lane & 15);
+    // chain: unit P of tile i, or unit P - U of tile i + 1
+    constexpr bool kChain = P < U || !kLast;
+    constexpr int cr = (P < U ? P : P - U) % NRT;
+    // operand of unit P + 1 when it starts a sub-tile
+    constexpr int nu = P + 1;
+    constexpr bool kLoad = (nu % NRT == 0) && (nu < U || !kLast);
+    constexpr int lsub = (nu < U ? nu : nu - U) / NRT;
+    score_phase16<D, kMaxMean, kMask, kChain, true, kLoad, er>(
+        st, qreg[cr], rp, nu < U ? buf_i : buf_n, lsub, beta[er], prow, key, cx.alpha, cx.G);
+    if constexpr (er == NRT - 1) {
+      // sub-tile es is complete in this lane: hand its partial to the other waves
+      if (!kMaxMean) {
+        st.part[3] += st.ex;   // the pending exp2 of the unit's last element
+        st.ex = 0.f;
+      }
+      red[i & (kRedBufs - 1)][w][(lane >> 4) * kRedGrp + es * 16 + (lane & 15)] =
+          (st.part[0] + st.part[1]) + (st.part[2] + st.part[3]);
+      st.part[0] = st.part[1] = st.part[2] = st.part[3] = 0.f;
+    }
+    tile_phases16<D, kMaxMean, NRT, kMask, kLast, P + 1>(cx, kp, rp, st, qreg, beta, red, i,
+                                                          next_page);
   }
 }
 
-// Sweep key tiles i0 .. i1-1 of one segment with TPW row tiles (of 32 rows) per wave:
-// kStages-1 tiles in flight through the direct-to-LDS pipeline and one barrier per tile.
-template <int D, bool kMaxMean, int TPW>
-__device__ __forceinline__ void score_sweep(const SweepCtx& cx, const KLoadPlan<D, kWaves>& kp,
-                                            const bf16x8 (&qreg)[kTilesPerWave][TileGeom<D>::kSteps],
-                                            char (*kbuf)[TileGeom<D>::kTileBytes],
-                                            float (*red)[kWaves][kKeyTile]) {
+// Sweep key tiles i0 .. i1-1 of one segment with NRT row tiles per wave.  K tiles stream
+// through kScoreStages LDS buffers (direct-to-LDS loads, kScoreStages - 1 tiles ahead),
+// one barrier per tile.
+template <int D, bool kMaxMean, int NRT>
+__device__ __forceinline__ void score_sweep16(const SweepCtx& cx, const KLoadPlan<D, kWaves>& kp,
+                                              const bf16x8 (&qreg)[kRowTilesPerWave][Geom16<D>::kSteps],
+                                              const float (&beta)[kRowTilesPerWave][4],
+                                              RedTile* red) {
   using Gm = TileGeom<D>;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  auto clamp_tile = [&](int64_t t) { return t < cx.i1 ? t : cx.i1 - 1; };
+  auto clamp_tile = [&](int t) { return t < cx.i1 ? t : cx.i1 - 1; };
 #pragma unroll
-  for (int p = 0; p < kStages - 1; ++p)
+  for (int p = 0; p < kScoreStages - 1; ++p)
     issue_k_tile<D, kWaves>(cx.kl + p * Gm::kTileBytes, cx.kv_bytes,
                             page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(cx.i0 + p)),
                             cx.page_bytes, kp);
   int64_t next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp,
-                                         clamp_tile(cx.i0 + kStages - 1));
-  for (int64_t i = cx.i0; i < cx.i1; ++i) {
-    const int st = (int)((i - cx.i0) % kStages);
-    // tile i has landed once at most the later tiles' loads are outstanding; the barrier
-    // also retires every wave's reads of the stage the next load overwrites
-    wait_vmcnt<(kStages - 2) * Gm::kLoadsPerWave>();
-    __builtin_amdgcn_s_barrier();
-    issue_k_tile<D, kWaves>(cx.kl + ((st + kStages - 1) % kStages) * Gm::kTileBytes, cx.kv_bytes,
-                            next_page, cx.page_bytes, kp);
-    next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(i + kStages));
-    const int64_t key0 = i * kKeyTile;
-    float* rd = red[i & 1][w];
-    // tiles that reach past the first action position may hold keys hidden from some rows;
-    // they take a separate, masked copy of the body so that the common body has no branch
-    // (a branch per row tile would keep all of a tile's exp2 results live at once)
-    if (key0 + kKeyTile - 1 > cx.mask_from)
-      score_tile<D, kMaxMean, TPW, true>(cx, qreg, kbuf[st], key0, rd);
-    else
-      score_tile<D, kMaxMean, TPW, false>(cx, qreg, kbuf[st], key0, rd);
-    wait_lgkmcnt0();
-    __builtin_amdgcn_s_barrier();
-    // wave w finishes keys 16w .. 16w+15 of tile i (fixed summation order over waves)
-    if (lane < kKeyTile / kWaves) {
-      const int kk = w * (kKeyTile / kWaves) + lane;
-      const int64_t key = key0 + kk;
-      if (key < cx.L) {
-        float v = 0.f;
+                                         clamp_tile(cx.i0 + kScoreStages - 1));
+  const KRead16 rp = make_k_read16<D>();
+  Pipe16<D> st;
+  st.part[0] = st.part[1] = st.part[2] = st.part[3] = 0.f;
+  st.ex = 0.f;
+  st.mx = 0.f;
+  st.c1 = f32x4{0.f, 0.f, 0.f, 0.f};
+  // prologue: tile i0 in LDS, the last stage filled, chains of units 0 and 1
+  wait_vmcnt<(kScoreStages - 2) * Gm::kLoadsPerWave>();
+  __builtin_amdgcn_s_barrier();
+  issue_k_tile<D, kWaves>(cx.kl + (kScoreStages - 1) * Gm::kTileBytes, cx.kv_bytes, next_page,
+                          cx.page_bytes, kp);
+  next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(cx.i0 + kScoreStages));
 #pragma unroll
-        for (int ww = 0; ww < kWaves; ++ww) v += red[i & 1][ww][kk];
-        cx.out[key] = v * cx.out_scale;
-      }
+  for (int ks = 0; ks < Geom16<D>::kSteps; ++ks) st.kr[ks] = lds_k16<D>(cx.kbuf, 0, rp, ks);
+  score_phase16<D, kMaxMean, false, true, false, 1 % NRT == 0, 0>(
+      st, qreg[0], rp, cx.kbuf, 1 / NRT, beta[0], nullptr, 0, cx.alpha, cx.G);
+  score_phase16<D, kMaxMean, false, true, false, 2 % NRT == 0, 0>(
+      st, qreg[1 % NRT], rp, cx.kbuf, 2 / NRT, beta[0], nullptr, 0, cx.alpha, cx.G);
+  for (int i = cx.i0; i < cx.i1; ++i) {
+    const bool mask = i * kKeyTile + kKeyTile - 1 > cx.mask_from;
+    if (i + 1 < cx.i1) {
+      if (mask)
+        tile_phases16<D, kMaxMean, NRT, true, false, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page);
+      else
+        tile_phases16<D, kMaxMean, NRT, false, false, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page);
+    } else {
+      if (mask)
+        tile_phases16<D, kMaxMean, NRT, true, true, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page);
+      else
+        tile_phases16<D, kMaxMean, NRT, false, true, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page);
     }
   }
+  // the last tile's partials
+  wait_lgkmcnt0();
+  __builtin_amdgcn_s_barrier();
+  finish_tile(cx, red[(cx.i1 - 1) & (kRedBufs - 1)], cx.i1 - 1);
 }
 
 template <int D, bool kMaxMean>
-__global__ __launch_bounds__(kThreads, 2) void score_kernel(
+__global__ __launch_bounds__(kThreads, 1) void score_kernel(
     DevProblem dp, const uint16_t* __restrict__ q_ptr, const uint16_t* __restrict__ kv_ptr,
     const int32_t* __restrict__ bt_ptr, const float* __restrict__ lse_ptr,
     float* __restrict__ scores_ptr, float* __restrict__ part_ptr, int64_t num_scores) {
   using Gm = TileGeom<D>;
-  __shared__ __align__(1024) char kbuf[kStages][Gm::kTileBytes];
+  __shared__ __align__(1024) char kbuf[kScoreStages][Gm::kTileBytes];
   __shared__ __align__(16) float beta_s[kRowsPerChunk];
   __shared__ __align__(16) int32_t pos_s[kRowsPerChunk];
-  __shared__ float red[2][kWaves][kKeyTile];
+  __shared__ RedTile red[kRedBufs];
 
-  const int tid = threadIdx.x, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int G = dp.G, Hq = dp.Hq, Hkv = dp.Hkv, C = dp.max_chunks;
+  const bool grouped = kMaxMean && (G == 8 || G == 16);
   const int64_t nseg = dp.num_segments;
   const int64_t total = dp.seg_cost[nseg];
   const int64_t c0 = total * blockIdx.x / gridDim.x, c1 = total * (blockIdx.x + 1) / gridDim.x;
@@ -370,13 +558,13 @@ __global__ __launch_bounds__(kThreads, 2) void score_kernel(
 
   SweepCtx cx;
   cx.kv_bytes = reinterpret_cast<const char*>(kv_ptr);
-  cx.beta_s = beta_s;
   cx.pos_s = pos_s;
+  cx.kbuf = &kbuf[0][0];
+  cx.kl = (uint32_t)(uintptr_t)(lds_char*)&kbuf[0][0];
   cx.page_bytes = (int64_t)kPageSize * Hkv * D * 2;
   cx.num_pages = dp.num_pages;
   cx.G = G;
   cx.alpha = dp.sm_scale * kLog2e;
-  cx.kl = (uint32_t)(uintptr_t)(lds_char*)&kbuf[0][0];
 
   // first segment: the largest s with seg_cost[s] <= c0 (it is never empty)
   int64_t lo = 0, hi = nseg;
@@ -393,11 +581,12 @@ __global__ __launch_bounds__(kThreads, 2) void score_kernel(
     decode_segment(s, C, Hkv, &r, &c, &h);
     const ReqPlan pl = dp.plan[r];
     const int L = pl.L, n = pl.n, M = G * n;
-    const int RT = chunk_row_tiles(M, c);
+    const int RT = chunk_row_tiles(M, c);   // 32-row tiles: the unit of the segment cost
     const int64_t ntiles = ceil_div64(L, kKeyTile);
-    cx.i0 = first ? (c0 - cs + RT - 1) / RT : 0;
-    cx.i1 = (c1 - cs + RT - 1) / RT;
-    if (cx.i1 > ntiles) cx.i1 = ntiles;
+    int64_t i1 = (c1 - cs + RT - 1) / RT;
+    if (i1 > ntiles) i1 = ntiles;
+    cx.i0 = first ? (int)((c0 - cs + RT - 1) / RT) : 0;   // c0 < ce: below ntiles
+    cx.i1 = (int)i1;
     first = false;
     if (cx.i0 >= cx.i1) continue;
 
@@ -406,15 +595,15 @@ __global__ __launch_bounds__(kThreads, 2) void score_kernel(
     __syncthreads();
     for (int m = tid; m < kRowsPerChunk; m += kThreads) {
       int j, g;
-      row_to_query(G, c, m / 32, m % 32, &j, &g);
+      score_row_query(G, grouped, c, m / kRowTile, m % kRowTile, &j, &g);
       beta_s[m] = j < n ? lse_ptr[(int64_t)(pl.q_off + j) * Hq + h * G + g] * kLog2e
                         : __builtin_inff();
       pos_s[m] = dp.causal ? L - n + j : L - 1;
     }
-    bf16x8 qreg[kTilesPerWave][Gm::kSteps];
+    bf16x8 qreg[kRowTilesPerWave][Geom16<D>::kSteps];
 #pragma unroll
-    for (int ti = 0; ti < kTilesPerWave; ++ti)
-      load_q_tile<D>(qreg[ti], q_ptr, G, Hq, h, pl.q_off, n, c, w + kWaves * ti);
+    for (int rt = 0; rt < kRowTilesPerWave; ++rt)
+      load_q16<D>(qreg[rt], q_ptr, G, grouped, Hq, h, pl.q_off, n, c, w + kWaves * rt);
     cx.bt_row = bt_ptr + (int64_t)r * dp.bt_stride;
     cx.L = L;
     cx.mask_from = dp.causal ? L - n : L;  // keys past this may be hidden from some rows
@@ -426,13 +615,21 @@ __global__ __launch_bounds__(kThreads, 2) void score_kernel(
     // sweep needs no compiler-inserted wait on the vector-memory queue
     wait_vmcnt<0>();
     __syncthreads();   // beta_s / pos_s visible
-    // row tiles past the chunk's RT are all padding (Q = 0, beta = +inf): each wave runs
-    // only as many of its row tiles as can hold real rows
-    const int tpw = (RT + kWaves - 1) / kWaves;
-    if (tpw >= 4) score_sweep<D, kMaxMean, 4>(cx, kp, qreg, kbuf, red);
-    else if (tpw == 3) score_sweep<D, kMaxMean, 3>(cx, kp, qreg, kbuf, red);
-    else if (tpw == 2) score_sweep<D, kMaxMean, 2>(cx, kp, qreg, kbuf, red);
-    else score_sweep<D, kMaxMean, 1>(cx, kp, qreg, kbuf, red);
+    // beta of this lane's rows (4*(l/16) + i of each row tile): fixed for the sweep
+    float beta[kRowTilesPerWave][4];
+#pragma unroll
+    for (int rt = 0; rt < kRowTilesPerWave; ++rt) {
+      const float4 b4 = *reinterpret_cast<const float4*>(beta_s + (w + kWaves * rt) * kRowTile +
+                                                         4 * (lane >> 4));
+      beta[rt][0] = b4.x; beta[rt][1] = b4.y; beta[rt][2] = b4.z; beta[rt][3] = b4.w;
+    }
+    // row tiles past the chunk's real rows are all padding (Q = 0, beta = +inf): every
+    // wave runs only as many row tiles as can hold real rows
+    const int nrt = chunk_wave_tiles(G, grouped, n, c);
+    if (nrt >= 4) score_sweep16<D, kMaxMean, 4>(cx, kp, qreg, beta, red);
+    else if (nrt == 3) score_sweep16<D, kMaxMean, 3>(cx, kp, qreg, beta, red);
+    else if (nrt == 2) score_sweep16<D, kMaxMean, 2>(cx, kp, qreg, beta, red);
+    else score_sweep16<D, kMaxMean, 1>(cx, kp, qreg, beta, red);
   }
   wait_vmcnt<0>();   // drain: no LDS write may be outstanding when the workgroup exits
 }
@@ -464,7 +661,7 @@ hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
   if (hipGetDevice(&dev) == hipSuccess) {
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 256;
   }
-  int64_t grid = (int64_t)cus * 2;   // two 4-wave workgroups per CU
+  int64_t grid = cus;   // one 8-wave workgroup per CU
   if (grid > hp.score_cost) grid = hp.score_cost > 0 ? hp.score_cost : 1;
   const bool mm = dp.agg == ACTKV_AGG_MAX_MEAN;
   if (dp.D == 128) {
