@@ -108,6 +108,22 @@ def test_select_ties_and_plateaus_are_bit_exact():
     np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
 
 
+@pytest.mark.parametrize("window", [7, 9])
+def test_select_long_segments_are_bit_exact(window):
+    """Segments at, just past and well past the LDS-resident length (38,400 keys) take both
+    select paths; window 7 uses the fixed 7-tap pool, 9 the general one."""
+    pb = custom(seq_lens=[38400, 38401, 50000], q_lens=[1, 1, 1], num_q_heads=1,
+                num_kv_heads=1, head_dim=64, budgets=[9600, 20000, 12345],
+                pool_window=window, spike_frac=0.0)
+    rng = np.random.default_rng(11)
+    raw = (rng.standard_exponential(oracle.num_scores(pb)) * 1e-3).astype(np.float32)
+    raw[::97] = raw[5]   # a plateau of equal values across the threshold region
+    bp, t = to_dev(pb)
+    kept, pooled = actkv.select(bp, torch.from_numpy(raw).cuda())
+    np.testing.assert_array_equal(pooled.cpu().numpy(), oracle.pool(pb, raw))
+    np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
+
+
 @pytest.mark.parametrize("case", sorted(CASES))
 def test_compact_is_bit_exact_given_the_oracle_selection(case):
     pb = CASES[case]()
