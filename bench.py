@@ -32,6 +32,7 @@ SCORE_SOURCES = ["paper_2609_31395_amd/csrc/score.hip",
                  "paper_2609_31395_amd/csrc/device_common.hpp",
                  "paper_2609_31395_amd/csrc/actkv_internal.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_kernel_batch32x35k_traffic.json")
+COPY_CALIB_BYTES = 512 << 20   # the known-size copy that calibrates FETCH_SIZE / WRITE_SIZE
 
 
 def parse():
@@ -43,9 +44,12 @@ def parse():
     ap.add_argument("--cpu-sample-reqs", type=int, default=8,
                     help="requests of the workload the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile-stage", choices=["score", "select", "compact", "lse", "step"],
+    ap.add_argument("--profile-stage",
+                    choices=["score", "select", "compact", "lse", "step", "copy"],
                     help="only run one entry point --steps times (for counter collection); "
-                         "prints a short JSON line instead of the benchmark record")
+                         "prints a short JSON line instead of the benchmark record.  'copy' "
+                         "is the calibration: a plain device-to-device copy of "
+                         "COPY_CALIB_BYTES bytes")
     return ap.parse_args()
 
 
@@ -109,6 +113,21 @@ def run_stage(stage, reps, bp, dp, bts, lse, scores, pooled, kept, free, freed, 
                       "avg_us": (time.perf_counter() - t0) / reps * 1e6}))
 
 
+def run_copy_calibration(reps):
+    """A plain copy of COPY_CALIB_BYTES bytes, `reps` times: it reads and writes exactly that
+    many bytes, so it scales the HBM counters of the other kernels."""
+    import torch
+    src = torch.empty(COPY_CALIB_BYTES, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"profile_stage": "copy", "reps": reps, "bytes": COPY_CALIB_BYTES,
+                      "avg_us": (time.perf_counter() - t0) / reps * 1e6}))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -121,6 +140,9 @@ def main():
     from paper_2609_31395_amd import workloads as W
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.profile_stage == "copy":
+        run_copy_calibration(args.steps)
+        return
     actkv.load_library()
     dev = torch.device("cuda:0")
     t_gen = time.time()
