@@ -350,8 +350,9 @@ __device__ __forceinline__ void score_phase16(Pipe16<D>& st, const bf16x8 (&q)[G
         }
       }
     }
-    __builtin_amdgcn_sched_barrier(0);
   }
+  // one scheduling region per phase: the compiler interleaves the chain and the epilogue
+  __builtin_amdgcn_sched_barrier(0);
   if (kEpi && kMaxMean) {
     const float m01 = fmaxf(prev[0], prev[1]), m23 = fmaxf(prev[2], prev[3]);
     if (G == 1) {
