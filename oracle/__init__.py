@@ -27,11 +27,11 @@ AGG = {"sum": 0, "max_mean": 1}
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (-O2, no fast-math, OpenMP)."""
+    """Compile the oracle with gcc (-O2, no fast-math, no fused multiply-add, OpenMP)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp"
-        subprocess.run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
-                        "-o", tmp, _SRC, "-lm"], check=True)
+        subprocess.run(["gcc", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
+                        "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"], check=True)
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -67,8 +67,11 @@ def _load():
         lib.actkv_oracle_totals.argtypes = [P, ctypes.POINTER(i64), ctypes.POINTER(i64),
                                             ctypes.POINTER(i64)]
         lib.actkv_oracle_compact.argtypes = [P, vp, vp, vp, vp, i64, vp, vp]
+        lib.actkv_oracle_hits.argtypes = [P, vp, ctypes.c_double, vp]
+        lib.actkv_oracle_lrfu_update.argtypes = [P, vp, vp, ctypes.c_float, vp]
         for f in ("actkv_oracle_lse", "actkv_oracle_scores", "actkv_oracle_pool",
-                  "actkv_oracle_select", "actkv_oracle_totals", "actkv_oracle_compact"):
+                  "actkv_oracle_select", "actkv_oracle_totals", "actkv_oracle_compact",
+                  "actkv_oracle_hits", "actkv_oracle_lrfu_update"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -205,6 +208,52 @@ def step(pb, lse_in: Optional[np.ndarray] = None, agg: str = "sum", **kw) -> dic
     kv2, bt2, freed, new_lens = compact(pb, kept, **kw)
     return dict(raw=raw, pooled=pooled, kept=kept, kv=kv2, block_table=bt2, freed=freed,
                 new_lens=new_lens)
+
+
+def hits(pb, att: np.ndarray, top_p: float, **kw) -> np.ndarray:
+    """Top-p hit mask (uint8, same layout as the scores) of the scores `att` (Alg. 1 step 3)."""
+    b = _Bound(pb, **kw)
+    att = np.ascontiguousarray(att, dtype=np.float32)
+    out = np.zeros(att.shape[0], dtype=np.uint8)
+    _check(_load().actkv_oracle_hits(b.ref, att.ctypes.data, float(top_p), out.ctypes.data),
+           "hits")
+    return out
+
+
+def lrfu_update(pb, att: np.ndarray, hit: np.ndarray, decay: float, ks: np.ndarray,
+                **kw) -> np.ndarray:
+    """KS' = decay * KS + hit * att in fp32 (Alg. 1 step 4), on a copy of ks."""
+    b = _Bound(pb, **kw)
+    att = np.ascontiguousarray(att, dtype=np.float32)
+    hit = np.ascontiguousarray(hit, dtype=np.uint8)
+    out = np.array(ks, dtype=np.float32, copy=True, order="C")
+    _check(_load().actkv_oracle_lrfu_update(b.ref, att.ctypes.data, hit.ctypes.data,
+                                            float(decay), out.ctypes.data), "lrfu_update")
+    return out
+
+
+def lrfu_step(pb, ks: np.ndarray, top_p: float, decay: float,
+              lse_in: Optional[np.ndarray] = None, agg: str = "sum", **kw) -> dict:
+    """The step with LRFU keep scores (Alg. 1 steps 1-6): score, pool, hit mask, keep-score
+    update, TopK on the keep scores, compaction.  `ks` holds the keep score of every cached
+    entry (0 for entries new since the last step); ks_kept are those of the kept entries
+    (KS'), in the order of `kept`."""
+    raw = scores(pb, lse_in=lse_in, agg=agg, **kw)
+    pooled = pool(pb, raw, **kw)
+    hit = hits(pb, pooled, top_p, **kw)
+    ks2 = lrfu_update(pb, pooled, hit, decay, ks, **kw)
+    kept = select(pb, ks2, **kw)
+    seg = np.concatenate([[0], np.cumsum(np.repeat(np.asarray(pb.seq_lens, np.int64),
+                                                   pb.num_kv_heads))])
+    ks_kept, off = np.zeros(kept.shape[0], np.float32), 0
+    for s_i in range(seg.shape[0] - 1):
+        r, h = divmod(s_i, pb.num_kv_heads)
+        k = int(min(max(int(pb.budgets[r * pb.num_kv_heads + h]), 0), int(pb.seq_lens[r])))
+        ks_kept[off:off + k] = ks2[seg[s_i] + kept[off:off + k]]
+        off += k
+    kv2, bt2, freed, new_lens = compact(pb, kept, **kw)
+    return dict(raw=raw, pooled=pooled, hit=hit, ks=ks2, kept=kept, ks_kept=ks_kept, kv=kv2,
+                block_table=bt2, freed=freed, new_lens=new_lens)
 
 
 def num_threads() -> int:

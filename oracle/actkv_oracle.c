@@ -18,6 +18,9 @@
  *               window 1 means none).
  *   select   -- TopK(score, k = budget) per (request, KV head) (Alg. 1, step 5), ties to
  *               the lower token index, emitted in ascending token order.
+ *   lrfu     -- (the eviction policy of Sec. 5.1 / Alg. 1 steps 2-5) a top-p hit mask over the
+ *               scores and the attention-aware LRFU keep-score update; selection then
+ *               runs on the keep scores.
  *   compact  -- the survivors' K/V rows are written, in ascending token order, into fresh
  *               pages taken from a free list; the block table row is rewritten and the old
  *               pages are returned (the freed-block return of Sec. 7.2; the paper's own
@@ -373,4 +376,58 @@ int actkv_oracle_step(const oracle_problem* p, const uint16_t* q, uint16_t* kv, 
   if (!rc) rc = actkv_oracle_compact(p, kv, bt, kept_out, free_pages, num_free, freed_out,
                                      new_lens);
   return rc;
+}
+
+/* ---------------------------------------------------------------------------------------
+ * Attention-aware LRFU keep scores (Sec. 5.1 keep-score update; Alg. 1 steps 2-5).
+ *
+ * Hit mask (Alg. 1 step 3, GetHitMask): per (request, KV head), order the entries by score
+ * descending (ties: lower token index first) and take the shortest prefix whose running
+ * sum reaches top_p times the segment's total.  Those entries are hits.  The running sum
+ * and the total are carried in double; a segment whose top_p * total is not positive has
+ * no hits.
+ * ------------------------------------------------------------------------------------- */
+int actkv_oracle_hits(const oracle_problem* p, const float* att, double top_p, uint8_t* hit) {
+  if (check_problem(p)) return -1;
+  for (int r = 0; r < p->num_reqs; ++r) {
+    const int64_t L = p->seq_lens[r], soff = score_offset(p, r);
+    for (int h = 0; h < p->num_kv_heads; ++h) {
+      const float* a = att + soff + h * L;
+      uint8_t* out = hit + soff + h * L;
+      double total = 0.0;
+      for (int64_t t = 0; t < L; ++t) total += (double)a[t];
+      for (int64_t t = 0; t < L; ++t) out[t] = 0;
+      const double need = top_p * total;
+      if (!(need > 0.0)) continue;
+      scored_entry* e = (scored_entry*)malloc(sizeof(scored_entry) * (size_t)(L > 0 ? L : 1));
+      for (int64_t t = 0; t < L; ++t) {
+        e[t].v = a[t] == 0.0f ? 0.0f : a[t];
+        e[t].t = (int32_t)t;
+      }
+      qsort(e, (size_t)L, sizeof(scored_entry), by_score_then_index);
+      double run = 0.0;
+      for (int64_t i = 0; i < L && run < need; ++i) {
+        out[e[i].t] = 1;
+        run += (double)e[i].v;
+      }
+      free(e);
+    }
+  }
+  return 0;
+}
+
+/* Keep-score update (Alg. 1 step 4): KS <- decay * KS, plus the entry's score if it is a
+ * hit.  KS is fp32 state; each of the two operations rounds to fp32 (no fused multiply-add),
+ * in this order. */
+int actkv_oracle_lrfu_update(const oracle_problem* p, const float* att, const uint8_t* hit,
+                             float decay, float* ks) {
+  if (check_problem(p)) return -1;
+  int64_t n = 0;
+  for (int r = 0; r < p->num_reqs; ++r) n += (int64_t)p->seq_lens[r] * p->num_kv_heads;
+  for (int64_t i = 0; i < n; ++i) {
+    volatile float scaled = decay * ks[i];
+    volatile float sum = scaled + (hit[i] ? att[i] : 0.0f);
+    ks[i] = sum;
+  }
+  return 0;
 }
