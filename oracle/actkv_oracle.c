@@ -385,7 +385,8 @@ int actkv_oracle_step(const oracle_problem* p, const uint16_t* q, uint16_t* kv, 
  * descending (ties: lower token index first) and take the shortest prefix whose running
  * sum reaches top_p times the segment's total.  Those entries are hits.  The running sum
  * and the total are carried in double; a segment whose top_p * total is not positive has
- * no hits.
+ * no hits.  top_p >= 1 asks for the whole mass: every entry with a positive score is a hit
+ * (the same set, without depending on how the running sum rounds against the total).
  * ------------------------------------------------------------------------------------- */
 int actkv_oracle_hits(const oracle_problem* p, const float* att, double top_p, uint8_t* hit) {
   if (check_problem(p)) return -1;
@@ -399,6 +400,10 @@ int actkv_oracle_hits(const oracle_problem* p, const float* att, double top_p, u
       for (int64_t t = 0; t < L; ++t) out[t] = 0;
       const double need = top_p * total;
       if (!(need > 0.0)) continue;
+      if (top_p >= 1.0) {
+        for (int64_t t = 0; t < L; ++t) out[t] = a[t] > 0.0f;
+        continue;
+      }
       scored_entry* e = (scored_entry*)malloc(sizeof(scored_entry) * (size_t)(L > 0 ? L : 1));
       for (int64_t t = 0; t < L; ++t) {
         e[t].v = a[t] == 0.0f ? 0.0f : a[t];

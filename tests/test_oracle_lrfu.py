@@ -24,7 +24,9 @@ def brute_hits(att, seq_lens, H, p):
         for _ in range(H):
             a = att[off:off + L].astype(np.float64)
             need = p * a.sum()
-            if need > 0:
+            if need > 0 and p >= 1:
+                out[off:off + L] = a > 0
+            elif need > 0:
                 order = np.lexsort((np.arange(L), -a))
                 run = np.cumsum(a[order])
                 m = int(np.searchsorted(run, need, side="left")) + 1   # first index reaching need
