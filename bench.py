@@ -10,6 +10,10 @@ Prints ONE JSON line (rank 0).  Default workload: 32 requests x 35,000 cached to
 Qwen3-30B head shapes (32 query / 4 KV heads, head_dim 128, 16-token pages), 64 action
 queries per request, 25% budget per KV head, pool window 7 -- drawn on the device from a
 seeded generator.
+
+Besides the headline step the record carries the per-stage durations, the step with the
+LSE pass included, and the step with LRFU eviction (Sec. 5.1: keep scores carried over,
+top-p 0.9 hit mask, decay 0.5) in the "lrfu" field.
 """
 from __future__ import annotations
 
@@ -33,6 +37,7 @@ SCORE_SOURCES = ["paper_2609_31395_amd/csrc/score.hip",
                  "paper_2609_31395_amd/csrc/actkv_internal.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_kernel_batch32x35k_traffic.json")
 COPY_CALIB_BYTES = 512 << 20   # the known-size copy that calibrates FETCH_SIZE / WRITE_SIZE
+LRFU_TOP_P, LRFU_DECAY = 0.9, 0.5   # the eviction policy's settings in the paper's evaluation
 
 
 def parse():
@@ -45,7 +50,8 @@ def parse():
                     help="requests of the workload the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-stage",
-                    choices=["score", "select", "compact", "lse", "step", "copy"],
+                    choices=["score", "select", "compact", "lse", "step", "lrfu_select",
+                             "lrfu_step", "copy"],
                     help="only run one entry point --steps times (for counter collection); "
                          "prints a short JSON line instead of the benchmark record.  'copy' "
                          "is the calibration: a plain device-to-device copy of "
@@ -94,6 +100,8 @@ def run_stage(stage, reps, bp, dp, bts, lse, scores, pooled, kept, free, freed, 
     first = bts[0].clone()   # bts are all pristine here; the prep step gets its own copy
     actkv.step(bp, dp.q, dp.kv, first, free, lse=lse, scores=scores, pooled=pooled, kept=kept,
                freed=freed, new_lens=new_lens, ws=ws, qy=qy)
+    ks = pooled.clone()   # keep scores of a previous step
+    ks_kept = torch.empty(max(qy["num_kept"], 1), dtype=torch.float32, device=scores.device)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(reps):
@@ -105,6 +113,13 @@ def run_stage(stage, reps, bp, dp, bts, lse, scores, pooled, kept, free, freed, 
             actkv.compact(bp, dp.kv, bts[i], kept, free, freed=freed, new_lens=new_lens, ws=ws)
         elif stage == "lse":
             actkv.lse(bp, dp.q, dp.kv, bts[i], out=lse, ws=ws)
+        elif stage == "lrfu_select":
+            actkv.lrfu_select(bp, scores, ks, LRFU_TOP_P, LRFU_DECAY, kept=kept, ks_kept=ks_kept,
+                              ws=ws)
+        elif stage == "lrfu_step":
+            actkv.step_lrfu(bp, dp.q, dp.kv, bts[i], free, ks, LRFU_TOP_P, LRFU_DECAY, lse=lse,
+                            scores=scores, kept=kept, ks_kept=ks_kept, freed=freed,
+                            new_lens=new_lens, ws=ws, qy=qy)
         else:
             actkv.step(bp, dp.q, dp.kv, bts[i], free, lse=lse, scores=scores, pooled=pooled,
                        kept=kept, freed=freed, new_lens=new_lens, ws=ws, qy=qy)
@@ -234,6 +249,36 @@ def main():
     log(f"stages (us) {np.round(stage_ms * 1e3, 1).tolist()}, step with LSE pass "
         f"{ms_with_lse * 1e3:.1f} us")
 
+    # ---- the step with LRFU eviction (keep scores carried from step to step, top-p hit
+    # mask), and its select stage on its own, both on the launch stream
+    ks = pooled.clone()   # the keep scores a previous step left
+    ks_kept = torch.empty(max(qy["num_kept"], 1), dtype=torch.float32, device=dev)
+    for b in bts:
+        b.copy_(bt0)
+    torch.cuda.synchronize()
+
+    def lrfu_step(bt):
+        actkv.step_lrfu(bp, dp.q, dp.kv, bt, free, ks, LRFU_TOP_P, LRFU_DECAY, lse=lse,
+                        scores=scores, kept=kept, ks_kept=ks_kept, freed=freed,
+                        new_lens=new_lens, ws=ws, qy=qy)
+
+    lrfu_step(bts[K])   # warm-up on its own pristine copy
+    torch.cuda.synchronize()
+    el[0].record(stream)
+    for i in range(K):
+        lrfu_step(bts[i])
+    el[1].record(stream)
+    torch.cuda.synchronize()
+    ms_lrfu = el[0].elapsed_time(el[1]) / K
+    el[0].record(stream)
+    for i in range(K):
+        actkv.lrfu_select(bp, scores, ks, LRFU_TOP_P, LRFU_DECAY, kept=kept, ks_kept=ks_kept,
+                          ws=ws)
+    el[1].record(stream)
+    torch.cuda.synchronize()
+    ms_lrfu_select = el[0].elapsed_time(el[1]) / K
+    log(f"LRFU step {ms_lrfu * 1e3:.1f} us, LRFU select {ms_lrfu_select * 1e3:.1f} us")
+
     sum_L = int(dp.seq_lens.astype(np.int64).sum())
     value = sum_L / (ms_per_step * 1e-3)
     alg_bytes = algorithmic_bytes(dp, qy["num_kept"])
@@ -298,6 +343,9 @@ def main():
         "stages_us": {"score": stage_ms[0] * 1e3, "select": stage_ms[1] * 1e3,
                       "compact": stage_ms[2] * 1e3},
         "step_with_lse_pass_us": ms_with_lse * 1e3,
+        "lrfu": {"top_p": LRFU_TOP_P, "decay": LRFU_DECAY, "step_us": ms_lrfu * 1e3,
+                 "select_us": ms_lrfu_select * 1e3,
+                 "tokens_per_s": sum_L / (ms_lrfu * 1e-3)},
         "roofline": {
             "kernel": "score_kernel (actkv_score, LSE supplied)",
             "bound": "mfma",

@@ -173,6 +173,49 @@ actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
                         int32_t* freed_pages, int32_t* new_lens, void* workspace,
                         size_t workspace_bytes, void* stream);
 
+/*
+ * Eviction with attention-aware LRFU keep scores (Sec. 5.1 keep-score update; Alg. 1
+ * steps 2-5) in place of plain TopK on the scores.  Per (request, KV head):
+ *   att     = the max-pooled scores (pool_window; 1 = the scores), also written to `pooled`
+ *             when it is not NULL;
+ *   hit     = the shortest prefix of the entries ordered by att descending (ties: lower
+ *             token index first) whose mass reaches top_p times the segment's total
+ *             (GetHitMask, step 3); none where that target is not positive; top_p = 1 hits
+ *             every entry with att > 0.  att is a probability-like score: entries with
+ *             att <= 0 carry no mass;
+ *   ks      = decay * ks + (hit ? att : 0), in place, in fp32 with the product and the sum
+ *             each rounded (step 4);
+ *   kept    = the k_rh entries with the largest ks, ties to the lower token index, written
+ *             ascending as in actkv_select (TopK on the keep scores, step 5);
+ *   ks_kept = ks of the kept entries, in the order of `kept`: the keep scores that travel
+ *             with the compacted K/V (KS' of Alg. 1).
+ * ks: fp32 [num_scores] in/out, same layout as the scores; entries new since the last step
+ * enter with 0 (step 2 is the caller's concatenation).  hit (nullable): uint8 [num_scores],
+ * 1 = hit.  ks_kept: fp32 [num_kept].  top_p and decay in [0, 1] (else
+ * ACTKV_ERR_INVALID_ARGUMENT).  ks must not overlap scores or pooled.  Segments longer than
+ * 38,400 entries: ACTKV_ERR_UNSUPPORTED.  The mass sums are exact 64-bit fixed-point sums of
+ * the scores scaled by a power of two (deterministic); where the prefix boundary falls within
+ * that resolution of the target, the boundary entry may differ from a floating-point
+ * evaluation.
+ */
+actkv_status actkv_lrfu_select(const actkv_problem* p, const float* scores, float top_p,
+                               float decay, float* ks, uint8_t* hit, float* pooled,
+                               int32_t* kept, float* ks_kept, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/*
+ * The whole step with LRFU eviction (Alg. 1 steps 1-6): score -> actkv_lrfu_select ->
+ * compact on `stream`.  Arguments as in actkv_step and actkv_lrfu_select; scores, pooled,
+ * hit and kept are optional outputs (NULL keeps them in the workspace, hit NULL: not
+ * written).
+ */
+actkv_status actkv_step_lrfu(const actkv_problem* p, const void* q, void* kv_cache,
+                             int32_t* block_table, const float* lse, const int32_t* free_pages,
+                             int64_t num_free, float top_p, float decay, float* ks,
+                             float* ks_kept, float* scores, float* pooled, uint8_t* hit,
+                             int32_t* kept, int32_t* freed_pages, int32_t* new_lens,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static text for a status code. */
 const char* actkv_status_str(actkv_status status);
 

@@ -63,8 +63,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.actkv_select.argtypes = [P, vp, vp, vp, vp, sz, vp]
     lib.actkv_compact.argtypes = [P, vp, vp, vp, vp, i64, vp, vp, vp, sz, vp]
     lib.actkv_step.argtypes = [P, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, sz, vp]
+    f32 = ctypes.c_float
+    lib.actkv_lrfu_select.argtypes = [P, vp, f32, f32, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.actkv_step_lrfu.argtypes = [P, vp, vp, vp, vp, vp, i64, f32, f32, vp, vp, vp, vp, vp,
+                                    vp, vp, vp, vp, sz, vp]
     for f in ("actkv_query", "actkv_lse", "actkv_score", "actkv_select", "actkv_compact",
-              "actkv_step"):
+              "actkv_step", "actkv_lrfu_select", "actkv_step_lrfu"):
         getattr(lib, f).restype = ctypes.c_int
     lib.actkv_status_str.argtypes = [ctypes.c_int]
     lib.actkv_status_str.restype = ctypes.c_char_p
@@ -246,6 +250,57 @@ def step(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch
                                         ws.numel(), _stream(stream)))
     return dict(freed=freed[:qy["pages_freed"]], new_lens=new_lens, scores=scores,
                 pooled=pooled, kept=None if kept is None else kept[:qy["num_kept"]])
+
+
+def lrfu_select(p: Problem, scores: torch.Tensor, ks: torch.Tensor, top_p: float,
+                decay: float, pooled: Optional[torch.Tensor] = None,
+                hit: Optional[torch.Tensor] = None, kept: Optional[torch.Tensor] = None,
+                ks_kept: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                stream=None) -> dict:
+    """LRFU eviction; ks (fp32, same layout as scores) is updated in place.  Returns kept,
+    ks_kept, and the optional pooled / hit outputs."""
+    lib = load_library()
+    dev = scores.device
+    nk = query(p)["num_kept"]
+    if kept is None:
+        kept = torch.empty(max(nk, 1), dtype=torch.int32, device=dev)
+    if ks_kept is None:
+        ks_kept = torch.empty(max(nk, 1), dtype=torch.float32, device=dev)
+    ws = workspace(p, dev) if ws is None else ws
+    c = p.cstruct()
+    _check("actkv_lrfu_select", lib.actkv_lrfu_select(
+        ctypes.byref(c), _ptr(scores), float(top_p), float(decay), _ptr(ks), _ptr(hit),
+        _ptr(pooled), _ptr(kept), _ptr(ks_kept), _ptr(ws), ws.numel(), _stream(stream)))
+    return dict(kept=kept[:nk], ks_kept=ks_kept[:nk], pooled=pooled, hit=hit)
+
+
+def step_lrfu(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch.Tensor,
+              free_pages: torch.Tensor, ks: torch.Tensor, top_p: float, decay: float,
+              lse: Optional[torch.Tensor] = None, scores: Optional[torch.Tensor] = None,
+              pooled: Optional[torch.Tensor] = None, hit: Optional[torch.Tensor] = None,
+              kept: Optional[torch.Tensor] = None, ks_kept: Optional[torch.Tensor] = None,
+              freed: Optional[torch.Tensor] = None, new_lens: Optional[torch.Tensor] = None,
+              ws: Optional[torch.Tensor] = None, stream=None, qy: Optional[dict] = None) -> dict:
+    """The whole step with LRFU eviction, in place on kv_cache / block_table / ks."""
+    lib = load_library()
+    dev = kv_cache.device
+    qy = query(p) if qy is None else qy
+    if freed is None:
+        freed = torch.empty(max(qy["pages_freed"], 1), dtype=torch.int32, device=dev)
+    if new_lens is None:
+        new_lens = torch.empty(p.num_reqs * p.num_kv_heads, dtype=torch.int32, device=dev)
+    if ks_kept is None:
+        ks_kept = torch.empty(max(qy["num_kept"], 1), dtype=torch.float32, device=dev)
+    ws = workspace(p, dev) if ws is None else ws
+    c = p.cstruct()
+    _check("actkv_step_lrfu", lib.actkv_step_lrfu(
+        ctypes.byref(c), _ptr(q), _ptr(kv_cache), _ptr(block_table), _ptr(lse),
+        _ptr(free_pages), free_pages.numel(), float(top_p), float(decay), _ptr(ks),
+        _ptr(ks_kept), _ptr(scores), _ptr(pooled), _ptr(hit), _ptr(kept), _ptr(freed),
+        _ptr(new_lens), _ptr(ws), ws.numel(), _stream(stream)))
+    return dict(freed=freed[:qy["pages_freed"]], new_lens=new_lens,
+                ks_kept=ks_kept[:qy["num_kept"]], scores=scores, pooled=pooled, hit=hit,
+                kept=None if kept is None else kept[:qy["num_kept"]])
 
 
 def status_str(code: int) -> str:

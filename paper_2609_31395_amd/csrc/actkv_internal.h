@@ -104,6 +104,11 @@ hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
                         float* score_part, hipStream_t s);
 hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
                          float* pooled, int32_t* kept, hipStream_t s);
+// LRFU selection (attention-aware keep scores): segments up to kLrfuMaxLen entries.
+constexpr int64_t kLrfuMaxLen = 38400;
+hipError_t launch_lrfu_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
+                              float top_p, float decay, float* ks, uint8_t* hit, float* pooled,
+                              int32_t* kept, float* ks_kept, hipStream_t s);
 hipError_t launch_compact(const DevProblem& dp, const HostPlan& hp, void* kv, int32_t* bt,
                           const int32_t* kept, const int32_t* free_pages, int32_t* freed,
                           int32_t* new_lens, hipStream_t s);

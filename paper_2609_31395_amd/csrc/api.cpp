@@ -232,6 +232,74 @@ actkv_status actkv_compact(const actkv_problem* p, void* kv_cache, int32_t* bloc
                                           freed_pages, new_lens, s));
 }
 
+namespace {
+actkv_status check_lrfu(const Ctx& cx, float top_p, float decay, const float* scores,
+                        const float* ks, const float* pooled, const int32_t* kept,
+                        const float* ks_kept) {
+  if (!(top_p >= 0.0f && top_p <= 1.0f) || !(decay >= 0.0f && decay <= 1.0f))
+    return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.max_L > actkv::kLrfuMaxLen) return ACTKV_ERR_UNSUPPORTED;
+  if (cx.hp.num_scores > 0 && !ks) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.num_kept > 0 && (!kept || !ks_kept)) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (ks && (ks == scores || ks == pooled)) return ACTKV_ERR_INVALID_ARGUMENT;
+  return ACTKV_OK;
+}
+}  // namespace
+
+actkv_status actkv_lrfu_select(const actkv_problem* p, const float* scores, float top_p,
+                               float decay, float* ks, uint8_t* hit, float* pooled,
+                               int32_t* kept, float* ks_kept, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  Ctx cx;
+  actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
+  if (st != ACTKV_OK) return st;
+  if (cx.hp.num_scores > 0 && !scores) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (pooled && scores && pooled == scores) return ACTKV_ERR_INVALID_ARGUMENT;
+  st = check_lrfu(cx, top_p, decay, scores, ks, pooled, kept, ks_kept);
+  if (st != ACTKV_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cx.hp.R == 0) return ACTKV_OK;
+  st = hip_status(actkv::launch_plan(cx.dp, s));
+  if (st != ACTKV_OK) return st;
+  return hip_status(actkv::launch_lrfu_select(cx.dp, cx.hp, scores, top_p, decay, ks, hit,
+                                              pooled, kept, ks_kept, s));
+}
+
+actkv_status actkv_step_lrfu(const actkv_problem* p, const void* q, void* kv_cache,
+                             int32_t* block_table, const float* lse, const int32_t* free_pages,
+                             int64_t num_free, float top_p, float decay, float* ks,
+                             float* ks_kept, float* scores, float* pooled, uint8_t* hit,
+                             int32_t* kept, int32_t* freed_pages, int32_t* new_lens,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  Ctx cx;
+  actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
+  if (st != ACTKV_OK) return st;
+  if (num_free < 0) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.R > 0 && (!block_table || !new_lens)) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.num_scores > 0 && !kv_cache) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.sum_n > 0 && !q) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.pages_freed > 0 && !freed_pages) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (num_free < cx.hp.fresh_needed) return ACTKV_ERR_OUT_OF_PAGES;
+  if (cx.hp.fresh_needed > 0 && !free_pages) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (scores && pooled && scores == pooled) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (!scores) scores = reinterpret_cast<float*>(cx.base + cx.ws.scores);
+  if (!pooled) pooled = reinterpret_cast<float*>(cx.base + cx.ws.pooled);
+  if (!kept) kept = reinterpret_cast<int32_t*>(cx.base + cx.ws.kept);
+  st = check_lrfu(cx, top_p, decay, scores, ks, pooled, kept, ks_kept);
+  if (st != ACTKV_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cx.hp.R == 0) return ACTKV_OK;
+  st = hip_status(actkv::launch_plan(cx.dp, s));
+  if (st != ACTKV_OK) return st;
+  st = run_score(cx, q, kv_cache, block_table, lse, scores, s);
+  if (st != ACTKV_OK) return st;
+  st = hip_status(actkv::launch_lrfu_select(cx.dp, cx.hp, scores, top_p, decay, ks, hit, pooled,
+                                            kept, ks_kept, s));
+  if (st != ACTKV_OK) return st;
+  return hip_status(actkv::launch_compact(cx.dp, cx.hp, kv_cache, block_table, kept, free_pages,
+                                          freed_pages, new_lens, s));
+}
+
 actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
                         int32_t* block_table, const float* lse, const int32_t* free_pages,
                         int64_t num_free, float* scores, float* pooled, int32_t* kept,

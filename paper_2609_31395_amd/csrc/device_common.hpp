@@ -35,35 +35,57 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-// Inclusive prefix sum over one wave (64 lanes) of a 64-bit value.
+// One DPP step on a 64-bit value (both halves moved by the same lane pattern); lanes with
+// no source, and lanes of rows outside kRowMask, read 0.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ int64_t dpp_i64(int64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, kCtrl, kRowMask,
+                                                            0xf, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(
+      0, (int)(uint32_t)((uint64_t)v >> 32), kCtrl, kRowMask, 0xf, false);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// The 64-bit value of lane `lane` (wave-uniform) for every lane.
+__device__ __forceinline__ int64_t readlane_i64(int64_t v, int lane) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), lane);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Inclusive prefix sum over one wave (64 lanes) of a 64-bit value: shifts by 1, 2, 4 and 8
+// lanes within each row of 16, then the last lane of row 0 (row 2) is added into row 1
+// (row 3), and the last lane of row 1 into rows 2 and 3.
 __device__ __forceinline__ int64_t wave_incl_scan_i64(int64_t v) {
-  const int lane = threadIdx.x & (kWave - 1);
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    int64_t o = __shfl_up(v, d, kWave);
-    if (lane >= d) v += o;
-  }
+  v += dpp_i64<0x111, 0xf>(v);   // row_shr:1
+  v += dpp_i64<0x112, 0xf>(v);   // row_shr:2
+  v += dpp_i64<0x114, 0xf>(v);   // row_shr:4
+  v += dpp_i64<0x118, 0xf>(v);   // row_shr:8
+  v += dpp_i64<0x142, 0xa>(v);   // row_bcast:15 into rows 1 and 3
+  v += dpp_i64<0x143, 0xc>(v);   // row_bcast:31 into rows 2 and 3
   return v;
 }
 
 // Exclusive prefix sum over the whole block (blockDim.x a multiple of 64, <= 1024).
-// `tmp` is __shared__ int64_t[16 + 1].  Returns the exclusive prefix; *total the sum.
+// `tmp` is __shared__ int64_t[16 + 1].  Returns the exclusive prefix; *total the sum.  Every
+// thread adds up the wave totals itself (broadcast LDS reads), so there is no serial step.
 __device__ __forceinline__ int64_t block_excl_scan_i64(int64_t v, int64_t* tmp, int64_t* total) {
   const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
   const int nw = blockDim.x / kWave;
-  int64_t inc = wave_incl_scan_i64(v);
+  const int64_t inc = wave_incl_scan_i64(v);
   if (lane == kWave - 1) tmp[w] = inc;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int64_t acc = 0;
-    for (int i = 0; i < nw; ++i) { int64_t t = tmp[i]; tmp[i] = acc; acc += t; }
-    tmp[16] = acc;
-  }
-  __syncthreads();
-  int64_t ex = tmp[w] + inc - v;
-  *total = tmp[16];
-  __syncthreads();
-  return ex;
+  // lanes 0..nw-1 of every wave pick up the wave totals and scan them within the first row
+  int64_t t = lane < nw ? tmp[lane] : 0;
+  t += dpp_i64<0x111, 0xf>(t);
+  t += dpp_i64<0x112, 0xf>(t);
+  t += dpp_i64<0x114, 0xf>(t);
+  t += dpp_i64<0x118, 0xf>(t);
+  const int64_t all = readlane_i64(t, nw - 1);
+  const int64_t before = w > 0 ? readlane_i64(t, w > 0 ? w - 1 : 0) : 0;
+  __syncthreads();   // tmp may be written again right after
+  *total = all;
+  return before + inc - v;
 }
 
 // Exclusive prefix count of a per-thread flag across the block, in thread order.

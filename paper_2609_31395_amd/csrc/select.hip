@@ -1,22 +1,26 @@
 // Eviction: per (request, KV head) keep the k = min(budget, L) entries with the largest
 // max-pooled score, ties to the lower token index (Alg. 1 step 5, TopK), emitted in
-// ascending token order.
+// ascending token order; and the attention-aware LRFU variant (Sec. 5.1) that ranks by
+// keep scores carried over from step to step instead.
 //
 // One 1024-thread workgroup per (request, KV head).  Every decision below is made on an
 // unsigned key derived from the fp32 bit pattern that orders exactly like the float, so the
 // result is exact and deterministic.
-//   pool    the raw scores of the segment are staged in LDS (coalesced loads, all in
-//           flight at once) and max-pooled over the window (clipped at the ends); the
-//           pooled scores go to `pooled` in global memory and their order keys stay in
-//           registers, then replace the raw scores in LDS.  Segments longer than the LDS
-//           capacity run the same passes on `pooled` itself.
-//   radix   three digit passes of 11, 11 and 10 bits over the register-resident keys (LDS
-//           histogram, most significant first) find the bit pattern tau of the k-th largest key and how many keys equal
-//           to tau to take.  The first digit spans the exponent and two mantissa bits, so
-//           even densely packed scores spread over many bins (few atomic collisions).
-//   emit    each thread owns a contiguous run of the segment; two workgroup prefix sums
-//           (equal-to-tau counts, then kept counts) give every thread its output offset,
-//           so the kept indices come out in ascending order.
+//   stage   the raw scores of the segment are loaded into LDS (coalesced raw buffer loads)
+//   pool    max-pooled in place over the window, clipped at the ends, and copied out
+//   radix   digit passes of up to 11 bits over the segment's key range (LDS histogram, most
+//           significant digit first) find the key tau of the k-th largest entry and how
+//           many entries equal to tau to take
+//   emit    each thread owns a contiguous run of the segment; one workgroup prefix sum of
+//           its (greater, equal) counts gives its output offset, so the kept indices come
+//           out in ascending order
+// From the pool to the emit LDS holds the order keys of the segment and every pass re-reads
+// its run from there.  The passes are bound by vector ALU issue (one workgroup per segment
+// leaves four waves per SIMD), so each visit of an entry is kept to a few instructions:
+// keys instead of floats (no conversion per pass), batched LDS reads at immediate offsets
+// (the LDS buffer is padded so a batch may read past the end of the segment), 32-bit digit
+// arithmetic.
+// Segments longer than the LDS capacity run the same steps on `pooled` in global memory.
 #include "device_common.hpp"
 
 namespace actkv {
@@ -25,9 +29,18 @@ namespace {
 
 constexpr int kSelectThreads = 1024;
 constexpr int kSelectLdsKeys = 38400;     // segment length kept in LDS (153,600 bytes)
+static_assert(kSelectLdsKeys == kLrfuMaxLen, "the LRFU selection runs on the LDS path only");
 constexpr int kMaxBins = 2048;            // largest digit: 11 bits
 constexpr int kDigits = 3;                // bits 31..21, 20..10, 9..0
-constexpr int kMaxPerThread = (kSelectLdsKeys + kSelectThreads - 1) / kSelectThreads;   // 38
+constexpr int kRows = (kSelectLdsKeys + kSelectThreads - 1) / kSelectThreads;   // 38
+constexpr int kRowBatch = kRows / 2;      // rows of a coalesced pass in flight together
+static_assert(kRows % 2 == 0, "the coalesced passes run in two batches of rows");
+constexpr int kRunBatch = 8;              // run entries whose LDS reads are issued together
+constexpr int kLdsPad = 16;               // LDS entries past the segment a batch may read
+constexpr int kPoolHalo = 3;              // pooling windows up to 7 run in place
+// Word 3 of a raw (stride 0) buffer resource on CDNA: 32-bit data format; reads at byte
+// offsets at or past num_records return 0 and writes there are dropped.
+constexpr int kBufferRsrcWord3 = 0x00020000;
 
 // Unsigned key that orders exactly like the float (negative values included; -0 == +0).
 __device__ __forceinline__ uint32_t order_key(float v) {
@@ -40,12 +53,28 @@ __device__ __forceinline__ float key_value(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
+// -0 as +0 (the pooled score of an entry is the value its order key stands for).
+__device__ __forceinline__ float canonical(float v) { return v == 0.0f ? 0.0f : v; }
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_over(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes,
+                                           kBufferRsrcWord3);
+}
+
+// Byte offset of this lane in a coalesced pass, opaque to the compiler so that the offsets
+// of two passes are not shared (and kept live) between them.
+__device__ __forceinline__ int lane_byte_offset() {
+  int off = (int)threadIdx.x * (int)sizeof(float);
+  asm volatile("" : "+v"(off));
+  return off;
+}
+
 // Among bins [0, nbins) (higher bin = larger key), find the bin b holding the need-th
 // largest element: sum_{b' > b} hist[b'] < need <= sum_{b' >= b} hist[b'].  Thread t covers
 // max(1, nbins / kSelectThreads) bins counted down from the top.  Returns b and the count
 // strictly above it through LDS.
-__device__ void find_bin(const uint32_t* hist, int nbins, uint32_t need, int64_t* scan_tmp,
-                         int* bin_out, uint32_t* above_out) {
+__device__ __forceinline__ void find_bin(const uint32_t* hist, int nbins, uint32_t need,
+                                         int64_t* scan_tmp, int* bin_out, uint32_t* above_out) {
   // 1 or 2 bins per thread; threads past the bins of a small histogram hold none
   const int t = threadIdx.x, per = nbins > kSelectThreads ? nbins / kSelectThreads : 1;
   const int top = nbins - 1 - t * per;                        // this thread's highest bin
@@ -68,7 +97,21 @@ __device__ void find_bin(const uint32_t* hist, int nbins, uint32_t need, int64_t
   __syncthreads();
 }
 
-}  // namespace
+// find_bin on 64-bit masses: the bin b where the mass strictly above it is below `need`
+// and the mass from b up reaches it (nbins <= kSelectThreads: one bin per thread).
+__device__ __forceinline__ void find_bin64(const uint64_t* hist, int nbins, uint64_t need,
+                                           int64_t* scan_tmp, int* bin_out,
+                                           uint64_t* above_out) {
+  const int t = threadIdx.x, top = nbins - 1 - t;
+  const uint64_t s = top >= 0 ? hist[top] : 0ull;
+  int64_t total;
+  const uint64_t ex = (uint64_t)block_excl_scan_i64((int64_t)s, scan_tmp, &total);
+  if (top >= 0 && ex < need && need <= ex + s) {
+    *bin_out = top;
+    *above_out = ex;
+  }
+  __syncthreads();
+}
 
 // Block-wide min and max of a per-thread value (every thread gets both).
 __device__ __forceinline__ void block_min_max(uint32_t lo, uint32_t hi, uint32_t* tmp,
@@ -89,94 +132,228 @@ __device__ __forceinline__ void block_min_max(uint32_t lo, uint32_t hi, uint32_t
   __syncthreads();
 }
 
-// Segments that fit in LDS.  Thread tid owns the contiguous run [tid * per, tid * per + per)
-// (per odd: the lanes' LDS accesses fall on distinct banks); its pooled order keys stay in
-// registers from the pool to the emit.
-__device__ void select_lds(int L, int k, int hw, const float* __restrict__ in, float* pout,
-                           int32_t* __restrict__ kout, uint32_t* lds, uint32_t* hist,
-                           int64_t* scan_tmp, uint32_t* mm_tmp, int* s_bin, uint32_t* s_above) {
-  constexpr int kRun = kMaxPerThread + 1;   // longest run: odd >= ceil(kSelectLdsKeys / threads)
-  const int tid = threadIdx.x;
-  float* vals = reinterpret_cast<float*>(lds);
-  int32_t* idx = reinterpret_cast<int32_t*>(lds);
-  {
-    // coalesced staging, every load of this thread in flight at once
-    float rv[kMaxPerThread];
-#pragma unroll
-    for (int u = 0; u < kMaxPerThread; ++u) {
-      const int t = tid + u * kSelectThreads;
-      rv[u] = t < L ? in[t] : 0.f;
-    }
-#pragma unroll
-    for (int u = 0; u < kMaxPerThread; ++u) {
-      const int t = tid + u * kSelectThreads;
-      if (t < L) vals[t] = rv[u];
-    }
-  }
-  __syncthreads();
+// ---- building blocks of the LDS-resident selections ---------------------------------
+// Thread tid owns the contiguous run [t0, t0 + n) of the segment, t0 = tid * per with per
+// odd (the lanes' LDS accesses fall on distinct banks).
+struct RunGeom {
+  int t0, n;
+};
 
+__device__ __forceinline__ RunGeom run_geom(int L) {
   const int per = ((L + kSelectThreads - 1) / kSelectThreads) | 1;
-  const int t0 = tid * per < L ? tid * per : L, t1 = t0 + per < L ? t0 + per : L;
-  const int n = t1 - t0;
+  const int t0 = threadIdx.x * per < L ? threadIdx.x * per : L;
+  const int t1 = t0 + per < L ? t0 + per : L;
+  return RunGeom{t0, t1 - t0};
+}
 
-  // ---- pool: max over [t - hw, t + hw] clipped to the segment, from the run and a halo of
-  // 3 on each side held in registers (hw <= 3); a general loop for wider windows
-  uint32_t key[kRun];
-  if (hw <= 3) {
-    // in three chunks of 13 (run + halo of 3 each side in registers)
-    constexpr int kHalo = 3, kChunk = kRun / 3;
-    static_assert(kRun % 3 == 0, "run splits into three chunks");
+// Visit this thread's run in batches: every LDS read of a batch is issued before any of its
+// values is used (one LDS round trip per batch).  f(i, key) receives the run position and
+// the key.  The last batch may read up to kRunBatch - 1 entries past the run (inside the
+// segment or its padding) and ignores them.
+template <typename F>
+__device__ __forceinline__ void visit_run(RunGeom g, const uint32_t* keys, F f) {
+  const uint32_t* run = keys + g.t0;
+  int c = 0;
+#pragma unroll 1
+  for (; c + kRunBatch <= g.n; c += kRunBatch) {
+    uint32_t v[kRunBatch];
 #pragma unroll
-    for (int c = 0; c < kRun; c += kChunk) {
-      float v[kChunk + 2 * kHalo];
+    for (int j = 0; j < kRunBatch; ++j) v[j] = run[c + j];
 #pragma unroll
-      for (int i = 0; i < kChunk + 2 * kHalo; ++i) {
-        const int t = t0 + c - kHalo + i;
-        v[i] = (t >= 0 && t < L && c + i < n + 2 * kHalo) ? vals[t] : -__builtin_inff();
-      }
+    for (int j = 0; j < kRunBatch; ++j) f(c + j, v[j]);
+  }
+  if (c < g.n) {
+    uint32_t v[kRunBatch];
 #pragma unroll
-      for (int i = 0; i < kChunk; ++i) {
-        float m = v[i + kHalo];
+    for (int j = 0; j < kRunBatch; ++j) v[j] = run[c + j];
 #pragma unroll
-        for (int d = 1; d <= kHalo; ++d)
-          if (d <= hw) m = fmaxf(m, fmaxf(v[i + kHalo - d], v[i + kHalo + d]));
-        key[c + i] = order_key(m);
-      }
-    }
-  } else {
+    for (int j = 0; j < kRunBatch; ++j)
+      if (c + j < g.n) f(c + j, v[j]);
+  }
+}
+
+// Coalesced load of a segment of fp32 into LDS: raw buffer loads over exactly L floats (the
+// hardware returns 0 past the end), a batch of rows in flight at once.
+__device__ __forceinline__ void stage_f32(int L, const float* __restrict__ in, uint32_t* vals) {
+  const __amdgpu_buffer_rsrc_t rsrc = buffer_over(in, L * (int)sizeof(float));
+  const int off = lane_byte_offset();
+  const int rows = (L + kSelectThreads - 1) / kSelectThreads;
+#pragma unroll 1
+  for (int r0 = 0; r0 < rows; r0 += kRowBatch) {
+    uint32_t v[kRowBatch];
 #pragma unroll
-    for (int i = 0; i < kRun; ++i) {
-      const int t = t0 + i;
-      float m = -__builtin_inff();
-      if (i < n) {
-        const int lo = t - hw < 0 ? 0 : t - hw, hi = t + hw >= L ? L - 1 : t + hw;
-        for (int x = lo; x <= hi; ++x) m = fmaxf(m, vals[x]);
-      }
-      key[i] = order_key(m);
+    for (int j = 0; j < kRowBatch; ++j)
+      v[j] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, off + (r0 + j) * kSelectThreads * 4, 0,
+                                                  0);
+#pragma unroll
+    for (int j = 0; j < kRowBatch; ++j) {
+      const int t = threadIdx.x + (r0 + j) * kSelectThreads;
+      if (t < L) vals[t] = v[j];
     }
   }
-  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+}
+
+// dst[t] = xf(src[t]) for t < n, from LDS to global memory, coalesced, through raw buffer
+// stores over exactly n words (the hardware drops stores at or past the end).
+// n <= kSelectLdsKeys.
+template <typename Xf>
+__device__ __forceinline__ void copy_out_u32(int n, const uint32_t* src, void* dst, Xf xf) {
+  const __amdgpu_buffer_rsrc_t rsrc = buffer_over(dst, n * (int)sizeof(uint32_t));
+  const int off = lane_byte_offset(), last = n > 0 ? n - 1 : 0;
+  const int rows = (n + kSelectThreads - 1) / kSelectThreads;
+#pragma unroll 1
+  for (int r0 = 0; r0 < rows; r0 += kRowBatch) {
+    uint32_t v[kRowBatch];
 #pragma unroll
-  for (int i = 0; i < kRun; ++i)
-    if (i < n) { kmin = min(kmin, key[i]); kmax = max(kmax, key[i]); }
-  __syncthreads();   // every read of the raw scores is done
-  // pooled scores out through LDS, coalesced (the key maps back to the value; -0 reads +0)
+    for (int j = 0; j < kRowBatch; ++j) {
+      const int t = threadIdx.x + (r0 + j) * kSelectThreads;
+      v[j] = src[t < last ? t : last];
+    }
 #pragma unroll
-  for (int i = 0; i < kRun; ++i)
-    if (i < n) vals[t0 + i] = key_value(key[i]);
+    for (int j = 0; j < kRowBatch; ++j)
+      if (r0 + j < rows)   // uniform
+        __builtin_amdgcn_raw_buffer_store_b32(xf(v[j]), rsrc,
+                                              off + (r0 + j) * kSelectThreads * 4, 0, 0);
+  }
+}
+
+struct AsIs {
+  __device__ uint32_t operator()(uint32_t x) const { return x; }
+};
+struct KeyToFloatBits {   // the float an order key stands for
+  __device__ uint32_t operator()(uint32_t k) const {
+    return (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+  }
+};
+
+// dst[j] = src[idx[j]] for j < n: indices from LDS, values gathered from global memory,
+// written out coalesced.  Every idx[j] < the length of src.
+__device__ __forceinline__ void gather_out_f32(int n, const int32_t* idx, const float* src,
+                                               float* dst) {
+  const __amdgpu_buffer_rsrc_t rsrc = buffer_over(dst, n * (int)sizeof(float));
+  const int off = lane_byte_offset(), last = n > 0 ? n - 1 : 0;
+  const int rows = (n + kSelectThreads - 1) / kSelectThreads;
+#pragma unroll 1
+  for (int r0 = 0; r0 < rows; r0 += kRowBatch) {
+    float v[kRowBatch];
+#pragma unroll
+    for (int j = 0; j < kRowBatch; ++j) {
+      const int t = threadIdx.x + (r0 + j) * kSelectThreads;
+      v[j] = r0 + j < rows ? src[idx[t < last ? t : last]] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < kRowBatch; ++j)
+      if (r0 + j < rows)   // uniform
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v[j]), rsrc,
+                                              off + (r0 + j) * kSelectThreads * 4, 0, 0);
+  }
+}
+
+// Max-pool in place for windows up to 2 * kPoolHalo + 1: each thread first reads the raw
+// scores just outside its run (the halo), then, once every thread has done so, slides a
+// window of registers along its own run, overwriting each entry with the order key of its
+// pooled score (the raw scores ahead of the window are still in LDS, those behind it in
+// registers).
+__device__ __forceinline__ void pool_narrow_in_place(int L, int hw, RunGeom g, uint32_t* vals) {
+  const float ninf = -__builtin_inff();
+  const int t1 = g.t0 + g.n;
+  auto raw = [&](int p) { return __uint_as_float(vals[p]); };
+  float halo_l[kPoolHalo], halo_r[kPoolHalo];
+#pragma unroll
+  for (int j = 0; j < kPoolHalo; ++j) {
+    const int pl = g.t0 - kPoolHalo + j, pr = t1 + j;   // pr <= L + 2: inside the padding
+    const float vl = raw(pl < 0 ? 0 : pl), vr = raw(pr);
+    halo_l[j] = (pl >= 0 && g.n > 0) ? vl : ninf;
+    halo_r[j] = (pr < L && g.n > 0) ? vr : ninf;
+  }
+  __syncthreads();   // no thread overwrites an entry before its neighbours read their halo
+  // raw score at p >= t0 that the window has not reached yet
+  auto ahead = [&](float lds_value, int p) {
+    const int d = p - t1;
+    return d < 0 ? lds_value
+                 : (d == 0 ? halo_r[0] : (d == 1 ? halo_r[1] : (d == 2 ? halo_r[2] : ninf)));
+  };
+  // win[x] = raw score at t - kPoolHalo + x for the entry t produced next; every LDS read
+  // below is at most t1 + 2 * kPoolHalo + kRunBatch - 3 < L + kLdsPad
+  float win[2 * kPoolHalo + 1];
+#pragma unroll
+  for (int x = 0; x < kPoolHalo; ++x) win[x] = halo_l[x];
+#pragma unroll
+  for (int x = 0; x <= kPoolHalo; ++x) win[kPoolHalo + x] = ahead(raw(g.t0 + x), g.t0 + x);
+#pragma unroll 1
+  for (int c = 0; c < g.n; c += kRunBatch) {
+    float nxt[kRunBatch];   // raw scores at t0 + c + kPoolHalo + 1 + j
+#pragma unroll
+    for (int j = 0; j < kRunBatch; ++j) nxt[j] = raw(g.t0 + c + kPoolHalo + 1 + j);
+#pragma unroll
+    for (int j = 0; j < kRunBatch; ++j) nxt[j] = ahead(nxt[j], g.t0 + c + kPoolHalo + 1 + j);
+#pragma unroll
+    for (int j = 0; j < kRunBatch; ++j) {
+      float m = win[kPoolHalo];
+#pragma unroll
+      for (int d = 1; d <= kPoolHalo; ++d)
+        if (d <= hw) m = fmaxf(m, fmaxf(win[kPoolHalo - d], win[kPoolHalo + d]));
+      if (c + j < g.n) vals[g.t0 + c + j] = order_key(m);
+#pragma unroll
+      for (int x = 0; x < 2 * kPoolHalo; ++x) win[x] = win[x + 1];
+      win[2 * kPoolHalo] = nxt[j];
+    }
+  }
+}
+
+// Wider windows: every thread pools its run into registers from the raw scores, then all
+// write back once every read is done (a straight loop per entry; uncommon).
+__device__ __forceinline__ void pool_wide_in_place(int L, int hw, RunGeom g, uint32_t* vals) {
+  constexpr int kRun = kRows + 1;   // longest run: odd >= ceil(kSelectLdsKeys / threads)
+  float m[kRun];
+#pragma unroll
+  for (int i = 0; i < kRun; ++i) {
+    const int t = g.t0 + i;
+    float x = -__builtin_inff();
+    if (i < g.n) {
+      const int lo = t - hw < 0 ? 0 : t - hw, hi = t + hw >= L ? L - 1 : t + hw;
+      for (int y = lo; y <= hi; ++y) x = fmaxf(x, __uint_as_float(vals[y]));
+    }
+    m[i] = x;
+  }
   __syncthreads();
-  for (int t = tid; t < L; t += kSelectThreads) pout[t] = vals[t];
-  if (k <= 0) return;
-  if (k >= L) {
-    for (int t = tid; t < L; t += kSelectThreads) kout[t] = t;
-    return;
-  }
+#pragma unroll
+  for (int i = 0; i < kRun; ++i)
+    if (i < g.n) vals[g.t0 + i] = order_key(m[i]);
+}
 
-  // ---- radix select on d = key - min key, over the bit width of the segment's key range
-  // (digits of up to 11 bits, most significant first): concentrated scores still spread
-  // over the whole first histogram.
-  uint32_t lo, hi;
-  block_min_max(kmin, kmax, mm_tmp, &lo, &hi);
+// Pool the staged raw scores in place (LDS then holds their order keys); the pooled scores
+// are also copied to `out` when given.
+__device__ __forceinline__ void pool_in_lds(int L, int hw, RunGeom g, uint32_t* vals,
+                                            float* out) {
+  if (hw <= kPoolHalo)
+    pool_narrow_in_place(L, hw, g, vals);
+  else
+    pool_wide_in_place(L, hw, g, vals);
+  __syncthreads();
+  if (out) copy_out_u32(L, vals, out, KeyToFloatBits());
+}
+
+// Smallest and largest order key of the segment in LDS (every thread gets both).
+__device__ __forceinline__ void seg_key_range(RunGeom g, const uint32_t* keys,
+                                              uint32_t* mm_tmp, uint32_t* lo, uint32_t* hi) {
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+  visit_run(g, keys, [&](int, uint32_t kk) {
+    kmin = min(kmin, kk);
+    kmax = max(kmax, kk);
+  });
+  block_min_max(kmin, kmax, mm_tmp, lo, hi);
+}
+
+// Radix select over the segment in LDS, keys in [lo, hi]: tau, the order key of the k-th
+// largest (0 < k < L), and `need`, how many keys equal to tau are taken.  Digits of up to
+// 11 bits over d = key - lo, within the bit width of the key range, so concentrated values
+// still spread over the whole first histogram.
+__device__ __forceinline__ void radix_tau(RunGeom g, const uint32_t* keys, int k,
+                                          uint32_t lo, uint32_t hi, uint32_t* hist,
+                                          int64_t* scan_tmp, int* s_bin, uint32_t* s_above,
+                                          uint32_t* tau_out, uint32_t* need_out) {
+  const int tid = threadIdx.x;
   const uint32_t range = hi - lo;
   int rem = range == 0 ? 0 : 32 - __clz(range);
   uint32_t need = (uint32_t)k, prefix = 0;
@@ -185,53 +362,93 @@ __device__ void select_lds(int L, int k, int hw, const float* __restrict__ in, f
     const int bits = rem < 11 ? rem : 11, sh = rem - bits, nbins = 1 << bits;
     for (int bb = tid; bb < nbins; bb += kSelectThreads) hist[bb] = 0;
     __syncthreads();
-#pragma unroll
-    for (int i = 0; i < kRun; ++i) {
-      const uint32_t d = key[i] - lo;
+    visit_run(g, keys, [&](int, uint32_t kk) {
+      const uint32_t dh = (kk - lo) >> sh;   // this digit and the ones above it
       // keys whose higher digits match the prefix found so far (none above the range)
-      if (i < n && (uint32_t)(((uint64_t)d) >> (sh + bits)) == prefix)
-        atomicAdd(&hist[(d >> sh) & (uint32_t)(nbins - 1)], 1u);
-    }
+      if ((dh >> bits) == prefix) atomicAdd(&hist[dh & (uint32_t)(nbins - 1)], 1u);
+    });
     __syncthreads();
     find_bin(hist, nbins, need, scan_tmp, s_bin, s_above);
     need -= *s_above;
     prefix = (prefix << bits) | (uint32_t)*s_bin;
     rem = sh;
   }
-  const uint32_t tau = lo + prefix;   // order key of the k-th largest pooled score
+  *tau_out = lo + prefix;
+  *need_out = need;
+}
 
-  // ---- emit: all keys > tau, then the first `need` keys == tau, in index order, staged in
-  // LDS (positions from two workgroup prefix sums) and written out coalesced
-  uint32_t n_gt = 0, n_eq = 0;
-#pragma unroll
-  for (int i = 0; i < kRun; ++i) {
-    n_gt += i < n && key[i] > tau;
-    n_eq += i < n && key[i] == tau;
-  }
+// Kept entries: every key > tau, then the first `need` keys == tau, in index order.  The
+// run's greater / equal flags are kept as bit masks; one workgroup prefix sum of both counts
+// places each thread's kept indices, which are staged in LDS (over vals) and written out
+// coalesced.  When vout is given, vout[j] = vsrc[kept[j]] (vsrc in global memory).
+__device__ __forceinline__ void emit_kept(RunGeom g, uint32_t* keys, uint32_t tau,
+                                          uint32_t need, int k, int64_t* scan_tmp,
+                                          int32_t* __restrict__ kout, const float* vsrc,
+                                          float* __restrict__ vout) {
+  uint64_t gtm = 0, eqm = 0;
+  visit_run(g, keys, [&](int i, uint32_t kk) {
+    gtm |= (uint64_t)(kk > tau) << i;
+    eqm |= (uint64_t)(kk == tau) << i;
+  });
+  const int64_t n_gt = __popcll(gtm), n_eq = __popcll(eqm);
+  // the tied entries are taken in thread order, so the threads before this one took
+  // min(need, eq_before) of them (each count sum < 2^32).  The scan's barriers also retire
+  // every thread's reads of vals above.
   int64_t tot;
-  const int64_t eq_before = block_excl_scan_i64(n_eq, scan_tmp, &tot);
+  const int64_t ex = block_excl_scan_i64((n_eq << 32) | n_gt, scan_tmp, &tot);
+  const int64_t eq_before = ex >> 32, gt_before = ex & 0xFFFFFFFFll;
   int64_t eq_take = (int64_t)need - eq_before;
   eq_take = eq_take < 0 ? 0 : (eq_take > n_eq ? n_eq : eq_take);
-  const int64_t at0 = block_excl_scan_i64(n_gt + eq_take, scan_tmp, &tot);
-  // branch-free positions (predicated stores, no pointer updates under divergent control)
-  int pos = 0, taken = 0;
-#pragma unroll
-  for (int i = 0; i < kRun; ++i) {
-    const bool gt = i < n && key[i] > tau;
-    const bool eq = i < n && key[i] == tau && taken < eq_take;
-    taken += eq ? 1 : 0;
-    if (gt || eq) idx[at0 + pos] = t0 + i;
-    pos += (gt || eq) ? 1 : 0;
+  for (int64_t drop = n_eq - eq_take; drop > 0; --drop)   // keep the first eq_take ties
+    eqm &= ~(1ull << (63 - __clzll(eqm)));
+  uint64_t keep = gtm | eqm;
+  int32_t* idx = reinterpret_cast<int32_t*>(keys);
+  int pos = (int)(gt_before + (eq_before < (int64_t)need ? eq_before : (int64_t)need));
+  while (keep) {
+    idx[pos++] = g.t0 + __builtin_ctzll(keep);
+    keep &= keep - 1;
   }
   __syncthreads();
-  for (int j = tid; j < k; j += kSelectThreads) kout[j] = idx[j];
+  copy_out_u32(k, reinterpret_cast<const uint32_t*>(idx), kout, AsIs());
+  if (vout) gather_out_f32(k, idx, vsrc, vout);
+}
+
+// TopK of the segment in LDS (0 <= k): indices to kout and, when vout is given, the kept
+// values (vsrc holds the values the keys stand for, in global memory).
+__device__ __forceinline__ void topk_lds(int L, int k, RunGeom g, uint32_t* keys, uint32_t* hist,
+                                         int64_t* scan_tmp, uint32_t* mm_tmp, int* s_bin,
+                                         uint32_t* s_above, int32_t* __restrict__ kout,
+                                         const float* vsrc, float* __restrict__ vout) {
+  if (k <= 0) return;
+  if (k >= L) {
+    for (int t = threadIdx.x; t < L; t += kSelectThreads) kout[t] = t;
+    if (vout) copy_out_u32(L, keys, vout, KeyToFloatBits());
+    return;
+  }
+  uint32_t lo, hi, tau, need;
+  seg_key_range(g, keys, mm_tmp, &lo, &hi);
+  radix_tau(g, keys, k, lo, hi, hist, scan_tmp, s_bin, s_above, &tau, &need);
+  emit_kept(g, keys, tau, need, k, scan_tmp, kout, vsrc, vout);
+}
+
+// Segments that fit in LDS: stage, pool, pooled scores out, radix select, emit.
+__device__ __forceinline__ void select_lds(int L, int k, int hw, const float* __restrict__ in,
+                                           float* pout, int32_t* __restrict__ kout, uint32_t* vals,
+                                           uint32_t* hist, int64_t* scan_tmp, uint32_t* mm_tmp,
+                                           int* s_bin, uint32_t* s_above) {
+  stage_f32(L, in, vals);
+  __syncthreads();
+  const RunGeom g = run_geom(L);
+  pool_in_lds(L, hw, g, vals, pout);
+  topk_lds(L, k, g, vals, hist, scan_tmp, mm_tmp, s_bin, s_above, kout, nullptr, nullptr);
 }
 
 // Segments longer than the LDS capacity: the same steps on the pooled scores in global
 // memory.
-__device__ void select_global(int L, int k, int hw, const float* __restrict__ in, float* pout,
-                              int32_t* __restrict__ kout, uint32_t* hist, int64_t* scan_tmp,
-                              int* s_bin, uint32_t* s_above) {
+__device__ __forceinline__ void select_global(int L, int k, int hw, const float* __restrict__ in,
+                                              float* pout, int32_t* __restrict__ kout,
+                                              uint32_t* hist, int64_t* scan_tmp, int* s_bin,
+                                              uint32_t* s_above) {
   const int tid = threadIdx.x;
   for (int t = tid; t < L; t += kSelectThreads) {
     const int lo = t - hw < 0 ? 0 : t - hw, hi = t + hw >= L ? L - 1 : t + hw;
@@ -287,6 +504,8 @@ __device__ void select_global(int L, int k, int hw, const float* __restrict__ in
   }
 }
 
+}  // namespace
+
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp,
                                                                 const float* __restrict__ scores,
                                                                 float* pooled,
@@ -313,11 +532,212 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp,
     select_global(L, k, hw, in, pout, kout, hist, scan_tmp, &s_bin, &s_above);
 }
 
+// ---- attention-aware LRFU keep scores (Sec. 5.1; Alg. 1 steps 2-5) -----------------------
+//
+// Hit mask (Alg. 1 step 3): the shortest prefix of the segment ordered by pooled score
+// descending (ties: lower index first) whose running mass reaches top_p times the total.
+// Masses are exact 64-bit fixed-point values (each score scaled by 2^S and truncated, S
+// chosen so that the segment's total cannot overflow), so every sum is exact and
+// order-independent: the same radix search as the selection, with mass histograms in place
+// of counts, finds the boundary key tau and the mass still needed from entries equal to tau;
+// those are then taken in index order.  Entries with a score <= 0 carry no mass.  A hit
+// entry always has a positive score, so the hit decision is carried from here on by the
+// contribution hit ? score : 0 that replaces the pooled score in LDS.
+namespace {
+
+// floor(v * 2^S) for the positive float whose order key is `key` (0 for v <= 0), by integer
+// shifts of the significand: exact, as long as the result stays below 2^64.
+__device__ __forceinline__ uint64_t fixed_mass(uint32_t key, int S) {
+  if (key <= 0x80000000u) return 0ull;   // negative or zero
+  const uint32_t u = key & 0x7FFFFFFFu, ex = u >> 23;
+  const uint64_t sig = (u & 0x7FFFFFu) | (ex ? 0x800000u : 0u);
+  const int sh = (ex ? (int)ex : 1) - 150 + S;   // v = sig * 2^((ex ? ex : 1) - 150)
+  return sh >= 0 ? sig << sh : (sh > -64 ? sig >> -sh : 0ull);
+}
+
+// Replace the key of each pooled score of this thread's run by the key of its contribution:
+// the score where keep(key) holds, else 0 (keep sees the run in index order).
+template <typename Keep>
+__device__ __forceinline__ void keep_contributions(RunGeom g, uint32_t* keys, Keep keep) {
+  constexpr uint32_t kZero = 0x80000000u;   // order_key(0.0f)
+  visit_run(g, keys, [&](int i, uint32_t kk) { keys[g.t0 + i] = keep(kk) ? kk : kZero; });
+}
+
+__device__ __forceinline__ void topp_contributions(int L, RunGeom g, uint32_t* keys, float top_p,
+                                                   uint64_t* hist64, int64_t* scan_tmp,
+                                                   uint32_t* mm_tmp, int* s_bin,
+                                                   uint64_t* s_above) {
+  const int tid = threadIdx.x;
+  uint32_t lo, hi;
+  seg_key_range(g, keys, mm_tmp, &lo, &hi);   // its barriers retire the pooled copy-out
+  const float vmax = key_value(hi);
+  if (!(vmax > 0.f) || !(top_p > 0.f)) {   // no positive mass to reach
+    keep_contributions(g, keys, [](uint32_t) { return false; });
+    return;
+  }
+  if (top_p >= 1.f) {   // the whole mass: every entry with a positive score
+    keep_contributions(g, keys, [](uint32_t kk) { return kk > 0x80000000u; });
+    return;
+  }
+  int e;
+  frexpf(vmax, &e);   // every score < 2^e
+  const int lg = 32 - __clz((uint32_t)L + 1u);   // L + 1 <= 2^lg
+  const int S = 62 - e - lg;                     // total < L * 2^(e + S) < 2^62
+  uint64_t mine = 0;
+  visit_run(g, keys, [&](int, uint32_t kk) { mine += fixed_mass(kk, S); });
+  int64_t total;
+  block_excl_scan_i64((int64_t)mine, scan_tmp, &total);
+  const double want = ceil((double)top_p * (double)total);
+  uint64_t need = want > 0.0 ? (uint64_t)want : 0ull;
+  if (need == 0) {
+    keep_contributions(g, keys, [](uint32_t) { return false; });
+    return;
+  }
+  // radix search over d = key - lo with 10-bit digits, masses as weights
+  const uint32_t range = hi - lo;
+  int rem = range == 0 ? 0 : 32 - __clz(range);
+  uint32_t prefix = 0;
+#pragma unroll 1
+  while (rem > 0) {
+    const int bits = rem < 10 ? rem : 10, sh = rem - bits, nbins = 1 << bits;
+    for (int bb = tid; bb < nbins; bb += kSelectThreads) hist64[bb] = 0;
+    if (tid == 0) { *s_bin = 0; *s_above = 0; }
+    __syncthreads();
+    visit_run(g, keys, [&](int, uint32_t kk) {
+      const uint32_t dh = (kk - lo) >> sh;
+      if ((dh >> bits) == prefix) {
+        const uint64_t m = fixed_mass(kk, S);
+        if (m != 0)
+          atomicAdd((unsigned long long*)&hist64[dh & (uint32_t)(nbins - 1)],
+                    (unsigned long long)m);
+      }
+    });
+    __syncthreads();
+    find_bin64(hist64, nbins, need, scan_tmp, s_bin, s_above);
+    need -= *s_above;
+    prefix = (prefix << bits) | (uint32_t)*s_bin;
+    rem = sh;
+    __syncthreads();
+  }
+  const uint32_t tau = lo + prefix;
+  // entries equal to tau (each of mass m > 0: the search only descends into bins with
+  // mass) are hit, in index order, while the mass before them is still short of the
+  // target: the first ceil(need / m) of them
+  const uint64_t m_tau = fixed_mass(tau, S);
+  uint32_t n_eq = 0;
+  visit_run(g, keys, [&](int, uint32_t kk) { n_eq += kk == tau; });
+  int64_t eq_total;
+  const int64_t eq_before = block_excl_scan_i64(n_eq, scan_tmp, &eq_total);
+  const int64_t take = m_tau == 0 ? eq_total : (int64_t)((need + m_tau - 1) / m_tau);
+  int64_t rank = eq_before;
+  keep_contributions(g, keys, [&](uint32_t kk) {
+    const bool eq = kk == tau;
+    const bool h = kk > tau || (eq && rank < take);
+    rank += eq ? 1 : 0;
+    return h;
+  });
+}
+
+// KS' = decay * KS + contribution, each operation rounded to fp32, over the whole segment
+// in coalesced order; KS' goes to ks (in place) and its key replaces the contribution in LDS, the
+// hit mask (contribution > 0) to hit_out when given.  Global reads and writes are raw
+// buffer accesses over exactly L elements (out-of-range lanes read 0 / are dropped).
+__device__ __forceinline__ void keep_score_update(int L, float decay, float* ks,
+                                                  uint8_t* hit_out, uint32_t* keys) {
+  const __amdgpu_buffer_rsrc_t rk = buffer_over(ks, L * (int)sizeof(float));
+  const __amdgpu_buffer_rsrc_t rh = buffer_over(hit_out, hit_out ? L : 0);
+  const int off = lane_byte_offset(), last = L > 0 ? L - 1 : 0;
+  const int rows = (L + kSelectThreads - 1) / kSelectThreads;
+#pragma unroll 1
+  for (int r0 = 0; r0 < rows; r0 += kRowBatch) {
+    float kv[kRowBatch], cv[kRowBatch];
+#pragma unroll
+    for (int j = 0; j < kRowBatch; ++j) {
+      const int t = threadIdx.x + (r0 + j) * kSelectThreads;
+      kv[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                            rk, off + (r0 + j) * kSelectThreads * 4, 0, 0));
+      cv[j] = key_value(keys[t < last ? t : last]);
+    }
+#pragma unroll
+    for (int j = 0; j < kRowBatch; ++j) {
+      const int t = threadIdx.x + (r0 + j) * kSelectThreads;
+      const float nk = __fadd_rn(__fmul_rn(decay, kv[j]), cv[j]);
+      if (t < L) keys[t] = order_key(nk);
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, nk), rk,
+                                            off + (r0 + j) * kSelectThreads * 4, 0, 0);
+      if (hit_out)
+        __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(cv[j] > 0.0f ? 1 : 0), rh,
+                                             (int)threadIdx.x + (r0 + j) * kSelectThreads, 0, 0);
+    }
+  }
+}
+
+// One (request, KV head): pool, top-p hit mask, keep-score update, TopK on the keep
+// scores with the kept keep scores.
+__device__ __forceinline__ void lrfu_lds(int L, int k, int hw, float top_p, float decay,
+                                         const float* __restrict__ in, float* pout, float* ks,
+                                         uint8_t* hit_out, int32_t* __restrict__ kout,
+                                         float* __restrict__ ks_kept, uint32_t* vals,
+                                         uint64_t* hist64, int64_t* scan_tmp, uint32_t* mm_tmp,
+                                         int* s_bin, uint32_t* s_above32, uint64_t* s_above64) {
+  stage_f32(L, in, vals);
+  __syncthreads();
+  const RunGeom g = run_geom(L);
+  pool_in_lds(L, hw, g, vals, pout);
+  topp_contributions(L, g, vals, top_p, hist64, scan_tmp, mm_tmp, s_bin, s_above64);
+  __syncthreads();
+  keep_score_update(L, decay, ks, hit_out, vals);
+  __syncthreads();   // also makes this workgroup's writes of ks visible to its own reads
+  topk_lds(L, k, g, vals, reinterpret_cast<uint32_t*>(hist64), scan_tmp, mm_tmp, s_bin,
+           s_above32, kout, ks, ks_kept);
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(kSelectThreads) void lrfu_select_kernel(
+    DevProblem dp, const float* __restrict__ scores, float top_p, float decay, float* ks,
+    uint8_t* hit, float* pooled, int32_t* __restrict__ kept, float* ks_kept) {
+  extern __shared__ uint32_t lds_keys[];
+  __shared__ uint64_t hist64[kMaxBins / 2];   // 8 KiB: 64-bit masses, or the 32-bit counts
+  __shared__ int64_t scan_tmp[17];
+  __shared__ uint32_t mm_tmp[32];
+  __shared__ int s_bin;
+  __shared__ uint32_t s_above32;
+  __shared__ uint64_t s_above64;
+
+  const int h = blockIdx.x, r = blockIdx.y, Hkv = dp.Hkv;
+  const ReqPlan pl = dp.plan[r];
+  const int L = pl.L;
+  const int b = dp.budgets[r * Hkv + h];
+  const int k = b < L ? b : L;
+  const int64_t seg = pl.seg_off + (int64_t)h * L;
+  const int64_t koff = dp.kept_off[r * Hkv + h];
+  lrfu_lds(L, k, dp.pool_window / 2, top_p, decay, scores + seg,
+           pooled ? pooled + seg : nullptr, ks + seg, hit ? hit + seg : nullptr, kept + koff,
+           ks_kept + koff, lds_keys, hist64, scan_tmp, mm_tmp, &s_bin, &s_above32, &s_above64);
+}
+
+hipError_t launch_lrfu_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
+                              float top_p, float decay, float* ks, uint8_t* hit, float* pooled,
+                              int32_t* kept, float* ks_kept, hipStream_t s) {
+  if (hp.R == 0) return hipSuccess;
+  const int64_t keys = hp.max_L < kSelectLdsKeys ? hp.max_L : kSelectLdsKeys;
+  const size_t lds = (size_t)(keys + kLdsPad) * sizeof(uint32_t);
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void*)lrfu_select_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(lrfu_select_kernel, dim3(hp.Hkv, hp.R), dim3(kSelectThreads), lds, s, dp,
+                     scores, top_p, decay, ks, hit, pooled, kept, ks_kept);
+  return hipGetLastError();
+}
+
 hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
                          float* pooled, int32_t* kept, hipStream_t s) {
   if (hp.R == 0) return hipSuccess;
   const int64_t keys = hp.max_L < kSelectLdsKeys ? hp.max_L : kSelectLdsKeys;
-  const size_t lds = (size_t)(keys > 0 ? keys : 1) * sizeof(uint32_t);
+  const size_t lds = (size_t)(keys + kLdsPad) * sizeof(uint32_t);
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)select_kernel,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -140,3 +140,42 @@ def test_compact_and_select_validate_before_launching():
     assert lib.actkv_select(ctypes.byref(c), FAKE, FAKE, None, FAKE, ws, None) == -1
     assert lib.actkv_score(ctypes.byref(c), FAKE, FAKE, FAKE, None, FAKE, FAKE, 16, None) == -3
     assert lib.actkv_lse(None, FAKE, FAKE, FAKE, FAKE, FAKE, ws, None) == -1
+
+
+def test_lrfu_entry_points_validate_before_launching():
+    lib = actkv.load_library()
+    p = _tiny()
+    c = p.cstruct()
+    c.seq_lens_d = c.q_lens_d = c.budgets_d = FAKE
+    ws = actkv.query(p)["workspace_bytes"]
+    ok = dict(top_p=0.9, decay=0.5)
+
+    def sel(top_p, decay, ks=FAKE + 64, ks_kept=FAKE):
+        return lib.actkv_lrfu_select(ctypes.byref(c), FAKE, top_p, decay, ks, None, None, FAKE,
+                                     ks_kept, FAKE, ws, None)
+
+    assert sel(1.5, ok["decay"]) == -1
+    assert sel(-0.1, ok["decay"]) == -1
+    assert sel(float("nan"), ok["decay"]) == -1
+    assert sel(ok["top_p"], 1.01) == -1
+    assert sel(ok["top_p"], ok["decay"], ks=None) == -1
+    assert sel(ok["top_p"], ok["decay"], ks_kept=None) == -1
+    # a keep-score array may not alias the scores it is updated from
+    assert lib.actkv_lrfu_select(ctypes.byref(c), FAKE, 0.9, 0.5, FAKE, None, None, FAKE,
+                                 FAKE, FAKE, ws, None) == -1
+    # the step checks its pages before anything else runs
+    assert lib.actkv_step_lrfu(ctypes.byref(c), FAKE, FAKE, FAKE, None, FAKE, 0, 0.9, 0.5,
+                               FAKE, FAKE, None, None, None, None, FAKE, FAKE, FAKE, ws,
+                               None) == -4
+
+
+def test_lrfu_rejects_segments_past_its_length_limit():
+    lib = actkv.load_library()
+    pb = W.make_custom(seq_lens=[38401], q_lens=[1], num_q_heads=1, num_kv_heads=1,
+                       head_dim=64, budgets=[10])
+    p = binding_problem(pb)
+    c = p.cstruct()
+    c.seq_lens_d = c.q_lens_d = c.budgets_d = FAKE
+    ws = actkv.query(p)["workspace_bytes"]
+    assert lib.actkv_lrfu_select(ctypes.byref(c), FAKE, 0.9, 0.5, FAKE + 64, None, None, FAKE,
+                                 FAKE, FAKE, ws, None) == -2
