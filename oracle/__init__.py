@@ -67,6 +67,8 @@ def _load():
         lib.actkv_oracle_totals.argtypes = [P, ctypes.POINTER(i64), ctypes.POINTER(i64),
                                             ctypes.POINTER(i64)]
         lib.actkv_oracle_compact.argtypes = [P, vp, vp, vp, vp, i64, vp, vp]
+        lib.actkv_oracle_compact_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp,
+                                                     ctypes.POINTER(i64)]
         lib.actkv_oracle_hits.argtypes = [P, vp, ctypes.c_double, vp]
         lib.actkv_oracle_lrfu_update.argtypes = [P, vp, vp, ctypes.c_float, vp]
         for f in ("actkv_oracle_lse", "actkv_oracle_scores", "actkv_oracle_pool",
@@ -208,6 +210,55 @@ def step(pb, lse_in: Optional[np.ndarray] = None, agg: str = "sum", **kw) -> dic
     kv2, bt2, freed, new_lens = compact(pb, kept, **kw)
     return dict(raw=raw, pooled=pooled, kept=kept, kv=kv2, block_table=bt2, freed=freed,
                 new_lens=new_lens)
+
+
+def inplace_pages_freed(pb, **kw) -> int:
+    """Pages the in-place compaction returns: Y - X per compacted request (Alg. 4)."""
+    b = _Bound(pb, **kw)
+    H, BS = pb.num_kv_heads, pb.page_size
+    total = 0
+    for r, L in enumerate(np.asarray(pb.seq_lens, np.int64)):
+        bud = b.bud[r * H:(r + 1) * H].astype(np.int64)
+        if (bud >= L).all():
+            continue
+        kmax = int(np.minimum(bud, L).max())
+        total += -(-int(L) // BS) - (-(-kmax // BS))
+    return total
+
+
+def compact_inplace(pb, kept: np.ndarray, kv: Optional[np.ndarray] = None,
+                    block_table: Optional[np.ndarray] = None, **kw) -> dict:
+    """In-place compaction (Alg. 4) on copies of the inputs.
+
+    Returns kv', block_table', freed pages, new_lens, new_order (the original token of
+    every new slot, laid out like kept) and the number of row copies."""
+    b = _Bound(pb, **kw)
+    kv2 = np.array(pb.kv if kv is None else kv, dtype=np.uint16, copy=True, order="C")
+    bt2 = np.array(pb.block_table if block_table is None else block_table, dtype=np.int32,
+                   copy=True, order="C")
+    kept = np.ascontiguousarray(kept, dtype=np.int32)
+    nfreed = inplace_pages_freed(pb, **kw)
+    freed = np.zeros(max(nfreed, 1), dtype=np.int32)
+    new_lens = np.zeros(b.bud.shape[0], dtype=np.int32)
+    new_order = np.zeros(max(kept.shape[0], 1), dtype=np.int32)
+    pairs = ctypes.c_int64(0)
+    rc = _load().actkv_oracle_compact_inplace(b.ref, kv2.ctypes.data, bt2.ctypes.data,
+                                              kept.ctypes.data if kept.size else None,
+                                              freed.ctypes.data, new_lens.ctypes.data,
+                                              new_order.ctypes.data, ctypes.byref(pairs))
+    _check(rc, "compact_inplace")
+    return dict(kv=kv2, block_table=bt2, freed=freed[:nfreed], new_lens=new_lens,
+                new_order=new_order[:kept.shape[0]], pairs=int(pairs.value))
+
+
+def step_inplace(pb, lse_in: Optional[np.ndarray] = None, agg: str = "sum", **kw) -> dict:
+    """The compression step with the in-place compaction of Alg. 4."""
+    raw = scores(pb, lse_in=lse_in, agg=agg, **kw)
+    pooled = pool(pb, raw, **kw)
+    kept = select(pb, pooled, **kw)
+    out = compact_inplace(pb, kept, **kw)
+    out.update(raw=raw, pooled=pooled, kept=kept)
+    return out
 
 
 def hits(pb, att: np.ndarray, top_p: float, **kw) -> np.ndarray:

@@ -23,8 +23,9 @@
  *               runs on the keep scores.
  *   compact  -- the survivors' K/V rows are written, in ascending token order, into fresh
  *               pages taken from a free list; the block table row is rewritten and the old
- *               pages are returned (the freed-block return of Sec. 7.2; the paper's own
- *               compaction is in place, Alg. 4 -- this oracle follows the fresh-page form).
+ *               pages are returned (the freed-block return of Sec. 7.2);
+ *   compact_inplace -- the paper's own in-place compaction (Alg. 4): survivors outside the
+ *               last blocks are paired with the evicted slots inside them and copied there.
  *
  * Every floating-point quantity is carried in double (fp64).  The raw per-entry score is
  * rounded once to float at the end; pooling and selection then act on those float values,
@@ -362,6 +363,108 @@ int actkv_oracle_compact(const oracle_problem* p, uint16_t* kv, int32_t* bt,
     fresh_off += X;
     freed_off += Y;
   }
+  return 0;
+}
+
+/*
+ * In-place compaction (Alg. 4 steps 1-6; the slot planning of Sec. 7.2).  Requests in order;
+ * a request whose every head keeps all its entries is skipped, as above.  Each KV head has
+ * its own keep set (k_h = min(budget, L) entries, `kept` ascending); the tail region is
+ * shared by the heads because a page holds every head's row of a slot, so X follows the
+ * largest k_h:
+ *   Step 1  Y = ceil(L / BS), X = ceil(max_h k_h / BS), Start = (Y - X) * BS,
+ *           End = Start + k_h;
+ *   Step 2  DstMask = not KeepMask[Start:End].  KeepMask covers the Y * BS logical slots of
+ *           the request; slots at or past L hold no entry, so they are destinations too
+ *           (they exist in the last block, and without them #dst < #src whenever End > L);
+ *   Step 3  KeepMask[Start:End] = False; SrcMask = KeepMask (kept entries outside the
+ *           region);
+ *   Step 4  logical slots -> physical slots through the request's block-table row;
+ *   Step 5  CopyPairs = Zip(SrcSlots, DstSlots), both in ascending logical order;
+ *   Step 6  the K and V rows of head h are copied for every pair.  Sources are kept and
+ *           destinations are not, so the two sets are disjoint and the order of the copies
+ *           does not matter.
+ * The survivors of head h then occupy logical slots [Start, Start + k_h), inside the last X
+ * blocks.  The block-table row becomes bt[r, Y - X .. Y) followed by -1 up to Y; the first
+ * Y - X pages go to freed_out (request order); new_lens[r, h] = k_h; new_order (laid out
+ * like kept) gets, for every new slot j < k_h, the original token index of the entry now
+ * there.  A skipped request keeps new_order = kept.  *num_pairs (if given) counts the
+ * copies.  Returns -3 if some head's source and destination counts differ (cannot happen
+ * for a valid keep set).
+ */
+int actkv_oracle_compact_inplace(const oracle_problem* p, uint16_t* kv, int32_t* bt,
+                                 const int32_t* kept, int32_t* freed_out, int32_t* new_lens,
+                                 int32_t* new_order, int64_t* num_pairs) {
+  if (check_problem(p)) return -1;
+  const int Hkv = p->num_kv_heads, D = p->head_dim, BS = p->page_size;
+  int64_t freed_off = 0, pairs_total = 0;
+  for (int r = 0; r < p->num_reqs; ++r) {
+    const int64_t L = p->seq_lens[r];
+    int32_t* row = bt + (int64_t)r * p->bt_stride;
+    int64_t kmax = 0, bmin = INT64_MAX;
+    for (int h = 0; h < Hkv; ++h) {
+      const int64_t b = p->budgets[r * Hkv + h];
+      if (b < 0) return -1;
+      const int64_t k = b > L ? L : b;
+      kmax = k > kmax ? k : kmax;
+      bmin = b < bmin ? b : bmin;
+    }
+    if (bmin >= L) {
+      for (int h = 0; h < Hkv; ++h) {
+        new_lens[r * Hkv + h] = (int32_t)L;
+        const int64_t ko = kept_offset(p, r, h);
+        for (int64_t j = 0; j < L; ++j) new_order[ko + j] = kept[ko + j];
+      }
+      continue;
+    }
+    /* Step 1 */
+    const int64_t Y = (L + BS - 1) / BS, X = (kmax + BS - 1) / BS;
+    const int64_t start = (Y - X) * BS, slots = Y * BS;
+    unsigned char* keep = (unsigned char*)malloc((size_t)slots);
+    int64_t* src = (int64_t*)malloc(sizeof(int64_t) * (size_t)(slots > 0 ? slots : 1));
+    int64_t* dst = (int64_t*)malloc(sizeof(int64_t) * (size_t)(slots > 0 ? slots : 1));
+    for (int h = 0; h < Hkv; ++h) {
+      const int64_t b = p->budgets[r * Hkv + h];
+      const int64_t k = b > L ? L : b;
+      const int64_t end = start + k;
+      const int64_t ko = kept_offset(p, r, h);
+      memset(keep, 0, (size_t)slots);
+      for (int64_t j = 0; j < k; ++j) keep[kept[ko + j]] = 1;
+      /* Step 2: destinations, and the new order of the entries already in the region */
+      int64_t nd = 0;
+      for (int64_t t = start; t < end; ++t) {
+        if (keep[t]) new_order[ko + (t - start)] = (int32_t)t;
+        else dst[nd++] = t;
+      }
+      /* Step 3 */
+      for (int64_t t = start; t < end; ++t) keep[t] = 0;
+      int64_t ns = 0;
+      for (int64_t t = 0; t < slots; ++t)
+        if (keep[t]) src[ns++] = t;
+      if (ns != nd) {
+        free(keep); free(src); free(dst);
+        return -3;
+      }
+      /* Steps 4-6 (physical slots through the row as it was before this call) */
+      for (int64_t i = 0; i < ns; ++i) {
+        const int64_t ps = actkv_oracle_slot(row, BS, src[i]);
+        const int64_t pd = actkv_oracle_slot(row, BS, dst[i]);
+        for (int which = 0; which < 2; ++which)
+          memcpy(kv_row_mut(p, kv, which, pd, h), kv_row(p, kv, which, ps, h),
+                 sizeof(uint16_t) * (size_t)D);
+        new_order[ko + (dst[i] - start)] = (int32_t)src[i];
+      }
+      pairs_total += ns;
+      new_lens[r * Hkv + h] = (int32_t)k;
+    }
+    free(keep); free(src); free(dst);
+    /* the freed blocks, then the row: the last X blocks move to the front */
+    for (int64_t i = 0; i < Y - X; ++i) freed_out[freed_off + i] = row[i];
+    for (int64_t i = 0; i < X; ++i) row[i] = row[Y - X + i];
+    for (int64_t i = X; i < Y; ++i) row[i] = -1;
+    freed_off += Y - X;
+  }
+  if (num_pairs) *num_pairs = pairs_total;
   return 0;
 }
 
