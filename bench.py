@@ -51,7 +51,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-stage",
                     choices=["score", "select", "compact", "lse", "step", "lrfu_select",
-                             "lrfu_step", "copy"],
+                             "lrfu_step", "inplace_compact", "copy"],
                     help="only run one entry point --steps times (for counter collection); "
                          "prints a short JSON line instead of the benchmark record.  'copy' "
                          "is the calibration: a plain device-to-device copy of "
@@ -102,6 +102,7 @@ def run_stage(stage, reps, bp, dp, bts, lse, scores, pooled, kept, free, freed, 
                freed=freed, new_lens=new_lens, ws=ws, qy=qy)
     ks = pooled.clone()   # keep scores of a previous step
     ks_kept = torch.empty(max(qy["num_kept"], 1), dtype=torch.float32, device=scores.device)
+    kv0 = dp.kv.clone() if stage == "inplace_compact" else None
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(reps):
@@ -116,6 +117,11 @@ def run_stage(stage, reps, bp, dp, bts, lse, scores, pooled, kept, free, freed, 
         elif stage == "lrfu_select":
             actkv.lrfu_select(bp, scores, ks, LRFU_TOP_P, LRFU_DECAY, kept=kept, ks_kept=ks_kept,
                               ws=ws)
+        elif stage == "inplace_compact":
+            # restores K/V and the table before each launch (a copy kernel between launches)
+            dp.kv.copy_(kv0)
+            bts[i].copy_(bts[-1])
+            actkv.compact_inplace(bp, dp.kv, bts[i], kept, ws=ws, want_order=False)
         elif stage == "lrfu_step":
             actkv.step_lrfu(bp, dp.q, dp.kv, bts[i], free, ks, LRFU_TOP_P, LRFU_DECAY, lse=lse,
                             scores=scores, kept=kept, ks_kept=ks_kept, freed=freed,
@@ -126,6 +132,26 @@ def run_stage(stage, reps, bp, dp, bts, lse, scores, pooled, kept, free, freed, 
     torch.cuda.synchronize()
     print(json.dumps({"profile_stage": stage, "reps": reps,
                       "avg_us": (time.perf_counter() - t0) / reps * 1e6}))
+
+
+def inplace_pairs(dp, kept) -> int:
+    """Row copies the in-place compaction makes for this selection (Alg. 4): per (r, h),
+    k minus the kept entries already inside [Start, Start + k)."""
+    H, BS = dp.num_kv_heads, dp.page_size
+    L = dp.seq_lens.astype(np.int64)
+    k = np.minimum(dp.budgets.reshape(-1, H).astype(np.int64), L[:, None])
+    off, pairs = 0, 0
+    for r in range(L.shape[0]):
+        skip = bool((dp.budgets[r * H:(r + 1) * H] >= L[r]).all())
+        Y, X = -(-int(L[r]) // BS), -(-int(k[r].max()) // BS)
+        start = (Y - X) * BS
+        for h in range(H):
+            kr = int(k[r, h])
+            seg = kept[off:off + kr]
+            off += kr
+            if not skip:
+                pairs += kr - int(((seg >= start) & (seg < start + kr)).sum())
+    return pairs
 
 
 def run_copy_calibration(reps):
@@ -279,6 +305,41 @@ def main():
     ms_lrfu_select = el[0].elapsed_time(el[1]) / K
     log(f"LRFU step {ms_lrfu * 1e3:.1f} us, LRFU select {ms_lrfu_select * 1e3:.1f} us")
 
+    # ---- the step with the paper's in-place compaction (Alg. 4), and that compaction on its
+    # own.  K/V and the block table are restored before every launch (enqueued on the same
+    # stream, outside the events); the host runs ahead of the device throughout.
+    kv0 = dp.kv.clone()
+    nfreed_ip = actkv.query_inplace(bp)
+    freed_ip = torch.empty(max(nfreed_ip, 1), dtype=torch.int32, device=dev)
+    order_ip = torch.empty(max(qy["num_kept"], 1), dtype=torch.int32, device=dev)
+    ev_ip = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(2 * K + 2)]
+    for i in range(K + 1):
+        dp.kv.copy_(kv0)
+        bts[0].copy_(bt0)
+        ev_ip[i][0].record(stream)
+        actkv.step_inplace(bp, dp.q, dp.kv, bts[0], lse=lse, scores=scores, pooled=pooled,
+                           kept=kept, freed=freed_ip, new_lens=new_lens, new_order=order_ip,
+                           ws=ws, qy=qy, nfreed=nfreed_ip)
+        ev_ip[i][1].record(stream)
+    for i in range(K + 1):
+        dp.kv.copy_(kv0)
+        bts[0].copy_(bt0)
+        ev_ip[K + 1 + i][0].record(stream)
+        actkv.compact_inplace(bp, dp.kv, bts[0], kept, freed=freed_ip, new_lens=new_lens,
+                              new_order=order_ip, ws=ws)
+        ev_ip[K + 1 + i][1].record(stream)
+    torch.cuda.synchronize()
+    ms_ip_step = float(np.mean([ev_ip[i][0].elapsed_time(ev_ip[i][1]) for i in range(1, K + 1)]))
+    ms_ip_compact = float(np.mean([ev_ip[K + 1 + i][0].elapsed_time(ev_ip[K + 1 + i][1])
+                                   for i in range(1, K + 1)]))
+    ip_pairs = inplace_pairs(dp, kept[:qy["num_kept"]].cpu().numpy())
+    ip_bytes = ip_pairs * 2 * 2 * dp.head_dim * 2   # K and V rows, read and written
+    dp.kv.copy_(kv0)
+    del kv0
+    torch.cuda.synchronize()
+    log(f"in-place step {ms_ip_step * 1e3:.1f} us, in-place compaction {ms_ip_compact * 1e3:.1f} us"
+        f" ({ip_pairs} row copies)")
+
     sum_L = int(dp.seq_lens.astype(np.int64).sum())
     value = sum_L / (ms_per_step * 1e-3)
     alg_bytes = algorithmic_bytes(dp, qy["num_kept"])
@@ -343,6 +404,10 @@ def main():
         "stages_us": {"score": stage_ms[0] * 1e3, "select": stage_ms[1] * 1e3,
                       "compact": stage_ms[2] * 1e3},
         "step_with_lse_pass_us": ms_with_lse * 1e3,
+        "inplace": {"step_us": ms_ip_step * 1e3, "compact_us": ms_ip_compact * 1e3,
+                    "row_copies": ip_pairs, "bytes_moved": ip_bytes,
+                    "compact_GBps": ip_bytes / (ms_ip_compact * 1e-3) / 1e9,
+                    "tokens_per_s": sum_L / (ms_ip_step * 1e-3)},
         "lrfu": {"top_p": LRFU_TOP_P, "decay": LRFU_DECAY, "step_us": ms_lrfu * 1e3,
                  "select_us": ms_lrfu_select * 1e3,
                  "tokens_per_s": sum_L / (ms_lrfu * 1e-3)},

@@ -6,8 +6,10 @@
  * The step standardises compression into three primitives (Sec. 3.3):
  *     AttnScore <- CalAttn(target queries, K cache)          actkv_score
  *     KeepMask  <- Eviction(AttnScore, Budget)               actkv_select
- *     KVCache   <- Compaction(KVCache, KeepMask)             actkv_compact
- * and actkv_step runs all three back to back on one stream.
+ *     KVCache   <- Compaction(KVCache, KeepMask)             actkv_compact (fresh pages)
+ *                                                            actkv_compact_inplace (Alg. 4)
+ * and actkv_step / actkv_step_inplace run all three back to back on one stream;
+ * actkv_lrfu_select / actkv_step_lrfu evict by LRFU keep scores (Sec. 5.1).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -215,6 +217,52 @@ actkv_status actkv_step_lrfu(const actkv_problem* p, const void* q, void* kv_cac
                              float* ks_kept, float* scores, float* pooled, uint8_t* hit,
                              int32_t* kept, int32_t* freed_pages, int32_t* new_lens,
                              void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Host-only planning for the in-place compaction: the pages it returns, sum over compacted
+ * requests of Y_r - X_r (Alg. 4: Y = ceil(L_r / page_size), X = ceil(max_h k_rh /
+ * page_size)).  pages_freed may be NULL.
+ */
+actkv_status actkv_query_inplace(const actkv_problem* p, int64_t* pages_freed);
+
+/*
+ * In-place compaction (Alg. 4, conflict-free slot planning of Sec. 7.2): no free list and
+ * no staging buffer.  For each request in order that is not left untouched, with
+ * Y = ceil(L_r / page_size), X = ceil(max_h k_rh / page_size) (shared by the heads: a page
+ * holds every head's row of a slot) and, per head h, Start = (Y - X) * page_size,
+ * End = Start + k_rh:
+ *   destinations = the logical slots of [Start, End) holding no kept entry, ascending
+ *                  (slots at or past L_r in the last page count: they exist and are free);
+ *   sources      = the kept entries outside [Start, End), ascending;
+ *   the i-th source's K and V rows of head h are copied bit for bit to the i-th
+ *   destination (through the block table as it was on entry).  Sources and destinations
+ *   are disjoint, so every copy runs in one pass.
+ * Afterwards head h's survivors occupy logical slots [Start, End), i.e. new slots
+ * [0, k_rh) of the shortened row: block_table[r, 0..X) = old block_table[r, Y-X..Y),
+ * block_table[r, X..Y) = -1; freed_pages receives the old block_table[r, 0..Y-X) (request
+ * order; pages_freed entries from actkv_query_inplace); new_lens[r * Hkv + h] = k_rh.
+ * Survivors do not stay in token order: new_order (nullable, int32 [num_kept], laid out like
+ * kept) receives for every new slot j < k_rh the original token index now there, so
+ * callers can carry per-entry state (e.g. the LRFU keep scores: next ks = ks_kept
+ * permuted by it).  Untouched requests keep their row and get new_order = kept.
+ * kept must be ascending within each (r, h) with entries in [0, L_r) (what actkv_select
+ * and actkv_lrfu_select write); otherwise the result is unspecified (out-of-range entries
+ * are never dereferenced).  Only destination rows are written.
+ */
+actkv_status actkv_compact_inplace(const actkv_problem* p, void* kv_cache, int32_t* block_table,
+                                   const int32_t* kept, int32_t* freed_pages, int32_t* new_lens,
+                                   int32_t* new_order, void* workspace, size_t workspace_bytes,
+                                   void* stream);
+
+/*
+ * The whole step with the in-place compaction: score -> select -> actkv_compact_inplace on
+ * `stream`.  Arguments as in actkv_step and actkv_compact_inplace (no free list).
+ */
+actkv_status actkv_step_inplace(const actkv_problem* p, const void* q, void* kv_cache,
+                                int32_t* block_table, const float* lse, float* scores,
+                                float* pooled, int32_t* kept, int32_t* freed_pages,
+                                int32_t* new_lens, int32_t* new_order, void* workspace,
+                                size_t workspace_bytes, void* stream);
 
 /* Static text for a status code. */
 const char* actkv_status_str(actkv_status status);

@@ -67,8 +67,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.actkv_lrfu_select.argtypes = [P, vp, f32, f32, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_step_lrfu.argtypes = [P, vp, vp, vp, vp, vp, i64, f32, f32, vp, vp, vp, vp, vp,
                                     vp, vp, vp, vp, sz, vp]
+    lib.actkv_query_inplace.argtypes = [P, ctypes.POINTER(i64)]
+    lib.actkv_compact_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.actkv_step_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for f in ("actkv_query", "actkv_lse", "actkv_score", "actkv_select", "actkv_compact",
-              "actkv_step", "actkv_lrfu_select", "actkv_step_lrfu"):
+              "actkv_step", "actkv_lrfu_select", "actkv_step_lrfu", "actkv_query_inplace",
+              "actkv_compact_inplace", "actkv_step_inplace"):
         getattr(lib, f).restype = ctypes.c_int
     lib.actkv_status_str.argtypes = [ctypes.c_int]
     lib.actkv_status_str.restype = ctypes.c_char_p
@@ -149,6 +153,15 @@ def query(p: Problem) -> dict:
                                           ctypes.byref(fresh), ctypes.byref(freed)))
     return dict(workspace_bytes=ws.value, num_kept=nk.value, fresh_pages_needed=fresh.value,
                 pages_freed=freed.value)
+
+
+def query_inplace(p: Problem) -> int:
+    """Host-only: pages the in-place compaction returns."""
+    lib = load_library()
+    c = p.cstruct()
+    freed = ctypes.c_int64()
+    _check("actkv_query_inplace", lib.actkv_query_inplace(ctypes.byref(c), ctypes.byref(freed)))
+    return freed.value
 
 
 def num_scores(p: Problem) -> int:
@@ -250,6 +263,58 @@ def step(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch
                                         ws.numel(), _stream(stream)))
     return dict(freed=freed[:qy["pages_freed"]], new_lens=new_lens, scores=scores,
                 pooled=pooled, kept=None if kept is None else kept[:qy["num_kept"]])
+
+
+def compact_inplace(p: Problem, kv_cache: torch.Tensor, block_table: torch.Tensor,
+                    kept: torch.Tensor, freed: Optional[torch.Tensor] = None,
+                    new_lens: Optional[torch.Tensor] = None,
+                    new_order: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                    stream=None, want_order: bool = True) -> dict:
+    """In-place compaction (Alg. 4) on kv_cache / block_table.  Returns freed, new_lens and
+    new_order (None unless requested)."""
+    lib = load_library()
+    dev = kv_cache.device
+    nfreed, nk = query_inplace(p), query(p)["num_kept"]
+    if freed is None:
+        freed = torch.empty(max(nfreed, 1), dtype=torch.int32, device=dev)
+    if new_lens is None:
+        new_lens = torch.empty(p.num_reqs * p.num_kv_heads, dtype=torch.int32, device=dev)
+    if new_order is None and want_order:
+        new_order = torch.empty(max(nk, 1), dtype=torch.int32, device=dev)
+    ws = workspace(p, dev) if ws is None else ws
+    c = p.cstruct()
+    _check("actkv_compact_inplace", lib.actkv_compact_inplace(
+        ctypes.byref(c), _ptr(kv_cache), _ptr(block_table), _ptr(kept), _ptr(freed),
+        _ptr(new_lens), _ptr(new_order), _ptr(ws), ws.numel(), _stream(stream)))
+    return dict(freed=freed[:nfreed], new_lens=new_lens,
+                new_order=None if new_order is None else new_order[:nk])
+
+
+def step_inplace(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch.Tensor,
+                 lse: Optional[torch.Tensor] = None, scores: Optional[torch.Tensor] = None,
+                 pooled: Optional[torch.Tensor] = None, kept: Optional[torch.Tensor] = None,
+                 freed: Optional[torch.Tensor] = None, new_lens: Optional[torch.Tensor] = None,
+                 new_order: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                 stream=None, qy: Optional[dict] = None, nfreed: Optional[int] = None) -> dict:
+    """The step with the in-place compaction, in place on kv_cache / block_table."""
+    lib = load_library()
+    dev = kv_cache.device
+    qy = query(p) if qy is None else qy
+    nfreed = query_inplace(p) if nfreed is None else nfreed
+    if freed is None:
+        freed = torch.empty(max(nfreed, 1), dtype=torch.int32, device=dev)
+    if new_lens is None:
+        new_lens = torch.empty(p.num_reqs * p.num_kv_heads, dtype=torch.int32, device=dev)
+    ws = workspace(p, dev) if ws is None else ws
+    c = p.cstruct()
+    _check("actkv_step_inplace", lib.actkv_step_inplace(
+        ctypes.byref(c), _ptr(q), _ptr(kv_cache), _ptr(block_table), _ptr(lse), _ptr(scores),
+        _ptr(pooled), _ptr(kept), _ptr(freed), _ptr(new_lens), _ptr(new_order), _ptr(ws),
+        ws.numel(), _stream(stream)))
+    nk = qy["num_kept"]
+    return dict(freed=freed[:nfreed], new_lens=new_lens, scores=scores, pooled=pooled,
+                kept=None if kept is None else kept[:nk],
+                new_order=None if new_order is None else new_order[:nk])
 
 
 def lrfu_select(p: Problem, scores: torch.Tensor, ks: torch.Tensor, top_p: float,

@@ -26,6 +26,7 @@ struct ReqPlan {
   int32_t fresh_off;       // sum of X over earlier requests
   int32_t freed_off;       // sum of Y over earlier requests
   int32_t lse_blocks;      // ceil(L / kLseKeysPerBlock)
+  int32_t ip_freed_off;    // sum of Y - X over earlier requests (in-place compaction)
   int64_t seg_off;         // Hkv * sum of L over earlier requests (score offset, head 0)
   int64_t lse_part_off;    // sum over earlier requests of n * Hq * lse_blocks
 };
@@ -36,6 +37,7 @@ struct HostPlan {
   int32_t max_chunks = 1;
   int64_t sum_n = 0, sum_L = 0, num_scores = 0;
   int64_t num_kept = 0, fresh_needed = 0, pages_freed = 0;
+  int64_t pages_freed_inplace = 0;  // sum of Y - X over compacted requests
   int64_t num_segments = 0;       // R * max_chunks * Hkv
   int64_t score_cost = 0;         // total scoring cost units (key tiles x row tiles)
   int64_t lse_parts = 0;          // sum_r n_r * Hq * lse_blocks_r
@@ -54,6 +56,8 @@ struct WsLayout {
   size_t score_part = 0;   // float[(max_chunks - 1) * num_scores]
   size_t pooled = 0;       // float[num_scores]
   size_t kept = 0;         // int32[num_kept]
+  size_t ip_src = 0;       // int32[num_kept]: in-place copy sources by rank, at kept_off
+  size_t ip_order = 0;     // int32[num_kept]: in-place new slot order when the caller has none
   size_t total = 0;
 };
 
@@ -72,6 +76,8 @@ inline WsLayout ws_layout(const HostPlan& hp) {
   w.score_part = take(sizeof(float) * (size_t)(hp.max_chunks - 1) * (size_t)hp.num_scores);
   w.pooled = take(sizeof(float) * (size_t)hp.num_scores);
   w.kept = take(sizeof(int32_t) * (size_t)hp.num_kept);
+  w.ip_src = take(sizeof(int32_t) * (size_t)hp.num_kept);
+  w.ip_order = take(sizeof(int32_t) * (size_t)hp.num_kept);
   w.total = o;
   return w;
 }
@@ -112,5 +118,11 @@ hipError_t launch_lrfu_select(const DevProblem& dp, const HostPlan& hp, const fl
 hipError_t launch_compact(const DevProblem& dp, const HostPlan& hp, void* kv, int32_t* bt,
                           const int32_t* kept, const int32_t* free_pages, int32_t* freed,
                           int32_t* new_lens, hipStream_t s);
+// In-place compaction (Alg. 4): slot planning into new_order (required), row copies,
+// block-table rewrite.
+hipError_t launch_compact_inplace(const DevProblem& dp, const HostPlan& hp, void* kv,
+                                  int32_t* bt, const int32_t* kept, int32_t* src_rank,
+                                  int32_t* freed, int32_t* new_lens, int32_t* new_order,
+                                  hipStream_t s);
 
 }  // namespace actkv

@@ -65,6 +65,7 @@ actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
     if (bmin < L) {
       hp->fresh_needed += (kmax + BS - 1) / BS;
       hp->pages_freed += (L + BS - 1) / BS;
+      hp->pages_freed_inplace += (L + BS - 1) / BS - (kmax + BS - 1) / BS;
     }
     hp->sum_n += n;
     hp->sum_L += L;
@@ -329,6 +330,80 @@ actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
   if (st != ACTKV_OK) return st;
   return hip_status(actkv::launch_compact(cx.dp, cx.hp, kv_cache, block_table, kept, free_pages,
                                           freed_pages, new_lens, s));
+}
+
+actkv_status actkv_query_inplace(const actkv_problem* p, int64_t* pages_freed) {
+  HostPlan hp;
+  actkv_status st = plan_host(p, &hp);
+  if (st != ACTKV_OK) return st;
+  if (pages_freed) *pages_freed = hp.pages_freed_inplace;
+  return ACTKV_OK;
+}
+
+namespace {
+actkv_status run_compact_inplace(const Ctx& cx, void* kv_cache, int32_t* block_table,
+                                 const int32_t* kept, int32_t* freed_pages, int32_t* new_lens,
+                                 int32_t* new_order, hipStream_t s) {
+  int32_t* src_rank = reinterpret_cast<int32_t*>(cx.base + cx.ws.ip_src);
+  if (!new_order) new_order = reinterpret_cast<int32_t*>(cx.base + cx.ws.ip_order);
+  return hip_status(actkv::launch_compact_inplace(cx.dp, cx.hp, kv_cache, block_table, kept,
+                                                  src_rank, freed_pages, new_lens, new_order,
+                                                  s));
+}
+
+actkv_status check_compact_inplace(const Ctx& cx, const void* kv_cache, const int32_t* block_table,
+                                   const int32_t* freed_pages, const int32_t* new_lens) {
+  if (cx.hp.R > 0 && (!block_table || !new_lens)) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.num_kept > 0 && !kv_cache) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.pages_freed_inplace > 0 && !freed_pages) return ACTKV_ERR_INVALID_ARGUMENT;
+  return ACTKV_OK;
+}
+}  // namespace
+
+actkv_status actkv_compact_inplace(const actkv_problem* p, void* kv_cache, int32_t* block_table,
+                                   const int32_t* kept, int32_t* freed_pages, int32_t* new_lens,
+                                   int32_t* new_order, void* workspace, size_t workspace_bytes,
+                                   void* stream) {
+  Ctx cx;
+  actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
+  if (st != ACTKV_OK) return st;
+  st = check_compact_inplace(cx, kv_cache, block_table, freed_pages, new_lens);
+  if (st != ACTKV_OK) return st;
+  if (cx.hp.num_kept > 0 && !kept) return ACTKV_ERR_INVALID_ARGUMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cx.hp.R == 0) return ACTKV_OK;
+  st = hip_status(actkv::launch_plan(cx.dp, s));
+  if (st != ACTKV_OK) return st;
+  return run_compact_inplace(cx, kv_cache, block_table, kept, freed_pages, new_lens, new_order,
+                             s);
+}
+
+actkv_status actkv_step_inplace(const actkv_problem* p, const void* q, void* kv_cache,
+                                int32_t* block_table, const float* lse, float* scores,
+                                float* pooled, int32_t* kept, int32_t* freed_pages,
+                                int32_t* new_lens, int32_t* new_order, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  Ctx cx;
+  actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
+  if (st != ACTKV_OK) return st;
+  st = check_compact_inplace(cx, kv_cache, block_table, freed_pages, new_lens);
+  if (st != ACTKV_OK) return st;
+  if (cx.hp.num_scores > 0 && !kv_cache) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.sum_n > 0 && !q) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (scores && pooled && scores == pooled) return ACTKV_ERR_INVALID_ARGUMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cx.hp.R == 0) return ACTKV_OK;
+  if (!scores) scores = reinterpret_cast<float*>(cx.base + cx.ws.scores);
+  if (!pooled) pooled = reinterpret_cast<float*>(cx.base + cx.ws.pooled);
+  if (!kept) kept = reinterpret_cast<int32_t*>(cx.base + cx.ws.kept);
+  st = hip_status(actkv::launch_plan(cx.dp, s));
+  if (st != ACTKV_OK) return st;
+  st = run_score(cx, q, kv_cache, block_table, lse, scores, s);
+  if (st != ACTKV_OK) return st;
+  st = hip_status(actkv::launch_select(cx.dp, cx.hp, scores, pooled, kept, s));
+  if (st != ACTKV_OK) return st;
+  return run_compact_inplace(cx, kv_cache, block_table, kept, freed_pages, new_lens, new_order,
+                             s);
 }
 
 const char* actkv_status_str(actkv_status status) {

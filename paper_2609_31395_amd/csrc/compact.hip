@@ -25,7 +25,11 @@ __host__ __device__ inline int compact_pages_per_wg(int Hkv) {
   return p < 1 ? 1 : p;
 }
 
-template <int D>
+// kInPlace = false: destination page q of request r is free_pages[fresh_off + q] and new
+// slot j gets token kept[j].  kInPlace = true (Alg. 4): destination page q is the request's
+// own page bt[r, Y - X + q] and new slot j gets token new_order[j] (`kept` below), a copy
+// only where that token is not already there.
+template <int D, bool kInPlace>
 __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
     DevProblem dp, uint16_t* kv, const int32_t* __restrict__ bt, const int32_t* __restrict__ kept,
     const int32_t* __restrict__ free_pages, int64_t num_fresh) {
@@ -52,10 +56,11 @@ __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
     const int j = (int)(f - pl.fresh_off) * kPageSize + s;
     const int bh = dp.budgets[lo * Hkv + h];
     const int kh = bh < pl.L ? bh : pl.L;
+    const int start = (pl.Y - pl.X) * kPageSize;   // in place: logical slot of new slot 0
     int64_t src = -1;
     if (j < kh) {
       const int t = kept[dp.kept_off[lo * Hkv + h] + j];
-      if (t >= 0 && t < pl.L) {
+      if (t >= 0 && t < pl.L && !(kInPlace && t == start + j)) {
         const int64_t page = bt[(int64_t)lo * dp.bt_stride + t / kPageSize];
         // pages outside the pool are never dereferenced (the slot is left unwritten)
         if (page >= 0 && page < dp.num_pages) src = page * kPageSize + t % kPageSize;
@@ -63,7 +68,9 @@ __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
     }
     src_slot[e] = src;
     if (s == 0 && h == 0) {
-      const int64_t dpg = free_pages[f];
+      const int64_t dpg = kInPlace
+          ? (int64_t)bt[(int64_t)lo * dp.bt_stride + (pl.Y - pl.X) + (f - pl.fresh_off)]
+          : (int64_t)free_pages[f];
       dst_page[p] = (dpg >= 0 && dpg < dp.num_pages) ? dpg : -1;
     }
   }
@@ -124,16 +131,161 @@ hipError_t launch_compact(const DevProblem& dp, const HostPlan& hp, void* kv, in
     const int ppw = compact_pages_per_wg(hp.Hkv);
     const unsigned grid = (unsigned)((hp.fresh_needed + ppw - 1) / ppw);
     if (dp.D == 128)
-      hipLaunchKernelGGL(compact_gather_kernel<128>, dim3(grid), dim3(kCompactThreads), 0, s, dp,
-                         static_cast<uint16_t*>(kv), bt, kept, free_pages, hp.fresh_needed);
+      hipLaunchKernelGGL((compact_gather_kernel<128, false>), dim3(grid), dim3(kCompactThreads),
+                         0, s, dp, static_cast<uint16_t*>(kv), bt, kept, free_pages,
+                         hp.fresh_needed);
     else
-      hipLaunchKernelGGL(compact_gather_kernel<64>, dim3(grid), dim3(kCompactThreads), 0, s, dp,
-                         static_cast<uint16_t*>(kv), bt, kept, free_pages, hp.fresh_needed);
+      hipLaunchKernelGGL((compact_gather_kernel<64, false>), dim3(grid), dim3(kCompactThreads),
+                         0, s, dp, static_cast<uint16_t*>(kv), bt, kept, free_pages,
+                         hp.fresh_needed);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(compact_rewrite_kernel, dim3(hp.R), dim3(256), 0, s, dp, bt, free_pages,
                      freed, new_lens);
+  return hipGetLastError();
+}
+
+// ---- in-place compaction (Alg. 4) --------------------------------------------------------
+//
+// Per compacted request, with Y = ceil(L / 16) and X = ceil(max_h k_h / 16) (shared by the
+// heads: a page holds every head's row of a slot), each head h has the tail region
+// [Start, End) = [(Y - X) * 16, (Y - X) * 16 + k_h).  Its destinations are the slots of the
+// region that hold no kept entry (slots at or past L included: they exist in the last
+// page), its sources the kept entries outside the region, both ascending; the i-th source
+// is copied to the i-th destination (Alg. 4 steps 2-6).  Sources are kept and destinations
+// are not, so no copy reads a slot another copy writes: one pass, no staging buffer.
+//
+// inplace_plan_kernel: one 1024-thread workgroup per (request, KV head).  With the kept
+//   indices ascending, the sources are kept[0, a) and kept[b, k), a and b the counts of kept
+//   entries below Start and below End (one workgroup sum); the destinations are the zero
+//   bits of a bitmap of the region (kept[a, b) set), ranked by one workgroup scan per
+//   32768 slots.  The plan is written as new_order: the token that new slot j = d - Start
+//   receives (the i-th source for the i-th destination d, the token itself for a survivor
+//   already in place).
+// compact_gather_kernel<D, true>: the copies, organised by destination page exactly like
+//   the fresh-page gather (the last X pages of every request in place of fresh pages),
+//   skipping the slots whose token is already there.
+// inplace_rewrite_kernel: per request, the first Y - X pages to the freed list, then the
+//   block-table row shifted left by Y - X (read before write within each chunk of 256
+//   entries) and -1 past X.
+constexpr int kIpPlanThreads = 1024;
+constexpr int kIpBitmapSlots = 32 * kIpPlanThreads;   // region slots per bitmap pass
+
+__global__ __launch_bounds__(kIpPlanThreads) void inplace_plan_kernel(
+    DevProblem dp, const int32_t* __restrict__ kept, int32_t* src_rank, int32_t* new_order) {
+  __shared__ uint32_t bits[kIpBitmapSlots / 32];
+  __shared__ int64_t scan_tmp[17];
+  const int seg = blockIdx.x, tid = threadIdx.x, Hkv = dp.Hkv;
+  const int r = seg / Hkv;
+  const ReqPlan pl = dp.plan[r];
+  const int L = pl.L;
+  const int bud = dp.budgets[seg];
+  const int k = bud < L ? bud : L;
+  const int64_t ko = dp.kept_off[seg];
+  const int32_t* kk = kept + ko;
+  int32_t* ps = src_rank + ko;
+  int32_t* no = new_order + ko;
+  if (pl.skip) {   // untouched request: nothing moves
+    for (int j = tid; j < k; j += kIpPlanThreads) no[j] = kk[j];
+    return;
+  }
+  const int start = (pl.Y - pl.X) * kPageSize, end = start + k;
+  // a = kept entries below Start, b = below End (each count < 2^31: one packed sum)
+  int64_t cnt = 0;
+  for (int j = tid; j < k; j += kIpPlanThreads) {
+    const int t = kk[j];
+    cnt += ((int64_t)(t < start) << 32) + (t < end);
+  }
+  int64_t tot;
+  block_excl_scan_i64(cnt, scan_tmp, &tot);
+  const int a = (int)(tot >> 32), b = (int)(tot & 0xFFFFFFFFll);
+  const int npairs = a + (k - b);
+  // sources in ascending order; survivors inside the region stay where they are
+  for (int j = tid; j < k; j += kIpPlanThreads) {
+    const int t = kk[j];
+    if (j < a) ps[j] = t;
+    else if (j >= b) ps[j - (b - a)] = t;
+    else if (t >= start && t < end) no[t - start] = t;
+  }
+  __syncthreads();   // the sources are read back below
+  // destinations: the holes of [start, end), ranked in ascending order
+  int64_t rank_base = 0;
+  for (int c0 = 0; c0 < k; c0 += kIpBitmapSlots) {
+    const int span = k - c0 < kIpBitmapSlots ? k - c0 : kIpBitmapSlots;
+    bits[tid] = 0;
+    __syncthreads();
+    for (int j = a + tid; j < b; j += kIpPlanThreads) {
+      const int off = kk[j] - start - c0;
+      if (off >= 0 && off < span) atomicOr(&bits[off >> 5], 1u << (off & 31));
+    }
+    __syncthreads();
+    const int valid = span - tid * 32;   // slots of this thread's word inside the span
+    uint32_t holes = valid <= 0 ? 0u : ~bits[tid];
+    if (valid > 0 && valid < 32) holes &= (1u << valid) - 1u;
+    int64_t rank = rank_base + block_excl_scan_i64(__popc(holes), scan_tmp, &tot);
+    while (holes) {
+      const int j = c0 + tid * 32 + __builtin_ctz(holes);   // new slot (destination - Start)
+      if (rank < npairs) no[j] = ps[rank];
+      ++rank;
+      holes &= holes - 1u;
+    }
+    rank_base += tot;
+    __syncthreads();   // the bitmap is cleared again by the next pass
+  }
+}
+
+__global__ __launch_bounds__(256) void inplace_rewrite_kernel(DevProblem dp, int32_t* bt,
+                                                              int32_t* __restrict__ freed,
+                                                              int32_t* __restrict__ new_lens) {
+  const int r = blockIdx.x, Hkv = dp.Hkv, tid = threadIdx.x;
+  const ReqPlan pl = dp.plan[r];
+  for (int h = tid; h < Hkv; h += 256) {
+    const int b = dp.budgets[r * Hkv + h];
+    new_lens[r * Hkv + h] = pl.skip ? pl.L : (b < pl.L ? b : pl.L);
+  }
+  if (pl.skip) return;
+  int32_t* row = bt + (int64_t)r * dp.bt_stride;
+  const int X = pl.X, F = pl.Y - pl.X;
+  for (int i = tid; i < F; i += 256) freed[pl.ip_freed_off + i] = row[i];
+  __syncthreads();   // every freed page read before the row is overwritten
+  for (int base = 0; base < X; base += 256) {
+    const int i = base + tid;
+    const int32_t v = i < X ? row[F + i] : 0;
+    __syncthreads();   // this chunk's reads before its writes (the ranges overlap if F < 256)
+    if (i < X) row[i] = v;
+    __syncthreads();
+  }
+  for (int i = X + tid; i < pl.Y; i += 256) row[i] = -1;
+}
+
+hipError_t launch_compact_inplace(const DevProblem& dp, const HostPlan& hp, void* kv,
+                                  int32_t* bt, const int32_t* kept, int32_t* src_rank,
+                                  int32_t* freed, int32_t* new_lens, int32_t* new_order,
+                                  hipStream_t s) {
+  if (hp.R == 0) return hipSuccess;
+  hipLaunchKernelGGL(inplace_plan_kernel, dim3((unsigned)(hp.R * hp.Hkv)), dim3(kIpPlanThreads),
+                     0, s, dp, kept, src_rank, new_order);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // the destination pages are the last X pages of every compacted request: as many, and at
+  // the same offsets, as the fresh pages of the other form
+  if (hp.fresh_needed > 0) {
+    const int ppw = compact_pages_per_wg(hp.Hkv);
+    const unsigned grid = (unsigned)((hp.fresh_needed + ppw - 1) / ppw);
+    if (dp.D == 128)
+      hipLaunchKernelGGL((compact_gather_kernel<128, true>), dim3(grid), dim3(kCompactThreads),
+                         0, s, dp, static_cast<uint16_t*>(kv), bt, new_order, nullptr,
+                         hp.fresh_needed);
+    else
+      hipLaunchKernelGGL((compact_gather_kernel<64, true>), dim3(grid), dim3(kCompactThreads),
+                         0, s, dp, static_cast<uint16_t*>(kv), bt, new_order, nullptr,
+                         hp.fresh_needed);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(inplace_rewrite_kernel, dim3(hp.R), dim3(256), 0, s, dp, bt, freed,
+                     new_lens);
   return hipGetLastError();
 }
 

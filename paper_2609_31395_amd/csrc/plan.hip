@@ -9,7 +9,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
   __shared__ int64_t tmp[17];
   const int R = dp.R, Hkv = dp.Hkv, G = dp.G, C = dp.max_chunks;
   int64_t carry_n = 0, carry_L = 0, carry_X = 0, carry_Y = 0, carry_k = 0, carry_cost = 0,
-          carry_lse = 0;
+          carry_lse = 0, carry_ip = 0;
   for (int base = 0; base < R; base += blockDim.x) {
     const int r = base + threadIdx.x;
     const bool ok = r < R;
@@ -48,11 +48,14 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
     const int64_t c_off = carry_cost + block_excl_scan_i64(cost, tmp, &tot); carry_cost += tot;
     const int64_t l_off = carry_lse + block_excl_scan_i64((int64_t)n * dp.Hq * lse_blocks, tmp, &tot);
     carry_lse += tot;
+    const int64_t f_off = carry_ip + block_excl_scan_i64(Y - X, tmp, &tot);
+    carry_ip += tot;
     if (ok) {
       ReqPlan p;
       p.L = L; p.n = n; p.X = X; p.Y = Y; p.skip = skip; p.nchunk = nchunk;
       p.q_off = (int32_t)q_off; p.fresh_off = (int32_t)x_off; p.freed_off = (int32_t)y_off;
       p.lse_blocks = lse_blocks; p.seg_off = seg_off; p.lse_part_off = l_off;
+      p.ip_freed_off = (int32_t)f_off;
       dp.plan[r] = p;
       // kept offsets per (r, h)
       int64_t ko = k_off;

@@ -179,3 +179,39 @@ def test_lrfu_rejects_segments_past_its_length_limit():
     ws = actkv.query(p)["workspace_bytes"]
     assert lib.actkv_lrfu_select(ctypes.byref(c), FAKE, 0.9, 0.5, FAKE + 64, None, None, FAKE,
                                  FAKE, FAKE, ws, None) == -2
+
+
+def test_inplace_page_accounting_matches_oracle():
+    rng = np.random.default_rng(4)
+    for _ in range(5):
+        seq = [int(x) for x in rng.integers(0, 200, size=5)]
+        H = 3
+        bud = [int(rng.integers(0, L + 20)) for L in seq for _ in range(H)]
+        pb = W.make_custom(seq_lens=seq, q_lens=[min(1, L) for L in seq], num_q_heads=H,
+                           num_kv_heads=H, head_dim=64, budgets=bud)
+        assert actkv.query_inplace(binding_problem(pb)) == oracle.inplace_pages_freed(pb)
+
+
+def test_inplace_entry_points_validate_before_launching():
+    lib = actkv.load_library()
+    p = _tiny()
+    c = p.cstruct()
+    c.seq_lens_d = c.q_lens_d = c.budgets_d = FAKE
+    ws = actkv.query(p)["workspace_bytes"]
+    assert actkv.query_inplace(p) > 0
+    # missing block table, lengths, kept indices or freed list
+    assert lib.actkv_compact_inplace(ctypes.byref(c), FAKE, None, FAKE, FAKE, FAKE, None, FAKE,
+                                     ws, None) == -1
+    assert lib.actkv_compact_inplace(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, None, None, FAKE,
+                                     ws, None) == -1
+    assert lib.actkv_compact_inplace(ctypes.byref(c), FAKE, FAKE, None, FAKE, FAKE, None, FAKE,
+                                     ws, None) == -1
+    assert lib.actkv_compact_inplace(ctypes.byref(c), FAKE, FAKE, FAKE, None, FAKE, None, FAKE,
+                                     ws, None) == -1
+    assert lib.actkv_compact_inplace(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                                     16, None) == -3
+    assert lib.actkv_step_inplace(ctypes.byref(c), None, FAKE, FAKE, None, None, None, None,
+                                  FAKE, FAKE, None, FAKE, ws, None) == -1
+    assert lib.actkv_step_inplace(ctypes.byref(c), FAKE, FAKE, FAKE, None, FAKE, FAKE, None,
+                                  FAKE, FAKE, None, FAKE, ws, None) == -1   # scores == pooled
+    assert lib.actkv_query_inplace(None, None) == -1
