@@ -49,6 +49,8 @@ def parse():
     ap.add_argument("--cpu-sample-reqs", type=int, default=8,
                     help="requests of the workload the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-table1", action="store_true",
+                    help="skip the Table 1 shapes (streaming scoring and compression ops)")
     ap.add_argument("--profile-stage",
                     choices=["score", "select", "compact", "lse", "step", "lrfu_select",
                              "lrfu_step", "inplace_compact", "copy"],
@@ -152,6 +154,110 @@ def inplace_pairs(dp, kept) -> int:
             if not skip:
                 pairs += kr - int(((seg >= start) & (seg < start + kr)).sum())
     return pairs
+
+
+def _binding(dp, dev, q_lens=None):
+    from paper_2609_31395_amd import actkv
+    return actkv.Problem(seq_lens=dp.seq_lens, q_lens=dp.q_lens if q_lens is None else q_lens,
+                         budgets=dp.budgets, num_q_heads=dp.num_q_heads,
+                         num_kv_heads=dp.num_kv_heads, head_dim=dp.head_dim,
+                         num_pages=dp.num_pages, bt_stride=dp.bt_stride, sm_scale=dp.sm_scale,
+                         pool_window=dp.pool_window, causal=dp.causal).to_device(dev)
+
+
+def _event_pairs(n):
+    import torch
+    return [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(n)]
+
+
+def _mean_ms(ev, skip=1):
+    return float(np.mean([a.elapsed_time(b) for a, b in ev[skip:]]))
+
+
+def run_table1(reps, dev, stream):
+    """Table 1 shapes (r requests compressed L -> B; 8 KV heads, d = 128): one streaming
+    scoring step (one action query per request, LSE supplied) and one compression operation
+    -- selection plus the in-place compaction of Alg. 4, and selection plus the fresh-page
+    compaction -- each timed with events on the launch stream; K/V and the block table are
+    restored before each compaction, outside the events."""
+    import torch
+    from paper_2609_31395_amd import actkv
+    from paper_2609_31395_amd import workloads as W
+    rows = []
+    for name in [k for k in W.CONFIGS if k.startswith("table1_")]:
+        dp = W.make_device_problem(name, device=dev)
+        bp = _binding(dp, dev)
+        qy = actkv.query(bp)
+        ws = torch.empty(qy["workspace_bytes"], dtype=torch.uint8, device=dev)
+        bt0 = torch.from_numpy(dp.block_table).to(dev)
+        bt = bt0.clone()
+        free = torch.from_numpy(dp.free_pages).to(dev)
+        lse = actkv.lse(bp, dp.q, dp.kv, bt0, ws=ws)
+        n_sc = actkv.num_scores(bp)
+        acc = torch.zeros(n_sc, dtype=torch.float32, device=dev)
+        pooled = torch.empty_like(acc)
+        kept = torch.empty(max(qy["num_kept"], 1), dtype=torch.int32, device=dev)
+        freed = torch.empty(max(qy["pages_freed"], 1), dtype=torch.int32, device=dev)
+        new_lens = torch.empty(bp.num_reqs * bp.num_kv_heads, dtype=torch.int32, device=dev)
+        kv0 = dp.kv.clone()
+        ev_s, ev_i, ev_f = _event_pairs(reps + 1), _event_pairs(reps + 1), _event_pairs(reps + 1)
+        for e in ev_s:
+            e[0].record(stream)
+            actkv.score_accumulate(bp, dp.q, dp.kv, bt0, acc, lse=lse, ws=ws)
+            e[1].record(stream)
+        for e in ev_i:
+            dp.kv.copy_(kv0)
+            bt.copy_(bt0)
+            e[0].record(stream)
+            actkv.select(bp, acc, pooled=pooled, kept=kept, ws=ws)
+            actkv.compact_inplace(bp, dp.kv, bt, kept, freed=freed, new_lens=new_lens, ws=ws,
+                                  want_order=False)
+            e[1].record(stream)
+        for e in ev_f:
+            bt.copy_(bt0)
+            e[0].record(stream)
+            actkv.select(bp, acc, pooled=pooled, kept=kept, ws=ws)
+            actkv.compact(bp, dp.kv, bt, kept, free, freed=freed, new_lens=new_lens, ws=ws)
+            e[1].record(stream)
+        torch.cuda.synchronize()
+        L, B = int(dp.seq_lens[0]), int(dp.budgets[0])
+        score_us = _mean_ms(ev_s) * 1e3
+        k_bytes = n_sc * dp.head_dim * 2
+        rows.append({"config": name, "requests": bp.num_reqs, "tokens": L, "budget": B,
+                     "score_step_us": score_us,
+                     "score_step_hbm_frac": k_bytes / (score_us * 1e-6) / (HBM_PEAK_GBS * 1e9),
+                     "compress_inplace_us": _mean_ms(ev_i) * 1e3,
+                     "compress_fresh_us": _mean_ms(ev_f) * 1e3})
+        del dp, kv0, ws
+        torch.cuda.synchronize()
+    return rows
+
+
+def run_streaming_batch(dp, bp_full, reps, dev, stream):
+    """One decode step of streaming scoring over the whole batch: every request scores its
+    cache with one action query (the first of its action queries), LSE supplied."""
+    import torch
+    from paper_2609_31395_amd import actkv
+    ones = np.ones_like(dp.q_lens)
+    bp = _binding(dp, dev, q_lens=ones)
+    first = torch.from_numpy(dp.cu_q[:-1].astype(np.int64)).to(dev)
+    q1 = dp.q[first].contiguous()
+    qy = actkv.query(bp)
+    ws = torch.empty(qy["workspace_bytes"], dtype=torch.uint8, device=dev)
+    bt0 = torch.from_numpy(dp.block_table).to(dev)
+    lse = actkv.lse(bp, q1, dp.kv, bt0, ws=ws)
+    acc = torch.zeros(actkv.num_scores(bp), dtype=torch.float32, device=dev)
+    ev = _event_pairs(reps + 1)
+    for e in ev:
+        e[0].record(stream)
+        actkv.score_accumulate(bp, q1, dp.kv, bt0, acc, lse=lse, ws=ws)
+        e[1].record(stream)
+    torch.cuda.synchronize()
+    us = _mean_ms(ev) * 1e3
+    k_bytes = actkv.num_scores(bp) * dp.head_dim * 2
+    return {"score_step_us": us, "k_bytes": k_bytes,
+            "hbm_GBps": k_bytes / (us * 1e-6) / 1e9,
+            "hbm_frac": k_bytes / (us * 1e-6) / (HBM_PEAK_GBS * 1e9)}
 
 
 def run_copy_calibration(reps):
@@ -353,6 +459,15 @@ def main():
         if tr.get("source_sha256") == source_digest() and tr.get("workload") == args.workload:
             traffic = int(tr["hbm_bytes_per_launch"])
 
+    streaming = run_streaming_batch(dp, bp, K, dev, stream)
+    log(f"streaming scoring step (1 query per request): {streaming['score_step_us']:.1f} us, "
+        f"{streaming['hbm_GBps']:.0f} GB/s")
+    table1 = run_table1(max(K // 2, 5), dev, stream) if not args.no_table1 else None
+    if table1:
+        for row in table1:
+            log(f"{row['config']:16s} score step {row['score_step_us']:7.1f} us  compress "
+                f"in place {row['compress_inplace_us']:7.1f} us  fresh {row['compress_fresh_us']:7.1f} us")
+
     cpu = None
     if not args.no_cpu_baseline and args.cpu_sample_reqs > 0:
         import oracle
@@ -408,6 +523,8 @@ def main():
                     "row_copies": ip_pairs, "bytes_moved": ip_bytes,
                     "compact_GBps": ip_bytes / (ms_ip_compact * 1e-3) / 1e9,
                     "tokens_per_s": sum_L / (ms_ip_step * 1e-3)},
+        "streaming": streaming,
+        "table1": table1,
         "lrfu": {"top_p": LRFU_TOP_P, "decay": LRFU_DECAY, "step_us": ms_lrfu * 1e3,
                  "select_us": ms_lrfu_select * 1e3,
                  "tokens_per_s": sum_L / (ms_lrfu * 1e-3)},

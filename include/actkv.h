@@ -133,6 +133,21 @@ actkv_status actkv_score(const actkv_problem* p, const void* q, const void* kv_c
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Streaming scoring (Alg. 3 as the paper runs it: one action query per request per decode
+ * step, its LSE from that step's attention, the per-entry aggregate updated in place and
+ * reset by the caller at the start of each action region): acc += the scores of this call,
+ * as actkv_score would compute them (q_lens[r] = the new queries of request r, usually 1;
+ * 0 adds nothing).  acc: fp32 in/out in the score layout of this call's seq_lens, 16-byte
+ * aligned; when a sequence grows between steps the caller extends its segment with zeros
+ * for the new entries.  n steps of one query each add up to one actkv_score call with all
+ * n queries (SUM; with MAX_MEAN each step adds max over the group, so acc / n is the
+ * running mean of Sec. 7.1).  The step's scores pass through the workspace.
+ */
+actkv_status actkv_score_accumulate(const actkv_problem* p, const void* q, const void* kv_cache,
+                                    const int32_t* block_table, const float* lse, float* acc,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Eviction (Alg. 1 step 5, TopK(score, k = B)): per (request, KV head) the
  * k_rh = min(budget_rh, L_r) entries with the largest pooled score are kept, ties going
  * to the lower token index, and written ascending into `kept` ([num_kept] int32).

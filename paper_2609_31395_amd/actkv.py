@@ -67,12 +67,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.actkv_lrfu_select.argtypes = [P, vp, f32, f32, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_step_lrfu.argtypes = [P, vp, vp, vp, vp, vp, i64, f32, f32, vp, vp, vp, vp, vp,
                                     vp, vp, vp, vp, sz, vp]
+    lib.actkv_score_accumulate.argtypes = [P, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_query_inplace.argtypes = [P, ctypes.POINTER(i64)]
     lib.actkv_compact_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_step_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for f in ("actkv_query", "actkv_lse", "actkv_score", "actkv_select", "actkv_compact",
               "actkv_step", "actkv_lrfu_select", "actkv_step_lrfu", "actkv_query_inplace",
-              "actkv_compact_inplace", "actkv_step_inplace"):
+              "actkv_compact_inplace", "actkv_step_inplace", "actkv_score_accumulate"):
         getattr(lib, f).restype = ctypes.c_int
     lib.actkv_status_str.argtypes = [ctypes.c_int]
     lib.actkv_status_str.restype = ctypes.c_char_p
@@ -200,6 +201,20 @@ def score(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torc
                                           _ptr(block_table), _ptr(lse), _ptr(out), _ptr(ws),
                                           ws.numel(), _stream(stream)))
     return out
+
+
+def score_accumulate(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor,
+                     block_table: torch.Tensor, acc: torch.Tensor,
+                     lse: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                     stream=None) -> torch.Tensor:
+    """acc += the scores of this call (streaming, one decode step)."""
+    lib = load_library()
+    ws = workspace(p, kv_cache.device) if ws is None else ws
+    c = p.cstruct()
+    _check("actkv_score_accumulate", lib.actkv_score_accumulate(
+        ctypes.byref(c), _ptr(q), _ptr(kv_cache), _ptr(block_table), _ptr(lse), _ptr(acc),
+        _ptr(ws), ws.numel(), _stream(stream)))
+    return acc
 
 
 def select(p: Problem, scores: torch.Tensor, pooled: Optional[torch.Tensor] = None,

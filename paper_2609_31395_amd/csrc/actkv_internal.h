@@ -108,6 +108,8 @@ hipError_t launch_lse(const DevProblem& dp, const HostPlan& hp, const void* q, c
 hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
                         const void* kv, const int32_t* bt, const float* lse, float* scores,
                         float* score_part, hipStream_t s);
+// acc[i] += s[i], i < n (both 16-byte aligned or n handled element-wise at the tail).
+hipError_t launch_accumulate(float* acc, const float* s, int64_t n, hipStream_t st);
 hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
                          float* pooled, int32_t* kept, hipStream_t s);
 // LRFU selection (attention-aware keep scores): segments up to kLrfuMaxLen entries.

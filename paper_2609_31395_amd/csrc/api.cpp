@@ -195,6 +195,25 @@ actkv_status actkv_score(const actkv_problem* p, const void* q, const void* kv_c
   return run_score(cx, q, kv_cache, block_table, lse, scores, s);
 }
 
+actkv_status actkv_score_accumulate(const actkv_problem* p, const void* q, const void* kv_cache,
+                                    const int32_t* block_table, const float* lse, float* acc,
+                                    void* workspace, size_t workspace_bytes, void* stream) {
+  Ctx cx;
+  actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
+  if (st != ACTKV_OK) return st;
+  if (cx.hp.num_scores > 0 && (!kv_cache || !block_table || !acc)) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (cx.hp.sum_n > 0 && !q) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (acc && (reinterpret_cast<uintptr_t>(acc) & 15)) return ACTKV_ERR_INVALID_ARGUMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cx.hp.R == 0 || cx.hp.num_scores == 0) return ACTKV_OK;
+  st = hip_status(actkv::launch_plan(cx.dp, s));
+  if (st != ACTKV_OK) return st;
+  float* step_scores = reinterpret_cast<float*>(cx.base + cx.ws.scores);
+  st = run_score(cx, q, kv_cache, block_table, lse, step_scores, s);
+  if (st != ACTKV_OK) return st;
+  return hip_status(actkv::launch_accumulate(acc, step_scores, cx.hp.num_scores, s));
+}
+
 actkv_status actkv_select(const actkv_problem* p, const float* scores, float* pooled,
                           int32_t* kept, void* workspace, size_t workspace_bytes,
                           void* stream) {

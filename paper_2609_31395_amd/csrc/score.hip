@@ -682,6 +682,29 @@ hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
   return e;
 }
 
+// acc[i] += s[i] (streaming aggregation: the scores of one decode step added to the running
+// aggregate).  Four floats per lane per step, grid-stride.
+__global__ __launch_bounds__(256) void accumulate_kernel(float* acc, const float* s, int64_t n) {
+  const int64_t n4 = n / 4;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    float4 a = reinterpret_cast<float4*>(acc)[i];
+    const float4 b = reinterpret_cast<const float4*>(s)[i];
+    a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+    reinterpret_cast<float4*>(acc)[i] = a;
+  }
+  for (int64_t i = n4 * 4 + (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    acc[i] += s[i];
+}
+
+hipError_t launch_accumulate(float* acc, const float* s, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n / 4 + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(accumulate_kernel, dim3((unsigned)blocks), dim3(256), 0, st, acc, s, n);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------------------
 // Log-sum-exp pass (online softmax).  Here K is the MFMA A operand and Q the B operand, so
 // each lane's accumulator column is one query row and its 16 registers 16 keys: the

@@ -80,6 +80,22 @@ CONFIGS: Dict[str, WorkloadConfig] = {
 }
 
 
+# Table 1 shapes (Sec. 8, paged compression kernels): block 16, 8 KV heads, head_dim 128,
+# r concurrent requests, each compressed from L to B entries.  The query-head count is not
+# given; 32 (G = 4) is the Qwen3 shape with 8 KV heads.  One action query per request: the
+# current decode step's query of the streaming scoring.  No pooling (the paper pools
+# nothing).
+TABLE1_SIZES = ((1024, 512), (2048, 1536), (6144, 4096))
+TABLE1_REQS = (1, 4, 16, 64)
+for _i, (_r, (_L, _B)) in enumerate([(r, lb) for r in TABLE1_REQS for lb in TABLE1_SIZES]):
+    _name = f"table1_r{_r}_{_L // 1024}k"
+    CONFIGS[_name] = WorkloadConfig(
+        _name, _r, 32, 8, 128, (_L, _L), (1, 1), ("fixed", _B), 1, 0.01, 2000 + _i,
+        description=f"Table 1 shape: {_r} request(s) compressed {_L} -> {_B} entries, 32q/8kv "
+                    f"heads, d=128, one action query (decode step), no pooling")
+del _i, _r, _L, _B, _name
+
+
 @dataclass
 class Problem:
     """Host-side (numpy) inputs of one compression step over one layer."""
