@@ -2,7 +2,8 @@
 
 Only ``tests/``, the package smoke check and the benchmark's CPU-baseline leg may import
 this module.  It wraps ``actkv_oracle.c`` (plain C, fp64, OpenMP over independent
-(request, KV head) pairs) through ctypes.  It shares no code with the HIP library; its
+(request, KV head) pairs) and ``confidence_oracle.c`` (the confidence monitor and budget
+rule of Alg. 2) through ctypes.  It shares no code with the HIP library; its
 inputs are host numpy arrays (bf16 carried as uint16 bit patterns).
 
 The functions take a ``problem`` object with the attributes of a synthetic workload
@@ -20,7 +21,7 @@ from typing import Optional
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "actkv_oracle.c")
+_SRCS = [os.path.join(_HERE, "actkv_oracle.c"), os.path.join(_HERE, "confidence_oracle.c")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 AGG = {"sum": 0, "max_mean": 1}
@@ -28,12 +29,17 @@ AGG = {"sum": 0, "max_mean": 1}
 
 def build(force: bool = True) -> str:
     """Compile the oracle with gcc (-O2, no fast-math, no fused multiply-add, OpenMP)."""
-    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+    if force or _stale():
         tmp = _LIB + ".tmp"
         subprocess.run(["gcc", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
-                        "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"], check=True)
+                        "-Wall", "-Wextra", "-o", tmp] + _SRCS + ["-lm"], check=True)
         os.replace(tmp, _LIB)
     return _LIB
+
+
+def _stale() -> bool:
+    return not os.path.exists(_LIB) or any(os.path.getmtime(_LIB) < os.path.getmtime(f)
+                                           for f in _SRCS)
 
 
 class _Problem(ctypes.Structure):
@@ -53,7 +59,7 @@ _lib = None
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        if _stale():
             build(force=True)
         lib = ctypes.CDLL(_LIB)
         P = ctypes.POINTER(_Problem)
@@ -70,6 +76,11 @@ def _load():
         lib.actkv_oracle_compact_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp,
                                                      ctypes.POINTER(i64)]
         lib.actkv_oracle_hits.argtypes = [P, vp, ctypes.c_double, vp]
+        lib.actkv_oracle_token_confidence.argtypes = [vp, i64, i64, i64, ctypes.c_int32, vp]
+        lib.actkv_oracle_budget_update.argtypes = [vp, vp, ctypes.c_int32, ctypes.c_int32,
+                                                   ctypes.c_int32, ctypes.c_double,
+                                                   ctypes.c_double, ctypes.c_int32, vp, vp, vp,
+                                                   vp, vp]
         lib.actkv_oracle_lrfu_update.argtypes = [P, vp, vp, ctypes.c_float, vp]
         for f in ("actkv_oracle_lse", "actkv_oracle_scores", "actkv_oracle_pool",
                   "actkv_oracle_select", "actkv_oracle_totals", "actkv_oracle_compact",
@@ -305,6 +316,41 @@ def lrfu_step(pb, ks: np.ndarray, top_p: float, decay: float,
     kv2, bt2, freed, new_lens = compact(pb, kept, **kw)
     return dict(raw=raw, pooled=pooled, hit=hit, ks=ks2, kept=kept, ks_kept=ks_kept, kv=kv2,
                 block_table=bt2, freed=freed, new_lens=new_lens)
+
+
+def token_confidence(logits: np.ndarray, k: int = 20) -> np.ndarray:
+    """T per row of `logits` ([rows, vocab] float32): -(1/k) sum of the log-probabilities of
+    the k most likely tokens (Sec. 6.1), fp64."""
+    x = np.ascontiguousarray(logits, dtype=np.float32)
+    rows, vocab = x.shape
+    out = np.zeros(rows, np.float64)
+    _check(_load().actkv_oracle_token_confidence(x.ctypes.data, rows, vocab, vocab, int(k),
+                                                 out.ctypes.data), "token_confidence")
+    return out
+
+
+def budget_update(conf_seqs, budgets, window: int = 64, stride: int = 8,
+                  bottom_pct: float = 10.0, scale_up: float = 1.75,
+                  budget_upper: int = 30000) -> dict:
+    """Alg. 2 steps 2-4 per request: trace-level confidence, trend, budget.  conf_seqs is a
+    list of float32 token-confidence sequences (one per request).  Parameters are passed as
+    the float32 values the GPU entry point receives."""
+    seqs = [np.ascontiguousarray(c, dtype=np.float32) for c in conf_seqs]
+    flat = np.concatenate(seqs) if seqs else np.zeros(0, np.float32)
+    flat = np.ascontiguousarray(flat if flat.size else np.zeros(1, np.float32))
+    offsets = np.concatenate([[0], np.cumsum([c.size for c in seqs])]).astype(np.int64)
+    R = len(seqs)
+    b_in = np.ascontiguousarray(budgets, dtype=np.int32)
+    b_out = np.zeros(max(R, 1), np.int32)
+    slopes = np.zeros(max(R, 1), np.float64)
+    thr = np.zeros(max(R, 1), np.float64)
+    kept = np.zeros(max(R, 1), np.int32)
+    _check(_load().actkv_oracle_budget_update(
+        flat.ctypes.data, offsets.ctypes.data, R, int(window), int(stride),
+        float(np.float32(bottom_pct)), float(np.float32(scale_up)), int(budget_upper),
+        b_in.ctypes.data, b_out.ctypes.data, slopes.ctypes.data, thr.ctypes.data,
+        kept.ctypes.data), "budget_update")
+    return dict(budgets=b_out[:R], slopes=slopes[:R], thresholds=thr[:R], retained=kept[:R])
 
 
 def num_threads() -> int:
