@@ -260,6 +260,40 @@ def run_streaming_batch(dp, bp_full, reps, dev, stream):
             "hbm_frac": k_bytes / (us * 1e-6) / (HBM_PEAK_GBS * 1e9)}
 
 
+CONF_VOCAB, CONF_TOPK = 151936, 20   # Qwen3 vocabulary; the paper's k
+
+
+def run_confidence(num_reqs, trace_len, reps, dev, stream):
+    """The confidence monitor of one decode step (one row of fp32 logits per request over
+    the Qwen3 vocabulary, top-20) and the budget update at a compression trigger (traces of
+    trace_len token confidences per request; w = 64, s = 8, b = 10%, x1.75, cap 30K)."""
+    import torch
+    from paper_2609_31395_amd import actkv
+    g = torch.Generator(device=dev).manual_seed(77)
+    logits = torch.randn((num_reqs, CONF_VOCAB), generator=g, device=dev) * 3.0
+    conf = torch.empty(num_reqs, dtype=torch.float32, device=dev)
+    ev = _event_pairs(reps + 1)
+    for e in ev:
+        e[0].record(stream)
+        actkv.token_confidence(logits, top_k=CONF_TOPK, out=conf)
+        e[1].record(stream)
+    trace = (torch.rand((num_reqs * trace_len,), generator=g, device=dev) * 2.0 + 8.0)
+    offsets = np.arange(num_reqs + 1, dtype=np.int64) * trace_len
+    budgets = torch.full((num_reqs,), 512, dtype=torch.int32, device=dev)
+    out = torch.empty_like(budgets)
+    eb = _event_pairs(reps + 1)
+    for e in eb:
+        e[0].record(stream)
+        actkv.budget_update(trace, offsets, budgets, out=out)
+        e[1].record(stream)
+    torch.cuda.synchronize()
+    us = _mean_ms(ev) * 1e3
+    nbytes = num_reqs * CONF_VOCAB * 4
+    return {"rows": num_reqs, "vocab": CONF_VOCAB, "top_k": CONF_TOPK,
+            "token_conf_us": us, "token_conf_GBps": nbytes / (us * 1e-6) / 1e9,
+            "trace_len": trace_len, "budget_update_us": _mean_ms(eb) * 1e3}
+
+
 def run_copy_calibration(reps):
     """A plain copy of COPY_CALIB_BYTES bytes, `reps` times: it reads and writes exactly that
     many bytes, so it scales the HBM counters of the other kernels."""
@@ -462,6 +496,10 @@ def main():
     streaming = run_streaming_batch(dp, bp, K, dev, stream)
     log(f"streaming scoring step (1 query per request): {streaming['score_step_us']:.1f} us, "
         f"{streaming['hbm_GBps']:.0f} GB/s")
+    confidence = run_confidence(dp.num_reqs, int(dp.seq_lens.max()), K, dev, stream)
+    log(f"confidence: token confidence {confidence['token_conf_us']:.1f} us "
+        f"({confidence['token_conf_GBps']:.0f} GB/s), budget update "
+        f"{confidence['budget_update_us']:.1f} us")
     table1 = run_table1(max(K // 2, 5), dev, stream) if not args.no_table1 else None
     if table1:
         for row in table1:
@@ -524,6 +562,7 @@ def main():
                     "compact_GBps": ip_bytes / (ms_ip_compact * 1e-3) / 1e9,
                     "tokens_per_s": sum_L / (ms_ip_step * 1e-3)},
         "streaming": streaming,
+        "confidence": confidence,
         "table1": table1,
         "lrfu": {"top_p": LRFU_TOP_P, "decay": LRFU_DECAY, "step_us": ms_lrfu * 1e3,
                  "select_us": ms_lrfu_select * 1e3,

@@ -279,6 +279,47 @@ actkv_status actkv_step_inplace(const actkv_problem* p, const void* q, void* kv_
                                 int32_t* new_lens, int32_t* new_order, void* workspace,
                                 size_t workspace_bytes, void* stream);
 
+/*
+ * Token-level confidence (Sec. 6.1; Alg. 2 step 1, GetTokenConf): for every row r of
+ * logits, the negative mean log-probability of the top_k most likely tokens,
+ *   conf[r] = LSE(logits[r]) - (1/k) sum of the k largest logits[r][v],  k = min(top_k, vocab).
+ * logits: fp32 [rows][row_stride] (the first `vocab` entries of each row are used; -inf
+ * entries are masked tokens); conf: fp32 [rows].  top_k in 1..64 and vocab up to 262,144
+ * (else ACTKV_ERR_UNSUPPORTED).  The log-sum-exp is accumulated in fp32 (fixed reduction
+ * order: deterministic), the top-k sum in fp64.  workspace: at least the bytes
+ * actkv_token_confidence_workspace reports.
+ */
+actkv_status actkv_token_confidence_workspace(int64_t rows, int64_t vocab, int32_t top_k,
+                                              size_t* workspace_bytes);
+actkv_status actkv_token_confidence(const float* logits, int64_t rows, int64_t vocab,
+                                    int64_t row_stride, int32_t top_k, float* conf,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Budget update before compression (Alg. 2 steps 2-4), per request r with token
+ * confidences T = token_conf[offsets[r] .. offsets[r + 1]) (the trace so far):
+ *   R'_m  = min T[m * stride .. m * stride + window), m = 0 .. (n - window) / stride;
+ *   Q     = the bottom_pct-th percentile of R' by linear interpolation between order
+ *           statistics (position bottom_pct / 100 * (M - 1));
+ *   alpha = least-squares slope of R'_m against m over the windows with R'_m <= Q, sums in
+ *           window order in fp64 (0 with fewer than two such windows or n < window);
+ *   budgets_out[r] = min(floor(budgets_in[r] * scale_up), budget_upper) if alpha < 0, else
+ *           budgets_in[r].
+ * The call is made when compression triggers (the paper's TriggerCompress).  offsets:
+ * int64 [num_reqs + 1] on the host (validation) and on the device; budgets int32 [num_reqs]
+ * on the device (budgets_out may alias budgets_in); slopes, thresholds (fp64, NaN with no
+ * window) and retained (int32 window counts) are optional device outputs.  At most 16,384
+ * windows per request (ACTKV_ERR_UNSUPPORTED beyond).  The percentile, the sums and the
+ * budget rule are evaluated in fp64 with every operation rounded on its own, so results
+ * are reproducible bit for bit.
+ */
+actkv_status actkv_budget_update(const float* token_conf, const int64_t* offsets_h,
+                                 const int64_t* offsets_d, int32_t num_reqs, int32_t window,
+                                 int32_t stride, float bottom_pct, float scale_up,
+                                 int32_t budget_upper, const int32_t* budgets_in,
+                                 int32_t* budgets_out, double* slopes, double* thresholds,
+                                 int32_t* retained, void* stream);
+
 /* Static text for a status code. */
 const char* actkv_status_str(actkv_status status);
 

@@ -68,12 +68,19 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.actkv_step_lrfu.argtypes = [P, vp, vp, vp, vp, vp, i64, f32, f32, vp, vp, vp, vp, vp,
                                     vp, vp, vp, vp, sz, vp]
     lib.actkv_score_accumulate.argtypes = [P, vp, vp, vp, vp, vp, vp, sz, vp]
+    i32 = ctypes.c_int32
+    lib.actkv_token_confidence_workspace.argtypes = [i64, i64, i32, ctypes.POINTER(sz)]
+    lib.actkv_token_confidence.argtypes = [vp, i64, i64, i64, i32, vp, vp, sz, vp]
+    lib.actkv_budget_update.argtypes = [vp, vp, vp, i32, i32, i32, f32, f32, i32, vp, vp, vp,
+                                        vp, vp, vp]
     lib.actkv_query_inplace.argtypes = [P, ctypes.POINTER(i64)]
     lib.actkv_compact_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_step_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for f in ("actkv_query", "actkv_lse", "actkv_score", "actkv_select", "actkv_compact",
               "actkv_step", "actkv_lrfu_select", "actkv_step_lrfu", "actkv_query_inplace",
-              "actkv_compact_inplace", "actkv_step_inplace", "actkv_score_accumulate"):
+              "actkv_compact_inplace", "actkv_step_inplace", "actkv_score_accumulate",
+              "actkv_token_confidence_workspace", "actkv_token_confidence",
+              "actkv_budget_update"):
         getattr(lib, f).restype = ctypes.c_int
     lib.actkv_status_str.argtypes = [ctypes.c_int]
     lib.actkv_status_str.restype = ctypes.c_char_p
@@ -381,6 +388,51 @@ def step_lrfu(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: 
     return dict(freed=freed[:qy["pages_freed"]], new_lens=new_lens,
                 ks_kept=ks_kept[:qy["num_kept"]], scores=scores, pooled=pooled, hit=hit,
                 kept=None if kept is None else kept[:qy["num_kept"]])
+
+
+def token_confidence(logits: torch.Tensor, top_k: int = 20, out: Optional[torch.Tensor] = None,
+                     ws: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Token-level confidence of every row of `logits` (fp32 [rows, >= vocab] with unit
+    column stride); vocab = logits.shape[1]."""
+    lib = load_library()
+    rows, vocab = int(logits.shape[0]), int(logits.shape[1])
+    if logits.dtype != torch.float32 or logits.stride(1) != 1:
+        raise ValueError("logits must be float32 with contiguous rows")
+    if out is None:
+        out = torch.empty(max(rows, 1), dtype=torch.float32, device=logits.device)
+    need = ctypes.c_size_t()
+    _check("actkv_token_confidence_workspace",
+           lib.actkv_token_confidence_workspace(rows, vocab, int(top_k), ctypes.byref(need)))
+    if ws is None:
+        ws = torch.empty(max(need.value, 1), dtype=torch.uint8, device=logits.device)
+    _check("actkv_token_confidence", lib.actkv_token_confidence(
+        _ptr(logits), rows, vocab, int(logits.stride(0)), int(top_k), _ptr(out), _ptr(ws),
+        ws.numel(), _stream(stream)))
+    return out[:rows]
+
+
+def budget_update(token_conf: torch.Tensor, offsets: np.ndarray, budgets: torch.Tensor,
+                  window: int = 64, stride: int = 8, bottom_pct: float = 10.0,
+                  scale_up: float = 1.75, budget_upper: int = 30000,
+                  out: Optional[torch.Tensor] = None, stream=None) -> dict:
+    """Alg. 2 steps 2-4 for every request (token confidences concatenated, int64 offsets
+    [R + 1] on the host).  Returns the new budgets, slopes, thresholds and retained counts."""
+    lib = load_library()
+    dev = budgets.device
+    off_h = np.ascontiguousarray(offsets, dtype=np.int64)
+    R = int(off_h.shape[0] - 1)
+    off_d = torch.from_numpy(off_h).to(dev)
+    if out is None:
+        out = torch.empty(max(R, 1), dtype=torch.int32, device=dev)
+    slopes = torch.empty(max(R, 1), dtype=torch.float64, device=dev)
+    thr = torch.empty_like(slopes)
+    kept = torch.empty(max(R, 1), dtype=torch.int32, device=dev)
+    _check("actkv_budget_update", lib.actkv_budget_update(
+        _ptr(token_conf), off_h.ctypes.data, _ptr(off_d), R, int(window), int(stride),
+        float(bottom_pct), float(scale_up), int(budget_upper), _ptr(budgets), _ptr(out),
+        _ptr(slopes), _ptr(thr), _ptr(kept), _stream(stream)))
+    return dict(budgets=out[:R], slopes=slopes[:R], thresholds=thr[:R], retained=kept[:R],
+                _keep=off_d)
 
 
 def status_str(code: int) -> str:

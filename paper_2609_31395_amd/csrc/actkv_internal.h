@@ -117,6 +117,20 @@ constexpr int64_t kLrfuMaxLen = 38400;
 hipError_t launch_lrfu_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
                               float top_p, float decay, float* ks, uint8_t* hit, float* pooled,
                               int32_t* kept, float* ks_kept, hipStream_t s);
+// Confidence monitor (Sec. 6.1, Alg. 2).
+constexpr int kConfMaxTopK = 64;          // largest k of the token confidence
+constexpr int kConfChunkLogits = 16384;   // logits one partial workgroup handles
+constexpr int kConfMaxSplits = 16;        // chunks per row: vocab <= 262,144
+constexpr int kMaxBudgetWindows = 16384;  // min-pool windows one request may have
+int conf_splits(int64_t vocab);
+hipError_t launch_token_confidence(const float* logits, int64_t rows, int64_t vocab,
+                                   int64_t row_stride, int k, float2* ms, float* top,
+                                   float* conf, hipStream_t s);
+hipError_t launch_budget_update(const float* tconf, const int64_t* offsets, int num_reqs,
+                                int window, int stride, float bottom_pct, float scale_up,
+                                int budget_upper, const int32_t* budgets_in,
+                                int32_t* budgets_out, double* slopes, double* thresholds,
+                                int32_t* retained, hipStream_t s);
 hipError_t launch_compact(const DevProblem& dp, const HostPlan& hp, void* kv, int32_t* bt,
                           const int32_t* kept, const int32_t* free_pages, int32_t* freed,
                           int32_t* new_lens, hipStream_t s);

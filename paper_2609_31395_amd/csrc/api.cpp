@@ -425,6 +425,73 @@ actkv_status actkv_step_inplace(const actkv_problem* p, const void* q, void* kv_
                              s);
 }
 
+namespace {
+size_t token_conf_ws(int64_t rows, int64_t vocab, int32_t top_k) {
+  const int64_t parts = rows * actkv::conf_splits(vocab);
+  return actkv::align256(sizeof(float2) * (size_t)parts) +
+         actkv::align256(sizeof(float) * (size_t)(parts * top_k));
+}
+actkv_status check_token_conf(int64_t rows, int64_t vocab, int32_t top_k) {
+  if (rows < 0 || vocab < 1 || top_k < 1) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (top_k > actkv::kConfMaxTopK) return ACTKV_ERR_UNSUPPORTED;
+  if (vocab > (int64_t)actkv::kConfMaxSplits * actkv::kConfChunkLogits) return ACTKV_ERR_UNSUPPORTED;
+  if (rows > INT32_MAX / actkv::kConfMaxSplits) return ACTKV_ERR_UNSUPPORTED;
+  return ACTKV_OK;
+}
+}  // namespace
+
+actkv_status actkv_token_confidence_workspace(int64_t rows, int64_t vocab, int32_t top_k,
+                                              size_t* workspace_bytes) {
+  actkv_status st = check_token_conf(rows, vocab, top_k);
+  if (st != ACTKV_OK) return st;
+  if (workspace_bytes) *workspace_bytes = token_conf_ws(rows, vocab, top_k);
+  return ACTKV_OK;
+}
+
+actkv_status actkv_token_confidence(const float* logits, int64_t rows, int64_t vocab,
+                                    int64_t row_stride, int32_t top_k, float* conf,
+                                    void* workspace, size_t workspace_bytes, void* stream) {
+  actkv_status st = check_token_conf(rows, vocab, top_k);
+  if (st != ACTKV_OK) return st;
+  if (row_stride < vocab) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (rows == 0) return ACTKV_OK;
+  if (!logits || !conf) return ACTKV_ERR_INVALID_ARGUMENT;
+  const size_t need = token_conf_ws(rows, vocab, top_k);
+  if (workspace_bytes < need) return ACTKV_ERR_WORKSPACE_TOO_SMALL;
+  if (!workspace) return ACTKV_ERR_INVALID_ARGUMENT;
+  char* base = static_cast<char*>(workspace);
+  const int64_t parts = rows * actkv::conf_splits(vocab);
+  float2* ms = reinterpret_cast<float2*>(base);
+  float* top = reinterpret_cast<float*>(base + actkv::align256(sizeof(float2) * (size_t)parts));
+  return hip_status(actkv::launch_token_confidence(logits, rows, vocab, row_stride, top_k, ms,
+                                                   top, conf, static_cast<hipStream_t>(stream)));
+}
+
+actkv_status actkv_budget_update(const float* token_conf, const int64_t* offsets_h,
+                                 const int64_t* offsets_d, int32_t num_reqs, int32_t window,
+                                 int32_t stride, float bottom_pct, float scale_up,
+                                 int32_t budget_upper, const int32_t* budgets_in,
+                                 int32_t* budgets_out, double* slopes, double* thresholds,
+                                 int32_t* retained, void* stream) {
+  if (num_reqs < 0 || window < 1 || stride < 1 || budget_upper < 0)
+    return ACTKV_ERR_INVALID_ARGUMENT;
+  if (!(bottom_pct >= 0.0f && bottom_pct <= 100.0f) || !(scale_up >= 1.0f) || !isfinite(scale_up))
+    return ACTKV_ERR_INVALID_ARGUMENT;
+  if (num_reqs == 0) return ACTKV_OK;
+  if (!offsets_h || !offsets_d || !budgets_in || !budgets_out) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (offsets_h[0] < 0) return ACTKV_ERR_INVALID_ARGUMENT;
+  for (int r = 0; r < num_reqs; ++r) {
+    const int64_t n = offsets_h[r + 1] - offsets_h[r];
+    if (n < 0) return ACTKV_ERR_INVALID_ARGUMENT;
+    if (n >= window && (n - window) / stride + 1 > actkv::kMaxBudgetWindows)
+      return ACTKV_ERR_UNSUPPORTED;
+  }
+  if (offsets_h[num_reqs] > offsets_h[0] && !token_conf) return ACTKV_ERR_INVALID_ARGUMENT;
+  return hip_status(actkv::launch_budget_update(
+      token_conf, offsets_d, num_reqs, window, stride, bottom_pct, scale_up, budget_upper,
+      budgets_in, budgets_out, slopes, thresholds, retained, static_cast<hipStream_t>(stream)));
+}
+
 const char* actkv_status_str(actkv_status status) {
   switch (status) {
     case ACTKV_OK: return "ok";

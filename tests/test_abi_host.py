@@ -215,3 +215,31 @@ def test_inplace_entry_points_validate_before_launching():
     assert lib.actkv_step_inplace(ctypes.byref(c), FAKE, FAKE, FAKE, None, FAKE, FAKE, None,
                                   FAKE, FAKE, None, FAKE, ws, None) == -1   # scores == pooled
     assert lib.actkv_query_inplace(None, None) == -1
+
+
+def test_confidence_entry_points_validate_before_launching():
+    lib = actkv.load_library()
+    sz = ctypes.c_size_t()
+    assert lib.actkv_token_confidence_workspace(4, 151936, 20, ctypes.byref(sz)) == 0
+    assert sz.value > 0
+    assert lib.actkv_token_confidence_workspace(4, 151936, 0, None) == -1
+    assert lib.actkv_token_confidence_workspace(4, 151936, 65, None) == -2
+    assert lib.actkv_token_confidence_workspace(4, 262145, 20, None) == -2
+    assert lib.actkv_token_confidence_workspace(-1, 100, 20, None) == -1
+    assert lib.actkv_token_confidence(FAKE, 4, 1000, 999, 20, FAKE, FAKE, 1 << 20, None) == -1
+    assert lib.actkv_token_confidence(None, 4, 1000, 1000, 20, FAKE, FAKE, 1 << 20, None) == -1
+    assert lib.actkv_token_confidence(FAKE, 4, 1000, 1000, 20, FAKE, FAKE, 16, None) == -3
+    off = np.array([0, 100, 300], np.int64)
+
+    def upd(off=off, window=64, stride=8, pct=10.0, scale=1.75, upper=30000):
+        return lib.actkv_budget_update(FAKE, off.ctypes.data, FAKE, off.shape[0] - 1, window,
+                                       stride, pct, scale, upper, FAKE, FAKE, None, None,
+                                       None, None)
+    assert upd(window=0) == -1
+    assert upd(stride=0) == -1
+    assert upd(pct=100.5) == -1
+    assert upd(pct=float("nan")) == -1
+    assert upd(scale=0.5) == -1
+    assert upd(upper=-1) == -1
+    assert upd(off=np.array([0, 100, 50], np.int64)) == -1
+    assert upd(off=np.array([0, 64 + 8 * 16384], np.int64)) == -2   # one window too many
