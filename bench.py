@@ -49,6 +49,8 @@ def parse():
     ap.add_argument("--cpu-sample-reqs", type=int, default=8,
                     help="requests of the workload the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="time only the headline step and its stages (for profiling)")
     ap.add_argument("--no-table1", action="store_true",
                     help="skip the Table 1 shapes (streaming scoring and compression ops)")
     ap.add_argument("--profile-stage",
@@ -309,6 +311,96 @@ def run_copy_calibration(reps):
                       "avg_us": (time.perf_counter() - t0) / reps * 1e6}))
 
 
+def run_lrfu(c):
+    """The step with LRFU eviction (Sec. 5.1: keep scores carried from step to step, top-p
+    hit mask, decay), and its selection on its own, on the launch stream."""
+    import torch
+    from paper_2609_31395_amd import actkv
+    bp, dp, qy, ws, lse, scores, pooled, kept = (c[k] for k in (
+        "bp", "dp", "qy", "ws", "lse", "scores", "pooled", "kept"))
+    free, freed, new_lens, bts, bt0, dev, stream, K = (c[k] for k in (
+        "free", "freed", "new_lens", "bts", "bt0", "dev", "stream", "K"))
+    el = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ks = pooled.clone()   # the keep scores a previous step left
+    ks_kept = torch.empty(max(qy["num_kept"], 1), dtype=torch.float32, device=dev)
+    for b in bts:
+        b.copy_(bt0)
+    torch.cuda.synchronize()
+
+    def lrfu_step(bt):
+        actkv.step_lrfu(bp, dp.q, dp.kv, bt, free, ks, LRFU_TOP_P, LRFU_DECAY, lse=lse,
+                        scores=scores, kept=kept, ks_kept=ks_kept, freed=freed,
+                        new_lens=new_lens, ws=ws, qy=qy)
+
+    lrfu_step(bts[K])   # warm-up on its own pristine copy
+    torch.cuda.synchronize()
+    el[0].record(stream)
+    for i in range(K):
+        lrfu_step(bts[i])
+    el[1].record(stream)
+    torch.cuda.synchronize()
+    ms_lrfu = el[0].elapsed_time(el[1]) / K
+    el[0].record(stream)
+    for i in range(K):
+        actkv.lrfu_select(bp, scores, ks, LRFU_TOP_P, LRFU_DECAY, kept=kept, ks_kept=ks_kept,
+                          ws=ws)
+    el[1].record(stream)
+    torch.cuda.synchronize()
+    ms_lrfu_select = el[0].elapsed_time(el[1]) / K
+    log(f"LRFU step {ms_lrfu * 1e3:.1f} us, LRFU select {ms_lrfu_select * 1e3:.1f} us")
+    for b in bts:
+        b.copy_(bt0)
+    return {"top_p": LRFU_TOP_P, "decay": LRFU_DECAY, "step_us": ms_lrfu * 1e3,
+            "select_us": ms_lrfu_select * 1e3, "tokens_per_s": c["sum_L"] / (ms_lrfu * 1e-3)}
+
+
+def run_inplace(c):
+    """The step with the paper's in-place compaction (Alg. 4), and that compaction on its
+    own.  K/V and the block table are restored before every launch (enqueued on the same
+    stream, outside the events); the host runs ahead of the device throughout."""
+    import torch
+    from paper_2609_31395_amd import actkv
+    bp, dp, qy, ws, lse, scores, pooled, kept = (c[k] for k in (
+        "bp", "dp", "qy", "ws", "lse", "scores", "pooled", "kept"))
+    new_lens, bts, bt0, dev, stream, K = (c[k] for k in (
+        "new_lens", "bts", "bt0", "dev", "stream", "K"))
+    kv0 = dp.kv.clone()
+    nfreed_ip = actkv.query_inplace(bp)
+    freed_ip = torch.empty(max(nfreed_ip, 1), dtype=torch.int32, device=dev)
+    order_ip = torch.empty(max(qy["num_kept"], 1), dtype=torch.int32, device=dev)
+    ev_ip = _event_pairs(2 * K + 2)
+    for i in range(K + 1):
+        dp.kv.copy_(kv0)
+        bts[0].copy_(bt0)
+        ev_ip[i][0].record(stream)
+        actkv.step_inplace(bp, dp.q, dp.kv, bts[0], lse=lse, scores=scores, pooled=pooled,
+                           kept=kept, freed=freed_ip, new_lens=new_lens, new_order=order_ip,
+                           ws=ws, qy=qy, nfreed=nfreed_ip)
+        ev_ip[i][1].record(stream)
+    for i in range(K + 1):
+        dp.kv.copy_(kv0)
+        bts[0].copy_(bt0)
+        ev_ip[K + 1 + i][0].record(stream)
+        actkv.compact_inplace(bp, dp.kv, bts[0], kept, freed=freed_ip, new_lens=new_lens,
+                              new_order=order_ip, ws=ws)
+        ev_ip[K + 1 + i][1].record(stream)
+    torch.cuda.synchronize()
+    ms_ip_step = _mean_ms(ev_ip[:K + 1])
+    ms_ip_compact = _mean_ms(ev_ip[K + 1:])
+    ip_pairs = inplace_pairs(dp, kept[:qy["num_kept"]].cpu().numpy())
+    ip_bytes = ip_pairs * 2 * 2 * dp.head_dim * 2   # K and V rows, read and written
+    dp.kv.copy_(kv0)
+    bts[0].copy_(bt0)
+    del kv0
+    torch.cuda.synchronize()
+    log(f"in-place step {ms_ip_step * 1e3:.1f} us, in-place compaction {ms_ip_compact * 1e3:.1f} us"
+        f" ({ip_pairs} row copies)")
+    return {"step_us": ms_ip_step * 1e3, "compact_us": ms_ip_compact * 1e3,
+            "row_copies": ip_pairs, "bytes_moved": ip_bytes,
+            "compact_GBps": ip_bytes / (ms_ip_compact * 1e-3) / 1e9,
+            "tokens_per_s": c["sum_L"] / (ms_ip_step * 1e-3)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -415,72 +507,14 @@ def main():
     log(f"stages (us) {np.round(stage_ms * 1e3, 1).tolist()}, step with LSE pass "
         f"{ms_with_lse * 1e3:.1f} us")
 
-    # ---- the step with LRFU eviction (keep scores carried from step to step, top-p hit
-    # mask), and its select stage on its own, both on the launch stream
-    ks = pooled.clone()   # the keep scores a previous step left
-    ks_kept = torch.empty(max(qy["num_kept"], 1), dtype=torch.float32, device=dev)
-    for b in bts:
-        b.copy_(bt0)
-    torch.cuda.synchronize()
-
-    def lrfu_step(bt):
-        actkv.step_lrfu(bp, dp.q, dp.kv, bt, free, ks, LRFU_TOP_P, LRFU_DECAY, lse=lse,
-                        scores=scores, kept=kept, ks_kept=ks_kept, freed=freed,
-                        new_lens=new_lens, ws=ws, qy=qy)
-
-    lrfu_step(bts[K])   # warm-up on its own pristine copy
-    torch.cuda.synchronize()
-    el[0].record(stream)
-    for i in range(K):
-        lrfu_step(bts[i])
-    el[1].record(stream)
-    torch.cuda.synchronize()
-    ms_lrfu = el[0].elapsed_time(el[1]) / K
-    el[0].record(stream)
-    for i in range(K):
-        actkv.lrfu_select(bp, scores, ks, LRFU_TOP_P, LRFU_DECAY, kept=kept, ks_kept=ks_kept,
-                          ws=ws)
-    el[1].record(stream)
-    torch.cuda.synchronize()
-    ms_lrfu_select = el[0].elapsed_time(el[1]) / K
-    log(f"LRFU step {ms_lrfu * 1e3:.1f} us, LRFU select {ms_lrfu_select * 1e3:.1f} us")
-
-    # ---- the step with the paper's in-place compaction (Alg. 4), and that compaction on its
-    # own.  K/V and the block table are restored before every launch (enqueued on the same
-    # stream, outside the events); the host runs ahead of the device throughout.
-    kv0 = dp.kv.clone()
-    nfreed_ip = actkv.query_inplace(bp)
-    freed_ip = torch.empty(max(nfreed_ip, 1), dtype=torch.int32, device=dev)
-    order_ip = torch.empty(max(qy["num_kept"], 1), dtype=torch.int32, device=dev)
-    ev_ip = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(2 * K + 2)]
-    for i in range(K + 1):
-        dp.kv.copy_(kv0)
-        bts[0].copy_(bt0)
-        ev_ip[i][0].record(stream)
-        actkv.step_inplace(bp, dp.q, dp.kv, bts[0], lse=lse, scores=scores, pooled=pooled,
-                           kept=kept, freed=freed_ip, new_lens=new_lens, new_order=order_ip,
-                           ws=ws, qy=qy, nfreed=nfreed_ip)
-        ev_ip[i][1].record(stream)
-    for i in range(K + 1):
-        dp.kv.copy_(kv0)
-        bts[0].copy_(bt0)
-        ev_ip[K + 1 + i][0].record(stream)
-        actkv.compact_inplace(bp, dp.kv, bts[0], kept, freed=freed_ip, new_lens=new_lens,
-                              new_order=order_ip, ws=ws)
-        ev_ip[K + 1 + i][1].record(stream)
-    torch.cuda.synchronize()
-    ms_ip_step = float(np.mean([ev_ip[i][0].elapsed_time(ev_ip[i][1]) for i in range(1, K + 1)]))
-    ms_ip_compact = float(np.mean([ev_ip[K + 1 + i][0].elapsed_time(ev_ip[K + 1 + i][1])
-                                   for i in range(1, K + 1)]))
-    ip_pairs = inplace_pairs(dp, kept[:qy["num_kept"]].cpu().numpy())
-    ip_bytes = ip_pairs * 2 * 2 * dp.head_dim * 2   # K and V rows, read and written
-    dp.kv.copy_(kv0)
-    del kv0
-    torch.cuda.synchronize()
-    log(f"in-place step {ms_ip_step * 1e3:.1f} us, in-place compaction {ms_ip_compact * 1e3:.1f} us"
-        f" ({ip_pairs} row copies)")
-
     sum_L = int(dp.seq_lens.astype(np.int64).sum())
+    extra = not args.headline_only
+    ctx = dict(bp=bp, dp=dp, qy=qy, ws=ws, lse=lse, scores=scores, pooled=pooled, kept=kept,
+               free=free, freed=freed, new_lens=new_lens, bts=bts, bt0=bt0, dev=dev,
+               stream=stream, K=K, sum_L=sum_L)
+    lrfu = run_lrfu(ctx) if extra else None
+    inplace = run_inplace(ctx) if extra else None
+
     value = sum_L / (ms_per_step * 1e-3)
     alg_bytes = algorithmic_bytes(dp, qy["num_kept"])
     flops = score_flops(dp)
@@ -493,14 +527,16 @@ def main():
         if tr.get("source_sha256") == source_digest() and tr.get("workload") == args.workload:
             traffic = int(tr["hbm_bytes_per_launch"])
 
-    streaming = run_streaming_batch(dp, bp, K, dev, stream)
-    log(f"streaming scoring step (1 query per request): {streaming['score_step_us']:.1f} us, "
-        f"{streaming['hbm_GBps']:.0f} GB/s")
-    confidence = run_confidence(dp.num_reqs, int(dp.seq_lens.max()), K, dev, stream)
-    log(f"confidence: token confidence {confidence['token_conf_us']:.1f} us "
-        f"({confidence['token_conf_GBps']:.0f} GB/s), budget update "
-        f"{confidence['budget_update_us']:.1f} us")
-    table1 = run_table1(max(K // 2, 5), dev, stream) if not args.no_table1 else None
+    streaming = confidence = table1 = None
+    if extra:
+        streaming = run_streaming_batch(dp, bp, K, dev, stream)
+        log(f"streaming scoring step (1 query per request): {streaming['score_step_us']:.1f} us,"
+            f" {streaming['hbm_GBps']:.0f} GB/s")
+        confidence = run_confidence(dp.num_reqs, int(dp.seq_lens.max()), K, dev, stream)
+        log(f"confidence: token confidence {confidence['token_conf_us']:.1f} us "
+            f"({confidence['token_conf_GBps']:.0f} GB/s), budget update "
+            f"{confidence['budget_update_us']:.1f} us")
+        table1 = run_table1(max(K // 2, 5), dev, stream) if not args.no_table1 else None
     if table1:
         for row in table1:
             log(f"{row['config']:16s} score step {row['score_step_us']:7.1f} us  compress "
@@ -557,16 +593,11 @@ def main():
         "stages_us": {"score": stage_ms[0] * 1e3, "select": stage_ms[1] * 1e3,
                       "compact": stage_ms[2] * 1e3},
         "step_with_lse_pass_us": ms_with_lse * 1e3,
-        "inplace": {"step_us": ms_ip_step * 1e3, "compact_us": ms_ip_compact * 1e3,
-                    "row_copies": ip_pairs, "bytes_moved": ip_bytes,
-                    "compact_GBps": ip_bytes / (ms_ip_compact * 1e-3) / 1e9,
-                    "tokens_per_s": sum_L / (ms_ip_step * 1e-3)},
+        "inplace": inplace,
         "streaming": streaming,
         "confidence": confidence,
         "table1": table1,
-        "lrfu": {"top_p": LRFU_TOP_P, "decay": LRFU_DECAY, "step_us": ms_lrfu * 1e3,
-                 "select_us": ms_lrfu_select * 1e3,
-                 "tokens_per_s": sum_L / (ms_lrfu * 1e-3)},
+        "lrfu": lrfu,
         "roofline": {
             "kernel": "score_kernel (actkv_score, LSE supplied)",
             "bound": "mfma",
