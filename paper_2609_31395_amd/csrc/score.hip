@@ -538,6 +538,52 @@ __device__ __forceinline__ void score_sweep16(const SweepCtx& cx, const KLoadPla
   finish_tile(cx, red[(cx.i1 - 1) & (kRedBufs - 1)], cx.i1 - 1);
 }
 
+// The sweep of a wave whose row tiles hold no real row (few query rows, e.g. one decode
+// query per request): the same K loads, barriers and tile finishes as score_sweep16, but no
+// MFMA and no epilogue; its partial slots stay zero.
+template <int D>
+__device__ __forceinline__ void score_sweep_idle(const SweepCtx& cx, const KLoadPlan<D, kWaves>& kp,
+                                                 RedTile* red) {
+  using Gm = TileGeom<D>;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  // this wave's partial slots of every reduction buffer: zero (no finish of the previous
+  // segment reads them any more)
+#pragma unroll
+  for (int b = 0; b < kRedBufs; ++b)
+#pragma unroll
+    for (int es = 0; es < kSubTiles; ++es)
+      red[b][w][(lane >> 4) * kRedGrp + es * 16 + (lane & 15)] = 0.f;
+  auto clamp_tile = [&](int t) { return t < cx.i1 ? t : cx.i1 - 1; };
+#pragma unroll
+  for (int p = 0; p < kScoreStages - 1; ++p)
+    issue_k_tile<D, kWaves>(cx.kl + p * Gm::kTileBytes, cx.kv_bytes,
+                            page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(cx.i0 + p)),
+                            cx.page_bytes, kp);
+  int64_t next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp,
+                                         clamp_tile(cx.i0 + kScoreStages - 1));
+  wait_vmcnt<(kScoreStages - 2) * Gm::kLoadsPerWave>();
+  wait_lgkmcnt0();
+  __builtin_amdgcn_s_barrier();
+  issue_k_tile<D, kWaves>(cx.kl + (kScoreStages - 1) * Gm::kTileBytes, cx.kv_bytes, next_page,
+                          cx.page_bytes, kp);
+  next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(cx.i0 + kScoreStages));
+  for (int i = cx.i0; i < cx.i1; ++i) {
+    // the barrier phase of tile i, as in tile_phases16
+    const int st_i = (i - cx.i0) & (kScoreStages - 1);
+    wait_vmcnt<(kScoreStages - 2) * Gm::kLoadsPerWave>();
+    wait_lgkmcnt0();
+    __builtin_amdgcn_s_barrier();
+    issue_k_tile<D, kWaves>(cx.kl + st_i * Gm::kTileBytes, cx.kv_bytes, next_page, cx.page_bytes,
+                            kp);
+    const int nt = i + kScoreStages + 1;
+    next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, nt < cx.i1 ? nt : cx.i1 - 1);
+    if (i > cx.i0) finish_tile(cx, red[(i - 1) & (kRedBufs - 1)], i - 1);
+  }
+  wait_lgkmcnt0();
+  __builtin_amdgcn_s_barrier();
+  finish_tile(cx, red[(cx.i1 - 1) & (kRedBufs - 1)], cx.i1 - 1);
+}
+
 template <int D, bool kMaxMean>
 __global__ __launch_bounds__(kThreads, 1) void score_kernel(
     DevProblem dp, const uint16_t* __restrict__ q_ptr, const uint16_t* __restrict__ kv_ptr,
@@ -627,7 +673,15 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
     // row tiles past the chunk's real rows are all padding (Q = 0, beta = +inf): every
     // wave runs only as many row tiles as can hold real rows
     const int nrt = chunk_wave_tiles(G, grouped, n, c);
-    if (nrt >= 4) score_sweep16<D, kMaxMean, 4>(cx, kp, qreg, beta, red);
+    // a wave none of whose row tiles holds a real row keeps the schedule but does no work
+    bool real = false;
+    for (int rt = 0; rt < (nrt < kRowTilesPerWave ? nrt : kRowTilesPerWave); ++rt) {
+      int j, g;
+      score_row_query(G, grouped, c, w + kWaves * rt, lane & 15, &j, &g);
+      real = real || j < n;
+    }
+    if (__ballot(real) == 0ull) score_sweep_idle<D>(cx, kp, red);
+    else if (nrt >= 4) score_sweep16<D, kMaxMean, 4>(cx, kp, qreg, beta, red);
     else if (nrt == 3) score_sweep16<D, kMaxMean, 3>(cx, kp, qreg, beta, red);
     else if (nrt == 2) score_sweep16<D, kMaxMean, 2>(cx, kp, qreg, beta, red);
     else score_sweep16<D, kMaxMean, 1>(cx, kp, qreg, beta, red);
