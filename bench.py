@@ -281,12 +281,13 @@ def run_confidence(num_reqs, trace_len, reps, dev, stream):
         e[1].record(stream)
     trace = (torch.rand((num_reqs * trace_len,), generator=g, device=dev) * 2.0 + 8.0)
     offsets = np.arange(num_reqs + 1, dtype=np.int64) * trace_len
+    offsets_d = torch.from_numpy(offsets).to(dev)
     budgets = torch.full((num_reqs,), 512, dtype=torch.int32, device=dev)
     out = torch.empty_like(budgets)
     eb = _event_pairs(reps + 1)
     for e in eb:
         e[0].record(stream)
-        actkv.budget_update(trace, offsets, budgets, out=out)
+        actkv.budget_update(trace, offsets, budgets, out=out, offsets_d=offsets_d)
         e[1].record(stream)
     torch.cuda.synchronize()
     us = _mean_ms(ev) * 1e3

@@ -414,14 +414,21 @@ def token_confidence(logits: torch.Tensor, top_k: int = 20, out: Optional[torch.
 def budget_update(token_conf: torch.Tensor, offsets: np.ndarray, budgets: torch.Tensor,
                   window: int = 64, stride: int = 8, bottom_pct: float = 10.0,
                   scale_up: float = 1.75, budget_upper: int = 30000,
-                  out: Optional[torch.Tensor] = None, stream=None) -> dict:
+                  out: Optional[torch.Tensor] = None, stream=None,
+                  offsets_d: Optional[torch.Tensor] = None) -> dict:
     """Alg. 2 steps 2-4 for every request (token confidences concatenated, int64 offsets
-    [R + 1] on the host).  Returns the new budgets, slopes, thresholds and retained counts."""
+    [R + 1] on the host; offsets_d, when given, holds the same values on the device and
+    saves the copy).  Returns the new budgets, slopes, thresholds and retained counts."""
     lib = load_library()
     dev = budgets.device
     off_h = np.ascontiguousarray(offsets, dtype=np.int64)
     R = int(off_h.shape[0] - 1)
-    off_d = torch.from_numpy(off_h).to(dev)
+    if offsets_d is None:
+        off_d = torch.from_numpy(off_h).to(dev)
+    else:
+        if offsets_d.dtype != torch.int64 or offsets_d.numel() != R + 1:
+            raise ValueError("offsets_d must be int64 [R + 1] on the device")
+        off_d = offsets_d
     if out is None:
         out = torch.empty(max(R, 1), dtype=torch.int32, device=dev)
     slopes = torch.empty(max(R, 1), dtype=torch.float64, device=dev)

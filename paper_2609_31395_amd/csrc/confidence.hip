@@ -1,19 +1,28 @@
-// Confidence-driven budget allocation (Sec. 6.1 confidence monitor; Alg. 2).
+// confidence.hip -- the confidence monitor and the budget rule of ActKV's adaptive budget
+// allocation (Sec. 6.1; Alg. 2).
 //
-// Token confidence (Alg. 2 step 1, GetTokenConf): for one row of logits x over the
-// vocabulary, T = -(1/k) sum_{j<=k} log P(j) = LSE(x) - (1/k) sum of the k largest logits.
-//   token_conf_partial_kernel  one 256-thread workgroup per (row, chunk of <= 16384 logits):
-//                              an online (max, sum of exp) over the chunk, and the chunk's
-//                              k largest logits by a 4-pass radix select on order keys
-//                              staged in LDS (exact; emitted as a multiset)
-//   token_conf_merge_kernel    one workgroup per row: the chunks' (max, sum) combined in chunk
-//                              order, the candidates sorted (bitonic, LDS), the k largest
-//                              summed in fp64 in sorted order, T written as fp32
+// Token confidence (Sec. 6.1): T = LSE(x) - (1/k) * (sum of the k largest logits of x), one
+// row of logits per generated token.  Two kernels:
+//   token_conf_partial_kernel  one 256-thread workgroup per (row, chunk of <= 16384 logits),
+//                              64 logits per thread held in registers (all loads issued at
+//                              once): the chunk's max, then sum exp(x - max) (hardware exp2,
+//                              fixed order),
+//                              then the chunk's k largest logits exactly: the k-th largest of
+//                              the lanes' maxima in each wave bounds the answer from below,
+//                              the few logits above that bound go to LDS, and a bisection on
+//                              their order keys finds the k-th largest (a bisection over all
+//                              64 registers of every thread when the bound keeps too many,
+//                              e.g. a flat row); emitted as a multiset
+//   token_conf_merge_kernel    one wave per row: the chunks' sums rescaled to the row max
+//                              and added in chunk order, the k largest of the chunks' candidates by the same
+//                              bound and bisection, sorted across the lanes (bitonic) and
+//                              summed in fp64 in that order, T written as fp32
 // Trace confidence, trend and budget (Alg. 2 steps 2-4): budget_kernel, one 1024-thread
-// workgroup per request: min-pooled windows into LDS, the two order statistics of the
-// percentile by radix select, the retained windows compacted in window order (in place),
-// then one thread sums them in that order in fp64 with every operation rounded on its own,
-// so the slope -- and the integer decision it drives -- is reproducible bit for bit.
+// workgroup per request: min-pooled windows into LDS (from minima of gcd(w, s)-token blocks,
+// read once and coalesced), the two order statistics of the percentile by radix select, the
+// retained windows compacted in window order (in place), then one thread sums them in that
+// order in fp64 with every operation rounded on its own, so the slope -- and the integer
+// decision it drives -- is reproducible bit for bit.
 #include "device_common.hpp"
 
 namespace actkv {
@@ -21,51 +30,167 @@ namespace actkv {
 namespace {
 
 constexpr int kConfThreads = 256;
+constexpr int kConfWaves = kConfThreads / 64;
 constexpr int kConfChunk = kConfChunkLogits;
-constexpr int kConfMaxCand = kConfMaxSplits * kConfMaxTopK;   // 1024 merge candidates
+constexpr int kConfPerThread = kConfChunk / kConfThreads;       // 64 logits per thread
+constexpr int kConfCandCap = 2048;                               // LDS candidates per chunk
+constexpr int kConfMaxCand = kConfMaxSplits * kConfMaxTopK;      // 1024 merge candidates
+constexpr int kMergePerLane = kConfMaxCand / 64;
 constexpr int kBudgetThreads = 1024;
+// Word 3 of a raw buffer resource on CDNA: 32-bit data format; reads at byte offsets at or
+// past num_records return 0.
+constexpr int kBufferRsrcWord3 = 0x00020000;
+
+static_assert(kConfChunk % kConfThreads == 0, "whole rows of logits per thread");
+static_assert(kConfMaxTopK <= 64, "the k largest fit one wave, one per lane");
 
 __device__ __forceinline__ uint32_t order_key_f(float v) {
   const uint32_t u = __float_as_uint(v == 0.0f ? 0.0f : v);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
+// The same order with -0 just below +0 (no canonicalisation): three operations.
+__device__ __forceinline__ uint32_t order_key_raw(float v) {
+  const uint32_t u = __float_as_uint(v);
+  return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+}
 __device__ __forceinline__ float key_value_f(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
-// (m, s) <- the combination of two partial (max, sum of exp(x - max)) pairs.
-__device__ __forceinline__ void lse_combine(float& m, float& s, float m2, float s2) {
-  const float M = fmaxf(m, m2);
-  if (M == -__builtin_inff()) return;   // both empty
-  s = (m == -__builtin_inff() ? 0.0f : s * expf(m - M)) +
-      (m2 == -__builtin_inff() ? 0.0f : s2 * expf(m2 - M));
-  m = M;
+__device__ __forceinline__ float wave_max_f(float v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v = fmaxf(v, __shfl_xor(v, d, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum_f(float v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+  return v;
+}
+__device__ __forceinline__ int wave_sum_i(int v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_max_u(uint32_t v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, d, 64));
+  return v;
+}
+// Lanes below this one whose bit is set in `mask`.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-// Radix select on 32-bit keys key_of(i), i < n (read from LDS): the key of rank `need`
-// counted from the top (descending, need >= 1) or from the bottom (ascending), four 8-bit
-// digits, most significant first.  Returns the key; *left gets how many keys equal to it
-// are still needed.  nthreads threads; hist is 256 words; ctl 2 words.
-template <bool kDescending, typename KeyOf>
-__device__ uint32_t radix_rank(KeyOf key_of, int n, uint32_t need, uint32_t* hist,
-                               uint32_t* ctl, int nthreads, uint32_t* left) {
+// The largest t with at least `need` lanes of the wave holding a key >= t, need in [1, 64]
+// (0 when fewer than `need` lanes hold a key >= 1).
+__device__ __forceinline__ uint32_t wave_kth_key(uint32_t key, int need) {
+  uint32_t p = 0;
+#pragma unroll
+  for (int b = 31; b >= 0; --b) {
+    const uint32_t t = p | (1u << b);
+    if (__popcll(__ballot(key >= t)) >= need) p = t;
+  }
+  return p;
+}
+
+// min(v, v of the lane kCtrl names) for a DPP row shift; lanes whose source lies outside
+// their row of 16 keep v.
+template <int kCtrl>
+__device__ __forceinline__ uint32_t min_dpp(uint32_t v) {
+  return min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, kCtrl, 0xf, 0xf, false));
+}
+
+// The minimum of v over lanes [i, i + 2^kLg) reaches every lane i that is a multiple of
+// 2^kLg (kLg <= 6; other lanes get partial minima).  Within a row of 16 by DPP row shifts
+// left, across rows by lane shuffles.
+template <int kLg>
+__device__ __forceinline__ uint32_t group_min_to_leader(uint32_t v) {
+  if constexpr (kLg >= 1) v = min_dpp<0x101>(v);   // row_shl:1
+  if constexpr (kLg >= 2) v = min_dpp<0x102>(v);   // row_shl:2
+  if constexpr (kLg >= 3) v = min_dpp<0x104>(v);   // row_shl:4
+  if constexpr (kLg >= 4) v = min_dpp<0x108>(v);   // row_shl:8
+  if constexpr (kLg >= 5) v = min(v, (uint32_t)__shfl_down((int)v, 16, 64));
+  if constexpr (kLg >= 6) v = min(v, (uint32_t)__shfl_down((int)v, 32, 64));
+  return v;
+}
+
+// Start of a bisection for a key in [lo, hi]: *p gets the bits of hi above the highest bit
+// where lo and hi differ (zeros below, so *p <= lo); returns how many low bits remain open.
+__device__ __forceinline__ int open_bits(uint32_t lo, uint32_t hi, uint32_t* p) {
+  if (lo == hi) {
+    *p = hi;
+    return 0;
+  }
+  const int nb = 32 - __builtin_clz(lo ^ hi);
+  *p = nb == 32 ? 0u : hi & ~((1u << nb) - 1u);
+  return nb;
+}
+
+// tau = the largest key t >= *tau (whose bits above `nb` are set already) with at least
+// `need` of the C keys in cand (LDS) >= t, by bisection over the nb open bits; one wave.
+// Keys are read into registers once (R per lane) when C <= 64 * R.
+template <int R>
+__device__ __forceinline__ uint32_t bisect_regs(const uint32_t* cand, int C, int nb,
+                                                uint32_t tau, int need) {
+  const int lane = threadIdx.x & 63;
+  uint32_t c[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) c[r] = r * 64 + lane < C ? cand[r * 64 + lane] : 0u;
+  for (int b = nb - 1; b >= 0; --b) {
+    const uint32_t t = tau | (1u << b);   // >= 1: the 0 padding never counts
+    int cnt = 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) cnt += __popcll(__ballot(c[r] >= t));
+    if (cnt >= need) tau = t;
+  }
+  return tau;
+}
+__device__ __forceinline__ uint32_t bisect_lds(const uint32_t* cand, int C, int nb,
+                                               uint32_t tau, int need) {
+  const int lane = threadIdx.x & 63;
+  if (C <= 64) return bisect_regs<1>(cand, C, nb, tau, need);
+  if (C <= 128) return bisect_regs<2>(cand, C, nb, tau, need);
+  if (C <= 256) return bisect_regs<4>(cand, C, nb, tau, need);
+  for (int b = nb - 1; b >= 0; --b) {
+    const uint32_t t = tau | (1u << b);
+    int cnt = 0;
+    for (int i0 = 0; i0 < C; i0 += 64) {
+      const int i = i0 + lane;
+      cnt += __popcll(__ballot(i < C && cand[i] >= t));
+    }
+    if (cnt >= need) tau = t;
+  }
+  return tau;
+}
+
+// The key of rank `need` (>= 1, counted from the smallest) among key_of(i), i < n (read from
+// LDS), all of them in [base, base + span]: radix select on d = key - base, 8-bit digits
+// from the highest one that span needs (so the first pass spreads the keys over its bins).
+// Returns the key; *left gets how many keys equal to it are still needed.  nthreads
+// threads; hist is 256 words; ctl 2 words.
+template <typename KeyOf>
+__device__ __forceinline__ uint32_t radix_rank_asc(KeyOf key_of, int n, uint32_t need,
+                                                   uint32_t base, uint32_t span, uint32_t* hist,
+                                                   uint32_t* ctl, int nthreads, uint32_t* left) {
   const int tid = threadIdx.x;
+  const int bits = span == 0u ? 1 : 32 - __builtin_clz(span);
   uint32_t prefix = 0;
 #pragma unroll 1
-  for (int sh = 24; sh >= 0; sh -= 8) {
+  for (int sh = (bits - 1) / 8 * 8; sh >= 0; sh -= 8) {
     for (int b = tid; b < 256; b += nthreads) hist[b] = 0;
     __syncthreads();
     for (int i = tid; i < n; i += nthreads) {
-      const uint32_t dh = key_of(i) >> sh;   // this digit and the ones above it
+      const uint32_t dh = (key_of(i) - base) >> sh;   // this digit and the ones above it
       if ((dh >> 8) == prefix) atomicAdd(&hist[dh & 255u], 1u);
     }
     __syncthreads();
-    if (tid < 64) {   // wave 0: 4 bins per lane, scanned in selection order
+    if (tid < 64) {   // wave 0: 4 bins per lane, scanned from the smallest
       uint32_t c[4], tot = 0;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int bin = kDescending ? 255 - (tid * 4 + u) : tid * 4 + u;
-        c[u] = hist[bin];
+        c[u] = hist[tid * 4 + u];
         tot += c[u];
       }
       uint32_t incl = tot;
@@ -79,7 +204,7 @@ __device__ uint32_t radix_rank(KeyOf key_of, int n, uint32_t need, uint32_t* his
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           if (before < need && need <= before + c[u]) {
-            ctl[0] = kDescending ? 255 - (tid * 4 + u) : tid * 4 + u;
+            ctl[0] = tid * 4 + u;
             ctl[1] = before;
           }
           before += c[u];
@@ -87,12 +212,13 @@ __device__ uint32_t radix_rank(KeyOf key_of, int n, uint32_t need, uint32_t* his
       }
     }
     __syncthreads();
+    // the next pass clears hist and writes ctl only after its first two barriers, which
+    // every thread reaches after these reads
     prefix = (prefix << 8) | ctl[0];
     need -= ctl[1];
-    __syncthreads();
   }
   *left = need;
-  return prefix;
+  return base + prefix;
 }
 
 }  // namespace
@@ -100,97 +226,255 @@ __device__ uint32_t radix_rank(KeyOf key_of, int n, uint32_t need, uint32_t* his
 __global__ __launch_bounds__(kConfThreads) void token_conf_partial_kernel(
     const float* __restrict__ logits, int64_t vocab, int64_t row_stride, int k, int splits,
     float2* __restrict__ ms_out, float* __restrict__ top_out) {
-  __shared__ uint32_t keys[kConfChunk];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t ctl[4];
-  __shared__ float2 wred[kConfThreads / 64];
-  const int tid = threadIdx.x, split = blockIdx.x;
+  __shared__ uint32_t cand[kConfCandCap];
+  __shared__ float wred[kConfWaves];
+  __shared__ uint32_t wkey[kConfWaves];
+  __shared__ int wcnt[2][kConfWaves];
+  __shared__ uint32_t ctl[2];   // candidates found; entries above the k-th largest emitted
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, split = blockIdx.x;
   const int64_t row = blockIdx.y;
   const int64_t c0 = (int64_t)split * kConfChunk;
   const int n = (int)(vocab - c0 < kConfChunk ? vocab - c0 : kConfChunk);
-  const float* x = logits + row * row_stride + c0;
+  const int kk = k < n ? k : n;   // >= 1: every chunk holds a logit and k >= 1
+  const int64_t slot = row * splits + split;
+  float* top = top_out + slot * k;
   const float ninf = -__builtin_inff();
-  // pass 1: keys into LDS, online (max, sum)
-  float m = ninf, s = 0.0f;
-  for (int i = tid; i < n; i += kConfThreads) {
-    const float v = x[i];
-    keys[i] = order_key_f(v);
-    if (v > m) {
-      s = (m == ninf ? 0.0f : s * expf(m - v)) + 1.0f;
-      m = v;
-    } else if (v > ninf) {
-      s += expf(v - m);
+  if (tid == 0) {
+    ctl[0] = 0;
+    ctl[1] = 0;
+  }
+  for (int j = kk + tid; j < k; j += kConfThreads) top[j] = ninf;   // padding
+  // logit tid + j * 256 of the chunk in v[j]; the hardware returns 0 past the chunk
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(logits + row * row_stride + c0), (short)0, n * (int)sizeof(float),
+      kBufferRsrcWord3);
+  float v[kConfPerThread];
+#pragma unroll
+  for (int j = 0; j < kConfPerThread; ++j)
+    v[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                         rs, (tid + j * kConfThreads) * 4, 0, 0));
+  // past a short chunk: -inf, which changes neither the max nor the sum, and among the k
+  // largest stands only where -inf belongs anyway (kk <= n real logits)
+  if (n < kConfChunk) {
+#pragma unroll
+    for (int j = 0; j < kConfPerThread; ++j)
+      if (tid + j * kConfThreads >= n) v[j] = ninf;
+  }
+  // the chunk's max, then sum exp(x - max): each thread in j order, then a fixed tree
+  float m = ninf;
+#pragma unroll
+  for (int j = 0; j < kConfPerThread; ++j) m = fmaxf(m, v[j]);
+  m = wave_max_f(m);
+  if (lane == 0) wred[wv] = m;
+  __syncthreads();
+  float M = wred[0];
+#pragma unroll
+  for (int w = 1; w < kConfWaves; ++w) M = fmaxf(M, wred[w]);
+  // exp(x - M) as 2^((x - M) log2 e) on the hardware exp2 (error about 1 ulp; x = M gives
+  // exactly 1); -inf adds 0
+  float s = 0.0f;
+  if (M != ninf) {
+    constexpr float kLog2e = 1.4426950408889634f;
+#pragma unroll
+    for (int j = 0; j < kConfPerThread; ++j) s += fast_exp2((v[j] - M) * kLog2e);
+  }
+  s = wave_sum_f(s);
+  // order keys (all >= 1) and the lanes' maxima
+  uint32_t u[kConfPerThread];
+  uint32_t lm = 0;
+#pragma unroll
+  for (int j = 0; j < kConfPerThread; ++j) {
+    u[j] = order_key_raw(v[j]);
+    lm = max(lm, u[j]);
+  }
+  // a lower bound of the kk-th largest key: in the wave that gives it, kk lanes hold a key
+  // at least that large
+  const uint32_t tw = wave_kth_key(lm, kk);
+  __syncthreads();   // every thread has read the maxima
+  if (lane == 0) {
+    wred[wv] = s;
+    wkey[wv] = tw;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float S = wred[0];
+    for (int w = 1; w < kConfWaves; ++w) S += wred[w];
+    ms_out[slot] = make_float2(M, S);
+  }
+  uint32_t lo = 1;
+#pragma unroll
+  for (int w = 0; w < kConfWaves; ++w) lo = max(lo, wkey[w]);
+  // the keys >= lo into LDS (at least kk of them)
+#pragma unroll
+  for (int j = 0; j < kConfPerThread; ++j) {
+    const bool p = u[j] >= lo;
+    const uint64_t b = __ballot(p);
+    if (b != 0ull) {
+      uint32_t base = 0;
+      if (lane == 0) base = atomicAdd(&ctl[0], (uint32_t)__popcll(b));
+      base = (uint32_t)__shfl((int)base, 0, 64);
+      const uint32_t pos = base + lanes_below(b);
+      if (p && pos < (uint32_t)kConfCandCap) cand[pos] = u[j];
     }
+  }
+  __syncthreads();
+  const int C = (int)ctl[0];
+  const uint32_t hi = order_key_f(M);   // >= every key of the chunk (-0 and +0 included)
+  // tau = the largest key t with at least kk keys >= t.  Counting the candidates only gives
+  // the same answer for every t tested: above lo they are all the keys, at or below it there
+  // are C >= kk of them.
+  uint32_t tau;
+  int nb = open_bits(lo, hi, &tau);
+  if (C <= kConfCandCap) {
+    if (wv != 0) return;
+    tau = bisect_lds(cand, C, nb, tau, kk);
+    // the keys above tau (fewer than kk), then kk minus that many copies of tau
+    int g = 0;
+    for (int i0 = 0; i0 < C; i0 += 64) {
+      const int i = i0 + lane;
+      const uint32_t key = i < C ? cand[i] : 0u;
+      const bool above = key > tau;
+      const uint64_t b = __ballot(above);
+      if (above) top[g + (int)lanes_below(b)] = key_value_f(key);
+      g += __popcll(b);
+    }
+    for (int j = g + lane; j < kk; j += 64) top[j] = key_value_f(tau);
+    return;
+  }
+  // too many keys at the bound (a flat or heavily tied chunk): bisect over all of them
+  for (int b = nb - 1; b >= 0; --b) {
+    const uint32_t t = tau | (1u << b);
+    int c = 0;
+#pragma unroll
+    for (int j = 0; j < kConfPerThread; ++j) c += u[j] >= t ? 1 : 0;
+    c = wave_sum_i(c);
+    if (lane == 0) wcnt[b & 1][wv] = c;
+    __syncthreads();
+    int tot = 0;
+#pragma unroll
+    for (int w = 0; w < kConfWaves; ++w) tot += wcnt[b & 1][w];
+    if (tot >= kk) tau = t;
   }
 #pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) {
-    const float m2 = __shfl_xor(m, d, 64), s2 = __shfl_xor(s, d, 64);
-    lse_combine(m, s, m2, s2);
-  }
-  if ((tid & 63) == 0) wred[tid >> 6] = make_float2(m, s);
-  __syncthreads();
-  const int64_t slot = row * splits + split;
-  if (tid == 0) {
-    float M = wred[0].x, S = wred[0].y;
-    for (int w = 1; w < kConfThreads / 64; ++w) lse_combine(M, S, wred[w].x, wred[w].y);
-    ms_out[slot] = make_float2(M, S);
-    ctl[2] = 0;
-  }
-  // the chunk's kk = min(k, n) largest logits
-  const int kk = k < n ? k : n;
-  float* top = top_out + slot * k;
-  for (int j = kk + tid; j < k; j += kConfThreads) top[j] = ninf;   // padding
-  if (kk <= 0) return;
-  uint32_t left;
-  const uint32_t tau = radix_rank<true>([&](int i) { return keys[i]; }, n, (uint32_t)kk, hist,
-                                         ctl, kConfThreads, &left);
-  // every key above tau, then `left` copies of tau (a multiset: order is irrelevant)
-  for (int i = tid; i < n; i += kConfThreads)
-    if (keys[i] > tau) top[atomicAdd(&ctl[2], 1u)] = key_value_f(keys[i]);
-  __syncthreads();
-  const int gt = (int)ctl[2];
-  for (int j = tid; j < (int)left; j += kConfThreads) top[gt + j] = key_value_f(tau);
-}
-
-__global__ __launch_bounds__(kConfThreads) void token_conf_merge_kernel(
-    const float2* __restrict__ ms, const float* __restrict__ top_in, int k, int splits,
-    int64_t vocab, float* __restrict__ conf) {
-  __shared__ float cand[kConfMaxCand];
-  const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;
-  const int nc = splits * k;
-  int p2 = 1;
-  while (p2 < nc) p2 <<= 1;
-  for (int i = tid; i < p2; i += kConfThreads)
-    cand[i] = i < nc ? top_in[row * nc + i] : -__builtin_inff();
-  __syncthreads();
-  // bitonic sort, descending
-  for (int size = 2; size <= p2; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = tid; i < p2 / 2; i += kConfThreads) {
-        const int lo = 2 * i - (i & (stride - 1));
-        const int hi = lo + stride;
-        const bool desc = (lo & size) == 0;
-        const float a = cand[lo], b = cand[hi];
-        if (desc ? (a < b) : (a > b)) { cand[lo] = b; cand[hi] = a; }
-      }
-      __syncthreads();
+  for (int j = 0; j < kConfPerThread; ++j) {
+    const bool above = u[j] > tau;
+    const uint64_t b = __ballot(above);
+    if (b != 0ull) {
+      uint32_t base = 0;
+      if (lane == 0) base = atomicAdd(&ctl[1], (uint32_t)__popcll(b));
+      base = (uint32_t)__shfl((int)base, 0, 64);
+      if (above) top[base + lanes_below(b)] = key_value_f(u[j]);
     }
   }
-  if (tid == 0) {
-    float M = -__builtin_inff(), S = 0.0f;
-    for (int c = 0; c < splits; ++c) lse_combine(M, S, ms[row * splits + c].x, ms[row * splits + c].y);
+  __syncthreads();
+  for (int j = (int)ctl[1] + tid; j < kk; j += kConfThreads) top[j] = key_value_f(tau);
+}
+
+__global__ __launch_bounds__(64) void token_conf_merge_kernel(
+    const float2* __restrict__ ms, const float* __restrict__ top_in, int k, int splits,
+    int64_t vocab, float* __restrict__ conf) {
+  __shared__ uint32_t cand[kConfMaxCand];
+  __shared__ float best[64];
+  const int lane = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const int nc = splits * k;   // <= kConfMaxCand
+  const float* in = top_in + row * nc;
+  const float ninf = -__builtin_inff();
+  // the k largest logits of the row are the kk = min(k, vocab) largest candidates: every
+  // chunk contributed its own min(k, chunk) largest, padded with -inf
+  const int kk = (int64_t)k < vocab ? k : (int)vocab;
+  const float2 msl = lane < splits ? ms[row * splits + lane] : make_float2(ninf, 0.0f);
+  uint32_t u[kMergePerLane];
+  uint32_t lm = 0;
+#pragma unroll
+  for (int s = 0; s < kMergePerLane; ++s) {
+    const int i = s * 64 + lane;
+    u[s] = i < nc ? order_key_f(in[i]) : 0u;
+    lm = max(lm, u[s]);
+  }
+  const uint32_t hi = wave_max_u(lm);
+  const uint32_t lo = max(wave_kth_key(lm, kk), 1u);
+  int C = 0;
+#pragma unroll
+  for (int s = 0; s < kMergePerLane; ++s) {
+    const bool p = u[s] >= lo;
+    const uint64_t b = __ballot(p);
+    if (p) cand[C + (int)lanes_below(b)] = u[s];
+    C += __popcll(b);
+  }
+  __syncthreads();
+  uint32_t tau;
+  const int nb = open_bits(lo, hi, &tau);
+  tau = bisect_lds(cand, C, nb, tau, kk);
+  int g = 0;
+  for (int i0 = 0; i0 < C; i0 += 64) {
+    const int i = i0 + lane;
+    const uint32_t key = i < C ? cand[i] : 0u;
+    const bool above = key > tau;
+    const uint64_t b = __ballot(above);
+    if (above) best[g + (int)lanes_below(b)] = key_value_f(key);
+    g += __popcll(b);
+  }
+  __syncthreads();
+  // one of the kk largest per lane, then a bitonic sort across the lanes, descending
+  float x = lane < g ? best[lane] : (lane < kk ? key_value_f(tau) : ninf);
+#pragma unroll
+  for (int size = 2; size <= 64; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      const float o = __shfl_xor(x, stride, 64);
+      const bool keep_max = ((lane & stride) == 0) == ((lane & size) == 0);
+      x = keep_max ? fmaxf(x, o) : fminf(x, o);
+    }
+  }
+  // the row's log-sum-exp: lane c holds chunk c's (max, sum); terms rescaled to the row max
+  // and added in chunk order
+  const float M = wave_max_f(msl.x);
+  const float term = M == ninf || msl.x == ninf ? 0.0f : msl.y * expf(msl.x - M);
+  float S = 0.0f;
+  for (int c = 0; c < splits; ++c)
+    S += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(term), c));
+  double sum = 0.0;
+  for (int j = 0; j < kk; ++j)
+    sum += (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), j));
+  if (lane == 0) {
     const double lse = (double)M + log((double)S);
-    // the k largest logits of the row are the first min(k, vocab) candidates in sorted order
-    // (every chunk contributed its own min(k, chunk) largest; padding sorts last)
-    const int kk = (int64_t)k < vocab ? k : (int)vocab;
-    double sum = 0.0;
-    for (int j = 0; j < kk; ++j) sum += (double)cand[j];
     conf[row] = (float)(lse - sum / (double)kk);
   }
 }
 
 // ---- Alg. 2 steps 2-4 -------------------------------------------------------------------
+constexpr int kBudgetTokBatch = 32;   // trace tokens in flight per thread
+
+// bkey[j] = the smallest order key of t[j g .. (j + 1) g), j < ntok / g, from one coalesced
+// pass over t[0 .. ntok).  kLg >= 0: g = 2^kLg <= 64, a block sits in g consecutive lanes
+// of one batch (its first token at a multiple of g), reduced across them and stored by the
+// first; kLg < 0: any g, LDS atomics (bkey set to all ones beforehand).
+template <int kLg>
+__device__ __forceinline__ void block_minima(const float* __restrict__ t, int ntok, int g,
+                                             uint32_t* bkey) {
+  const int tid = threadIdx.x;
+  for (int e0 = 0; e0 < ntok; e0 += kBudgetThreads * kBudgetTokBatch) {
+    float v[kBudgetTokBatch];
+#pragma unroll
+    for (int u = 0; u < kBudgetTokBatch; ++u) {
+      const int e = e0 + u * kBudgetThreads + tid;
+      v[u] = e < ntok ? t[e] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < kBudgetTokBatch; ++u) {
+      const int e = e0 + u * kBudgetThreads + tid;
+      uint32_t kv = e < ntok ? order_key_f(v[u]) : 0xFFFFFFFFu;
+      if constexpr (kLg >= 0) {
+        kv = group_min_to_leader<kLg>(kv);
+        if (e < ntok && (e & ((1 << kLg) - 1)) == 0) bkey[e >> kLg] = kv;
+      } else {
+        if (e < ntok) atomicMin(&bkey[e / g], kv);
+      }
+    }
+  }
+}
+
 __global__ __launch_bounds__(kBudgetThreads) void budget_kernel(
     const float* __restrict__ tconf, const int64_t* __restrict__ offsets, int window,
     int stride, float bottom_pct, float scale_up, int budget_upper,
@@ -198,32 +482,91 @@ __global__ __launch_bounds__(kBudgetThreads) void budget_kernel(
     double* __restrict__ slopes, double* __restrict__ thresholds, int32_t* __restrict__ retained) {
 #pragma clang fp contract(off)
   __shared__ float rp[kMaxBudgetWindows];       // R'_m, then the retained values in order
-  __shared__ int32_t rm[kMaxBudgetWindows];     // window index of each retained value
+  __shared__ int32_t rm[kMaxBudgetWindows];     // block minima (as keys), then window indices
+  __shared__ double2 pq[kBudgetThreads];        // products of the slope's sums, one batch
   __shared__ uint32_t hist[256];
   __shared__ uint32_t ctl[4];
   __shared__ int64_t scan_tmp[17];
-  __shared__ uint32_t mm_tmp[kBudgetThreads / 64];
-  const int r = blockIdx.x, tid = threadIdx.x;
+  __shared__ uint32_t mm_tmp[2][kBudgetThreads / 64];
+  __shared__ double mean_tmp[2];
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int64_t n = offsets[r + 1] - offsets[r];
   const float* t = tconf + offsets[r];
   double alpha = 0.0, q = __builtin_nan("");
   int kept = 0;
   if (n >= window) {
     const int M = (int)((n - window) / stride + 1);
-    for (int m = tid; m < M; m += kBudgetThreads) {
-      float v = t[(int64_t)m * stride];
-      for (int i = 1; i < window; ++i) v = fminf(v, t[(int64_t)m * stride + i]);
-      rp[m] = v;
+    // windows are whole blocks of g = gcd(w, s) tokens: the minima of the blocks the windows
+    // cover, from one coalesced pass over those tokens, then each window's minimum over its
+    // w / g blocks in LDS.  Minima are taken on order keys (-0 and +0 alike).
+    int g = window, b = stride;
+    while (b != 0) {
+      const int r0 = g % b;
+      g = b;
+      b = r0;
+    }
+    const int64_t nbl = ((int64_t)(M - 1) * stride + window) / g;
+    if (nbl <= kMaxBudgetWindows && nbl * g < (int64_t)1 << 30) {
+      uint32_t* bkey = reinterpret_cast<uint32_t*>(rm);
+      const int ntok = (int)nbl * g;   // <= n
+      switch ((g & (g - 1)) == 0 && g <= 64 ? __builtin_ctz(g) : -1) {
+        case 0: block_minima<0>(t, ntok, g, bkey); break;
+        case 1: block_minima<1>(t, ntok, g, bkey); break;
+        case 2: block_minima<2>(t, ntok, g, bkey); break;
+        case 3: block_minima<3>(t, ntok, g, bkey); break;
+        case 4: block_minima<4>(t, ntok, g, bkey); break;
+        case 5: block_minima<5>(t, ntok, g, bkey); break;
+        case 6: block_minima<6>(t, ntok, g, bkey); break;
+        default:
+          for (int j = tid; j < (int)nbl; j += kBudgetThreads) bkey[j] = 0xFFFFFFFFu;
+          __syncthreads();
+          block_minima<-1>(t, ntok, g, bkey);
+      }
+      __syncthreads();
+      const int wb = window / g, sb = stride / g;
+      for (int m = tid; m < M; m += kBudgetThreads) {
+        uint32_t kv = bkey[m * sb];
+        for (int i = 1; i < wb; ++i) kv = min(kv, bkey[m * sb + i]);
+        rp[m] = key_value_f(kv);
+      }
+    } else {
+      for (int m = tid; m < M; m += kBudgetThreads) {
+        float v = t[(int64_t)m * stride];
+        for (int i = 1; i < window; ++i) v = fminf(v, t[(int64_t)m * stride + i]);
+        rp[m] = v;
+      }
     }
     __syncthreads();
+    // the range of the window keys, for the radix select
+    uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+    for (int m = tid; m < M; m += kBudgetThreads) {
+      const uint32_t km = order_key_f(rp[m]);
+      kmin = min(kmin, km);
+      kmax = max(kmax, km);
+    }
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+      kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, d, 64));
+      kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, d, 64));
+    }
+    if (lane == 0) {
+      mm_tmp[0][wv] = kmin;
+      mm_tmp[1][wv] = kmax;
+    }
+    __syncthreads();
+    for (int w = 0; w < kBudgetThreads / 64; ++w) {
+      kmin = min(kmin, mm_tmp[0][w]);
+      kmax = max(kmax, mm_tmp[1][w]);
+    }
+    __syncthreads();   // mm_tmp is written again below
     // percentile: order statistics lo and lo + 1 (ascending), linear interpolation
     const double pos = ((double)bottom_pct / 100.0) * (double)(M - 1);
     const int lo = (int)floor(pos);
     const double frac = pos - (double)lo;
     uint32_t left;
     auto key_of = [&](int i) { return order_key_f(rp[i]); };
-    const uint32_t klo = radix_rank<false>(key_of, M, (uint32_t)lo + 1u, hist, ctl,
-                                           kBudgetThreads, &left);
+    const uint32_t klo = radix_rank_asc(key_of, M, (uint32_t)lo + 1u, kmin, kmax - kmin, hist,
+                                        ctl, kBudgetThreads, &left);
     const double vlo = (double)key_value_f(klo);
     double vhi = vlo;
     if (lo + 1 < M) {
@@ -238,9 +581,9 @@ __global__ __launch_bounds__(kBudgetThreads) void budget_kernel(
       block_excl_scan_i64(cnt_le, scan_tmp, &tot);
 #pragma unroll
       for (int d = 32; d >= 1; d >>= 1) next = min(next, (uint32_t)__shfl_xor((int)next, d, 64));
-      if ((tid & 63) == 0) mm_tmp[tid >> 6] = next;
+      if (lane == 0) mm_tmp[0][wv] = next;
       __syncthreads();
-      for (int w = 0; w < kBudgetThreads / 64; ++w) next = min(next, mm_tmp[w]);
+      for (int w = 0; w < kBudgetThreads / 64; ++w) next = min(next, mm_tmp[0][w]);
       vhi = tot >= (int64_t)lo + 2 ? vlo : (double)key_value_f(next);
       q = vlo + frac * (vhi - vlo);
     } else {
@@ -253,10 +596,13 @@ __global__ __launch_bounds__(kBudgetThreads) void budget_kernel(
     constexpr int kMaxPer = kMaxBudgetWindows / kBudgetThreads;
     float yv[kMaxPer];
     uint32_t cnt = 0;
+    int64_t msum = 0;
 #pragma unroll
     for (int u = 0; u < kMaxPer; ++u) {
       yv[u] = m0 + u < m1 ? rp[m0 + u] : 0.0f;
-      cnt += (m0 + u < m1 && (double)yv[u] <= q) ? 1u : 0u;
+      const bool keep = m0 + u < m1 && (double)yv[u] <= q;
+      cnt += keep ? 1u : 0u;
+      msum += keep ? m0 + u : 0;
     }
     int64_t total;
     int64_t at = block_excl_scan_i64(cnt, scan_tmp, &total);   // its barriers retire the reads
@@ -267,20 +613,60 @@ __global__ __launch_bounds__(kBudgetThreads) void budget_kernel(
         rm[at] = m0 + u;
         ++at;
       }
-    __syncthreads();
+    int64_t sxi;
+    block_excl_scan_i64(msum, scan_tmp, &sxi);   // its first barrier orders the writes too
     kept = (int)total;
-    if (tid == 0 && kept >= 2) {   // least squares in window order
-      double sx = 0.0, sy = 0.0;
-      for (int i = 0; i < kept; ++i) {
-        sx = sx + (double)rm[i];
-        sy = sy + (double)rp[i];
+    if (kept >= 2) {
+      // least squares in window order, every operation rounded on its own.  Sum of m: an
+      // integer below 2^53 at every step, so the exact integer sum is the fp64 sum in any
+      // order.  Sum of R': one thread, in order.  The products of the second pass do not
+      // depend on the order, so the block forms them, 1024 at a time, and one thread adds
+      // them up in order.
+      if (tid == 0) {
+        constexpr int kB = 16;
+        double sy = 0.0;
+        int i0 = 0;
+        for (; i0 + kB <= kept; i0 += kB) {
+          float y[kB];
+#pragma unroll
+          for (int u = 0; u < kB; ++u) y[u] = rp[i0 + u];
+#pragma unroll
+          for (int u = 0; u < kB; ++u) sy = sy + (double)y[u];
+        }
+        for (; i0 < kept; ++i0) sy = sy + (double)rp[i0];
+        mean_tmp[0] = (double)sxi / (double)kept;
+        mean_tmp[1] = sy / (double)kept;
       }
-      const double mx = sx / (double)kept, my = sy / (double)kept;
+      __syncthreads();
+      const double mx = mean_tmp[0], my = mean_tmp[1];
       double num = 0.0, den = 0.0;
-      for (int i = 0; i < kept; ++i) {
-        const double dx = (double)rm[i] - mx, dy = (double)rp[i] - my;
-        num = num + dx * dy;
-        den = den + dx * dx;
+      for (int b0 = 0; b0 < kept; b0 += kBudgetThreads) {
+        const int i = b0 + tid;
+        if (i < kept) {
+          const double dx = (double)rm[i] - mx, dy = (double)rp[i] - my;
+          pq[tid] = make_double2(dx * dy, dx * dx);
+        }
+        __syncthreads();
+        if (tid == 0) {
+          const int cb = kept - b0 < kBudgetThreads ? kept - b0 : kBudgetThreads;
+          constexpr int kB = 8;
+          int j0 = 0;
+          for (; j0 + kB <= cb; j0 += kB) {
+            double2 a[kB];
+#pragma unroll
+            for (int u = 0; u < kB; ++u) a[u] = pq[j0 + u];
+#pragma unroll
+            for (int u = 0; u < kB; ++u) {
+              num = num + a[u].x;
+              den = den + a[u].y;
+            }
+          }
+          for (; j0 < cb; ++j0) {
+            num = num + pq[j0].x;
+            den = den + pq[j0].y;
+          }
+        }
+        __syncthreads();
       }
       alpha = num / den;
     }
@@ -309,7 +695,7 @@ hipError_t launch_token_confidence(const float* logits, int64_t rows, int64_t vo
                      0, s, logits, vocab, row_stride, k, splits, ms, top);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(token_conf_merge_kernel, dim3((unsigned)rows), dim3(kConfThreads), 0, s, ms,
+  hipLaunchKernelGGL(token_conf_merge_kernel, dim3((unsigned)rows), dim3(64), 0, s, ms,
                      top, k, splits, vocab, conf);
   return hipGetLastError();
 }

@@ -46,6 +46,26 @@ def test_token_confidence_matches_the_oracle(vocab, k):
     np.testing.assert_allclose(got, ref, rtol=1e-6, atol=1e-5)
 
 
+@pytest.mark.parametrize("k", [1, 20, 64])
+def test_token_confidence_on_flat_and_few_valued_rows(k):
+    """Rows where thousands of logits tie at the k-th largest value (a flat row, three
+    distinct values, a row masked but for a few tokens, zeros of both signs): the exact
+    top-k then cannot come from a short candidate list and is found over the whole chunk."""
+    V = 151936
+    rng = np.random.default_rng(k)
+    x = np.empty((5, V), np.float32)
+    x[0] = 3.25
+    x[1] = rng.integers(0, 3, V).astype(np.float32)
+    x[2] = -np.inf
+    x[2, rng.choice(V, 5, replace=False)] = rng.standard_normal(5).astype(np.float32)
+    x[3] = np.where(rng.random(V) < 0.5, 7.0, rng.standard_normal(V)).astype(np.float32)
+    x[4] = np.where(rng.random(V) < 0.5, np.float32(-0.0), np.float32(0.0))   # signed zeros
+    x[4, rng.random(V) < 0.3] = -1.0
+    got = actkv.token_confidence(torch.from_numpy(x).cuda(), top_k=k).cpu().numpy()
+    ref = oracle.token_confidence(x, k)
+    np.testing.assert_allclose(got, ref, rtol=1e-6, atol=1e-5)
+
+
 def test_token_confidence_with_row_stride():
     rng = np.random.default_rng(1)
     x = rng.standard_normal((4, 5000)).astype(np.float32)
@@ -68,7 +88,12 @@ def _seqs(rng):
 
 @pytest.mark.parametrize("params", [dict(), dict(window=2, stride=1, bottom_pct=50.0),
                                     dict(window=16, stride=16, bottom_pct=0.0),
-                                    dict(bottom_pct=100.0, scale_up=1.0, budget_upper=600)])
+                                    dict(bottom_pct=100.0, scale_up=1.0, budget_upper=600),
+                                    # blocks of gcd(w, s) tokens: 32 and 64 (lane groups
+                                    # across rows of 16), 3 and 128 (not lane groups)
+                                    dict(window=64, stride=32), dict(window=128, stride=64),
+                                    dict(window=24, stride=9, bottom_pct=25.0),
+                                    dict(window=256, stride=128, bottom_pct=30.0)])
 def test_budget_update_is_bit_exact(params):
     rng = np.random.default_rng(7)
     w, st = params.get("window", 64), params.get("stride", 8)
@@ -108,7 +133,8 @@ def test_monitor_end_to_end_over_decode_steps():
     offsets = np.concatenate([[0], np.cumsum([s.size for s in seqs])]).astype(np.int64)
     budgets = np.full(R, 512, np.int32)
     got = actkv.budget_update(torch.from_numpy(np.concatenate(seqs)).cuda(), offsets,
-                              torch.from_numpy(budgets).cuda())
+                              torch.from_numpy(budgets).cuda(),
+                              offsets_d=torch.from_numpy(offsets).cuda())
     ref = oracle.budget_update(seqs, budgets)
     np.testing.assert_array_equal(got["budgets"].cpu().numpy(), ref["budgets"])
     np.testing.assert_array_equal(got["slopes"].cpu().numpy().view(np.int64),
