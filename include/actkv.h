@@ -141,7 +141,10 @@ actkv_status actkv_score(const actkv_problem* p, const void* q, const void* kv_c
  * aligned; when a sequence grows between steps the caller extends its segment with zeros
  * for the new entries.  n steps of one query each add up to one actkv_score call with all
  * n queries (SUM; with MAX_MEAN each step adds max over the group, so acc / n is the
- * running mean of Sec. 7.1).  The step's scores pass through the workspace.
+ * running mean of Sec. 7.1).  A call with at most one query per request (a decode step)
+ * and a group of at most 16 query heads is scored and added in one pass; otherwise the
+ * step's scores pass through the workspace.  Either way each entry of acc is updated by
+ * exactly one thread (no atomics): results do not depend on scheduling.
  */
 actkv_status actkv_score_accumulate(const actkv_problem* p, const void* q, const void* kv_cache,
                                     const int32_t* block_table, const float* lse, float* acc,

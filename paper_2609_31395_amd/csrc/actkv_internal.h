@@ -43,6 +43,7 @@ struct HostPlan {
   int64_t lse_parts = 0;          // sum_r n_r * Hq * lse_blocks_r
   int64_t max_lse_blocks = 0;     // max_r ceil(L_r / kLseKeysPerBlock)
   int64_t max_L = 0;              // longest request
+  int64_t max_n = 0;              // most action queries of one request
 };
 
 // Byte offsets of the workspace regions (each 256-byte aligned).
@@ -110,6 +111,12 @@ hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
                         float* score_part, hipStream_t s);
 // acc[i] += s[i], i < n (both 16-byte aligned or n handled element-wise at the tail).
 hipError_t launch_accumulate(float* acc, const float* s, int64_t n, hipStream_t st);
+// Decode-step scoring added straight into acc: every request has at most one action query
+// and G <= kDecodeMaxGroup (the caller checks).
+constexpr int kDecodeMaxGroup = 16;
+hipError_t launch_score_decode(const DevProblem& dp, const HostPlan& hp, const void* q,
+                               const void* kv, const int32_t* bt, const float* lse, float* acc,
+                               hipStream_t s);
 hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
                          float* pooled, int32_t* kept, hipStream_t s);
 // LRFU selection (attention-aware keep scores): segments up to kLrfuMaxLen entries.

@@ -70,6 +70,7 @@ actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
     hp->sum_n += n;
     hp->sum_L += L;
     hp->max_L = L > hp->max_L ? L : hp->max_L;
+    hp->max_n = n > hp->max_n ? n : hp->max_n;
     const int64_t ntiles = (L + actkv::kKeyTile - 1) / actkv::kKeyTile;
     const int64_t M = n * G;
     const int32_t chunks = M > 0 ? (int32_t)((M + actkv::kRowsPerChunk - 1) / actkv::kRowsPerChunk) : 1;
@@ -208,6 +209,18 @@ actkv_status actkv_score_accumulate(const actkv_problem* p, const void* q, const
   if (cx.hp.R == 0 || cx.hp.num_scores == 0) return ACTKV_OK;
   st = hip_status(actkv::launch_plan(cx.dp, s));
   if (st != ACTKV_OK) return st;
+  if (cx.hp.max_n <= 1 && cx.hp.G <= actkv::kDecodeMaxGroup) {
+    // a decode step (one action query per request at most): scored and added in one pass
+    if (cx.hp.sum_n == 0) return ACTKV_OK;
+    if (!lse) {
+      float* lse_ws = reinterpret_cast<float*>(cx.base + cx.ws.lse);
+      st = run_lse(cx, q, kv_cache, block_table, lse_ws, s);
+      if (st != ACTKV_OK) return st;
+      lse = lse_ws;
+    }
+    return hip_status(actkv::launch_score_decode(cx.dp, cx.hp, q, kv_cache, block_table, lse,
+                                                 acc, s));
+  }
   float* step_scores = reinterpret_cast<float*>(cx.base + cx.ws.scores);
   st = run_score(cx, q, kv_cache, block_table, lse, step_scores, s);
   if (st != ACTKV_OK) return st;

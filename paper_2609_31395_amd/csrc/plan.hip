@@ -5,8 +5,43 @@
 
 namespace actkv {
 
+namespace {
+
+// Exclusive prefix sums of N values at once over the block (blockDim.x a multiple of 64,
+// <= 1024): wave scans, then every thread adds up the totals of the waves before its own
+// (broadcast LDS reads).  v is replaced by its exclusive prefix, tot gets the block sums.
+template <int N>
+__device__ __forceinline__ void block_excl_scan_n(int64_t (&v)[N], int64_t (*tmp)[N],
+                                                  int64_t (&tot)[N]) {
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  const int nw = blockDim.x / kWave;
+  int64_t inc[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) inc[i] = wave_incl_scan_i64(v[i]);
+  if (lane == kWave - 1) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) tmp[w][i] = inc[i];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    int64_t before = 0, all = 0;
+    for (int u = 0; u < nw; ++u) {
+      const int64_t t = tmp[u][i];
+      before += u < w ? t : 0;
+      all += t;
+    }
+    tot[i] = all;
+    v[i] = before + inc[i] - v[i];
+  }
+  __syncthreads();   // tmp is written again by the next call
+}
+
+}  // namespace
+
 __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
-  __shared__ int64_t tmp[17];
+  constexpr int kScans = 8;
+  __shared__ int64_t tmp[1024 / kWave][kScans];
   const int R = dp.R, Hkv = dp.Hkv, G = dp.G, C = dp.max_chunks;
   int64_t carry_n = 0, carry_L = 0, carry_X = 0, carry_Y = 0, carry_k = 0, carry_cost = 0,
           carry_lse = 0, carry_ip = 0;
@@ -19,12 +54,20 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
       L = dp.seq_lens[r];
       n = dp.q_lens[r];
       int32_t kmax = 0, bmin = INT32_MAX;
-      for (int h = 0; h < Hkv; ++h) {
-        const int32_t b = dp.budgets[r * Hkv + h];
-        const int32_t k = b < L ? b : L;
-        ksum += k;
-        kmax = k > kmax ? k : kmax;
-        bmin = b < bmin ? b : bmin;
+      // budgets 8 at a time, every load of a batch issued before any is used
+      for (int h0 = 0; h0 < Hkv; h0 += 8) {
+        int32_t bb[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) bb[u] = h0 + u < Hkv ? dp.budgets[r * Hkv + h0 + u] : INT32_MAX;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (h0 + u >= Hkv) break;
+          const int32_t b = bb[u];
+          const int32_t k = b < L ? b : L;
+          ksum += k;
+          kmax = k > kmax ? k : kmax;
+          bmin = b < bmin ? b : bmin;
+        }
       }
       skip = bmin >= L;
       X = skip ? 0 : ceil_div(kmax, kPageSize);
@@ -39,17 +82,15 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
       }
       lse_blocks = (int32_t)ceil_div64(L, kLseKeysPerBlock);
     }
-    int64_t tot;
-    const int64_t q_off = carry_n + block_excl_scan_i64(n, tmp, &tot); carry_n += tot;
-    const int64_t seg_off = carry_L + block_excl_scan_i64((int64_t)L * Hkv, tmp, &tot); carry_L += tot;
-    const int64_t x_off = carry_X + block_excl_scan_i64(X, tmp, &tot); carry_X += tot;
-    const int64_t y_off = carry_Y + block_excl_scan_i64(Y, tmp, &tot); carry_Y += tot;
-    const int64_t k_off = carry_k + block_excl_scan_i64(ksum, tmp, &tot); carry_k += tot;
-    const int64_t c_off = carry_cost + block_excl_scan_i64(cost, tmp, &tot); carry_cost += tot;
-    const int64_t l_off = carry_lse + block_excl_scan_i64((int64_t)n * dp.Hq * lse_blocks, tmp, &tot);
-    carry_lse += tot;
-    const int64_t f_off = carry_ip + block_excl_scan_i64(Y - X, tmp, &tot);
-    carry_ip += tot;
+    int64_t sv[kScans] = {n, (int64_t)L * Hkv, X, Y, ksum, cost, (int64_t)n * dp.Hq * lse_blocks,
+                          Y - X};
+    int64_t tot[kScans];
+    block_excl_scan_n<kScans>(sv, tmp, tot);
+    const int64_t q_off = carry_n + sv[0], seg_off = carry_L + sv[1], x_off = carry_X + sv[2],
+                  y_off = carry_Y + sv[3], k_off = carry_k + sv[4], c_off = carry_cost + sv[5],
+                  l_off = carry_lse + sv[6], f_off = carry_ip + sv[7];
+    carry_n += tot[0]; carry_L += tot[1]; carry_X += tot[2]; carry_Y += tot[3];
+    carry_k += tot[4]; carry_cost += tot[5]; carry_lse += tot[6]; carry_ip += tot[7];
     if (ok) {
       ReqPlan p;
       p.L = L; p.n = n; p.X = X; p.Y = Y; p.skip = skip; p.nchunk = nchunk;
@@ -59,10 +100,16 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
       dp.plan[r] = p;
       // kept offsets per (r, h)
       int64_t ko = k_off;
-      for (int h = 0; h < Hkv; ++h) {
-        dp.kept_off[r * Hkv + h] = ko;
-        const int32_t b = dp.budgets[r * Hkv + h];
-        ko += b < L ? b : L;
+      for (int h0 = 0; h0 < Hkv; h0 += 8) {
+        int32_t bb[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) bb[u] = h0 + u < Hkv ? dp.budgets[r * Hkv + h0 + u] : 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (h0 + u >= Hkv) break;
+          dp.kept_off[r * Hkv + h0 + u] = ko;
+          ko += bb[u] < L ? bb[u] : L;
+        }
       }
       // scoring cost prefix per segment (r, c, h), c < max_chunks
       const int M = G * n;
@@ -87,7 +134,10 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
 }
 
 hipError_t launch_plan(const DevProblem& dp, hipStream_t s) {
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, dp);
+  // one workgroup; as many waves as the requests need (a scan step per 1024 requests)
+  int threads = (dp.R + kWave - 1) / kWave * kWave;
+  threads = threads < kWave ? kWave : (threads > 1024 ? 1024 : threads);
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(threads), 0, s, dp);
   return hipGetLastError();
 }
 

@@ -22,6 +22,8 @@
 //   * A lane's accumulator column is one key and 4 query rows, so the row sum is in-lane;
 //     the 4 lane groups and 8 waves are combined through LDS in a fixed order (no
 //     atomics: deterministic, and independent of where the pages physically live).
+#include <atomic>
+
 #include "device_common.hpp"
 
 namespace actkv {
@@ -757,6 +759,197 @@ hipError_t launch_accumulate(float* acc, const float* s, int64_t n, hipStream_t 
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(accumulate_kernel, dim3((unsigned)blocks), dim3(256), 0, st, acc, s, n);
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------
+// Decode-step scoring (one action query per request: Alg. 3 as run once per generated
+// token).  The G <= 16 query rows of a KV head fill one 16-row MFMA tile (rows past G are
+// zero with beta = +inf).  A wave streams whole pages of its head's K (16 keys) from global
+// memory straight into the MFMA B operand, kDecRing pages in flight, and keeps the pages'
+// scores in LDS; every kDecFlushPages pages it adds them to the aggregate with contiguous
+// 256-byte loads and stores.  (A store inside the page loop would make every later wait for
+// a K load wait for the store as well.)  The waves of a workgroup are the KV heads (up to
+// 8 per workgroup, head groups along y) and walk the same pages: a page's heads are
+// interleaved in memory (slot-major rows), so reading them at about the same time keeps the
+// DRAM accesses of a page together.  Workgroups take equal contiguous shares of the
+// (request, 64-key tile) list.  Bound by reading K; no barriers.
+// ---------------------------------------------------------------------------------------
+constexpr int kDecMaxWaves = 8;      // KV heads per workgroup
+constexpr int kDecRing = 4;          // pages of K in flight per wave
+constexpr int kDecFlushPages = 64;   // pages whose scores a wave holds in LDS
+
+template <int D, bool kMaxMean>
+__global__ __launch_bounds__(kDecMaxWaves * 64) void score_decode_kernel(
+    DevProblem dp, const uint16_t* __restrict__ q_ptr, const char* __restrict__ kv_bytes,
+    const int32_t* __restrict__ bt_ptr, const float* __restrict__ lse_ptr,
+    float* __restrict__ acc_ptr) {
+  constexpr int S = Geom16<D>::kSteps;
+  constexpr int kFlushKeys = kDecFlushPages * kPageSize;
+  __shared__ float res_s[kDecMaxWaves][kFlushKeys];
+  const int lane = threadIdx.x & 63;
+  const int G = dp.G, Hq = dp.Hq, Hkv = dp.Hkv, R = dp.R;
+  // this wave's head, through readfirstlane: everything derived from it is then known to be
+  // wave-uniform (scalar loads of the plan and block table, scalar branches)
+  const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int h = (int)blockIdx.y * (int)(blockDim.x / 64) + wv;
+  float* res = res_s[wv];
+  // with at most one query a request's cost is Hkv x its 64-key tiles (one row tile), so
+  // seg_cost[r * Hkv] / Hkv is the number of tiles before request r
+  auto tiles_before = [&](int rr) { return dp.seg_cost[(int64_t)rr * Hkv] / Hkv; };
+  const int64_t total = tiles_before(R);
+  const int64_t c0 = total * blockIdx.x / gridDim.x, c1 = total * (blockIdx.x + 1) / gridDim.x;
+  if (c0 >= c1) return;
+  const float alpha = dp.sm_scale * kLog2e;
+  const int64_t page_bytes = (int64_t)kPageSize * Hkv * D * 2;
+  // first request: the largest r with tiles_before(r) <= c0 (a prefix of 0 .. R, since
+  // tiles_before does not decrease), 64 candidates per load and ballot
+  int lo = 0;
+  for (int base = 0; base <= R; base += 64) {
+    const int rr = base + lane;
+    const uint64_t m = __ballot(rr <= R && tiles_before(rr) <= c0);
+    if (m == 0ull) break;
+    lo = base + 63 - __builtin_clzll(m);
+    if (m != ~0ull) break;
+  }
+  for (int r = lo; r < R; ++r) {
+    const int64_t cs = tiles_before(r);
+    if (cs >= c1) break;
+    const ReqPlan pl = dp.plan[r];
+    if (pl.n == 0 || pl.L == 0) continue;   // nothing to add
+    const int L = pl.L;
+    const int64_t ntiles = ceil_div64(L, kKeyTile);
+    const int64_t t0 = c0 > cs ? c0 - cs : 0, t1 = c1 - cs < ntiles ? c1 - cs : ntiles;
+    const int npages = ceil_div(L, kPageSize);
+    const int p0 = (int)t0 * (kKeyTile / kPageSize);
+    const int p1 = (int)t1 * (kKeyTile / kPageSize) < npages ? (int)t1 * (kKeyTile / kPageSize)
+                                                              : npages;
+    if (p0 >= p1) continue;
+    // the query's G rows (row m = head m of the group) and beta of this lane's rows
+    bf16x8 qr[S];
+    load_q16<D>(qr, q_ptr, G, false, Hq, h, pl.q_off, 1, 0, 0);
+    float beta[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = 4 * (lane >> 4) + i;
+      beta[i] = m < G ? lse_ptr[(int64_t)pl.q_off * Hq + h * G + m] * kLog2e : __builtin_inff();
+    }
+    const int32_t* bt_row = bt_ptr + (int64_t)r * dp.bt_stride;
+    float* out = acc_ptr + pl.seg_off + (int64_t)h * L;
+    // the aggregate of this segment: reads past L return 0, writes there are dropped
+    const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
+        out, (short)0, L * (int)sizeof(float), 0x00020000);
+    const uint32_t lane_off = (uint32_t)((((lane & 15) * Hkv + h) * D) * 2 + (lane >> 4) * 16);
+    for (int fb = p0; fb < p1; fb += kDecFlushPages) {
+      const int pe = fb + kDecFlushPages < p1 ? fb + kDecFlushPages : p1;
+      u32x4 kb[kDecRing][S];
+      auto issue = [&](int slot, int p) {
+        int64_t page = bt_row[p];
+        if (page < 0 || page >= dp.num_pages) page = 0;   // never dereference outside the pool
+        const char* base = kv_bytes + page * page_bytes + lane_off;
+#pragma unroll
+        for (int ks = 0; ks < S; ++ks)
+          kb[slot][ks] = *reinterpret_cast<const u32x4*>(base + 64 * ks);
+      };
+      // Every slot is refilled after its use on every step (past the block's last page: that
+      // page again) and every step computes; steps past the block keep nothing.  With no
+      // conditional loads in the loop a slot keeps its registers from step to step and the
+      // compiler's waits stay partial.
+      const int last = pe - 1;
+#pragma unroll
+      for (int j = 0; j < kDecRing; ++j) issue(j, fb + j < pe ? fb + j : last);
+      for (int pb = fb; pb < pe; pb += kDecRing) {
+#pragma unroll
+        for (int j = 0; j < kDecRing; ++j) {
+          const int p = pb + j;
+          f32x4 cacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < S; ++ks) cacc = mfma16(qr[ks], as_bf16x8(kb[j][ks]), cacc);
+          // this lane's 4 rows in order, then the lane groups (rows 4-7, 8-15) in order
+          float v = 0.f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float e = fast_exp2(__builtin_fmaf(cacc[i], alpha, -beta[i]));
+            v = kMaxMean ? fmaxf(v, e) : v + e;
+          }
+          if (G > 4) {
+            const float o = __shfl_xor(v, 16, 64);
+            v = kMaxMean ? fmaxf(v, o) : v + o;
+          }
+          if (G > 8) {
+            const float o = __shfl_xor(v, 32, 64);
+            v = kMaxMean ? fmaxf(v, o) : v + o;
+          }
+          if (lane < 16 && p < pe) res[(p - fb) * kPageSize + lane] = v;
+          // the slot is refilled only now, once the chain that read it has finished (an earlier
+          // refill would need other registers, and the loop edge would then wait for them)
+          issue(j, p + kDecRing < pe ? p + kDecRing : last);
+        }
+      }
+      // add the block's scores to the aggregate: lane l takes keys 16 fb + 64 i + l.  All
+      // loads first and no conditional ones, so the stores follow a single wait; keys past
+      // the block (the next block's, or another workgroup's share) use an offset past the
+      // buffer: read as 0, not written
+      const int nk = (pe - fb) * kPageSize;
+      float a[kFlushKeys / 64];
+#pragma unroll
+      for (int i = 0; i < kFlushKeys / 64; ++i) {
+        const int k = i * 64 + lane;
+        a[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                             ars, k < nk ? (fb * kPageSize + k) * 4 : 0x7FFFFFF0,
+                                             0, 0));
+      }
+#pragma unroll
+      for (int i = 0; i < kFlushKeys / 64; ++i) {
+        const int k = i * 64 + lane;
+        const float sc = k < nk ? res[k] : 0.f;
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, a[i] + sc), ars,
+                                              k < nk ? (fb * kPageSize + k) * 4 : 0x7FFFFFF0, 0,
+                                              0);
+      }
+    }
+  }
+}
+
+hipError_t launch_score_decode(const DevProblem& dp, const HostPlan& hp, const void* q,
+                               const void* kv, const int32_t* bt, const float* lse, float* acc,
+                               hipStream_t s) {
+  if (hp.num_scores == 0 || hp.sum_n == 0) return hipSuccess;
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess) {
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 256;
+  }
+  const uint16_t* qq = static_cast<const uint16_t*>(q);
+  const char* kk = static_cast<const char*>(kv);
+  const bool mm = dp.agg == ACTKV_AGG_MAX_MEAN;
+  // waves per workgroup: the largest divisor of Hkv up to kDecMaxWaves (every wave a head)
+  int waves = 1;
+  for (int w = 1; w <= kDecMaxWaves; ++w)
+    if (hp.Hkv % w == 0) waves = w;
+  const unsigned groups = (unsigned)(hp.Hkv / waves);
+  const int64_t tiles = hp.score_cost / hp.Hkv;   // (request, 64-key tile) pairs
+  // one resident round of workgroups (equal contiguous shares: a second round would only
+  // add a tail), at most one per tile.  Residency per CU is asked once per kernel and
+  // workgroup size (it depends on nothing else).
+  static std::atomic<int> cached[2][2][kDecMaxWaves + 1];   // [D == 128][MAX_MEAN][waves]
+  auto launch = [&](auto kernel) -> hipError_t {
+    std::atomic<int>& slot = cached[dp.D == 128][mm][waves];
+    int per_cu = slot.load(std::memory_order_relaxed);
+    if (per_cu == 0) {
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, waves * 64, 0) != hipSuccess ||
+          per_cu < 1)
+        per_cu = 1;
+      slot.store(per_cu, std::memory_order_relaxed);
+    }
+    int64_t blocks = (int64_t)cus * per_cu / groups;
+    if (blocks > tiles) blocks = tiles;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks, groups), dim3(waves * 64), 0, s, dp, qq, kk,
+                       bt, lse, acc);
+    return hipGetLastError();
+  };
+  if (dp.D == 128)
+    return mm ? launch(score_decode_kernel<128, true>) : launch(score_decode_kernel<128, false>);
+  return mm ? launch(score_decode_kernel<64, true>) : launch(score_decode_kernel<64, false>);
 }
 
 // ---------------------------------------------------------------------------------------

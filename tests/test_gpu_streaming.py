@@ -6,8 +6,15 @@ the Table 1 shapes on the GPU, against the oracle.
     queries (and to the oracle's scores) within the score tolerance;
   * on the Table 1 shapes (8 KV heads, d = 128, one action query), the streaming scores
     match the oracle, the selection matches outside near-ties, and the in-place and
-    fresh-page compactions of the GPU's selection are bit-exact.
+    fresh-page compactions of the GPU's selection are bit-exact;
+  * decode steps (at most one query per request) run their own kernel, which adds into the
+    aggregate in place: every group size and lane layout, both aggregations, both head
+    sizes, requests without a query, nothing written outside the aggregate, and at full
+    size (32 x 35,000 tokens) equal to the batched kernel and, on sampled requests, to the
+    oracle; calls with several queries per request keep the batched path.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -116,3 +123,100 @@ def test_table1_shapes_against_the_oracle(name):
     assert_compaction_matches(pb, kept_gpu, pb.kv, t["kv"].cpu().numpy().view(np.uint16),
                               t["bt"].cpu().numpy(), freed.cpu().numpy(),
                               new_lens.cpu().numpy())
+
+
+# Decode steps (at most one action query per request) are scored and added in one pass by
+# their own kernel: every group size (lane groups 1, 2 and 4 of the 16-row tile), both
+# aggregations, both head sizes, requests without a query this step, ragged page tails.
+DECODE_CASES = {
+    "g1": dict(num_q_heads=2, num_kv_heads=2),
+    "g4": dict(num_q_heads=8, num_kv_heads=2),
+    "g8": dict(num_q_heads=16, num_kv_heads=2),
+    "g16_d64": dict(num_q_heads=16, num_kv_heads=1, head_dim=64),
+    "g2_d64": dict(num_q_heads=4, num_kv_heads=2, head_dim=64),
+}
+
+
+@pytest.mark.parametrize("agg", ["sum", "max_mean"])
+@pytest.mark.parametrize("case", sorted(DECODE_CASES))
+def test_decode_step_against_the_oracle(case, agg):
+    kw = DECODE_CASES[case]
+    lens = [300, 77, 1030, 5, 16, 129]
+    H = kw["num_kv_heads"]
+    pb = custom(seq_lens=lens, q_lens=[1, 1, 0, 1, 1, 1], budgets=[8] * (len(lens) * H),
+                pool_window=1, **kw)
+    lse = oracle.lse(pb).astype(np.float32)
+    bp, t = to_dev(pb, agg=agg)
+    n = oracle.num_scores(pb)
+    # the aggregate inside a guarded buffer: nothing outside it may change
+    buf = torch.full((n + 64,), -7.0, dtype=torch.float32, device="cuda")
+    acc = buf[32:32 + n]
+    acc.zero_()
+    lse_d = torch.from_numpy(lse).cuda()
+    actkv.score_accumulate(bp, t["q"], t["kv"], t["bt"], acc, lse=lse_d)
+    torch.cuda.synchronize()
+    ref = oracle.scores(pb, lse_in=lse, agg=agg)
+    assert_scores_close(acc.cpu().numpy(), ref, what="decode step vs oracle")
+    # a second step adds to what is there
+    actkv.score_accumulate(bp, t["q"], t["kv"], t["bt"], acc, lse=lse_d)
+    torch.cuda.synchronize()
+    assert_scores_close(acc.cpu().numpy(), 2 * ref, what="two decode steps")
+    guard = buf.cpu().numpy()
+    assert (guard[:32] == -7.0).all() and (guard[32 + n:] == -7.0).all()
+    # the request without a query this step is left alone
+    off = int(H * sum(lens[:2]))
+    assert (acc.cpu().numpy()[off:off + H * lens[2]] == 0).all()
+
+
+def test_decode_step_computes_its_own_lse():
+    pb = custom(seq_lens=[500, 33], q_lens=[1, 1], budgets=[8] * 4, pool_window=1,
+                num_q_heads=16, num_kv_heads=2)
+    bp, t = to_dev(pb)
+    acc = torch.zeros(oracle.num_scores(pb), dtype=torch.float32, device="cuda")
+    actkv.score_accumulate(bp, t["q"], t["kv"], t["bt"], acc)
+    torch.cuda.synchronize()
+    assert_scores_close(acc.cpu().numpy(), oracle.scores(pb), what="decode step, own LSE")
+
+
+def test_several_queries_per_request_take_the_batched_path():
+    pb = custom(seq_lens=[300, 77, 640], q_lens=[3, 1, 2], budgets=[8] * 6, pool_window=1)
+    lse = oracle.lse(pb).astype(np.float32)
+    bp, t = to_dev(pb)
+    n = oracle.num_scores(pb)
+    acc0 = np.random.default_rng(5).random(n).astype(np.float32) * 1e-3
+    acc = torch.from_numpy(acc0).cuda()
+    actkv.score_accumulate(bp, t["q"], t["kv"], t["bt"], acc, lse=torch.from_numpy(lse).cuda())
+    torch.cuda.synchronize()
+    ref = acc0.astype(np.float64) + oracle.scores(pb, lse_in=lse)
+    assert_scores_close(acc.cpu().numpy(), ref, what="accumulate, several queries")
+
+
+def test_decode_step_at_full_size_matches_the_batched_kernel():
+    """The 32 x 35,000-token cache with one query per request (as the streaming benchmark
+    runs it): the decode kernel's scores against the batched kernel's, everywhere, and
+    against the oracle on two sampled requests."""
+    dev = torch.device("cuda:0")
+    dp = W.make_device_problem("batch32x35k", device=dev)
+    ones = np.ones_like(dp.q_lens)
+    bp = actkv.Problem(seq_lens=dp.seq_lens, q_lens=ones, budgets=dp.budgets,
+                       num_q_heads=dp.num_q_heads, num_kv_heads=dp.num_kv_heads,
+                       head_dim=dp.head_dim, num_pages=dp.num_pages, bt_stride=dp.bt_stride,
+                       sm_scale=dp.sm_scale, pool_window=1, causal=dp.causal).to_device(dev)
+    q1 = dp.q[torch.from_numpy(dp.cu_q[:-1].astype(np.int64)).to(dev)].contiguous()
+    bt = torch.from_numpy(dp.block_table).to(dev)
+    lse = actkv.lse(bp, q1, dp.kv, bt)
+    acc = torch.zeros(actkv.num_scores(bp), dtype=torch.float32, device=dev)
+    actkv.score_accumulate(bp, q1, dp.kv, bt, acc, lse=lse)
+    batched = actkv.score(bp, q1, dp.kv, bt, lse=lse)
+    torch.cuda.synchronize()
+    got = acc.cpu().numpy()
+    assert_scores_close(got, batched.cpu().numpy(), what="decode vs batched kernel")
+    H = dp.num_kv_heads
+    offs = np.concatenate([[0], np.cumsum(dp.seq_lens.astype(np.int64) * H)])
+    for r in (0, dp.num_reqs - 1):
+        host = dp.host_subset([r])
+        # that request with its first action query only
+        one = dataclasses.replace(host, q_lens=np.ones(1, np.int32), q=host.q[:1].copy(),
+                                  pool_window=1)
+        ref = oracle.scores(one)   # the oracle's own fp64 LSE
+        assert_scores_close(got[offs[r]:offs[r + 1]], ref, what=f"request {r} vs oracle")
