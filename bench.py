@@ -37,6 +37,10 @@ SCORE_SOURCES = ["paper_2609_31395_amd/csrc/score.hip",
                  "paper_2609_31395_amd/csrc/actkv_internal.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_kernel_batch32x35k_traffic.json")
 COPY_CALIB_BYTES = 512 << 20   # the known-size copy that calibrates FETCH_SIZE / WRITE_SIZE
+# fp32 VALU issue slots per second without packed fp32 (256 CUs x 4 SIMDs x 16 lanes x
+# 2.4 GHz); v_exp_f32 is a quarter-rate transcendental (4 slots)
+VALU_SLOTS_PER_S = 256 * 4 * 16 * 2.4e9
+EXP_SLOTS = 4
 LRFU_TOP_P, LRFU_DECAY = 0.9, 0.5   # the eviction policy's settings in the paper's evaluation
 
 
@@ -55,7 +59,7 @@ def parse():
                     help="skip the Table 1 shapes (streaming scoring and compression ops)")
     ap.add_argument("--profile-stage",
                     choices=["score", "select", "compact", "lse", "step", "lrfu_select",
-                             "lrfu_step", "inplace_compact", "copy"],
+                             "lrfu_step", "inplace_compact", "streaming", "copy"],
                     help="only run one entry point --steps times (for counter collection); "
                          "prints a short JSON line instead of the benchmark record.  'copy' "
                          "is the calibration: a plain device-to-device copy of "
@@ -91,6 +95,29 @@ def score_flops(dp) -> int:
     G = dp.num_q_heads // dp.num_kv_heads
     return int(sum(2 * G * int(n) * int(L) * dp.head_dim * dp.num_kv_heads
                    for L, n in zip(dp.seq_lens, dp.q_lens)))
+
+
+def score_epilogue_slots(dp) -> float:
+    """VALU issue slots of the scoring epilogue: per (query row, key) one FMA (scale and
+    LSE), one exp2 (quarter rate) and one add."""
+    exps = score_flops(dp) / (2 * dp.head_dim)
+    return exps * (1 + EXP_SLOTS + 1)
+
+
+def measure_copy_bw(dev, reps=10) -> float:
+    """Device-to-device copy of COPY_CALIB_BYTES, timed with events: read plus written
+    bytes per second (the practical HBM ceiling of a streaming kernel on this machine)."""
+    import torch
+    src = torch.empty(COPY_CALIB_BYTES, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    ev = _event_pairs(reps)
+    for a, b in ev:
+        a.record()
+        dst.copy_(src)
+        b.record()
+    torch.cuda.synchronize()
+    return 2 * COPY_CALIB_BYTES / (_mean_ms(ev) * 1e-3)
 
 
 def log(msg: str) -> None:
@@ -235,9 +262,9 @@ def run_table1(reps, dev, stream):
     return rows
 
 
-def run_streaming_batch(dp, bp_full, reps, dev, stream):
-    """One decode step of streaming scoring over the whole batch: every request scores its
-    cache with one action query (the first of its action queries), LSE supplied."""
+def streaming_setup(dp, dev):
+    """The workload as one decode step sees it: every request scores its cache with one
+    action query (the first of its action queries), LSE supplied."""
     import torch
     from paper_2609_31395_amd import actkv
     ones = np.ones_like(dp.q_lens)
@@ -249,6 +276,13 @@ def run_streaming_batch(dp, bp_full, reps, dev, stream):
     bt0 = torch.from_numpy(dp.block_table).to(dev)
     lse = actkv.lse(bp, q1, dp.kv, bt0, ws=ws)
     acc = torch.zeros(actkv.num_scores(bp), dtype=torch.float32, device=dev)
+    return bp, q1, bt0, lse, acc, ws
+
+
+def run_streaming_batch(dp, bp_full, reps, dev, stream):
+    """One decode step of streaming scoring over the whole batch (streaming_setup)."""
+    from paper_2609_31395_amd import actkv
+    bp, q1, bt0, lse, acc, ws = streaming_setup(dp, dev)
     ev = _event_pairs(reps + 1)
     for e in ev:
         e[0].record(stream)
@@ -450,6 +484,16 @@ def main():
     # (a compacted table must never be reused with the original lengths)
     bts = [bt0.clone() for _ in range(K + max(Wm, 1))]
 
+    if args.profile_stage == "streaming":
+        bp1, q1, bt1, lse1, acc1, ws1 = streaming_setup(dp, dev)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(K + Wm):
+            actkv.score_accumulate(bp1, q1, dp.kv, bt1, acc1, lse=lse1, ws=ws1)
+        torch.cuda.synchronize()
+        print(json.dumps({"profile_stage": "streaming", "reps": K + Wm,
+                          "avg_us": (time.perf_counter() - t0) / (K + Wm) * 1e6}))
+        return
     if args.profile_stage:
         run_stage(args.profile_stage, K + Wm, bp, dp, bts, lse, scores, pooled, kept, free, freed,
                   new_lens, ws, qy)
@@ -519,6 +563,10 @@ def main():
     value = sum_L / (ms_per_step * 1e-3)
     alg_bytes = algorithmic_bytes(dp, qy["num_kept"])
     flops = score_flops(dp)
+    copy_bw = measure_copy_bw(dev)
+    t_hbm = alg_bytes / (HBM_PEAK_GBS * 1e9)
+    t_mfma = flops / (BF16_PEAK_TFLOPS * 1e12)
+    t_valu = score_epilogue_slots(dp) / VALU_SLOTS_PER_S
     score_s = stage_ms[0] * 1e-3
     achieved_tflops = flops / score_s / 1e12
     traffic = None
@@ -589,8 +637,14 @@ def main():
         "step_us_p10_p90": [float(np.percentile(step_ms, 10) * 1e3),
                             float(np.percentile(step_ms, 90) * 1e3)],
         "hbm_roofline": {"algorithmic_bytes": alg_bytes,
-                         "t_hbm_us": alg_bytes / (HBM_PEAK_GBS * 1e9) * 1e6,
-                         "frac": (alg_bytes / (HBM_PEAK_GBS * 1e9)) / (ms_per_step * 1e-3)},
+                         "t_hbm_us": t_hbm * 1e6,
+                         "frac": t_hbm / (ms_per_step * 1e-3),
+                         "copy_GBps": copy_bw / 1e9,
+                         "frac_vs_copy": (alg_bytes / copy_bw) / (ms_per_step * 1e-3)},
+        "combined_roofline": {"t_hbm_us": t_hbm * 1e6, "t_mfma_us": t_mfma * 1e6,
+                              "t_valu_us": t_valu * 1e6,
+                              "bound_us": max(t_hbm, t_mfma, t_valu) * 1e6,
+                              "frac": max(t_hbm, t_mfma, t_valu) / (ms_per_step * 1e-3)},
         "stages_us": {"score": stage_ms[0] * 1e3, "select": stage_ms[1] * 1e3,
                       "compact": stage_ms[2] * 1e3},
         "step_with_lse_pass_us": ms_with_lse * 1e3,
