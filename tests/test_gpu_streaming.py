@@ -134,6 +134,9 @@ DECODE_CASES = {
     "g8": dict(num_q_heads=16, num_kv_heads=2),
     "g16_d64": dict(num_q_heads=16, num_kv_heads=1, head_dim=64),
     "g2_d64": dict(num_q_heads=4, num_kv_heads=2, head_dim=64),
+    # workgroups of 6 heads in two groups, and of 8 heads in two groups
+    "g1_12kv": dict(num_q_heads=12, num_kv_heads=12),
+    "g2_16kv": dict(num_q_heads=32, num_kv_heads=16),
 }
 
 
