@@ -281,6 +281,7 @@ def streaming_setup(dp, dev):
 
 def run_streaming_batch(dp, bp_full, reps, dev, stream):
     """One decode step of streaming scoring over the whole batch (streaming_setup)."""
+    import torch
     from paper_2609_31395_amd import actkv
     bp, q1, bt0, lse, acc, ws = streaming_setup(dp, dev)
     ev = _event_pairs(reps + 1)

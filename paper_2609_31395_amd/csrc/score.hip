@@ -1005,6 +1005,9 @@ __global__ __launch_bounds__(kLseThreads, 1) void lse_partial_kernel(
                                page_of<D, kLseWaves>(bt_row, L, dp.num_pages, kp, clamp_tile(t0 + p)),
                                page_bytes, kp);
   int64_t next_page = page_of<D, kLseWaves>(bt_row, L, dp.num_pages, kp, clamp_tile(t0 + kStages - 1));
+  // keys up to the first action query's position are visible to every real row (rows past
+  // n, all padding, are never written): tiles below it need no mask
+  const int64_t open_to = dp.causal ? (int64_t)L - n : (int64_t)L - 1;
   for (int64_t i = t0; i < t1; ++i) {
     const int st = (int)((i - t0) % kStages);
     wait_vmcnt<(kStages - 2) * Gm::kLoadsPerWave>();
@@ -1012,6 +1015,7 @@ __global__ __launch_bounds__(kLseThreads, 1) void lse_partial_kernel(
     issue_k_tile<D, kLseWaves>(kl + ((st + kStages - 1) % kStages) * Gm::kTileBytes, kv_bytes,
                                next_page, page_bytes, kp);
     next_page = page_of<D, kLseWaves>(bt_row, L, dp.num_pages, kp, clamp_tile(i + kStages));
+    const bool masked = i * kKeyTile + kKeyTile - 1 > open_to;
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
       bf16x8 kreg[Gm::kSteps];
@@ -1023,19 +1027,27 @@ __global__ __launch_bounds__(kLseThreads, 1) void lse_partial_kernel(
           f32x16 x = {};
 #pragma unroll
           for (int ks = 0; ks < Gm::kSteps; ++ks) x = mfma32(kreg[ks], qreg[ti][ks], x);
-          float mx = rm[ti];
+          // the running max on the raw dot products (alpha > 0 keeps the order), then
+          // 2^(alpha x - m) with the scale and the shift in one FMA
+          float mx = -__builtin_inff();
+          if (masked) {
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int key = keybase + 8 * (v / 4) + (v % 4);
-            x[v] = key <= pos[ti] ? x[v] * alpha : -__builtin_inff();
-            mx = fmaxf(mx, x[v]);
+            for (int v = 0; v < 16; ++v) {
+              const int key = keybase + 8 * (v / 4) + (v % 4);
+              x[v] = key <= pos[ti] ? x[v] : -__builtin_inff();
+              mx = fmaxf(mx, x[v]);
+            }
+          } else {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) mx = fmaxf(mx, x[v]);
           }
-          if (mx != -__builtin_inff()) {
-            float sum = rs[ti] * fast_exp2(rm[ti] - mx);
+          const float m = fmaxf(rm[ti], mx * alpha);
+          if (m != -__builtin_inff()) {
+            float sum = rs[ti] * fast_exp2(rm[ti] - m);
 #pragma unroll
-            for (int v = 0; v < 16; ++v) sum += fast_exp2(x[v] - mx);
+            for (int v = 0; v < 16; ++v) sum += fast_exp2(__builtin_fmaf(x[v], alpha, -m));
             rs[ti] = sum;
-            rm[ti] = mx;
+            rm[ti] = m;
           }
         }
       }
