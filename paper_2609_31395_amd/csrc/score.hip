@@ -1073,22 +1073,40 @@ __global__ __launch_bounds__(kLseThreads, 1) void lse_partial_kernel(
   }
 }
 
+// One thread per (request, query row): the row's block partials in block order, eight
+// loads in flight at a time.  Grid: (requests, ceil(max rows per request / 256)).
 __global__ __launch_bounds__(256) void lse_merge_kernel(DevProblem dp, const float2* part,
                                                         float* lse) {
+  constexpr int kBatch = 8;
   const int r = blockIdx.x;
   const ReqPlan pl = dp.plan[r];
   const int rows = pl.n * dp.Hq;
-  for (int row = threadIdx.x; row < rows; row += 256) {
-    const float2* pp = part + pl.lse_part_off + (int64_t)row * pl.lse_blocks;
-    float m = -__builtin_inff();
-    for (int b = 0; b < pl.lse_blocks; ++b) m = fmaxf(m, pp[b].x);
-    float s = 0.f;
-    if (m != -__builtin_inff())
-      for (int b = 0; b < pl.lse_blocks; ++b) s += pp[b].y * fast_exp2(pp[b].x - m);
-    // natural-log LSE = (m + log2 s) * ln 2
-    lse[(int64_t)pl.q_off * dp.Hq + row] =
-        m == -__builtin_inff() ? -__builtin_inff() : (m + __log2f(s)) * 0.6931471805599453f;
+  const int row = blockIdx.y * 256 + threadIdx.x;
+  if (row >= rows) return;
+  const float2* pp = part + pl.lse_part_off + (int64_t)row * pl.lse_blocks;
+  const int nb = pl.lse_blocks;
+  float m = -__builtin_inff();
+  for (int b0 = 0; b0 < nb; b0 += kBatch) {
+    float2 v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) v[u] = b0 + u < nb ? pp[b0 + u] : make_float2(-__builtin_inff(), 0.f);
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) m = fmaxf(m, v[u].x);
   }
+  float s = 0.f;
+  if (m != -__builtin_inff()) {
+    for (int b0 = 0; b0 < nb; b0 += kBatch) {
+      float2 v[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) v[u] = b0 + u < nb ? pp[b0 + u] : make_float2(-__builtin_inff(), 0.f);
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u)
+        if (b0 + u < nb) s += v[u].y * fast_exp2(v[u].x - m);
+    }
+  }
+  // natural-log LSE = (m + log2 s) * ln 2
+  lse[(int64_t)pl.q_off * dp.Hq + row] =
+      m == -__builtin_inff() ? -__builtin_inff() : (m + __log2f(s)) * 0.6931471805599453f;
 }
 
 hipError_t launch_lse(const DevProblem& dp, const HostPlan& hp, const void* q, const void* kv,
@@ -1106,7 +1124,9 @@ hipError_t launch_lse(const DevProblem& dp, const HostPlan& hp, const void* q, c
                        lse_part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(lse_merge_kernel, dim3(hp.R), dim3(256), 0, s, dp, lse_part, lse_out);
+  const int64_t max_rows = hp.max_n * hp.Hq;
+  hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)hp.R, (unsigned)((max_rows + 255) / 256)),
+                     dim3(256), 0, s, dp, lse_part, lse_out);
   return hipGetLastError();
 }
 
