@@ -57,13 +57,16 @@ def parse():
                     help="time only the headline step and its stages (for profiling)")
     ap.add_argument("--no-table1", action="store_true",
                     help="skip the Table 1 shapes (streaming scoring and compression ops)")
+    ap.add_argument("--no-fullmodel", action="store_true",
+                    help="skip the full-model leg (48 layers over one ~138 GB page pool)")
     ap.add_argument("--profile-stage",
                     choices=["score", "select", "compact", "lse", "step", "lrfu_select",
-                             "lrfu_step", "inplace_compact", "streaming", "copy"],
+                             "lrfu_step", "inplace_compact", "streaming", "copy",
+                             "fullmodel"],
                     help="only run one entry point --steps times (for counter collection); "
                          "prints a short JSON line instead of the benchmark record.  'copy' "
                          "is the calibration: a plain device-to-device copy of "
-                         "COPY_CALIB_BYTES bytes")
+                         "COPY_CALIB_BYTES bytes; 'fullmodel' times only the full-model leg")
     return ap.parse_args()
 
 
@@ -437,6 +440,61 @@ def run_inplace(c):
             "tokens_per_s": c["sum_L"] / (ms_ip_step * 1e-3)}
 
 
+def run_fullmodel(reps, dev, stream):
+    """The full-model workload: the steps of all 48 layers back to back over one shared page
+    pool (LSE supplied: produced per layer by actkv_lse outside the timed region).  Every
+    layer writes its compacted rows into the pool's spare pages, so the cache the layers
+    read is the same in every repetition; the block tables are restored before each
+    repetition, outside the events."""
+    import torch
+    from paper_2609_31395_amd import actkv
+    from paper_2609_31395_amd import workloads as W
+    torch.cuda.empty_cache()
+    t0 = time.perf_counter()
+    layers = W.make_device_model("model48x32", device=dev)
+    torch.cuda.synchronize()
+    t_gen = time.perf_counter() - t0
+    spare = torch.from_numpy(layers[0].free_pages).to(dev)
+    kv = layers[0].kv
+    ctx, alg_bytes, flops, tokens = [], 0, 0, 0
+    for dp in layers:
+        bp = _binding(dp, dev)
+        qy = actkv.query(bp)
+        ws = torch.empty(qy["workspace_bytes"], dtype=torch.uint8, device=dev)
+        bt0 = torch.from_numpy(dp.block_table).to(dev)
+        lse = actkv.lse(bp, dp.q, dp.kv, bt0, ws=ws)
+        freed = torch.empty(max(qy["pages_freed"], 1), dtype=torch.int32, device=dev)
+        new_lens = torch.empty(bp.num_reqs * bp.num_kv_heads, dtype=torch.int32, device=dev)
+        ctx.append((bp, qy, ws, bt0, bt0.clone(), lse, freed, new_lens, dp.q))
+        alg_bytes += algorithmic_bytes(dp, qy["num_kept"])
+        flops += score_flops(dp)
+        tokens += int(dp.seq_lens.astype(np.int64).sum())
+    ev = _event_pairs(reps + 1)
+    for i in range(reps + 1):
+        for c in ctx:
+            c[4].copy_(c[3])
+        ev[i][0].record(stream)
+        for bp, qy, ws, _, bt, lse, freed, new_lens, q in ctx:
+            actkv.step(bp, q, kv, bt, spare, lse=lse, freed=freed, new_lens=new_lens, ws=ws,
+                       qy=qy)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    ms = _mean_ms(ev)
+    d0 = layers[0]
+    out = {"workload": "model48x32", "layers": len(layers), "requests": d0.num_reqs,
+           "seq_len_range": [int(d0.seq_lens.min()), int(d0.seq_lens.max())],
+           "pool_GB": kv.numel() * kv.element_size() / 1e9, "gen_s": t_gen,
+           "cached_tokens_all_layers": tokens, "step_ms": ms,
+           "layer_step_us": ms * 1e3 / len(layers),
+           "tokens_per_s": tokens / (ms * 1e-3),
+           "hbm_roofline_frac": alg_bytes / (HBM_PEAK_GBS * 1e9) / (ms * 1e-3),
+           "score_mfma_bound_ms": flops / (BF16_PEAK_TFLOPS * 1e12) * 1e3}
+    del ctx, layers, kv, spare
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -451,6 +509,11 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.profile_stage == "copy":
         run_copy_calibration(args.steps)
+        return
+    if args.profile_stage == "fullmodel":
+        actkv.load_library()
+        fm = run_fullmodel(args.steps, torch.device("cuda:0"), torch.cuda.current_stream())
+        print(json.dumps({"profile_stage": "fullmodel", "reps": args.steps, **fm}))
         return
     actkv.load_library()
     dev = torch.device("cuda:0")
@@ -577,7 +640,7 @@ def main():
         if tr.get("source_sha256") == source_digest() and tr.get("workload") == args.workload:
             traffic = int(tr["hbm_bytes_per_launch"])
 
-    streaming = confidence = table1 = None
+    streaming = confidence = table1 = fullmodel = None
     if extra:
         streaming = run_streaming_batch(dp, bp, K, dev, stream)
         log(f"streaming scoring step (1 query per request): {streaming['score_step_us']:.1f} us,"
@@ -587,6 +650,11 @@ def main():
             f"({confidence['token_conf_GBps']:.0f} GB/s), budget update "
             f"{confidence['budget_update_us']:.1f} us")
         table1 = run_table1(max(K // 2, 5), dev, stream) if not args.no_table1 else None
+        fullmodel = run_fullmodel(max(K // 4, 3), dev, stream) if not args.no_fullmodel else None
+        if fullmodel:
+            log(f"full model (48 layers x 32 requests, 16K-64K tokens): "
+                f"{fullmodel['step_ms']:.1f} ms, {fullmodel['layer_step_us']:.0f} us per layer, "
+                f"{fullmodel['hbm_roofline_frac']:.2f} of the HBM roofline")
     if table1:
         for row in table1:
             log(f"{row['config']:16s} score step {row['score_step_us']:7.1f} us  compress "
@@ -653,6 +721,7 @@ def main():
         "streaming": streaming,
         "confidence": confidence,
         "table1": table1,
+        "fullmodel": fullmodel,
         "lrfu": lrfu,
         "roofline": {
             "kernel": "score_kernel (actkv_score, LSE supplied)",

@@ -96,6 +96,22 @@ for _i, (_r, (_L, _B)) in enumerate([(r, lb) for r in TABLE1_REQS for lb in TABL
 del _i, _r, _L, _B, _name
 
 
+# Full-model compression step: every layer of a 48-layer model (Qwen3-30B-A3B's depth)
+# compressed back to back, over one page pool that all layers share.  The requests -- their
+# lengths and action-query counts -- are the same in every layer; Q, K, V, spikes and the
+# Dirichlet budgets are drawn per layer, and each layer's pages lie at random places in the
+# pool.  The pool holds the pages of all layers plus one layer's worth of spare pages, so
+# K/V byte offsets run past 2^36.
+MODEL_CONFIGS: Dict[str, Tuple[int, WorkloadConfig]] = {
+    "model48x32": (48, WorkloadConfig(
+        "model48x32", 32, 32, 4, 128, (16000, 64000), (64, 64), ("dirichlet", 0.5, 0.25), 7,
+        0.01, 1007,
+        description="48 layers x 32 requests, L ~ U[16000, 64000], Qwen3-30B heads "
+                    "(32q/4kv, d=128), 64 action queries, 1% spikes, pool 7, per-layer "
+                    "Dirichlet(0.5) split of 25% of Hkv*L, one shared page pool")),
+}
+
+
 @dataclass
 class Problem:
     """Host-side (numpy) inputs of one compression step over one layer."""
@@ -374,9 +390,73 @@ def make_device_problem(name: str, device="cuda", *, seed: Optional[int] = None,
     block_table = np.full((R, bt_stride), -1, dtype=np.int32)
     kv = torch.empty((2, P, BS, Hkv, D), dtype=torch.bfloat16, device=device)
     q_all = torch.empty((int(n.sum()), Hq, D), dtype=torch.bfloat16, device=device)
+    pages_list = _fill_device(kv, q_all, block_table, perm[:used], L, n, G, cfg.spike_frac,
+                              req_ss, device)
+    free_pages = perm[used:].copy()
+    sm_scale = float(np.float32(1.0) / np.sqrt(np.float32(D)))
+    return DeviceProblem(cfg.name, Hq, Hkv, D, BS, L.astype(np.int32), n.astype(np.int32),
+                         budgets.astype(np.int32), block_table, free_pages, sm_scale,
+                         cfg.pool_window, cfg.causal, q_all.view(torch.int16),
+                         kv.view(torch.int16), pages_list)
+
+
+def make_device_model(name: str, device="cuda", *, num_layers: Optional[int] = None,
+                      overrides: Optional[dict] = None) -> List[DeviceProblem]:
+    """Draw the full-model workload `name` (see MODEL_CONFIGS) into one device page pool.
+
+    Returns one DeviceProblem per layer.  They share the kv tensor (all layers' pages and the
+    spare pages) and the request lengths; each has its own Q, budgets, block table and page
+    lists.  Every layer's free_pages is the pool's spare pages, which is what a layer run on
+    its own draws from; a back-to-back run of the layers can instead hand each layer the
+    pages the previous layer freed.
+    """
+    import torch
+    layers, cfg = MODEL_CONFIGS[name]
+    if num_layers is not None:
+        layers = int(num_layers)
+    if overrides:
+        cfg = WorkloadConfig(**{**cfg.__dict__, **overrides})
+    ss = np.random.SeedSequence(cfg.seed)
+    meta_ss, page_ss, *layer_ss = ss.spawn(2 + layers)
+    R, Hq, Hkv, D, BS = cfg.num_reqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, PAGE_SIZE
+    G = Hq // Hkv
+    L, n = _draw_lengths(np.random.Generator(np.random.PCG64(meta_ss)), cfg)
+    Y = (L.astype(np.int64) + BS - 1) // BS
+    used = int(Y.sum())
+    P = (layers + 1) * used
+    perm = np.random.Generator(np.random.PCG64(page_ss)).permutation(P).astype(np.int32)
+    spare = perm[layers * used:].copy()
+    bt_stride = int(max(1, Y.max(initial=0)))
+    kv = torch.empty((2, P, BS, Hkv, D), dtype=torch.bfloat16, device=device)
+    sm_scale = float(np.float32(1.0) / np.sqrt(np.float32(D)))
+    out = []
+    for l in range(layers):
+        budget_ss, *req_ss = layer_ss[l].spawn(1 + R)
+        budgets = _draw_budgets(np.random.Generator(np.random.PCG64(budget_ss)), cfg, L)
+        block_table = np.full((R, bt_stride), -1, dtype=np.int32)
+        q_all = torch.empty((int(n.sum()), Hq, D), dtype=torch.bfloat16, device=device)
+        pages_list = _fill_device(kv, q_all, block_table, perm[l * used:(l + 1) * used], L, n,
+                                  G, cfg.spike_frac, req_ss, device)
+        out.append(DeviceProblem(f"{cfg.name}[layer {l}]", Hq, Hkv, D, BS, L.astype(np.int32),
+                                 n.astype(np.int32), budgets.astype(np.int32), block_table,
+                                 spare, sm_scale, cfg.pool_window, cfg.causal,
+                                 q_all.view(torch.int16), kv.view(torch.int16), pages_list))
+    return out
+
+
+def _fill_device(kv, q_all, block_table, pages_in_use, L, n, G, spike_frac, req_ss,
+                 device) -> List[np.ndarray]:
+    """Draw each request's Q, K, V on the device (one torch generator per request, seeded
+    from its SeedSequence), plant the spike keys, and scatter K/V into the pages
+    `pages_in_use` in request order; fills block_table and q_all, returns the page lists."""
+    import torch
+    BS = PAGE_SIZE
+    _, _, _, Hkv, D = kv.shape
+    Hq = q_all.shape[1]
+    Y = (L.astype(np.int64) + BS - 1) // BS
     pages_list = []
     off_page, off_q = 0, 0
-    for r in range(R):
+    for r in range(int(L.shape[0])):
         Lr, nr, Yr = int(L[r]), int(n[r]), int(Y[r])
         gen = torch.Generator(device=device)
         gen.manual_seed(int(req_ss[r].generate_state(1, dtype=np.uint64)[0] & 0x7FFFFFFFFFFFFFFF))
@@ -385,14 +465,14 @@ def make_device_problem(name: str, device="cuda", *, seed: Optional[int] = None,
         v = torch.randn((Yr * BS, Hkv, D), generator=gen, device=device)
         k[Lr:] = 0
         v[Lr:] = 0
-        cnt = int(round(cfg.spike_frac * Lr))
+        cnt = int(round(spike_frac * Lr))
         if cnt > 0 and nr > 0:
             qf = q.float()
             for h in range(Hkv):
                 mean = qf[:, h * G:(h + 1) * G, :].reshape(-1, D).double().mean(0).float()
                 idx = torch.randperm(Lr, generator=gen, device=device)[:cnt]
                 k[idx, h, :] += 3.0 * mean
-        pages = perm[off_page:off_page + Yr]
+        pages = pages_in_use[off_page:off_page + Yr]
         block_table[r, :Yr] = pages
         pg = torch.from_numpy(pages.astype(np.int64)).to(device)
         kv[0].index_copy_(0, pg, k.to(torch.bfloat16).view(Yr, BS, Hkv, D))
@@ -402,9 +482,4 @@ def make_device_problem(name: str, device="cuda", *, seed: Optional[int] = None,
         off_page += Yr
         off_q += nr
         del k, v
-    free_pages = perm[used:].copy()
-    sm_scale = float(np.float32(1.0) / np.sqrt(np.float32(D)))
-    return DeviceProblem(cfg.name, Hq, Hkv, D, BS, L.astype(np.int32), n.astype(np.int32),
-                         budgets.astype(np.int32), block_table, free_pages, sm_scale,
-                         cfg.pool_window, cfg.causal, q_all.view(torch.int16),
-                         kv.view(torch.int16), pages_list)
+    return pages_list
