@@ -20,7 +20,9 @@
 // keys instead of floats (no conversion per pass), batched LDS reads at immediate offsets
 // (the LDS buffer is padded so a batch may read past the end of the segment), 32-bit digit
 // arithmetic.
-// Segments longer than the LDS capacity run the same steps on `pooled` in global memory.
+// Segments longer than the LDS capacity, up to 64,512 entries, hold their keys in registers
+// instead (windows up to 7); longer ones, or wider windows, run the same steps on `pooled` in
+// global memory.
 #include "device_common.hpp"
 
 namespace actkv {
@@ -334,25 +336,37 @@ __device__ __forceinline__ void pool_in_lds(int L, int hw, RunGeom g, uint32_t* 
   if (out) copy_out_u32(L, vals, out, KeyToFloatBits());
 }
 
-// Smallest and largest order key of the segment in LDS (every thread gets both).
-__device__ __forceinline__ void seg_key_range(RunGeom g, const uint32_t* keys,
-                                              uint32_t* mm_tmp, uint32_t* lo, uint32_t* hi) {
+// The steps below see the segment's keys through a visitor: visit(f) calls f(i, key) for
+// every entry of this thread's run (i = position in the run), whether the keys sit in LDS
+// (visit_run) or in registers (visit_regs).
+
+// Smallest and largest key of the segment (every thread gets both).
+template <typename Visit>
+__device__ __forceinline__ void key_range_by(Visit visit, uint32_t* mm_tmp, uint32_t* lo,
+                                             uint32_t* hi) {
   uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
-  visit_run(g, keys, [&](int, uint32_t kk) {
+  visit([&](int, uint32_t kk) {
     kmin = min(kmin, kk);
     kmax = max(kmax, kk);
   });
   block_min_max(kmin, kmax, mm_tmp, lo, hi);
 }
 
-// Radix select over the segment in LDS, keys in [lo, hi]: tau, the order key of the k-th
-// largest (0 < k < L), and `need`, how many keys equal to tau are taken.  Digits of up to
-// 11 bits over d = key - lo, within the bit width of the key range, so concentrated values
-// still spread over the whole first histogram.
-__device__ __forceinline__ void radix_tau(RunGeom g, const uint32_t* keys, int k,
-                                          uint32_t lo, uint32_t hi, uint32_t* hist,
-                                          int64_t* scan_tmp, int* s_bin, uint32_t* s_above,
-                                          uint32_t* tau_out, uint32_t* need_out) {
+// Smallest and largest order key of the segment in LDS.
+__device__ __forceinline__ void seg_key_range(RunGeom g, const uint32_t* keys,
+                                              uint32_t* mm_tmp, uint32_t* lo, uint32_t* hi) {
+  key_range_by([&](auto f) { visit_run(g, keys, f); }, mm_tmp, lo, hi);
+}
+
+// Radix select over the segment, keys in [lo, hi]: tau, the order key of the k-th largest
+// (0 < k < L), and `need`, how many keys equal to tau are taken.  Digits of up to 11 bits
+// over d = key - lo, within the bit width of the key range, so concentrated values still
+// spread over the whole first histogram.
+template <typename Visit>
+__device__ __forceinline__ void radix_tau_by(Visit visit, int k, uint32_t lo, uint32_t hi,
+                                             uint32_t* hist, int64_t* scan_tmp, int* s_bin,
+                                             uint32_t* s_above, uint32_t* tau_out,
+                                             uint32_t* need_out) {
   const int tid = threadIdx.x;
   const uint32_t range = hi - lo;
   int rem = range == 0 ? 0 : 32 - __clz(range);
@@ -362,7 +376,7 @@ __device__ __forceinline__ void radix_tau(RunGeom g, const uint32_t* keys, int k
     const int bits = rem < 11 ? rem : 11, sh = rem - bits, nbins = 1 << bits;
     for (int bb = tid; bb < nbins; bb += kSelectThreads) hist[bb] = 0;
     __syncthreads();
-    visit_run(g, keys, [&](int, uint32_t kk) {
+    visit([&](int, uint32_t kk) {
       const uint32_t dh = (kk - lo) >> sh;   // this digit and the ones above it
       // keys whose higher digits match the prefix found so far (none above the range)
       if ((dh >> bits) == prefix) atomicAdd(&hist[dh & (uint32_t)(nbins - 1)], 1u);
@@ -379,21 +393,24 @@ __device__ __forceinline__ void radix_tau(RunGeom g, const uint32_t* keys, int k
 
 // Kept entries: every key > tau, then the first `need` keys == tau, in index order.  The
 // run's greater / equal flags are kept as bit masks; one workgroup prefix sum of both counts
-// places each thread's kept indices, which are staged in LDS (over vals) and written out
-// coalesced.  When vout is given, vout[j] = vsrc[kept[j]] (vsrc in global memory).
-__device__ __forceinline__ void emit_kept(RunGeom g, uint32_t* keys, uint32_t tau,
-                                          uint32_t need, int k, int64_t* scan_tmp,
-                                          int32_t* __restrict__ kout, const float* vsrc,
-                                          float* __restrict__ vout) {
+// places each thread's kept indices, which are staged in LDS (`idx`, kSelectLdsKeys entries
+// at a time) and written out coalesced.  When vout is given, vout[j] = vsrc[kept[j]] (vsrc in
+// global memory).  Every read of the keys is done before idx is written: idx may overlay
+// them.
+template <typename Visit>
+__device__ __forceinline__ void emit_kept_by(Visit visit, RunGeom g, uint32_t tau,
+                                             uint32_t need, int k, int64_t* scan_tmp,
+                                             int32_t* idx, int32_t* __restrict__ kout,
+                                             const float* vsrc, float* __restrict__ vout) {
   uint64_t gtm = 0, eqm = 0;
-  visit_run(g, keys, [&](int i, uint32_t kk) {
+  visit([&](int i, uint32_t kk) {
     gtm |= (uint64_t)(kk > tau) << i;
     eqm |= (uint64_t)(kk == tau) << i;
   });
   const int64_t n_gt = __popcll(gtm), n_eq = __popcll(eqm);
   // the tied entries are taken in thread order, so the threads before this one took
   // min(need, eq_before) of them (each count sum < 2^32).  The scan's barriers also retire
-  // every thread's reads of vals above.
+  // every thread's reads of the keys above.
   int64_t tot;
   const int64_t ex = block_excl_scan_i64((n_eq << 32) | n_gt, scan_tmp, &tot);
   const int64_t eq_before = ex >> 32, gt_before = ex & 0xFFFFFFFFll;
@@ -401,16 +418,19 @@ __device__ __forceinline__ void emit_kept(RunGeom g, uint32_t* keys, uint32_t ta
   eq_take = eq_take < 0 ? 0 : (eq_take > n_eq ? n_eq : eq_take);
   for (int64_t drop = n_eq - eq_take; drop > 0; --drop)   // keep the first eq_take ties
     eqm &= ~(1ull << (63 - __clzll(eqm)));
-  uint64_t keep = gtm | eqm;
-  int32_t* idx = reinterpret_cast<int32_t*>(keys);
-  int pos = (int)(gt_before + (eq_before < (int64_t)need ? eq_before : (int64_t)need));
-  while (keep) {
-    idx[pos++] = g.t0 + __builtin_ctzll(keep);
-    keep &= keep - 1;
+  const uint64_t keep = gtm | eqm;
+  const int pos0 = (int)(gt_before + (eq_before < (int64_t)need ? eq_before : (int64_t)need));
+#pragma unroll 1
+  for (int b = 0; b < k; b += kSelectLdsKeys) {   // uniform: one chunk unless k > the LDS
+    const int nc = k - b < kSelectLdsKeys ? k - b : kSelectLdsKeys;
+    uint64_t m = keep;
+    for (int pos = pos0; m; ++pos, m &= m - 1)
+      if (pos >= b && pos < b + nc) idx[pos - b] = g.t0 + __builtin_ctzll(m);
+    __syncthreads();
+    copy_out_u32(nc, reinterpret_cast<const uint32_t*>(idx), kout + b, AsIs());
+    if (vout) gather_out_f32(nc, idx, vsrc, vout + b);
+    __syncthreads();
   }
-  __syncthreads();
-  copy_out_u32(k, reinterpret_cast<const uint32_t*>(idx), kout, AsIs());
-  if (vout) gather_out_f32(k, idx, vsrc, vout);
 }
 
 // TopK of the segment in LDS (0 <= k): indices to kout and, when vout is given, the kept
@@ -426,9 +446,11 @@ __device__ __forceinline__ void topk_lds(int L, int k, RunGeom g, uint32_t* keys
     return;
   }
   uint32_t lo, hi, tau, need;
-  seg_key_range(g, keys, mm_tmp, &lo, &hi);
-  radix_tau(g, keys, k, lo, hi, hist, scan_tmp, s_bin, s_above, &tau, &need);
-  emit_kept(g, keys, tau, need, k, scan_tmp, kout, vsrc, vout);
+  auto visit = [&](auto f) { visit_run(g, keys, f); };
+  key_range_by(visit, mm_tmp, &lo, &hi);
+  radix_tau_by(visit, k, lo, hi, hist, scan_tmp, s_bin, s_above, &tau, &need);
+  emit_kept_by(visit, g, tau, need, k, scan_tmp, reinterpret_cast<int32_t*>(keys), kout, vsrc,
+               vout);
 }
 
 // Segments that fit in LDS: stage, pool, pooled scores out, radix select, emit.
@@ -441,6 +463,107 @@ __device__ __forceinline__ void select_lds(int L, int k, int hw, const float* __
   const RunGeom g = run_geom(L);
   pool_in_lds(L, hw, g, vals, pout);
   topk_lds(L, k, g, vals, hist, scan_tmp, mm_tmp, s_bin, s_above, kout, nullptr, nullptr);
+}
+
+// ---- segments longer than the LDS capacity: keys in registers ---------------------------
+// Thread tid owns the run [t0, t0 + n) as above (odd stride, at most kRegRun entries) and
+// holds it in registers, with the pooling halo on either side.  LDS serves as the transpose
+// buffer of the coalesced loads and stores, kSelectLdsKeys entries at a time, and stages the
+// kept indices.  Windows up to 2 * kPoolHalo + 1.
+constexpr int kRegRun = 63;                                  // odd: conflict-free LDS strides
+constexpr int kSelectRegKeys = kRegRun * kSelectThreads;     // 64,512
+constexpr int kRegSlots = kRegRun + 2 * kPoolHalo;
+static_assert(kSelectRegKeys < 2 * kSelectLdsKeys, "a segment passes through LDS in two chunks");
+
+// r[j] = the raw score at position t0 - kPoolHalo + j where that position lies in
+// [t0 - kPoolHalo, t0 + n + kPoolHalo) and in [0, L); -inf elsewhere.
+__device__ __forceinline__ void stage_regs(int L, const float* __restrict__ in, RunGeom g,
+                                           uint32_t* vals, uint32_t (&r)[kRegSlots]) {
+  const int q0 = g.t0 - kPoolHalo;                 // position of r[0]
+  const int qlo = q0 < 0 ? 0 : q0;
+  const int qhi = g.n == 0 ? qlo : (g.t0 + g.n + kPoolHalo < L ? g.t0 + g.n + kPoolHalo : L);
+#pragma unroll
+  for (int j = 0; j < kRegSlots; ++j) r[j] = __float_as_uint(-__builtin_inff());
+#pragma unroll 1
+  for (int b = 0; b < L; b += kSelectLdsKeys) {   // uniform: two chunks
+    const int nc = L - b < kSelectLdsKeys ? L - b : kSelectLdsKeys;
+    stage_f32(nc, in + b, vals);
+    __syncthreads();
+    // slots [lo, hi) of this thread fall in the chunk [b, b + nc)
+    const int lo = (qlo > b ? qlo : b) - q0, hi = (qhi < b + nc ? qhi : b + nc) - q0;
+#pragma unroll
+    for (int j = 0; j < kRegSlots; ++j)
+      if (j >= lo && j < hi) r[j] = vals[q0 + j - b];
+    __syncthreads();
+  }
+}
+
+// Max-pool in place: r[i] becomes the order key of the pooled score of run entry i (which
+// needs r[i .. i + 2 * kPoolHalo], none of them overwritten yet), and 0 for i >= n.  Key 0
+// lies below the key of every float but one NaN pattern, so these padding entries rank
+// below every real entry: the visits below take all kRegRun slots with no per-entry
+// condition (such conditions would be kept as one lane mask per slot in scalar registers).
+__device__ __forceinline__ void pool_regs(int hw, int n, uint32_t (&r)[kRegSlots]) {
+#pragma unroll
+  for (int i = 0; i < kRegRun; ++i) {
+    float m = __uint_as_float(r[i + kPoolHalo]);
+#pragma unroll
+    for (int d = 1; d <= kPoolHalo; ++d)
+      if (d <= hw)
+        m = fmaxf(m, fmaxf(__uint_as_float(r[i + kPoolHalo - d]),
+                           __uint_as_float(r[i + kPoolHalo + d])));
+    r[i] = i < n ? order_key(m) : 0u;
+  }
+}
+
+// Every slot of the run, padding included (0 < k < L: the k-th largest key is a real one,
+// and padding keys never exceed or equal it).
+template <typename F>
+__device__ __forceinline__ void visit_regs(const uint32_t (&r)[kRegSlots], F f) {
+#pragma unroll
+  for (int i = 0; i < kRegRun; ++i) f(i, r[i]);
+}
+
+// The pooled scores out, through LDS a chunk at a time (coalesced stores).
+__device__ __forceinline__ void pooled_out_regs(int L, RunGeom g, const uint32_t (&r)[kRegSlots],
+                                                uint32_t* vals, float* pout) {
+#pragma unroll 1
+  for (int b = 0; b < L; b += kSelectLdsKeys) {
+    const int nc = L - b < kSelectLdsKeys ? L - b : kSelectLdsKeys;
+    // run entries [lo, hi) lie in the chunk
+    const int lo = b - g.t0 > 0 ? b - g.t0 : 0, hi = b + nc - g.t0 < g.n ? b + nc - g.t0 : g.n;
+#pragma unroll
+    for (int i = 0; i < kRegRun; ++i)
+      if (i >= lo && i < hi) vals[g.t0 + i - b] = r[i];
+    __syncthreads();
+    copy_out_u32(nc, vals, pout + b, KeyToFloatBits());
+    __syncthreads();
+  }
+}
+
+// kSelectLdsKeys < L <= kSelectRegKeys, hw <= kPoolHalo: stage, pool, pooled scores out,
+// radix select, emit -- the steps of select_lds with the keys in registers.
+__device__ __forceinline__ void select_regs(int L, int k, int hw, const float* __restrict__ in,
+                                            float* pout, int32_t* __restrict__ kout,
+                                            uint32_t* vals, uint32_t* hist, int64_t* scan_tmp,
+                                            uint32_t* mm_tmp, int* s_bin, uint32_t* s_above) {
+  const RunGeom g = run_geom(L);
+  uint32_t r[kRegSlots];
+  stage_regs(L, in, g, vals, r);
+  pool_regs(hw, g.n, r);
+  if (pout) pooled_out_regs(L, g, r, vals, pout);
+  if (k <= 0) return;
+  if (k >= L) {
+    for (int t = threadIdx.x; t < L; t += kSelectThreads) kout[t] = t;
+    return;
+  }
+  // the range's low end is 0 where a thread holds padding (the digits then also cover it)
+  uint32_t lo, hi, tau, need;
+  auto visit = [&](auto f) { visit_regs(r, f); };
+  key_range_by(visit, mm_tmp, &lo, &hi);
+  radix_tau_by(visit, k, lo, hi, hist, scan_tmp, s_bin, s_above, &tau, &need);
+  emit_kept_by(visit, g, tau, need, k, scan_tmp, reinterpret_cast<int32_t*>(vals), kout,
+               nullptr, nullptr);
 }
 
 // Segments longer than the LDS capacity: the same steps on the pooled scores in global
@@ -528,6 +651,8 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp,
   const int hw = dp.pool_window / 2;
   if (L <= kSelectLdsKeys)
     select_lds(L, k, hw, in, pout, kout, lds_keys, hist, scan_tmp, mm_tmp, &s_bin, &s_above);
+  else if (L <= kSelectRegKeys && hw <= kPoolHalo)
+    select_regs(L, k, hw, in, pout, kout, lds_keys, hist, scan_tmp, mm_tmp, &s_bin, &s_above);
   else
     select_global(L, k, hw, in, pout, kout, hist, scan_tmp, &s_bin, &s_above);
 }

@@ -108,16 +108,34 @@ def test_select_ties_and_plateaus_are_bit_exact():
     np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
 
 
-@pytest.mark.parametrize("window", [7, 9])
+@pytest.mark.parametrize("window", [1, 5, 7, 9])
 def test_select_long_segments_are_bit_exact(window):
-    """Segments at, just past and well past the LDS-resident length (38,400 keys) take both
-    select paths; window 7 uses the fixed 7-tap pool, 9 the general one."""
-    pb = custom(seq_lens=[38400, 38401, 50000], q_lens=[1, 1, 1], num_q_heads=1,
-                num_kv_heads=1, head_dim=64, budgets=[9600, 20000, 12345],
+    """Segments at and past the LDS-resident length (38,400 keys) take the three select
+    paths: LDS (<= 38,400), registers (<= 64,512 and windows <= 7) and global memory (longer,
+    or window 9).  Budgets past 38,400 kept entries write the indices in two chunks."""
+    pb = custom(seq_lens=[38400, 38401, 50000, 64512, 64513], q_lens=[1] * 5, num_q_heads=1,
+                num_kv_heads=1, head_dim=64, budgets=[9600, 20000, 12345, 50000, 64512],
                 pool_window=window, spike_frac=0.0)
     rng = np.random.default_rng(11)
     raw = (rng.standard_exponential(oracle.num_scores(pb)) * 1e-3).astype(np.float32)
     raw[::97] = raw[5]   # a plateau of equal values across the threshold region
+    bp, t = to_dev(pb)
+    kept, pooled = actkv.select(bp, torch.from_numpy(raw).cuda())
+    np.testing.assert_array_equal(pooled.cpu().numpy(), oracle.pool(pb, raw))
+    np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
+
+
+@pytest.mark.parametrize("L,k", [(40000, 1), (40000, 39999), (47104, 23552), (64511, 777)])
+def test_register_select_on_signed_and_tied_scores(L, k):
+    """The register-resident path (38,400 < L <= 64,512) on scores of both signs (the key
+    range spans all 32 bits), signed zeros and runs of equal values, at extreme budgets."""
+    pb = custom(seq_lens=[L], q_lens=[1], num_q_heads=1, num_kv_heads=1, head_dim=64,
+                budgets=[k], pool_window=7, spike_frac=0.0)
+    rng = np.random.default_rng(L + k)
+    raw = rng.standard_normal(L).astype(np.float32)
+    raw[rng.random(L) < 0.2] = 0.0
+    raw[rng.random(L) < 0.1] = np.float32(-0.0)
+    raw[rng.random(L) < 0.2] = np.float32(0.5)
     bp, t = to_dev(pb)
     kept, pooled = actkv.select(bp, torch.from_numpy(raw).cuda())
     np.testing.assert_array_equal(pooled.cpu().numpy(), oracle.pool(pb, raw))
