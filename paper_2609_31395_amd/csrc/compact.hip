@@ -36,6 +36,8 @@ __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
   constexpr int CH = D / 8;                 // 16-byte chunks per row
   __shared__ int64_t src_slot[kCompactTable];   // flat source slot, -1: nothing to copy
   __shared__ int64_t dst_page[kCompactTable / kPageSize];
+  __shared__ int16_t live[kCompactTable];       // the entries with a source, ascending
+  __shared__ int wave_live[kCompactThreads / 64];
   const int Hkv = dp.Hkv;
   const int ppw = compact_pages_per_wg(Hkv);
   const int64_t f0 = (int64_t)blockIdx.x * ppw;
@@ -76,10 +78,32 @@ __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
   }
   __syncthreads();
 
-  // ---- copy: consecutive threads move consecutive 16-byte chunks of the destination pages
-  // (K half, then V half), so every store is part of a contiguous run
+  // ---- the entries that copy a row, in ascending order (with unequal head budgets or in
+  // place, many slots of a destination page receive nothing; the copy loop skips them)
+  int n_live = 0;   // uniform
+  for (int e0 = 0; e0 < entries; e0 += kCompactThreads) {
+    const int e = e0 + (int)threadIdx.x, w = threadIdx.x >> 6;
+    const bool has = e < entries && src_slot[e] >= 0;
+    const uint64_t bal = __ballot(has);
+    if ((threadIdx.x & 63) == 0) wave_live[w] = __popcll(bal);
+    __syncthreads();
+    int before = n_live, total = 0;
+    for (int i = 0; i < kCompactThreads / 64; ++i) {
+      before += i < w ? wave_live[i] : 0;
+      total += wave_live[i];
+    }
+    if (has)
+      live[before + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u))] =
+          (int16_t)e;
+    n_live += total;
+    __syncthreads();
+  }
+
+  // ---- copy: consecutive threads move consecutive 16-byte chunks of the live rows (K half,
+  // then V half), so the stores of a destination page form contiguous runs
   const int64_t plane = dp.num_pages * kPageSize * Hkv * (int64_t)D;   // K -> V offset
-  const int rows = 2 * entries;
+  const int rows = 2 * n_live;
   const int items = rows * CH;
   constexpr int kBatch = 16;
   for (int base = 0; base < items; base += kCompactThreads * kBatch) {
@@ -91,7 +115,7 @@ __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
       const int it = base + kCompactThreads * u + threadIdx.x;
       if (it >= items) continue;
       const int row = it / CH, ch = it % CH;
-      const int which = row / entries, e = row % entries;
+      const int which = row / n_live, e = live[row % n_live];
       const int p = e / (kPageSize * Hkv), s = (e / Hkv) % kPageSize, h = e % Hkv;
       const int64_t src = src_slot[e], dpg = dst_page[p];
       if (src < 0 || dpg < 0) continue;
