@@ -213,7 +213,8 @@ actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
  * enter with 0 (step 2 is the caller's concatenation).  hit (nullable): uint8 [num_scores],
  * 1 = hit.  ks_kept: fp32 [num_kept].  top_p and decay in [0, 1] (else
  * ACTKV_ERR_INVALID_ARGUMENT).  ks must not overlap scores or pooled.  Segments longer than
- * 38,400 entries: ACTKV_ERR_UNSUPPORTED.  The mass sums are exact 64-bit fixed-point sums of
+ * 64,512 entries, or longer than 38,400 with a pool_window above 7: ACTKV_ERR_UNSUPPORTED.
+ * The mass sums are exact 64-bit fixed-point sums of
  * the scores scaled by a power of two (deterministic); where the prefix boundary falls within
  * that resolution of the target, the boundary entry may differ from a floating-point
  * evaluation.

@@ -119,8 +119,11 @@ hipError_t launch_score_decode(const DevProblem& dp, const HostPlan& hp, const v
                                hipStream_t s);
 hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
                          float* pooled, int32_t* kept, hipStream_t s);
-// LRFU selection (attention-aware keep scores): segments up to kLrfuMaxLen entries.
-constexpr int64_t kLrfuMaxLen = 38400;
+// LRFU selection (attention-aware keep scores): segments up to kLrfuMaxLen entries; those
+// longer than kLrfuLdsLen only with pooling windows up to kLrfuRegMaxWindow.
+constexpr int64_t kLrfuLdsLen = 38400;
+constexpr int64_t kLrfuMaxLen = 64512;
+constexpr int kLrfuRegMaxWindow = 7;
 hipError_t launch_lrfu_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
                               float top_p, float decay, float* ks, uint8_t* hit, float* pooled,
                               int32_t* kept, float* ks_kept, hipStream_t s);

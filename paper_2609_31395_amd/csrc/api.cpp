@@ -272,6 +272,8 @@ actkv_status check_lrfu(const Ctx& cx, float top_p, float decay, const float* sc
   if (!(top_p >= 0.0f && top_p <= 1.0f) || !(decay >= 0.0f && decay <= 1.0f))
     return ACTKV_ERR_INVALID_ARGUMENT;
   if (cx.hp.max_L > actkv::kLrfuMaxLen) return ACTKV_ERR_UNSUPPORTED;
+  if (cx.hp.max_L > actkv::kLrfuLdsLen && cx.dp.pool_window > actkv::kLrfuRegMaxWindow)
+    return ACTKV_ERR_UNSUPPORTED;
   if (cx.hp.num_scores > 0 && !ks) return ACTKV_ERR_INVALID_ARGUMENT;
   if (cx.hp.num_kept > 0 && (!kept || !ks_kept)) return ACTKV_ERR_INVALID_ARGUMENT;
   if (ks && (ks == scores || ks == pooled)) return ACTKV_ERR_INVALID_ARGUMENT;

@@ -31,7 +31,7 @@ namespace {
 
 constexpr int kSelectThreads = 1024;
 constexpr int kSelectLdsKeys = 38400;     // segment length kept in LDS (153,600 bytes)
-static_assert(kSelectLdsKeys == kLrfuMaxLen, "the LRFU selection runs on the LDS path only");
+static_assert(kSelectLdsKeys == kLrfuLdsLen, "LRFU segments up to this length stay in LDS");
 constexpr int kMaxBins = 2048;            // largest digit: 11 bits
 constexpr int kDigits = 3;                // bits 31..21, 20..10, 9..0
 constexpr int kRows = (kSelectLdsKeys + kSelectThreads - 1) / kSelectThreads;   // 38
@@ -474,6 +474,8 @@ constexpr int kRegRun = 63;                                  // odd: conflict-fr
 constexpr int kSelectRegKeys = kRegRun * kSelectThreads;     // 64,512
 constexpr int kRegSlots = kRegRun + 2 * kPoolHalo;
 static_assert(kSelectRegKeys < 2 * kSelectLdsKeys, "a segment passes through LDS in two chunks");
+static_assert(kSelectRegKeys == kLrfuMaxLen && 2 * kPoolHalo + 1 == kLrfuRegMaxWindow,
+              "the LRFU selection's limits are those of the register-resident path");
 
 // r[j] = the raw score at position t0 - kPoolHalo + j where that position lies in
 // [t0 - kPoolHalo, t0 + n + kPoolHalo) and in [0, L); -inf elsewhere.
@@ -517,11 +519,18 @@ __device__ __forceinline__ void pool_regs(int hw, int n, uint32_t (&r)[kRegSlots
 }
 
 // Every slot of the run, padding included (0 < k < L: the k-th largest key is a real one,
-// and padding keys never exceed or equal it).
+// and padding keys never exceed or equal it).  Each key passes through an empty asm
+// statement, so nothing computed from the keys in one visit is kept for the next (the
+// compiler would otherwise hoist per-slot values out of the radix loops, 63 of them at a
+// time, and spill).
 template <typename F>
 __device__ __forceinline__ void visit_regs(const uint32_t (&r)[kRegSlots], F f) {
 #pragma unroll
-  for (int i = 0; i < kRegRun; ++i) f(i, r[i]);
+  for (int i = 0; i < kRegRun; ++i) {
+    uint32_t kk = r[i];
+    asm volatile("" : "+v"(kk));
+    f(i, kk);
+  }
 }
 
 // The pooled scores out, through LDS a chunk at a time (coalesced stores).
@@ -680,28 +689,28 @@ __device__ __forceinline__ uint64_t fixed_mass(uint32_t key, int S) {
   return sh >= 0 ? sig << sh : (sh > -64 ? sig >> -sh : 0ull);
 }
 
-// Replace the key of each pooled score of this thread's run by the key of its contribution:
-// the score where keep(key) holds, else 0 (keep sees the run in index order).
-template <typename Keep>
-__device__ __forceinline__ void keep_contributions(RunGeom g, uint32_t* keys, Keep keep) {
+// The top-p hit mask turned into contributions: every key of the run is replaced by the key
+// of its contribution, the pooled score where it is hit, else 0.  visit(f) reads the keys as
+// in the selection; rewrite(f) replaces each key kk of the run by f(kk), in index order.
+template <typename Visit, typename Rewrite>
+__device__ __forceinline__ void topp_contributions_by(int L, Visit visit, Rewrite rewrite,
+                                                      float top_p, uint64_t* hist64,
+                                                      int64_t* scan_tmp, uint32_t* mm_tmp,
+                                                      int* s_bin, uint64_t* s_above) {
   constexpr uint32_t kZero = 0x80000000u;   // order_key(0.0f)
-  visit_run(g, keys, [&](int i, uint32_t kk) { keys[g.t0 + i] = keep(kk) ? kk : kZero; });
-}
-
-__device__ __forceinline__ void topp_contributions(int L, RunGeom g, uint32_t* keys, float top_p,
-                                                   uint64_t* hist64, int64_t* scan_tmp,
-                                                   uint32_t* mm_tmp, int* s_bin,
-                                                   uint64_t* s_above) {
+  auto keep_contributions = [&](auto keep) {
+    rewrite([&](uint32_t kk) { return keep(kk) ? kk : kZero; });
+  };
   const int tid = threadIdx.x;
   uint32_t lo, hi;
-  seg_key_range(g, keys, mm_tmp, &lo, &hi);   // its barriers retire the pooled copy-out
+  key_range_by(visit, mm_tmp, &lo, &hi);   // its barriers retire the pooled copy-out
   const float vmax = key_value(hi);
   if (!(vmax > 0.f) || !(top_p > 0.f)) {   // no positive mass to reach
-    keep_contributions(g, keys, [](uint32_t) { return false; });
+    keep_contributions([](uint32_t) { return false; });
     return;
   }
   if (top_p >= 1.f) {   // the whole mass: every entry with a positive score
-    keep_contributions(g, keys, [](uint32_t kk) { return kk > 0x80000000u; });
+    keep_contributions([](uint32_t kk) { return kk > 0x80000000u; });
     return;
   }
   int e;
@@ -709,13 +718,19 @@ __device__ __forceinline__ void topp_contributions(int L, RunGeom g, uint32_t* k
   const int lg = 32 - __clz((uint32_t)L + 1u);   // L + 1 <= 2^lg
   const int S = 62 - e - lg;                     // total < L * 2^(e + S) < 2^62
   uint64_t mine = 0;
-  visit_run(g, keys, [&](int, uint32_t kk) { mine += fixed_mass(kk, S); });
+  // each mass passes through an empty asm statement before it is added: the sum then runs
+  // slot by slot instead of all of a run's 64-bit masses being held at once
+  visit([&](int, uint32_t kk) {
+    uint64_t m = fixed_mass(kk, S);
+    asm volatile("" : "+v"(m));
+    mine += m;
+  });
   int64_t total;
   block_excl_scan_i64((int64_t)mine, scan_tmp, &total);
   const double want = ceil((double)top_p * (double)total);
   uint64_t need = want > 0.0 ? (uint64_t)want : 0ull;
   if (need == 0) {
-    keep_contributions(g, keys, [](uint32_t) { return false; });
+    keep_contributions([](uint32_t) { return false; });
     return;
   }
   // radix search over d = key - lo with 10-bit digits, masses as weights
@@ -728,10 +743,11 @@ __device__ __forceinline__ void topp_contributions(int L, RunGeom g, uint32_t* k
     for (int bb = tid; bb < nbins; bb += kSelectThreads) hist64[bb] = 0;
     if (tid == 0) { *s_bin = 0; *s_above = 0; }
     __syncthreads();
-    visit_run(g, keys, [&](int, uint32_t kk) {
+    visit([&](int, uint32_t kk) {
       const uint32_t dh = (kk - lo) >> sh;
       if ((dh >> bits) == prefix) {
-        const uint64_t m = fixed_mass(kk, S);
+        uint64_t m = fixed_mass(kk, S);
+        asm volatile("" : "+v"(m));
         if (m != 0)
           atomicAdd((unsigned long long*)&hist64[dh & (uint32_t)(nbins - 1)],
                     (unsigned long long)m);
@@ -750,17 +766,28 @@ __device__ __forceinline__ void topp_contributions(int L, RunGeom g, uint32_t* k
   // target: the first ceil(need / m) of them
   const uint64_t m_tau = fixed_mass(tau, S);
   uint32_t n_eq = 0;
-  visit_run(g, keys, [&](int, uint32_t kk) { n_eq += kk == tau; });
+  visit([&](int, uint32_t kk) { n_eq += kk == tau; });
   int64_t eq_total;
   const int64_t eq_before = block_excl_scan_i64(n_eq, scan_tmp, &eq_total);
   const int64_t take = m_tau == 0 ? eq_total : (int64_t)((need + m_tau - 1) / m_tau);
   int64_t rank = eq_before;
-  keep_contributions(g, keys, [&](uint32_t kk) {
+  keep_contributions([&](uint32_t kk) {
     const bool eq = kk == tau;
     const bool h = kk > tau || (eq && rank < take);
     rank += eq ? 1 : 0;
     return h;
   });
+}
+
+// The same over the segment's keys in LDS.
+__device__ __forceinline__ void topp_contributions(int L, RunGeom g, uint32_t* keys, float top_p,
+                                                   uint64_t* hist64, int64_t* scan_tmp,
+                                                   uint32_t* mm_tmp, int* s_bin,
+                                                   uint64_t* s_above) {
+  topp_contributions_by(
+      L, [&](auto f) { visit_run(g, keys, f); },
+      [&](auto f) { visit_run(g, keys, [&](int i, uint32_t kk) { keys[g.t0 + i] = f(kk); }); },
+      top_p, hist64, scan_tmp, mm_tmp, s_bin, s_above);
 }
 
 // KS' = decay * KS + contribution, each operation rounded to fp32, over the whole segment
@@ -817,8 +844,76 @@ __device__ __forceinline__ void lrfu_lds(int L, int k, int hw, float top_p, floa
            s_above32, kout, ks, ks_kept);
 }
 
+// keep_score_update with the run in registers (contribution keys in, KS' keys out; padding
+// slots stay 0): ks passes through LDS a chunk at a time, coalesced both ways; the hit flags
+// are stored from the registers.
+__device__ __forceinline__ void keep_score_update_regs(int L, float decay, float* ks,
+                                                       uint8_t* hit_out, RunGeom g,
+                                                       uint32_t (&r)[kRegSlots], uint32_t* vals) {
+#pragma unroll 1
+  for (int b = 0; b < L; b += kSelectLdsKeys) {   // uniform: two chunks
+    const int nc = L - b < kSelectLdsKeys ? L - b : kSelectLdsKeys;
+    stage_f32(nc, ks + b, vals);
+    __syncthreads();
+    const int lo = b - g.t0 > 0 ? b - g.t0 : 0, hi = b + nc - g.t0 < g.n ? b + nc - g.t0 : g.n;
+#pragma unroll
+    for (int i = 0; i < kRegRun; ++i)
+      if (i >= lo && i < hi) {
+        const int p = g.t0 + i - b;
+        const float c = key_value(r[i]);
+        const float nk = __fadd_rn(__fmul_rn(decay, __uint_as_float(vals[p])), c);
+        vals[p] = __float_as_uint(nk);
+        r[i] = order_key(nk);
+        if (hit_out) hit_out[g.t0 + i] = c > 0.0f ? 1 : 0;
+      }
+    __syncthreads();
+    copy_out_u32(nc, vals, ks + b, AsIs());
+    __syncthreads();   // also makes this workgroup's writes of ks visible to its own reads
+  }
+}
+
+// lrfu_lds for kLrfuLdsLen < L <= kSelectRegKeys, hw <= kPoolHalo, with the keys in registers.
+__device__ __forceinline__ void lrfu_regs(int L, int k, int hw, float top_p, float decay,
+                                          const float* __restrict__ in, float* pout, float* ks,
+                                          uint8_t* hit_out, int32_t* __restrict__ kout,
+                                          float* __restrict__ ks_kept, uint32_t* vals,
+                                          uint64_t* hist64, int64_t* scan_tmp, uint32_t* mm_tmp,
+                                          int* s_bin, uint32_t* s_above32, uint64_t* s_above64) {
+  const RunGeom g = run_geom(L);
+  uint32_t r[kRegSlots];
+  stage_regs(L, in, g, vals, r);
+  pool_regs(hw, g.n, r);
+  if (pout) pooled_out_regs(L, g, r, vals, pout);
+  auto visit = [&](auto f) { visit_regs(r, f); };
+  auto rewrite = [&](auto f) {
+#pragma unroll
+    for (int i = 0; i < kRegRun; ++i) r[i] = r[i] == 0u ? 0u : f(r[i]);   // padding stays 0
+  };
+  topp_contributions_by(L, visit, rewrite, top_p, hist64, scan_tmp, mm_tmp, s_bin, s_above64);
+  __syncthreads();
+  keep_score_update_regs(L, decay, ks, hit_out, g, r, vals);
+  if (k <= 0) return;
+  if (k >= L) {
+    for (int t = threadIdx.x; t < L; t += kSelectThreads) {
+      kout[t] = t;
+      ks_kept[t] = ks[t];
+    }
+    return;
+  }
+  uint32_t lo, hi, tau, need;
+  key_range_by(visit, mm_tmp, &lo, &hi);
+  radix_tau_by(visit, k, lo, hi, reinterpret_cast<uint32_t*>(hist64), scan_tmp, s_bin,
+               s_above32, &tau, &need);
+  emit_kept_by(visit, g, tau, need, k, scan_tmp, reinterpret_cast<int32_t*>(vals), kout, ks,
+               ks_kept);
+}
+
 }  // namespace
 
+// kLong = false: the segments that fit in LDS; kLong = true: the longer ones (a separate
+// kernel, launched only when there are any: the register-resident path needs far more
+// registers than the LDS path, which keeps its own allocation).
+template <bool kLong>
 __global__ __launch_bounds__(kSelectThreads) void lrfu_select_kernel(
     DevProblem dp, const float* __restrict__ scores, float top_p, float decay, float* ks,
     uint8_t* hit, float* pooled, int32_t* __restrict__ kept, float* ks_kept) {
@@ -837,9 +932,16 @@ __global__ __launch_bounds__(kSelectThreads) void lrfu_select_kernel(
   const int k = b < L ? b : L;
   const int64_t seg = pl.seg_off + (int64_t)h * L;
   const int64_t koff = dp.kept_off[r * Hkv + h];
-  lrfu_lds(L, k, dp.pool_window / 2, top_p, decay, scores + seg,
-           pooled ? pooled + seg : nullptr, ks + seg, hit ? hit + seg : nullptr, kept + koff,
-           ks_kept + koff, lds_keys, hist64, scan_tmp, mm_tmp, &s_bin, &s_above32, &s_above64);
+  const int hw = dp.pool_window / 2;
+  // the host rejects segments past kSelectRegKeys, and past the LDS with wider windows
+  if (!kLong && L <= kSelectLdsKeys)
+    lrfu_lds(L, k, hw, top_p, decay, scores + seg, pooled ? pooled + seg : nullptr, ks + seg,
+             hit ? hit + seg : nullptr, kept + koff, ks_kept + koff, lds_keys, hist64, scan_tmp,
+             mm_tmp, &s_bin, &s_above32, &s_above64);
+  else if (kLong && L > kSelectLdsKeys && L <= kSelectRegKeys && hw <= kPoolHalo)
+    lrfu_regs(L, k, hw, top_p, decay, scores + seg, pooled ? pooled + seg : nullptr, ks + seg,
+              hit ? hit + seg : nullptr, kept + koff, ks_kept + koff, lds_keys, hist64,
+              scan_tmp, mm_tmp, &s_bin, &s_above32, &s_above64);
 }
 
 hipError_t launch_lrfu_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
@@ -848,13 +950,20 @@ hipError_t launch_lrfu_select(const DevProblem& dp, const HostPlan& hp, const fl
   if (hp.R == 0) return hipSuccess;
   const int64_t keys = hp.max_L < kSelectLdsKeys ? hp.max_L : kSelectLdsKeys;
   const size_t lds = (size_t)(keys + kLdsPad) * sizeof(uint32_t);
+  const bool any_long = hp.max_L > kSelectLdsKeys;
   if (lds > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void*)lrfu_select_kernel,
+    hipError_t e = hipFuncSetAttribute((const void*)lrfu_select_kernel<false>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e == hipSuccess && any_long)
+      e = hipFuncSetAttribute((const void*)lrfu_select_kernel<true>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(lrfu_select_kernel, dim3(hp.Hkv, hp.R), dim3(kSelectThreads), lds, s, dp,
-                     scores, top_p, decay, ks, hit, pooled, kept, ks_kept);
+  hipLaunchKernelGGL(lrfu_select_kernel<false>, dim3(hp.Hkv, hp.R), dim3(kSelectThreads), lds, s,
+                     dp, scores, top_p, decay, ks, hit, pooled, kept, ks_kept);
+  if (any_long)
+    hipLaunchKernelGGL(lrfu_select_kernel<true>, dim3(hp.Hkv, hp.R), dim3(kSelectThreads), lds,
+                       s, dp, scores, top_p, decay, ks, hit, pooled, kept, ks_kept);
   return hipGetLastError();
 }
 

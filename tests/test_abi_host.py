@@ -169,16 +169,22 @@ def test_lrfu_entry_points_validate_before_launching():
                                None) == -4
 
 
-def test_lrfu_rejects_segments_past_its_length_limit():
+@pytest.mark.parametrize("L,window,code", [(64513, 7, -2), (38401, 9, -2), (64512, 7, -1),
+                                           (38400, 9, -1)])
+def test_lrfu_rejects_segments_past_its_length_limit(L, window, code):
+    """Up to 38,400 entries any window; up to 64,512 windows of at most 7; longer segments are
+    unsupported (-2).  The call passes no keep-score buffer, which the library checks right
+    after the lengths: an accepted length then reports that missing argument (-1) instead,
+    and nothing is ever launched."""
     lib = actkv.load_library()
-    pb = W.make_custom(seq_lens=[38401], q_lens=[1], num_q_heads=1, num_kv_heads=1,
-                       head_dim=64, budgets=[10])
+    pb = W.make_custom(seq_lens=[L], q_lens=[1], num_q_heads=1, num_kv_heads=1,
+                       head_dim=64, budgets=[10], pool_window=window)
     p = binding_problem(pb)
     c = p.cstruct()
     c.seq_lens_d = c.q_lens_d = c.budgets_d = FAKE
     ws = actkv.query(p)["workspace_bytes"]
-    assert lib.actkv_lrfu_select(ctypes.byref(c), FAKE, 0.9, 0.5, FAKE + 64, None, None, FAKE,
-                                 FAKE, FAKE, ws, None) == -2
+    assert lib.actkv_lrfu_select(ctypes.byref(c), FAKE, 0.9, 0.5, None, None, None, FAKE,
+                                 FAKE, FAKE, ws, None) == code
 
 
 def test_inplace_page_accounting_matches_oracle():

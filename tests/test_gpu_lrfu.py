@@ -111,6 +111,22 @@ def test_lrfu_select_long_segment_at_the_limit():
     check_stage(pb, raw, ks_in, 0.9, 0.5)
 
 
+@pytest.mark.parametrize("top_p,decay", [(0.9, 0.5), (1.0, 0.25), (0.0, 0.5)])
+def test_lrfu_select_segments_past_the_lds(top_p, decay):
+    """Segments of 38,401-64,512 entries (register-resident keys, a kernel of their own)
+    beside one that fits in LDS: budgets past 38,400 kept entries, one keeping everything,
+    one keeping nothing, windows of 7."""
+    L = [38401, 64512, 50000, 1000, 40000]
+    pb = W.make_custom(seq_lens=L, q_lens=[1] * 5, num_q_heads=1, num_kv_heads=1, head_dim=64,
+                       budgets=[9600, 50000, 0, 300, 40000], pool_window=7)
+    rng = np.random.default_rng(13)
+    n = sum(L)
+    raw = rng.lognormal(-10, 2.0, size=n).astype(np.float32)
+    raw[rng.random(n) < 0.05] = 0.0
+    ks_in = (rng.lognormal(-10, 2.0, size=n) * (rng.random(n) < 0.7)).astype(np.float32)
+    check_stage(pb, raw, ks_in, top_p, decay)
+
+
 @pytest.mark.parametrize("case", ["tiny_config", "ragged_g4_d128", "two_row_chunks_g8",
                                   "short_and_empty"])
 def test_step_lrfu_end_to_end(case):
