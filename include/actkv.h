@@ -155,7 +155,8 @@ actkv_status actkv_score_accumulate(const actkv_problem* p, const void* q, const
  * k_rh = min(budget_rh, L_r) entries with the largest pooled score are kept, ties going
  * to the lower token index, and written ascending into `kept` ([num_kept] int32).
  * pooled (nullable): fp32, same layout as scores, receives the max-pooled scores
- * (pool_window 1 copies them).  scores is not modified.
+ * (pool_window 1 copies them; -0 is written as +0).  scores is not modified.  Scores may
+ * be any fp32 values but NaN (NaN scores give unspecified selections, never a fault).
  */
 actkv_status actkv_select(const actkv_problem* p, const float* scores, float* pooled,
                           int32_t* kept, void* workspace, size_t workspace_bytes,
