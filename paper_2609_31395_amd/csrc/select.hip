@@ -586,7 +586,7 @@ __device__ __forceinline__ void select_global(int L, int k, int hw, const float*
     const int lo = t - hw < 0 ? 0 : t - hw, hi = t + hw >= L ? L - 1 : t + hw;
     float m = in[t];
     for (int x = lo; x <= hi; ++x) m = fmaxf(m, in[x]);
-    pout[t] = m;
+    pout[t] = canonical(m);   // -0 as +0, as the other paths write it
   }
   __threadfence_block();
   __syncthreads();

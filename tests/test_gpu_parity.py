@@ -142,6 +142,24 @@ def test_register_select_on_signed_and_tied_scores(L, k):
     np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
 
 
+@pytest.mark.parametrize("L,window", [(1000, 7), (40000, 7), (40000, 9), (64513, 3)])
+def test_pooled_scores_write_zero_as_positive_zero(L, window):
+    """Every select path (LDS, registers, global memory) writes a pooled -0 as +0 and keeps
+    the oracle's selection on signed zeros."""
+    pb = custom(seq_lens=[L], q_lens=[1], num_q_heads=1, num_kv_heads=1, head_dim=64,
+                budgets=[L // 3], pool_window=window, spike_frac=0.0)
+    rng = np.random.default_rng(L + window)
+    raw = np.where(rng.random(L) < 0.5, np.float32(-0.0), np.float32(0.0)).astype(np.float32)
+    raw[rng.random(L) < 0.2] = np.float32(-1.5)
+    raw[rng.random(L) < 0.01] = np.float32(2.0)
+    bp, t = to_dev(pb)
+    kept, pooled = actkv.select(bp, torch.from_numpy(raw).cuda())
+    got = pooled.cpu().numpy()
+    assert not np.any((got == 0) & np.signbit(got))
+    np.testing.assert_array_equal(got, oracle.pool(pb, raw))
+    np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
+
+
 @pytest.mark.parametrize("case", sorted(CASES))
 def test_compact_is_bit_exact_given_the_oracle_selection(case):
     pb = CASES[case]()
