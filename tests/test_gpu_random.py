@@ -1,0 +1,71 @@
+"""Seeded random problems through the whole step, each against the oracle: request counts,
+lengths (empty and single-token requests included), query counts, GQA groups, head dims,
+pooling windows, budgets (zero, partial, at and past the length), causal and non-causal,
+SUM and MAX_MEAN, the LSE supplied or computed by the library.  Scores within 2e-3
+relative; pooling and selection exact functions of the GPU scores; compaction bit-exact."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import assert_compaction_matches, assert_scores_close, to_dev
+from paper_2609_31395_amd import actkv
+from paper_2609_31395_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _random_problem(seed):
+    rng = np.random.default_rng(10_000 + seed)
+    R = int(rng.integers(1, 5))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 3, 4, 8, 16]))
+    D = int(rng.choice([64, 128]))
+    causal = bool(rng.random() < 0.8)
+    L = rng.integers(0, 3000, size=R)
+    L[rng.random(R) < 0.15] = 0
+    L[rng.random(R) < 0.1] = 1
+    if causal:
+        n = np.array([int(rng.integers(0, min(l, 80) + 1)) for l in L])
+    else:
+        n = rng.integers(0, 81, size=R)
+    b = rng.integers(0, np.maximum(L, 1)[:, None] + 10, size=(R, Hkv))
+    b[rng.random((R, Hkv)) < 0.1] = 0
+    window = int(rng.choice([1, 3, 5, 7, 9]))
+    agg = "max_mean" if (G in (1, 2, 4, 8, 16) and rng.random() < 0.3) else "sum"
+    supplied = bool(rng.random() < 0.5)
+    pb = W.make_custom(seq_lens=L, q_lens=n, num_q_heads=G * Hkv, num_kv_heads=Hkv,
+                       head_dim=D, budgets=b.reshape(-1), pool_window=window,
+                       spike_frac=0.02, seed=seed, causal=causal)
+    return pb, agg, supplied
+
+
+@pytest.mark.parametrize("seed", range(150))
+def test_random_problem_step_matches_the_oracle(seed):
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    actkv.load_library()
+    pb, agg, supplied = _random_problem(seed)
+    lse = oracle.lse(pb).astype(np.float32) if supplied else None
+    bp, t = to_dev(pb, agg=agg)
+    n_sc = actkv.num_scores(bp)
+    qy = actkv.query(bp)
+    scores = torch.empty(max(n_sc, 1), dtype=torch.float32, device="cuda")
+    pooled = torch.empty_like(scores)
+    kept = torch.empty(max(qy["num_kept"], 1), dtype=torch.int32, device="cuda")
+    res = actkv.step(bp, t["q"], t["kv"], t["bt"], t["free"],
+                     lse=None if lse is None else torch.from_numpy(lse).cuda(),
+                     scores=scores, pooled=pooled, kept=kept)
+    torch.cuda.synchronize()
+    what = (f"seed {seed}: R={pb.num_reqs} L={pb.seq_lens.tolist()} n={pb.q_lens.tolist()} "
+            f"Hq/Hkv={pb.num_q_heads}/{pb.num_kv_heads} D={pb.head_dim} w={pb.pool_window} "
+            f"{agg} causal={pb.causal} lse={'supplied' if supplied else 'library'}")
+    raw_ref = oracle.scores(pb, lse_in=lse, agg=agg)
+    got = scores[:n_sc].cpu().numpy()
+    assert_scores_close(got, raw_ref, what=what)
+    pooled_gpu = pooled[:n_sc].cpu().numpy()
+    np.testing.assert_array_equal(pooled_gpu, oracle.pool(pb, got), err_msg=what)
+    kept_gpu = res["kept"].cpu().numpy()
+    np.testing.assert_array_equal(kept_gpu, oracle.select(pb, pooled_gpu), err_msg=what)
+    assert_compaction_matches(pb, kept_gpu, pb.kv, t["kv"].cpu().numpy().view(np.uint16),
+                              t["bt"].cpu().numpy(), res["freed"].cpu().numpy(),
+                              res["new_lens"].cpu().numpy())
