@@ -2,7 +2,9 @@
 lengths (empty and single-token requests included), query counts, GQA groups, head dims,
 pooling windows, budgets (zero, partial, at and past the length), causal and non-causal,
 SUM and MAX_MEAN, the LSE supplied or computed by the library.  Scores within 2e-3
-relative; pooling and selection exact functions of the GPU scores; compaction bit-exact."""
+relative; pooling and selection exact functions of the GPU scores; compaction bit-exact.
+The same problems also go through the in-place compaction (given the oracle's selection)
+and, with one query per request, through the decode-step scoring."""
 import numpy as np
 import pytest
 import torch
@@ -69,3 +71,37 @@ def test_random_problem_step_matches_the_oracle(seed):
     assert_compaction_matches(pb, kept_gpu, pb.kv, t["kv"].cpu().numpy().view(np.uint16),
                               t["bt"].cpu().numpy(), res["freed"].cpu().numpy(),
                               res["new_lens"].cpu().numpy())
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_problem_inplace_compaction_matches_the_oracle(seed):
+    """The in-place compaction (Alg. 4) of the oracle's selection on the same random
+    problems: the whole cache, block tables, freed lists, lengths and slot order exact."""
+    from test_gpu_inplace import _assert_same, _run_inplace
+    pb, agg, _ = _random_problem(seed)
+    kept = oracle.select(pb, oracle.pool(pb, oracle.scores(pb, agg=agg)))
+    _assert_same(_run_inplace(pb, kept), oracle.compact_inplace(pb, kept))
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_decode_step_matches_the_oracle(seed):
+    """One action query per request (the decode-step scoring kernel when G <= 16), added
+    twice to an aggregate that starts at zero: twice the oracle's scores."""
+    pb, agg, _ = _random_problem(seed)
+    if not pb.causal:
+        pytest.skip("decode steps are causal")
+    n1 = np.minimum(pb.q_lens, 1).astype(np.int32)
+    pb1 = W.make_custom(seq_lens=pb.seq_lens, q_lens=n1, num_q_heads=pb.num_q_heads,
+                        num_kv_heads=pb.num_kv_heads, head_dim=pb.head_dim,
+                        budgets=pb.budgets, pool_window=pb.pool_window, spike_frac=0.0,
+                        seed=seed, causal=True)
+    lse = oracle.lse(pb1).astype(np.float32)
+    bp, t = to_dev(pb1, agg=agg)
+    n_sc = actkv.num_scores(bp)
+    acc = torch.zeros(max(n_sc, 1), dtype=torch.float32, device="cuda")
+    lse_d = torch.from_numpy(lse).cuda()
+    for _ in range(2):
+        actkv.score_accumulate(bp, t["q"], t["kv"], t["bt"], acc, lse=lse_d)
+    torch.cuda.synchronize()
+    ref = 2.0 * oracle.scores(pb1, lse_in=lse, agg=agg)
+    assert_scores_close(acc[:n_sc].cpu().numpy(), ref, what=f"decode seed {seed}")
