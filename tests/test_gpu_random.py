@@ -3,8 +3,8 @@ lengths (empty and single-token requests included), query counts, GQA groups, he
 pooling windows, budgets (zero, partial, at and past the length), causal and non-causal,
 SUM and MAX_MEAN, the LSE supplied or computed by the library.  Scores within 2e-3
 relative; pooling and selection exact functions of the GPU scores; compaction bit-exact.
-The same problems also go through the in-place compaction (given the oracle's selection)
-and, with one query per request, through the decode-step scoring."""
+The same problems also go through the in-place compaction (given the oracle's selection),
+the LRFU selection and, with one query per request, the decode-step scoring."""
 import numpy as np
 import pytest
 import torch
@@ -105,3 +105,19 @@ def test_random_decode_step_matches_the_oracle(seed):
     torch.cuda.synchronize()
     ref = 2.0 * oracle.scores(pb1, lse_in=lse, agg=agg)
     assert_scores_close(acc[:n_sc].cpu().numpy(), ref, what=f"decode seed {seed}")
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_problem_lrfu_select_matches_the_oracle(seed):
+    """LRFU keep scores (Sec. 5.1) on the oracle's scores of the same random problems, with
+    random keep scores, top-p and decay: hit mask outside the boundary band, keep scores,
+    selection and the kept keep scores exact."""
+    from test_gpu_lrfu import check_stage
+    pb, agg, _ = _random_problem(seed)
+    rng = np.random.default_rng(20_000 + seed)
+    raw = oracle.scores(pb, agg=agg).astype(np.float32)
+    ks_in = (rng.random(raw.shape[0]) * rng.choice([1e-3, 0.1, 1.0])).astype(np.float32)
+    ks_in[rng.random(raw.shape[0]) < 0.3] = 0.0
+    top_p = float(rng.choice([0.0, 0.5, 0.9, 0.97, 1.0]))
+    decay = float(rng.choice([0.0, 0.25, 0.5, 1.0]))
+    check_stage(pb, raw, ks_in, top_p, decay)
