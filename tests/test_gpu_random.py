@@ -4,7 +4,8 @@ pooling windows, budgets (zero, partial, at and past the length), causal and non
 SUM and MAX_MEAN, the LSE supplied or computed by the library.  Scores within 2e-3
 relative; pooling and selection exact functions of the GPU scores; compaction bit-exact.
 The same problems also go through the in-place compaction (given the oracle's selection),
-the LRFU selection and, with one query per request, the decode-step scoring."""
+the LRFU selection and, with one query per request, the decode-step scoring; the confidence
+monitor gets random draws of its own."""
 import numpy as np
 import pytest
 import torch
@@ -121,3 +122,57 @@ def test_random_problem_lrfu_select_matches_the_oracle(seed):
     top_p = float(rng.choice([0.0, 0.5, 0.9, 0.97, 1.0]))
     decay = float(rng.choice([0.0, 0.25, 0.5, 1.0]))
     check_stage(pb, raw, ks_in, top_p, decay)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_token_confidence_matches_the_oracle(seed):
+    """Token confidence (Sec. 6.1) over random vocabularies up to 262,144 logits, top-k up to
+    64, rows of different scales, ties and masked logits."""
+    rng = np.random.default_rng(30_000 + seed)
+    rows = int(rng.integers(1, 9))
+    vocab = int(rng.choice([1, 2, 63, 64, 65, 1000, 16383, 16384, 16385, 100_000, 151_936,
+                            262_144]))
+    k = int(rng.integers(1, 65))
+    x = (rng.standard_normal((rows, vocab)) * rng.uniform(0.1, 8.0, (rows, 1))).astype(np.float32)
+    if rng.random() < 0.3:
+        x = np.round(x)                                   # heavy ties
+    x[rng.random((rows, vocab)) < rng.choice([0.0, 0.2])] = -np.inf
+    x[:, 0] = np.where(np.isinf(x[:, 0]), 0.0, x[:, 0])   # at least one finite logit per row
+    got = actkv.token_confidence(torch.from_numpy(x).cuda(), top_k=k).cpu().numpy()
+    np.testing.assert_allclose(got, oracle.token_confidence(x, k), rtol=1e-6, atol=1e-5,
+                               err_msg=f"seed {seed}: rows={rows} vocab={vocab} k={k}")
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_budget_update_is_bit_exact(seed):
+    """The budget rule (Alg. 2) on random traces and parameters: budgets, slopes, thresholds
+    and retained counts bit-exact."""
+    rng = np.random.default_rng(40_000 + seed)
+    R = int(rng.integers(1, 7))
+    w = int(rng.choice([1, 2, 8, 24, 64, 128]))
+    st = int(rng.choice([1, 3, 8, 16, 64]))
+    params = dict(window=w, stride=st, bottom_pct=float(rng.choice([0.0, 5.0, 10.0, 50.0, 100.0])),
+                  scale_up=float(rng.choice([1.0, 1.75, 2.5])),
+                  budget_upper=int(rng.choice([600, 30000])))
+    seqs = []
+    for _ in range(R):
+        n = int(rng.integers(0, 6000))
+        if n >= w:   # stay within the window count one request may have
+            n = min(n, w + st * 16383)
+        t = (10 + rng.choice([-1.0, 0.0, 1.0]) * np.linspace(0, 1, n)
+             + 0.3 * rng.standard_normal(n))
+        t[rng.random(n) < 0.1] = 9.5
+        seqs.append(np.abs(t).astype(np.float32))
+    budgets = rng.integers(100, 30001, size=R).astype(np.int32)
+    offsets = np.concatenate([[0], np.cumsum([s.size for s in seqs])]).astype(np.int64)
+    flat = torch.from_numpy(np.concatenate(seqs) if seqs else np.zeros(0, np.float32)).cuda()
+    got = actkv.budget_update(flat, offsets, torch.from_numpy(budgets).cuda(), **params)
+    torch.cuda.synchronize()
+    ref = oracle.budget_update(seqs, budgets, **params)
+    np.testing.assert_array_equal(got["budgets"].cpu().numpy(), ref["budgets"])
+    np.testing.assert_array_equal(got["retained"].cpu().numpy(), ref["retained"])
+    np.testing.assert_array_equal(got["slopes"].cpu().numpy().view(np.int64),
+                                  ref["slopes"].view(np.int64))
+    g_thr, r_thr = got["thresholds"].cpu().numpy(), ref["thresholds"]
+    assert np.array_equal(np.isnan(g_thr), np.isnan(r_thr))
+    np.testing.assert_array_equal(g_thr[~np.isnan(g_thr)], r_thr[~np.isnan(r_thr)])
