@@ -490,6 +490,44 @@ def run_inplace(c):
             "tokens_per_s": c["sum_L"] / (ms_ip_step * 1e-3)}
 
 
+def run_other_configs(reps, dev, stream):
+    """The step (LSE supplied) on the ragged batched workload and on its Dirichlet-budget
+    variant: each block table restored before every step, outside the events."""
+    import torch
+    from paper_2609_31395_amd import actkv
+    from paper_2609_31395_amd import workloads as W
+    out = {}
+    for name in ("batched", "adaptive"):
+        dp = W.make_device_problem(name, device=dev)
+        bp = _binding(dp, dev)
+        qy = actkv.query(bp)
+        ws = torch.empty(qy["workspace_bytes"], dtype=torch.uint8, device=dev)
+        bt0 = torch.from_numpy(dp.block_table).to(dev)
+        bt = bt0.clone()
+        free = torch.from_numpy(dp.free_pages).to(dev)
+        lse = actkv.lse(bp, dp.q, dp.kv, bt0, ws=ws)
+        freed = torch.empty(max(qy["pages_freed"], 1), dtype=torch.int32, device=dev)
+        new_lens = torch.empty(bp.num_reqs * bp.num_kv_heads, dtype=torch.int32, device=dev)
+        ev = _event_pairs(reps + 1)
+        for a, b in ev:
+            bt.copy_(bt0)
+            a.record(stream)
+            actkv.step(bp, dp.q, dp.kv, bt, free, lse=lse, freed=freed, new_lens=new_lens, ws=ws,
+                       qy=qy)
+            b.record(stream)
+        torch.cuda.synchronize()
+        ms = _mean_ms(ev)
+        tokens = int(dp.seq_lens.astype(np.int64).sum())
+        out[name] = {"requests": dp.num_reqs, "cached_tokens": tokens,
+                     "action_queries": int(dp.q_lens.sum()), "kept_entries": qy["num_kept"],
+                     "step_us": ms * 1e3, "tokens_per_s": tokens / (ms * 1e-3),
+                     "hbm_roofline_frac": algorithmic_bytes(dp, qy["num_kept"])
+                     / (HBM_PEAK_GBS * 1e9) / (ms * 1e-3)}
+        del dp, ws, bt0, bt, free, lse
+        torch.cuda.synchronize()
+    return out
+
+
 def run_fullmodel(reps, dev, stream):
     """The full-model workload: the steps of all 48 layers back to back over one shared page
     pool (LSE supplied: produced per layer by actkv_lse outside the timed region).  Every
@@ -690,7 +728,7 @@ def main():
         if tr.get("source_sha256") == source_digest() and tr.get("workload") == args.workload:
             traffic = int(tr["hbm_bytes_per_launch"])
 
-    streaming = confidence = table1 = fullmodel = None
+    streaming = confidence = table1 = fullmodel = others = None
     if extra:
         streaming = run_streaming_batch(dp, bp, K, dev, stream)
         log(f"streaming scoring step (1 query per request): {streaming['score_step_us']:.1f} us,"
@@ -700,6 +738,10 @@ def main():
             f"({confidence['token_conf_GBps']:.0f} GB/s), budget update "
             f"{confidence['budget_update_us']:.1f} us")
         table1 = run_table1(max(K // 2, 5), dev, stream) if not args.no_table1 else None
+        others = run_other_configs(K, dev, stream)
+        for nm, o in others.items():
+            log(f"{nm}: step {o['step_us']:.1f} us, {o['tokens_per_s'] / 1e9:.3f} G tokens/s, "
+                f"{o['hbm_roofline_frac']:.2f} of its HBM roofline")
         fullmodel = run_fullmodel(max(K // 4, 3), dev, stream) if not args.no_fullmodel else None
         if fullmodel:
             log(f"full model (48 layers x 32 requests, 16K-64K tokens): "
@@ -774,6 +816,7 @@ def main():
         "streaming": streaming,
         "confidence": confidence,
         "table1": table1,
+        "other_configs": others,
         "fullmodel": fullmodel,
         "lrfu": lrfu,
         "roofline": {

@@ -13,6 +13,12 @@ namespace actkv {
 constexpr int kPageSize = 16;        // slots per page (the only page size built)
 constexpr int kRowsPerChunk = 512;   // query rows (G * n) one scoring pass holds on chip
 constexpr int kKeyTile = 64;         // keys per scoring / LSE pipeline step (4 pages)
+// Scoring cost of one 64-key tile of a segment whose row chunk holds rt 32-row tiles: the
+// work grows with rt, but each tile also pays a fixed share (the K gather, the barrier, the
+// per-key finish) worth about seven 32-row tiles (measured: a 128-row chunk takes ~48% of
+// the time of a 512-row one).  Workgroups split the scoring by this cost.
+constexpr int kTileCostFixed = 7;
+__host__ __device__ constexpr int64_t score_tile_cost(int64_t rt) { return rt + kTileCostFixed; }
 constexpr int kLseKeysPerBlock = 2048;  // keys one LSE workgroup reduces (32 key tiles)
 constexpr int kMaxPoolWindow = 63;
 

@@ -77,7 +77,7 @@ actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
     for (int c = 0; c < chunks; ++c) {
       const int64_t rows = M - (int64_t)c * actkv::kRowsPerChunk;
       const int64_t rt = rows <= 0 ? 1 : ((rows < actkv::kRowsPerChunk ? rows : actkv::kRowsPerChunk) + 31) / 32;
-      hp->score_cost += ntiles * rt * p->num_kv_heads;
+      hp->score_cost += ntiles * actkv::score_tile_cost(rt) * p->num_kv_heads;
     }
     const int64_t lb = (L + actkv::kLseKeysPerBlock - 1) / actkv::kLseKeysPerBlock;
     hp->lse_parts += n * p->num_q_heads * lb;

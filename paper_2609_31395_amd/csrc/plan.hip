@@ -78,7 +78,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
       for (int c = 0; c < nchunk; ++c) {
         const int rows = M - c * kRowsPerChunk;
         const int rt = rows <= 0 ? 1 : ceil_div(rows < kRowsPerChunk ? rows : kRowsPerChunk, 32);
-        cost += ntiles * rt * Hkv;
+        cost += ntiles * score_tile_cost(rt) * Hkv;
       }
       lse_blocks = (int32_t)ceil_div64(L, kLseKeysPerBlock);
     }
@@ -121,7 +121,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
           if (c < nchunk) {
             const int rows = M - c * kRowsPerChunk;
             const int rt = rows <= 0 ? 1 : ceil_div(rows < kRowsPerChunk ? rows : kRowsPerChunk, 32);
-            co += ntiles * rt;
+            co += ntiles * score_tile_cost(rt);
           }
         }
       }

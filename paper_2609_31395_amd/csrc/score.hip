@@ -630,11 +630,12 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
     decode_segment(s, C, Hkv, &r, &c, &h);
     const ReqPlan pl = dp.plan[r];
     const int L = pl.L, n = pl.n, M = G * n;
-    const int RT = chunk_row_tiles(M, c);   // 32-row tiles: the unit of the segment cost
+    // cost of each of the segment's key tiles (the unit of the split over workgroups)
+    const int64_t TC = score_tile_cost(chunk_row_tiles(M, c));
     const int64_t ntiles = ceil_div64(L, kKeyTile);
-    int64_t i1 = (c1 - cs + RT - 1) / RT;
+    int64_t i1 = (c1 - cs + TC - 1) / TC;
     if (i1 > ntiles) i1 = ntiles;
-    cx.i0 = first ? (int)((c0 - cs + RT - 1) / RT) : 0;   // c0 < ce: below ntiles
+    cx.i0 = first ? (int)((c0 - cs + TC - 1) / TC) : 0;   // c0 < ce: below ntiles
     cx.i1 = (int)i1;
     first = false;
     if (cx.i0 >= cx.i1) continue;
@@ -794,8 +795,11 @@ __global__ __launch_bounds__(kDecMaxWaves * 64) void score_decode_kernel(
   const int h = (int)blockIdx.y * (int)(blockDim.x / 64) + wv;
   float* res = res_s[wv];
   // with at most one query a request's cost is Hkv x its 64-key tiles (one row tile), so
-  // seg_cost[r * Hkv] / Hkv is the number of tiles before request r
-  auto tiles_before = [&](int rr) { return dp.seg_cost[(int64_t)rr * Hkv] / Hkv; };
+  // one query per request: every tile costs score_tile_cost(1), so
+  // seg_cost[r * Hkv] / (Hkv * score_tile_cost(1)) is the number of tiles before request r
+  auto tiles_before = [&](int rr) {
+    return dp.seg_cost[(int64_t)rr * Hkv] / (Hkv * score_tile_cost(1));
+  };
   const int64_t total = tiles_before(R);
   const int64_t c0 = total * blockIdx.x / gridDim.x, c1 = total * (blockIdx.x + 1) / gridDim.x;
   if (c0 >= c1) return;
@@ -926,7 +930,7 @@ hipError_t launch_score_decode(const DevProblem& dp, const HostPlan& hp, const v
   for (int w = 1; w <= kDecMaxWaves; ++w)
     if (hp.Hkv % w == 0) waves = w;
   const unsigned groups = (unsigned)(hp.Hkv / waves);
-  const int64_t tiles = hp.score_cost / hp.Hkv;   // (request, 64-key tile) pairs
+  const int64_t tiles = hp.score_cost / (hp.Hkv * score_tile_cost(1));   // (request, key tile) pairs
   // one resident round of workgroups (equal contiguous shares: a second round would only
   // add a tail), at most one per tile.  Residency per CU is asked once per kernel and
   // workgroup size (it depends on nothing else).
