@@ -583,6 +583,22 @@ def run_fullmodel(reps, dev, stream):
     return out
 
 
+def _leg(name, fn, *args):
+    """Run one optional bench leg; a failure (say, out of device memory on a box with less
+    free HBM) is logged and the leg reported as null, so the headline line still prints."""
+    import torch
+    try:
+        return fn(*args)
+    except Exception as e:   # noqa: BLE001 -- every optional leg is best effort
+        log(f"{name} leg not measured: {type(e).__name__}: {e}")
+        try:
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+        except Exception:   # noqa: BLE001
+            pass
+        return None
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -709,8 +725,8 @@ def main():
     ctx = dict(bp=bp, dp=dp, qy=qy, ws=ws, lse=lse, scores=scores, pooled=pooled, kept=kept,
                free=free, freed=freed, new_lens=new_lens, bts=bts, bt0=bt0, dev=dev,
                stream=stream, K=K, sum_L=sum_L)
-    lrfu = run_lrfu(ctx) if extra else None
-    inplace = run_inplace(ctx) if extra else None
+    lrfu = _leg("lrfu", run_lrfu, ctx) if extra else None
+    inplace = _leg("inplace", run_inplace, ctx) if extra else None
 
     value = sum_L / (ms_per_step * 1e-3)
     alg_bytes = algorithmic_bytes(dp, qy["num_kept"])
@@ -730,19 +746,24 @@ def main():
 
     streaming = confidence = table1 = fullmodel = others = None
     if extra:
-        streaming = run_streaming_batch(dp, bp, K, dev, stream)
-        log(f"streaming scoring step (1 query per request): {streaming['score_step_us']:.1f} us,"
-            f" {streaming['hbm_GBps']:.0f} GB/s")
-        confidence = run_confidence(dp.num_reqs, int(dp.seq_lens.max()), K, dev, stream)
-        log(f"confidence: token confidence {confidence['token_conf_us']:.1f} us "
-            f"({confidence['token_conf_GBps']:.0f} GB/s), budget update "
-            f"{confidence['budget_update_us']:.1f} us")
-        table1 = run_table1(max(K // 2, 5), dev, stream) if not args.no_table1 else None
-        others = run_other_configs(K, dev, stream)
-        for nm, o in others.items():
+        streaming = _leg("streaming", run_streaming_batch, dp, bp, K, dev, stream)
+        if streaming:
+            log(f"streaming scoring step (1 query per request): "
+                f"{streaming['score_step_us']:.1f} us, {streaming['hbm_GBps']:.0f} GB/s")
+        confidence = _leg("confidence", run_confidence, dp.num_reqs, int(dp.seq_lens.max()), K,
+                          dev, stream)
+        if confidence:
+            log(f"confidence: token confidence {confidence['token_conf_us']:.1f} us "
+                f"({confidence['token_conf_GBps']:.0f} GB/s), budget update "
+                f"{confidence['budget_update_us']:.1f} us")
+        table1 = (_leg("table1", run_table1, max(K // 2, 5), dev, stream)
+                  if not args.no_table1 else None)
+        others = _leg("other_configs", run_other_configs, K, dev, stream)
+        for nm, o in (others or {}).items():
             log(f"{nm}: step {o['step_us']:.1f} us, {o['tokens_per_s'] / 1e9:.3f} G tokens/s, "
                 f"{o['hbm_roofline_frac']:.2f} of its HBM roofline")
-        fullmodel = run_fullmodel(max(K // 4, 3), dev, stream) if not args.no_fullmodel else None
+        fullmodel = (_leg("fullmodel", run_fullmodel, max(K // 4, 3), dev, stream)
+                     if not args.no_fullmodel else None)
         if fullmodel:
             log(f"full model (48 layers x 32 requests, 16K-64K tokens): "
                 f"{fullmodel['step_ms']:.1f} ms, {fullmodel['layer_step_us']:.0f} us per layer, "
@@ -755,8 +776,7 @@ def main():
                 + (f"  | graph: score step {gr['score_step_us']:6.1f} us, fresh "
                    f"{gr['compress_fresh_us']:6.1f} us" if gr else ""))
 
-    cpu = None
-    if not args.no_cpu_baseline and args.cpu_sample_reqs > 0:
+    def cpu_leg():
         import oracle
         reqs = list(range(min(args.cpu_sample_reqs, dp.num_reqs)))
         sample = dp.host_subset(reqs)
@@ -765,10 +785,14 @@ def main():
         oracle.step(sample)   # the oracle's own full step (it derives the LSE itself)
         cpu_s = time.perf_counter() - t1
         s_tokens = int(sample.seq_lens.astype(np.int64).sum())
-        cpu = {"value": s_tokens / cpu_s, "unit": "tokens/s", "cores": oracle.num_threads(),
-               "kind": "oracle",
-               "sample": f"{len(reqs)} of {dp.num_reqs} requests of {args.workload} "
-                         f"({s_tokens} cached tokens, all stages, fp64), {cpu_s:.1f} s"}
+        return {"value": s_tokens / cpu_s, "unit": "tokens/s", "cores": oracle.num_threads(),
+                "kind": "oracle",
+                "sample": f"{len(reqs)} of {dp.num_reqs} requests of {args.workload} "
+                          f"({s_tokens} cached tokens, all stages, fp64), {cpu_s:.1f} s"}
+
+    cpu = None
+    if not args.no_cpu_baseline and args.cpu_sample_reqs > 0:
+        cpu = _leg("cpu_baseline", cpu_leg)
 
     cfg = W.CONFIGS[args.workload]
     out = {
