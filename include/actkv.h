@@ -29,8 +29,10 @@
  *    concatenated in (r, h) order; segment (r, h) holds k_rh = min(budget_rh, L_r)
  *    entries.
  *  - Ownership: the caller owns every buffer, including the workspace whose size
- *    actkv_query reports.  The library allocates and frees nothing, keeps no pointer after
- *    a call returns and has no mutable global state: calls are reentrant.
+ *    actkv_query reports.  The library allocates and frees nothing and keeps no pointer
+ *    after a call returns.  Its only process-wide state is a cache of per-kernel occupancy
+ *    figures (written once per kernel, with atomics; the same for every gfx950 device), so
+ *    concurrent calls are safe as long as their buffers do not overlap.
  *  - Asynchrony: each call validates its arguments on the host, then enqueues kernels on
  *    `stream` (a hipStream_t; NULL is the default stream) and returns without
  *    synchronising.  Outputs are valid once the stream reaches that point.
@@ -99,13 +101,16 @@ typedef struct actkv_problem {
 } actkv_problem;
 
 /*
- * Host-only planning: no GPU work, callable without a device.  Reports the workspace
- * size the other calls need for `p` (the maximum over them, so one workspace serves
- * every entry point), the number of kept entries sum_{r,h} min(budget, L_r), the fresh
- * pages compaction pops from the free list (sum over compacted requests of
- * ceil(max_h k_rh / page_size)) and the pages it returns (sum of ceil(L_r / page_size)
- * over compacted requests).  A request whose every head has budget >= L_r is left
- * untouched by compaction.  Any output pointer may be NULL.
+ * Host-only planning (the per-request counts of Alg. 4, steps 1-5: Y = ceil(L_r /
+ * page_size) blocks in use, X = ceil(k / page_size) blocks the survivors need; here k is
+ * the largest per-head budget of the request, capped at L_r): no GPU work, callable
+ * without a device.  Reports the workspace size the other calls need for `p` (the maximum
+ * over them, so one workspace serves every entry point), the number of kept entries
+ * sum_{r,h} min(budget, L_r), the fresh pages compaction pops from the free list (the sum
+ * of X over compacted requests) and the pages it returns (the sum of Y over compacted
+ * requests).  A request whose every head has budget >= L_r is left untouched by
+ * compaction.  Errors: ACTKV_ERR_INVALID_ARGUMENT / ACTKV_ERR_UNSUPPORTED as for every
+ * entry point, nothing written.  Any output pointer may be NULL.
  */
 actkv_status actkv_query(const actkv_problem* p, size_t* workspace_bytes, int64_t* num_kept,
                          int64_t* fresh_pages_needed, int64_t* pages_freed);

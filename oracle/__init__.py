@@ -272,12 +272,19 @@ def step_inplace(pb, lse_in: Optional[np.ndarray] = None, agg: str = "sum", **kw
     return out
 
 
+def as_f32(x: float) -> float:
+    """x rounded to the nearest float32, as a Python float: the value a float32 parameter of
+    the GPU entry points carries (the oracle then computes with exactly that value)."""
+    return float(np.float32(x))
+
+
 def hits(pb, att: np.ndarray, top_p: float, **kw) -> np.ndarray:
-    """Top-p hit mask (uint8, same layout as the scores) of the scores `att` (Alg. 1 step 3)."""
+    """Top-p hit mask (uint8, same layout as the scores) of the scores `att` (Alg. 1 step 3).
+    top_p is rounded to float32 first, the precision the GPU entry point receives it in."""
     b = _Bound(pb, **kw)
     att = np.ascontiguousarray(att, dtype=np.float32)
     out = np.zeros(att.shape[0], dtype=np.uint8)
-    _check(_load().actkv_oracle_hits(b.ref, att.ctypes.data, float(top_p), out.ctypes.data),
+    _check(_load().actkv_oracle_hits(b.ref, att.ctypes.data, as_f32(top_p), out.ctypes.data),
            "hits")
     return out
 
@@ -290,7 +297,7 @@ def lrfu_update(pb, att: np.ndarray, hit: np.ndarray, decay: float, ks: np.ndarr
     hit = np.ascontiguousarray(hit, dtype=np.uint8)
     out = np.array(ks, dtype=np.float32, copy=True, order="C")
     _check(_load().actkv_oracle_lrfu_update(b.ref, att.ctypes.data, hit.ctypes.data,
-                                            float(decay), out.ctypes.data), "lrfu_update")
+                                            as_f32(decay), out.ctypes.data), "lrfu_update")
     return out
 
 
@@ -299,7 +306,8 @@ def lrfu_step(pb, ks: np.ndarray, top_p: float, decay: float,
     """The step with LRFU keep scores (Alg. 1 steps 1-6): score, pool, hit mask, keep-score
     update, TopK on the keep scores, compaction.  `ks` holds the keep score of every cached
     entry (0 for entries new since the last step); ks_kept are those of the kept entries
-    (KS'), in the order of `kept`."""
+    (KS'), in the order of `kept`.  top_p and decay are float32 parameters (rounded here as
+    the GPU entry point receives them)."""
     raw = scores(pb, lse_in=lse_in, agg=agg, **kw)
     pooled = pool(pb, raw, **kw)
     hit = hits(pb, pooled, top_p, **kw)

@@ -367,30 +367,29 @@ int actkv_oracle_compact(const oracle_problem* p, uint16_t* kv, int32_t* bt,
 }
 
 /*
- * In-place compaction (Alg. 4 steps 1-6; the slot planning of Sec. 7.2).  Requests in order;
- * a request whose every head keeps all its entries is skipped, as above.  Each KV head has
- * its own keep set (k_h = min(budget, L) entries, `kept` ascending); the tail region is
- * shared by the heads because a page holds every head's row of a slot, so X follows the
- * largest k_h:
- *   Step 1  Y = ceil(L / BS), X = ceil(max_h k_h / BS), Start = (Y - X) * BS,
- *           End = Start + k_h;
- *   Step 2  DstMask = not KeepMask[Start:End].  KeepMask covers the Y * BS logical slots of
- *           the request; slots at or past L hold no entry, so they are destinations too
- *           (they exist in the last block, and without them #dst < #src whenever End > L);
- *   Step 3  KeepMask[Start:End] = False; SrcMask = KeepMask (kept entries outside the
- *           region);
- *   Step 4  logical slots -> physical slots through the request's block-table row;
- *   Step 5  CopyPairs = Zip(SrcSlots, DstSlots), both in ascending logical order;
- *   Step 6  the K and V rows of head h are copied for every pair.  Sources are kept and
- *           destinations are not, so the two sets are disjoint and the order of the copies
- *           does not matter.
- * The survivors of head h then occupy logical slots [Start, Start + k_h), inside the last X
- * blocks.  The block-table row becomes bt[r, Y - X .. Y) followed by -1 up to Y; the first
- * Y - X pages go to freed_out (request order); new_lens[r, h] = k_h; new_order (laid out
+ * In-place compaction (Alg. 4, Sec. 7.2): the survivors of a request are packed into the
+ * request's own last blocks instead of fresh pages.  Requests are handled in order; one
+ * whose every head keeps all its entries is left untouched, as above.
+ *
+ * Definition used here.  Y = ceil(L / BS) blocks hold the request; X = ceil(max_h k_h / BS)
+ * of them, the last X, are kept.  Every KV head has its own keep set (its k_h = min(budget,
+ * L) kept token indices, ascending), but a block holds every head's row of a slot, so all
+ * heads share the same tail: it starts at logical slot Start = (Y - X) * BS, and head h
+ * fills [Start, Start + k_h).  Inside that range, a slot already holding a kept entry stays
+ * as it is; every other slot of the range -- including slots at or past L in a partly
+ * filled last block, which exist but hold no entry -- receives one kept entry from outside
+ * the range.  Kept entries outside the range and free slots inside it are paired in
+ * ascending order of their logical slots, and each pair copies the K and V rows of head h
+ * (physical slots through the request's block-table row as it was before this call).
+ * Sources are kept entries and destinations are not, so no copy overwrites a row another
+ * copy still reads.
+ *
+ * Afterwards the block-table row is bt[r, Y - X .. Y) followed by -1 up to Y; the first
+ * Y - X blocks go to freed_out (request order); new_lens[r, h] = k_h; new_order (laid out
  * like kept) gets, for every new slot j < k_h, the original token index of the entry now
  * there.  A skipped request keeps new_order = kept.  *num_pairs (if given) counts the
- * copies.  Returns -3 if some head's source and destination counts differ (cannot happen
- * for a valid keep set).
+ * copies.  Returns -3 if a head's free slots and outside entries are not equal in number
+ * (cannot happen for a valid keep set).
  */
 int actkv_oracle_compact_inplace(const oracle_problem* p, uint16_t* kv, int32_t* bt,
                                  const int32_t* kept, int32_t* freed_out, int32_t* new_lens,
@@ -417,47 +416,46 @@ int actkv_oracle_compact_inplace(const oracle_problem* p, uint16_t* kv, int32_t*
       }
       continue;
     }
-    /* Step 1 */
+    /* the shared tail: the last X of the request's Y blocks */
     const int64_t Y = (L + BS - 1) / BS, X = (kmax + BS - 1) / BS;
     const int64_t start = (Y - X) * BS, slots = Y * BS;
-    unsigned char* keep = (unsigned char*)malloc((size_t)slots);
-    int64_t* src = (int64_t*)malloc(sizeof(int64_t) * (size_t)(slots > 0 ? slots : 1));
-    int64_t* dst = (int64_t*)malloc(sizeof(int64_t) * (size_t)(slots > 0 ? slots : 1));
+    unsigned char* is_kept = (unsigned char*)malloc((size_t)slots);
+    int64_t* outside = (int64_t*)malloc(sizeof(int64_t) * (size_t)(slots > 0 ? slots : 1));
+    int64_t* holes = (int64_t*)malloc(sizeof(int64_t) * (size_t)(slots > 0 ? slots : 1));
     for (int h = 0; h < Hkv; ++h) {
       const int64_t b = p->budgets[r * Hkv + h];
       const int64_t k = b > L ? L : b;
       const int64_t end = start + k;
       const int64_t ko = kept_offset(p, r, h);
-      memset(keep, 0, (size_t)slots);
-      for (int64_t j = 0; j < k; ++j) keep[kept[ko + j]] = 1;
-      /* Step 2: destinations, and the new order of the entries already in the region */
-      int64_t nd = 0;
+      memset(is_kept, 0, (size_t)slots);
+      for (int64_t j = 0; j < k; ++j) is_kept[kept[ko + j]] = 1;
+      /* slots of [start, end): a kept entry already there stays, the rest are holes */
+      int64_t n_holes = 0;
       for (int64_t t = start; t < end; ++t) {
-        if (keep[t]) new_order[ko + (t - start)] = (int32_t)t;
-        else dst[nd++] = t;
+        if (is_kept[t]) new_order[ko + (t - start)] = (int32_t)t;
+        else holes[n_holes++] = t;
       }
-      /* Step 3 */
-      for (int64_t t = start; t < end; ++t) keep[t] = 0;
-      int64_t ns = 0;
+      /* kept entries outside [start, end), ascending */
+      int64_t n_out = 0;
       for (int64_t t = 0; t < slots; ++t)
-        if (keep[t]) src[ns++] = t;
-      if (ns != nd) {
-        free(keep); free(src); free(dst);
+        if (is_kept[t] && (t < start || t >= end)) outside[n_out++] = t;
+      if (n_out != n_holes) {
+        free(is_kept); free(outside); free(holes);
         return -3;
       }
-      /* Steps 4-6 (physical slots through the row as it was before this call) */
-      for (int64_t i = 0; i < ns; ++i) {
-        const int64_t ps = actkv_oracle_slot(row, BS, src[i]);
-        const int64_t pd = actkv_oracle_slot(row, BS, dst[i]);
+      /* the i-th outside entry moves into the i-th hole */
+      for (int64_t i = 0; i < n_out; ++i) {
+        const int64_t ps = actkv_oracle_slot(row, BS, outside[i]);
+        const int64_t pd = actkv_oracle_slot(row, BS, holes[i]);
         for (int which = 0; which < 2; ++which)
           memcpy(kv_row_mut(p, kv, which, pd, h), kv_row(p, kv, which, ps, h),
                  sizeof(uint16_t) * (size_t)D);
-        new_order[ko + (dst[i] - start)] = (int32_t)src[i];
+        new_order[ko + (holes[i] - start)] = (int32_t)outside[i];
       }
-      pairs_total += ns;
+      pairs_total += n_out;
       new_lens[r * Hkv + h] = (int32_t)k;
     }
-    free(keep); free(src); free(dst);
+    free(is_kept); free(outside); free(holes);
     /* the freed blocks, then the row: the last X blocks move to the front */
     for (int64_t i = 0; i < Y - X; ++i) freed_out[freed_off + i] = row[i];
     for (int64_t i = 0; i < X; ++i) row[i] = row[Y - X + i];

@@ -152,6 +152,98 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
+_BITS16 = (torch.bfloat16, torch.int16, torch.uint16)   # bf16 data or its bit pattern
+_I32, _F32, _U8 = (torch.int32,), (torch.float32,), (torch.uint8,)
+
+
+def _need(name: str, t: Optional[torch.Tensor], dtypes, numel: int, required: bool = True,
+          seen: Optional[list] = None):
+    """Checks one tensor argument before its pointer reaches the C ABI: element type, a
+    contiguous layout, at least `numel` elements, resident on a GPU.  A missing tensor is an
+    error only when `required` and the call has elements for it.  With `seen`, the device
+    check is left to _on_gpu(seen) once every argument has passed the others."""
+    if t is None:
+        if required and numel > 0:
+            raise ValueError(f"{name} is required ({numel} elements)")
+        return
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor, got {type(t).__name__}")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError(f"{name} must be {' or '.join(str(d) for d in dtypes)}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, the call needs {numel}")
+    if seen is None:
+        _on_gpu([(name, t)])
+    else:
+        seen.append((name, t))
+
+
+def _on_gpu(named) -> None:
+    """Every tensor resident on the same GPU."""
+    first = None
+    for name, t in named:
+        if t.device.type != "cuda":
+            raise ValueError(f"{name} must be on the GPU, got {t.device}")
+        if first is None:
+            first = (name, t.device)
+        elif t.device != first[1]:
+            raise ValueError(f"{name} is on {t.device}, {first[0]} on {first[1]}")
+
+
+class _Sizes:
+    """Element counts of every array an entry point reads or writes, from the problem and
+    the host-only planning query."""
+
+    def __init__(self, p: Problem, qy: Optional[dict] = None):
+        qy = query(p) if qy is None else qy
+        R, Hkv = p.num_reqs, p.num_kv_heads
+        self.qy = qy
+        self.sum_n = int(p.q_lens.astype(np.int64).sum())
+        self.q = self.sum_n * p.num_q_heads * p.head_dim
+        self.lse = self.sum_n * p.num_q_heads
+        self.kv = 2 * int(p.num_pages) * p.page_size * Hkv * p.head_dim
+        self.bt = R * int(p.bt_stride)
+        self.scores = num_scores(p)
+        self.kept = int(qy["num_kept"])
+        self.freed = int(qy["pages_freed"])
+        self.fresh = int(qy["fresh_pages_needed"])
+        self.lens = R * Hkv
+        self.ws = int(qy["workspace_bytes"])
+        self.seen: list = []
+        self.mirrors = []
+        if R > 0:
+            for name, t, n in (("seq_lens_d", p.seq_lens_d, R), ("q_lens_d", p.q_lens_d, R),
+                               ("budgets_d", p.budgets_d, R * Hkv)):
+                _need(name, t, _I32, n, seen=self.mirrors)
+
+    def need(self, name, t, dtypes, numel, required=True):
+        _need(name, t, dtypes, numel, required=required, seen=self.seen)
+
+    def check_ws(self, ws: Optional[torch.Tensor]):
+        """The caller's workspace, if any; then every argument's device (call last)."""
+        if ws is not None:
+            self.need("ws", ws, None, 0)
+            if _ws_bytes(ws) < self.ws:
+                raise ValueError(f"ws holds {_ws_bytes(ws)} bytes, the call needs {self.ws}")
+        _on_gpu(self.seen + self.mirrors)
+
+    def kv_args(self, q, kv_cache, block_table, lse=None):
+        self.need("q", q, _BITS16, self.q)
+        self.need("kv_cache", kv_cache, _BITS16, self.kv if self.scores or self.kept else 0)
+        self.need("block_table", block_table, _I32, self.bt)
+        self.need("lse", lse, _F32, self.lse, required=False)
+
+
+def _numel(t: Optional[torch.Tensor]) -> int:
+    return 0 if t is None else t.numel()
+
+
+def _ws_bytes(ws: torch.Tensor) -> int:
+    return ws.numel() * ws.element_size()
+
+
 def query(p: Problem) -> dict:
     """Host-only: workspace bytes, kept entries, fresh pages needed, pages freed."""
     lib = load_library()
@@ -184,13 +276,17 @@ def lse(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch.
         out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
         stream=None) -> torch.Tensor:
     lib = load_library()
+    z = _Sizes(p)
+    z.kv_args(q, kv_cache, block_table)
+    z.need("out", out, _F32, z.lse, required=False)
+    z.check_ws(ws)
     dev = kv_cache.device
     if out is None:
-        out = torch.empty((int(p.q_lens.sum()), p.num_q_heads), dtype=torch.float32, device=dev)
+        out = torch.empty((z.sum_n, p.num_q_heads), dtype=torch.float32, device=dev)
     ws = workspace(p, dev) if ws is None else ws
     c = p.cstruct()
     _check("actkv_lse", lib.actkv_lse(ctypes.byref(c), _ptr(q), _ptr(kv_cache),
-                                      _ptr(block_table), _ptr(out), _ptr(ws), ws.numel(),
+                                      _ptr(block_table), _ptr(out), _ptr(ws), _ws_bytes(ws),
                                       _stream(stream)))
     return out
 
@@ -199,14 +295,18 @@ def score(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torc
           lse: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
           ws: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     lib = load_library()
+    z = _Sizes(p)
+    z.kv_args(q, kv_cache, block_table, lse)
+    z.need("out", out, _F32, z.scores, required=False)
+    z.check_ws(ws)
     dev = kv_cache.device
     if out is None:
-        out = torch.empty(num_scores(p), dtype=torch.float32, device=dev)
+        out = torch.empty(z.scores, dtype=torch.float32, device=dev)
     ws = workspace(p, dev) if ws is None else ws
     c = p.cstruct()
     _check("actkv_score", lib.actkv_score(ctypes.byref(c), _ptr(q), _ptr(kv_cache),
                                           _ptr(block_table), _ptr(lse), _ptr(out), _ptr(ws),
-                                          ws.numel(), _stream(stream)))
+                                          _ws_bytes(ws), _stream(stream)))
     return out
 
 
@@ -216,11 +316,15 @@ def score_accumulate(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor,
                      stream=None) -> torch.Tensor:
     """acc += the scores of this call (streaming, one decode step)."""
     lib = load_library()
+    z = _Sizes(p)
+    z.kv_args(q, kv_cache, block_table, lse)
+    z.need("acc", acc, _F32, z.scores)
+    z.check_ws(ws)
     ws = workspace(p, kv_cache.device) if ws is None else ws
     c = p.cstruct()
     _check("actkv_score_accumulate", lib.actkv_score_accumulate(
         ctypes.byref(c), _ptr(q), _ptr(kv_cache), _ptr(block_table), _ptr(lse), _ptr(acc),
-        _ptr(ws), ws.numel(), _stream(stream)))
+        _ptr(ws), _ws_bytes(ws), _stream(stream)))
     return acc
 
 
@@ -229,16 +333,31 @@ def select(p: Problem, scores: torch.Tensor, pooled: Optional[torch.Tensor] = No
            stream=None, want_pooled: bool = True):
     """Returns (kept, pooled); pooled is None when not requested."""
     lib = load_library()
+    z = _Sizes(p)
+    z.need("scores", scores, _F32, z.scores)
+    z.need("pooled", pooled, _F32, z.scores, required=False)
+    z.need("kept", kept, _I32, z.kept, required=False)
+    z.check_ws(ws)
     dev = scores.device
     if kept is None:
-        kept = torch.empty(max(query(p)["num_kept"], 1), dtype=torch.int32, device=dev)
+        kept = torch.empty(max(z.kept, 1), dtype=torch.int32, device=dev)
     if pooled is None and want_pooled:
         pooled = torch.empty_like(scores)
     ws = workspace(p, dev) if ws is None else ws
     c = p.cstruct()
     _check("actkv_select", lib.actkv_select(ctypes.byref(c), _ptr(scores), _ptr(pooled),
-                                            _ptr(kept), _ptr(ws), ws.numel(), _stream(stream)))
-    return kept[:query(p)["num_kept"]], pooled
+                                            _ptr(kept), _ptr(ws), _ws_bytes(ws),
+                                            _stream(stream)))
+    return kept[:z.kept], pooled
+
+
+def _compact_outputs(z: _Sizes, kv_cache, block_table, free_pages, freed, new_lens):
+    z.need("kv_cache", kv_cache, _BITS16, z.kv if z.kept else 0)
+    z.need("block_table", block_table, _I32, z.bt)
+    if free_pages is not None or z.fresh:
+        z.need("free_pages", free_pages, _I32, z.fresh)
+    z.need("freed", freed, _I32, z.freed, required=False)
+    z.need("new_lens", new_lens, _I32, z.lens, required=False)
 
 
 def compact(p: Problem, kv_cache: torch.Tensor, block_table: torch.Tensor, kept: torch.Tensor,
@@ -247,19 +366,32 @@ def compact(p: Problem, kv_cache: torch.Tensor, block_table: torch.Tensor, kept:
             stream=None):
     """In place on kv_cache / block_table.  Returns (freed_pages, new_lens)."""
     lib = load_library()
+    z = _Sizes(p)
+    _compact_outputs(z, kv_cache, block_table, free_pages, freed, new_lens)
+    z.need("kept", kept, _I32, z.kept)
+    z.check_ws(ws)
     dev = kv_cache.device
-    qy = query(p)
     if freed is None:
-        freed = torch.empty(max(qy["pages_freed"], 1), dtype=torch.int32, device=dev)
+        freed = torch.empty(max(z.freed, 1), dtype=torch.int32, device=dev)
     if new_lens is None:
-        new_lens = torch.empty(p.num_reqs * p.num_kv_heads, dtype=torch.int32, device=dev)
+        new_lens = torch.empty(z.lens, dtype=torch.int32, device=dev)
     ws = workspace(p, dev) if ws is None else ws
     c = p.cstruct()
     _check("actkv_compact", lib.actkv_compact(ctypes.byref(c), _ptr(kv_cache), _ptr(block_table),
-                                              _ptr(kept), _ptr(free_pages), free_pages.numel(),
-                                              _ptr(freed), _ptr(new_lens), _ptr(ws), ws.numel(),
-                                              _stream(stream)))
-    return freed[:qy["pages_freed"]], new_lens
+                                              _ptr(kept), _ptr(free_pages), _numel(free_pages),
+                                              _ptr(freed), _ptr(new_lens), _ptr(ws),
+                                              _ws_bytes(ws), _stream(stream)))
+    return freed[:z.freed], new_lens
+
+
+def _step_args(z: _Sizes, q, kv_cache, block_table, free_pages, lse, scores, pooled, kept,
+               freed, new_lens, ws):
+    z.kv_args(q, kv_cache, block_table, lse)
+    _compact_outputs(z, kv_cache, block_table, free_pages, freed, new_lens)
+    z.need("scores", scores, _F32, z.scores, required=False)
+    z.need("pooled", pooled, _F32, z.scores, required=False)
+    z.need("kept", kept, _I32, z.kept, required=False)
+    z.check_ws(ws)
 
 
 def step(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch.Tensor,
@@ -270,21 +402,23 @@ def step(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch
          stream=None, qy: Optional[dict] = None) -> dict:
     """The whole step, in place on kv_cache / block_table; optional intermediates."""
     lib = load_library()
+    z = _Sizes(p, qy)
+    _step_args(z, q, kv_cache, block_table, free_pages, lse, scores, pooled, kept, freed,
+               new_lens, ws)
     dev = kv_cache.device
-    qy = query(p) if qy is None else qy
     if freed is None:
-        freed = torch.empty(max(qy["pages_freed"], 1), dtype=torch.int32, device=dev)
+        freed = torch.empty(max(z.freed, 1), dtype=torch.int32, device=dev)
     if new_lens is None:
-        new_lens = torch.empty(p.num_reqs * p.num_kv_heads, dtype=torch.int32, device=dev)
+        new_lens = torch.empty(z.lens, dtype=torch.int32, device=dev)
     ws = workspace(p, dev) if ws is None else ws
     c = p.cstruct()
     _check("actkv_step", lib.actkv_step(ctypes.byref(c), _ptr(q), _ptr(kv_cache),
                                         _ptr(block_table), _ptr(lse), _ptr(free_pages),
-                                        free_pages.numel(), _ptr(scores), _ptr(pooled),
+                                        _numel(free_pages), _ptr(scores), _ptr(pooled),
                                         _ptr(kept), _ptr(freed), _ptr(new_lens), _ptr(ws),
-                                        ws.numel(), _stream(stream)))
-    return dict(freed=freed[:qy["pages_freed"]], new_lens=new_lens, scores=scores,
-                pooled=pooled, kept=None if kept is None else kept[:qy["num_kept"]])
+                                        _ws_bytes(ws), _stream(stream)))
+    return dict(freed=freed[:z.freed], new_lens=new_lens, scores=scores,
+                pooled=pooled, kept=None if kept is None else kept[:z.kept])
 
 
 def compact_inplace(p: Problem, kv_cache: torch.Tensor, block_table: torch.Tensor,
@@ -295,21 +429,29 @@ def compact_inplace(p: Problem, kv_cache: torch.Tensor, block_table: torch.Tenso
     """In-place compaction (Alg. 4) on kv_cache / block_table.  Returns freed, new_lens and
     new_order (None unless requested)."""
     lib = load_library()
+    z = _Sizes(p)
+    nfreed = query_inplace(p)
+    z.need("kv_cache", kv_cache, _BITS16, z.kv if z.kept else 0)
+    z.need("block_table", block_table, _I32, z.bt)
+    z.need("kept", kept, _I32, z.kept)
+    z.need("freed", freed, _I32, nfreed, required=False)
+    z.need("new_lens", new_lens, _I32, z.lens, required=False)
+    z.need("new_order", new_order, _I32, z.kept, required=False)
+    z.check_ws(ws)
     dev = kv_cache.device
-    nfreed, nk = query_inplace(p), query(p)["num_kept"]
     if freed is None:
         freed = torch.empty(max(nfreed, 1), dtype=torch.int32, device=dev)
     if new_lens is None:
-        new_lens = torch.empty(p.num_reqs * p.num_kv_heads, dtype=torch.int32, device=dev)
+        new_lens = torch.empty(z.lens, dtype=torch.int32, device=dev)
     if new_order is None and want_order:
-        new_order = torch.empty(max(nk, 1), dtype=torch.int32, device=dev)
+        new_order = torch.empty(max(z.kept, 1), dtype=torch.int32, device=dev)
     ws = workspace(p, dev) if ws is None else ws
     c = p.cstruct()
     _check("actkv_compact_inplace", lib.actkv_compact_inplace(
         ctypes.byref(c), _ptr(kv_cache), _ptr(block_table), _ptr(kept), _ptr(freed),
-        _ptr(new_lens), _ptr(new_order), _ptr(ws), ws.numel(), _stream(stream)))
+        _ptr(new_lens), _ptr(new_order), _ptr(ws), _ws_bytes(ws), _stream(stream)))
     return dict(freed=freed[:nfreed], new_lens=new_lens,
-                new_order=None if new_order is None else new_order[:nk])
+                new_order=None if new_order is None else new_order[:z.kept])
 
 
 def step_inplace(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch.Tensor,
@@ -320,23 +462,30 @@ def step_inplace(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_tabl
                  stream=None, qy: Optional[dict] = None, nfreed: Optional[int] = None) -> dict:
     """The step with the in-place compaction, in place on kv_cache / block_table."""
     lib = load_library()
-    dev = kv_cache.device
-    qy = query(p) if qy is None else qy
+    z = _Sizes(p, qy)
     nfreed = query_inplace(p) if nfreed is None else nfreed
+    z.kv_args(q, kv_cache, block_table, lse)
+    z.need("scores", scores, _F32, z.scores, required=False)
+    z.need("pooled", pooled, _F32, z.scores, required=False)
+    z.need("kept", kept, _I32, z.kept, required=False)
+    z.need("freed", freed, _I32, nfreed, required=False)
+    z.need("new_lens", new_lens, _I32, z.lens, required=False)
+    z.need("new_order", new_order, _I32, z.kept, required=False)
+    z.check_ws(ws)
+    dev = kv_cache.device
     if freed is None:
         freed = torch.empty(max(nfreed, 1), dtype=torch.int32, device=dev)
     if new_lens is None:
-        new_lens = torch.empty(p.num_reqs * p.num_kv_heads, dtype=torch.int32, device=dev)
+        new_lens = torch.empty(z.lens, dtype=torch.int32, device=dev)
     ws = workspace(p, dev) if ws is None else ws
     c = p.cstruct()
     _check("actkv_step_inplace", lib.actkv_step_inplace(
         ctypes.byref(c), _ptr(q), _ptr(kv_cache), _ptr(block_table), _ptr(lse), _ptr(scores),
         _ptr(pooled), _ptr(kept), _ptr(freed), _ptr(new_lens), _ptr(new_order), _ptr(ws),
-        ws.numel(), _stream(stream)))
-    nk = qy["num_kept"]
+        _ws_bytes(ws), _stream(stream)))
     return dict(freed=freed[:nfreed], new_lens=new_lens, scores=scores, pooled=pooled,
-                kept=None if kept is None else kept[:nk],
-                new_order=None if new_order is None else new_order[:nk])
+                kept=None if kept is None else kept[:z.kept],
+                new_order=None if new_order is None else new_order[:z.kept])
 
 
 def lrfu_select(p: Problem, scores: torch.Tensor, ks: torch.Tensor, top_p: float,
@@ -345,20 +494,27 @@ def lrfu_select(p: Problem, scores: torch.Tensor, ks: torch.Tensor, top_p: float
                 ks_kept: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
                 stream=None) -> dict:
     """LRFU eviction; ks (fp32, same layout as scores) is updated in place.  Returns kept,
-    ks_kept, and the optional pooled / hit outputs."""
+    ks_kept, and the optional pooled / hit outputs.  top_p and decay travel as float32."""
     lib = load_library()
+    z = _Sizes(p)
+    z.need("scores", scores, _F32, z.scores)
+    z.need("ks", ks, _F32, z.scores)
+    z.need("pooled", pooled, _F32, z.scores, required=False)
+    z.need("hit", hit, _U8, z.scores, required=False)
+    z.need("kept", kept, _I32, z.kept, required=False)
+    z.need("ks_kept", ks_kept, _F32, z.kept, required=False)
+    z.check_ws(ws)
     dev = scores.device
-    nk = query(p)["num_kept"]
     if kept is None:
-        kept = torch.empty(max(nk, 1), dtype=torch.int32, device=dev)
+        kept = torch.empty(max(z.kept, 1), dtype=torch.int32, device=dev)
     if ks_kept is None:
-        ks_kept = torch.empty(max(nk, 1), dtype=torch.float32, device=dev)
+        ks_kept = torch.empty(max(z.kept, 1), dtype=torch.float32, device=dev)
     ws = workspace(p, dev) if ws is None else ws
     c = p.cstruct()
     _check("actkv_lrfu_select", lib.actkv_lrfu_select(
         ctypes.byref(c), _ptr(scores), float(top_p), float(decay), _ptr(ks), _ptr(hit),
-        _ptr(pooled), _ptr(kept), _ptr(ks_kept), _ptr(ws), ws.numel(), _stream(stream)))
-    return dict(kept=kept[:nk], ks_kept=ks_kept[:nk], pooled=pooled, hit=hit)
+        _ptr(pooled), _ptr(kept), _ptr(ks_kept), _ptr(ws), _ws_bytes(ws), _stream(stream)))
+    return dict(kept=kept[:z.kept], ks_kept=ks_kept[:z.kept], pooled=pooled, hit=hit)
 
 
 def step_lrfu(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch.Tensor,
@@ -370,24 +526,29 @@ def step_lrfu(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: 
               ws: Optional[torch.Tensor] = None, stream=None, qy: Optional[dict] = None) -> dict:
     """The whole step with LRFU eviction, in place on kv_cache / block_table / ks."""
     lib = load_library()
+    z = _Sizes(p, qy)
+    z.need("ks", ks, _F32, z.scores)
+    z.need("hit", hit, _U8, z.scores, required=False)
+    z.need("ks_kept", ks_kept, _F32, z.kept, required=False)
+    _step_args(z, q, kv_cache, block_table, free_pages, lse, scores, pooled, kept, freed,
+               new_lens, ws)
     dev = kv_cache.device
-    qy = query(p) if qy is None else qy
     if freed is None:
-        freed = torch.empty(max(qy["pages_freed"], 1), dtype=torch.int32, device=dev)
+        freed = torch.empty(max(z.freed, 1), dtype=torch.int32, device=dev)
     if new_lens is None:
-        new_lens = torch.empty(p.num_reqs * p.num_kv_heads, dtype=torch.int32, device=dev)
+        new_lens = torch.empty(z.lens, dtype=torch.int32, device=dev)
     if ks_kept is None:
-        ks_kept = torch.empty(max(qy["num_kept"], 1), dtype=torch.float32, device=dev)
+        ks_kept = torch.empty(max(z.kept, 1), dtype=torch.float32, device=dev)
     ws = workspace(p, dev) if ws is None else ws
     c = p.cstruct()
     _check("actkv_step_lrfu", lib.actkv_step_lrfu(
         ctypes.byref(c), _ptr(q), _ptr(kv_cache), _ptr(block_table), _ptr(lse),
-        _ptr(free_pages), free_pages.numel(), float(top_p), float(decay), _ptr(ks),
+        _ptr(free_pages), _numel(free_pages), float(top_p), float(decay), _ptr(ks),
         _ptr(ks_kept), _ptr(scores), _ptr(pooled), _ptr(hit), _ptr(kept), _ptr(freed),
-        _ptr(new_lens), _ptr(ws), ws.numel(), _stream(stream)))
-    return dict(freed=freed[:qy["pages_freed"]], new_lens=new_lens,
-                ks_kept=ks_kept[:qy["num_kept"]], scores=scores, pooled=pooled, hit=hit,
-                kept=None if kept is None else kept[:qy["num_kept"]])
+        _ptr(new_lens), _ptr(ws), _ws_bytes(ws), _stream(stream)))
+    return dict(freed=freed[:z.freed], new_lens=new_lens,
+                ks_kept=ks_kept[:z.kept], scores=scores, pooled=pooled, hit=hit,
+                kept=None if kept is None else kept[:z.kept])
 
 
 def token_confidence(logits: torch.Tensor, top_k: int = 20, out: Optional[torch.Tensor] = None,
@@ -395,19 +556,30 @@ def token_confidence(logits: torch.Tensor, top_k: int = 20, out: Optional[torch.
     """Token-level confidence of every row of `logits` (fp32 [rows, >= vocab] with unit
     column stride); vocab = logits.shape[1]."""
     lib = load_library()
+    if not isinstance(logits, torch.Tensor) or logits.dim() != 2:
+        raise ValueError("logits must be a 2-D tensor [rows, vocab]")
     rows, vocab = int(logits.shape[0]), int(logits.shape[1])
-    if logits.dtype != torch.float32 or logits.stride(1) != 1:
+    if logits.dtype != torch.float32 or (rows > 0 and logits.stride(1) != 1):
         raise ValueError("logits must be float32 with contiguous rows")
-    if out is None:
-        out = torch.empty(max(rows, 1), dtype=torch.float32, device=logits.device)
+    if rows > 1 and logits.stride(0) < vocab:
+        raise ValueError("logits rows must not overlap")
+    if logits.device.type != "cuda":
+        raise ValueError(f"logits must be on the GPU, got {logits.device}")
+    _need("out", out, _F32, rows, required=False)
     need = ctypes.c_size_t()
     _check("actkv_token_confidence_workspace",
            lib.actkv_token_confidence_workspace(rows, vocab, int(top_k), ctypes.byref(need)))
+    if ws is not None:
+        _need("ws", ws, None, 0)
+        if _ws_bytes(ws) < need.value:
+            raise ValueError(f"ws holds {_ws_bytes(ws)} bytes, the call needs {need.value}")
+    if out is None:
+        out = torch.empty(max(rows, 1), dtype=torch.float32, device=logits.device)
     if ws is None:
         ws = torch.empty(max(need.value, 1), dtype=torch.uint8, device=logits.device)
     _check("actkv_token_confidence", lib.actkv_token_confidence(
-        _ptr(logits), rows, vocab, int(logits.stride(0)), int(top_k), _ptr(out), _ptr(ws),
-        ws.numel(), _stream(stream)))
+        _ptr(logits), rows, vocab, int(logits.stride(0)) if rows > 0 else vocab, int(top_k),
+        _ptr(out), _ptr(ws), _ws_bytes(ws), _stream(stream)))
     return out[:rows]
 
 
@@ -420,15 +592,21 @@ def budget_update(token_conf: torch.Tensor, offsets: np.ndarray, budgets: torch.
     [R + 1] on the host; offsets_d, when given, holds the same values on the device and
     saves the copy).  Returns the new budgets, slopes, thresholds and retained counts."""
     lib = load_library()
-    dev = budgets.device
-    off_h = np.ascontiguousarray(offsets, dtype=np.int64)
+    off_h = np.ascontiguousarray(offsets, dtype=np.int64).reshape(-1)
     R = int(off_h.shape[0] - 1)
-    if offsets_d is None:
-        off_d = torch.from_numpy(off_h).to(dev)
-    else:
-        if offsets_d.dtype != torch.int64 or offsets_d.numel() != R + 1:
-            raise ValueError("offsets_d must be int64 [R + 1] on the device")
-        off_d = offsets_d
+    if R < 0:
+        raise ValueError("offsets must hold R + 1 values")
+    n_conf = int(off_h[-1]) if R > 0 else 0
+    seen: list = []
+    _need("token_conf", token_conf, _F32, n_conf, required=n_conf > 0, seen=seen)
+    _need("budgets", budgets, _I32, R, seen=seen)
+    _need("out", out, _I32, R, required=False, seen=seen)
+    _need("offsets_d", offsets_d, (torch.int64,), R + 1, required=False, seen=seen)
+    if offsets_d is not None and offsets_d.numel() != R + 1:
+        raise ValueError("offsets_d must be int64 [R + 1] on the device")
+    _on_gpu(seen)
+    dev = budgets.device
+    off_d = torch.from_numpy(off_h).to(dev) if offsets_d is None else offsets_d
     if out is None:
         out = torch.empty(max(R, 1), dtype=torch.int32, device=dev)
     slopes = torch.empty(max(R, 1), dtype=torch.float64, device=dev)

@@ -367,32 +367,72 @@ class DeviceProblem:
                        kd, vd, [])
 
 
-def make_device_problem(name: str, device="cuda", *, seed: Optional[int] = None,
-                        overrides: Optional[dict] = None) -> DeviceProblem:
-    """Draw workload `name` directly into device memory (torch, seeded)."""
-    import torch
+@dataclass
+class DeviceLayout:
+    """The host-side metadata of a device-drawn workload: lengths, budgets, pool size, the
+    page permutation (its first `used` pages are the requests' pages in request order, the
+    rest the free list) and the per-request random streams of the data."""
+    cfg: WorkloadConfig
+    seq_lens: np.ndarray
+    q_lens: np.ndarray
+    budgets: np.ndarray
+    num_pages: int
+    perm: np.ndarray
+    used: int
+    req_ss: list
+
+    @property
+    def free_pages(self) -> np.ndarray:
+        return self.perm[self.used:].copy()
+
+    @property
+    def block_table(self) -> np.ndarray:
+        """Request r's row: the next ceil(L_r / 16) pages of the permutation (the layout
+        _fill_device writes)."""
+        Y = (self.seq_lens.astype(np.int64) + PAGE_SIZE - 1) // PAGE_SIZE
+        bt = np.full((self.seq_lens.shape[0], int(max(1, Y.max(initial=0)))), -1, np.int32)
+        off = 0
+        for r, y in enumerate(Y):
+            bt[r, :y] = self.perm[off:off + y]
+            off += int(y)
+        return bt
+
+
+def device_layout(name: str, *, seed: Optional[int] = None,
+                  overrides: Optional[dict] = None) -> DeviceLayout:
+    """The metadata make_device_problem draws for workload `name`, without any data."""
     cfg = CONFIGS[name]
     if overrides:
         cfg = WorkloadConfig(**{**cfg.__dict__, **overrides})
     base_seed = cfg.seed if seed is None else seed
     ss = np.random.SeedSequence(base_seed)
     meta_ss, page_ss, budget_ss, *req_ss = ss.spawn(3 + cfg.num_reqs)
-    R, Hq, Hkv, D, BS = cfg.num_reqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, PAGE_SIZE
-    G = Hq // Hkv
     L, n = _draw_lengths(np.random.Generator(np.random.PCG64(meta_ss)), cfg)
     budgets = _draw_budgets(np.random.Generator(np.random.PCG64(budget_ss)), cfg, L)
-    Y = (L.astype(np.int64) + BS - 1) // BS
+    Y = (L.astype(np.int64) + PAGE_SIZE - 1) // PAGE_SIZE
     used = int(Y.sum())
     P = cfg.fixed_pool_pages if cfg.fixed_pool_pages is not None else \
         max(used + 1, int(math.ceil(cfg.pool_factor * used)))
     perm = np.random.Generator(np.random.PCG64(page_ss)).permutation(P).astype(np.int32)
+    return DeviceLayout(cfg, L, n, budgets, P, perm, used, req_ss)
+
+
+def make_device_problem(name: str, device="cuda", *, seed: Optional[int] = None,
+                        overrides: Optional[dict] = None) -> DeviceProblem:
+    """Draw workload `name` directly into device memory (torch, seeded)."""
+    import torch
+    lay = device_layout(name, seed=seed, overrides=overrides)
+    cfg, L, n, budgets, P = lay.cfg, lay.seq_lens, lay.q_lens, lay.budgets, lay.num_pages
+    R, Hq, Hkv, D, BS = cfg.num_reqs, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, PAGE_SIZE
+    G = Hq // Hkv
+    Y = (L.astype(np.int64) + BS - 1) // BS
     bt_stride = int(max(1, Y.max(initial=0)))
     block_table = np.full((R, bt_stride), -1, dtype=np.int32)
     kv = torch.empty((2, P, BS, Hkv, D), dtype=torch.bfloat16, device=device)
     q_all = torch.empty((int(n.sum()), Hq, D), dtype=torch.bfloat16, device=device)
-    pages_list = _fill_device(kv, q_all, block_table, perm[:used], L, n, G, cfg.spike_frac,
-                              req_ss, device)
-    free_pages = perm[used:].copy()
+    pages_list = _fill_device(kv, q_all, block_table, lay.perm[:lay.used], L, n, G,
+                              cfg.spike_frac, lay.req_ss, device)
+    free_pages = lay.free_pages
     sm_scale = float(np.float32(1.0) / np.sqrt(np.float32(D)))
     return DeviceProblem(cfg.name, Hq, Hkv, D, BS, L.astype(np.int32), n.astype(np.int32),
                          budgets.astype(np.int32), block_table, free_pages, sm_scale,

@@ -8,8 +8,13 @@ Checked on the device for the whole batch, against the definition:
     target region did not move;
   * nothing but the destination rows changed anywhere in the cache;
   * block tables keep their last X blocks, the first Y - X are freed in request order;
-  * selection equals the oracle's function of the GPU's own scores.
+  * selection equals the oracle's function of the GPU's own scores;
+  * on sampled requests, new_order, the lengths and the freed pages equal the oracle's
+    in-place compaction (Alg. 4) of the same kept entries: the ascending pairing of the kept
+    entries outside the tail region with the free slots inside it.
 """
+import types
+
 import numpy as np
 import pytest
 import torch
@@ -17,7 +22,7 @@ import torch
 import oracle
 from paper_2609_31395_amd import actkv
 from paper_2609_31395_amd import workloads as W
-from test_gpu_fullsize import WORKLOADS, _offsets, _shape_only
+from test_gpu_fullsize import SAMPLE, WORKLOADS, _offsets, _shape_only
 
 pytestmark = pytest.mark.gpu
 
@@ -103,3 +108,40 @@ def test_whole_batch_inplace_compaction(run_ip):
                                   np.concatenate(freed_ref) if freed_ref else np.zeros(0))
     changed = (kv != kv0).any(dim=-1).any(dim=0)   # [page, slot, head]
     assert not bool((changed & ~written).any()), "rows outside the destinations changed"
+
+
+def test_new_order_matches_the_oracle_on_sampled_requests(run_ip):
+    """The oracle's in-place compaction of request r on its own (one request, its pages
+    numbered 0 .. Y-1) gives the same slot order, lengths and freed blocks (as positions in
+    the request's row) as the whole-batch GPU call."""
+    dp = run_ip["dp"]
+    H, BS = dp.num_kv_heads, dp.page_size
+    _, koff, _ = _offsets(dp)
+    kept = run_ip["kept"].cpu().numpy()
+    order = run_ip["order"].cpu().numpy()
+    freed_off = 0
+    starts = {}
+    for r in range(dp.num_reqs):   # where request r's freed blocks start in the list
+        starts[r] = freed_off
+        L = int(dp.seq_lens[r])
+        k = np.minimum(dp.budgets[r * H:(r + 1) * H].astype(np.int64), L)
+        if not (dp.budgets[r * H:(r + 1) * H] >= L).all():
+            freed_off += -(-L // BS) - -(-int(k.max()) // BS)
+    for r in [r for r in SAMPLE if r < dp.num_reqs]:
+        L = int(dp.seq_lens[r])
+        Y = -(-L // BS)
+        pb = types.SimpleNamespace(
+            seq_lens=np.array([L], np.int32), q_lens=np.array([int(dp.q_lens[r])], np.int32),
+            budgets=dp.budgets[r * H:(r + 1) * H].copy(), num_q_heads=dp.num_q_heads,
+            num_kv_heads=H, head_dim=dp.head_dim, page_size=BS,
+            kv=np.zeros((2, Y, BS, H, dp.head_dim), np.uint16),
+            block_table=np.arange(Y, dtype=np.int32)[None, :], sm_scale=dp.sm_scale,
+            pool_window=dp.pool_window, causal=dp.causal)
+        a, b = int(koff[r * H]), int(koff[(r + 1) * H])
+        ref = oracle.compact_inplace(pb, kept[a:b])
+        np.testing.assert_array_equal(order[a:b], ref["new_order"],
+                                      err_msg=f"{dp.cfg_name} request {r}")
+        np.testing.assert_array_equal(run_ip["new_lens"][r * H:(r + 1) * H], ref["new_lens"])
+        nf = ref["freed"].size
+        got = run_ip["freed"][starts[r]:starts[r] + nf]
+        np.testing.assert_array_equal(got, dp.block_table[r, ref["freed"]])

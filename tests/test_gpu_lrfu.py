@@ -1,11 +1,13 @@
 """GPU parity of the LRFU eviction (actkv_lrfu_select, actkv_step_lrfu) against the oracle.
 
-The hit mask is compared exactly except where the prefix boundary is within rounding of the
-target: the oracle sums the masses in fp64 in sorted order, the GPU in exact 64-bit fixed
-point, so an entry whose preceding mass lies within 1e-9 of the total from the target may
-legitimately fall either way.  Given the GPU's hit mask, the keep-score update is compared
-bit for bit, and the selection, the kept keep scores and the compaction are compared
-bit for bit as the oracle's functions of the GPU's own keep scores."""
+Both sides get the same float32 top_p and decay (the oracle wrapper rounds them as the entry
+point receives them).  The hit mask is compared exactly except where the prefix boundary is
+within rounding of the target: the oracle sums the masses in fp64 in sorted order, the GPU
+sums exact 64-bit fixed-point masses (each score truncated to a multiple of 2^-S), so an
+entry whose preceding mass lies within that truncation and rounding bound of the target may
+legitimately fall either way (boundary_band).  Given the GPU's hit mask, the keep-score
+update is compared bit for bit, and the selection, the kept keep scores and the compaction
+are compared bit for bit as the oracle's functions of the GPU's own keep scores."""
 import numpy as np
 import pytest
 import torch
@@ -18,31 +20,44 @@ from test_gpu_parity import CASES
 
 pytestmark = pytest.mark.gpu
 
-BAND = 1e-9
-
-
 @pytest.fixture(scope="module", autouse=True)
 def _gpu():
     assert torch.cuda.is_available(), "GPU tests need a HIP device"
     actkv.load_library()
 
 
+def fixed_point_shift(vmax: float, L: int) -> int:
+    """The GPU's fixed-point scale for a segment of L entries whose largest score is vmax:
+    masses are floor(v * 2^S) with S = 62 - e - lg, 2^e > vmax (frexp), 2^lg >= L + 1."""
+    _, e = np.frexp(np.float32(vmax))
+    return 62 - int(e) - int(L + 1).bit_length()
+
+
 def boundary_band(pb, att, top_p):
-    """Entries whose running mass before them (oracle order, fp64) is within BAND * total
-    of top_p * total: their hit decision is not fixed by the arithmetic."""
+    """Entries whose hit decision the arithmetic does not fix.  With T the total mass and
+    `before` the mass ahead of an entry in the oracle's order, both sides hit the entry when
+    before < p * T (p the float32 top_p).  The GPU's fixed-point sums are short of the exact
+    ones by less than one unit 2^-S per entry (at most L units, for `before` and for T), its
+    product p * T rounds once in fp64, and the oracle's fp64 sums of L positive terms are
+    within L * 2^-53 * T; an entry is in the band when |before - p * T| is within the sum
+    of those bounds (twice over, for margin)."""
+    p = oracle.as_f32(top_p)
     H = pb.num_kv_heads
     band = np.zeros(att.shape[0], bool)
     off = 0
     for L in pb.seq_lens:
+        L = int(L)
         for _ in range(H):
-            a = att[off:off + int(L)].astype(np.float64)
+            a = np.where(att[off:off + L] > 0, att[off:off + L], 0).astype(np.float64)
             T = a.sum()
-            if T > 0 and 0 < top_p < 1:
-                order = np.lexsort((np.arange(int(L)), -a))
+            if T > 0 and 0 < p < 1:
+                unit = 2.0 ** -fixed_point_shift(a.max(), L)
+                tol = 2 * ((1 + p) * L * unit + p * T * 2.0 ** -52 + 2 * L * 2.0 ** -53 * T)
+                order = np.lexsort((np.arange(L), -a))
                 before = np.concatenate([[0.0], np.cumsum(a[order])[:-1]])
-                near = np.abs(before - top_p * T) <= BAND * T
+                near = np.abs(before - p * T) <= tol
                 band[off + order[near]] = True
-            off += int(L)
+            off += L
     return band
 
 
@@ -100,6 +115,24 @@ def test_lrfu_select_with_ties_and_plateaus():
     ks_in = (rng.integers(0, 8, size=raw.shape[0]) / 16).astype(np.float32)
     hit, band = check_stage(pb, raw, ks_in, 0.9, 0.5)
     assert hit.any() and not hit.all()
+
+
+def test_lrfu_hit_boundary_at_the_float32_top_p():
+    """Two scores a0 = fl32(0.9), a1 = 1 - a0 (total exactly 1, every mass exact in the GPU's
+    fixed point): with the float32 top_p = a0 the first entry alone reaches the target, so
+    only it is hit, on the GPU as in the oracle (the band would excuse this entry, so the
+    mask is asserted directly)."""
+    pb = W.make_custom(seq_lens=[2], q_lens=[1], num_q_heads=1, num_kv_heads=1, head_dim=64,
+                       budgets=[1], pool_window=1)
+    a0 = np.float32(0.9)
+    raw = np.array([a0, np.float32(1.0 - float(a0))], np.float32)
+    bp, _ = to_dev(pb)
+    hit = torch.empty(2, dtype=torch.uint8, device="cuda")
+    ks = torch.zeros(2, dtype=torch.float32, device="cuda")
+    actkv.lrfu_select(bp, torch.from_numpy(raw).cuda(), ks, 0.9, 0.5, hit=hit)
+    torch.cuda.synchronize()
+    assert hit.cpu().numpy().tolist() == oracle.hits(pb, raw, 0.9).tolist() == [1, 0]
+    assert ks.cpu().numpy().tolist() == [float(a0), 0.0]
 
 
 def test_lrfu_select_long_segment_at_the_limit():

@@ -18,6 +18,14 @@ from paper_2609_31395_amd import workloads as W
 pytestmark = pytest.mark.gpu
 
 
+def _random_causal(seed):
+    """Whether seed's random problem is causal (its first draws, without the data)."""
+    rng = np.random.default_rng(10_000 + seed)
+    rng.integers(1, 5), rng.choice([1, 2, 4, 8]), rng.choice([1, 2, 3, 4, 8, 16])
+    rng.choice([64, 128])
+    return bool(rng.random() < 0.8)
+
+
 def _random_problem(seed):
     rng = np.random.default_rng(10_000 + seed)
     R = int(rng.integers(1, 5))
@@ -25,6 +33,7 @@ def _random_problem(seed):
     G = int(rng.choice([1, 2, 3, 4, 8, 16]))
     D = int(rng.choice([64, 128]))
     causal = bool(rng.random() < 0.8)
+    assert causal == _random_causal(seed)
     L = rng.integers(0, 3000, size=R)
     L[rng.random(R) < 0.15] = 0
     L[rng.random(R) < 0.1] = 1
@@ -84,13 +93,12 @@ def test_random_problem_inplace_compaction_matches_the_oracle(seed):
     _assert_same(_run_inplace(pb, kept), oracle.compact_inplace(pb, kept))
 
 
-@pytest.mark.parametrize("seed", range(60))
+@pytest.mark.parametrize("seed", [s for s in range(80) if _random_causal(s)][:60])
 def test_random_decode_step_matches_the_oracle(seed):
     """One action query per request (the decode-step scoring kernel when G <= 16), added
-    twice to an aggregate that starts at zero: twice the oracle's scores."""
+    twice to an aggregate that starts at zero: twice the oracle's scores.  Decode steps are
+    causal, so only the causal random problems run."""
     pb, agg, _ = _random_problem(seed)
-    if not pb.causal:
-        pytest.skip("decode steps are causal")
     n1 = np.minimum(pb.q_lens, 1).astype(np.int32)
     pb1 = W.make_custom(seq_lens=pb.seq_lens, q_lens=n1, num_q_heads=pb.num_q_heads,
                         num_kv_heads=pb.num_kv_heads, head_dim=pb.head_dim,

@@ -46,7 +46,7 @@ def test_hand_worked_region_past_the_end():
     # L = 40, budget 10: Y = 3, X = 1, Start = 32, End = 42 > L.  Kept inside [32, 42): 33,
     # 35, 38, 39.  Destinations (not kept, ascending): 32, 34, 36, 37, 40, 41 -- the last two
     # are past L but exist in the third block.  Sources (kept outside, ascending): 2, 3, 5,
-    # 20, 21, 30.  Zip: 2->32, 3->34, 5->36, 20->37, 21->40, 30->41.
+    # 20, 21, 30.  Pairs: 2->32, 3->34, 5->36, 20->37, 21->40, 30->41.
     pb = _pb([40], [10])
     kept = np.array([2, 3, 5, 20, 21, 30, 33, 35, 38, 39], np.int32)
     out = oracle.compact_inplace(pb, kept)

@@ -18,7 +18,9 @@ def _pb(seq_lens, budgets=None, H=1, window=1):
 
 
 def brute_hits(att, seq_lens, H, p):
-    """Shortest prefix of the (score desc, index asc) order whose running sum reaches p x total."""
+    """Shortest prefix of the (score desc, index asc) order whose running sum reaches p x total
+    (p as the float32 the entry points take)."""
+    p = float(np.float32(p))
     out, off = np.zeros(att.shape[0], np.uint8), 0
     for L in seq_lens:
         for _ in range(H):
@@ -54,6 +56,23 @@ def test_hits_hand_worked():
     assert oracle.hits(pb, att, 1.0).tolist() == [1, 1, 0, 1]      # the zero is never needed
     assert oracle.hits(pb, att, 0.0).tolist() == [0, 0, 0, 0]
     assert oracle.hits(pb, np.zeros(4, np.float32), 0.9).tolist() == [0, 0, 0, 0]
+
+
+def test_top_p_is_taken_as_float32():
+    """The oracle wrapper rounds top_p to float32, the type of the GPU entry point's argument.
+    Two scores a0 = fl32(0.9) and a1 = 1 - a0 sum to exactly 1: with p = fl32(0.9) the first
+    entry alone reaches p x total, with the double 0.9 the second is needed as well."""
+    a0 = np.float32(0.9)
+    a1 = np.float32(1.0 - float(a0))
+    assert float(a0) + float(a1) == 1.0 and float(a0) < 0.9
+    pb = _pb([2])
+    att = np.array([a0, a1], np.float32)
+    assert oracle.as_f32(0.9) == float(a0)
+    assert oracle.hits(pb, att, 0.9).tolist() == [1, 0]
+    assert oracle.hits(pb, att, float(np.nextafter(a0, np.float32(1.0)))).tolist() == [1, 1]
+    ks = oracle.lrfu_update(pb, att, np.array([1, 0], np.uint8), 0.1, np.ones(2, np.float32))
+    assert ks.tolist() == [float(np.float32(np.float32(0.1) * np.float32(1.0)) + a0),
+                           float(np.float32(0.1))]
 
 
 def test_equal_scores_are_hit_lower_index_first():
