@@ -37,9 +37,6 @@ constexpr int kConfCandCap = 2048;                               // LDS candidat
 constexpr int kConfMaxCand = kConfMaxSplits * kConfMaxTopK;      // 1024 merge candidates
 constexpr int kMergePerLane = kConfMaxCand / 64;
 constexpr int kBudgetThreads = 1024;
-// Word 3 of a raw buffer resource on CDNA: 32-bit data format; reads at byte offsets at or
-// past num_records return 0.
-constexpr int kBufferRsrcWord3 = 0x00020000;
 
 static_assert(kConfChunk % kConfThreads == 0, "whole rows of logits per thread");
 static_assert(kConfMaxTopK <= 64, "the k largest fit one wave, one per lane");
@@ -245,9 +242,8 @@ __global__ __launch_bounds__(kConfThreads) void token_conf_partial_kernel(
   }
   for (int j = kk + tid; j < k; j += kConfThreads) top[j] = ninf;   // padding
   // logit tid + j * 256 of the chunk in v[j]; the hardware returns 0 past the chunk
-  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(logits + row * row_stride + c0), (short)0, n * (int)sizeof(float),
-      kBufferRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rs =
+      buffer_over(logits + row * row_stride + c0, n * (int)sizeof(float));
   float v[kConfPerThread];
 #pragma unroll
   for (int j = 0; j < kConfPerThread; ++j)

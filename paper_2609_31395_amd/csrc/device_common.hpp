@@ -35,6 +35,27 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Word 3 of a raw (stride 0) buffer resource on CDNA: 32-bit data format; reads at byte
+// offsets at or past num_records return 0 and writes there are dropped.
+constexpr int kBufferRsrcWord3 = 0x00020000;
+
+// A raw buffer resource over `bytes` bytes at p.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_over(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes,
+                                           kBufferRsrcWord3);
+}
+
+// The same for a pointer and size that every lane of the wave holds, taken from the first
+// lane: the compiler then keeps the resource in scalar registers (a resource it cannot
+// prove uniform is applied lane group by lane group, in a loop).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_over_uniform(const void* p, int bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  return buffer_over(reinterpret_cast<const void*>(((uint64_t)hi << 32) | lo),
+                     __builtin_amdgcn_readfirstlane(bytes));
+}
+
 // One DPP step on a 64-bit value (both halves moved by the same lane pattern); lanes with
 // no source, and lanes of rows outside kRowMask, read 0.
 template <int kCtrl, int kRowMask>

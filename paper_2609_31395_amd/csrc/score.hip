@@ -122,14 +122,11 @@ __device__ __forceinline__ KLoadPlan<D, W> make_k_load_plan(int h, int Hkv) {
 // wave-uniform page id of that run (keys past L map to the request's last page); it is
 // fetched a tile ahead so that the scalar load never stalls the DMA issue.
 template <int D, int W>
-__device__ __forceinline__ int64_t page_of(const int32_t* __restrict__ bt_row, int L,
-                                           int64_t num_pages, const KLoadPlan<D, W>& kp,
-                                           int64_t tile) {
+__device__ __forceinline__ int32_t page_of(const int32_t* __restrict__ bt_row, int L,
+                                           const KLoadPlan<D, W>& kp, int64_t tile) {
   using Gm = TileGeom<D, W>;
   const int64_t kbase = tile * kKeyTile + kp.wl0 * Gm::kRowsPerLoad;   // wave-uniform
-  int64_t page = bt_row[(kbase < L ? kbase : L - 1) / kPageSize];
-  if (page < 0 || page >= num_pages) page = 0;   // never dereference outside the pool
-  return page;
+  return bt_row[(kbase < L ? kbase : L - 1) / kPageSize];
 }
 
 // This wave's share of a K tile whose keys live in page `page`, fetched straight into the
@@ -137,12 +134,15 @@ __device__ __forceinline__ int64_t page_of(const int32_t* __restrict__ bt_row, i
 // (their results are discarded).
 template <int D, int W>
 __device__ __forceinline__ void issue_k_tile(uint32_t dst, const char* __restrict__ kv_bytes,
-                                             int64_t page, int64_t page_bytes,
-                                             const KLoadPlan<D, W>& kp) {
+                                             int32_t page_entry, int64_t num_pages,
+                                             int64_t page_bytes, const KLoadPlan<D, W>& kp) {
   using Gm = TileGeom<D, W>;
   static_assert(Gm::kRowsPerLoad * Gm::kLoadsPerWave <= kPageSize &&
                     kPageSize % (Gm::kRowsPerLoad * Gm::kLoadsPerWave) == 0,
                 "a wave's loads of one tile must stay inside one page");
+  // never dereference outside the pool (checked here, where the entry is used, so that the
+  // scalar load that fetched it is not waited for a tile early)
+  const int64_t page = (page_entry < 0 || page_entry >= num_pages) ? 0 : page_entry;
   const char* base = kv_bytes + page * page_bytes;
 #pragma unroll
   for (int u = 0; u < Gm::kLoadsPerWave; ++u)
@@ -310,18 +310,20 @@ __device__ __forceinline__ bf16x8 lds_k16(const char* tile_buf, int sub, const K
 template <int D>
 struct Pipe16 {
   f32x4 c1, c2;                       // accumulators of units g-1 and g-2
-  bf16x8 kr[Geom16<D>::kSteps];       // B operand of the next chain
+  bf16x8 kb[2][Geom16<D>::kSteps];    // B operands: sub-tile s of a tile reads kb[s & 1]
   float part[4];                      // the lane's partials of the current sub-tile, one per
                                       // accumulator element (independent add chains)
   float ex;                           // SUM: the last exp2 result, added one slot later
   float mx;                           // MAX_MEAN, G = 8 / 16: running group max
 };
 
-// One phase.  kChain: chain of row tile q against st.kr.  kEpi: epilogue of st.c2 for row
-// tile kRt (beta bt, causal positions at prow, key `key`).  kLoad: after the MFMA of
-// k-step ks, st.kr[ks] <- the next unit's operand (sub-tile next_sub of next_buf).
+// One phase.  kChain: chain of row tile q against operand kr.  kEpi: epilogue of st.c2 for
+// row tile kRt (beta bt, causal positions at prow, key `key`).  kLoad: kl <- the operand of
+// sub-tile next_sub of next_buf (read from LDS here, used a whole sub-tile later).
 template <int D, bool kMaxMean, bool kMask, bool kChain, bool kEpi, bool kLoad, int kRt>
 __device__ __forceinline__ void score_phase16(Pipe16<D>& st, const bf16x8 (&q)[Geom16<D>::kSteps],
+                                              const bf16x8 (&kr)[Geom16<D>::kSteps],
+                                              bf16x8 (&kl)[Geom16<D>::kSteps],
                                               const KRead16& rp, const char* next_buf, int next_sub,
                                               const float (&bt)[4], const int32_t* prow, int key,
                                               float alpha, int G) {
@@ -333,11 +335,14 @@ __device__ __forceinline__ void score_phase16(Pipe16<D>& st, const bf16x8 (&q)[G
     const int4 p4 = *reinterpret_cast<const int4*>(prow);
     pt[0] = p4.x; pt[1] = p4.y; pt[2] = p4.z; pt[3] = p4.w;
   }
+  if (kLoad) {
+#pragma unroll
+    for (int ks = 0; ks < S; ++ks) kl[ks] = lds_k16<D>(next_buf, next_sub, rp, ks);
+  }
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int ks = 0; ks < S; ++ks) {
-    if (kChain) acc = mfma16(q[ks], st.kr[ks], acc);
-    if (kLoad) st.kr[ks] = lds_k16<D>(next_buf, next_sub, rp, ks);
+    if (kChain) acc = mfma16(q[ks], kr[ks], acc);
     if (kEpi) {
 #pragma unroll
       for (int v = ks * EPS; v < (ks + 1) * EPS; ++v) {
@@ -384,7 +389,8 @@ struct SweepCtx {
   const char* kv_bytes;
   const int32_t* bt_row;
   const int32_t* pos_s;    // LDS: causal position of every row of the chunk
-  float* out;              // scores (or chunk partials) of this (request, KV head)
+  __amdgpu_buffer_rsrc_t out;   // scores (or chunk partials) of this (request, KV head):
+                                // exactly L floats, stores past them are dropped
   const char* kbuf;        // LDS: the K stages
   int64_t page_bytes, num_pages;
   int i0, i1;              // key tiles of this workgroup
@@ -403,39 +409,67 @@ constexpr int kRedBufs = 4;   // a tile's partials are read one tile later
 
 // Sum of the 32 partials of each key of tile t in a fixed order; wave w finishes keys
 // 8w .. 8w+7.  Lane l takes key 8w + l/8 and the four partials of wave l%8, then the
-// eight lanes of a key are summed pairwise (xor 1, 2, 4).
+// eight lanes of a key are summed pairwise (xor 1, xor 2, then the other four).
 __device__ __forceinline__ float dpp_xor1(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
 }
 __device__ __forceinline__ float dpp_xor2(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
 }
-__device__ __forceinline__ float swz_xor4(float v) {
-  // ds_swizzle bit mode: and 0x1f, or 0, xor 4 (within 32-lane halves)
-  return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x101F));
+// Lane 7 - i of the lane's group of eight (DPP row_half_mirror).  After the xor 1 and xor 2
+// sums every lane of a group of four holds the same value, so this adds the other four.
+__device__ __forceinline__ float dpp_half_mirror(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
 }
 
-__device__ __forceinline__ void finish_tile(const SweepCtx& cx, const RedTile& red, int t) {
+// The finish of a tile in two halves, a phase apart, so that the LDS reads are not waited
+// for at once: finish_read fetches this lane's four partials, finish_write sums them and
+// the eight lanes of its key, and stores the key's score (only when `valid`).  Every lane
+// takes part in the store (lanes that do not write use an offset past the buffer), so each
+// wave issues exactly one vector-memory store per call whatever the keys, with no branch:
+// the K pipeline's waits count on that.
+__device__ __forceinline__ float4 finish_read(const RedTile& red) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int kk = w * (kKeyTile / kWaves) + (lane >> 3), ww = lane & 7;
   const float* rr = red[ww] + kk;
-  float v = (rr[0] + rr[kRedGrp]) + (rr[2 * kRedGrp] + rr[3 * kRedGrp]);
-  v += dpp_xor1(v);
-  v += dpp_xor2(v);
-  v += swz_xor4(v);
-  const int key = t * kKeyTile + kk;
-  if (ww == 0 && key < cx.L) cx.out[key] = v * cx.out_scale;
+  return make_float4(rr[0], rr[kRedGrp], rr[2 * kRedGrp], rr[3 * kRedGrp]);
 }
 
+__device__ __forceinline__ void finish_write(const SweepCtx& cx, float4 p, int t, bool valid) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int kk = w * (kKeyTile / kWaves) + (lane >> 3), ww = lane & 7;
+  float v = (p.x + p.y) + (p.z + p.w);
+  v += dpp_xor1(v);
+  v += dpp_xor2(v);
+  v += dpp_half_mirror(v);
+  const int key = t * kKeyTile + kk;
+  const uint32_t off = (valid && ww == 0 && key < cx.L) ? (uint32_t)key * 4u : 0x7FFFFFF0u;
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v * cx.out_scale), cx.out, off, 0, 0);
+}
+
+// The K pipeline's vector-memory sequence per wave is, from the first tile of a segment on,
+// (loads of one K tile, one score store) repeated: the sweep's prologue issues a store that
+// writes nothing after each of its tile loads, and the tile after the first one finishes
+// nothing real.  So at the barrier of every tile, when the loads of tile i + 1 must have
+// landed, exactly the stores and loads of the two tiles after it (and a store) may still be
+// in flight: one wait count for every tile, and no branch in the loop body.
+template <int D>
+constexpr int kTileVmcnt = (kScoreStages - 2) * (TileGeom<D>::kLoadsPerWave + 1) + 1;
+
 // Phases P = 2 .. U+1 of tile i, U = 4 * NRT units per tile: the chain of unit P (of tile
-// i, or of tile i+1 once P >= U) and the epilogue of unit P - 2 of tile i.
+// i, or of tile i+1 once P >= U) and the epilogue of unit P - 2 of tile i.  The chain of
+// the first unit of a sub-tile also reads the next sub-tile's operand from LDS, a whole
+// sub-tile ahead of its use.  Phase 3 NRT (the first unit of sub-tile 3) reads sub-tile 0
+// of tile i+1: the barrier that makes tile i+1 visible sits there, and once every wave has
+// passed it no wave reads tile i's stage any more, which is then refilled.
 // kMask: tile i holds keys hidden from some rows.  kLast: no tile follows.
 template <int D, bool kMaxMean, int NRT, bool kMask, bool kLast, int P>
 __device__ __forceinline__ void tile_phases16(const SweepCtx& cx, const KLoadPlan<D, kWaves>& kp,
                                               const KRead16& rp, Pipe16<D>& st,
                                               const bf16x8 (&qreg)[kRowTilesPerWave][Geom16<D>::kSteps],
                                               const float (&beta)[kRowTilesPerWave][4],
-                                              RedTile* red, int i, int64_t& next_page) {
+                                              RedTile* red, int i, int32_t& next_page,
+                                              float4& fin) {
   constexpr int U = kSubTiles * NRT;
   if constexpr (P <= U + 1) {
     using Gm = TileGeom<D>;
@@ -444,32 +478,34 @@ __device__ __forceinline__ void tile_phases16(const SweepCtx& cx, const KLoadPla
     const int st_i = (i - cx.i0) & (kScoreStages - 1), st_n = (i + 1 - cx.i0) & (kScoreStages - 1);
     const char* buf_i = cx.kbuf + st_i * Gm::kTileBytes;
     const char* buf_n = cx.kbuf + st_n * Gm::kTileBytes;
-    if constexpr (P == U - 1) {
+    constexpr int kBarrier = 3 * NRT;
+    if constexpr (P == kBarrier) {
       // tile i + 1 is read from this phase on: this wave's loads of it have landed, this
       // wave's LDS traffic of tile i is retired, then the barrier
-      wait_vmcnt<(kScoreStages - 2) * Gm::kLoadsPerWave>();
+      wait_vmcnt<kTileVmcnt<D>>();
       wait_lgkmcnt0();
       __builtin_amdgcn_s_barrier();
       // no wave reads tile i any more: refill its stage with tile i + kScoreStages
       issue_k_tile<D, kWaves>(cx.kl + st_i * Gm::kTileBytes, cx.kv_bytes, next_page,
-                              cx.page_bytes, kp);
+                              cx.num_pages, cx.page_bytes, kp);
       const int nt = i + kScoreStages + 1;
-      next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, nt < cx.i1 ? nt : cx.i1 - 1);
-      if (i > cx.i0) finish_tile(cx, red[(i - 1) & (kRedBufs - 1)], i - 1);
+      next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp, nt < cx.i1 ? nt : cx.i1 - 1);
+      fin = finish_read(red[(i - 1) & (kRedBufs - 1)]);   // unused in the first tile
     }
     // epilogue: unit P - 2 of tile i
     constexpr int eu = P - 2, es = eu / NRT, er = eu % NRT;
     const int32_t* prow = cx.pos_s + (w + kWaves * er) * kRowTile + 4 * (lane >> 4);
     const int key = i * kKeyTile + es * 16 + (lane & 15);
-    // chain: unit P of tile i, or unit P - U of tile i + 1
+    // chain: unit cu of tile i (P < U) or of tile i + 1
     constexpr bool kChain = P < U || !kLast;
-    constexpr int cr = (P < U ? P : P - U) % NRT;
-    // operand of unit P + 1 when it starts a sub-tile
-    constexpr int nu = P + 1;
-    constexpr bool kLoad = (nu % NRT == 0) && (nu < U || !kLast);
-    constexpr int lsub = (nu < U ? nu : nu - U) / NRT;
+    constexpr int cu = P < U ? P : P - U, cs = cu / NRT, cr = cu % NRT;
+    // the first unit of a sub-tile reads the operand of the next one
+    constexpr bool kNextTile = P < U && cs + 1 == kSubTiles;
+    constexpr bool kLoad = kChain && cu % NRT == 0 && !(kNextTile && kLast);
+    constexpr int lsub = (cs + 1) % kSubTiles;
     score_phase16<D, kMaxMean, kMask, kChain, true, kLoad, er>(
-        st, qreg[cr], rp, nu < U ? buf_i : buf_n, lsub, beta[er], prow, key, cx.alpha, cx.G);
+        st, qreg[cr], st.kb[cs & 1], st.kb[(cs + 1) & 1], rp,
+        (P < U && !kNextTile) ? buf_i : buf_n, lsub, beta[er], prow, key, cx.alpha, cx.G);
     if constexpr (er == NRT - 1) {
       // sub-tile es is complete in this lane: hand its partial to the other waves
       if (!kMaxMean) {
@@ -480,8 +516,12 @@ __device__ __forceinline__ void tile_phases16(const SweepCtx& cx, const KLoadPla
           (st.part[0] + st.part[1]) + (st.part[2] + st.part[3]);
       st.part[0] = st.part[1] = st.part[2] = st.part[3] = 0.f;
     }
+    if constexpr (P == kBarrier + 1) {
+      // the finish of tile i - 1, whose partials were read a phase ago
+      finish_write(cx, fin, i - 1, i > cx.i0);
+    }
     tile_phases16<D, kMaxMean, NRT, kMask, kLast, P + 1>(cx, kp, rp, st, qreg, beta, red, i,
-                                                          next_page);
+                                                          next_page, fin);
   }
 }
 
@@ -495,12 +535,15 @@ __device__ __forceinline__ void score_sweep16(const SweepCtx& cx, const KLoadPla
                                               RedTile* red) {
   using Gm = TileGeom<D>;
   auto clamp_tile = [&](int t) { return t < cx.i1 ? t : cx.i1 - 1; };
+  float4 fin = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int p = 0; p < kScoreStages - 1; ++p)
+  for (int p = 0; p < kScoreStages - 1; ++p) {
     issue_k_tile<D, kWaves>(cx.kl + p * Gm::kTileBytes, cx.kv_bytes,
-                            page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(cx.i0 + p)),
-                            cx.page_bytes, kp);
-  int64_t next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp,
+                            page_of<D, kWaves>(cx.bt_row, cx.L, kp, clamp_tile(cx.i0 + p)),
+                            cx.num_pages, cx.page_bytes, kp);
+    finish_write(cx, fin, 0, false);   // the store slot of the tile (writes nothing)
+  }
+  int32_t next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp,
                                          clamp_tile(cx.i0 + kScoreStages - 1));
   const KRead16 rp = make_k_read16<D>();
   Pipe16<D> st;
@@ -508,36 +551,39 @@ __device__ __forceinline__ void score_sweep16(const SweepCtx& cx, const KLoadPla
   st.ex = 0.f;
   st.mx = 0.f;
   st.c1 = f32x4{0.f, 0.f, 0.f, 0.f};
-  // prologue: tile i0 in LDS, the last stage filled, chains of units 0 and 1
-  wait_vmcnt<(kScoreStages - 2) * Gm::kLoadsPerWave>();
+  // prologue: tile i0 in LDS, the last stage filled, operand of sub-tile 0, chains of units
+  // 0 and 1 (each reading the next sub-tile's operand when it starts a sub-tile)
+  wait_vmcnt<kTileVmcnt<D>>();
   __builtin_amdgcn_s_barrier();
   issue_k_tile<D, kWaves>(cx.kl + (kScoreStages - 1) * Gm::kTileBytes, cx.kv_bytes, next_page,
-                          cx.page_bytes, kp);
-  next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(cx.i0 + kScoreStages));
+                          cx.num_pages, cx.page_bytes, kp);
+  finish_write(cx, fin, 0, false);
+  next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp, clamp_tile(cx.i0 + kScoreStages));
 #pragma unroll
-  for (int ks = 0; ks < Geom16<D>::kSteps; ++ks) st.kr[ks] = lds_k16<D>(cx.kbuf, 0, rp, ks);
-  score_phase16<D, kMaxMean, false, true, false, 1 % NRT == 0, 0>(
-      st, qreg[0], rp, cx.kbuf, 1 / NRT, beta[0], nullptr, 0, cx.alpha, cx.G);
-  score_phase16<D, kMaxMean, false, true, false, 2 % NRT == 0, 0>(
-      st, qreg[1 % NRT], rp, cx.kbuf, 2 / NRT, beta[0], nullptr, 0, cx.alpha, cx.G);
+  for (int ks = 0; ks < Geom16<D>::kSteps; ++ks) st.kb[0][ks] = lds_k16<D>(cx.kbuf, 0, rp, ks);
+  score_phase16<D, kMaxMean, false, true, false, true, 0>(
+      st, qreg[0], st.kb[0], st.kb[1], rp, cx.kbuf, 1, beta[0], nullptr, 0, cx.alpha, cx.G);
+  score_phase16<D, kMaxMean, false, true, false, NRT == 1, 0>(
+      st, qreg[1 % NRT], st.kb[(1 / NRT) & 1], st.kb[(1 / NRT + 1) & 1], rp, cx.kbuf, 2,
+      beta[0], nullptr, 0, cx.alpha, cx.G);
   for (int i = cx.i0; i < cx.i1; ++i) {
     const bool mask = i * kKeyTile + kKeyTile - 1 > cx.mask_from;
     if (i + 1 < cx.i1) {
       if (mask)
-        tile_phases16<D, kMaxMean, NRT, true, false, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page);
+        tile_phases16<D, kMaxMean, NRT, true, false, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page, fin);
       else
-        tile_phases16<D, kMaxMean, NRT, false, false, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page);
+        tile_phases16<D, kMaxMean, NRT, false, false, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page, fin);
     } else {
       if (mask)
-        tile_phases16<D, kMaxMean, NRT, true, true, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page);
+        tile_phases16<D, kMaxMean, NRT, true, true, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page, fin);
       else
-        tile_phases16<D, kMaxMean, NRT, false, true, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page);
+        tile_phases16<D, kMaxMean, NRT, false, true, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page, fin);
     }
   }
   // the last tile's partials
   wait_lgkmcnt0();
   __builtin_amdgcn_s_barrier();
-  finish_tile(cx, red[(cx.i1 - 1) & (kRedBufs - 1)], cx.i1 - 1);
+  finish_write(cx, finish_read(red[(cx.i1 - 1) & (kRedBufs - 1)]), cx.i1 - 1, true);
 }
 
 // The sweep of a wave whose row tiles hold no real row (few query rows, e.g. one decode
@@ -559,31 +605,31 @@ __device__ __forceinline__ void score_sweep_idle(const SweepCtx& cx, const KLoad
 #pragma unroll
   for (int p = 0; p < kScoreStages - 1; ++p)
     issue_k_tile<D, kWaves>(cx.kl + p * Gm::kTileBytes, cx.kv_bytes,
-                            page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(cx.i0 + p)),
-                            cx.page_bytes, kp);
-  int64_t next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp,
+                            page_of<D, kWaves>(cx.bt_row, cx.L, kp, clamp_tile(cx.i0 + p)),
+                            cx.num_pages, cx.page_bytes, kp);
+  int32_t next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp,
                                          clamp_tile(cx.i0 + kScoreStages - 1));
   wait_vmcnt<(kScoreStages - 2) * Gm::kLoadsPerWave>();
   wait_lgkmcnt0();
   __builtin_amdgcn_s_barrier();
   issue_k_tile<D, kWaves>(cx.kl + (kScoreStages - 1) * Gm::kTileBytes, cx.kv_bytes, next_page,
-                          cx.page_bytes, kp);
-  next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, clamp_tile(cx.i0 + kScoreStages));
+                          cx.num_pages, cx.page_bytes, kp);
+  next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp, clamp_tile(cx.i0 + kScoreStages));
   for (int i = cx.i0; i < cx.i1; ++i) {
     // the barrier phase of tile i, as in tile_phases16
     const int st_i = (i - cx.i0) & (kScoreStages - 1);
     wait_vmcnt<(kScoreStages - 2) * Gm::kLoadsPerWave>();
     wait_lgkmcnt0();
     __builtin_amdgcn_s_barrier();
-    issue_k_tile<D, kWaves>(cx.kl + st_i * Gm::kTileBytes, cx.kv_bytes, next_page, cx.page_bytes,
-                            kp);
+    issue_k_tile<D, kWaves>(cx.kl + st_i * Gm::kTileBytes, cx.kv_bytes, next_page, cx.num_pages,
+                            cx.page_bytes, kp);
     const int nt = i + kScoreStages + 1;
-    next_page = page_of<D, kWaves>(cx.bt_row, cx.L, cx.num_pages, kp, nt < cx.i1 ? nt : cx.i1 - 1);
-    if (i > cx.i0) finish_tile(cx, red[(i - 1) & (kRedBufs - 1)], i - 1);
+    next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp, nt < cx.i1 ? nt : cx.i1 - 1);
+    finish_write(cx, finish_read(red[(i - 1) & (kRedBufs - 1)]), i - 1, i > cx.i0);
   }
   wait_lgkmcnt0();
   __builtin_amdgcn_s_barrier();
-  finish_tile(cx, red[(cx.i1 - 1) & (kRedBufs - 1)], cx.i1 - 1);
+  finish_write(cx, finish_read(red[(cx.i1 - 1) & (kRedBufs - 1)]), cx.i1 - 1, true);
 }
 
 template <int D, bool kMaxMean>
@@ -658,8 +704,10 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
     cx.L = L;
     cx.mask_from = dp.causal ? L - n : L;  // keys past this may be hidden from some rows
     cx.out_scale = (kMaxMean && pl.nchunk == 1) ? (n > 0 ? 1.0f / n : 0.0f) : 1.0f;
-    cx.out = (c == 0) ? scores_ptr + pl.seg_off + (int64_t)h * L
-                      : part_ptr + (int64_t)(c - 1) * num_scores + pl.seg_off + (int64_t)h * L;
+    cx.out = buffer_over_uniform((c == 0) ? scores_ptr + pl.seg_off + (int64_t)h * L
+                                          : part_ptr + (int64_t)(c - 1) * num_scores +
+                                                pl.seg_off + (int64_t)h * L,
+                                 L * (int)sizeof(float));
     const KLoadPlan<D, kWaves> kp = make_k_load_plan<D, kWaves>(h, Hkv);
     // every ordinary load of the setup has landed before the K pipeline starts, so the
     // sweep needs no compiler-inserted wait on the vector-memory queue
@@ -840,8 +888,7 @@ __global__ __launch_bounds__(kDecMaxWaves * 64) void score_decode_kernel(
     const int32_t* bt_row = bt_ptr + (int64_t)r * dp.bt_stride;
     float* out = acc_ptr + pl.seg_off + (int64_t)h * L;
     // the aggregate of this segment: reads past L return 0, writes there are dropped
-    const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
-        out, (short)0, L * (int)sizeof(float), 0x00020000);
+    const __amdgpu_buffer_rsrc_t ars = buffer_over(out, L * (int)sizeof(float));
     const uint32_t lane_off = (uint32_t)((((lane & 15) * Hkv + h) * D) * 2 + (lane >> 4) * 16);
     for (int fb = p0; fb < p1; fb += kDecFlushPages) {
       const int pe = fb + kDecFlushPages < p1 ? fb + kDecFlushPages : p1;
@@ -1006,9 +1053,9 @@ __global__ __launch_bounds__(kLseThreads, 1) void lse_partial_kernel(
 #pragma unroll
   for (int p = 0; p < kStages - 1; ++p)
     issue_k_tile<D, kLseWaves>(kl + p * Gm::kTileBytes, kv_bytes,
-                               page_of<D, kLseWaves>(bt_row, L, dp.num_pages, kp, clamp_tile(t0 + p)),
-                               page_bytes, kp);
-  int64_t next_page = page_of<D, kLseWaves>(bt_row, L, dp.num_pages, kp, clamp_tile(t0 + kStages - 1));
+                               page_of<D, kLseWaves>(bt_row, L, kp, clamp_tile(t0 + p)),
+                               dp.num_pages, page_bytes, kp);
+  int32_t next_page = page_of<D, kLseWaves>(bt_row, L, kp, clamp_tile(t0 + kStages - 1));
   // keys up to the first action query's position are visible to every real row (rows past
   // n, all padding, are never written): tiles below it need no mask
   const int64_t open_to = dp.causal ? (int64_t)L - n : (int64_t)L - 1;
@@ -1017,8 +1064,8 @@ __global__ __launch_bounds__(kLseThreads, 1) void lse_partial_kernel(
     wait_vmcnt<(kStages - 2) * Gm::kLoadsPerWave>();
     __builtin_amdgcn_s_barrier();
     issue_k_tile<D, kLseWaves>(kl + ((st + kStages - 1) % kStages) * Gm::kTileBytes, kv_bytes,
-                               next_page, page_bytes, kp);
-    next_page = page_of<D, kLseWaves>(bt_row, L, dp.num_pages, kp, clamp_tile(i + kStages));
+                               next_page, dp.num_pages, page_bytes, kp);
+    next_page = page_of<D, kLseWaves>(bt_row, L, kp, clamp_tile(i + kStages));
     const bool masked = i * kKeyTile + kKeyTile - 1 > open_to;
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {

@@ -40,10 +40,6 @@ static_assert(kRows % 2 == 0, "the coalesced passes run in two batches of rows")
 constexpr int kRunBatch = 8;              // run entries whose LDS reads are issued together
 constexpr int kLdsPad = 16;               // LDS entries past the segment a batch may read
 constexpr int kPoolHalo = 3;              // pooling windows up to 7 run in place
-// Word 3 of a raw (stride 0) buffer resource on CDNA: 32-bit data format; reads at byte
-// offsets at or past num_records return 0 and writes there are dropped.
-constexpr int kBufferRsrcWord3 = 0x00020000;
-
 // Unsigned key that orders exactly like the float (negative values included; -0 == +0).
 __device__ __forceinline__ uint32_t order_key(float v) {
   const uint32_t u = __float_as_uint(v == 0.0f ? 0.0f : v);
@@ -57,11 +53,6 @@ __device__ __forceinline__ float key_value(uint32_t k) {
 
 // -0 as +0 (the pooled score of an entry is the value its order key stands for).
 __device__ __forceinline__ float canonical(float v) { return v == 0.0f ? 0.0f : v; }
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_over(const void* p, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes,
-                                           kBufferRsrcWord3);
-}
 
 // Byte offset of this lane in a coalesced pass, opaque to the compiler so that the offsets
 // of two passes are not shared (and kept live) between them.
