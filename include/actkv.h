@@ -200,6 +200,27 @@ actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
                         size_t workspace_bytes, void* stream);
 
 /*
+ * actkv_step for callers that cannot allocate: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, results and errors as actkv_step,
+ * but no workspace argument: the step's intermediates live in a static device array of
+ * ACTKV_NOALLOC_SCRATCH_BYTES bytes inside the library, of which every GPU the library runs
+ * on holds its own copy until the process ends.  Neither this call nor any kernel it
+ * launches allocates or frees memory.  A problem whose workspace (actkv_query) exceeds the
+ * array is refused with ACTKV_ERR_WORKSPACE_TOO_SMALL before anything else happens (the
+ * array holds the 32 x 35,000-token, 32/4-head, d = 128, 64-query batch); ACTKV_ERR_HIP if
+ * the array's device address cannot be looked up.  All calls on one GPU share that GPU's
+ * array, so calls that overlap in time on one GPU (concurrent streams, or several host
+ * threads) race: order them on one stream.  The array keeps the last call's contents; no
+ * part of it needs to start at zero.
+ */
+#define ACTKV_NOALLOC_SCRATCH_BYTES (64u << 20)
+actkv_status actkv_step_noalloc(const actkv_problem* p, const void* q, void* kv_cache,
+                                int32_t* block_table, const float* lse,
+                                const int32_t* free_pages, int64_t num_free, float* scores,
+                                float* pooled, int32_t* kept, int32_t* freed_pages,
+                                int32_t* new_lens, void* stream);
+
+/*
  * Eviction with attention-aware LRFU keep scores (Sec. 5.1 keep-score update; Alg. 1
  * steps 2-5) in place of plain TopK on the scores.  Per (request, KV head):
  *   att     = the max-pooled scores (pool_window; 1 = the scores), also written to `pooled`

@@ -63,6 +63,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.actkv_select.argtypes = [P, vp, vp, vp, vp, sz, vp]
     lib.actkv_compact.argtypes = [P, vp, vp, vp, vp, i64, vp, vp, vp, sz, vp]
     lib.actkv_step.argtypes = [P, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.actkv_step_noalloc.argtypes = [P, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp]
     f32 = ctypes.c_float
     lib.actkv_lrfu_select.argtypes = [P, vp, f32, f32, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_step_lrfu.argtypes = [P, vp, vp, vp, vp, vp, i64, f32, f32, vp, vp, vp, vp, vp,
@@ -77,7 +78,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.actkv_compact_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_step_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for f in ("actkv_query", "actkv_lse", "actkv_score", "actkv_select", "actkv_compact",
-              "actkv_step", "actkv_lrfu_select", "actkv_step_lrfu", "actkv_query_inplace",
+              "actkv_step", "actkv_step_noalloc", "actkv_lrfu_select", "actkv_step_lrfu", "actkv_query_inplace",
               "actkv_compact_inplace", "actkv_step_inplace", "actkv_score_accumulate",
               "actkv_token_confidence_workspace", "actkv_token_confidence",
               "actkv_budget_update"):
@@ -419,6 +420,31 @@ def step(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch
                                         _ws_bytes(ws), _stream(stream)))
     return dict(freed=freed[:z.freed], new_lens=new_lens, scores=scores,
                 pooled=pooled, kept=None if kept is None else kept[:z.kept])
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20   # ACTKV_NOALLOC_SCRATCH_BYTES
+
+
+def step_noalloc(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch.Tensor,
+                 free_pages: torch.Tensor, freed: torch.Tensor, new_lens: torch.Tensor,
+                 lse: Optional[torch.Tensor] = None, scores: Optional[torch.Tensor] = None,
+                 pooled: Optional[torch.Tensor] = None, kept: Optional[torch.Tensor] = None,
+                 stream=None, qy: Optional[dict] = None) -> dict:
+    """actkv_step with the library's static scratch array as its workspace: nothing is
+    allocated, here or in the library, so every output buffer comes from the caller."""
+    lib = load_library()
+    z = _Sizes(p, qy)
+    z.need("freed", freed, _I32, z.freed)
+    z.need("new_lens", new_lens, _I32, z.lens)
+    _step_args(z, q, kv_cache, block_table, free_pages, lse, scores, pooled, kept, freed,
+               new_lens, None)
+    c = p.cstruct()
+    _check("actkv_step_noalloc", lib.actkv_step_noalloc(
+        ctypes.byref(c), _ptr(q), _ptr(kv_cache), _ptr(block_table), _ptr(lse),
+        _ptr(free_pages), _numel(free_pages), _ptr(scores), _ptr(pooled), _ptr(kept),
+        _ptr(freed), _ptr(new_lens), _stream(stream)))
+    return dict(freed=freed[:z.freed], new_lens=new_lens, scores=scores, pooled=pooled,
+                kept=None if kept is None else kept[:z.kept])
 
 
 def compact_inplace(p: Problem, kv_cache: torch.Tensor, block_table: torch.Tensor,

@@ -19,7 +19,8 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libactkv.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "plan.hip", "score.hip", "select.hip", "compact.hip", "confidence.hip"]
+SOURCES = ["api.cpp", "plan.hip", "score.hip", "select.hip", "compact.hip", "confidence.hip",
+           "noalloc.hip"]
 HEADERS = ["actkv_internal.h", "device_common.hpp"]
 
 # Packed fp32 VALU forms are turned off for all device code; the host pass of hipcc warns

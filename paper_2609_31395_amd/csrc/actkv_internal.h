@@ -108,6 +108,14 @@ struct DevProblem {
   int64_t num_segments;
 };
 
+// The whole step (actkv_step) on a caller-chosen workspace: validation, planning and the
+// launches of every stage.  actkv_step_noalloc passes its static scratch array.
+actkv_status step_impl(const actkv_problem* p, const void* q, void* kv_cache,
+                       int32_t* block_table, const float* lse, const int32_t* free_pages,
+                       int64_t num_free, float* scores, float* pooled, int32_t* kept,
+                       int32_t* freed_pages, int32_t* new_lens, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
 // Kernel launchers (each returns the hipGetLastError() of its launches).
 hipError_t launch_plan(const DevProblem& dp, hipStream_t s);
 hipError_t launch_lse(const DevProblem& dp, const HostPlan& hp, const void* q, const void* kv,

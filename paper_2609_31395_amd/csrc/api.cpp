@@ -340,6 +340,19 @@ actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
                         int64_t num_free, float* scores, float* pooled, int32_t* kept,
                         int32_t* freed_pages, int32_t* new_lens, void* workspace,
                         size_t workspace_bytes, void* stream) {
+  return actkv::step_impl(p, q, kv_cache, block_table, lse, free_pages, num_free, scores, pooled,
+                          kept, freed_pages, new_lens, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+// The body of actkv_step, shared with actkv_step_noalloc (which passes its static scratch
+// array as the workspace).
+actkv_status actkv::step_impl(const actkv_problem* p, const void* q, void* kv_cache,
+                              int32_t* block_table, const float* lse, const int32_t* free_pages,
+                              int64_t num_free, float* scores, float* pooled, int32_t* kept,
+                              int32_t* freed_pages, int32_t* new_lens, void* workspace,
+                              size_t workspace_bytes, void* stream) {
   Ctx cx;
   actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
   if (st != ACTKV_OK) return st;
@@ -365,6 +378,8 @@ actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
   return hip_status(actkv::launch_compact(cx.dp, cx.hp, kv_cache, block_table, kept, free_pages,
                                           freed_pages, new_lens, s));
 }
+
+extern "C" {
 
 actkv_status actkv_query_inplace(const actkv_problem* p, int64_t* pages_freed) {
   HostPlan hp;

@@ -249,3 +249,24 @@ def test_confidence_entry_points_validate_before_launching():
     assert upd(upper=-1) == -1
     assert upd(off=np.array([0, 100, 50], np.int64)) == -1
     assert upd(off=np.array([0, 64 + 8 * 16384], np.int64)) == -2   # one window too many
+
+
+def test_noalloc_step_refuses_a_problem_past_its_scratch_array_on_the_host():
+    """The size check of actkv_step_noalloc runs on the host before any HIP call: a problem
+    needing more workspace than the static array is refused (ACTKV_ERR_WORKSPACE_TOO_SMALL)
+    with every data pointer NULL."""
+    import ctypes
+    R, H = 32, 4
+    p = actkv.Problem(seq_lens=[120_000] * R, q_lens=[64] * R, budgets=[30_000] * (R * H),
+                      num_q_heads=32, num_kv_heads=H, head_dim=128, num_pages=1 << 20,
+                      bt_stride=7500)
+    assert actkv.query(p)["workspace_bytes"] > actkv.NOALLOC_SCRATCH_BYTES
+    c = p.cstruct()
+    rc = actkv.load_library().actkv_step_noalloc(ctypes.byref(c), None, None, None, None, None,
+                                                 0, None, None, None, None, None, None)
+    assert rc == -3
+    bad = actkv.Problem(seq_lens=[10], q_lens=[11], budgets=[1], num_q_heads=1, num_kv_heads=1,
+                        head_dim=64, num_pages=4, bt_stride=1)   # causal query past the cache
+    c = bad.cstruct()
+    assert actkv.load_library().actkv_step_noalloc(ctypes.byref(c), None, None, None, None, None,
+                                                   0, None, None, None, None, None, None) == -1
