@@ -53,6 +53,11 @@ def parse():
     ap.add_argument("--cpu-sample-reqs", type=int, default=8,
                     help="requests of the workload the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-plan", action="store_true",
+                    help="time the CPU oracle on the whole timing plan (the tiny and single "
+                         "35K-token layers at 1 thread and all threads; the 32 x 35K batch, "
+                         "the ragged and adaptive batches in full; two layers of the 48-layer "
+                         "model) and print that record instead of the benchmark line")
     ap.add_argument("--headline-only", action="store_true",
                     help="time only the headline step and its stages (for profiling)")
     ap.add_argument("--no-table1", action="store_true",
@@ -121,6 +126,26 @@ def measure_copy_bw(dev, reps=10) -> float:
         b.record()
     torch.cuda.synchronize()
     return 2 * COPY_CALIB_BYTES / (_mean_ms(ev) * 1e-3)
+
+
+MALL_FLUSH_BYTES = 512 << 20   # twice the 256 MB MALL: touched between cold repetitions
+
+
+def percentiles(us):
+    """[p10, p90] of a list of microsecond timings."""
+    return [float(np.percentile(us, 10)), float(np.percentile(us, 90))]
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def log(msg: str) -> None:
@@ -517,15 +542,123 @@ def run_other_configs(reps, dev, stream):
             b.record(stream)
         torch.cuda.synchronize()
         ms = _mean_ms(ev)
+        us = [a.elapsed_time(b) * 1e3 for a, b in ev[1:]]
         tokens = int(dp.seq_lens.astype(np.int64).sum())
         out[name] = {"requests": dp.num_reqs, "cached_tokens": tokens,
                      "action_queries": int(dp.q_lens.sum()), "kept_entries": qy["num_kept"],
-                     "step_us": ms * 1e3, "tokens_per_s": tokens / (ms * 1e-3),
+                     "step_us": ms * 1e3, "step_us_p10_p90": percentiles(us),
+                     "tokens_per_s": tokens / (ms * 1e-3),
                      "hbm_roofline_frac": algorithmic_bytes(dp, qy["num_kept"])
                      / (HBM_PEAK_GBS * 1e9) / (ms * 1e-3)}
         del dp, ws, bt0, bt, free, lse
         torch.cuda.synchronize()
     return out
+
+
+def run_small_configs(reps, dev, stream):
+    """The tiny single-request layer (2,048 tokens, 8/2 heads, d = 64) and the single
+    35,000-token Qwen3-30B-shaped layer: the step (LSE supplied) per repetition, timed with
+    HIP events after the block table is restored and a 512 MB buffer is written, so that
+    the 256 MB MALL holds none of the layer (both layers fit in it otherwise); median,
+    p10 and p90.  The tiny layer is bound by kernel launches (its HBM roofline is 0.14 us)."""
+    import torch
+    from paper_2609_31395_amd import actkv
+    from paper_2609_31395_amd import workloads as W
+    out = {}
+    flush = torch.empty(MALL_FLUSH_BYTES, dtype=torch.uint8, device=dev)
+    for name in ("tiny", "single35k"):
+        dp = W.make_device_problem(name, device=dev)
+        bp = _binding(dp, dev)
+        qy = actkv.query(bp)
+        ws = torch.empty(qy["workspace_bytes"], dtype=torch.uint8, device=dev)
+        bt0 = torch.from_numpy(dp.block_table).to(dev)
+        bt = bt0.clone()
+        free = torch.from_numpy(dp.free_pages).to(dev)
+        lse = actkv.lse(bp, dp.q, dp.kv, bt0, ws=ws)
+        freed = torch.empty(max(qy["pages_freed"], 1), dtype=torch.int32, device=dev)
+        new_lens = torch.empty(bp.num_reqs * bp.num_kv_heads, dtype=torch.int32, device=dev)
+        ev = _event_pairs(reps + 1)
+        for i, (a, b) in enumerate(ev):
+            bt.copy_(bt0)
+            flush.fill_(i & 0xFF)
+            a.record(stream)
+            actkv.step(bp, dp.q, dp.kv, bt, free, lse=lse, freed=freed, new_lens=new_lens, ws=ws,
+                       qy=qy)
+            b.record(stream)
+        torch.cuda.synchronize()
+        us = [a.elapsed_time(b) * 1e3 for a, b in ev[1:]]
+        med = float(np.median(us))
+        tokens = int(dp.seq_lens.astype(np.int64).sum())
+        alg = algorithmic_bytes(dp, qy["num_kept"])
+        out[name] = {"requests": dp.num_reqs, "cached_tokens": tokens,
+                     "kept_entries": qy["num_kept"], "step_us_median": med,
+                     "step_us_p10_p90": percentiles(us), "tokens_per_s": tokens / (med * 1e-6),
+                     "algorithmic_bytes": alg,
+                     "hbm_roofline_frac": alg / (HBM_PEAK_GBS * 1e9) / (med * 1e-6),
+                     "mall": "flushed before every repetition"}
+        log(f"{name}: step {med:.1f} us (p10 {out[name]['step_us_p10_p90'][0]:.1f}, p90 "
+            f"{out[name]['step_us_p10_p90'][1]:.1f}), MALL flushed")
+        del dp, ws, bt0, bt, free, lse
+        torch.cuda.synchronize()
+    del flush
+    torch.cuda.empty_cache()
+    return out
+
+
+def _time_oracle_step(sample, threads=None):
+    """Seconds of one oracle step (all stages, fp64) on host arrays already in memory, at
+    `threads` OpenMP threads (None: all the host has)."""
+    import oracle
+    full = oracle.num_threads()
+    oracle.set_threads(threads or full)
+    try:
+        t1 = time.perf_counter()
+        oracle.step(sample)
+        return time.perf_counter() - t1, oracle.threads_in_use()
+    finally:
+        oracle.set_threads(full)
+
+
+def run_cpu_plan(dev):
+    """The CPU oracle's timing plan: the tiny and the single 35K-token layers at one thread
+    and at all threads; the 32 x 35K batch, the ragged batch and its Dirichlet-budget
+    variant in full at all threads; two layers of the 48-layer model, scaled by 24 to the
+    whole model.  Tokens per second per layer, with the CPU model and thread counts."""
+    from paper_2609_31395_amd import workloads as W
+    import torch
+    rows = []
+
+    def add(name, sample, threads, scale=1.0, note=""):
+        sec, used = _time_oracle_step(sample, threads)
+        tokens = int(sample.seq_lens.astype(np.int64).sum())
+        rows.append({"workload": name, "threads": used, "seconds": sec,
+                     "cached_tokens": tokens, "tokens_per_s": tokens / sec,
+                     "extrapolated_s": sec * scale if scale != 1.0 else None, "note": note})
+        log(f"cpu oracle {name} ({used} threads): {sec:.2f} s, {tokens / sec:.0f} tokens/s")
+
+    for name in ("tiny", "single35k"):
+        dp = W.make_device_problem(name, device=dev)
+        host = dp.host_subset(list(range(dp.num_reqs)))
+        del dp
+        add(name, host, 1)
+        add(name, host, None)
+    for name in ("batch32x35k", "batched", "adaptive"):
+        dp = W.make_device_problem(name, device=dev)
+        host = dp.host_subset(list(range(dp.num_reqs)))
+        del dp
+        torch.cuda.empty_cache()
+        add(name, host, None)
+        del host
+    layers = W.make_device_model("model48x32", device=dev, num_layers=2)
+    for li, dp in enumerate(layers):
+        host = dp.host_subset(list(range(dp.num_reqs)))
+        add(f"model48x32 layer {li}", host, None, scale=24.0,
+            note="x24: the 48-layer step from two sampled layers")
+        del host
+    del layers
+    torch.cuda.empty_cache()
+    import oracle
+    return {"cpu_model": cpu_model(), "host_threads": oracle.num_threads(), "rows": rows}
 
 
 def run_fullmodel(reps, dev, stream):
@@ -614,6 +747,10 @@ def main():
     if args.profile_stage == "copy":
         run_copy_calibration(args.steps)
         return
+    if args.cpu_plan:
+        actkv.load_library()
+        print(json.dumps({"cpu_plan": run_cpu_plan(torch.device("cuda:0"))}))
+        return
     if args.profile_stage == "fullmodel":
         actkv.load_library()
         fm = run_fullmodel(args.steps, torch.device("cuda:0"), torch.cuda.current_stream())
@@ -686,23 +823,41 @@ def main():
     ms_per_step = ev[0].elapsed_time(ev[K]) / K
     log(f"timed {K} steps: {ms_per_step * 1e3:.1f} us/step")
 
-    # ---- per-stage durations (same work, the three entry points called one by one, with
-    # events between them on the launch stream)
+    # ---- per-stage durations (same work: the plan once, then the three entry points with
+    # the plan flag, events between them on the launch stream)
     for b in bts:
         b.copy_(bt0)
     torch.cuda.synchronize()
-    se = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    pp = bp.planned()
+    se = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
     for i in range(K):
         se[i][0].record(stream)
-        actkv.score(bp, dp.q, dp.kv, bts[i], lse=lse, out=scores, ws=ws)
+        actkv.plan(bp, ws)
         se[i][1].record(stream)
-        actkv.select(bp, scores, pooled=pooled, kept=kept, ws=ws)
+        actkv.score(pp, dp.q, dp.kv, bts[i], lse=lse, out=scores, ws=ws)
         se[i][2].record(stream)
-        actkv.compact(bp, dp.kv, bts[i], kept, free, freed=freed, new_lens=new_lens, ws=ws)
+        actkv.select(pp, scores, pooled=pooled, kept=kept, ws=ws)
         se[i][3].record(stream)
+        actkv.compact(pp, dp.kv, bts[i], kept, free, freed=freed, new_lens=new_lens, ws=ws)
+        se[i][4].record(stream)
     torch.cuda.synchronize()
-    stage_ms = np.array([[se[i][j].elapsed_time(se[i][j + 1]) for j in range(3)]
+    stage_ms = np.array([[se[i][j].elapsed_time(se[i][j + 1]) for j in range(4)]
                          for i in range(K)]).mean(axis=0)
+
+    # ---- the scoring kernel alone: with the plan already in the workspace, actkv_score
+    # launches score_kernel and nothing else (one row chunk per request here), so the events
+    # around it time that kernel's launches back to back
+    actkv.plan(bp, ws)
+    for _ in range(2):
+        actkv.score(pp, dp.q, dp.kv, bt0, lse=lse, out=scores, ws=ws)
+    ek = _event_pairs(K)
+    for a, b in ek:
+        a.record(stream)
+        actkv.score(pp, dp.q, dp.kv, bt0, lse=lse, out=scores, ws=ws)
+        b.record(stream)
+    torch.cuda.synchronize()
+    score_kernel_us = [a.elapsed_time(b) * 1e3 for a, b in ek]
+    log(f"score_kernel alone: {np.mean(score_kernel_us):.1f} us")
 
     # ---- the step with the LSE pass included (library computes the normaliser)
     for b in bts:
@@ -717,8 +872,8 @@ def main():
     el[1].record(stream)
     torch.cuda.synchronize()
     ms_with_lse = el[0].elapsed_time(el[1]) / K
-    log(f"stages (us) {np.round(stage_ms * 1e3, 1).tolist()}, step with LSE pass "
-        f"{ms_with_lse * 1e3:.1f} us")
+    log(f"stages plan/score/select/compact (us) {np.round(stage_ms * 1e3, 1).tolist()}, step "
+        f"with LSE pass {ms_with_lse * 1e3:.1f} us")
 
     sum_L = int(dp.seq_lens.astype(np.int64).sum())
     extra = not args.headline_only
@@ -735,7 +890,7 @@ def main():
     t_hbm = alg_bytes / (HBM_PEAK_GBS * 1e9)
     t_mfma = flops / (BF16_PEAK_TFLOPS * 1e12)
     t_valu = score_epilogue_slots(dp) / VALU_SLOTS_PER_S
-    score_s = stage_ms[0] * 1e-3
+    score_s = float(np.mean(score_kernel_us)) * 1e-6
     achieved_tflops = flops / score_s / 1e12
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
@@ -744,7 +899,7 @@ def main():
         if tr.get("source_sha256") == source_digest() and tr.get("workload") == args.workload:
             traffic = int(tr["hbm_bytes_per_launch"])
 
-    streaming = confidence = table1 = fullmodel = others = None
+    streaming = confidence = table1 = fullmodel = others = small = None
     if extra:
         streaming = _leg("streaming", run_streaming_batch, dp, bp, K, dev, stream)
         if streaming:
@@ -759,6 +914,7 @@ def main():
         table1 = (_leg("table1", run_table1, max(K // 2, 5), dev, stream)
                   if not args.no_table1 else None)
         others = _leg("other_configs", run_other_configs, K, dev, stream)
+        small = _leg("small_configs", run_small_configs, K, dev, stream)
         for nm, o in (others or {}).items():
             log(f"{nm}: step {o['step_us']:.1f} us, {o['tokens_per_s'] / 1e9:.3f} G tokens/s, "
                 f"{o['hbm_roofline_frac']:.2f} of its HBM roofline")
@@ -777,18 +933,29 @@ def main():
                    f"{gr['compress_fresh_us']:6.1f} us" if gr else ""))
 
     def cpu_leg():
-        import oracle
         reqs = list(range(min(args.cpu_sample_reqs, dp.num_reqs)))
         sample = dp.host_subset(reqs)
-        log(f"timing the CPU oracle on {len(reqs)} requests ({oracle.num_threads()} threads)")
-        t1 = time.perf_counter()
-        oracle.step(sample)   # the oracle's own full step (it derives the LSE itself)
-        cpu_s = time.perf_counter() - t1
+        log(f"timing the CPU oracle on {len(reqs)} requests")
+        # the oracle's own full step (it derives the LSE itself), all host threads
+        cpu_s, used = _time_oracle_step(sample)
         s_tokens = int(sample.seq_lens.astype(np.int64).sum())
-        return {"value": s_tokens / cpu_s, "unit": "tokens/s", "cores": oracle.num_threads(),
-                "kind": "oracle",
+        small = {}
+        for name in ("tiny", "single35k"):
+            sp = W.make_device_problem(name, device=dev)
+            host = sp.host_subset(list(range(sp.num_reqs)))
+            del sp
+            t_one, _ = _time_oracle_step(host, 1)
+            t_all, n_all = _time_oracle_step(host)
+            small[name] = {"seconds_1_thread": t_one, "seconds_all_threads": t_all,
+                           "threads": n_all}
+            log(f"cpu oracle {name}: {t_one * 1e3:.1f} ms at 1 thread, {t_all * 1e3:.1f} ms at "
+                f"{n_all}")
+        return {"value": s_tokens / cpu_s, "unit": "tokens/s", "cores": used,
+                "kind": "oracle", "cpu_model": cpu_model(),
                 "sample": f"{len(reqs)} of {dp.num_reqs} requests of {args.workload} "
-                          f"({s_tokens} cached tokens, all stages, fp64), {cpu_s:.1f} s"}
+                          f"({s_tokens} cached tokens, all stages, fp64), {cpu_s:.1f} s at "
+                          f"{used} threads",
+                "single_layers": small}
 
     cpu = None
     if not args.no_cpu_baseline and args.cpu_sample_reqs > 0:
@@ -833,18 +1000,22 @@ def main():
                               "t_valu_us": t_valu * 1e6,
                               "bound_us": max(t_hbm, t_mfma, t_valu) * 1e6,
                               "frac": max(t_hbm, t_mfma, t_valu) / (ms_per_step * 1e-3)},
-        "stages_us": {"score": stage_ms[0] * 1e3, "select": stage_ms[1] * 1e3,
-                      "compact": stage_ms[2] * 1e3},
+        "stages_us": {"plan": stage_ms[0] * 1e3, "score": stage_ms[1] * 1e3,
+                      "select": stage_ms[2] * 1e3, "compact": stage_ms[3] * 1e3},
+        "score_kernel_us": {"mean": float(np.mean(score_kernel_us)),
+                            "p10_p90": percentiles(score_kernel_us)},
         "step_with_lse_pass_us": ms_with_lse * 1e3,
         "inplace": inplace,
         "streaming": streaming,
         "confidence": confidence,
         "table1": table1,
         "other_configs": others,
+        "small_configs": small,
         "fullmodel": fullmodel,
         "lrfu": lrfu,
         "roofline": {
-            "kernel": "score_kernel (actkv_score, LSE supplied)",
+            "kernel": "score_kernel (actkv_score with the plan flag: that kernel alone, LSE "
+                      "supplied)",
             "bound": "mfma",
             "achieved": achieved_tflops,
             "peak": BF16_PEAK_TFLOPS,

@@ -98,7 +98,19 @@ typedef struct actkv_problem {
                                1 = no pooling                                            */
   int32_t causal;           /* 1: causal visibility (see conventions), 0: all keys       */
   int32_t agg;              /* actkv_agg                                                 */
+  uint32_t flags;           /* ACTKV_FLAG_*; 0 for the default behaviour                 */
 } actkv_problem;
+
+/*
+ * ACTKV_FLAG_PLANNED: the workspace already holds this problem's per-request plan (the
+ * offsets, page counts and scoring split every kernel reads), written by actkv_plan or by
+ * any earlier call on the same problem and the same workspace; the call then does not plan
+ * again.  Lets a caller that composes the stages (actkv_score, actkv_select, actkv_compact,
+ * ...) plan once per step.  The plan carries a signature of the problem (its sizes and its
+ * lengths, query counts and budgets); a kernel that finds a plan of another problem in the
+ * workspace returns at once, so a wrong flag leaves the outputs unwritten, never a fault.
+ */
+#define ACTKV_FLAG_PLANNED 1u
 
 /*
  * Host-only planning (the per-request counts of Alg. 4, steps 1-5: Y = ceil(L_r /
@@ -114,6 +126,16 @@ typedef struct actkv_problem {
  */
 actkv_status actkv_query(const actkv_problem* p, size_t* workspace_bytes, int64_t* num_kept,
                          int64_t* fresh_pages_needed, int64_t* pages_freed);
+
+/*
+ * Writes the problem's plan into the workspace (the per-request counts and offsets of Alg. 4
+ * steps 1-5 -- blocks in use, blocks kept, where each request's scores, kept entries, fresh
+ * and freed pages start -- and the split of the scoring over the workgroups), for later
+ * calls that pass ACTKV_FLAG_PLANNED.  Every other launching entry point plans by itself
+ * unless that flag is set.  Errors as for every entry point.
+ */
+actkv_status actkv_plan(const actkv_problem* p, void* workspace, size_t workspace_bytes,
+                        void* stream);
 
 /*
  * Log-sum-exp of every action-query row (Sec. 7.1: LSE = log sum_j exp(s_ij) over the

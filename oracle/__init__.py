@@ -82,6 +82,8 @@ def _load():
                                                    ctypes.c_double, ctypes.c_int32, vp, vp, vp,
                                                    vp, vp]
         lib.actkv_oracle_lrfu_update.argtypes = [P, vp, vp, ctypes.c_float, vp]
+        lib.actkv_oracle_get_threads.restype = ctypes.c_int
+        lib.actkv_oracle_set_threads.argtypes = [ctypes.c_int]
         for f in ("actkv_oracle_lse", "actkv_oracle_scores", "actkv_oracle_pool",
                   "actkv_oracle_select", "actkv_oracle_totals", "actkv_oracle_compact",
                   "actkv_oracle_hits", "actkv_oracle_lrfu_update"):
@@ -359,6 +361,16 @@ def budget_update(conf_seqs, budgets, window: int = 64, stride: int = 8,
         b_in.ctypes.data, b_out.ctypes.data, slopes.ctypes.data, thr.ctypes.data,
         kept.ctypes.data), "budget_update")
     return dict(budgets=b_out[:R], slopes=slopes[:R], thresholds=thr[:R], retained=kept[:R])
+
+
+def set_threads(n: int) -> None:
+    """Threads the oracle's parallel loops use from now on (timing only)."""
+    _load().actkv_oracle_set_threads(int(n))
+
+
+def threads_in_use() -> int:
+    """Threads the oracle's parallel loops use now (OpenMP's own count)."""
+    return int(_load().actkv_oracle_get_threads())
 
 
 def num_threads() -> int:

@@ -537,3 +537,10 @@ int actkv_oracle_lrfu_update(const oracle_problem* p, const float* att, const ui
   }
   return 0;
 }
+
+/* Timing support (not part of what the oracle computes): the OpenMP thread count the
+ * parallel loops above use, and setting it (the benchmark times the oracle at one thread
+ * and at all host threads). */
+#include <omp.h>
+int actkv_oracle_get_threads(void) { return omp_get_max_threads(); }
+void actkv_oracle_set_threads(int n) { if (n > 0) omp_set_num_threads(n); }

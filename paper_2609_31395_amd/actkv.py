@@ -40,7 +40,10 @@ class CProblem(ctypes.Structure):
                 ("budgets_h", ctypes.c_void_p), ("seq_lens_d", ctypes.c_void_p),
                 ("q_lens_d", ctypes.c_void_p), ("budgets_d", ctypes.c_void_p),
                 ("sm_scale", ctypes.c_float), ("pool_window", ctypes.c_int32),
-                ("causal", ctypes.c_int32), ("agg", ctypes.c_int32)]
+                ("causal", ctypes.c_int32), ("agg", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+
+
+FLAG_PLANNED = 1   # ACTKV_FLAG_PLANNED: the workspace already holds this problem's plan
 
 
 _lib = None
@@ -58,6 +61,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     vp, i64, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
     lib.actkv_query.argtypes = [P, ctypes.POINTER(sz), ctypes.POINTER(i64), ctypes.POINTER(i64),
                                 ctypes.POINTER(i64)]
+    lib.actkv_plan.argtypes = [P, vp, sz, vp]
     lib.actkv_lse.argtypes = [P, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_score.argtypes = [P, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_select.argtypes = [P, vp, vp, vp, vp, sz, vp]
@@ -77,7 +81,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.actkv_query_inplace.argtypes = [P, ctypes.POINTER(i64)]
     lib.actkv_compact_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_step_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
-    for f in ("actkv_query", "actkv_lse", "actkv_score", "actkv_select", "actkv_compact",
+    for f in ("actkv_query", "actkv_plan", "actkv_lse", "actkv_score", "actkv_select", "actkv_compact",
               "actkv_step", "actkv_step_noalloc", "actkv_lrfu_select", "actkv_step_lrfu", "actkv_query_inplace",
               "actkv_compact_inplace", "actkv_step_inplace", "actkv_score_accumulate",
               "actkv_token_confidence_workspace", "actkv_token_confidence",
@@ -108,6 +112,7 @@ class Problem:
     q_lens_d: Optional[torch.Tensor] = None
     budgets_d: Optional[torch.Tensor] = None
     page_size: int = PAGE_SIZE
+    flags: int = 0
 
     def __post_init__(self):
         self.seq_lens = np.ascontiguousarray(self.seq_lens, dtype=np.int32).reshape(-1)
@@ -124,7 +129,32 @@ class Problem:
     def num_reqs(self) -> int:
         return int(self.seq_lens.shape[0])
 
+    def _key(self):
+        """Everything the C view of the problem and its planning depend on (the host arrays'
+        contents, the scalars, the device mirrors' addresses)."""
+        def dptr(t):
+            return None if t is None else t.data_ptr()
+        return (self.seq_lens.tobytes(), self.q_lens.tobytes(), self.budgets.tobytes(),
+                self.num_q_heads, self.num_kv_heads, self.head_dim, self.num_pages,
+                self.bt_stride, self.sm_scale, self.pool_window, self.causal, self.agg,
+                self.page_size, self.flags, dptr(self.seq_lens_d), dptr(self.q_lens_d),
+                dptr(self.budgets_d))
+
+    def _cached(self):
+        """(key, C struct, query result, sizes) of the problem as it is now; rebuilt when any
+        of its inputs changed since the last call."""
+        key = self._key()
+        c = self.__dict__.get("_cache")
+        if c is None or c[0] != key:
+            struct = self._make_cstruct()
+            c = (key, struct, None, None)
+            self.__dict__["_cache"] = c
+        return c
+
     def cstruct(self) -> CProblem:
+        return self._cached()[1]
+
+    def _make_cstruct(self) -> CProblem:
         def dptr(t):
             return None if t is None else t.data_ptr()
         return CProblem(
@@ -135,7 +165,13 @@ class Problem:
             budgets_h=self.budgets.ctypes.data, seq_lens_d=dptr(self.seq_lens_d),
             q_lens_d=dptr(self.q_lens_d), budgets_d=dptr(self.budgets_d),
             sm_scale=float(self.sm_scale), pool_window=int(self.pool_window),
-            causal=int(bool(self.causal)), agg=AGG[self.agg])
+            causal=int(bool(self.causal)), agg=AGG[self.agg], flags=int(self.flags))
+
+    def planned(self) -> "Problem":
+        """The same problem with ACTKV_FLAG_PLANNED: calls skip the plan kernel and use the
+        plan already in the workspace (from plan() or an earlier call on this problem)."""
+        import dataclasses
+        return dataclasses.replace(self, flags=self.flags | FLAG_PLANNED)
 
 
 def _check(fn: str, code: int):
@@ -185,35 +221,38 @@ def _on_gpu(named) -> None:
     """Every tensor resident on the same GPU."""
     first = None
     for name, t in named:
-        if t.device.type != "cuda":
+        if not t.is_cuda:
             raise ValueError(f"{name} must be on the GPU, got {t.device}")
         if first is None:
-            first = (name, t.device)
-        elif t.device != first[1]:
-            raise ValueError(f"{name} is on {t.device}, {first[0]} on {first[1]}")
+            first = (name, t.get_device())
+        elif t.get_device() != first[1]:
+            raise ValueError(f"{name} is on cuda:{t.get_device()}, {first[0]} on cuda:{first[1]}")
 
 
 class _Sizes:
     """Element counts of every array an entry point reads or writes, from the problem and
-    the host-only planning query."""
+    its host-only planning query (both cached on the problem while it is unchanged; a qy
+    the caller passes is not trusted for sizes)."""
 
     def __init__(self, p: Problem, qy: Optional[dict] = None):
-        qy = query(p) if qy is None else qy
-        R, Hkv = p.num_reqs, p.num_kv_heads
+        qy = query(p)
+        cache = p._cached()
+        st = cache[3]
+        if st is None:
+            R, Hkv = p.num_reqs, p.num_kv_heads
+            sum_n = int(p.q_lens.astype(np.int64).sum())
+            st = dict(sum_n=sum_n, q=sum_n * p.num_q_heads * p.head_dim,
+                      lse=sum_n * p.num_q_heads,
+                      kv=2 * int(p.num_pages) * p.page_size * Hkv * p.head_dim,
+                      bt=R * int(p.bt_stride), scores=num_scores(p), kept=int(qy["num_kept"]),
+                      freed=int(qy["pages_freed"]), fresh=int(qy["fresh_pages_needed"]),
+                      lens=R * Hkv, ws=int(qy["workspace_bytes"]))
+            p.__dict__["_cache"] = (cache[0], cache[1], cache[2], st)
         self.qy = qy
-        self.sum_n = int(p.q_lens.astype(np.int64).sum())
-        self.q = self.sum_n * p.num_q_heads * p.head_dim
-        self.lse = self.sum_n * p.num_q_heads
-        self.kv = 2 * int(p.num_pages) * p.page_size * Hkv * p.head_dim
-        self.bt = R * int(p.bt_stride)
-        self.scores = num_scores(p)
-        self.kept = int(qy["num_kept"])
-        self.freed = int(qy["pages_freed"])
-        self.fresh = int(qy["fresh_pages_needed"])
-        self.lens = R * Hkv
-        self.ws = int(qy["workspace_bytes"])
+        self.__dict__.update(st)
         self.seen: list = []
         self.mirrors = []
+        R, Hkv = p.num_reqs, p.num_kv_heads
         if R > 0:
             for name, t, n in (("seq_lens_d", p.seq_lens_d, R), ("q_lens_d", p.q_lens_d, R),
                                ("budgets_d", p.budgets_d, R * Hkv)):
@@ -247,13 +286,18 @@ def _ws_bytes(ws: torch.Tensor) -> int:
 
 def query(p: Problem) -> dict:
     """Host-only: workspace bytes, kept entries, fresh pages needed, pages freed."""
+    cache = p._cached()
+    if cache[2] is not None:
+        return dict(cache[2])
     lib = load_library()
-    c = p.cstruct()
+    c = cache[1]
     ws, nk, fresh, freed = ctypes.c_size_t(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     _check("actkv_query", lib.actkv_query(ctypes.byref(c), ctypes.byref(ws), ctypes.byref(nk),
                                           ctypes.byref(fresh), ctypes.byref(freed)))
-    return dict(workspace_bytes=ws.value, num_kept=nk.value, fresh_pages_needed=fresh.value,
-                pages_freed=freed.value)
+    out = dict(workspace_bytes=ws.value, num_kept=nk.value, fresh_pages_needed=fresh.value,
+               pages_freed=freed.value)
+    p.__dict__["_cache"] = (cache[0], c, out, cache[3])
+    return dict(out)
 
 
 def query_inplace(p: Problem) -> int:
@@ -271,6 +315,19 @@ def num_scores(p: Problem) -> int:
 
 def workspace(p: Problem, device="cuda") -> torch.Tensor:
     return torch.empty(max(query(p)["workspace_bytes"], 1), dtype=torch.uint8, device=device)
+
+
+def plan(p: Problem, ws: torch.Tensor, stream=None) -> torch.Tensor:
+    """Writes p's plan into ws (for later calls with p.planned())."""
+    lib = load_library()
+    z = _Sizes(p)
+    z.need("ws", ws, None, 0)
+    if _ws_bytes(ws) < z.ws:
+        raise ValueError(f"ws holds {_ws_bytes(ws)} bytes, the call needs {z.ws}")
+    _on_gpu(z.seen + z.mirrors)
+    c = p.cstruct()
+    _check("actkv_plan", lib.actkv_plan(ctypes.byref(c), _ptr(ws), _ws_bytes(ws), _stream(stream)))
+    return ws
 
 
 def lse(p: Problem, q: torch.Tensor, kv_cache: torch.Tensor, block_table: torch.Tensor,

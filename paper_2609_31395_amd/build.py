@@ -26,6 +26,11 @@ HEADERS = ["actkv_internal.h", "device_common.hpp"]
 # Packed fp32 VALU forms are turned off for all device code; the host pass of hipcc warns
 # that it does not know the feature, which is harmless.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Per-source device flags.  The scoring kernel keeps its MFMA accumulators in ordinary
+# VGPRs (its epilogue reads every accumulator element with VALU instructions, which cannot
+# take AGPR operands); left to its heuristics the compiler put them in AGPRs and copied each
+# element out, one extra VALU instruction per element.
+SOURCE_FLAGS = {"score.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def hipcc() -> str:
@@ -40,7 +45,7 @@ def _compile(src: str) -> str:
     cmd = [hipcc(), "-c", "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
            "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-function"]
     if src.endswith(".hip"):
-        cmd += ["-x", "hip"] + DEVICE_FLAGS
+        cmd += ["-x", "hip"] + DEVICE_FLAGS + SOURCE_FLAGS.get(src, [])
     cmd += [os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     msgs = "\n".join(l for l in (r.stdout + r.stderr).splitlines()

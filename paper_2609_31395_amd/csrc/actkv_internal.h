@@ -54,6 +54,7 @@ struct HostPlan {
 
 // Byte offsets of the workspace regions (each 256-byte aligned).
 struct WsLayout {
+  size_t sig = 0;          // uint64: signature of the problem whose plan the workspace holds
   size_t plan = 0;         // ReqPlan[R]
   size_t kept_off = 0;     // int64[R * Hkv + 1]
   size_t seg_cost = 0;     // int64[num_segments + 1]
@@ -74,6 +75,7 @@ inline WsLayout ws_layout(const HostPlan& hp) {
   WsLayout w;
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t at = o; o = align256(o + bytes); return at; };
+  w.sig = take(sizeof(uint64_t));
   w.plan = take(sizeof(ReqPlan) * (size_t)(hp.R > 0 ? hp.R : 1));
   w.kept_off = take(sizeof(int64_t) * (size_t)(hp.R * hp.Hkv + 1));
   w.seg_cost = take(sizeof(int64_t) * (size_t)(hp.num_segments + 1));
@@ -106,7 +108,10 @@ struct DevProblem {
   int64_t* kept_off;       // workspace [R*Hkv + 1]
   int64_t* seg_cost;       // workspace [num_segments + 1]
   int64_t num_segments;
+  uint64_t sig;            // signature of this problem (host-computed)
+  uint64_t* plan_sig;      // workspace: signature of the problem the plan was written for
 };
+
 
 // The whole step (actkv_step) on a caller-chosen workspace: validation, planning and the
 // launches of every stage.  actkv_step_noalloc passes its static scratch array.

@@ -25,6 +25,7 @@ actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
   if (p->causal != 0 && p->causal != 1) return ACTKV_ERR_INVALID_ARGUMENT;
   if (p->agg != ACTKV_AGG_SUM && p->agg != ACTKV_AGG_MAX_MEAN) return ACTKV_ERR_INVALID_ARGUMENT;
   if (!isfinite(p->sm_scale) || p->sm_scale < 0.f) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (p->flags & ~ACTKV_FLAG_PLANNED) return ACTKV_ERR_INVALID_ARGUMENT;
   if (p->head_dim != 64 && p->head_dim != 128) return ACTKV_ERR_UNSUPPORTED;
   if (p->page_size != actkv::kPageSize) return ACTKV_ERR_UNSUPPORTED;
   if (p->num_kv_heads > 64) return ACTKV_ERR_UNSUPPORTED;
@@ -89,6 +90,30 @@ actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
   return ACTKV_OK;
 }
 
+// 64-bit FNV-1a over the problem's sizes and its host arrays: the signature a plan in the
+// workspace carries (see ACTKV_FLAG_PLANNED).
+struct Fnv {
+  uint64_t h = 1469598103934665603ull;
+  void add(const void* p, size_t n) {
+    const unsigned char* b = static_cast<const unsigned char*>(p);
+    for (size_t i = 0; i < n; ++i) h = (h ^ b[i]) * 1099511628211ull;
+  }
+  template <typename T> void add(T v) { add(&v, sizeof v); }
+};
+
+uint64_t problem_signature(const actkv_problem* p) {
+  Fnv f;
+  f.add(p->num_reqs); f.add(p->num_q_heads); f.add(p->num_kv_heads); f.add(p->head_dim);
+  f.add(p->page_size); f.add(p->num_pages); f.add(p->bt_stride); f.add(p->pool_window);
+  f.add(p->causal); f.add(p->agg);
+  if (p->num_reqs > 0) {
+    f.add(p->seq_lens_h, sizeof(int32_t) * (size_t)p->num_reqs);
+    f.add(p->q_lens_h, sizeof(int32_t) * (size_t)p->num_reqs);
+    f.add(p->budgets_h, sizeof(int32_t) * (size_t)p->num_reqs * (size_t)p->num_kv_heads);
+  }
+  return f.h | 1ull;   // never 0, so a zeroed workspace holds no plan
+}
+
 struct Ctx {
   HostPlan hp;
   WsLayout ws;
@@ -127,10 +152,19 @@ actkv_status prepare(const actkv_problem* p, void* workspace, size_t workspace_b
   d.kept_off = reinterpret_cast<int64_t*>(cx->base + cx->ws.kept_off);
   d.seg_cost = reinterpret_cast<int64_t*>(cx->base + cx->ws.seg_cost);
   d.num_segments = cx->hp.num_segments;
+  d.sig = problem_signature(p);
+  d.plan_sig = reinterpret_cast<uint64_t*>(cx->base + cx->ws.sig);
   return ACTKV_OK;
 }
 
+
 actkv_status hip_status(hipError_t e) { return e == hipSuccess ? ACTKV_OK : ACTKV_ERR_HIP; }
+
+// The plan kernel, unless the caller says the workspace already holds this problem's plan.
+actkv_status plan_step(const Ctx& cx, const actkv_problem* p, hipStream_t s) {
+  if (p->flags & ACTKV_FLAG_PLANNED) return ACTKV_OK;
+  return hip_status(actkv::launch_plan(cx.dp, s));
+}
 
 actkv_status run_lse(const Ctx& cx, const void* q, const void* kv, const int32_t* bt,
                      float* lse_out, hipStream_t s) {
@@ -166,6 +200,15 @@ actkv_status actkv_query(const actkv_problem* p, size_t* workspace_bytes, int64_
   return ACTKV_OK;
 }
 
+actkv_status actkv_plan(const actkv_problem* p, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+  Ctx cx;
+  actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
+  if (st != ACTKV_OK) return st;
+  if (cx.hp.R == 0) return ACTKV_OK;
+  return hip_status(actkv::launch_plan(cx.dp, static_cast<hipStream_t>(stream)));
+}
+
 actkv_status actkv_lse(const actkv_problem* p, const void* q, const void* kv_cache,
                        const int32_t* block_table, float* lse_out, void* workspace,
                        size_t workspace_bytes, void* stream) {
@@ -176,7 +219,7 @@ actkv_status actkv_lse(const actkv_problem* p, const void* q, const void* kv_cac
     return ACTKV_ERR_INVALID_ARGUMENT;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (cx.hp.R == 0) return ACTKV_OK;
-  st = hip_status(actkv::launch_plan(cx.dp, s));
+  st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
   return run_lse(cx, q, kv_cache, block_table, lse_out, s);
 }
@@ -191,7 +234,7 @@ actkv_status actkv_score(const actkv_problem* p, const void* q, const void* kv_c
   if (cx.hp.sum_n > 0 && !q) return ACTKV_ERR_INVALID_ARGUMENT;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (cx.hp.R == 0) return ACTKV_OK;
-  st = hip_status(actkv::launch_plan(cx.dp, s));
+  st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
   return run_score(cx, q, kv_cache, block_table, lse, scores, s);
 }
@@ -207,7 +250,7 @@ actkv_status actkv_score_accumulate(const actkv_problem* p, const void* q, const
   if (acc && (reinterpret_cast<uintptr_t>(acc) & 15)) return ACTKV_ERR_INVALID_ARGUMENT;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (cx.hp.R == 0 || cx.hp.num_scores == 0) return ACTKV_OK;
-  st = hip_status(actkv::launch_plan(cx.dp, s));
+  st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
   if (cx.hp.max_n <= 1 && cx.hp.G <= actkv::kDecodeMaxGroup) {
     // a decode step (one action query per request at most): scored and added in one pass
@@ -239,7 +282,7 @@ actkv_status actkv_select(const actkv_problem* p, const float* scores, float* po
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (cx.hp.R == 0) return ACTKV_OK;
   if (!pooled) pooled = reinterpret_cast<float*>(cx.base + cx.ws.pooled);
-  st = hip_status(actkv::launch_plan(cx.dp, s));
+  st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
   return hip_status(actkv::launch_select(cx.dp, cx.hp, scores, pooled, kept, s));
 }
@@ -259,7 +302,7 @@ actkv_status actkv_compact(const actkv_problem* p, void* kv_cache, int32_t* bloc
   if (cx.hp.fresh_needed > 0 && !free_pages) return ACTKV_ERR_INVALID_ARGUMENT;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (cx.hp.R == 0) return ACTKV_OK;
-  st = hip_status(actkv::launch_plan(cx.dp, s));
+  st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
   return hip_status(actkv::launch_compact(cx.dp, cx.hp, kv_cache, block_table, kept, free_pages,
                                           freed_pages, new_lens, s));
@@ -294,7 +337,7 @@ actkv_status actkv_lrfu_select(const actkv_problem* p, const float* scores, floa
   if (st != ACTKV_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (cx.hp.R == 0) return ACTKV_OK;
-  st = hip_status(actkv::launch_plan(cx.dp, s));
+  st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
   return hip_status(actkv::launch_lrfu_select(cx.dp, cx.hp, scores, top_p, decay, ks, hit,
                                               pooled, kept, ks_kept, s));
@@ -324,7 +367,7 @@ actkv_status actkv_step_lrfu(const actkv_problem* p, const void* q, void* kv_cac
   if (st != ACTKV_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (cx.hp.R == 0) return ACTKV_OK;
-  st = hip_status(actkv::launch_plan(cx.dp, s));
+  st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
   st = run_score(cx, q, kv_cache, block_table, lse, scores, s);
   if (st != ACTKV_OK) return st;
@@ -369,7 +412,7 @@ actkv_status actkv::step_impl(const actkv_problem* p, const void* q, void* kv_ca
   if (!scores) scores = reinterpret_cast<float*>(cx.base + cx.ws.scores);
   if (!pooled) pooled = reinterpret_cast<float*>(cx.base + cx.ws.pooled);
   if (!kept) kept = reinterpret_cast<int32_t*>(cx.base + cx.ws.kept);
-  st = hip_status(actkv::launch_plan(cx.dp, s));
+  st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
   st = run_score(cx, q, kv_cache, block_table, lse, scores, s);
   if (st != ACTKV_OK) return st;
@@ -421,7 +464,7 @@ actkv_status actkv_compact_inplace(const actkv_problem* p, void* kv_cache, int32
   if (cx.hp.num_kept > 0 && !kept) return ACTKV_ERR_INVALID_ARGUMENT;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (cx.hp.R == 0) return ACTKV_OK;
-  st = hip_status(actkv::launch_plan(cx.dp, s));
+  st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
   return run_compact_inplace(cx, kv_cache, block_table, kept, freed_pages, new_lens, new_order,
                              s);
@@ -445,7 +488,7 @@ actkv_status actkv_step_inplace(const actkv_problem* p, const void* q, void* kv_
   if (!scores) scores = reinterpret_cast<float*>(cx.base + cx.ws.scores);
   if (!pooled) pooled = reinterpret_cast<float*>(cx.base + cx.ws.pooled);
   if (!kept) kept = reinterpret_cast<int32_t*>(cx.base + cx.ws.kept);
-  st = hip_status(actkv::launch_plan(cx.dp, s));
+  st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
   st = run_score(cx, q, kv_cache, block_table, lse, scores, s);
   if (st != ACTKV_OK) return st;

@@ -33,6 +33,7 @@ template <int D, bool kInPlace>
 __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
     DevProblem dp, uint16_t* kv, const int32_t* __restrict__ bt, const int32_t* __restrict__ kept,
     const int32_t* __restrict__ free_pages, int64_t num_fresh) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   constexpr int CH = D / 8;                 // 16-byte chunks per row
   __shared__ int64_t src_slot[kCompactTable];   // flat source slot, -1: nothing to copy
   __shared__ int64_t dst_page[kCompactTable / kPageSize];
@@ -132,6 +133,7 @@ __global__ __launch_bounds__(256) void compact_rewrite_kernel(DevProblem dp, int
                                                               const int32_t* __restrict__ free_pages,
                                                               int32_t* __restrict__ freed,
                                                               int32_t* __restrict__ new_lens) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   const int r = blockIdx.x, Hkv = dp.Hkv;
   const ReqPlan pl = dp.plan[r];
   for (int h = threadIdx.x; h < Hkv; h += 256) {
@@ -198,6 +200,7 @@ constexpr int kIpBitmapSlots = 32 * kIpPlanThreads;   // region slots per bitmap
 
 __global__ __launch_bounds__(kIpPlanThreads) void inplace_plan_kernel(
     DevProblem dp, const int32_t* __restrict__ kept, int32_t* src_rank, int32_t* new_order) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   __shared__ uint32_t bits[kIpBitmapSlots / 32];
   __shared__ int64_t scan_tmp[17];
   const int seg = blockIdx.x, tid = threadIdx.x, Hkv = dp.Hkv;
@@ -262,6 +265,7 @@ __global__ __launch_bounds__(kIpPlanThreads) void inplace_plan_kernel(
 __global__ __launch_bounds__(256) void inplace_rewrite_kernel(DevProblem dp, int32_t* bt,
                                                               int32_t* __restrict__ freed,
                                                               int32_t* __restrict__ new_lens) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   const int r = blockIdx.x, Hkv = dp.Hkv, tid = threadIdx.x;
   const ReqPlan pl = dp.plan[r];
   for (int h = tid; h < Hkv; h += 256) {

@@ -35,6 +35,14 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// True when the workspace holds this problem's plan.  Every kernel that reads the plan
+// checks this first and returns at once (the whole workgroup) when it does not hold: a
+// caller that claims a plan it does not have gets no output, never an access outside its
+// buffers.
+__device__ __forceinline__ bool plan_ok(const DevProblem& dp) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(*dp.plan_sig == dp.sig)) != 0u;
+}
+
 // Word 3 of a raw (stride 0) buffer resource on CDNA: 32-bit data format; reads at byte
 // offsets at or past num_records return 0 and writes there are dropped.
 constexpr int kBufferRsrcWord3 = 0x00020000;

@@ -130,6 +130,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
   if (threadIdx.x == 0) {
     dp.kept_off[(int64_t)R * Hkv] = carry_k;
     dp.seg_cost[dp.num_segments] = carry_cost;
+    *dp.plan_sig = dp.sig;   // the plan now belongs to this problem
   }
 }
 

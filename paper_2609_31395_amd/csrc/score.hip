@@ -8,19 +8,21 @@
 // accumulation; the exp2 / add epilogue runs on the VALU.
 //
 // Kernel layout (score_kernel):
-//   * One workgroup of 8 waves per CU (two waves per SIMD), persistent: the list of
+//   * One workgroup of 4 waves per CU (one wave per SIMD), persistent: the list of
 //     (segment, 64-key tile) work, segment = (request, row chunk of up to 512 query rows,
 //     KV head), is cut into equal-cost contiguous ranges, one per workgroup, so ragged
 //     lengths and query counts stay balanced and Q is loaded once per segment.
-//   * Each wave holds 4 row tiles of 16 query rows in registers (v_mfma_f32_16x16x32_bf16
-//     A operand) and the beta of its rows.  K tiles (64 keys, 4 pages) are gathered
+//   * Each wave holds 8 row tiles of 16 query rows in registers (v_mfma_f32_16x16x32_bf16
+//     A operand) and the beta of its rows.  Every wave reads each K tile from LDS once per
+//     sub-tile, so the LDS read traffic per tile is (waves x tile bytes): four waves of 128
+//     rows read half of what eight waves of 64 rows would.  K tiles (64 keys, 4 pages) are gathered
 //     through the block table straight into LDS (global_load_lds_dwordx4, 16 bytes per
 //     lane, chunk-swizzled rows), kScoreStages - 1 tiles ahead, one barrier per tile.
 //   * The MFMA chains and the exp2 epilogue are software-pipelined inside each wave (see
 //     the sweep below): the VALU works on one 16x16 unit while the matrix core works on
 //     another.
 //   * A lane's accumulator column is one key and 4 query rows, so the row sum is in-lane;
-//     the 4 lane groups and 8 waves are combined through LDS in a fixed order (no
+//     the 4 lane groups and 4 waves are combined through LDS in a fixed order (no
 //     atomics: deterministic, and independent of where the pages physically live).
 #include <atomic>
 
@@ -30,9 +32,10 @@ namespace actkv {
 
 namespace {
 
-// Scoring: 8 waves per workgroup (two per SIMD), 64 query rows per wave, one workgroup per
-// CU.
-constexpr int kThreads = 512;
+// Scoring: 4 waves per workgroup (one per SIMD, up to 512 registers each), 128 query rows
+// per wave, one workgroup per CU.  Every wave reads the whole K tile from LDS, so fewer,
+// taller waves read less: LDS traffic, not arithmetic, bounded the 8-wave form.
+constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kScoreStages = 4;   // K tiles resident in LDS for scoring (three in flight)
 constexpr int kStages = 3;        // the same for the LSE pass
@@ -212,13 +215,21 @@ __device__ __forceinline__ int chunk_row_tiles(int M, int c) {
 // Phase g issues the chain of unit g one MFMA per slot and, between those MFMAs, the
 // epilogue of unit g - 2, whose accumulator was finished a whole phase earlier.  The two
 // are independent, so the VALU works on one unit while the matrix core works on the other.
-// When unit g + 1 starts a new sub-tile its K operand is read from LDS during phase g,
-// each k-step right after the MFMA that last uses the old value.
+// The K operand of a sub-tile is read from LDS kOperandAhead sub-tiles before its first
+// chain (rotating operand buffers), so the reads' latency is hidden behind that many
+// sub-tiles of work (LDS reads queue behind the K tiles' direct-to-LDS writes).
 
 constexpr int kRowTile = 16;
-constexpr int kRowTilesPerWave = kRowsPerChunk / kRowTile / kWaves;   // 4
+constexpr int kRowTilesPerWave = kRowsPerChunk / kRowTile / kWaves;   // 8
 constexpr int kSubTiles = kKeyTile / 16;                              // 4
-static_assert(kRowTilesPerWave == 4 && kSubTiles == 4, "unit bookkeeping below");
+static_assert(kRowTilesPerWave == 8 && kSubTiles == 4, "unit bookkeeping below");
+// Sub-tiles of lookahead of the operand reads, and the buffers they rotate through (sub-tile
+// s of every tile uses buffer s % kOperandBufs, so the count divides the sub-tiles).
+constexpr int kOperandAhead = 2;
+constexpr int kOperandBufs = 4;
+static_assert(kOperandAhead >= 1 && kOperandAhead <= 2 && kOperandBufs > kOperandAhead &&
+                  kSubTiles % kOperandBufs == 0,
+              "a chain in the next tile (units 0 and 1) reads ahead within that tile");
 
 template <int D>
 struct Geom16 {
@@ -227,8 +238,8 @@ struct Geom16 {
 
 // Query row at (row tile T = w + kWaves * rt, tile row mm) of row chunk c.  The natural
 // order m = j * G + g is used unless the group max of MAX_MEAN needs a query's G = 8 or 16
-// heads in one lane: then they sit at the same lane position of 2 or 4 of the wave's row
-// tiles (heads 4*(rt % 2) + i, resp. 4*rt + i).
+// heads in one lane: then they sit at the same lane position of 2 or 4 consecutive row
+// tiles of the wave (heads 4*(rt % 2) + i, resp. 4*(rt % 4) + i).
 __device__ __forceinline__ void score_row_query(int G, bool grouped, int c, int T, int mm,
                                                 int* j, int* g) {
   if (!grouped) {
@@ -242,8 +253,8 @@ __device__ __forceinline__ void score_row_query(int G, bool grouped, int c, int 
     *j = c * (kRowsPerChunk / 8) + (rt >> 1) * (4 * kWaves) + w * 4 + a;
     *g = 4 * (rt & 1) + i;
   } else {
-    *j = c * (kRowsPerChunk / 16) + w * 4 + a;
-    *g = 4 * rt + i;
+    *j = c * (kRowsPerChunk / 16) + (rt >> 2) * (4 * kWaves) + w * 4 + a;
+    *g = 4 * (rt & 3) + i;
   }
 }
 
@@ -255,11 +266,11 @@ __device__ __forceinline__ int chunk_wave_tiles(int G, bool grouped, int n, int 
     const int r = rows < kRowsPerChunk ? rows : kRowsPerChunk;
     return ceil_div(r, kRowTile * kWaves);
   }
-  if (G == 8) {
-    const int qn = n - c * (kRowsPerChunk / 8);
-    return qn <= 4 * kWaves ? 2 : 4;
-  }
-  return 4;
+  // row tiles come in groups of G / 4 (one group: 4 queries per wave)
+  const int per = G / 4, qn = n - c * (kRowsPerChunk / G);
+  const int groups = qn <= 0 ? 1 : ceil_div(qn, 4 * kWaves);
+  const int t = groups * per;
+  return t < kRowTilesPerWave ? t : kRowTilesPerWave;
 }
 
 // Row tile rt of this wave as the 16x16x32 A operand: lane l holds row l%16 with head-dim
@@ -310,7 +321,7 @@ __device__ __forceinline__ bf16x8 lds_k16(const char* tile_buf, int sub, const K
 template <int D>
 struct Pipe16 {
   f32x4 c1, c2;                       // accumulators of units g-1 and g-2
-  bf16x8 kb[2][Geom16<D>::kSteps];    // B operands: sub-tile s of a tile reads kb[s & 1]
+  bf16x8 kb[kOperandBufs][Geom16<D>::kSteps];   // B operands: sub-tile s reads kb[s % bufs]
   float part[4];                      // the lane's partials of the current sub-tile, one per
                                       // accumulator element (independent add chains)
   float ex;                           // SUM: the last exp2 result, added one slot later
@@ -373,10 +384,10 @@ __device__ __forceinline__ void score_phase16(Pipe16<D>& st, const bf16x8 (&q)[G
       const float m = fmaxf(m01, m23);
       if (kRt & 1) st.part[0] += fmaxf(st.mx, m); else st.mx = m;
     } else {
-      // G == 16: heads 4*rt .. 4*rt+3 in row tile rt
+      // G == 16: heads 4*(rt%4) .. +3 in row tile rt, four row tiles per query group
       const float m = fmaxf(m01, m23);
-      st.mx = kRt == 0 ? m : fmaxf(st.mx, m);
-      if (kRt == kRowTilesPerWave - 1) st.part[0] += st.mx;
+      st.mx = (kRt & 3) == 0 ? m : fmaxf(st.mx, m);
+      if ((kRt & 3) == 3) st.part[0] += st.mx;
     }
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -401,25 +412,20 @@ struct SweepCtx {
 
 // Per-key partials of one tile: wave w, lane group q = l/16, key k at
 // red[w][q * kRedGrp + k].  The padded strides keep both the writes (64 lanes: 4 groups x
-// 16 keys) and the finishing reads (8 waves x 8 keys) on 64 distinct banks.
-constexpr int kRedGrp = kKeyTile + 16;     // 80 floats: group stride = 16 banks apart
-constexpr int kRedRow = 4 * kRedGrp + 8;   // 328 floats: wave stride = 8 banks apart
+// 16 keys) and the finishing reads (4 waves x 16 keys) on 64 distinct banks.
+constexpr int kRedGrp = kKeyTile + 16;      // 80 floats: group stride = 16 banks apart
+constexpr int kRedRow = 4 * kRedGrp + 16;   // 336 floats: wave stride = 16 banks apart
 typedef float RedTile[kWaves][kRedRow];
 constexpr int kRedBufs = 4;   // a tile's partials are read one tile later
 
-// Sum of the 32 partials of each key of tile t in a fixed order; wave w finishes keys
-// 8w .. 8w+7.  Lane l takes key 8w + l/8 and the four partials of wave l%8, then the
-// eight lanes of a key are summed pairwise (xor 1, xor 2, then the other four).
+// Sum of the 16 partials of each key of tile t in a fixed order; wave w finishes keys
+// 16w .. 16w+15.  Lane l takes key 16w + l/4 and the four partials of wave l%4, then the
+// four lanes of a key are summed pairwise (xor 1, then xor 2).
 __device__ __forceinline__ float dpp_xor1(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
 }
 __device__ __forceinline__ float dpp_xor2(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
-}
-// Lane 7 - i of the lane's group of eight (DPP row_half_mirror).  After the xor 1 and xor 2
-// sums every lane of a group of four holds the same value, so this adds the other four.
-__device__ __forceinline__ float dpp_half_mirror(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
 }
 
 // The finish of a tile in two halves, a phase apart, so that the LDS reads are not waited
@@ -430,18 +436,17 @@ __device__ __forceinline__ float dpp_half_mirror(float v) {
 // the K pipeline's waits count on that.
 __device__ __forceinline__ float4 finish_read(const RedTile& red) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int kk = w * (kKeyTile / kWaves) + (lane >> 3), ww = lane & 7;
+  const int kk = w * (kKeyTile / kWaves) + (lane >> 2), ww = lane & 3;
   const float* rr = red[ww] + kk;
   return make_float4(rr[0], rr[kRedGrp], rr[2 * kRedGrp], rr[3 * kRedGrp]);
 }
 
 __device__ __forceinline__ void finish_write(const SweepCtx& cx, float4 p, int t, bool valid) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int kk = w * (kKeyTile / kWaves) + (lane >> 3), ww = lane & 7;
+  const int kk = w * (kKeyTile / kWaves) + (lane >> 2), ww = lane & 3;
   float v = (p.x + p.y) + (p.z + p.w);
   v += dpp_xor1(v);
   v += dpp_xor2(v);
-  v += dpp_half_mirror(v);
   const int key = t * kKeyTile + kk;
   const uint32_t off = (valid && ww == 0 && key < cx.L) ? (uint32_t)key * 4u : 0x7FFFFFF0u;
   __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v * cx.out_scale), cx.out, off, 0, 0);
@@ -458,10 +463,11 @@ constexpr int kTileVmcnt = (kScoreStages - 2) * (TileGeom<D>::kLoadsPerWave + 1)
 
 // Phases P = 2 .. U+1 of tile i, U = 4 * NRT units per tile: the chain of unit P (of tile
 // i, or of tile i+1 once P >= U) and the epilogue of unit P - 2 of tile i.  The chain of
-// the first unit of a sub-tile also reads the next sub-tile's operand from LDS, a whole
-// sub-tile ahead of its use.  Phase 3 NRT (the first unit of sub-tile 3) reads sub-tile 0
-// of tile i+1: the barrier that makes tile i+1 visible sits there, and once every wave has
-// passed it no wave reads tile i's stage any more, which is then refilled.
+// the first unit of sub-tile s also reads the operand of sub-tile s + kOperandAhead from
+// LDS.  Phase (4 - kOperandAhead) NRT is the first to read sub-tile 0 of tile i+1: the
+// barrier that makes tile i+1 visible sits there, and once every wave has passed it no wave
+// reads tile i's stage any more (its last sub-tile was read kOperandAhead sub-tiles
+// earlier), which is then refilled.
 // kMask: tile i holds keys hidden from some rows.  kLast: no tile follows.
 template <int D, bool kMaxMean, int NRT, bool kMask, bool kLast, int P>
 __device__ __forceinline__ void tile_phases16(const SweepCtx& cx, const KLoadPlan<D, kWaves>& kp,
@@ -478,18 +484,22 @@ __device__ __forceinline__ void tile_phases16(const SweepCtx& cx, const KLoadPla
     const int st_i = (i - cx.i0) & (kScoreStages - 1), st_n = (i + 1 - cx.i0) & (kScoreStages - 1);
     const char* buf_i = cx.kbuf + st_i * Gm::kTileBytes;
     const char* buf_n = cx.kbuf + st_n * Gm::kTileBytes;
-    constexpr int kBarrier = 3 * NRT;
+    constexpr int kBarrier = (kSubTiles - kOperandAhead) * NRT;
     if constexpr (P == kBarrier) {
+      // the page of the tile after the one refilled below: a scalar load, issued before the
+      // barrier's full wait so that it is retired there (an outstanding scalar load would
+      // make every later LDS wait of the tile a wait for all LDS traffic)
+      const int32_t page = next_page;
+      const int nt = i + kScoreStages + 1;
+      next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp, nt < cx.i1 ? nt : cx.i1 - 1);
       // tile i + 1 is read from this phase on: this wave's loads of it have landed, this
       // wave's LDS traffic of tile i is retired, then the barrier
       wait_vmcnt<kTileVmcnt<D>>();
       wait_lgkmcnt0();
       __builtin_amdgcn_s_barrier();
       // no wave reads tile i any more: refill its stage with tile i + kScoreStages
-      issue_k_tile<D, kWaves>(cx.kl + st_i * Gm::kTileBytes, cx.kv_bytes, next_page,
-                              cx.num_pages, cx.page_bytes, kp);
-      const int nt = i + kScoreStages + 1;
-      next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp, nt < cx.i1 ? nt : cx.i1 - 1);
+      issue_k_tile<D, kWaves>(cx.kl + st_i * Gm::kTileBytes, cx.kv_bytes, page, cx.num_pages,
+                              cx.page_bytes, kp);
       fin = finish_read(red[(i - 1) & (kRedBufs - 1)]);   // unused in the first tile
     }
     // epilogue: unit P - 2 of tile i
@@ -499,12 +509,14 @@ __device__ __forceinline__ void tile_phases16(const SweepCtx& cx, const KLoadPla
     // chain: unit cu of tile i (P < U) or of tile i + 1
     constexpr bool kChain = P < U || !kLast;
     constexpr int cu = P < U ? P : P - U, cs = cu / NRT, cr = cu % NRT;
-    // the first unit of a sub-tile reads the operand of the next one
-    constexpr bool kNextTile = P < U && cs + 1 == kSubTiles;
+    // the first unit of a sub-tile reads the operand kOperandAhead sub-tiles on (in tile i+1
+    // once that passes the tile's end; a chain already in tile i+1 reads within it)
+    constexpr int ls = cs + kOperandAhead;
+    constexpr bool kNextTile = P < U && ls >= kSubTiles;
     constexpr bool kLoad = kChain && cu % NRT == 0 && !(kNextTile && kLast);
-    constexpr int lsub = (cs + 1) % kSubTiles;
+    constexpr int lsub = ls % kSubTiles;
     score_phase16<D, kMaxMean, kMask, kChain, true, kLoad, er>(
-        st, qreg[cr], st.kb[cs & 1], st.kb[(cs + 1) & 1], rp,
+        st, qreg[cr], st.kb[cs % kOperandBufs], st.kb[lsub % kOperandBufs], rp,
         (P < U && !kNextTile) ? buf_i : buf_n, lsub, beta[er], prow, key, cx.alpha, cx.G);
     if constexpr (er == NRT - 1) {
       // sub-tile es is complete in this lane: hand its partial to the other waves
@@ -551,8 +563,8 @@ __device__ __forceinline__ void score_sweep16(const SweepCtx& cx, const KLoadPla
   st.ex = 0.f;
   st.mx = 0.f;
   st.c1 = f32x4{0.f, 0.f, 0.f, 0.f};
-  // prologue: tile i0 in LDS, the last stage filled, operand of sub-tile 0, chains of units
-  // 0 and 1 (each reading the next sub-tile's operand when it starts a sub-tile)
+  // prologue: tile i0 in LDS, the last stage filled, operands of the first kOperandAhead
+  // sub-tiles, chains of units 0 and 1 (each reading ahead when it starts a sub-tile)
   wait_vmcnt<kTileVmcnt<D>>();
   __builtin_amdgcn_s_barrier();
   issue_k_tile<D, kWaves>(cx.kl + (kScoreStages - 1) * Gm::kTileBytes, cx.kv_bytes, next_page,
@@ -560,12 +572,16 @@ __device__ __forceinline__ void score_sweep16(const SweepCtx& cx, const KLoadPla
   finish_write(cx, fin, 0, false);
   next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp, clamp_tile(cx.i0 + kScoreStages));
 #pragma unroll
-  for (int ks = 0; ks < Geom16<D>::kSteps; ++ks) st.kb[0][ks] = lds_k16<D>(cx.kbuf, 0, rp, ks);
+  for (int sb = 0; sb < kOperandAhead; ++sb)
+#pragma unroll
+    for (int ks = 0; ks < Geom16<D>::kSteps; ++ks) st.kb[sb][ks] = lds_k16<D>(cx.kbuf, sb, rp, ks);
   score_phase16<D, kMaxMean, false, true, false, true, 0>(
-      st, qreg[0], st.kb[0], st.kb[1], rp, cx.kbuf, 1, beta[0], nullptr, 0, cx.alpha, cx.G);
-  score_phase16<D, kMaxMean, false, true, false, NRT == 1, 0>(
-      st, qreg[1 % NRT], st.kb[(1 / NRT) & 1], st.kb[(1 / NRT + 1) & 1], rp, cx.kbuf, 2,
+      st, qreg[0], st.kb[0], st.kb[kOperandAhead % kOperandBufs], rp, cx.kbuf, kOperandAhead,
       beta[0], nullptr, 0, cx.alpha, cx.G);
+  constexpr int s1 = 1 / NRT;   // sub-tile of unit 1
+  score_phase16<D, kMaxMean, false, true, false, NRT == 1, 0>(
+      st, qreg[1 % NRT], st.kb[s1 % kOperandBufs], st.kb[(s1 + kOperandAhead) % kOperandBufs],
+      rp, cx.kbuf, s1 + kOperandAhead, beta[0], nullptr, 0, cx.alpha, cx.G);
   for (int i = cx.i0; i < cx.i1; ++i) {
     const bool mask = i * kKeyTile + kKeyTile - 1 > cx.mask_from;
     if (i + 1 < cx.i1) {
@@ -637,6 +653,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
     DevProblem dp, const uint16_t* __restrict__ q_ptr, const uint16_t* __restrict__ kv_ptr,
     const int32_t* __restrict__ bt_ptr, const float* __restrict__ lse_ptr,
     float* __restrict__ scores_ptr, float* __restrict__ part_ptr, int64_t num_scores) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   using Gm = TileGeom<D>;
   __shared__ __align__(1024) char kbuf[kScoreStages][Gm::kTileBytes];
   __shared__ __align__(16) float beta_s[kRowsPerChunk];
@@ -731,11 +748,20 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
       score_row_query(G, grouped, c, w + kWaves * rt, lane & 15, &j, &g);
       real = real || j < n;
     }
-    if (__ballot(real) == 0ull) score_sweep_idle<D>(cx, kp, red);
-    else if (nrt >= 4) score_sweep16<D, kMaxMean, 4>(cx, kp, qreg, beta, red);
-    else if (nrt == 3) score_sweep16<D, kMaxMean, 3>(cx, kp, qreg, beta, red);
-    else if (nrt == 2) score_sweep16<D, kMaxMean, 2>(cx, kp, qreg, beta, red);
-    else score_sweep16<D, kMaxMean, 1>(cx, kp, qreg, beta, red);
+    if (__ballot(real) == 0ull) {
+      score_sweep_idle<D>(cx, kp, red);
+    } else {
+      switch (nrt < kRowTilesPerWave ? nrt : kRowTilesPerWave) {
+        case 1: score_sweep16<D, kMaxMean, 1>(cx, kp, qreg, beta, red); break;
+        case 2: score_sweep16<D, kMaxMean, 2>(cx, kp, qreg, beta, red); break;
+        case 3: score_sweep16<D, kMaxMean, 3>(cx, kp, qreg, beta, red); break;
+        case 4: score_sweep16<D, kMaxMean, 4>(cx, kp, qreg, beta, red); break;
+        case 5: score_sweep16<D, kMaxMean, 5>(cx, kp, qreg, beta, red); break;
+        case 6: score_sweep16<D, kMaxMean, 6>(cx, kp, qreg, beta, red); break;
+        case 7: score_sweep16<D, kMaxMean, 7>(cx, kp, qreg, beta, red); break;
+        default: score_sweep16<D, kMaxMean, 8>(cx, kp, qreg, beta, red); break;
+      }
+    }
   }
   wait_vmcnt<0>();   // drain: no LDS write may be outstanding when the workgroup exits
 }
@@ -745,6 +771,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
 __global__ __launch_bounds__(256) void chunk_reduce_kernel(DevProblem dp, float* scores,
                                                            const float* part,
                                                            int64_t num_scores) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   const int r = blockIdx.y, h = blockIdx.z;
   const ReqPlan pl = dp.plan[r];
   if (pl.nchunk <= 1) return;
@@ -832,6 +859,7 @@ __global__ __launch_bounds__(kDecMaxWaves * 64) void score_decode_kernel(
     DevProblem dp, const uint16_t* __restrict__ q_ptr, const char* __restrict__ kv_bytes,
     const int32_t* __restrict__ bt_ptr, const float* __restrict__ lse_ptr,
     float* __restrict__ acc_ptr) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   constexpr int S = Geom16<D>::kSteps;
   constexpr int kFlushKeys = kDecFlushPages * kPageSize;
   __shared__ float res_s[kDecMaxWaves][kFlushKeys];
@@ -1014,6 +1042,7 @@ template <int D>
 __global__ __launch_bounds__(kLseThreads, 1) void lse_partial_kernel(
     DevProblem dp, const uint16_t* __restrict__ q, const uint16_t* __restrict__ kv,
     const int32_t* __restrict__ bt, float2* __restrict__ part) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   using Gm = TileGeom<D, kLseWaves>;
   __shared__ __align__(1024) char kbuf[kStages][Gm::kTileBytes];
   const uint32_t kl = (uint32_t)(uintptr_t)(lds_char*)&kbuf[0][0];
@@ -1128,6 +1157,7 @@ __global__ __launch_bounds__(kLseThreads, 1) void lse_partial_kernel(
 // loads in flight at a time.  Grid: (requests, ceil(max rows per request / 256)).
 __global__ __launch_bounds__(256) void lse_merge_kernel(DevProblem dp, const float2* part,
                                                         float* lse) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   constexpr int kBatch = 8;
   const int r = blockIdx.x;
   const ReqPlan pl = dp.plan[r];

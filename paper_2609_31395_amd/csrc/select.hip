@@ -633,6 +633,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp,
                                                                 const float* __restrict__ scores,
                                                                 float* pooled,
                                                                 int32_t* __restrict__ kept) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   extern __shared__ uint32_t lds_keys[];
   __shared__ uint32_t hist[kMaxBins];
   __shared__ int64_t scan_tmp[17];
@@ -908,6 +909,7 @@ template <bool kLong>
 __global__ __launch_bounds__(kSelectThreads) void lrfu_select_kernel(
     DevProblem dp, const float* __restrict__ scores, float top_p, float decay, float* ks,
     uint8_t* hit, float* pooled, int32_t* __restrict__ kept, float* ks_kept) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   extern __shared__ uint32_t lds_keys[];
   __shared__ uint64_t hist64[kMaxBins / 2];   // 8 KiB: 64-bit masses, or the 32-bit counts
   __shared__ int64_t scan_tmp[17];

@@ -270,3 +270,15 @@ def test_noalloc_step_refuses_a_problem_past_its_scratch_array_on_the_host():
     c = bad.cstruct()
     assert actkv.load_library().actkv_step_noalloc(ctypes.byref(c), None, None, None, None, None,
                                                    0, None, None, None, None, None, None) == -1
+
+
+def test_unknown_flags_are_rejected():
+    p = _tiny()
+    p.flags = 2
+    lib = actkv.load_library()
+    import ctypes
+    c = p.cstruct()
+    assert lib.actkv_query(ctypes.byref(c), None, None, None, None) == -1
+    p.flags = actkv.FLAG_PLANNED
+    c = p.cstruct()
+    assert lib.actkv_query(ctypes.byref(c), None, None, None, None) == 0

@@ -280,3 +280,54 @@ def test_second_step_with_the_same_budgets_is_a_no_op():
     assert second["freed"].numel() == 0
     np.testing.assert_array_equal(second["new_lens"].cpu().numpy(),
                                   np.repeat(L2, pb.num_kv_heads))
+
+
+def test_plan_once_then_the_stages_equal_the_step():
+    """actkv_plan once, then score, select and compact with ACTKV_FLAG_PLANNED (no plan
+    kernel of their own): bit-identical to actkv_step on the same inputs."""
+    pb = CASES["two_row_chunks_g8"]()
+    lse = torch.from_numpy(_lse32(pb)).cuda()
+    bp, t = to_dev(pb)
+    qy = actkv.query(bp)
+    ref = actkv.step(bp, t["q"], t["kv"], t["bt"], t["free"], lse=lse,
+                     scores=torch.empty(actkv.num_scores(bp), device="cuda"),
+                     pooled=torch.empty(actkv.num_scores(bp), device="cuda"),
+                     kept=torch.empty(qy["num_kept"], dtype=torch.int32, device="cuda"))
+    torch.cuda.synchronize()
+    bp2, t2 = to_dev(pb)
+    ws = actkv.workspace(bp2)
+    actkv.plan(bp2, ws)
+    pp = bp2.planned()
+    scores = actkv.score(pp, t2["q"], t2["kv"], t2["bt"], lse=lse, ws=ws)
+    kept, pooled = actkv.select(pp, scores, ws=ws)
+    freed, new_lens = actkv.compact(pp, t2["kv"], t2["bt"], kept, t2["free"], ws=ws)
+    torch.cuda.synchronize()
+    for a, b in [(scores, ref["scores"]), (pooled, ref["pooled"]), (kept, ref["kept"]),
+                 (freed, ref["freed"]), (new_lens, ref["new_lens"]), (t2["kv"], t["kv"]),
+                 (t2["bt"], t["bt"])]:
+        assert torch.equal(a, b)
+
+
+def test_a_plan_of_another_problem_makes_the_kernels_write_nothing():
+    """ACTKV_FLAG_PLANNED on a workspace planned for a different problem: every kernel sees
+    the signature mismatch and returns, so the outputs keep their sentinels (no fault)."""
+    pa = CASES["ragged_g4_d128"]()
+    pb = custom(seq_lens=[100, 37, 600], q_lens=[7, 1, 20], budgets=[30, 50, 10, 37, 200, 1])
+    ba, _ = to_dev(pa)
+    bb, tb = to_dev(pb)
+    ws = torch.zeros(max(actkv.query(ba)["workspace_bytes"], actkv.query(bb)["workspace_bytes"]),
+                     dtype=torch.uint8, device="cuda")
+    actkv.plan(ba, ws)
+    pp = bb.planned()
+    n = actkv.num_scores(bb)
+    scores = torch.full((n,), -7.0, device="cuda")
+    actkv.score(pp, tb["q"], tb["kv"], tb["bt"], lse=torch.from_numpy(_lse32(pb)).cuda(),
+                out=scores, ws=ws)
+    kept = torch.full((actkv.query(bb)["num_kept"],), -7, dtype=torch.int32, device="cuda")
+    actkv.select(pp, scores, kept=kept, ws=ws)
+    bt0 = tb["bt"].clone()
+    kv0 = tb["kv"].clone()
+    actkv.compact(pp, tb["kv"], tb["bt"], kept, tb["free"], ws=ws)
+    torch.cuda.synchronize()
+    assert bool((scores == -7.0).all()) and bool((kept == -7).all())
+    assert torch.equal(tb["bt"], bt0) and torch.equal(tb["kv"], kv0)
