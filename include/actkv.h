@@ -113,6 +113,17 @@ typedef struct actkv_problem {
 #define ACTKV_FLAG_PLANNED 1u
 
 /*
+ * ACTKV_FLAG_SMALL_SELECT: TopK selection (actkv_select, actkv_step, actkv_step_inplace)
+ * runs on the small-footprint kernel (256 threads and about 17 KB of LDS per segment, the
+ * segment read from global memory in each pass) in place of the default one (1024 threads,
+ * the segment held in LDS or registers).  Same results, bit for bit; slower alone, but it
+ * fits beside a resident scoring workgroup, so it can run concurrently with scoring or
+ * other kernels on another stream (the pipelined actkv_step uses it that way whatever the
+ * flag).
+ */
+#define ACTKV_FLAG_SMALL_SELECT 2u
+
+/*
  * Host-only planning (the per-request counts of Alg. 4, steps 1-5: Y = ceil(L_r /
  * page_size) blocks in use, X = ceil(k / page_size) blocks the survivors need; here k is
  * the largest per-head budget of the request, capped at L_r): no GPU work, callable
@@ -214,12 +225,30 @@ actkv_status actkv_compact(const actkv_problem* p, void* kv_cache, int32_t* bloc
  * The whole step (Alg. 1 steps 1, 5 and 6): score -> select -> compact on `stream`.
  * scores, pooled and kept are optional outputs (NULL keeps them in the workspace);
  * lse may be NULL as in actkv_score.  The other arguments are as above.
+ * A large batch (several requests) is cut into request groups and pipelined: while group
+ * g is scored on `stream`, group g - 1 is selected and compacted on a second stream that
+ * the library creates on first use (one per device, default priority, never destroyed),
+ * with events between the two; the call returns with `stream` waiting for all of it, so
+ * work queued on `stream` afterwards sees the whole step.  Calls from several host threads
+ * are serialised while they enqueue.  Results are identical, bit for bit, to the
+ * unpipelined order.  See actkv_set_overlap.
  */
 actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
                         int32_t* block_table, const float* lse, const int32_t* free_pages,
                         int64_t num_free, float* scores, float* pooled, int32_t* kept,
                         int32_t* freed_pages, int32_t* new_lens, void* workspace,
                         size_t workspace_bytes, void* stream);
+
+/*
+ * Tuning of actkv_step's pipelining, process-wide: groups = 0 (the default) chooses
+ * automatically (at present: never, the sequential order measuring faster on MI355X);
+ * 1 never pipelines; 2 .. ACTKV_MAX_OVERLAP_GROUPS pipelines every batch of at least two
+ * requests in that many groups (fewer when there are fewer requests).  Other values: ACTKV_ERR_INVALID_ARGUMENT.  actkv_get_overlap
+ * returns the current setting.  actkv_step_noalloc never pipelines.
+ */
+#define ACTKV_MAX_OVERLAP_GROUPS 8
+actkv_status actkv_set_overlap(int32_t groups);
+int32_t actkv_get_overlap(void);
 
 /*
  * actkv_step for callers that cannot allocate: code under HIP graph capture, tight serving

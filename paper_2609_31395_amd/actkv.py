@@ -44,6 +44,8 @@ class CProblem(ctypes.Structure):
 
 
 FLAG_PLANNED = 1   # ACTKV_FLAG_PLANNED: the workspace already holds this problem's plan
+FLAG_SMALL_SELECT = 2   # ACTKV_FLAG_SMALL_SELECT: selection on the small-footprint kernel
+MAX_OVERLAP_GROUPS = 8   # ACTKV_MAX_OVERLAP_GROUPS
 
 
 _lib = None
@@ -87,6 +89,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
               "actkv_token_confidence_workspace", "actkv_token_confidence",
               "actkv_budget_update"):
         getattr(lib, f).restype = ctypes.c_int
+    lib.actkv_set_overlap.argtypes = [i32]
+    lib.actkv_set_overlap.restype = ctypes.c_int
+    lib.actkv_get_overlap.argtypes = []
+    lib.actkv_get_overlap.restype = i32
     lib.actkv_status_str.argtypes = [ctypes.c_int]
     lib.actkv_status_str.restype = ctypes.c_char_p
     _lib = lib
@@ -172,6 +178,12 @@ class Problem:
         plan already in the workspace (from plan() or an earlier call on this problem)."""
         import dataclasses
         return dataclasses.replace(self, flags=self.flags | FLAG_PLANNED)
+
+    def small_select(self) -> "Problem":
+        """The same problem with ACTKV_FLAG_SMALL_SELECT: TopK selection runs on the
+        small-footprint kernel (same results)."""
+        import dataclasses
+        return dataclasses.replace(self, flags=self.flags | FLAG_SMALL_SELECT)
 
 
 def _check(fn: str, code: int):
@@ -701,6 +713,16 @@ def budget_update(token_conf: torch.Tensor, offsets: np.ndarray, budgets: torch.
         _ptr(slopes), _ptr(thr), _ptr(kept), _stream(stream)))
     return dict(budgets=out[:R], slopes=slopes[:R], thresholds=thr[:R], retained=kept[:R],
                 _keep=off_d)
+
+
+def set_overlap(groups: int) -> None:
+    """actkv_set_overlap: 0 = automatic pipelining of large steps, 1 = never, 2 ..
+    MAX_OVERLAP_GROUPS = pipeline every step that can be, in that many request groups."""
+    _check("actkv_set_overlap", load_library().actkv_set_overlap(int(groups)))
+
+
+def get_overlap() -> int:
+    return int(load_library().actkv_get_overlap())
 
 
 def status_str(code: int) -> str:

@@ -71,6 +71,20 @@ struct WsLayout {
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Compute units of the current device (asked once per device; 256 if the query fails).
+inline int device_cus() {
+  static int cache[64] = {};   // 0: not asked yet
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int c = __atomic_load_n(&cache[dev], __ATOMIC_RELAXED);
+  if (c > 0) return c;
+  if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      c <= 0)
+    c = 256;
+  __atomic_store_n(&cache[dev], c, __ATOMIC_RELAXED);
+  return c;
+}
+
 inline WsLayout ws_layout(const HostPlan& hp) {
   WsLayout w;
   size_t o = 0;
@@ -114,12 +128,13 @@ struct DevProblem {
 
 
 // The whole step (actkv_step) on a caller-chosen workspace: validation, planning and the
-// launches of every stage.  actkv_step_noalloc passes its static scratch array.
+// launches of every stage.  actkv_step_noalloc passes its static scratch array and
+// may_overlap = false (the overlapped form creates a stream and events on first use).
 actkv_status step_impl(const actkv_problem* p, const void* q, void* kv_cache,
                        int32_t* block_table, const float* lse, const int32_t* free_pages,
                        int64_t num_free, float* scores, float* pooled, int32_t* kept,
                        int32_t* freed_pages, int32_t* new_lens, void* workspace,
-                       size_t workspace_bytes, void* stream);
+                       size_t workspace_bytes, void* stream, bool may_overlap);
 
 // Kernel launchers (each returns the hipGetLastError() of its launches).
 hipError_t launch_plan(const DevProblem& dp, hipStream_t s);
@@ -128,6 +143,12 @@ hipError_t launch_lse(const DevProblem& dp, const HostPlan& hp, const void* q, c
 hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
                         const void* kv, const int32_t* bt, const float* lse, float* scores,
                         float* score_part, hipStream_t s);
+// The scoring of requests [r0, r1), whose cost units sum to `cost` (the scoring kernel,
+// then the row-chunk reduction of those requests when some request has several chunks).
+hipError_t launch_score_range(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
+                              int64_t cost, const void* q, const void* kv, const int32_t* bt,
+                              const float* lse, float* scores, float* score_part,
+                              hipStream_t s);
 // acc[i] += s[i], i < n (both 16-byte aligned or n handled element-wise at the tail).
 hipError_t launch_accumulate(float* acc, const float* s, int64_t n, hipStream_t st);
 // Decode-step scoring added straight into acc: every request has at most one action query
@@ -138,6 +159,15 @@ hipError_t launch_score_decode(const DevProblem& dp, const HostPlan& hp, const v
                                hipStream_t s);
 hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
                          float* pooled, int32_t* kept, hipStream_t s);
+// The selection of requests [r0, r1) only: select_kernel (one 1024-thread workgroup per
+// segment), or select_side_kernel (256 threads, small LDS: fits beside a resident scoring
+// workgroup).  Both give the same pooled scores and kept indices.
+hipError_t launch_select_range(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
+                               const float* scores, float* pooled, int32_t* kept,
+                               hipStream_t s);
+hipError_t launch_select_side(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
+                              const float* scores, float* pooled, int32_t* kept,
+                              hipStream_t s);
 // LRFU selection (attention-aware keep scores): segments up to kLrfuMaxLen entries; those
 // longer than kLrfuLdsLen only with pooling windows up to kLrfuRegMaxWindow.
 constexpr int64_t kLrfuLdsLen = 38400;
@@ -163,6 +193,11 @@ hipError_t launch_budget_update(const float* tconf, const int64_t* offsets, int 
 hipError_t launch_compact(const DevProblem& dp, const HostPlan& hp, void* kv, int32_t* bt,
                           const int32_t* kept, const int32_t* free_pages, int32_t* freed,
                           int32_t* new_lens, hipStream_t s);
+// The compaction of requests [r0, r1), whose fresh pages are [f_lo, f_hi).
+hipError_t launch_compact_range(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
+                                int64_t f_lo, int64_t f_hi, void* kv, int32_t* bt,
+                                const int32_t* kept, const int32_t* free_pages, int32_t* freed,
+                                int32_t* new_lens, hipStream_t s);
 // In-place compaction (Alg. 4): slot planning into new_order (required), row copies,
 // block-table rewrite.
 hipError_t launch_compact_inplace(const DevProblem& dp, const HostPlan& hp, void* kv,

@@ -3,6 +3,10 @@
 #include <math.h>
 #include <string.h>
 
+#include <atomic>
+#include <mutex>
+#include <vector>
+
 #include "actkv.h"
 #include "actkv_internal.h"
 
@@ -13,6 +17,35 @@ using actkv::WsLayout;
 namespace {
 
 bool valid_pool_window(int32_t w) { return w >= 1 && w <= actkv::kMaxPoolWindow && (w % 2) == 1; }
+
+// Scoring cost units of a request (every row chunk and KV head): its key tiles times
+// score_tile_cost of each chunk's row tiles.
+int64_t request_score_cost(int64_t L, int64_t n, int32_t G, int32_t Hkv) {
+  const int64_t ntiles = (L + actkv::kKeyTile - 1) / actkv::kKeyTile;
+  const int64_t M = n * G;
+  const int64_t chunks = M > 0 ? (M + actkv::kRowsPerChunk - 1) / actkv::kRowsPerChunk : 1;
+  int64_t cost = 0;
+  for (int64_t c = 0; c < chunks; ++c) {
+    const int64_t rows = M - c * actkv::kRowsPerChunk;
+    const int64_t rt = rows <= 0 ? 1 : ((rows < actkv::kRowsPerChunk ? rows : actkv::kRowsPerChunk) + 31) / 32;
+    cost += ntiles * actkv::score_tile_cost(rt) * Hkv;
+  }
+  return cost;
+}
+
+// Fresh pages request r takes (X; 0 when every head keeps everything).  Budgets are
+// checked non-negative by plan_host.
+int64_t request_fresh_pages(const actkv_problem* p, int r) {
+  const int64_t L = p->seq_lens_h[r];
+  int64_t kmax = 0, bmin = INT64_MAX;
+  for (int h = 0; h < p->num_kv_heads; ++h) {
+    const int64_t b = p->budgets_h[(int64_t)r * p->num_kv_heads + h];
+    const int64_t k = b < L ? b : L;
+    kmax = k > kmax ? k : kmax;
+    bmin = b < bmin ? b : bmin;
+  }
+  return bmin < L ? (kmax + actkv::kPageSize - 1) / actkv::kPageSize : 0;
+}
 
 // Validates `p` and derives the host plan from the host mirrors.  Touches no device memory.
 actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
@@ -25,7 +58,7 @@ actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
   if (p->causal != 0 && p->causal != 1) return ACTKV_ERR_INVALID_ARGUMENT;
   if (p->agg != ACTKV_AGG_SUM && p->agg != ACTKV_AGG_MAX_MEAN) return ACTKV_ERR_INVALID_ARGUMENT;
   if (!isfinite(p->sm_scale) || p->sm_scale < 0.f) return ACTKV_ERR_INVALID_ARGUMENT;
-  if (p->flags & ~ACTKV_FLAG_PLANNED) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (p->flags & ~(ACTKV_FLAG_PLANNED | ACTKV_FLAG_SMALL_SELECT)) return ACTKV_ERR_INVALID_ARGUMENT;
   if (p->head_dim != 64 && p->head_dim != 128) return ACTKV_ERR_UNSUPPORTED;
   if (p->page_size != actkv::kPageSize) return ACTKV_ERR_UNSUPPORTED;
   if (p->num_kv_heads > 64) return ACTKV_ERR_UNSUPPORTED;
@@ -72,14 +105,7 @@ actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
     hp->sum_L += L;
     hp->max_L = L > hp->max_L ? L : hp->max_L;
     hp->max_n = n > hp->max_n ? n : hp->max_n;
-    const int64_t ntiles = (L + actkv::kKeyTile - 1) / actkv::kKeyTile;
-    const int64_t M = n * G;
-    const int32_t chunks = M > 0 ? (int32_t)((M + actkv::kRowsPerChunk - 1) / actkv::kRowsPerChunk) : 1;
-    for (int c = 0; c < chunks; ++c) {
-      const int64_t rows = M - (int64_t)c * actkv::kRowsPerChunk;
-      const int64_t rt = rows <= 0 ? 1 : ((rows < actkv::kRowsPerChunk ? rows : actkv::kRowsPerChunk) + 31) / 32;
-      hp->score_cost += ntiles * actkv::score_tile_cost(rt) * p->num_kv_heads;
-    }
+    hp->score_cost += request_score_cost(L, n, G, p->num_kv_heads);
     const int64_t lb = (L + actkv::kLseKeysPerBlock - 1) / actkv::kLseKeysPerBlock;
     hp->lse_parts += n * p->num_q_heads * lb;
     hp->max_lse_blocks = lb > hp->max_lse_blocks ? lb : hp->max_lse_blocks;
@@ -166,6 +192,106 @@ actkv_status plan_step(const Ctx& cx, const actkv_problem* p, hipStream_t s) {
   return hip_status(actkv::launch_plan(cx.dp, s));
 }
 
+// TopK selection of every request, on the kernel the problem's flags ask for.
+hipError_t run_select(const Ctx& cx, const actkv_problem* p, const float* scores, float* pooled,
+                      int32_t* kept, hipStream_t s) {
+  if (p->flags & ACTKV_FLAG_SMALL_SELECT)
+    return actkv::launch_select_side(cx.dp, cx.hp, 0, cx.hp.R, scores, pooled, kept, s);
+  return actkv::launch_select(cx.dp, cx.hp, scores, pooled, kept, s);
+}
+
+// ---- the pipelined step ---------------------------------------------------------------
+// Scoring is bound by the matrix and vector units and leaves HBM bandwidth and CU space
+// (registers, LDS) idle; selection and compaction are bound by latency and HBM and leave
+// the matrix units idle.  With the batch cut into request groups, group g is scored on the
+// caller's stream while group g - 1 is selected (select_side_kernel, small enough to sit
+// beside a scoring workgroup) and compacted on a second stream, so their kernels run on
+// the CUs the scoring kernel occupies.  The last group is selected and compacted on the
+// caller's stream once all scoring is done (the whole GPU is then free for it).  Every
+// order between the streams goes through an event: the side stream waits for a group's
+// scores; the caller's stream waits for the side stream at the end.  Requests of different
+// groups share no output, so no other order is needed.
+
+constexpr int kMaxOverlapGroups = ACTKV_MAX_OVERLAP_GROUPS;
+constexpr int kAutoOverlapGroups = 4;
+// Automatic pipelining from this much scoring (cost units).  Off for now: on MI355X the
+// side kernels, sharing CUs with the scoring kernel, run slower than the scoring of the
+// next group (the selection's passes are chains of L2 round trips; the gather keeps too
+// few loads in flight), so the pipelined step measured slower than the sequential one.
+constexpr int64_t kOverlapMinCost = INT64_MAX;
+// Share of the scoring cost in the last group: its selection and compaction are not hidden.
+constexpr double kOverlapLastShare = 0.125;
+
+std::atomic<int32_t> g_overlap{0};
+
+struct SideStream {
+  hipStream_t stream = nullptr;
+  hipEvent_t ev[kMaxOverlapGroups] = {};
+};
+constexpr int kMaxSideDevices = 64;
+std::mutex g_side_mu;   // held while a pipelined step enqueues (the events are shared)
+SideStream g_side[kMaxSideDevices];
+
+// The current device's side stream and events, created on first use.  g_side_mu held.
+actkv_status side_stream(SideStream** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ACTKV_ERR_HIP;
+  if (dev < 0 || dev >= kMaxSideDevices) return ACTKV_ERR_UNSUPPORTED;
+  SideStream& ss = g_side[dev];
+  if (!ss.stream) {
+    SideStream made;
+    for (hipEvent_t& e : made.ev)
+      if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return ACTKV_ERR_HIP;
+    if (hipStreamCreateWithFlags(&made.stream, hipStreamNonBlocking) != hipSuccess)
+      return ACTKV_ERR_HIP;
+    ss = made;
+  }
+  *out = &ss;
+  return ACTKV_OK;
+}
+
+// Request groups of a pipelined step: group g is requests [r[g], r[g + 1]), its scoring
+// cost cost[g] and its fresh pages [f[g], f[g + 1]).
+struct OverlapPlan {
+  int n = 0;
+  int r[kMaxOverlapGroups + 1] = {};
+  int64_t cost[kMaxOverlapGroups] = {};
+  int64_t f[kMaxOverlapGroups + 1] = {};
+};
+
+// Whether the step is pipelined, and its groups: groups 0 .. n-2 split (1 - last share)
+// of the scoring cost evenly, the last group takes the rest; every group holds at least one
+// request.
+bool plan_overlap(const actkv_problem* p, const HostPlan& hp, OverlapPlan* op) {
+  const int32_t mode = g_overlap.load(std::memory_order_relaxed);
+  if (mode == 1 || hp.R < 2 || hp.num_scores == 0) return false;
+  int G = mode >= 2 ? mode : kAutoOverlapGroups;
+  if (mode == 0 && hp.score_cost < kOverlapMinCost) return false;
+  if (G > hp.R) G = hp.R;
+  std::vector<int64_t> cost(hp.R);
+  for (int r = 0; r < hp.R; ++r)
+    cost[r] = request_score_cost(p->seq_lens_h[r], p->q_lens_h[r], hp.G, hp.Hkv);
+  const double total = (double)hp.score_cost;
+  int r = 0;
+  int64_t acc = 0, facc = 0;
+  op->n = G;
+  for (int g = 0; g < G; ++g) {
+    const int last_end = hp.R - (G - 1 - g);   // leave a request for every later group
+    const double target = (g + 1) * (1.0 - kOverlapLastShare) / (G - 1) * total;
+    int64_t gc = 0;
+    do {
+      gc += cost[r];
+      acc += cost[r];
+      facc += request_fresh_pages(p, r);
+      ++r;
+    } while (r < last_end && (g == G - 1 || (double)acc < target));
+    op->r[g + 1] = r;
+    op->cost[g] = gc;
+    op->f[g + 1] = facc;
+  }
+  return true;
+}
+
 actkv_status run_lse(const Ctx& cx, const void* q, const void* kv, const int32_t* bt,
                      float* lse_out, hipStream_t s) {
   float2* part = reinterpret_cast<float2*>(cx.base + cx.ws.lse_part);
@@ -182,6 +308,44 @@ actkv_status run_score(const Ctx& cx, const void* q, const void* kv, const int32
   }
   float* part = reinterpret_cast<float*>(cx.base + cx.ws.score_part);
   return hip_status(actkv::launch_score(cx.dp, cx.hp, q, kv, bt, lse, scores, part, s));
+}
+
+// The pipelined step's launches (the plan and the LSE, if any, already queued on s).
+actkv_status run_overlapped(const Ctx& cx, const OverlapPlan& op, const void* q, void* kv,
+                            int32_t* bt, const float* lse, const int32_t* free_pages,
+                            float* scores, float* pooled, int32_t* kept, int32_t* freed,
+                            int32_t* new_lens, hipStream_t s) {
+  std::lock_guard<std::mutex> lock(g_side_mu);
+  SideStream* ss = nullptr;
+  actkv_status st = side_stream(&ss);
+  if (st != ACTKV_OK) return st;
+  const DevProblem& dp = cx.dp;
+  const HostPlan& hp = cx.hp;
+  float* part = reinterpret_cast<float*>(cx.base + cx.ws.score_part);
+  const int G = op.n;
+  hipError_t e = hipSuccess;
+  for (int g = 0; g < G && e == hipSuccess; ++g) {
+    e = actkv::launch_score_range(dp, hp, op.r[g], op.r[g + 1], op.cost[g], q, kv, bt, lse,
+                                  scores, part, s);
+    if (e != hipSuccess || g == G - 1) break;
+    e = hipEventRecord(ss->ev[g], s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(ss->stream, ss->ev[g], 0);
+    if (e == hipSuccess)
+      e = actkv::launch_select_side(dp, hp, op.r[g], op.r[g + 1], scores, pooled, kept,
+                                    ss->stream);
+    if (e == hipSuccess)
+      e = actkv::launch_compact_range(dp, hp, op.r[g], op.r[g + 1], op.f[g], op.f[g + 1], kv,
+                                      bt, kept, free_pages, freed, new_lens, ss->stream);
+  }
+  if (e == hipSuccess)
+    e = actkv::launch_select_range(dp, hp, op.r[G - 1], op.r[G], scores, pooled, kept, s);
+  if (e == hipSuccess)
+    e = actkv::launch_compact_range(dp, hp, op.r[G - 1], op.r[G], op.f[G - 1], op.f[G], kv, bt,
+                                    kept, free_pages, freed, new_lens, s);
+  // join, also after a failed launch: nothing queued here may outlive the caller's order
+  hipError_t j = hipEventRecord(ss->ev[G - 1], ss->stream);
+  if (j == hipSuccess) j = hipStreamWaitEvent(s, ss->ev[G - 1], 0);
+  return hip_status(e != hipSuccess ? e : j);
 }
 
 }  // namespace
@@ -284,7 +448,7 @@ actkv_status actkv_select(const actkv_problem* p, const float* scores, float* po
   if (!pooled) pooled = reinterpret_cast<float*>(cx.base + cx.ws.pooled);
   st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
-  return hip_status(actkv::launch_select(cx.dp, cx.hp, scores, pooled, kept, s));
+  return hip_status(run_select(cx, p, scores, pooled, kept, s));
 }
 
 actkv_status actkv_compact(const actkv_problem* p, void* kv_cache, int32_t* block_table,
@@ -384,8 +548,16 @@ actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
                         int32_t* freed_pages, int32_t* new_lens, void* workspace,
                         size_t workspace_bytes, void* stream) {
   return actkv::step_impl(p, q, kv_cache, block_table, lse, free_pages, num_free, scores, pooled,
-                          kept, freed_pages, new_lens, workspace, workspace_bytes, stream);
+                          kept, freed_pages, new_lens, workspace, workspace_bytes, stream, true);
 }
+
+actkv_status actkv_set_overlap(int32_t groups) {
+  if (groups < 0 || groups > ACTKV_MAX_OVERLAP_GROUPS) return ACTKV_ERR_INVALID_ARGUMENT;
+  g_overlap.store(groups, std::memory_order_relaxed);
+  return ACTKV_OK;
+}
+
+int32_t actkv_get_overlap(void) { return g_overlap.load(std::memory_order_relaxed); }
 
 }  // extern "C"
 
@@ -395,7 +567,7 @@ actkv_status actkv::step_impl(const actkv_problem* p, const void* q, void* kv_ca
                               int32_t* block_table, const float* lse, const int32_t* free_pages,
                               int64_t num_free, float* scores, float* pooled, int32_t* kept,
                               int32_t* freed_pages, int32_t* new_lens, void* workspace,
-                              size_t workspace_bytes, void* stream) {
+                              size_t workspace_bytes, void* stream, bool may_overlap) {
   Ctx cx;
   actkv_status st = prepare(p, workspace, workspace_bytes, &cx);
   if (st != ACTKV_OK) return st;
@@ -414,9 +586,20 @@ actkv_status actkv::step_impl(const actkv_problem* p, const void* q, void* kv_ca
   if (!kept) kept = reinterpret_cast<int32_t*>(cx.base + cx.ws.kept);
   st = plan_step(cx, p, s);
   if (st != ACTKV_OK) return st;
+  OverlapPlan op;
+  if (may_overlap && plan_overlap(p, cx.hp, &op)) {
+    if (!lse) {
+      float* lse_ws = reinterpret_cast<float*>(cx.base + cx.ws.lse);
+      st = run_lse(cx, q, kv_cache, block_table, lse_ws, s);
+      if (st != ACTKV_OK) return st;
+      lse = lse_ws;
+    }
+    return run_overlapped(cx, op, q, kv_cache, block_table, lse, free_pages, scores, pooled,
+                          kept, freed_pages, new_lens, s);
+  }
   st = run_score(cx, q, kv_cache, block_table, lse, scores, s);
   if (st != ACTKV_OK) return st;
-  st = hip_status(actkv::launch_select(cx.dp, cx.hp, scores, pooled, kept, s));
+  st = hip_status(run_select(cx, p, scores, pooled, kept, s));
   if (st != ACTKV_OK) return st;
   return hip_status(actkv::launch_compact(cx.dp, cx.hp, kv_cache, block_table, kept, free_pages,
                                           freed_pages, new_lens, s));
@@ -492,7 +675,7 @@ actkv_status actkv_step_inplace(const actkv_problem* p, const void* q, void* kv_
   if (st != ACTKV_OK) return st;
   st = run_score(cx, q, kv_cache, block_table, lse, scores, s);
   if (st != ACTKV_OK) return st;
-  st = hip_status(actkv::launch_select(cx.dp, cx.hp, scores, pooled, kept, s));
+  st = hip_status(run_select(cx, p, scores, pooled, kept, s));
   if (st != ACTKV_OK) return st;
   return run_compact_inplace(cx, kv_cache, block_table, kept, freed_pages, new_lens, new_order,
                              s);

@@ -32,7 +32,7 @@ __host__ __device__ inline int compact_pages_per_wg(int Hkv) {
 template <int D, bool kInPlace>
 __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
     DevProblem dp, uint16_t* kv, const int32_t* __restrict__ bt, const int32_t* __restrict__ kept,
-    const int32_t* __restrict__ free_pages, int64_t num_fresh) {
+    const int32_t* __restrict__ free_pages, int64_t f_lo, int64_t f_hi) {
   if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   constexpr int CH = D / 8;                 // 16-byte chunks per row
   __shared__ int64_t src_slot[kCompactTable];   // flat source slot, -1: nothing to copy
@@ -41,8 +41,9 @@ __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
   __shared__ int wave_live[kCompactThreads / 64];
   const int Hkv = dp.Hkv;
   const int ppw = compact_pages_per_wg(Hkv);
-  const int64_t f0 = (int64_t)blockIdx.x * ppw;
-  const int npages = (int)(num_fresh - f0 < ppw ? num_fresh - f0 : ppw);
+  // destination pages [f_lo, f_hi) of this launch (whole requests' runs of them)
+  const int64_t f0 = f_lo + (int64_t)blockIdx.x * ppw;
+  const int npages = (int)(f_hi - f0 < ppw ? f_hi - f0 : ppw);
   const int entries = npages * kPageSize * Hkv;
 
   // ---- resolve every (page, slot, head) of this workgroup to its source slot once
@@ -129,12 +130,12 @@ __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
   }
 }
 
-__global__ __launch_bounds__(256) void compact_rewrite_kernel(DevProblem dp, int32_t* bt,
+__global__ __launch_bounds__(256) void compact_rewrite_kernel(DevProblem dp, int r0, int32_t* bt,
                                                               const int32_t* __restrict__ free_pages,
                                                               int32_t* __restrict__ freed,
                                                               int32_t* __restrict__ new_lens) {
   if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
-  const int r = blockIdx.x, Hkv = dp.Hkv;
+  const int r = r0 + (int)blockIdx.x, Hkv = dp.Hkv;
   const ReqPlan pl = dp.plan[r];
   for (int h = threadIdx.x; h < Hkv; h += 256) {
     const int b = dp.budgets[r * Hkv + h];
@@ -149,27 +150,33 @@ __global__ __launch_bounds__(256) void compact_rewrite_kernel(DevProblem dp, int
   }
 }
 
-hipError_t launch_compact(const DevProblem& dp, const HostPlan& hp, void* kv, int32_t* bt,
-                          const int32_t* kept, const int32_t* free_pages, int32_t* freed,
-                          int32_t* new_lens, hipStream_t s) {
-  if (hp.R == 0) return hipSuccess;
-  if (hp.fresh_needed > 0) {
+hipError_t launch_compact_range(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
+                                int64_t f_lo, int64_t f_hi, void* kv, int32_t* bt,
+                                const int32_t* kept, const int32_t* free_pages, int32_t* freed,
+                                int32_t* new_lens, hipStream_t s) {
+  if (r0 >= r1) return hipSuccess;
+  if (f_hi > f_lo) {
     const int ppw = compact_pages_per_wg(hp.Hkv);
-    const unsigned grid = (unsigned)((hp.fresh_needed + ppw - 1) / ppw);
+    const unsigned grid = (unsigned)((f_hi - f_lo + ppw - 1) / ppw);
     if (dp.D == 128)
       hipLaunchKernelGGL((compact_gather_kernel<128, false>), dim3(grid), dim3(kCompactThreads),
-                         0, s, dp, static_cast<uint16_t*>(kv), bt, kept, free_pages,
-                         hp.fresh_needed);
+                         0, s, dp, static_cast<uint16_t*>(kv), bt, kept, free_pages, f_lo, f_hi);
     else
       hipLaunchKernelGGL((compact_gather_kernel<64, false>), dim3(grid), dim3(kCompactThreads),
-                         0, s, dp, static_cast<uint16_t*>(kv), bt, kept, free_pages,
-                         hp.fresh_needed);
+                         0, s, dp, static_cast<uint16_t*>(kv), bt, kept, free_pages, f_lo, f_hi);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(compact_rewrite_kernel, dim3(hp.R), dim3(256), 0, s, dp, bt, free_pages,
-                     freed, new_lens);
+  hipLaunchKernelGGL(compact_rewrite_kernel, dim3(r1 - r0), dim3(256), 0, s, dp, r0, bt,
+                     free_pages, freed, new_lens);
   return hipGetLastError();
+}
+
+hipError_t launch_compact(const DevProblem& dp, const HostPlan& hp, void* kv, int32_t* bt,
+                          const int32_t* kept, const int32_t* free_pages, int32_t* freed,
+                          int32_t* new_lens, hipStream_t s) {
+  return launch_compact_range(dp, hp, 0, hp.R, 0, hp.fresh_needed, kv, bt, kept, free_pages,
+                              freed, new_lens, s);
 }
 
 // ---- in-place compaction (Alg. 4) --------------------------------------------------------
@@ -304,11 +311,11 @@ hipError_t launch_compact_inplace(const DevProblem& dp, const HostPlan& hp, void
     if (dp.D == 128)
       hipLaunchKernelGGL((compact_gather_kernel<128, true>), dim3(grid), dim3(kCompactThreads),
                          0, s, dp, static_cast<uint16_t*>(kv), bt, new_order, nullptr,
-                         hp.fresh_needed);
+                         (int64_t)0, hp.fresh_needed);
     else
       hipLaunchKernelGGL((compact_gather_kernel<64, true>), dim3(grid), dim3(kCompactThreads),
                          0, s, dp, static_cast<uint16_t*>(kv), bt, new_order, nullptr,
-                         hp.fresh_needed);
+                         (int64_t)0, hp.fresh_needed);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -56,5 +56,5 @@ extern "C" actkv_status actkv_step_noalloc(const actkv_problem* p, const void* q
   if (st != ACTKV_OK) return st;
   return actkv::step_impl(p, q, kv_cache, block_table, lse, free_pages, num_free, scores,
                           pooled, kept, freed_pages, new_lens, ptr,
-                          (size_t)ACTKV_NOALLOC_SCRATCH_BYTES, stream);
+                          (size_t)ACTKV_NOALLOC_SCRATCH_BYTES, stream, false);
 }

@@ -652,7 +652,8 @@ template <int D, bool kMaxMean>
 __global__ __launch_bounds__(kThreads, 1) void score_kernel(
     DevProblem dp, const uint16_t* __restrict__ q_ptr, const uint16_t* __restrict__ kv_ptr,
     const int32_t* __restrict__ bt_ptr, const float* __restrict__ lse_ptr,
-    float* __restrict__ scores_ptr, float* __restrict__ part_ptr, int64_t num_scores) {
+    float* __restrict__ scores_ptr, float* __restrict__ part_ptr, int64_t num_scores,
+    int64_t seg_lo, int64_t seg_hi) {
   if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   using Gm = TileGeom<D>;
   __shared__ __align__(1024) char kbuf[kScoreStages][Gm::kTileBytes];
@@ -663,9 +664,11 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int G = dp.G, Hq = dp.Hq, Hkv = dp.Hkv, C = dp.max_chunks;
   const bool grouped = kMaxMean && (G == 8 || G == 16);
-  const int64_t nseg = dp.num_segments;
-  const int64_t total = dp.seg_cost[nseg];
-  const int64_t c0 = total * blockIdx.x / gridDim.x, c1 = total * (blockIdx.x + 1) / gridDim.x;
+  // this launch scores segments [seg_lo, seg_hi) (whole requests: a request's segments are
+  // consecutive); workgroup b takes the b-th equal share of their cost
+  const int64_t base = dp.seg_cost[seg_lo], total = dp.seg_cost[seg_hi] - base;
+  const int64_t c0 = base + total * blockIdx.x / gridDim.x;
+  const int64_t c1 = base + total * (blockIdx.x + 1) / gridDim.x;
   if (c0 >= c1) return;
 
   SweepCtx cx;
@@ -679,13 +682,13 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
   cx.alpha = dp.sm_scale * kLog2e;
 
   // first segment: the largest s with seg_cost[s] <= c0 (it is never empty)
-  int64_t lo = 0, hi = nseg;
+  int64_t lo = seg_lo, hi = seg_hi;
   while (lo < hi) {
     const int64_t mid = (lo + hi + 1) / 2;
     if (dp.seg_cost[mid] <= c0) lo = mid; else hi = mid - 1;
   }
   bool first = true;
-  for (int64_t s = lo; s < nseg; ++s) {
+  for (int64_t s = lo; s < seg_hi; ++s) {
     const int64_t cs = dp.seg_cost[s], ce = dp.seg_cost[s + 1];
     if (cs >= c1) break;
     if (ce == cs) continue;
@@ -768,11 +771,11 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
 
 // scores = (scores + sum_{c >= 1} partial_c) * scale, for requests scored in several row
 // chunks (fixed order: deterministic).
-__global__ __launch_bounds__(256) void chunk_reduce_kernel(DevProblem dp, float* scores,
+__global__ __launch_bounds__(256) void chunk_reduce_kernel(DevProblem dp, int r0, float* scores,
                                                            const float* part,
                                                            int64_t num_scores) {
   if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
-  const int r = blockIdx.y, h = blockIdx.z;
+  const int r = r0 + (int)blockIdx.y, h = blockIdx.z;
   const ReqPlan pl = dp.plan[r];
   if (pl.nchunk <= 1) return;
   const float scale = dp.agg == ACTKV_AGG_MAX_MEAN ? (pl.n > 0 ? 1.0f / pl.n : 0.f) : 1.f;
@@ -784,34 +787,41 @@ __global__ __launch_bounds__(256) void chunk_reduce_kernel(DevProblem dp, float*
   }
 }
 
-hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
-                        const void* kv, const int32_t* bt, const float* lse, float* scores,
-                        float* score_part, hipStream_t s) {
-  if (hp.num_scores == 0) return hipSuccess;
+hipError_t launch_score_range(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
+                              int64_t cost, const void* q, const void* kv, const int32_t* bt,
+                              const float* lse, float* scores, float* score_part,
+                              hipStream_t s) {
+  if (hp.num_scores == 0 || r0 >= r1 || cost <= 0) return hipSuccess;
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const uint16_t* kk = static_cast<const uint16_t*>(kv);
-  int dev = 0, cus = 256;
-  if (hipGetDevice(&dev) == hipSuccess) {
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 256;
-  }
-  int64_t grid = cus;   // one 8-wave workgroup per CU
-  if (grid > hp.score_cost) grid = hp.score_cost > 0 ? hp.score_cost : 1;
+  const int64_t spr = (int64_t)hp.max_chunks * hp.Hkv;   // a request's segments are consecutive
+  const int64_t seg_lo = r0 * spr, seg_hi = r1 * spr;
+  int64_t grid = device_cus();   // one workgroup per CU
+  if (grid > cost) grid = cost;
   const bool mm = dp.agg == ACTKV_AGG_MAX_MEAN;
+  const int64_t n = hp.num_scores;
   if (dp.D == 128) {
-    if (mm) hipLaunchKernelGGL((score_kernel<128, true>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, hp.num_scores);
-    else hipLaunchKernelGGL((score_kernel<128, false>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, hp.num_scores);
+    if (mm) hipLaunchKernelGGL((score_kernel<128, true>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
+    else hipLaunchKernelGGL((score_kernel<128, false>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
   } else {
-    if (mm) hipLaunchKernelGGL((score_kernel<64, true>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, hp.num_scores);
-    else hipLaunchKernelGGL((score_kernel<64, false>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, hp.num_scores);
+    if (mm) hipLaunchKernelGGL((score_kernel<64, true>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
+    else hipLaunchKernelGGL((score_kernel<64, false>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (hp.max_chunks > 1) {
-    hipLaunchKernelGGL(chunk_reduce_kernel, dim3(64, hp.R, hp.Hkv), dim3(256), 0, s, dp, scores,
-                       score_part, hp.num_scores);
+    hipLaunchKernelGGL(chunk_reduce_kernel, dim3(64, r1 - r0, hp.Hkv), dim3(256), 0, s, dp, r0,
+                       scores, score_part, hp.num_scores);
     e = hipGetLastError();
   }
   return e;
+}
+
+hipError_t launch_score(const DevProblem& dp, const HostPlan& hp, const void* q,
+                        const void* kv, const int32_t* bt, const float* lse, float* scores,
+                        float* score_part, hipStream_t s) {
+  return launch_score_range(dp, hp, 0, hp.R, hp.score_cost, q, kv, bt, lse, scores, score_part,
+                            s);
 }
 
 // acc[i] += s[i] (streaming aggregation: the scores of one decode step added to the running
@@ -993,10 +1003,7 @@ hipError_t launch_score_decode(const DevProblem& dp, const HostPlan& hp, const v
                                const void* kv, const int32_t* bt, const float* lse, float* acc,
                                hipStream_t s) {
   if (hp.num_scores == 0 || hp.sum_n == 0) return hipSuccess;
-  int dev = 0, cus = 256;
-  if (hipGetDevice(&dev) == hipSuccess) {
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 256;
-  }
+  const int cus = device_cus();
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const char* kk = static_cast<const char*>(kv);
   const bool mm = dp.agg == ACTKV_AGG_MAX_MEAN;

@@ -63,13 +63,15 @@ __device__ __forceinline__ int lane_byte_offset() {
 }
 
 // Among bins [0, nbins) (higher bin = larger key), find the bin b holding the need-th
-// largest element: sum_{b' > b} hist[b'] < need <= sum_{b' >= b} hist[b'].  Thread t covers
-// max(1, nbins / kSelectThreads) bins counted down from the top.  Returns b and the count
-// strictly above it through LDS.
+// largest element: sum_{b' > b} hist[b'] < need <= sum_{b' >= b} hist[b'].  Thread t of NT
+// covers max(1, nbins / NT) bins counted down from the top (nbins a power of two).  Returns b
+// and the count strictly above it through LDS.
+template <int NT = kSelectThreads>
 __device__ __forceinline__ void find_bin(const uint32_t* hist, int nbins, uint32_t need,
                                          int64_t* scan_tmp, int* bin_out, uint32_t* above_out) {
-  // 1 or 2 bins per thread; threads past the bins of a small histogram hold none
-  const int t = threadIdx.x, per = nbins > kSelectThreads ? nbins / kSelectThreads : 1;
+  // nbins / NT bins per thread (at least 1); threads past the bins of a small histogram
+  // hold none
+  const int t = threadIdx.x, per = nbins > NT ? nbins / NT : 1;
   const int top = nbins - 1 - t * per;                        // this thread's highest bin
   uint32_t s = 0;
   for (int u = 0; u < per; ++u) s += top - u >= 0 ? hist[top - u] : 0u;
@@ -629,7 +631,7 @@ __device__ __forceinline__ void select_global(int L, int k, int hw, const float*
 
 }  // namespace
 
-__global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp,
+__global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp, int r0,
                                                                 const float* __restrict__ scores,
                                                                 float* pooled,
                                                                 int32_t* __restrict__ kept) {
@@ -641,7 +643,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp,
   __shared__ int s_bin;
   __shared__ uint32_t s_above;
 
-  const int h = blockIdx.x, r = blockIdx.y, Hkv = dp.Hkv;
+  const int h = blockIdx.x, r = r0 + (int)blockIdx.y, Hkv = dp.Hkv;
   const ReqPlan pl = dp.plan[r];
   const int L = pl.L;
   const int b = dp.budgets[r * Hkv + h];
@@ -656,6 +658,165 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp,
     select_regs(L, k, hw, in, pout, kout, lds_keys, hist, scan_tmp, mm_tmp, &s_bin, &s_above);
   else
     select_global(L, k, hw, in, pout, kout, hist, scan_tmp, &s_bin, &s_above);
+}
+
+// ---- the same selection beside a running scoring kernel ----------------------------------
+//
+// select_side_kernel computes exactly what select_kernel computes (the pooled scores and the
+// kept indices of every (request, KV head) of a range of requests), in a footprint small
+// enough to share a CU with a resident scoring workgroup: 256 threads, about 17 KB of LDS
+// and few registers.  The pipelined step runs it on a second stream for one group of
+// requests while the next group is scored.  The segment stays in global memory (it was
+// just written, so the passes read it from L2):
+//   pool   tiles of kSideTile raw scores plus the window's halo are staged in LDS, pooled,
+//          written out, and counted into the first histogram (key bits 31..21)
+//   radix  two passes over the pooled scores count bits 20..10, then 9..0, of the keys that
+//          match the digits found so far: tau, the key of the k-th largest entry, and how
+//          many entries equal to tau are taken
+//   emit   tile by tile, each thread owns kSidePer consecutive entries; a workgroup prefix
+//          sum of (greater, equal) counts, carried from tile to tile, places the kept indices
+//          in ascending order (ties to the lower index)
+namespace {
+
+constexpr int kSideThreads = 256;
+constexpr int kSidePer = 8;                            // entries per thread and tile
+constexpr int kSideTile = kSideThreads * kSidePer;     // 2048
+constexpr int kSideHalo = kMaxPoolWindow / 2;          // widest pooling half-window
+constexpr int kSideStage = kSideTile + 2 * kSideHalo;  // staged raw scores per tile
+constexpr int kSideLoads = (kSideStage + kSideThreads - 1) / kSideThreads;
+
+// f(t, v) for every entry t < L of the segment, v = p[t]: coalesced, kSidePer loads of a
+// thread in flight together.
+template <typename F>
+__device__ __forceinline__ void side_visit(const float* p, int L, F f) {
+  const int tid = threadIdx.x;
+#pragma unroll 1
+  for (int base = 0; base < L; base += kSideTile) {
+    float v[kSidePer];
+#pragma unroll
+    for (int j = 0; j < kSidePer; ++j) {
+      const int t = base + j * kSideThreads + tid;
+      v[j] = t < L ? p[t] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < kSidePer; ++j) {
+      const int t = base + j * kSideThreads + tid;
+      if (t < L) f(t, v[j]);
+    }
+  }
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(kSideThreads) void select_side_kernel(
+    DevProblem dp, int r0, const float* __restrict__ scores, float* pooled,
+    int32_t* __restrict__ kept) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
+  __shared__ float raw[kSideLoads * kSideThreads];
+  __shared__ uint32_t hist[kMaxBins];
+  __shared__ int64_t scan_tmp[17];
+  __shared__ int s_bin;
+  __shared__ uint32_t s_above;
+
+  const int tid = threadIdx.x;
+  const int h = blockIdx.x, r = r0 + (int)blockIdx.y, Hkv = dp.Hkv;
+  const ReqPlan pl = dp.plan[r];
+  const int L = pl.L;
+  const int b = dp.budgets[r * Hkv + h];
+  const int k = b < L ? b : L;
+  const float* in = scores + pl.seg_off + (int64_t)h * L;
+  float* pout = pooled + pl.seg_off + (int64_t)h * L;
+  int32_t* kout = kept + dp.kept_off[r * Hkv + h];
+  const int hw = dp.pool_window / 2;
+  const float ninf = -__builtin_inff();
+
+  // ---- pool (window clipped at the segment's ends) and the first digit
+  for (int i = tid; i < kMaxBins; i += kSideThreads) hist[i] = 0;
+#pragma unroll 1
+  for (int base = 0; base < L; base += kSideTile) {
+    float v[kSideLoads];
+#pragma unroll
+    for (int u = 0; u < kSideLoads; ++u) {
+      const int t = base - hw + u * kSideThreads + tid;
+      v[u] = (t >= 0 && t < L) ? in[t] : ninf;
+    }
+    __syncthreads();   // the previous tile's window reads are done (and hist is zeroed)
+#pragma unroll
+    for (int u = 0; u < kSideLoads; ++u) raw[u * kSideThreads + tid] = v[u];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kSidePer; ++j) {
+      const int i = j * kSideThreads + tid, t = base + i;
+      if (t < L) {
+        float m = raw[i + hw];
+        for (int d = 1; d <= hw; ++d) m = fmaxf(m, fmaxf(raw[i + hw - d], raw[i + hw + d]));
+        const uint32_t key = order_key(m);
+        pout[t] = key_value(key);
+        atomicAdd(&hist[key >> 21], 1u);
+      }
+    }
+  }
+  __syncthreads();   // pooled scores written (and visible to the workgroup), hist complete
+  if (k <= 0) return;
+  if (k >= L) {
+    for (int t = tid; t < L; t += kSideThreads) kout[t] = t;
+    return;
+  }
+
+  // ---- radix: tau and how many of the entries equal to it are taken
+  uint32_t need = (uint32_t)k;
+  find_bin<kSideThreads>(hist, kMaxBins, need, scan_tmp, &s_bin, &s_above);
+  uint32_t prefix = (uint32_t)s_bin;
+  need -= s_above;
+  for (int i = tid; i < kMaxBins; i += kSideThreads) hist[i] = 0;
+  __syncthreads();
+  side_visit(pout, L, [&](int, float v) {
+    const uint32_t key = order_key(v);
+    if ((key >> 21) == prefix) atomicAdd(&hist[(key >> 10) & (kMaxBins - 1)], 1u);
+  });
+  __syncthreads();
+  find_bin<kSideThreads>(hist, kMaxBins, need, scan_tmp, &s_bin, &s_above);
+  prefix = (prefix << 11) | (uint32_t)s_bin;
+  need -= s_above;
+  for (int i = tid; i < kMaxBins / 2; i += kSideThreads) hist[i] = 0;
+  __syncthreads();
+  side_visit(pout, L, [&](int, float v) {
+    const uint32_t key = order_key(v);
+    if ((key >> 10) == prefix) atomicAdd(&hist[key & (kMaxBins / 2 - 1)], 1u);
+  });
+  __syncthreads();
+  find_bin<kSideThreads>(hist, kMaxBins / 2, need, scan_tmp, &s_bin, &s_above);
+  const uint32_t tau = (prefix << 10) | (uint32_t)s_bin;
+  need -= s_above;
+
+  // ---- emit: every key > tau, then the first `need` keys == tau, in index order
+  int64_t gt_carry = 0, eq_carry = 0;   // uniform: counts of the tiles before
+#pragma unroll 1
+  for (int base = 0; base < L; base += kSideTile) {
+    const int t0 = base + tid * kSidePer;
+    uint32_t gtm = 0, eqm = 0;
+#pragma unroll
+    for (int j = 0; j < kSidePer; ++j) {
+      if (t0 + j < L) {
+        const uint32_t key = order_key(pout[t0 + j]);
+        gtm |= (uint32_t)(key > tau) << j;
+        eqm |= (uint32_t)(key == tau) << j;
+      }
+    }
+    const int64_t n_gt = __popc(gtm), n_eq = __popc(eqm);
+    int64_t tot;
+    const int64_t ex = block_excl_scan_i64((n_eq << 32) | n_gt, scan_tmp, &tot);
+    const int64_t eq_before = eq_carry + (ex >> 32), gt_before = gt_carry + (ex & 0xFFFFFFFFll);
+    int64_t eq_take = (int64_t)need - eq_before;
+    eq_take = eq_take < 0 ? 0 : (eq_take > n_eq ? n_eq : eq_take);
+    for (int64_t drop = n_eq - eq_take; drop > 0; --drop)   // keep the first eq_take ties
+      eqm &= ~(1u << (31 - __clz(eqm)));
+    int64_t pos = gt_before + (eq_before < (int64_t)need ? eq_before : (int64_t)need);
+    for (uint32_t m = gtm | eqm; m; m &= m - 1, ++pos)   // pos < k by the counts above
+      if (pos < k) kout[pos] = t0 + __builtin_ctz(m);
+    gt_carry += tot & 0xFFFFFFFFll;
+    eq_carry += tot >> 32;
+  }
 }
 
 // ---- attention-aware LRFU keep scores (Sec. 5.1; Alg. 1 steps 2-5) -----------------------
@@ -960,9 +1121,10 @@ hipError_t launch_lrfu_select(const DevProblem& dp, const HostPlan& hp, const fl
   return hipGetLastError();
 }
 
-hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
-                         float* pooled, int32_t* kept, hipStream_t s) {
-  if (hp.R == 0) return hipSuccess;
+hipError_t launch_select_range(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
+                               const float* scores, float* pooled, int32_t* kept,
+                               hipStream_t s) {
+  if (r0 >= r1) return hipSuccess;
   const int64_t keys = hp.max_L < kSelectLdsKeys ? hp.max_L : kSelectLdsKeys;
   const size_t lds = (size_t)(keys + kLdsPad) * sizeof(uint32_t);
   if (lds > 64 * 1024) {
@@ -970,8 +1132,22 @@ hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* 
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(select_kernel, dim3(hp.Hkv, hp.R), dim3(kSelectThreads), lds, s, dp, scores,
-                     pooled, kept);
+  hipLaunchKernelGGL(select_kernel, dim3(hp.Hkv, r1 - r0), dim3(kSelectThreads), lds, s, dp, r0,
+                     scores, pooled, kept);
+  return hipGetLastError();
+}
+
+hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
+                         float* pooled, int32_t* kept, hipStream_t s) {
+  return launch_select_range(dp, hp, 0, hp.R, scores, pooled, kept, s);
+}
+
+hipError_t launch_select_side(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
+                              const float* scores, float* pooled, int32_t* kept,
+                              hipStream_t s) {
+  if (r0 >= r1) return hipSuccess;
+  hipLaunchKernelGGL(select_side_kernel, dim3(hp.Hkv, r1 - r0), dim3(kSideThreads), 0, s, dp,
+                     r0, scores, pooled, kept);
   return hipGetLastError();
 }
 

@@ -274,11 +274,28 @@ def test_noalloc_step_refuses_a_problem_past_its_scratch_array_on_the_host():
 
 def test_unknown_flags_are_rejected():
     p = _tiny()
-    p.flags = 2
     lib = actkv.load_library()
     import ctypes
-    c = p.cstruct()
-    assert lib.actkv_query(ctypes.byref(c), None, None, None, None) == -1
-    p.flags = actkv.FLAG_PLANNED
-    c = p.cstruct()
-    assert lib.actkv_query(ctypes.byref(c), None, None, None, None) == 0
+    for flags, code in [(4, -1), (8, -1), (1 << 31, -1), (actkv.FLAG_PLANNED, 0),
+                        (actkv.FLAG_SMALL_SELECT, 0),
+                        (actkv.FLAG_PLANNED | actkv.FLAG_SMALL_SELECT, 0)]:
+        p.flags = flags
+        c = p.cstruct()
+        assert lib.actkv_query(ctypes.byref(c), None, None, None, None) == code, flags
+
+
+def test_overlap_setting_is_validated_and_kept():
+    """actkv_set_overlap: 0 .. ACTKV_MAX_OVERLAP_GROUPS accepted and read back; anything
+    else refused with the setting unchanged (host only, no device needed)."""
+    lib = actkv.load_library()
+    assert actkv.get_overlap() == 0
+    try:
+        for g in range(actkv.MAX_OVERLAP_GROUPS + 1):
+            actkv.set_overlap(g)
+            assert actkv.get_overlap() == g
+        actkv.set_overlap(3)
+        for bad in (-1, actkv.MAX_OVERLAP_GROUPS + 1, 1 << 20):
+            assert lib.actkv_set_overlap(bad) == -1
+            assert actkv.get_overlap() == 3
+    finally:
+        actkv.set_overlap(0)

@@ -56,6 +56,16 @@ def _lse32(pb):
     return oracle.lse(pb).astype(np.float32)
 
 
+# the two selection kernels: the default one and the small-footprint one
+# (ACTKV_FLAG_SMALL_SELECT) must give the same bits
+SELECT_KERNELS = ["default", "small"]
+
+
+def _select(bp, raw, kernel):
+    p = bp.small_select() if kernel == "small" else bp
+    return actkv.select(p, torch.from_numpy(raw).cuda())
+
+
 @pytest.mark.parametrize("case", sorted(CASES))
 def test_lse_matches_oracle(case):
     pb = CASES[case]()
@@ -88,30 +98,33 @@ def test_scores_with_library_lse(case):
     assert_scores_close(got.cpu().numpy(), oracle.scores(pb))
 
 
+@pytest.mark.parametrize("kernel", SELECT_KERNELS)
 @pytest.mark.parametrize("case", sorted(CASES))
-def test_select_is_bit_exact_on_the_oracle_scores(case):
+def test_select_is_bit_exact_on_the_oracle_scores(case, kernel):
     pb = CASES[case]()
     raw = oracle.scores(pb, lse_in=_lse32(pb))
     bp, t = to_dev(pb)
-    kept, pooled = actkv.select(bp, torch.from_numpy(raw).cuda())
+    kept, pooled = _select(bp, raw, kernel)
     np.testing.assert_array_equal(pooled.cpu().numpy(), oracle.pool(pb, raw))
     np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
 
 
-def test_select_ties_and_plateaus_are_bit_exact():
+@pytest.mark.parametrize("kernel", SELECT_KERNELS)
+def test_select_ties_and_plateaus_are_bit_exact(kernel):
     """Many equal scores (max-pool plateaus, quantised values): ties go to the lower index."""
     pb = custom(seq_lens=[5000, 777], q_lens=[1, 1], budgets=[1234, 2500, 1, 776],
                 pool_window=9)
     rng = np.random.default_rng(3)
     raw = (rng.integers(0, 40, size=oracle.num_scores(pb)) / 64).astype(np.float32)
     bp, t = to_dev(pb)
-    kept, pooled = actkv.select(bp, torch.from_numpy(raw).cuda())
+    kept, pooled = _select(bp, raw, kernel)
     np.testing.assert_array_equal(pooled.cpu().numpy(), oracle.pool(pb, raw))
     np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
 
 
+@pytest.mark.parametrize("kernel", SELECT_KERNELS)
 @pytest.mark.parametrize("window", [1, 5, 7, 9])
-def test_select_long_segments_are_bit_exact(window):
+def test_select_long_segments_are_bit_exact(window, kernel):
     """Segments at and past the LDS-resident length (38,400 keys) take the three select
     paths: LDS (<= 38,400), registers (<= 64,512 and windows <= 7) and global memory (longer,
     or window 9).  Budgets past 38,400 kept entries write the indices in two chunks."""
@@ -122,13 +135,14 @@ def test_select_long_segments_are_bit_exact(window):
     raw = (rng.standard_exponential(oracle.num_scores(pb)) * 1e-3).astype(np.float32)
     raw[::97] = raw[5]   # a plateau of equal values across the threshold region
     bp, t = to_dev(pb)
-    kept, pooled = actkv.select(bp, torch.from_numpy(raw).cuda())
+    kept, pooled = _select(bp, raw, kernel)
     np.testing.assert_array_equal(pooled.cpu().numpy(), oracle.pool(pb, raw))
     np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
 
 
+@pytest.mark.parametrize("kernel", SELECT_KERNELS)
 @pytest.mark.parametrize("L,k", [(40000, 1), (40000, 39999), (47104, 23552), (64511, 777)])
-def test_register_select_on_signed_and_tied_scores(L, k):
+def test_register_select_on_signed_and_tied_scores(L, k, kernel):
     """The register-resident path (38,400 < L <= 64,512) on scores of both signs (the key
     range spans all 32 bits), signed zeros and runs of equal values, at extreme budgets."""
     pb = custom(seq_lens=[L], q_lens=[1], num_q_heads=1, num_kv_heads=1, head_dim=64,
@@ -139,13 +153,14 @@ def test_register_select_on_signed_and_tied_scores(L, k):
     raw[rng.random(L) < 0.1] = np.float32(-0.0)
     raw[rng.random(L) < 0.2] = np.float32(0.5)
     bp, t = to_dev(pb)
-    kept, pooled = actkv.select(bp, torch.from_numpy(raw).cuda())
+    kept, pooled = _select(bp, raw, kernel)
     np.testing.assert_array_equal(pooled.cpu().numpy(), oracle.pool(pb, raw))
     np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
 
 
+@pytest.mark.parametrize("kernel", SELECT_KERNELS)
 @pytest.mark.parametrize("L,window", [(1000, 7), (40000, 7), (40000, 9), (64513, 3)])
-def test_pooled_scores_write_zero_as_positive_zero(L, window):
+def test_pooled_scores_write_zero_as_positive_zero(L, window, kernel):
     """Every select path (LDS, registers, global memory) writes a pooled -0 as +0 and keeps
     the oracle's selection on signed zeros."""
     pb = custom(seq_lens=[L], q_lens=[1], num_q_heads=1, num_kv_heads=1, head_dim=64,
@@ -155,10 +170,28 @@ def test_pooled_scores_write_zero_as_positive_zero(L, window):
     raw[rng.random(L) < 0.2] = np.float32(-1.5)
     raw[rng.random(L) < 0.01] = np.float32(2.0)
     bp, t = to_dev(pb)
-    kept, pooled = actkv.select(bp, torch.from_numpy(raw).cuda())
+    kept, pooled = _select(bp, raw, kernel)
     got = pooled.cpu().numpy()
     assert not np.any((got == 0) & np.signbit(got))
     np.testing.assert_array_equal(got, oracle.pool(pb, raw))
+    np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
+
+
+@pytest.mark.parametrize("kernel", SELECT_KERNELS)
+@pytest.mark.parametrize("window", [15, 63])
+def test_select_wide_windows_are_bit_exact(window, kernel):
+    """Pooling windows up to the largest supported (63) on segments shorter and longer than
+    a tile of the small kernel (2,048 entries) and than the window itself, with k at 0, 1,
+    L - 1 and L."""
+    pb = custom(seq_lens=[40, 2048, 2049, 7000, 31], q_lens=[1] * 5, num_q_heads=2,
+                num_kv_heads=2, head_dim=64, pool_window=window, spike_frac=0.0,
+                budgets=[0, 40, 1, 2047, 2048, 2000, 6999, 3500, 31, 30])
+    rng = np.random.default_rng(window)
+    raw = (rng.standard_exponential(oracle.num_scores(pb)) * 1e-2).astype(np.float32)
+    raw[rng.random(raw.size) < 0.3] = np.float32(0.25)
+    bp, t = to_dev(pb)
+    kept, pooled = _select(bp, raw, kernel)
+    np.testing.assert_array_equal(pooled.cpu().numpy(), oracle.pool(pb, raw))
     np.testing.assert_array_equal(kept.cpu().numpy(), oracle.select(pb, oracle.pool(pb, raw)))
 
 
