@@ -116,10 +116,10 @@ typedef struct actkv_problem {
  * ACTKV_FLAG_SMALL_SELECT: TopK selection (actkv_select, actkv_step, actkv_step_inplace)
  * runs on the small-footprint kernel (256 threads and about 17 KB of LDS per segment, the
  * segment read from global memory in each pass) in place of the default one (1024 threads,
- * the segment held in LDS or registers).  Same results, bit for bit; slower alone, but it
- * fits beside a resident scoring workgroup, so it can run concurrently with scoring or
- * other kernels on another stream (the pipelined actkv_step uses it that way whatever the
- * flag).
+ * the segment held in LDS or registers).  Same results, bit for bit; slower alone (about
+ * 95 us against 41 us for 128 segments of 35,000 entries on MI355X), but its small
+ * register and LDS budget lets it run beside other kernels on another stream (the
+ * pipelined actkv_step uses it for all groups but the last, whatever the flag).
  */
 #define ACTKV_FLAG_SMALL_SELECT 2u
 

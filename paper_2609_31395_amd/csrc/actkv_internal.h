@@ -43,6 +43,7 @@ struct HostPlan {
   int32_t max_chunks = 1;
   int64_t sum_n = 0, sum_L = 0, num_scores = 0;
   int64_t num_kept = 0, fresh_needed = 0, pages_freed = 0;
+  int64_t max_fresh = 0;          // most fresh pages (X) of one request
   int64_t pages_freed_inplace = 0;  // sum of Y - X over compacted requests
   int64_t num_segments = 0;       // R * max_chunks * Hkv
   int64_t score_cost = 0;         // total scoring cost units (key tiles x row tiles)
@@ -160,8 +161,8 @@ hipError_t launch_score_decode(const DevProblem& dp, const HostPlan& hp, const v
 hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
                          float* pooled, int32_t* kept, hipStream_t s);
 // The selection of requests [r0, r1) only: select_kernel (one 1024-thread workgroup per
-// segment), or select_side_kernel (256 threads, small LDS: fits beside a resident scoring
-// workgroup).  Both give the same pooled scores and kept indices.
+// segment), or select_side_kernel (512 threads, few registers, small LDS: for running beside
+// other kernels).  Both give the same pooled scores and kept indices.
 hipError_t launch_select_range(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
                                const float* scores, float* pooled, int32_t* kept,
                                hipStream_t s);
@@ -193,11 +194,11 @@ hipError_t launch_budget_update(const float* tconf, const int64_t* offsets, int 
 hipError_t launch_compact(const DevProblem& dp, const HostPlan& hp, void* kv, int32_t* bt,
                           const int32_t* kept, const int32_t* free_pages, int32_t* freed,
                           int32_t* new_lens, hipStream_t s);
-// The compaction of requests [r0, r1), whose fresh pages are [f_lo, f_hi).
+// The compaction of requests [r0, r1), of which none takes more than max_x fresh pages.
 hipError_t launch_compact_range(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
-                                int64_t f_lo, int64_t f_hi, void* kv, int32_t* bt,
-                                const int32_t* kept, const int32_t* free_pages, int32_t* freed,
-                                int32_t* new_lens, hipStream_t s);
+                                int64_t max_x, void* kv, int32_t* bt, const int32_t* kept,
+                                const int32_t* free_pages, int32_t* freed, int32_t* new_lens,
+                                hipStream_t s);
 // In-place compaction (Alg. 4): slot planning into new_order (required), row copies,
 // block-table rewrite.
 hipError_t launch_compact_inplace(const DevProblem& dp, const HostPlan& hp, void* kv,

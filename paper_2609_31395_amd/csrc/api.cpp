@@ -97,7 +97,9 @@ actkv_status plan_host(const actkv_problem* p, HostPlan* hp) {
       bmin = b < bmin ? b : bmin;
     }
     if (bmin < L) {
-      hp->fresh_needed += (kmax + BS - 1) / BS;
+      const int64_t X = (kmax + BS - 1) / BS;
+      hp->max_fresh = X > hp->max_fresh ? X : hp->max_fresh;
+      hp->fresh_needed += X;
       hp->pages_freed += (L + BS - 1) / BS;
       hp->pages_freed_inplace += (L + BS - 1) / BS - (kmax + BS - 1) / BS;
     }
@@ -204,20 +206,23 @@ hipError_t run_select(const Ctx& cx, const actkv_problem* p, const float* scores
 // Scoring is bound by the matrix and vector units and leaves HBM bandwidth and CU space
 // (registers, LDS) idle; selection and compaction are bound by latency and HBM and leave
 // the matrix units idle.  With the batch cut into request groups, group g is scored on the
-// caller's stream while group g - 1 is selected (select_side_kernel, small enough to sit
-// beside a scoring workgroup) and compacted on a second stream, so their kernels run on
-// the CUs the scoring kernel occupies.  The last group is selected and compacted on the
-// caller's stream once all scoring is done (the whole GPU is then free for it).  Every
-// order between the streams goes through an event: the side stream waits for a group's
-// scores; the caller's stream waits for the side stream at the end.  Requests of different
-// groups share no output, so no other order is needed.
+// caller's stream while group g - 1 is selected (select_side_kernel, the small-budget
+// selection) and compacted on a second stream, meant to run on the CUs the scoring kernel
+// occupies.  The last group is selected and compacted on the caller's stream once all
+// scoring is done (the whole GPU is then free for it).  Every order between the streams
+// goes through an event: the side stream waits for a group's scores; the caller's stream
+// waits for the side stream at the end.  Requests of different groups share no output, so
+// no other order is needed.
+// Measured on MI355X (32 x 35,000 tokens): the gather does run beside the scoring
+// workgroups, but slows them by about as much time as it saves; the selection is not
+// placed beside them at all and waits for free CUs; and scoring in several launches costs
+// 5-14% over one launch.  The pipelined step came out 9-32% slower than the sequential
+// one, so automatic mode does not pipeline.
 
 constexpr int kMaxOverlapGroups = ACTKV_MAX_OVERLAP_GROUPS;
 constexpr int kAutoOverlapGroups = 4;
-// Automatic pipelining from this much scoring (cost units).  Off for now: on MI355X the
-// side kernels, sharing CUs with the scoring kernel, run slower than the scoring of the
-// next group (the selection's passes are chains of L2 round trips; the gather keeps too
-// few loads in flight), so the pipelined step measured slower than the sequential one.
+// Automatic pipelining from this much scoring (cost units): never, for the measurements
+// above.
 constexpr int64_t kOverlapMinCost = INT64_MAX;
 // Share of the scoring cost in the last group: its selection and compaction are not hidden.
 constexpr double kOverlapLastShare = 0.125;
@@ -251,12 +256,12 @@ actkv_status side_stream(SideStream** out) {
 }
 
 // Request groups of a pipelined step: group g is requests [r[g], r[g + 1]), its scoring
-// cost cost[g] and its fresh pages [f[g], f[g + 1]).
+// cost cost[g] and the most fresh pages one of its requests takes, max_x[g].
 struct OverlapPlan {
   int n = 0;
   int r[kMaxOverlapGroups + 1] = {};
   int64_t cost[kMaxOverlapGroups] = {};
-  int64_t f[kMaxOverlapGroups + 1] = {};
+  int64_t max_x[kMaxOverlapGroups] = {};
 };
 
 // Whether the step is pipelined, and its groups: groups 0 .. n-2 split (1 - last share)
@@ -273,21 +278,22 @@ bool plan_overlap(const actkv_problem* p, const HostPlan& hp, OverlapPlan* op) {
     cost[r] = request_score_cost(p->seq_lens_h[r], p->q_lens_h[r], hp.G, hp.Hkv);
   const double total = (double)hp.score_cost;
   int r = 0;
-  int64_t acc = 0, facc = 0;
+  int64_t acc = 0;
   op->n = G;
   for (int g = 0; g < G; ++g) {
     const int last_end = hp.R - (G - 1 - g);   // leave a request for every later group
     const double target = (g + 1) * (1.0 - kOverlapLastShare) / (G - 1) * total;
-    int64_t gc = 0;
+    int64_t gc = 0, mx = 0;
     do {
       gc += cost[r];
       acc += cost[r];
-      facc += request_fresh_pages(p, r);
+      const int64_t x = request_fresh_pages(p, r);
+      mx = x > mx ? x : mx;
       ++r;
     } while (r < last_end && (g == G - 1 || (double)acc < target));
     op->r[g + 1] = r;
     op->cost[g] = gc;
-    op->f[g + 1] = facc;
+    op->max_x[g] = mx;
   }
   return true;
 }
@@ -334,14 +340,14 @@ actkv_status run_overlapped(const Ctx& cx, const OverlapPlan& op, const void* q,
       e = actkv::launch_select_side(dp, hp, op.r[g], op.r[g + 1], scores, pooled, kept,
                                     ss->stream);
     if (e == hipSuccess)
-      e = actkv::launch_compact_range(dp, hp, op.r[g], op.r[g + 1], op.f[g], op.f[g + 1], kv,
-                                      bt, kept, free_pages, freed, new_lens, ss->stream);
+      e = actkv::launch_compact_range(dp, hp, op.r[g], op.r[g + 1], op.max_x[g], kv, bt, kept,
+                                      free_pages, freed, new_lens, ss->stream);
   }
   if (e == hipSuccess)
     e = actkv::launch_select_range(dp, hp, op.r[G - 1], op.r[G], scores, pooled, kept, s);
   if (e == hipSuccess)
-    e = actkv::launch_compact_range(dp, hp, op.r[G - 1], op.r[G], op.f[G - 1], op.f[G], kv, bt,
-                                    kept, free_pages, freed, new_lens, s);
+    e = actkv::launch_compact_range(dp, hp, op.r[G - 1], op.r[G], op.max_x[G - 1], kv, bt, kept,
+                                    free_pages, freed, new_lens, s);
   // join, also after a failed launch: nothing queued here may outlive the caller's order
   hipError_t j = hipEventRecord(ss->ev[G - 1], ss->stream);
   if (j == hipSuccess) j = hipStreamWaitEvent(s, ss->ev[G - 1], 0);

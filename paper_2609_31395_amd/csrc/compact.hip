@@ -3,8 +3,9 @@
 // row is then rewritten and the old pages returned (Sec. 7.2: freed blocks go back to the
 // serving system).
 //
-// compact_gather_kernel: one 256-thread workgroup per group of destination (fresh) pages.
-// It first resolves every (page, slot, head) to its source slot through the kept indices
+// compact_gather_kernel: one 256-thread workgroup per group of destination (fresh) pages of
+// one request (grid: page groups of the longest request x requests; the workgroups past a
+// request's own pages return at once).  It first resolves every (page, slot, head) to its source slot through the kept indices
 // and the OLD block table (one lookup per thread, into LDS), then streams the rows: each
 // destination page is written contiguously ([slot][head][D] rows, 16 bytes per lane) and
 // each source row is read as one contiguous run.  Destination pages are disjoint from
@@ -16,7 +17,10 @@
 namespace actkv {
 
 constexpr int kCompactThreads = 256;
+// at most 72 registers: two of its waves fit on a SIMD beside a resident scoring wave
+constexpr int kCompactMinWaves = 7;
 constexpr int kCompactTable = 1024;   // (page, slot, head) source entries per workgroup
+constexpr int kCompactBatch = 8;      // 16-byte loads of a thread in flight together
 
 // Fresh pages handled by one workgroup: enough (page, slot, head) rows to give every
 // thread one source lookup, at least one page.
@@ -30,9 +34,9 @@ __host__ __device__ inline int compact_pages_per_wg(int Hkv) {
 // own page bt[r, Y - X + q] and new slot j gets token new_order[j] (`kept` below), a copy
 // only where that token is not already there.
 template <int D, bool kInPlace>
-__global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
-    DevProblem dp, uint16_t* kv, const int32_t* __restrict__ bt, const int32_t* __restrict__ kept,
-    const int32_t* __restrict__ free_pages, int64_t f_lo, int64_t f_hi) {
+__global__ __launch_bounds__(kCompactThreads, kCompactMinWaves) void compact_gather_kernel(
+    DevProblem dp, int r0, uint16_t* kv, const int32_t* __restrict__ bt,
+    const int32_t* __restrict__ kept, const int32_t* __restrict__ free_pages) {
   if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   constexpr int CH = D / 8;                 // 16-byte chunks per row
   __shared__ int64_t src_slot[kCompactTable];   // flat source slot, -1: nothing to copy
@@ -41,31 +45,26 @@ __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
   __shared__ int wave_live[kCompactThreads / 64];
   const int Hkv = dp.Hkv;
   const int ppw = compact_pages_per_wg(Hkv);
-  // destination pages [f_lo, f_hi) of this launch (whole requests' runs of them)
-  const int64_t f0 = f_lo + (int64_t)blockIdx.x * ppw;
-  const int npages = (int)(f_hi - f0 < ppw ? f_hi - f0 : ppw);
+  // request r's destination pages q0 .. q0 + npages - 1 (of its X)
+  const int r = r0 + (int)blockIdx.y;
+  const ReqPlan pl = dp.plan[r];
+  const int q0 = (int)blockIdx.x * ppw;
+  if (q0 >= pl.X) return;   // the request has fewer pages than the grid's longest
+  const int npages = pl.X - q0 < ppw ? pl.X - q0 : ppw;
   const int entries = npages * kPageSize * Hkv;
+  const int start = (pl.Y - pl.X) * kPageSize;   // in place: logical slot of new slot 0
 
   // ---- resolve every (page, slot, head) of this workgroup to its source slot once
   for (int e = threadIdx.x; e < entries; e += kCompactThreads) {
     const int p = e / (kPageSize * Hkv), s = (e / Hkv) % kPageSize, h = e % Hkv;
-    const int64_t f = f0 + p;
-    // request owning fresh page f: the largest r with fresh_off[r] <= f
-    int lo = 0, hi = dp.R - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) / 2;
-      if (dp.plan[mid].fresh_off <= f) lo = mid; else hi = mid - 1;
-    }
-    const ReqPlan pl = dp.plan[lo];
-    const int j = (int)(f - pl.fresh_off) * kPageSize + s;
-    const int bh = dp.budgets[lo * Hkv + h];
+    const int j = (q0 + p) * kPageSize + s;
+    const int bh = dp.budgets[r * Hkv + h];
     const int kh = bh < pl.L ? bh : pl.L;
-    const int start = (pl.Y - pl.X) * kPageSize;   // in place: logical slot of new slot 0
     int64_t src = -1;
     if (j < kh) {
-      const int t = kept[dp.kept_off[lo * Hkv + h] + j];
+      const int t = kept[dp.kept_off[r * Hkv + h] + j];
       if (t >= 0 && t < pl.L && !(kInPlace && t == start + j)) {
-        const int64_t page = bt[(int64_t)lo * dp.bt_stride + t / kPageSize];
+        const int64_t page = bt[(int64_t)r * dp.bt_stride + t / kPageSize];
         // pages outside the pool are never dereferenced (the slot is left unwritten)
         if (page >= 0 && page < dp.num_pages) src = page * kPageSize + t % kPageSize;
       }
@@ -73,8 +72,8 @@ __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
     src_slot[e] = src;
     if (s == 0 && h == 0) {
       const int64_t dpg = kInPlace
-          ? (int64_t)bt[(int64_t)lo * dp.bt_stride + (pl.Y - pl.X) + (f - pl.fresh_off)]
-          : (int64_t)free_pages[f];
+          ? (int64_t)bt[(int64_t)r * dp.bt_stride + (pl.Y - pl.X) + q0 + p]
+          : (int64_t)free_pages[pl.fresh_off + q0 + p];
       dst_page[p] = (dpg >= 0 && dpg < dp.num_pages) ? dpg : -1;
     }
   }
@@ -107,7 +106,7 @@ __global__ __launch_bounds__(kCompactThreads) void compact_gather_kernel(
   const int64_t plane = dp.num_pages * kPageSize * Hkv * (int64_t)D;   // K -> V offset
   const int rows = 2 * n_live;
   const int items = rows * CH;
-  constexpr int kBatch = 16;
+  constexpr int kBatch = kCompactBatch;
   for (int base = 0; base < items; base += kCompactThreads * kBatch) {
     u32x4 v[kBatch];
     int64_t dst[kBatch];
@@ -151,19 +150,19 @@ __global__ __launch_bounds__(256) void compact_rewrite_kernel(DevProblem dp, int
 }
 
 hipError_t launch_compact_range(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
-                                int64_t f_lo, int64_t f_hi, void* kv, int32_t* bt,
-                                const int32_t* kept, const int32_t* free_pages, int32_t* freed,
-                                int32_t* new_lens, hipStream_t s) {
+                                int64_t max_x, void* kv, int32_t* bt, const int32_t* kept,
+                                const int32_t* free_pages, int32_t* freed, int32_t* new_lens,
+                                hipStream_t s) {
   if (r0 >= r1) return hipSuccess;
-  if (f_hi > f_lo) {
+  if (max_x > 0) {
     const int ppw = compact_pages_per_wg(hp.Hkv);
-    const unsigned grid = (unsigned)((f_hi - f_lo + ppw - 1) / ppw);
+    const dim3 grid((unsigned)((max_x + ppw - 1) / ppw), (unsigned)(r1 - r0));
     if (dp.D == 128)
-      hipLaunchKernelGGL((compact_gather_kernel<128, false>), dim3(grid), dim3(kCompactThreads),
-                         0, s, dp, static_cast<uint16_t*>(kv), bt, kept, free_pages, f_lo, f_hi);
+      hipLaunchKernelGGL((compact_gather_kernel<128, false>), grid, dim3(kCompactThreads), 0, s,
+                         dp, r0, static_cast<uint16_t*>(kv), bt, kept, free_pages);
     else
-      hipLaunchKernelGGL((compact_gather_kernel<64, false>), dim3(grid), dim3(kCompactThreads),
-                         0, s, dp, static_cast<uint16_t*>(kv), bt, kept, free_pages, f_lo, f_hi);
+      hipLaunchKernelGGL((compact_gather_kernel<64, false>), grid, dim3(kCompactThreads), 0, s,
+                         dp, r0, static_cast<uint16_t*>(kv), bt, kept, free_pages);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -175,8 +174,8 @@ hipError_t launch_compact_range(const DevProblem& dp, const HostPlan& hp, int r0
 hipError_t launch_compact(const DevProblem& dp, const HostPlan& hp, void* kv, int32_t* bt,
                           const int32_t* kept, const int32_t* free_pages, int32_t* freed,
                           int32_t* new_lens, hipStream_t s) {
-  return launch_compact_range(dp, hp, 0, hp.R, 0, hp.fresh_needed, kv, bt, kept, free_pages,
-                              freed, new_lens, s);
+  return launch_compact_range(dp, hp, 0, hp.R, hp.max_fresh, kv, bt, kept, free_pages, freed,
+                              new_lens, s);
 }
 
 // ---- in-place compaction (Alg. 4) --------------------------------------------------------
@@ -305,17 +304,15 @@ hipError_t launch_compact_inplace(const DevProblem& dp, const HostPlan& hp, void
   if (e != hipSuccess) return e;
   // the destination pages are the last X pages of every compacted request: as many, and at
   // the same offsets, as the fresh pages of the other form
-  if (hp.fresh_needed > 0) {
+  if (hp.max_fresh > 0) {
     const int ppw = compact_pages_per_wg(hp.Hkv);
-    const unsigned grid = (unsigned)((hp.fresh_needed + ppw - 1) / ppw);
+    const dim3 grid((unsigned)((hp.max_fresh + ppw - 1) / ppw), (unsigned)hp.R);
     if (dp.D == 128)
-      hipLaunchKernelGGL((compact_gather_kernel<128, true>), dim3(grid), dim3(kCompactThreads),
-                         0, s, dp, static_cast<uint16_t*>(kv), bt, new_order, nullptr,
-                         (int64_t)0, hp.fresh_needed);
+      hipLaunchKernelGGL((compact_gather_kernel<128, true>), grid, dim3(kCompactThreads), 0, s,
+                         dp, 0, static_cast<uint16_t*>(kv), bt, new_order, nullptr);
     else
-      hipLaunchKernelGGL((compact_gather_kernel<64, true>), dim3(grid), dim3(kCompactThreads),
-                         0, s, dp, static_cast<uint16_t*>(kv), bt, new_order, nullptr,
-                         (int64_t)0, hp.fresh_needed);
+      hipLaunchKernelGGL((compact_gather_kernel<64, true>), grid, dim3(kCompactThreads), 0, s,
+                         dp, 0, static_cast<uint16_t*>(kv), bt, new_order, nullptr);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

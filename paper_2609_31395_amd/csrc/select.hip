@@ -663,60 +663,98 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp, i
 // ---- the same selection beside a running scoring kernel ----------------------------------
 //
 // select_side_kernel computes exactly what select_kernel computes (the pooled scores and the
-// kept indices of every (request, KV head) of a range of requests), in a footprint small
-// enough to share a CU with a resident scoring workgroup: 256 threads, about 17 KB of LDS
-// and few registers.  The pipelined step runs it on a second stream for one group of
-// requests while the next group is scored.  The segment stays in global memory (it was
-// just written, so the passes read it from L2):
-//   pool   tiles of kSideTile raw scores plus the window's halo are staged in LDS, pooled,
-//          written out, and counted into the first histogram (key bits 31..21)
-//   radix  two passes over the pooled scores count bits 20..10, then 9..0, of the keys that
-//          match the digits found so far: tau, the key of the k-th largest entry, and how
-//          many entries equal to tau are taken
-//   emit   tile by tile, each thread owns kSidePer consecutive entries; a workgroup prefix
-//          sum of (greater, equal) counts, carried from tile to tile, places the kept indices
-//          in ascending order (ties to the lower index)
+// kept indices of every (request, KV head) of a range of requests) on a small budget: 512
+// threads of at most 72 registers and about 45 KB of LDS, meant to run beside other kernels
+// (the pipelined step runs it on a second stream).  By the register and LDS counts two of
+// its waves per SIMD fit beside a scoring wave; measured on MI355X they are not placed
+// there, and the kernel starts as the scoring kernel's workgroups leave.  The segment stays
+// in global memory (it was just written: the passes read it from L2), in tiles of kSideTile
+// entries whose successor is always in flight:
+//   pool   each tile plus the window's halo is staged in LDS (two buffers, one barrier per
+//          tile), pooled, written out and counted into the first histogram (key bits 31..21)
+//   radix  the second histogram (bits 20..10) counts the keys that match the first digit,
+//          which are also gathered into LDS when they fit (kSideCand of them); the third
+//          (bits 9..0) is then counted from LDS, else by another pass.  Result: tau, the key
+//          of the k-th largest entry, and how many entries equal to tau are taken
+//   emit   each thread owns kSidePer consecutive entries of a tile; a workgroup prefix sum of
+//          (greater, equal) counts, carried from tile to tile, places the kept indices in
+//          ascending order (ties to the lower index)
 namespace {
 
-constexpr int kSideThreads = 256;
+constexpr int kSideThreads = 512;
+constexpr int kSideWaves = kSideThreads / 64;
 constexpr int kSidePer = 8;                            // entries per thread and tile
-constexpr int kSideTile = kSideThreads * kSidePer;     // 2048
+constexpr int kSideTile = kSideThreads * kSidePer;     // 4096
 constexpr int kSideHalo = kMaxPoolWindow / 2;          // widest pooling half-window
 constexpr int kSideStage = kSideTile + 2 * kSideHalo;  // staged raw scores per tile
-constexpr int kSideLoads = (kSideStage + kSideThreads - 1) / kSideThreads;
+constexpr int kSideLoads = (kSideStage + kSideThreads - 1) / kSideThreads;   // 9
+constexpr int kSideBuf = kSideLoads * kSideThreads;    // one staging buffer (floats)
+constexpr int kSideCand = 2 * kSideBuf;                // candidate keys the buffers hold
 
-// f(t, v) for every entry t < L of the segment, v = p[t]: coalesced, kSidePer loads of a
-// thread in flight together.
+// f(v, t) for every entry t < L of the segment, v = p[t], thread tid taking entries
+// base + j * kSideThreads + tid of each tile: coalesced, the next tile's loads issued before
+// the current tile is processed.
 template <typename F>
-__device__ __forceinline__ void side_visit(const float* p, int L, F f) {
+__device__ __forceinline__ void side_pass(const float* __restrict__ p, int L, F f) {
   const int tid = threadIdx.x;
+  float cur[kSidePer], nxt[kSidePer];
+#pragma unroll
+  for (int j = 0; j < kSidePer; ++j) {
+    const int t = j * kSideThreads + tid;
+    cur[j] = t < L ? p[t] : 0.0f;
+  }
 #pragma unroll 1
   for (int base = 0; base < L; base += kSideTile) {
-    float v[kSidePer];
+    const int nb = base + kSideTile;
 #pragma unroll
     for (int j = 0; j < kSidePer; ++j) {
-      const int t = base + j * kSideThreads + tid;
-      v[j] = t < L ? p[t] : 0.0f;
+      const int t = nb + j * kSideThreads + tid;
+      nxt[j] = t < L ? p[t] : 0.0f;
     }
 #pragma unroll
     for (int j = 0; j < kSidePer; ++j) {
       const int t = base + j * kSideThreads + tid;
-      if (t < L) f(t, v[j]);
+      if (t < L) f(cur[j], t);
     }
+#pragma unroll
+    for (int j = 0; j < kSidePer; ++j) cur[j] = nxt[j];
   }
+}
+
+// The entries of this thread's run in tile `base` (kSidePer consecutive from
+// base + tid * kSidePer), -inf past the end (never compared: masked by the caller).
+__device__ __forceinline__ void side_run_load(const float* __restrict__ p, int L, int base,
+                                              float (&v)[kSidePer]) {
+  const int t0 = base + (int)threadIdx.x * kSidePer;
+#pragma unroll
+  for (int j = 0; j < kSidePer; ++j) v[j] = t0 + j < L ? p[t0 + j] : -__builtin_inff();
+}
+
+// Appends this lane's key to the LDS list when `take` (one LDS atomic per wave).
+__device__ __forceinline__ void side_append(bool take, uint32_t key, uint32_t* list,
+                                            uint32_t* count, int cap) {
+  const uint64_t bal = __ballot(take);
+  if (!bal) return;
+  const int lane = threadIdx.x & 63;
+  uint32_t at = 0;
+  if (lane == __builtin_ctzll(bal)) at = atomicAdd(count, (uint32_t)__popcll(bal));
+  at = __shfl((int)at, __builtin_ctzll(bal), 64);
+  const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+  if (take && at + below < (uint32_t)cap) list[at + below] = key;
 }
 
 }  // namespace
 
-__global__ __launch_bounds__(kSideThreads) void select_side_kernel(
+__global__ __launch_bounds__(kSideThreads, 7) void select_side_kernel(
     DevProblem dp, int r0, const float* __restrict__ scores, float* pooled,
     int32_t* __restrict__ kept) {
   if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
-  __shared__ float raw[kSideLoads * kSideThreads];
+  __shared__ float raw[2][kSideBuf];
   __shared__ uint32_t hist[kMaxBins];
   __shared__ int64_t scan_tmp[17];
   __shared__ int s_bin;
-  __shared__ uint32_t s_above;
+  __shared__ uint32_t s_above, s_count, s_ncand;
 
   const int tid = threadIdx.x;
   const int h = blockIdx.x, r = r0 + (int)blockIdx.y, Hkv = dp.Hkv;
@@ -730,26 +768,34 @@ __global__ __launch_bounds__(kSideThreads) void select_side_kernel(
   const int hw = dp.pool_window / 2;
   const float ninf = -__builtin_inff();
 
-  // ---- pool (window clipped at the segment's ends) and the first digit
+  // ---- pool (window clipped at the segment's ends) and the first digit.  Tile i is staged
+  // in raw[i & 1]: that buffer was last read while pooling tile i - 2, before the barrier of
+  // tile i - 1, so one barrier per tile suffices.
   for (int i = tid; i < kMaxBins; i += kSideThreads) hist[i] = 0;
+  float v[kSideLoads];
+#pragma unroll
+  for (int u = 0; u < kSideLoads; ++u) {
+    const int t = -hw + u * kSideThreads + tid;
+    v[u] = (t >= 0 && t < L) ? in[t] : ninf;
+  }
 #pragma unroll 1
-  for (int base = 0; base < L; base += kSideTile) {
-    float v[kSideLoads];
+  for (int base = 0, tile = 0; base < L; base += kSideTile, ++tile) {
+    float* buf = raw[tile & 1];
 #pragma unroll
-    for (int u = 0; u < kSideLoads; ++u) {
-      const int t = base - hw + u * kSideThreads + tid;
-      v[u] = (t >= 0 && t < L) ? in[t] : ninf;
+    for (int u = 0; u < kSideLoads; ++u) buf[u * kSideThreads + tid] = v[u];
+    __syncthreads();   // the staged tile is visible (and, before tile 0, hist is zeroed)
+    const int nb = base + kSideTile;
+#pragma unroll
+    for (int u = 0; u < kSideLoads; ++u) {   // the next tile's loads, in flight while pooling
+      const int t = nb - hw + u * kSideThreads + tid;
+      v[u] = (nb < L && t >= 0 && t < L) ? in[t] : ninf;
     }
-    __syncthreads();   // the previous tile's window reads are done (and hist is zeroed)
-#pragma unroll
-    for (int u = 0; u < kSideLoads; ++u) raw[u * kSideThreads + tid] = v[u];
-    __syncthreads();
 #pragma unroll
     for (int j = 0; j < kSidePer; ++j) {
       const int i = j * kSideThreads + tid, t = base + i;
       if (t < L) {
-        float m = raw[i + hw];
-        for (int d = 1; d <= hw; ++d) m = fmaxf(m, fmaxf(raw[i + hw - d], raw[i + hw + d]));
+        float m = buf[i + hw];
+        for (int d = 1; d <= hw; ++d) m = fmaxf(m, fmaxf(buf[i + hw - d], buf[i + hw + d]));
         const uint32_t key = order_key(m);
         pout[t] = key_value(key);
         atomicAdd(&hist[key >> 21], 1u);
@@ -768,11 +814,17 @@ __global__ __launch_bounds__(kSideThreads) void select_side_kernel(
   find_bin<kSideThreads>(hist, kMaxBins, need, scan_tmp, &s_bin, &s_above);
   uint32_t prefix = (uint32_t)s_bin;
   need -= s_above;
+  if (tid == 0) { s_count = hist[prefix]; s_ncand = 0; }
+  __syncthreads();
+  const bool in_lds = s_count <= (uint32_t)kSideCand;   // uniform
+  uint32_t* cand = reinterpret_cast<uint32_t*>(&raw[0][0]);
   for (int i = tid; i < kMaxBins; i += kSideThreads) hist[i] = 0;
   __syncthreads();
-  side_visit(pout, L, [&](int, float v) {
-    const uint32_t key = order_key(v);
-    if ((key >> 21) == prefix) atomicAdd(&hist[(key >> 10) & (kMaxBins - 1)], 1u);
+  side_pass(pout, L, [&](float x, int) {
+    const uint32_t key = order_key(x);
+    const bool match = (key >> 21) == prefix;
+    if (match) atomicAdd(&hist[(key >> 10) & (kMaxBins - 1)], 1u);
+    if (in_lds) side_append(match, key, cand, &s_ncand, kSideCand);
   });
   __syncthreads();
   find_bin<kSideThreads>(hist, kMaxBins, need, scan_tmp, &s_bin, &s_above);
@@ -780,10 +832,18 @@ __global__ __launch_bounds__(kSideThreads) void select_side_kernel(
   need -= s_above;
   for (int i = tid; i < kMaxBins / 2; i += kSideThreads) hist[i] = 0;
   __syncthreads();
-  side_visit(pout, L, [&](int, float v) {
-    const uint32_t key = order_key(v);
-    if ((key >> 10) == prefix) atomicAdd(&hist[key & (kMaxBins / 2 - 1)], 1u);
-  });
+  if (in_lds) {
+    const int nc = (int)s_count;
+    for (int i = tid; i < nc; i += kSideThreads) {
+      const uint32_t key = cand[i];
+      if ((key >> 10) == prefix) atomicAdd(&hist[key & (kMaxBins / 2 - 1)], 1u);
+    }
+  } else {
+    side_pass(pout, L, [&](float x, int) {
+      const uint32_t key = order_key(x);
+      if ((key >> 10) == prefix) atomicAdd(&hist[key & (kMaxBins / 2 - 1)], 1u);
+    });
+  }
   __syncthreads();
   find_bin<kSideThreads>(hist, kMaxBins / 2, need, scan_tmp, &s_bin, &s_above);
   const uint32_t tau = (prefix << 10) | (uint32_t)s_bin;
@@ -791,17 +851,19 @@ __global__ __launch_bounds__(kSideThreads) void select_side_kernel(
 
   // ---- emit: every key > tau, then the first `need` keys == tau, in index order
   int64_t gt_carry = 0, eq_carry = 0;   // uniform: counts of the tiles before
+  float cur[kSidePer], nxt[kSidePer];
+  side_run_load(pout, L, 0, cur);
 #pragma unroll 1
   for (int base = 0; base < L; base += kSideTile) {
+    side_run_load(pout, L, base + kSideTile, nxt);   // in flight during this tile
     const int t0 = base + tid * kSidePer;
     uint32_t gtm = 0, eqm = 0;
 #pragma unroll
     for (int j = 0; j < kSidePer; ++j) {
-      if (t0 + j < L) {
-        const uint32_t key = order_key(pout[t0 + j]);
-        gtm |= (uint32_t)(key > tau) << j;
-        eqm |= (uint32_t)(key == tau) << j;
-      }
+      const uint32_t key = order_key(cur[j]);
+      const bool in_seg = t0 + j < L;
+      gtm |= (uint32_t)(in_seg && key > tau) << j;
+      eqm |= (uint32_t)(in_seg && key == tau) << j;
     }
     const int64_t n_gt = __popc(gtm), n_eq = __popc(eqm);
     int64_t tot;
@@ -816,6 +878,8 @@ __global__ __launch_bounds__(kSideThreads) void select_side_kernel(
       if (pos < k) kout[pos] = t0 + __builtin_ctz(m);
     gt_carry += tot & 0xFFFFFFFFll;
     eq_carry += tot >> 32;
+#pragma unroll
+    for (int j = 0; j < kSidePer; ++j) cur[j] = nxt[j];
   }
 }
 
