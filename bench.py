@@ -38,9 +38,10 @@ SCORE_SOURCES = ["paper_2609_31395_amd/csrc/score.hip",
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_kernel_batch32x35k_traffic.json")
 COPY_CALIB_BYTES = 512 << 20   # the known-size copy that calibrates FETCH_SIZE / WRITE_SIZE
 # fp32 VALU issue slots per second without packed fp32 (256 CUs x 4 SIMDs x 16 lanes x
-# 2.4 GHz); v_exp_f32 is a quarter-rate transcendental (4 slots)
+# 2.4 GHz); v_exp_f32 takes 2 slots: measured on MI355X with register-only probes, a SIMD
+# retires one wave64 v_exp_f32 per ~8.8 cycles against one FMA per ~4-5.6
 VALU_SLOTS_PER_S = 256 * 4 * 16 * 2.4e9
-EXP_SLOTS = 4
+EXP_SLOTS = 2
 LRFU_TOP_P, LRFU_DECAY = 0.9, 0.5   # the eviction policy's settings in the paper's evaluation
 
 
@@ -107,7 +108,7 @@ def score_flops(dp) -> int:
 
 def score_epilogue_slots(dp) -> float:
     """VALU issue slots of the scoring epilogue: per (query row, key) one FMA (scale and
-    LSE), one exp2 (quarter rate) and one add."""
+    LSE), one exp2 (half rate) and one add."""
     exps = score_flops(dp) / (2 * dp.head_dim)
     return exps * (1 + EXP_SLOTS + 1)
 
@@ -255,7 +256,8 @@ def run_table1(reps, dev, stream):
     scoring step (one action query per request, LSE supplied) and one compression operation
     -- selection plus the in-place compaction of Alg. 4, and selection plus the fresh-page
     compaction -- each timed with events on the launch stream; K/V and the block table are
-    restored before each compaction, outside the events."""
+    restored before each compaction, outside the events.  The compression operations use
+    the plan the score step leaves in the workspace (ACTKV_FLAG_PLANNED)."""
     import torch
     from paper_2609_31395_amd import actkv
     from paper_2609_31395_amd import workloads as W
@@ -281,19 +283,22 @@ def run_table1(reps, dev, stream):
             e[0].record(stream)
             actkv.score_accumulate(bp, dp.q, dp.kv, bt0, acc, lse=lse, ws=ws)
             e[1].record(stream)
+        # the compression operations reuse the plan the score step left in the workspace
+        # (same problem): no plan kernel of their own
+        pp = bp.planned()
         for e in ev_i:
             dp.kv.copy_(kv0)
             bt.copy_(bt0)
             e[0].record(stream)
-            actkv.select(bp, acc, pooled=pooled, kept=kept, ws=ws)
-            actkv.compact_inplace(bp, dp.kv, bt, kept, freed=freed, new_lens=new_lens, ws=ws,
+            actkv.select(pp, acc, pooled=pooled, kept=kept, ws=ws)
+            actkv.compact_inplace(pp, dp.kv, bt, kept, freed=freed, new_lens=new_lens, ws=ws,
                                   want_order=False)
             e[1].record(stream)
         for e in ev_f:
             bt.copy_(bt0)
             e[0].record(stream)
-            actkv.select(bp, acc, pooled=pooled, kept=kept, ws=ws)
-            actkv.compact(bp, dp.kv, bt, kept, free, freed=freed, new_lens=new_lens, ws=ws)
+            actkv.select_compact(pp, acc, dp.kv, bt, free, pooled=pooled, kept=kept,
+                                 freed=freed, new_lens=new_lens, ws=ws)
             e[1].record(stream)
         torch.cuda.synchronize()
         # the score step and the fresh-page compression replayed from HIP graphs: GPU time
@@ -307,8 +312,8 @@ def run_table1(reps, dev, stream):
 
             def fresh():
                 restore_bt()
-                actkv.select(bp, acc, pooled=pooled, kept=kept, ws=ws)
-                actkv.compact(bp, dp.kv, bt, kept, free, freed=freed, new_lens=new_lens, ws=ws)
+                actkv.select_compact(pp, acc, dp.kv, bt, free, pooled=pooled, kept=kept,
+                                     freed=freed, new_lens=new_lens, ws=ws)
 
             side = torch.cuda.Stream()
             side.wait_stream(torch.cuda.current_stream())

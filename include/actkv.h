@@ -222,9 +222,26 @@ actkv_status actkv_compact(const actkv_problem* p, void* kv_cache, int32_t* bloc
                            size_t workspace_bytes, void* stream);
 
 /*
+ * Eviction then fresh-page compaction (Alg. 1 steps 5 and 6): actkv_select followed by
+ * actkv_compact on the kept entries, in one call.  Arguments as there; pooled and kept
+ * may be NULL (kept in the workspace).  Results are those of the two calls, bit for bit.
+ * For small problems (at most 32 (request, KV head) segments keeping at most 512 entries
+ * each, and without ACTKV_FLAG_SMALL_SELECT) both run in a single kernel: one workgroup per
+ * segment selects and then copies its own head's rows, and the last workgroup of a request
+ * to finish rewrites its block-table row (a counter per request in the workspace; nothing
+ * waits on another workgroup).
+ */
+actkv_status actkv_select_compact(const actkv_problem* p, const float* scores, float* pooled,
+                                  int32_t* kept, void* kv_cache, int32_t* block_table,
+                                  const int32_t* free_pages, int64_t num_free,
+                                  int32_t* freed_pages, int32_t* new_lens, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/*
  * The whole step (Alg. 1 steps 1, 5 and 6): score -> select -> compact on `stream`.
  * scores, pooled and kept are optional outputs (NULL keeps them in the workspace);
- * lse may be NULL as in actkv_score.  The other arguments are as above.
+ * lse may be NULL as in actkv_score.  The other arguments are as above.  Selection and
+ * compaction run as in actkv_select_compact.
  * A large batch (several requests) is cut into request groups and pipelined: while group
  * g is scored on `stream`, group g - 1 is selected and compacted on a second stream that
  * the library creates on first use (one per device, default priority, never destroyed),

@@ -68,6 +68,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.actkv_score.argtypes = [P, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_select.argtypes = [P, vp, vp, vp, vp, sz, vp]
     lib.actkv_compact.argtypes = [P, vp, vp, vp, vp, i64, vp, vp, vp, sz, vp]
+    lib.actkv_select_compact.argtypes = [P, vp, vp, vp, vp, vp, vp, i64, vp, vp, vp, sz, vp]
     lib.actkv_step.argtypes = [P, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_step_noalloc.argtypes = [P, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp]
     f32 = ctypes.c_float
@@ -84,6 +85,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.actkv_compact_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.actkv_step_inplace.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for f in ("actkv_query", "actkv_plan", "actkv_lse", "actkv_score", "actkv_select", "actkv_compact",
+              "actkv_select_compact",
               "actkv_step", "actkv_step_noalloc", "actkv_lrfu_select", "actkv_step_lrfu", "actkv_query_inplace",
               "actkv_compact_inplace", "actkv_step_inplace", "actkv_score_accumulate",
               "actkv_token_confidence_workspace", "actkv_token_confidence",
@@ -452,6 +454,35 @@ def compact(p: Problem, kv_cache: torch.Tensor, block_table: torch.Tensor, kept:
                                               _ptr(freed), _ptr(new_lens), _ptr(ws),
                                               _ws_bytes(ws), _stream(stream)))
     return freed[:z.freed], new_lens
+
+
+def select_compact(p: Problem, scores: torch.Tensor, kv_cache: torch.Tensor,
+                   block_table: torch.Tensor, free_pages: torch.Tensor,
+                   pooled: Optional[torch.Tensor] = None, kept: Optional[torch.Tensor] = None,
+                   freed: Optional[torch.Tensor] = None, new_lens: Optional[torch.Tensor] = None,
+                   ws: Optional[torch.Tensor] = None, stream=None) -> dict:
+    """actkv_select_compact: selection then fresh-page compaction in one call (in place on
+    kv_cache / block_table).  Returns freed, new_lens and the given pooled / kept."""
+    lib = load_library()
+    z = _Sizes(p)
+    z.need("scores", scores, _F32, z.scores)
+    z.need("pooled", pooled, _F32, z.scores, required=False)
+    z.need("kept", kept, _I32, z.kept, required=False)
+    _compact_outputs(z, kv_cache, block_table, free_pages, freed, new_lens)
+    z.check_ws(ws)
+    dev = kv_cache.device
+    if freed is None:
+        freed = torch.empty(max(z.freed, 1), dtype=torch.int32, device=dev)
+    if new_lens is None:
+        new_lens = torch.empty(z.lens, dtype=torch.int32, device=dev)
+    ws = workspace(p, dev) if ws is None else ws
+    c = p.cstruct()
+    _check("actkv_select_compact", lib.actkv_select_compact(
+        ctypes.byref(c), _ptr(scores), _ptr(pooled), _ptr(kept), _ptr(kv_cache),
+        _ptr(block_table), _ptr(free_pages), _numel(free_pages), _ptr(freed), _ptr(new_lens),
+        _ptr(ws), _ws_bytes(ws), _stream(stream)))
+    return dict(freed=freed[:z.freed], new_lens=new_lens, pooled=pooled,
+                kept=None if kept is None else kept[:z.kept])
 
 
 def _step_args(z: _Sizes, q, kv_cache, block_table, free_pages, lse, scores, pooled, kept,

@@ -44,6 +44,7 @@ struct HostPlan {
   int64_t sum_n = 0, sum_L = 0, num_scores = 0;
   int64_t num_kept = 0, fresh_needed = 0, pages_freed = 0;
   int64_t max_fresh = 0;          // most fresh pages (X) of one request
+  int64_t max_k = 0;              // most kept entries of one (request, KV head)
   int64_t pages_freed_inplace = 0;  // sum of Y - X over compacted requests
   int64_t num_segments = 0;       // R * max_chunks * Hkv
   int64_t score_cost = 0;         // total scoring cost units (key tiles x row tiles)
@@ -67,6 +68,7 @@ struct WsLayout {
   size_t kept = 0;         // int32[num_kept]
   size_t ip_src = 0;       // int32[num_kept]: in-place copy sources by rank, at kept_off
   size_t ip_order = 0;     // int32[num_kept]: in-place new slot order when the caller has none
+  size_t req_done = 0;     // int32[R]: per-request counters of the fused selection+compaction
   size_t total = 0;
 };
 
@@ -102,6 +104,7 @@ inline WsLayout ws_layout(const HostPlan& hp) {
   w.kept = take(sizeof(int32_t) * (size_t)hp.num_kept);
   w.ip_src = take(sizeof(int32_t) * (size_t)hp.num_kept);
   w.ip_order = take(sizeof(int32_t) * (size_t)hp.num_kept);
+  w.req_done = take(sizeof(int32_t) * (size_t)(hp.R > 0 ? hp.R : 1));
   w.total = o;
   return w;
 }
@@ -125,6 +128,7 @@ struct DevProblem {
   int64_t num_segments;
   uint64_t sig;            // signature of this problem (host-computed)
   uint64_t* plan_sig;      // workspace: signature of the problem the plan was written for
+  int32_t* req_done;       // workspace [R]: zero between launches (see select_compact_kernel)
 };
 
 
@@ -169,6 +173,13 @@ hipError_t launch_select_range(const DevProblem& dp, const HostPlan& hp, int r0,
 hipError_t launch_select_side(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
                               const float* scores, float* pooled, int32_t* kept,
                               hipStream_t s);
+// Selection and fresh-page compaction of every request in one kernel (one workgroup per
+// segment; the rewrite of a request by its last workgroup): the results of launch_select
+// then launch_compact.
+hipError_t launch_select_compact(const DevProblem& dp, const HostPlan& hp, const float* scores,
+                                 float* pooled, int32_t* kept, void* kv, int32_t* bt,
+                                 const int32_t* free_pages, int32_t* freed, int32_t* new_lens,
+                                 hipStream_t s);
 // LRFU selection (attention-aware keep scores): segments up to kLrfuMaxLen entries; those
 // longer than kLrfuLdsLen only with pooling windows up to kLrfuRegMaxWindow.
 constexpr int64_t kLrfuLdsLen = 38400;

@@ -98,6 +98,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
       p.lse_blocks = lse_blocks; p.seg_off = seg_off; p.lse_part_off = l_off;
       p.ip_freed_off = (int32_t)f_off;
       dp.plan[r] = p;
+      dp.req_done[r] = 0;
       // kept offsets per (r, h)
       int64_t ko = k_off;
       for (int h0 = 0; h0 < Hkv; h0 += 8) {

@@ -629,6 +629,28 @@ __device__ __forceinline__ void select_global(int L, int k, int hw, const float*
   }
 }
 
+// The selection of segment (r, h): pooled scores and kept indices.  Returns k.
+__device__ __forceinline__ int select_segment(const DevProblem& dp, const ReqPlan& pl, int r,
+                                              int h, const float* __restrict__ scores,
+                                              float* pooled, int32_t* __restrict__ kout,
+                                              uint32_t* lds_keys, uint32_t* hist,
+                                              int64_t* scan_tmp, uint32_t* mm_tmp, int* s_bin,
+                                              uint32_t* s_above) {
+  const int L = pl.L;
+  const int b = dp.budgets[r * dp.Hkv + h];
+  const int k = b < L ? b : L;
+  const float* in = scores + pl.seg_off + (int64_t)h * L;
+  float* pout = pooled + pl.seg_off + (int64_t)h * L;
+  const int hw = dp.pool_window / 2;
+  if (L <= kSelectLdsKeys)
+    select_lds(L, k, hw, in, pout, kout, lds_keys, hist, scan_tmp, mm_tmp, s_bin, s_above);
+  else if (L <= kSelectRegKeys && hw <= kPoolHalo)
+    select_regs(L, k, hw, in, pout, kout, lds_keys, hist, scan_tmp, mm_tmp, s_bin, s_above);
+  else
+    select_global(L, k, hw, in, pout, kout, hist, scan_tmp, s_bin, s_above);
+  return k;
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp, int r0,
@@ -643,21 +665,119 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp, i
   __shared__ int s_bin;
   __shared__ uint32_t s_above;
 
-  const int h = blockIdx.x, r = r0 + (int)blockIdx.y, Hkv = dp.Hkv;
+  const int h = blockIdx.x, r = r0 + (int)blockIdx.y;
   const ReqPlan pl = dp.plan[r];
-  const int L = pl.L;
-  const int b = dp.budgets[r * Hkv + h];
-  const int k = b < L ? b : L;
-  const float* in = scores + pl.seg_off + (int64_t)h * L;
-  float* pout = pooled + pl.seg_off + (int64_t)h * L;
+  select_segment(dp, pl, r, h, scores, pooled, kept + dp.kept_off[r * dp.Hkv + h], lds_keys,
+                 hist, scan_tmp, mm_tmp, &s_bin, &s_above);
+}
+
+// ---- selection and fresh-page compaction in one kernel (small problems) ------------------
+//
+// One 1024-thread workgroup per (request, KV head) selects the segment as select_kernel does,
+// then copies its own head's kept K and V rows to their fresh slots (new slot j of head h is
+// row (j % 16, h) of fresh page j / 16: the heads of a page are disjoint rows, so the
+// workgroups of a request never write the same bytes), and writes the head's new length.
+// The block-table rewrite of a request must follow every read of its old row, so it falls to
+// the request's last workgroup to finish: each workgroup counts itself in a per-request
+// counter once its reads are done, and the one that completes the count rewrites the row
+// and the freed list and sets the counter back to zero for the next launch (the plan kernel
+// zeroes the counters too).  Nothing waits on another workgroup.  Results equal
+// select_kernel then the fresh-page compaction, bit for bit; used where the whole
+// compaction is small enough that a single workgroup per segment copies it faster than the
+// separate launches would (one launch instead of three).
+constexpr int kFusedRows = kSelectThreads;   // destination slots resolved per chunk
+constexpr int kFusedBatch = 8;               // 16-byte loads of a thread in flight together
+// LDS the copy tables overlay on the selection's dynamic LDS: source and destination row
+// of every slot of a chunk.
+constexpr size_t kFusedLdsBytes = 2 * sizeof(int64_t) * kFusedRows;
+
+__global__ __launch_bounds__(kSelectThreads) void select_compact_kernel(
+    DevProblem dp, const float* __restrict__ scores, float* pooled, int32_t* __restrict__ kept,
+    uint16_t* kv, int32_t* bt, const int32_t* __restrict__ free_pages,
+    int32_t* __restrict__ freed, int32_t* __restrict__ new_lens) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
+  extern __shared__ uint32_t lds_keys[];
+  __shared__ uint32_t hist[kMaxBins];
+  __shared__ int64_t scan_tmp[17];
+  __shared__ uint32_t mm_tmp[32];
+  __shared__ int s_bin;
+  __shared__ uint32_t s_above;
+  __shared__ int s_last;
+
+  const int tid = threadIdx.x;
+  const int h = blockIdx.x, r = blockIdx.y, Hkv = dp.Hkv, D = dp.D;
+  const ReqPlan pl = dp.plan[r];
   int32_t* kout = kept + dp.kept_off[r * Hkv + h];
-  const int hw = dp.pool_window / 2;
-  if (L <= kSelectLdsKeys)
-    select_lds(L, k, hw, in, pout, kout, lds_keys, hist, scan_tmp, mm_tmp, &s_bin, &s_above);
-  else if (L <= kSelectRegKeys && hw <= kPoolHalo)
-    select_regs(L, k, hw, in, pout, kout, lds_keys, hist, scan_tmp, mm_tmp, &s_bin, &s_above);
-  else
-    select_global(L, k, hw, in, pout, kout, hist, scan_tmp, &s_bin, &s_above);
+  const int k = select_segment(dp, pl, r, h, scores, pooled, kout, lds_keys, hist, scan_tmp,
+                               mm_tmp, &s_bin, &s_above);
+  if (tid == 0) new_lens[r * Hkv + h] = pl.skip ? pl.L : k;
+  if (pl.skip) return;   // every head keeps everything: the request is left as it is
+  __syncthreads();   // the kept indices written above are visible to the workgroup
+
+  // ---- copies: chunks of kFusedRows new slots, resolved to (source, destination) rows in
+  // LDS, then moved in 16-byte pieces (K plane, then V plane)
+  int64_t* src_row = reinterpret_cast<int64_t*>(lds_keys);
+  int64_t* dst_row = src_row + kFusedRows;
+  const int CH = D / 8;
+  const int64_t plane = dp.num_pages * kPageSize * Hkv * (int64_t)D;   // K -> V, elements
+  const int32_t* bt_row = bt + (int64_t)r * dp.bt_stride;
+#pragma unroll 1
+  for (int j0 = 0; j0 < k; j0 += kFusedRows) {
+    const int nj = k - j0 < kFusedRows ? k - j0 : kFusedRows;
+    if (tid < nj) {
+      const int j = j0 + tid;
+      const int t = kout[j];
+      int64_t src = -1, dst = -1;
+      if (t >= 0 && t < pl.L) {
+        const int64_t page = bt_row[t / kPageSize];
+        // pages outside the pool are never dereferenced (the slot is left unwritten)
+        if (page >= 0 && page < dp.num_pages) src = (page * kPageSize + t % kPageSize) * Hkv + h;
+      }
+      const int64_t dpg = free_pages[pl.fresh_off + j / kPageSize];
+      if (dpg >= 0 && dpg < dp.num_pages) dst = (dpg * kPageSize + j % kPageSize) * Hkv + h;
+      src_row[tid] = dst >= 0 ? src : -1;
+      dst_row[tid] = dst;
+    }
+    __syncthreads();
+    const int items = 2 * nj * CH;
+#pragma unroll 1
+    for (int base = 0; base < items; base += kSelectThreads * kFusedBatch) {
+      u32x4 v[kFusedBatch];
+      int64_t to[kFusedBatch];
+#pragma unroll
+      for (int u = 0; u < kFusedBatch; ++u) {
+        to[u] = -1;
+        const int it = base + u * kSelectThreads + tid;
+        if (it >= items) continue;
+        const int ch = it % CH, rest = it / CH;
+        const int jj = rest % nj, which = rest / nj;
+        const int64_t sr = src_row[jj];
+        if (sr < 0) continue;
+        to[u] = which * plane + dst_row[jj] * D + ch * 8;
+        v[u] = *reinterpret_cast<const u32x4*>(kv + which * plane + sr * D + ch * 8);
+      }
+#pragma unroll
+      for (int u = 0; u < kFusedBatch; ++u)
+        if (to[u] >= 0) *reinterpret_cast<u32x4*>(kv + to[u]) = v[u];
+    }
+    __syncthreads();   // the tables are rewritten by the next chunk
+  }
+
+  // ---- the request's last workgroup rewrites its block-table row and freed list
+  if (tid == 0) {
+    __threadfence();   // this workgroup's reads of the old row are done
+    s_last = atomicAdd(&dp.req_done[r], 1) == Hkv - 1;
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  int32_t* row = bt + (int64_t)r * dp.bt_stride;
+  for (int i = tid; i < pl.Y; i += kSelectThreads) {
+    const int32_t old = row[i];
+    freed[pl.freed_off + i] = old;
+    row[i] = i < pl.X ? free_pages[pl.fresh_off + i] : -1;
+  }
+  if (tid == 0) dp.req_done[r] = 0;   // ready for the next launch on this workspace
 }
 
 // ---- the same selection beside a running scoring kernel ----------------------------------
@@ -1204,6 +1324,25 @@ hipError_t launch_select_range(const DevProblem& dp, const HostPlan& hp, int r0,
 hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* scores,
                          float* pooled, int32_t* kept, hipStream_t s) {
   return launch_select_range(dp, hp, 0, hp.R, scores, pooled, kept, s);
+}
+
+hipError_t launch_select_compact(const DevProblem& dp, const HostPlan& hp, const float* scores,
+                                 float* pooled, int32_t* kept, void* kv, int32_t* bt,
+                                 const int32_t* free_pages, int32_t* freed, int32_t* new_lens,
+                                 hipStream_t s) {
+  if (hp.R == 0) return hipSuccess;
+  const int64_t keys = hp.max_L < kSelectLdsKeys ? hp.max_L : kSelectLdsKeys;
+  size_t lds = (size_t)(keys + kLdsPad) * sizeof(uint32_t);
+  if (lds < kFusedLdsBytes) lds = kFusedLdsBytes;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void*)select_compact_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(select_compact_kernel, dim3(hp.Hkv, hp.R), dim3(kSelectThreads), lds, s,
+                     dp, scores, pooled, kept, static_cast<uint16_t*>(kv), bt, free_pages, freed,
+                     new_lens);
+  return hipGetLastError();
 }
 
 hipError_t launch_select_side(const DevProblem& dp, const HostPlan& hp, int r0, int r1,

@@ -142,6 +142,30 @@ def test_compact_and_select_validate_before_launching():
     assert lib.actkv_lse(None, FAKE, FAKE, FAKE, FAKE, FAKE, ws, None) == -1
 
 
+def test_select_compact_validates_before_launching():
+    """actkv_select_compact refuses, before any launch: a short free list, scores given as
+    pooled, a missing score array, block table or new_lens, a negative free count and a
+    small workspace."""
+    lib = actkv.load_library()
+    p = _tiny()
+    c = p.cstruct()
+    c.seq_lens_d = c.q_lens_d = c.budgets_d = FAKE
+    q = actkv.query(p)
+    ws, need = q["workspace_bytes"], q["fresh_pages_needed"]
+
+    def call(scores=FAKE, pooled=None, bt=FAKE, num_free=1000, new_lens=FAKE, ws_bytes=ws):
+        return lib.actkv_select_compact(ctypes.byref(c), scores, pooled, None, FAKE, bt, FAKE,
+                                        num_free, FAKE, new_lens, FAKE, ws_bytes, None)
+
+    assert call(num_free=need - 1) == -4
+    assert call(pooled=FAKE) == -1
+    assert call(scores=None) == -1
+    assert call(bt=None) == -1
+    assert call(new_lens=None) == -1
+    assert call(num_free=-1) == -1
+    assert call(ws_bytes=ws - 1) == -3
+
+
 def test_lrfu_entry_points_validate_before_launching():
     lib = actkv.load_library()
     p = _tiny()
