@@ -420,6 +420,35 @@ actkv_status actkv_budget_update(const float* token_conf, const int64_t* offsets
                                  int32_t* retained, void* stream);
 
 /* Static text for a status code. */
+/*
+ * Device-side check of what the fresh-page compaction takes on trust (the caller's
+ * guarantee to actkv_compact and actkv_step: the copies of Sec. 7.2 are conflict-free only
+ * when no page written is one that is read).  On `stream`, with the device mirrors of `p`:
+ *   ACTKV_CHECK_MIRRORS     the device seq_lens, q_lens or budgets differ from the host ones
+ *                           (compared through a 64-bit checksum of each array);
+ *   ACTKV_CHECK_TABLE_RANGE an entry bt[r, 0 .. ceil(L_r / page_size)) lies outside
+ *                           [0, num_pages);
+ *   ACTKV_CHECK_FREE_RANGE  one of the pages the step would take, free_pages[0 ..
+ *                           fresh_pages_needed), lies outside [0, num_pages);
+ *   ACTKV_CHECK_FRESH_LIVE  one of them is live (appears in such a block-table entry);
+ *   ACTKV_CHECK_FRESH_DUP   one of them appears twice.
+ * The bits found are OR-ed into *status (device, uint32, set to 0 first); 0 means all of
+ * it holds.  scratch: device memory of at least ACTKV_CHECK_SCRATCH_BYTES(num_pages) bytes
+ * (two page bitmaps), overwritten.  Host errors as for actkv_compact (OUT_OF_PAGES when
+ * num_free < fresh_pages_needed; WORKSPACE_TOO_SMALL for a short scratch), nothing enqueued
+ * then.  The kernels only read the problem's arrays and never index with a page they have
+ * not range-checked, so any content of them is safe to check.
+ */
+#define ACTKV_CHECK_MIRRORS 1u
+#define ACTKV_CHECK_TABLE_RANGE 2u
+#define ACTKV_CHECK_FREE_RANGE 4u
+#define ACTKV_CHECK_FRESH_LIVE 8u
+#define ACTKV_CHECK_FRESH_DUP 16u
+#define ACTKV_CHECK_SCRATCH_BYTES(num_pages) (8u * (((size_t)(num_pages) + 31u) / 32u))
+actkv_status actkv_check_pages(const actkv_problem* p, const int32_t* block_table,
+                               const int32_t* free_pages, int64_t num_free, uint32_t* status,
+                               void* scratch, size_t scratch_bytes, void* stream);
+
 const char* actkv_status_str(actkv_status status);
 
 #ifdef __cplusplus

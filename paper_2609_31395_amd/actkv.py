@@ -46,6 +46,14 @@ class CProblem(ctypes.Structure):
 FLAG_PLANNED = 1   # ACTKV_FLAG_PLANNED: the workspace already holds this problem's plan
 FLAG_SMALL_SELECT = 2   # ACTKV_FLAG_SMALL_SELECT: selection on the small-footprint kernel
 MAX_OVERLAP_GROUPS = 8   # ACTKV_MAX_OVERLAP_GROUPS
+# actkv_check_pages status bits
+CHECK_MIRRORS, CHECK_TABLE_RANGE, CHECK_FREE_RANGE, CHECK_FRESH_LIVE, CHECK_FRESH_DUP = (
+    1, 2, 4, 8, 16)
+
+
+def check_scratch_bytes(num_pages: int) -> int:
+    """ACTKV_CHECK_SCRATCH_BYTES: two page bitmaps."""
+    return 8 * ((int(num_pages) + 31) // 32)
 
 
 _lib = None
@@ -91,6 +99,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
               "actkv_token_confidence_workspace", "actkv_token_confidence",
               "actkv_budget_update"):
         getattr(lib, f).restype = ctypes.c_int
+    lib.actkv_check_pages.argtypes = [P, vp, vp, i64, vp, vp, sz, vp]
+    lib.actkv_check_pages.restype = ctypes.c_int
     lib.actkv_set_overlap.argtypes = [i32]
     lib.actkv_set_overlap.restype = ctypes.c_int
     lib.actkv_get_overlap.argtypes = []
@@ -744,6 +754,32 @@ def budget_update(token_conf: torch.Tensor, offsets: np.ndarray, budgets: torch.
         _ptr(slopes), _ptr(thr), _ptr(kept), _stream(stream)))
     return dict(budgets=out[:R], slopes=slopes[:R], thresholds=thr[:R], retained=kept[:R],
                 _keep=off_d)
+
+
+def check_pages(p: Problem, block_table: torch.Tensor, free_pages: Optional[torch.Tensor],
+                status: Optional[torch.Tensor] = None, scratch: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    """actkv_check_pages: the compaction's preconditions checked on the device.  Returns the
+    one-element int32 status tensor (0: everything holds; else CHECK_* bits), valid once the
+    stream gets there."""
+    lib = load_library()
+    z = _Sizes(p)
+    z.need("block_table", block_table, _I32, z.bt)
+    if free_pages is not None or z.fresh:
+        z.need("free_pages", free_pages, _I32, z.fresh)
+    z.need("status", status, _I32, 1, required=False)
+    if scratch is not None:
+        z.need("scratch", scratch, (torch.uint8,), check_scratch_bytes(p.num_pages))
+    z.check_ws(None)
+    dev = block_table.device
+    if status is None:
+        status = torch.empty(1, dtype=torch.int32, device=dev)
+    if scratch is None:
+        scratch = torch.empty(check_scratch_bytes(p.num_pages), dtype=torch.uint8, device=dev)
+    _check("actkv_check_pages", lib.actkv_check_pages(
+        ctypes.byref(p.cstruct()), _ptr(block_table), _ptr(free_pages), _numel(free_pages),
+        _ptr(status), _ptr(scratch), _numel(scratch), _stream(stream)))
+    return status
 
 
 def set_overlap(groups: int) -> None:

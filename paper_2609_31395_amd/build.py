@@ -20,7 +20,7 @@ LIB = os.path.join(PKG, "libactkv.so")
 ARCH = "gfx950"
 
 SOURCES = ["api.cpp", "plan.hip", "score.hip", "select.hip", "compact.hip", "confidence.hip",
-           "noalloc.hip"]
+           "noalloc.hip", "check.hip"]
 HEADERS = ["actkv_internal.h", "device_common.hpp"]
 
 # Packed fp32 VALU forms are turned off for all device code; the host pass of hipcc warns

@@ -132,6 +132,22 @@ struct DevProblem {
 };
 
 
+// Page and mirror check (actkv_check_pages): one term of the order-dependent checksum of a
+// mirrored array (sum over i of term(i, v[i]), modulo 2^64), the same on host and device.
+__host__ __device__ inline uint64_t mirror_term(int64_t i, int32_t v) {
+  return (uint64_t)(uint32_t)v * (0x9E3779B97F4A7C15ull * (uint64_t)(i + 1));
+}
+// 32-bit words of one page bitmap.
+__host__ __device__ inline int64_t check_bitmap_words(int64_t num_pages) {
+  return (num_pages + 31) / 32;
+}
+// The check's kernels; scratch holds two bitmaps of check_bitmap_words(num_pages) words.
+hipError_t launch_check_pages(const int32_t* seq_lens, const int32_t* q_lens,
+                              const int32_t* budgets, int R, int Hkv, const int32_t* bt,
+                              int bt_stride, int64_t num_pages, const int32_t* free_pages,
+                              int64_t n_fresh, const uint64_t want[3], uint32_t* status,
+                              uint32_t* scratch, hipStream_t s);
+
 // The whole step (actkv_step) on a caller-chosen workspace: validation, planning and the
 // launches of every stage.  actkv_step_noalloc passes its static scratch array and
 // may_overlap = false (the overlapped form creates a stream and events on first use).

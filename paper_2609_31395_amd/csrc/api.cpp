@@ -610,6 +610,31 @@ actkv_status actkv_step(const actkv_problem* p, const void* q, void* kv_cache,
                           kept, freed_pages, new_lens, workspace, workspace_bytes, stream, true);
 }
 
+actkv_status actkv_check_pages(const actkv_problem* p, const int32_t* block_table,
+                               const int32_t* free_pages, int64_t num_free, uint32_t* status,
+                               void* scratch, size_t scratch_bytes, void* stream) {
+  HostPlan hp;
+  actkv_status st = plan_host(p, &hp);
+  if (st != ACTKV_OK) return st;
+  if (!status || !scratch || num_free < 0) return ACTKV_ERR_INVALID_ARGUMENT;
+  if (hp.R > 0 && (!p->seq_lens_d || !p->q_lens_d || !p->budgets_d || !block_table))
+    return ACTKV_ERR_INVALID_ARGUMENT;
+  if (scratch_bytes < ACTKV_CHECK_SCRATCH_BYTES(p->num_pages)) return ACTKV_ERR_WORKSPACE_TOO_SMALL;
+  if (num_free < hp.fresh_needed) return ACTKV_ERR_OUT_OF_PAGES;
+  if (hp.fresh_needed > 0 && !free_pages) return ACTKV_ERR_INVALID_ARGUMENT;
+  uint64_t want[3] = {0, 0, 0};
+  for (int r = 0; r < hp.R; ++r) {
+    want[0] += actkv::mirror_term(r, p->seq_lens_h[r]);
+    want[1] += actkv::mirror_term(r, p->q_lens_h[r]);
+  }
+  for (int64_t i = 0; i < (int64_t)hp.R * hp.Hkv; ++i)
+    want[2] += actkv::mirror_term(i, p->budgets_h[i]);
+  return hip_status(actkv::launch_check_pages(
+      p->seq_lens_d, p->q_lens_d, p->budgets_d, hp.R, hp.Hkv, block_table, p->bt_stride,
+      p->num_pages, free_pages, hp.fresh_needed, want, status, static_cast<uint32_t*>(scratch),
+      static_cast<hipStream_t>(stream)));
+}
+
 actkv_status actkv_set_overlap(int32_t groups) {
   if (groups < 0 || groups > ACTKV_MAX_OVERLAP_GROUPS) return ACTKV_ERR_INVALID_ARGUMENT;
   g_overlap.store(groups, std::memory_order_relaxed);

@@ -166,6 +166,33 @@ def test_select_compact_validates_before_launching():
     assert call(ws_bytes=ws - 1) == -3
 
 
+def test_check_pages_validates_before_launching():
+    """actkv_check_pages refuses, before any launch: a missing status or scratch, a short
+    scratch, a short free list, a negative free count, missing device mirrors."""
+    lib = actkv.load_library()
+    p = _tiny()
+    c = p.cstruct()
+    c.seq_lens_d = c.q_lens_d = c.budgets_d = FAKE
+    q = actkv.query(p)
+    need = actkv.check_scratch_bytes(p.num_pages)
+
+    def call(status=FAKE, scratch=FAKE, nbytes=need, num_free=1000, cs=c):
+        return lib.actkv_check_pages(ctypes.byref(cs), FAKE, FAKE, num_free, status, scratch,
+                                     nbytes, None)
+
+    assert call(status=None) == -1
+    assert call(scratch=None) == -1
+    assert call(nbytes=need - 1) == -3
+    assert call(num_free=q["fresh_pages_needed"] - 1) == -4
+    assert call(num_free=-1) == -1
+    assert call(cs=_tiny().cstruct()) == -1   # no device mirrors
+
+
+def test_check_scratch_size_matches_the_header():
+    for n in (1, 31, 32, 33, 4_200_000):
+        assert actkv.check_scratch_bytes(n) == 8 * ((n + 31) // 32)
+
+
 def test_lrfu_entry_points_validate_before_launching():
     lib = actkv.load_library()
     p = _tiny()
