@@ -8,22 +8,23 @@
 // accumulation; the exp2 / add epilogue runs on the VALU.
 //
 // Kernel layout (score_kernel):
-//   * One workgroup of 4 waves per CU (one wave per SIMD), persistent: the list of
-//     (segment, 64-key tile) work, segment = (request, row chunk of up to 512 query rows,
-//     KV head), is cut into equal-cost contiguous ranges, one per workgroup, so ragged
-//     lengths and query counts stay balanced and Q is loaded once per segment.
-//   * Each wave holds 8 row tiles of 16 query rows in registers (v_mfma_f32_16x16x32_bf16
-//     A operand) and the beta of its rows.  Every wave reads each K tile from LDS once per
-//     sub-tile, so the LDS read traffic per tile is (waves x tile bytes): four waves of 128
-//     rows read half of what eight waves of 64 rows would.  K tiles (64 keys, 4 pages) are gathered
-//     through the block table straight into LDS (global_load_lds_dwordx4, 16 bytes per
-//     lane, chunk-swizzled rows), kScoreStages - 1 tiles ahead, one barrier per tile.
-//   * The MFMA chains and the exp2 epilogue are software-pipelined inside each wave (see
-//     the sweep below): the VALU works on one 16x16 unit while the matrix core works on
-//     another.
+//   * One workgroup of 8 waves per CU (two per SIMD), persistent: the list of (segment,
+//     64-key tile) work, segment = (request, row chunk of up to 512 query rows, KV head), is
+//     cut into equal-cost contiguous ranges, one per workgroup, so ragged lengths and query
+//     counts stay balanced and Q is loaded once per segment.
+//   * Each wave holds 4 row tiles of 16 query rows in registers (v_mfma_f32_16x16x32_bf16 A
+//     operand) and the beta of its rows.  K tiles (64 keys, 4 pages) are gathered through
+//     the block table straight into LDS (global_load_lds_dwordx4, 16 bytes per lane,
+//     chunk-swizzled rows), three tiles ahead, one barrier per tile; every wave reads each
+//     16-key sub-tile as its MFMA B operand.
+//   * Two waves share each SIMD.  On gfx950 a wave gains little from mixing its own MFMA
+//     chains and exp2 epilogue (measured with register-only probes: 68 ns per 16x16x128
+//     unit and SIMD for one wave, 50 ns for two), so the overlap of the matrix core and the
+//     VALU comes from the pair: while one wave waits on its chain, an exp2 or an LDS read,
+//     the other issues.
 //   * A lane's accumulator column is one key and 4 query rows, so the row sum is in-lane;
-//     the 4 lane groups and 4 waves are combined through LDS in a fixed order (no
-//     atomics: deterministic, and independent of where the pages physically live).
+//     the 4 lane groups and 8 waves are combined through LDS in a fixed order (no atomics:
+//     deterministic, and independent of where the pages physically live).
 #include <atomic>
 
 #include "device_common.hpp"
@@ -32,13 +33,7 @@ namespace actkv {
 
 namespace {
 
-// Scoring: 4 waves per workgroup (one per SIMD, up to 512 registers each), 128 query rows
-// per wave, one workgroup per CU.  Every wave reads the whole K tile from LDS, so fewer,
-// taller waves read less: LDS traffic, not arithmetic, bounded the 8-wave form.
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
-constexpr int kScoreStages = 4;   // K tiles resident in LDS for scoring (three in flight)
-constexpr int kStages = 3;        // the same for the LSE pass
+constexpr int kStages = 3;   // K tiles resident in LDS for the LSE pass
 // The LSE pass keeps 8 waves x 2 row tiles (its per-row running max/sum stay in registers).
 constexpr int kLseThreads = 512;
 constexpr int kLseWaves = kLseThreads / 64;
@@ -48,7 +43,8 @@ constexpr int kLseTilesPerWave = kRowsPerChunk / 32 / kLseWaves;
 // instead the 16-byte chunk c of row r sits in slot c ^ (r % kChunks), which keeps both
 // the direct-to-LDS loads (64 lanes write one contiguous KiB) and the MFMA operand reads
 // (lanes l and l+1 read rows r, r+1 at the same logical chunk) free of bank conflicts.
-template <int D, int W = kWaves>
+// W is the number of waves that share a tile's loads; the row geometry does not depend on it.
+template <int D, int W = 8>
 struct TileGeom {
   static constexpr int kSteps = D / 16;                  // MFMA k-steps per row
   static constexpr int kRowBytes = D * 2;
@@ -203,95 +199,23 @@ __device__ __forceinline__ int chunk_row_tiles(int M, int c) {
 
 }  // namespace
 
-// ---- scoring: software-pipelined 16x16x32 MFMA units -----------------------------------
+// ---- scoring: 16x16x32 MFMA units on two waves per SIMD --------------------------------
 //
-// A wave owns kRowTilesPerWave row tiles of 16 query rows (the MFMA A operand, held in
-// registers for the whole segment).  Each 64-key tile in LDS is cut into 4 sub-tiles of 16
-// keys (the B operand).  A "unit" is one (sub-tile, row tile) pair: kSteps16 dependent
-// MFMAs into a 16x16 accumulator -- lane l holds key l%16 and rows 4*(l/16) .. +3 -- and
-// then its epilogue: exp2 of the 4 elements, summed (or max-reduced over the GQA group)
-// into the lane's partial for that key.
-//
-// Phase g issues the chain of unit g one MFMA per slot and, between those MFMAs, the
-// epilogue of unit g - 2, whose accumulator was finished a whole phase earlier.  The two
-// are independent, so the VALU works on one unit while the matrix core works on the other.
-// The K operand of a sub-tile is read from LDS kOperandAhead sub-tiles before its first
-// chain (rotating operand buffers), so the reads' latency is hidden behind that many
-// sub-tiles of work (LDS reads queue behind the K tiles' direct-to-LDS writes).
+// A wave owns 4 row tiles of 16 query rows (the MFMA A operand, held in registers for the
+// whole segment).  Each 64-key tile in LDS is cut into 4 sub-tiles of 16 keys (the B
+// operand).  A "unit" is one (sub-tile, row tile) pair: kSteps dependent MFMAs into a 16x16
+// accumulator -- lane l holds key l%16 and rows 4*(l/16) .. +3 -- and then its epilogue:
+// exp2 of the 4 elements, summed (or max-reduced over the GQA group) into the lane's
+// partial for that key.
 
 constexpr int kRowTile = 16;
-constexpr int kRowTilesPerWave = kRowsPerChunk / kRowTile / kWaves;   // 8
-constexpr int kSubTiles = kKeyTile / 16;                              // 4
-static_assert(kRowTilesPerWave == 8 && kSubTiles == 4, "unit bookkeeping below");
-// Sub-tiles of lookahead of the operand reads, and the buffers they rotate through (sub-tile
-// s of every tile uses buffer s % kOperandBufs, so the count divides the sub-tiles).
-constexpr int kOperandAhead = 2;
-constexpr int kOperandBufs = 4;
-static_assert(kOperandAhead >= 1 && kOperandAhead <= 2 && kOperandBufs > kOperandAhead &&
-                  kSubTiles % kOperandBufs == 0,
-              "a chain in the next tile (units 0 and 1) reads ahead within that tile");
+constexpr int kSubTiles = kKeyTile / 16;   // 4
+static_assert(kSubTiles == 4, "unit bookkeeping below");
 
 template <int D>
 struct Geom16 {
   static constexpr int kSteps = D / 32;   // k-steps of 32 per head
 };
-
-// Query row at (row tile T = w + kWaves * rt, tile row mm) of row chunk c.  The natural
-// order m = j * G + g is used unless the group max of MAX_MEAN needs a query's G = 8 or 16
-// heads in one lane: then they sit at the same lane position of 2 or 4 consecutive row
-// tiles of the wave (heads 4*(rt % 2) + i, resp. 4*(rt % 4) + i).
-__device__ __forceinline__ void score_row_query(int G, bool grouped, int c, int T, int mm,
-                                                int* j, int* g) {
-  if (!grouped) {
-    const int m = c * kRowsPerChunk + T * kRowTile + mm;
-    *j = m / G;
-    *g = m % G;
-    return;
-  }
-  const int w = T % kWaves, rt = T / kWaves, a = mm >> 2, i = mm & 3;
-  if (G == 8) {
-    *j = c * (kRowsPerChunk / 8) + (rt >> 1) * (4 * kWaves) + w * 4 + a;
-    *g = 4 * (rt & 1) + i;
-  } else {
-    *j = c * (kRowsPerChunk / 16) + (rt >> 2) * (4 * kWaves) + w * 4 + a;
-    *g = 4 * (rt & 3) + i;
-  }
-}
-
-// Row tiles per wave that can hold real rows of chunk c (the same for every wave).
-__device__ __forceinline__ int chunk_wave_tiles(int G, bool grouped, int n, int c) {
-  if (!grouped) {
-    const int rows = G * n - c * kRowsPerChunk;
-    if (rows <= 0) return 1;
-    const int r = rows < kRowsPerChunk ? rows : kRowsPerChunk;
-    return ceil_div(r, kRowTile * kWaves);
-  }
-  // row tiles come in groups of G / 4 (one group: 4 queries per wave)
-  const int per = G / 4, qn = n - c * (kRowsPerChunk / G);
-  const int groups = qn <= 0 ? 1 : ceil_div(qn, 4 * kWaves);
-  const int t = groups * per;
-  return t < kRowTilesPerWave ? t : kRowTilesPerWave;
-}
-
-// Row tile rt of this wave as the 16x16x32 A operand: lane l holds row l%16 with head-dim
-// elements 32*ks + 8*(l/16) .. +8; rows past n are zero.
-template <int D>
-__device__ __forceinline__ void load_q16(bf16x8 (&qr)[Geom16<D>::kSteps],
-                                         const uint16_t* __restrict__ q, int G, bool grouped,
-                                         int Hq, int h, int q_off, int n, int c, int T) {
-  const int lane = threadIdx.x & 63;
-  int j, g;
-  score_row_query(G, grouped, c, T, lane & 15, &j, &g);
-  if (j < n) {
-    const uint16_t* src = q + ((int64_t)(q_off + j) * Hq + h * G + g) * D + (lane >> 4) * 8;
-#pragma unroll
-    for (int ks = 0; ks < Geom16<D>::kSteps; ++ks)
-      qr[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + ks * 32));
-  } else {
-#pragma unroll
-    for (int ks = 0; ks < Geom16<D>::kSteps; ++ks) qr[ks] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
-  }
-}
 
 // LDS offset of this lane's B-operand chunk for k-step ks of sub-tile 0 (sub-tile s is
 // 16 rows further).  Row r = l%16 holds chunk c = 4 ks + l/16 at slot c ^ (r % kChunks):
@@ -317,110 +241,6 @@ __device__ __forceinline__ bf16x8 lds_k16(const char* tile_buf, int sub, const K
   return as_bf16x8(*reinterpret_cast<const u32x4*>(tile_buf + sub * 16 * TileGeom<D>::kRowBytes + off));
 }
 
-// Per-wave state carried from phase to phase.
-template <int D>
-struct Pipe16 {
-  f32x4 c1, c2;                       // accumulators of units g-1 and g-2
-  bf16x8 kb[kOperandBufs][Geom16<D>::kSteps];   // B operands: sub-tile s reads kb[s % bufs]
-  float part[4];                      // the lane's partials of the current sub-tile, one per
-                                      // accumulator element (independent add chains)
-  float ex;                           // SUM: the last exp2 result, added one slot later
-  float mx;                           // MAX_MEAN, G = 8 / 16: running group max
-};
-
-// One phase.  kChain: chain of row tile q against operand kr.  kEpi: epilogue of st.c2 for
-// row tile kRt (beta bt, causal positions at prow, key `key`).  kLoad: kl <- the operand of
-// sub-tile next_sub of next_buf (read from LDS here, used a whole sub-tile later).
-template <int D, bool kMaxMean, bool kMask, bool kChain, bool kEpi, bool kLoad, int kRt>
-__device__ __forceinline__ void score_phase16(Pipe16<D>& st, const bf16x8 (&q)[Geom16<D>::kSteps],
-                                              const bf16x8 (&kr)[Geom16<D>::kSteps],
-                                              bf16x8 (&kl)[Geom16<D>::kSteps],
-                                              const KRead16& rp, const char* next_buf, int next_sub,
-                                              const float (&bt)[4], const int32_t* prow, int key,
-                                              float alpha, int G) {
-  constexpr int S = Geom16<D>::kSteps;
-  constexpr int EPS = 4 / S;   // epilogue elements per MFMA slot
-  f32x4 prev = st.c2;
-  int pt[4] = {0, 0, 0, 0};
-  if (kEpi && kMask) {
-    const int4 p4 = *reinterpret_cast<const int4*>(prow);
-    pt[0] = p4.x; pt[1] = p4.y; pt[2] = p4.z; pt[3] = p4.w;
-  }
-  if (kLoad) {
-#pragma unroll
-    for (int ks = 0; ks < S; ++ks) kl[ks] = lds_k16<D>(next_buf, next_sub, rp, ks);
-  }
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int ks = 0; ks < S; ++ks) {
-    if (kChain) acc = mfma16(q[ks], kr[ks], acc);
-    if (kEpi) {
-#pragma unroll
-      for (int v = ks * EPS; v < (ks + 1) * EPS; ++v) {
-        float x = __builtin_fmaf(prev[v], alpha, -bt[v]);
-        if (kMask) x = key > pt[v] ? -__builtin_inff() : x;   // exp2(-inf) = 0
-        if (!kMaxMean) {
-          // the previous element's exp2 is added now, off the exp2 latency path
-          st.part[(v + 3) & 3] += st.ex;
-          st.ex = fast_exp2(x);
-        } else {
-          prev[v] = fast_exp2(x);
-        }
-      }
-    }
-  }
-  // one scheduling region per phase: the compiler interleaves the chain and the epilogue
-  __builtin_amdgcn_sched_barrier(0);
-  if (kEpi && kMaxMean) {
-    const float m01 = fmaxf(prev[0], prev[1]), m23 = fmaxf(prev[2], prev[3]);
-    if (G == 1) {
-      st.part[0] += (prev[0] + prev[1]) + (prev[2] + prev[3]);
-    } else if (G == 2) {
-      st.part[0] += m01 + m23;
-    } else if (G == 4) {
-      st.part[0] += fmaxf(m01, m23);
-    } else if (G == 8) {
-      // heads 0-3 in even row tiles, 4-7 in the next one
-      const float m = fmaxf(m01, m23);
-      if (kRt & 1) st.part[0] += fmaxf(st.mx, m); else st.mx = m;
-    } else {
-      // G == 16: heads 4*(rt%4) .. +3 in row tile rt, four row tiles per query group
-      const float m = fmaxf(m01, m23);
-      st.mx = (kRt & 3) == 0 ? m : fmaxf(st.mx, m);
-      if ((kRt & 3) == 3) st.part[0] += st.mx;
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  st.c2 = st.c1;
-  if (kChain) st.c1 = acc;
-}
-
-// Everything the key sweep of one segment needs besides the register-resident Q and beta.
-struct SweepCtx {
-  const char* kv_bytes;
-  const int32_t* bt_row;
-  const int32_t* pos_s;    // LDS: causal position of every row of the chunk
-  __amdgpu_buffer_rsrc_t out;   // scores (or chunk partials) of this (request, KV head):
-                                // exactly L floats, stores past them are dropped
-  const char* kbuf;        // LDS: the K stages
-  int64_t page_bytes, num_pages;
-  int i0, i1;              // key tiles of this workgroup
-  int L, mask_from, G;
-  float alpha, out_scale;
-  uint32_t kl;             // LDS byte address of the K stages
-};
-
-// Per-key partials of one tile: wave w, lane group q = l/16, key k at
-// red[w][q * kRedGrp + k].  The padded strides keep both the writes (64 lanes: 4 groups x
-// 16 keys) and the finishing reads (4 waves x 16 keys) on 64 distinct banks.
-constexpr int kRedGrp = kKeyTile + 16;      // 80 floats: group stride = 16 banks apart
-constexpr int kRedRow = 4 * kRedGrp + 16;   // 336 floats: wave stride = 16 banks apart
-typedef float RedTile[kWaves][kRedRow];
-constexpr int kRedBufs = 4;   // a tile's partials are read one tile later
-
-// Sum of the 16 partials of each key of tile t in a fixed order; wave w finishes keys
-// 16w .. 16w+15.  Lane l takes key 16w + l/4 and the four partials of wave l%4, then the
-// four lanes of a key are summed pairwise (xor 1, then xor 2).
 __device__ __forceinline__ float dpp_xor1(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
 }
@@ -428,260 +248,302 @@ __device__ __forceinline__ float dpp_xor2(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
 }
 
-// The finish of a tile in two halves, a phase apart, so that the LDS reads are not waited
-// for at once: finish_read fetches this lane's four partials, finish_write sums them and
-// the eight lanes of its key, and stores the key's score (only when `valid`).  Every lane
-// takes part in the store (lanes that do not write use an offset past the buffer), so each
-// wave issues exactly one vector-memory store per call whatever the keys, with no branch:
-// the K pipeline's waits count on that.
-__device__ __forceinline__ float4 finish_read(const RedTile& red) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int kk = w * (kKeyTile / kWaves) + (lane >> 2), ww = lane & 3;
-  const float* rr = red[ww] + kk;
-  return make_float4(rr[0], rr[kRedGrp], rr[2 * kRedGrp], rr[3 * kRedGrp]);
+
+// The sweep.  Per tile: page ids prefetched a tile ahead (scalar), a wait for the tile's
+// direct-to-LDS loads, one barrier, the loads of the tile three ahead, the finish of the
+// previous tile, then 4 sub-tiles x NRT units.  A unit's exp2 epilogue runs after the next
+// unit's MFMA chain (lag one), and a tile's last unit is finished before the next barrier.
+// Each wave reads every K sub-tile from LDS: twice the LDS reads of four waves of 128 rows,
+// which measured faster anyway (one wave per SIMD leaves the SIMD idle whenever it waits).
+namespace {
+
+constexpr int k2wThreads = 512;
+constexpr int k2wWaves = k2wThreads / 64;
+constexpr int k2wRowTiles = kRowsPerChunk / kRowTile / k2wWaves;   // 4
+static_assert(k2wRowTiles == 4, "row-tile bookkeeping below");
+constexpr int k2wStages = 4;   // K tiles in LDS (three in flight)
+constexpr int k2wRedBufs = 2;  // per-key partials of a tile are read one tile later
+// Per-key partials of one tile: wave w, lane group g = l/16, key k at
+// red[w * k2wRedRow + g * k2wRedGrp + k]; the strides keep the writes (64 lanes) and the
+// finishing reads (8 source waves x 4 keys per half-wave) on distinct banks.
+constexpr int k2wRedGrp = kKeyTile + 16;          // 80 floats
+constexpr int k2wRedRow = 4 * k2wRedGrp + 4;      // 324 floats
+constexpr int k2wRedTile = k2wWaves * k2wRedRow;  // floats per buffer
+
+// Query row at (row tile T = w + 8 * rt, tile row mm) of row chunk c: the natural order
+// m = j * G + g, unless the group max of MAX_MEAN needs a query's G = 8 or 16 heads in one
+// lane: then they sit at the same lane position of 2 or 4 consecutive row tiles of a wave.
+__device__ __forceinline__ void row_query_2w(int G, bool grouped, int c, int T, int mm, int* j,
+                                             int* g) {
+  if (!grouped) {
+    const int m = c * kRowsPerChunk + T * kRowTile + mm;
+    *j = m / G;
+    *g = m % G;
+    return;
+  }
+  const int w = T % k2wWaves, rt = T / k2wWaves, a = mm >> 2, i = mm & 3;
+  if (G == 8) {
+    *j = c * (kRowsPerChunk / 8) + (rt >> 1) * (4 * k2wWaves) + w * 4 + a;
+    *g = 4 * (rt & 1) + i;
+  } else {
+    *j = c * (kRowsPerChunk / 16) + w * 4 + a;
+    *g = 4 * (rt & 3) + i;
+  }
 }
 
-__device__ __forceinline__ void finish_write(const SweepCtx& cx, float4 p, int t, bool valid) {
+// Row tiles per wave that can hold real rows of chunk c (the same for every wave).
+__device__ __forceinline__ int wave_tiles_2w(int G, bool grouped, int n, int c) {
+  if (!grouped) {
+    const int rows = G * n - c * kRowsPerChunk;
+    if (rows <= 0) return 1;
+    const int r = rows < kRowsPerChunk ? rows : kRowsPerChunk;
+    return ceil_div(r, kRowTile * k2wWaves);
+  }
+  const int per = G / 4, qn = n - c * (kRowsPerChunk / G);
+  const int groups = qn <= 0 ? 1 : ceil_div(qn, 4 * k2wWaves);
+  const int t = groups * per;
+  return t < k2wRowTiles ? t : k2wRowTiles;
+}
+
+// Row tile T of chunk c as the 16x16x32 A operand: lane l holds row l%16 with head-dim
+// elements 32*ks + 8*(l/16) .. +8; rows past n are zero.
+template <int D>
+__device__ __forceinline__ void load_q16(bf16x8 (&qr)[Geom16<D>::kSteps],
+                                         const uint16_t* __restrict__ q, int G, bool grouped,
+                                         int Hq, int h, int q_off, int n, int c, int T) {
+  const int lane = threadIdx.x & 63;
+  int j, g;
+  row_query_2w(G, grouped, c, T, lane & 15, &j, &g);
+  if (j < n) {
+    const uint16_t* src = q + ((int64_t)(q_off + j) * Hq + h * G + g) * D + (lane >> 4) * 8;
+#pragma unroll
+    for (int ks = 0; ks < Geom16<D>::kSteps; ++ks)
+      qr[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + ks * 32));
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < Geom16<D>::kSteps; ++ks) qr[ks] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+  }
+}
+
+struct Ctx2w {
+  const char* kv_bytes;
+  const int32_t* bt_row;
+  const int32_t* pos_s;    // LDS: causal position of every row of the chunk
+  __amdgpu_buffer_rsrc_t out;   // scores (or chunk partials) of this (request, KV head)
+  const char* kbuf;        // LDS: the K stages
+  float* red;              // LDS: k2wRedBufs partial tiles
+  int64_t page_bytes, num_pages;
+  int i0, i1;              // key tiles of this workgroup
+  int L, mask_from, G;
+  float alpha, out_scale;
+  uint32_t kl;             // LDS byte address of the K stages
+};
+
+// The finish of tile t: the 32 partials of every key (8 waves x 4 lane groups) summed in a
+// fixed order and stored.  Wave w finishes keys 8w .. 8w+7: lane l takes key 8w + l/8 and
+// the 4 partials of source wave l%8, then the 8 lanes of a key are added pairwise (xor 1,
+// xor 2, then lane 4 of each group of 8 takes the other half by a row shift of 4).  Every
+// lane takes part in one buffer store (lanes with nothing to write store past the end).
+__device__ __forceinline__ void finish_2w(const Ctx2w& cx, int t, bool valid) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int kk = w * (kKeyTile / kWaves) + (lane >> 2), ww = lane & 3;
-  float v = (p.x + p.y) + (p.z + p.w);
+  const int kk = w * (kKeyTile / k2wWaves) + (lane >> 3), ww = lane & 7;
+  const float* rr = cx.red + (t & (k2wRedBufs - 1)) * k2wRedTile + ww * k2wRedRow + kk;
+  float v = (rr[0] + rr[k2wRedGrp]) + (rr[2 * k2wRedGrp] + rr[3 * k2wRedGrp]);
   v += dpp_xor1(v);
   v += dpp_xor2(v);
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x114, 0xF, 0xF, false));
   const int key = t * kKeyTile + kk;
-  const uint32_t off = (valid && ww == 0 && key < cx.L) ? (uint32_t)key * 4u : 0x7FFFFFF0u;
+  const uint32_t off = (valid && ww == 4 && key < cx.L) ? (uint32_t)key * 4u : 0x7FFFFFF0u;
   __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v * cx.out_scale), cx.out, off, 0, 0);
 }
 
-// The K pipeline's vector-memory sequence per wave is, from the first tile of a segment on,
-// (loads of one K tile, one score store) repeated: the sweep's prologue issues a store that
-// writes nothing after each of its tile loads, and the tile after the first one finishes
-// nothing real.  So at the barrier of every tile, when the loads of tile i + 1 must have
-// landed, exactly the stores and loads of the two tiles after it (and a store) may still be
-// in flight: one wait count for every tile, and no branch in the loop body.
-template <int D>
-constexpr int kTileVmcnt = (kScoreStages - 2) * (TileGeom<D>::kLoadsPerWave + 1) + 1;
+// Per-wave epilogue state.
+struct Epi2w {
+  float part[4];   // the lane's partials of the current sub-tile (independent add chains)
+  float ex;        // SUM: the last exp2, added one element later
+  float mx;        // MAX_MEAN, G = 8 / 16: running group max over the row tiles of a query
+};
 
-// Phases P = 2 .. U+1 of tile i, U = 4 * NRT units per tile: the chain of unit P (of tile
-// i, or of tile i+1 once P >= U) and the epilogue of unit P - 2 of tile i.  The chain of
-// the first unit of sub-tile s also reads the operand of sub-tile s + kOperandAhead from
-// LDS.  Phase (4 - kOperandAhead) NRT is the first to read sub-tile 0 of tile i+1: the
-// barrier that makes tile i+1 visible sits there, and once every wave has passed it no wave
-// reads tile i's stage any more (its last sub-tile was read kOperandAhead sub-tiles
-// earlier), which is then refilled.
-// kMask: tile i holds keys hidden from some rows.  kLast: no tile follows.
-template <int D, bool kMaxMean, int NRT, bool kMask, bool kLast, int P>
-__device__ __forceinline__ void tile_phases16(const SweepCtx& cx, const KLoadPlan<D, kWaves>& kp,
-                                              const KRead16& rp, Pipe16<D>& st,
-                                              const bf16x8 (&qreg)[kRowTilesPerWave][Geom16<D>::kSteps],
-                                              const float (&beta)[kRowTilesPerWave][4],
-                                              RedTile* red, int i, int32_t& next_page,
-                                              float4& fin) {
-  constexpr int U = kSubTiles * NRT;
-  if constexpr (P <= U + 1) {
-    using Gm = TileGeom<D>;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    static_assert((kScoreStages & (kScoreStages - 1)) == 0, "stage index uses a mask");
-    const int st_i = (i - cx.i0) & (kScoreStages - 1), st_n = (i + 1 - cx.i0) & (kScoreStages - 1);
-    const char* buf_i = cx.kbuf + st_i * Gm::kTileBytes;
-    const char* buf_n = cx.kbuf + st_n * Gm::kTileBytes;
-    constexpr int kBarrier = (kSubTiles - kOperandAhead) * NRT;
-    if constexpr (P == kBarrier) {
-      // the page of the tile after the one refilled below: a scalar load, issued before the
-      // barrier's full wait so that it is retired there (an outstanding scalar load would
-      // make every later LDS wait of the tile a wait for all LDS traffic)
-      const int32_t page = next_page;
-      const int nt = i + kScoreStages + 1;
-      next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp, nt < cx.i1 ? nt : cx.i1 - 1);
-      // tile i + 1 is read from this phase on: this wave's loads of it have landed, this
-      // wave's LDS traffic of tile i is retired, then the barrier
-      wait_vmcnt<kTileVmcnt<D>>();
-      wait_lgkmcnt0();
-      __builtin_amdgcn_s_barrier();
-      // no wave reads tile i any more: refill its stage with tile i + kScoreStages
-      issue_k_tile<D, kWaves>(cx.kl + st_i * Gm::kTileBytes, cx.kv_bytes, page, cx.num_pages,
-                              cx.page_bytes, kp);
-      fin = finish_read(red[(i - 1) & (kRedBufs - 1)]);   // unused in the first tile
-    }
-    // epilogue: unit P - 2 of tile i
-    constexpr int eu = P - 2, es = eu / NRT, er = eu % NRT;
-    const int32_t* prow = cx.pos_s + (w + kWaves * er) * kRowTile + 4 * (lane >> 4);
-    const int key = i * kKeyTile + es * 16 + (lane & 15);
-    // chain: unit cu of tile i (P < U) or of tile i + 1
-    constexpr bool kChain = P < U || !kLast;
-    constexpr int cu = P < U ? P : P - U, cs = cu / NRT, cr = cu % NRT;
-    // the first unit of a sub-tile reads the operand kOperandAhead sub-tiles on (in tile i+1
-    // once that passes the tile's end; a chain already in tile i+1 reads within it)
-    constexpr int ls = cs + kOperandAhead;
-    constexpr bool kNextTile = P < U && ls >= kSubTiles;
-    constexpr bool kLoad = kChain && cu % NRT == 0 && !(kNextTile && kLast);
-    constexpr int lsub = ls % kSubTiles;
-    score_phase16<D, kMaxMean, kMask, kChain, true, kLoad, er>(
-        st, qreg[cr], st.kb[cs % kOperandBufs], st.kb[lsub % kOperandBufs], rp,
-        (P < U && !kNextTile) ? buf_i : buf_n, lsub, beta[er], prow, key, cx.alpha, cx.G);
-    if constexpr (er == NRT - 1) {
-      // sub-tile es is complete in this lane: hand its partial to the other waves
-      if (!kMaxMean) {
-        st.part[3] += st.ex;   // the pending exp2 of the unit's last element
-        st.ex = 0.f;
-      }
-      red[i & (kRedBufs - 1)][w][(lane >> 4) * kRedGrp + es * 16 + (lane & 15)] =
-          (st.part[0] + st.part[1]) + (st.part[2] + st.part[3]);
-      st.part[0] = st.part[1] = st.part[2] = st.part[3] = 0.f;
-    }
-    if constexpr (P == kBarrier + 1) {
-      // the finish of tile i - 1, whose partials were read a phase ago
-      finish_write(cx, fin, i - 1, i > cx.i0);
-    }
-    tile_phases16<D, kMaxMean, NRT, kMask, kLast, P + 1>(cx, kp, rp, st, qreg, beta, red, i,
-                                                          next_page, fin);
+// Epilogue of one unit: accumulator c of row tile rt (beta bt), keys of sub-tile at `key`.
+template <bool kMaxMean, bool kMask>
+__device__ __forceinline__ void epilogue_2w(Epi2w& e, f32x4 c, int rt, const float (&bt)[4],
+                                            const int32_t* prow, int key, float alpha, int G) {
+  int pt[4] = {0, 0, 0, 0};
+  if (kMask) {
+    const int4 p4 = *reinterpret_cast<const int4*>(prow);
+    pt[0] = p4.x; pt[1] = p4.y; pt[2] = p4.z; pt[3] = p4.w;
   }
-}
-
-// Sweep key tiles i0 .. i1-1 of one segment with NRT row tiles per wave.  K tiles stream
-// through kScoreStages LDS buffers (direct-to-LDS loads, kScoreStages - 1 tiles ahead),
-// one barrier per tile.
-template <int D, bool kMaxMean, int NRT>
-__device__ __forceinline__ void score_sweep16(const SweepCtx& cx, const KLoadPlan<D, kWaves>& kp,
-                                              const bf16x8 (&qreg)[kRowTilesPerWave][Geom16<D>::kSteps],
-                                              const float (&beta)[kRowTilesPerWave][4],
-                                              RedTile* red) {
-  using Gm = TileGeom<D>;
-  auto clamp_tile = [&](int t) { return t < cx.i1 ? t : cx.i1 - 1; };
-  float4 fin = make_float4(0.f, 0.f, 0.f, 0.f);
+  float p[4];
 #pragma unroll
-  for (int p = 0; p < kScoreStages - 1; ++p) {
-    issue_k_tile<D, kWaves>(cx.kl + p * Gm::kTileBytes, cx.kv_bytes,
-                            page_of<D, kWaves>(cx.bt_row, cx.L, kp, clamp_tile(cx.i0 + p)),
-                            cx.num_pages, cx.page_bytes, kp);
-    finish_write(cx, fin, 0, false);   // the store slot of the tile (writes nothing)
-  }
-  int32_t next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp,
-                                         clamp_tile(cx.i0 + kScoreStages - 1));
-  const KRead16 rp = make_k_read16<D>();
-  Pipe16<D> st;
-  st.part[0] = st.part[1] = st.part[2] = st.part[3] = 0.f;
-  st.ex = 0.f;
-  st.mx = 0.f;
-  st.c1 = f32x4{0.f, 0.f, 0.f, 0.f};
-  // prologue: tile i0 in LDS, the last stage filled, operands of the first kOperandAhead
-  // sub-tiles, chains of units 0 and 1 (each reading ahead when it starts a sub-tile)
-  wait_vmcnt<kTileVmcnt<D>>();
-  __builtin_amdgcn_s_barrier();
-  issue_k_tile<D, kWaves>(cx.kl + (kScoreStages - 1) * Gm::kTileBytes, cx.kv_bytes, next_page,
-                          cx.num_pages, cx.page_bytes, kp);
-  finish_write(cx, fin, 0, false);
-  next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp, clamp_tile(cx.i0 + kScoreStages));
-#pragma unroll
-  for (int sb = 0; sb < kOperandAhead; ++sb)
-#pragma unroll
-    for (int ks = 0; ks < Geom16<D>::kSteps; ++ks) st.kb[sb][ks] = lds_k16<D>(cx.kbuf, sb, rp, ks);
-  score_phase16<D, kMaxMean, false, true, false, true, 0>(
-      st, qreg[0], st.kb[0], st.kb[kOperandAhead % kOperandBufs], rp, cx.kbuf, kOperandAhead,
-      beta[0], nullptr, 0, cx.alpha, cx.G);
-  constexpr int s1 = 1 / NRT;   // sub-tile of unit 1
-  score_phase16<D, kMaxMean, false, true, false, NRT == 1, 0>(
-      st, qreg[1 % NRT], st.kb[s1 % kOperandBufs], st.kb[(s1 + kOperandAhead) % kOperandBufs],
-      rp, cx.kbuf, s1 + kOperandAhead, beta[0], nullptr, 0, cx.alpha, cx.G);
-  for (int i = cx.i0; i < cx.i1; ++i) {
-    const bool mask = i * kKeyTile + kKeyTile - 1 > cx.mask_from;
-    if (i + 1 < cx.i1) {
-      if (mask)
-        tile_phases16<D, kMaxMean, NRT, true, false, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page, fin);
-      else
-        tile_phases16<D, kMaxMean, NRT, false, false, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page, fin);
+  for (int v = 0; v < 4; ++v) {
+    float x = __builtin_fmaf(c[v], alpha, -bt[v]);
+    if (kMask) x = key > pt[v] ? -__builtin_inff() : x;   // exp2(-inf) = 0
+    if (!kMaxMean) {
+      e.part[(v + 3) & 3] += e.ex;   // the previous exp2, off the latency path
+      e.ex = fast_exp2(x);
     } else {
-      if (mask)
-        tile_phases16<D, kMaxMean, NRT, true, true, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page, fin);
-      else
-        tile_phases16<D, kMaxMean, NRT, false, true, 2>(cx, kp, rp, st, qreg, beta, red, i, next_page, fin);
+      p[v] = fast_exp2(x);
     }
   }
-  // the last tile's partials
-  wait_lgkmcnt0();
-  __builtin_amdgcn_s_barrier();
-  finish_write(cx, finish_read(red[(cx.i1 - 1) & (kRedBufs - 1)]), cx.i1 - 1, true);
+  if (kMaxMean) {
+    const float m01 = fmaxf(p[0], p[1]), m23 = fmaxf(p[2], p[3]);
+    if (G == 1) {
+      e.part[0] += (p[0] + p[1]) + (p[2] + p[3]);
+    } else if (G == 2) {
+      e.part[0] += m01 + m23;
+    } else if (G == 4) {
+      e.part[0] += fmaxf(m01, m23);
+    } else if (G == 8) {
+      const float m = fmaxf(m01, m23);
+      if (rt & 1) e.part[0] += fmaxf(e.mx, m); else e.mx = m;
+    } else {
+      const float m = fmaxf(m01, m23);
+      e.mx = (rt & 3) == 0 ? m : fmaxf(e.mx, m);
+      if ((rt & 3) == 3) e.part[0] += e.mx;
+    }
+  }
 }
 
-// The sweep of a wave whose row tiles hold no real row (few query rows, e.g. one decode
-// query per request): the same K loads, barriers and tile finishes as score_sweep16, but no
-// MFMA and no epilogue; its partial slots stay zero.
-template <int D>
-__device__ __forceinline__ void score_sweep_idle(const SweepCtx& cx, const KLoadPlan<D, kWaves>& kp,
-                                                 RedTile* red) {
-  using Gm = TileGeom<D>;
+// The lane's partial of sub-tile s of tile t goes to LDS; the partials restart.
+__device__ __forceinline__ void put_partial_2w(const Ctx2w& cx, Epi2w& e, int t, int s) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  // this wave's partial slots of every reduction buffer: zero (no finish of the previous
-  // segment reads them any more)
+  e.part[3] += e.ex;
+  e.ex = 0.f;
+  cx.red[(t & (k2wRedBufs - 1)) * k2wRedTile + w * k2wRedRow + (lane >> 4) * k2wRedGrp + s * 16 +
+         (lane & 15)] = (e.part[0] + e.part[1]) + (e.part[2] + e.part[3]);
+  e.part[0] = e.part[1] = e.part[2] = e.part[3] = 0.f;
+}
+
+// The units of tile t (4 sub-tiles x NRT row tiles), lag-one epilogues, all finished.
+template <int D, bool kMaxMean, int NRT, bool kMask>
+__device__ __forceinline__ void tile_units_2w(const Ctx2w& cx, Epi2w& e, const char* tb, int t,
+                                              const KRead16& rp,
+                                              const bf16x8 (&qreg)[k2wRowTiles][Geom16<D>::kSteps],
+                                              const float (&beta)[k2wRowTiles][4]) {
+  constexpr int S = Geom16<D>::kSteps;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  f32x4 prev = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int b = 0; b < kRedBufs; ++b)
+  for (int s = 0; s < kSubTiles; ++s) {
+    bf16x8 kb[S];
 #pragma unroll
-    for (int es = 0; es < kSubTiles; ++es)
-      red[b][w][(lane >> 4) * kRedGrp + es * 16 + (lane & 15)] = 0.f;
+    for (int ks = 0; ks < S; ++ks) kb[ks] = lds_k16<D>(tb, s, rp, ks);
+#pragma unroll
+    for (int rt = 0; rt < NRT; ++rt) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < S; ++ks) acc = mfma16(qreg[rt][ks], kb[ks], acc);
+      // the previous unit's epilogue (sub-tile s of row tile rt - 1, or the last row tile
+      // of sub-tile s - 1), independent of this chain
+      if (s > 0 || rt > 0) {
+        const int ps = rt > 0 ? s : s - 1, prt = rt > 0 ? rt - 1 : NRT - 1;
+        epilogue_2w<kMaxMean, kMask>(e, prev, prt, beta[prt],
+                                     cx.pos_s + (w + k2wWaves * prt) * kRowTile + 4 * (lane >> 4),
+                                     t * kKeyTile + ps * 16 + (lane & 15), cx.alpha, cx.G);
+        if (prt == NRT - 1) put_partial_2w(cx, e, t, ps);
+      }
+      prev = acc;
+    }
+  }
+  epilogue_2w<kMaxMean, kMask>(e, prev, NRT - 1, beta[NRT - 1],
+                               cx.pos_s + (w + k2wWaves * (NRT - 1)) * kRowTile + 4 * (lane >> 4),
+                               t * kKeyTile + (kSubTiles - 1) * 16 + (lane & 15), cx.alpha, cx.G);
+  put_partial_2w(cx, e, t, kSubTiles - 1);
+}
+
+// Sweep key tiles i0 .. i1-1 of one segment.  NRT == 0: a wave none of whose row tiles holds
+// a real row (its partial slots stay zero; it keeps the loads, barriers and finishes).
+// The vector-memory sequence of every wave is (one tile's loads, one store) per tile from
+// the prologue on, so one wait count serves every tile: when tile i must have landed, the
+// loads of tiles i+1 and i+2 and three stores may still be in flight.
+template <int D, bool kMaxMean, int NRT>
+__device__ __forceinline__ void sweep_2w(const Ctx2w& cx, const KLoadPlan<D, k2wWaves>& kp,
+                                         const bf16x8 (&qreg)[k2wRowTiles][Geom16<D>::kSteps],
+                                         const float (&beta)[k2wRowTiles][4]) {
+  using Gm = TileGeom<D, k2wWaves>;
+  constexpr int kVm = (k2wStages - 2) * (Gm::kLoadsPerWave + 1) + 1;
   auto clamp_tile = [&](int t) { return t < cx.i1 ? t : cx.i1 - 1; };
+  if constexpr (NRT == 0) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
-  for (int p = 0; p < kScoreStages - 1; ++p)
-    issue_k_tile<D, kWaves>(cx.kl + p * Gm::kTileBytes, cx.kv_bytes,
-                            page_of<D, kWaves>(cx.bt_row, cx.L, kp, clamp_tile(cx.i0 + p)),
-                            cx.num_pages, cx.page_bytes, kp);
-  int32_t next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp,
-                                         clamp_tile(cx.i0 + kScoreStages - 1));
-  wait_vmcnt<(kScoreStages - 2) * Gm::kLoadsPerWave>();
-  wait_lgkmcnt0();
-  __builtin_amdgcn_s_barrier();
-  issue_k_tile<D, kWaves>(cx.kl + (kScoreStages - 1) * Gm::kTileBytes, cx.kv_bytes, next_page,
-                          cx.num_pages, cx.page_bytes, kp);
-  next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp, clamp_tile(cx.i0 + kScoreStages));
+    for (int b = 0; b < k2wRedBufs; ++b)
+#pragma unroll
+      for (int s = 0; s < kSubTiles; ++s)
+        cx.red[b * k2wRedTile + w * k2wRedRow + (lane >> 4) * k2wRedGrp + s * 16 + (lane & 15)] = 0.f;
+  }
+#pragma unroll
+  for (int p = 0; p < k2wStages - 1; ++p) {
+    issue_k_tile<D, k2wWaves>(cx.kl + p * Gm::kTileBytes, cx.kv_bytes,
+                              page_of<D, k2wWaves>(cx.bt_row, cx.L, kp, clamp_tile(cx.i0 + p)),
+                              cx.num_pages, cx.page_bytes, kp);
+    finish_2w(cx, 0, false);   // the store slot of the tile (writes nothing)
+  }
+  int32_t next_page = page_of<D, k2wWaves>(cx.bt_row, cx.L, kp, clamp_tile(cx.i0 + k2wStages - 1));
+  const KRead16 rp = make_k_read16<D>();
+  Epi2w e;
+  e.part[0] = e.part[1] = e.part[2] = e.part[3] = 0.f;
+  e.ex = 0.f;
+  e.mx = 0.f;
   for (int i = cx.i0; i < cx.i1; ++i) {
-    // the barrier phase of tile i, as in tile_phases16
-    const int st_i = (i - cx.i0) & (kScoreStages - 1);
-    wait_vmcnt<(kScoreStages - 2) * Gm::kLoadsPerWave>();
-    wait_lgkmcnt0();
+    const int32_t page = next_page;
+    // the page of the tile after the one issued below: a scalar load, retired by the full
+    // wait before the barrier (an outstanding scalar load would make every later LDS wait
+    // of the tile a wait for all LDS traffic)
+    next_page = page_of<D, k2wWaves>(cx.bt_row, cx.L, kp, clamp_tile(i + k2wStages));
+    wait_vmcnt<kVm>();   // tile i has landed
+    wait_lgkmcnt0();     // this wave's partials of tile i - 1 are written
     __builtin_amdgcn_s_barrier();
-    issue_k_tile<D, kWaves>(cx.kl + st_i * Gm::kTileBytes, cx.kv_bytes, next_page, cx.num_pages,
-                            cx.page_bytes, kp);
-    const int nt = i + kScoreStages + 1;
-    next_page = page_of<D, kWaves>(cx.bt_row, cx.L, kp, nt < cx.i1 ? nt : cx.i1 - 1);
-    finish_write(cx, finish_read(red[(i - 1) & (kRedBufs - 1)]), i - 1, i > cx.i0);
+    // no wave reads tile i - 1 any more: its stage takes tile i + 3
+    issue_k_tile<D, k2wWaves>(cx.kl + ((i - cx.i0 + k2wStages - 1) & (k2wStages - 1)) * Gm::kTileBytes,
+                              cx.kv_bytes, page, cx.num_pages, cx.page_bytes, kp);
+    finish_2w(cx, i - 1, i > cx.i0);
+    if constexpr (NRT > 0) {
+      const char* tb = cx.kbuf + ((i - cx.i0) & (k2wStages - 1)) * Gm::kTileBytes;
+      if (i * kKeyTile + kKeyTile - 1 > cx.mask_from)
+        tile_units_2w<D, kMaxMean, NRT, true>(cx, e, tb, i, rp, qreg, beta);
+      else
+        tile_units_2w<D, kMaxMean, NRT, false>(cx, e, tb, i, rp, qreg, beta);
+    }
   }
   wait_lgkmcnt0();
   __builtin_amdgcn_s_barrier();
-  finish_write(cx, finish_read(red[(cx.i1 - 1) & (kRedBufs - 1)]), cx.i1 - 1, true);
+  finish_2w(cx, cx.i1 - 1, true);
 }
+
+}  // namespace
 
 template <int D, bool kMaxMean>
-__global__ __launch_bounds__(kThreads, 1) void score_kernel(
+__global__ __launch_bounds__(k2wThreads, 1) void score_kernel(
     DevProblem dp, const uint16_t* __restrict__ q_ptr, const uint16_t* __restrict__ kv_ptr,
     const int32_t* __restrict__ bt_ptr, const float* __restrict__ lse_ptr,
     float* __restrict__ scores_ptr, float* __restrict__ part_ptr, int64_t num_scores,
     int64_t seg_lo, int64_t seg_hi) {
   if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
-  using Gm = TileGeom<D>;
-  __shared__ __align__(1024) char kbuf[kScoreStages][Gm::kTileBytes];
+  using Gm = TileGeom<D, k2wWaves>;
+  __shared__ __align__(1024) char kbuf[k2wStages][Gm::kTileBytes];
   __shared__ __align__(16) float beta_s[kRowsPerChunk];
   __shared__ __align__(16) int32_t pos_s[kRowsPerChunk];
-  __shared__ RedTile red[kRedBufs];
+  __shared__ __align__(16) float red[k2wRedBufs * k2wRedTile];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int G = dp.G, Hq = dp.Hq, Hkv = dp.Hkv, C = dp.max_chunks;
   const bool grouped = kMaxMean && (G == 8 || G == 16);
-  // this launch scores segments [seg_lo, seg_hi) (whole requests: a request's segments are
-  // consecutive); workgroup b takes the b-th equal share of their cost
   const int64_t base = dp.seg_cost[seg_lo], total = dp.seg_cost[seg_hi] - base;
   const int64_t c0 = base + total * blockIdx.x / gridDim.x;
   const int64_t c1 = base + total * (blockIdx.x + 1) / gridDim.x;
   if (c0 >= c1) return;
 
-  SweepCtx cx;
+  Ctx2w cx;
   cx.kv_bytes = reinterpret_cast<const char*>(kv_ptr);
   cx.pos_s = pos_s;
   cx.kbuf = &kbuf[0][0];
+  cx.red = red;
   cx.kl = (uint32_t)(uintptr_t)(lds_char*)&kbuf[0][0];
   cx.page_bytes = (int64_t)kPageSize * Hkv * D * 2;
   cx.num_pages = dp.num_pages;
   cx.G = G;
   cx.alpha = dp.sm_scale * kLog2e;
 
-  // first segment: the largest s with seg_cost[s] <= c0 (it is never empty)
   int64_t lo = seg_lo, hi = seg_hi;
   while (lo < hi) {
     const int64_t mid = (lo + hi + 1) / 2;
@@ -696,74 +558,59 @@ __global__ __launch_bounds__(kThreads, 1) void score_kernel(
     decode_segment(s, C, Hkv, &r, &c, &h);
     const ReqPlan pl = dp.plan[r];
     const int L = pl.L, n = pl.n, M = G * n;
-    // cost of each of the segment's key tiles (the unit of the split over workgroups)
     const int64_t TC = score_tile_cost(chunk_row_tiles(M, c));
     const int64_t ntiles = ceil_div64(L, kKeyTile);
     int64_t i1 = (c1 - cs + TC - 1) / TC;
     if (i1 > ntiles) i1 = ntiles;
-    cx.i0 = first ? (int)((c0 - cs + TC - 1) / TC) : 0;   // c0 < ce: below ntiles
+    cx.i0 = first ? (int)((c0 - cs + TC - 1) / TC) : 0;
     cx.i1 = (int)i1;
     first = false;
     if (cx.i0 >= cx.i1) continue;
 
-    // ---- segment setup: beta / causal position of every row, Q rows into registers
     wait_vmcnt<0>();   // no load of the previous segment may still land in a K buffer
     __syncthreads();
-    for (int m = tid; m < kRowsPerChunk; m += kThreads) {
+    for (int m = tid; m < kRowsPerChunk; m += k2wThreads) {
       int j, g;
-      score_row_query(G, grouped, c, m / kRowTile, m % kRowTile, &j, &g);
+      row_query_2w(G, grouped, c, m / kRowTile, m % kRowTile, &j, &g);
       beta_s[m] = j < n ? lse_ptr[(int64_t)(pl.q_off + j) * Hq + h * G + g] * kLog2e
                         : __builtin_inff();
       pos_s[m] = dp.causal ? L - n + j : L - 1;
     }
-    bf16x8 qreg[kRowTilesPerWave][Geom16<D>::kSteps];
+    bf16x8 qreg[k2wRowTiles][Geom16<D>::kSteps];
 #pragma unroll
-    for (int rt = 0; rt < kRowTilesPerWave; ++rt)
-      load_q16<D>(qreg[rt], q_ptr, G, grouped, Hq, h, pl.q_off, n, c, w + kWaves * rt);
+    for (int rt = 0; rt < k2wRowTiles; ++rt)
+      load_q16<D>(qreg[rt], q_ptr, G, grouped, Hq, h, pl.q_off, n, c, w + k2wWaves * rt);
     cx.bt_row = bt_ptr + (int64_t)r * dp.bt_stride;
     cx.L = L;
-    cx.mask_from = dp.causal ? L - n : L;  // keys past this may be hidden from some rows
+    cx.mask_from = dp.causal ? L - n : L;
     cx.out_scale = (kMaxMean && pl.nchunk == 1) ? (n > 0 ? 1.0f / n : 0.0f) : 1.0f;
     cx.out = buffer_over_uniform((c == 0) ? scores_ptr + pl.seg_off + (int64_t)h * L
                                           : part_ptr + (int64_t)(c - 1) * num_scores +
                                                 pl.seg_off + (int64_t)h * L,
                                  L * (int)sizeof(float));
-    const KLoadPlan<D, kWaves> kp = make_k_load_plan<D, kWaves>(h, Hkv);
-    // every ordinary load of the setup has landed before the K pipeline starts, so the
-    // sweep needs no compiler-inserted wait on the vector-memory queue
+    const KLoadPlan<D, k2wWaves> kp = make_k_load_plan<D, k2wWaves>(h, Hkv);
     wait_vmcnt<0>();
     __syncthreads();   // beta_s / pos_s visible
-    // beta of this lane's rows (4*(l/16) + i of each row tile): fixed for the sweep
-    float beta[kRowTilesPerWave][4];
+    float beta[k2wRowTiles][4];
 #pragma unroll
-    for (int rt = 0; rt < kRowTilesPerWave; ++rt) {
-      const float4 b4 = *reinterpret_cast<const float4*>(beta_s + (w + kWaves * rt) * kRowTile +
+    for (int rt = 0; rt < k2wRowTiles; ++rt) {
+      const float4 b4 = *reinterpret_cast<const float4*>(beta_s + (w + k2wWaves * rt) * kRowTile +
                                                          4 * (lane >> 4));
       beta[rt][0] = b4.x; beta[rt][1] = b4.y; beta[rt][2] = b4.z; beta[rt][3] = b4.w;
     }
-    // row tiles past the chunk's real rows are all padding (Q = 0, beta = +inf): every
-    // wave runs only as many row tiles as can hold real rows
-    const int nrt = chunk_wave_tiles(G, grouped, n, c);
-    // a wave none of whose row tiles holds a real row keeps the schedule but does no work
+    const int nrt = wave_tiles_2w(G, grouped, n, c);
     bool real = false;
-    for (int rt = 0; rt < (nrt < kRowTilesPerWave ? nrt : kRowTilesPerWave); ++rt) {
+    for (int rt = 0; rt < nrt; ++rt) {
       int j, g;
-      score_row_query(G, grouped, c, w + kWaves * rt, lane & 15, &j, &g);
+      row_query_2w(G, grouped, c, w + k2wWaves * rt, lane & 15, &j, &g);
       real = real || j < n;
     }
-    if (__ballot(real) == 0ull) {
-      score_sweep_idle<D>(cx, kp, red);
-    } else {
-      switch (nrt < kRowTilesPerWave ? nrt : kRowTilesPerWave) {
-        case 1: score_sweep16<D, kMaxMean, 1>(cx, kp, qreg, beta, red); break;
-        case 2: score_sweep16<D, kMaxMean, 2>(cx, kp, qreg, beta, red); break;
-        case 3: score_sweep16<D, kMaxMean, 3>(cx, kp, qreg, beta, red); break;
-        case 4: score_sweep16<D, kMaxMean, 4>(cx, kp, qreg, beta, red); break;
-        case 5: score_sweep16<D, kMaxMean, 5>(cx, kp, qreg, beta, red); break;
-        case 6: score_sweep16<D, kMaxMean, 6>(cx, kp, qreg, beta, red); break;
-        case 7: score_sweep16<D, kMaxMean, 7>(cx, kp, qreg, beta, red); break;
-        default: score_sweep16<D, kMaxMean, 8>(cx, kp, qreg, beta, red); break;
-      }
+    switch (__ballot(real) == 0ull ? 0 : nrt) {
+      case 0: sweep_2w<D, kMaxMean, 0>(cx, kp, qreg, beta); break;
+      case 1: sweep_2w<D, kMaxMean, 1>(cx, kp, qreg, beta); break;
+      case 2: sweep_2w<D, kMaxMean, 2>(cx, kp, qreg, beta); break;
+      case 3: sweep_2w<D, kMaxMean, 3>(cx, kp, qreg, beta); break;
+      default: sweep_2w<D, kMaxMean, 4>(cx, kp, qreg, beta); break;
     }
   }
   wait_vmcnt<0>();   // drain: no LDS write may be outstanding when the workgroup exits
@@ -801,11 +648,11 @@ hipError_t launch_score_range(const DevProblem& dp, const HostPlan& hp, int r0, 
   const bool mm = dp.agg == ACTKV_AGG_MAX_MEAN;
   const int64_t n = hp.num_scores;
   if (dp.D == 128) {
-    if (mm) hipLaunchKernelGGL((score_kernel<128, true>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
-    else hipLaunchKernelGGL((score_kernel<128, false>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
+    if (mm) hipLaunchKernelGGL((score_kernel<128, true>), dim3(grid), dim3(k2wThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
+    else hipLaunchKernelGGL((score_kernel<128, false>), dim3(grid), dim3(k2wThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
   } else {
-    if (mm) hipLaunchKernelGGL((score_kernel<64, true>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
-    else hipLaunchKernelGGL((score_kernel<64, false>), dim3(grid), dim3(kThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
+    if (mm) hipLaunchKernelGGL((score_kernel<64, true>), dim3(grid), dim3(k2wThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
+    else hipLaunchKernelGGL((score_kernel<64, false>), dim3(grid), dim3(k2wThreads), 0, s, dp, qq, kk, bt, lse, scores, score_part, n, seg_lo, seg_hi);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
