@@ -73,6 +73,11 @@ def parse():
                          "prints a short JSON line instead of the benchmark record.  'copy' "
                          "is the calibration: a plain device-to-device copy of "
                          "COPY_CALIB_BYTES bytes; 'fullmodel' times only the full-model leg")
+    ap.add_argument("--score-data-probe", action="store_true",
+                    help="time the scoring kernel alone on the workload as drawn, then with "
+                         "every K/V and Q element set to bf16 1.0, then to 0 (the same "
+                         "instructions on data that toggles fewer bits): a power-limited "
+                         "kernel runs faster on the latter; prints a JSON line")
     return ap.parse_args()
 
 
@@ -249,6 +254,41 @@ def _graph_us(body, reps_in_graph=10, replays=5):
         b.record()
     torch.cuda.synchronize()
     return _mean_ms(ev, skip=0) * 1e3 / reps_in_graph
+
+
+def run_score_data_probe(reps, bp, dp, bt0, lse, scores, ws, stream):
+    """The scoring kernel alone (actkv_score with the plan flag) on three contents of the
+    same K/V and Q: as drawn (bf16 N(0,1) with spikes), every element 1.0, every element 0.
+    The instructions and memory accesses are the same; only the switching activity of the
+    data differs.  Rounds of `reps` launches per content, interleaved, median per content."""
+    import torch
+    from paper_2609_31395_amd import actkv
+    pp = bp.planned()
+    kv0, q0 = dp.kv.clone(), dp.q.clone()
+    contents = {"drawn": None, "ones": 0x3F80, "zeros": 0}
+    times = {k: [] for k in contents}
+    actkv.plan(bp, ws)
+    for _ in range(3):
+        for name, bits in contents.items():
+            if bits is None:
+                dp.kv.copy_(kv0)
+                dp.q.copy_(q0)
+            else:
+                dp.kv.fill_(bits)
+                dp.q.fill_(bits)
+            actkv.score(pp, dp.q, dp.kv, bt0, lse=lse, out=scores, ws=ws)
+            ev = _event_pairs(reps)
+            for a, b in ev:
+                a.record(stream)
+                actkv.score(pp, dp.q, dp.kv, bt0, lse=lse, out=scores, ws=ws)
+                b.record(stream)
+            torch.cuda.synchronize()
+            times[name] += [a.elapsed_time(b) * 1e3 for a, b in ev]
+    dp.kv.copy_(kv0)
+    dp.q.copy_(q0)
+    return {"score_data_probe": {k: {"median_us": float(np.median(v)),
+                                     "p10_p90": percentiles(v)} for k, v in times.items()},
+            "workload": dp.cfg_name, "launches_per_content": 3 * reps}
 
 
 def run_table1(reps, dev, stream):
@@ -549,12 +589,21 @@ def run_other_configs(reps, dev, stream):
         ms = _mean_ms(ev)
         us = [a.elapsed_time(b) * 1e3 for a, b in ev[1:]]
         tokens = int(dp.seq_lens.astype(np.int64).sum())
+        t_hbm = algorithmic_bytes(dp, qy["num_kept"]) / (HBM_PEAK_GBS * 1e9)
+        t_mfma = score_flops(dp) / (BF16_PEAK_TFLOPS * 1e12)
+        t_valu = score_epilogue_slots(dp) / VALU_SLOTS_PER_S
+        bound = max(t_hbm, t_mfma, t_valu)
         out[name] = {"requests": dp.num_reqs, "cached_tokens": tokens,
                      "action_queries": int(dp.q_lens.sum()), "kept_entries": qy["num_kept"],
                      "step_us": ms * 1e3, "step_us_p10_p90": percentiles(us),
                      "tokens_per_s": tokens / (ms * 1e-3),
-                     "hbm_roofline_frac": algorithmic_bytes(dp, qy["num_kept"])
-                     / (HBM_PEAK_GBS * 1e9) / (ms * 1e-3)}
+                     "hbm_roofline_frac": t_hbm / (ms * 1e-3),
+                     # these batches carry more query rows per cached token than the
+                     # headline (32-128 queries, mean ~80): the bound is the larger of the
+                     # HBM, MFMA and VALU times
+                     "combined_roofline": {"t_hbm_us": t_hbm * 1e6, "t_mfma_us": t_mfma * 1e6,
+                                           "t_valu_us": t_valu * 1e6, "bound_us": bound * 1e6,
+                                           "frac": bound / (ms * 1e-3)}}
         del dp, ws, bt0, bt, free, lse
         torch.cuda.synchronize()
     return out
@@ -803,6 +852,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"profile_stage": "streaming", "reps": K + Wm,
                           "avg_us": (time.perf_counter() - t0) / (K + Wm) * 1e6}))
+        return
+    if args.score_data_probe:
+        print(json.dumps(run_score_data_probe(K, bp, dp, bt0, lse, scores, ws, stream)))
         return
     if args.profile_stage:
         run_stage(args.profile_stage, K + Wm, bp, dp, bts, lse, scores, pooled, kept, free, freed,

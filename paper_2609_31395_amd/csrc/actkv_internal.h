@@ -13,12 +13,22 @@ namespace actkv {
 constexpr int kPageSize = 16;        // slots per page (the only page size built)
 constexpr int kRowsPerChunk = 512;   // query rows (G * n) one scoring pass holds on chip
 constexpr int kKeyTile = 64;         // keys per scoring / LSE pipeline step (4 pages)
-// Scoring cost of one 64-key tile of a segment whose row chunk holds rt 32-row tiles: the
-// work grows with rt, but each tile also pays a fixed share (the K gather, the barrier, the
-// per-key finish) worth about seven 32-row tiles (measured: a 128-row chunk takes ~48% of
-// the time of a 512-row one).  Workgroups split the scoring by this cost.
+// Scoring cost of one 64-key tile of a row chunk, in units of 32 query rows: the scoring
+// kernel adds rows in steps of kScoreRowStep (one 16-row tile in each of its 8 waves), so a
+// chunk of `rows` rows costs its rows rounded up to that step, plus a fixed share per tile
+// (the K gather, the barrier, the per-key finish) worth seven units.  Workgroups split the
+// scoring by this cost.  (Measured on the ragged 32-request batch: rounding to 128-row steps
+// instead of 32 took the scoring from 646 to 602 us; fixed shares of 7 and 10 were equal, 4
+// was slower.)
+constexpr int kScoreRowStep = 128;
 constexpr int kTileCostFixed = 7;
-__host__ __device__ constexpr int64_t score_tile_cost(int64_t rt) { return rt + kTileCostFixed; }
+__host__ __device__ constexpr int64_t score_tile_cost(int64_t units) { return units + kTileCostFixed; }
+// 32-row units of one key tile of a row chunk holding `rows` query rows (a chunk with no
+// row costs what one row costs)
+__host__ __device__ constexpr int64_t chunk_units(int64_t rows) {
+  return ((rows <= 0 ? 1 : rows < kRowsPerChunk ? rows : kRowsPerChunk) + kScoreRowStep - 1) /
+         kScoreRowStep * (kScoreRowStep / 32);
+}
 constexpr int kLseKeysPerBlock = 2048;  // keys one LSE workgroup reduces (32 key tiles)
 constexpr int kMaxPoolWindow = 63;
 

@@ -27,7 +27,7 @@ int64_t request_score_cost(int64_t L, int64_t n, int32_t G, int32_t Hkv) {
   int64_t cost = 0;
   for (int64_t c = 0; c < chunks; ++c) {
     const int64_t rows = M - c * actkv::kRowsPerChunk;
-    const int64_t rt = rows <= 0 ? 1 : ((rows < actkv::kRowsPerChunk ? rows : actkv::kRowsPerChunk) + 31) / 32;
+    const int64_t rt = actkv::chunk_units(rows);
     cost += ntiles * actkv::score_tile_cost(rt) * Hkv;
   }
   return cost;

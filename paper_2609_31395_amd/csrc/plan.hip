@@ -77,7 +77,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
       const int64_t ntiles = ceil_div64(L, kKeyTile);
       for (int c = 0; c < nchunk; ++c) {
         const int rows = M - c * kRowsPerChunk;
-        const int rt = rows <= 0 ? 1 : ceil_div(rows < kRowsPerChunk ? rows : kRowsPerChunk, 32);
+        const int rt = (int)chunk_units(rows);
         cost += ntiles * score_tile_cost(rt) * Hkv;
       }
       lse_blocks = (int32_t)ceil_div64(L, kLseKeysPerBlock);
@@ -121,7 +121,7 @@ __global__ __launch_bounds__(1024) void plan_kernel(DevProblem dp) {
           dp.seg_cost[((int64_t)r * C + c) * Hkv + h] = co;
           if (c < nchunk) {
             const int rows = M - c * kRowsPerChunk;
-            const int rt = rows <= 0 ? 1 : ceil_div(rows < kRowsPerChunk ? rows : kRowsPerChunk, 32);
+            const int rt = (int)chunk_units(rows);
             co += ntiles * score_tile_cost(rt);
           }
         }

@@ -261,6 +261,7 @@ constexpr int k2wThreads = 512;
 constexpr int k2wWaves = k2wThreads / 64;
 constexpr int k2wRowTiles = kRowsPerChunk / kRowTile / k2wWaves;   // 4
 static_assert(k2wRowTiles == 4, "row-tile bookkeeping below");
+static_assert(k2wWaves * kRowTile == kScoreRowStep, "the scoring cost counts rows in these steps");
 constexpr int k2wStages = 4;   // K tiles in LDS (three in flight)
 constexpr int k2wRedBufs = 2;  // per-key partials of a tile are read one tile later
 // Per-key partials of one tile: wave w, lane group g = l/16, key k at
@@ -558,7 +559,7 @@ __global__ __launch_bounds__(k2wThreads, 1) void score_kernel(
     decode_segment(s, C, Hkv, &r, &c, &h);
     const ReqPlan pl = dp.plan[r];
     const int L = pl.L, n = pl.n, M = G * n;
-    const int64_t TC = score_tile_cost(chunk_row_tiles(M, c));
+    const int64_t TC = score_tile_cost(chunk_units(M - (int64_t)c * kRowsPerChunk));
     const int64_t ntiles = ceil_div64(L, kKeyTile);
     int64_t i1 = (c1 - cs + TC - 1) / TC;
     if (i1 > ntiles) i1 = ntiles;
@@ -727,11 +728,11 @@ __global__ __launch_bounds__(kDecMaxWaves * 64) void score_decode_kernel(
   const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int h = (int)blockIdx.y * (int)(blockDim.x / 64) + wv;
   float* res = res_s[wv];
-  // with at most one query a request's cost is Hkv x its 64-key tiles (one row tile), so
-  // one query per request: every tile costs score_tile_cost(1), so
-  // seg_cost[r * Hkv] / (Hkv * score_tile_cost(1)) is the number of tiles before request r
+  // with at most one query per request every key tile costs the same,
+  // score_tile_cost(chunk_units(1)), so seg_cost[r * Hkv] / (Hkv * that cost) is the number
+  // of (request, key tile) pairs before request r
   auto tiles_before = [&](int rr) {
-    return dp.seg_cost[(int64_t)rr * Hkv] / (Hkv * score_tile_cost(1));
+    return dp.seg_cost[(int64_t)rr * Hkv] / (Hkv * score_tile_cost(chunk_units(1)));
   };
   const int64_t total = tiles_before(R);
   const int64_t c0 = total * blockIdx.x / gridDim.x, c1 = total * (blockIdx.x + 1) / gridDim.x;
@@ -859,7 +860,7 @@ hipError_t launch_score_decode(const DevProblem& dp, const HostPlan& hp, const v
   for (int w = 1; w <= kDecMaxWaves; ++w)
     if (hp.Hkv % w == 0) waves = w;
   const unsigned groups = (unsigned)(hp.Hkv / waves);
-  const int64_t tiles = hp.score_cost / (hp.Hkv * score_tile_cost(1));   // (request, key tile) pairs
+  const int64_t tiles = hp.score_cost / (hp.Hkv * score_tile_cost(chunk_units(1)));   // (request, key tile) pairs
   // one resident round of workgroups (equal contiguous shares: a second round would only
   // add a tail), at most one per tile.  Residency per CU is asked once per kernel and
   // workgroup size (it depends on nothing else).
