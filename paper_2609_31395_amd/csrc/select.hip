@@ -754,11 +754,11 @@ __global__ __launch_bounds__(kSelectThreads) void select_compact_kernel(
         const int64_t sr = src_row[jj];
         if (sr < 0) continue;
         to[u] = which * plane + dst_row[jj] * D + ch * 8;
-        v[u] = *reinterpret_cast<const u32x4*>(kv + which * plane + sr * D + ch * 8);
+        v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kv + which * plane + sr * D + ch * 8));
       }
 #pragma unroll
       for (int u = 0; u < kFusedBatch; ++u)
-        if (to[u] >= 0) *reinterpret_cast<u32x4*>(kv + to[u]) = v[u];
+        if (to[u] >= 0) __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(kv + to[u]));
     }
     __syncthreads();   // the tables are rewritten by the next chunk
   }
