@@ -714,51 +714,80 @@ __global__ __launch_bounds__(kSelectThreads) void select_compact_kernel(
   if (pl.skip) return;   // every head keeps everything: the request is left as it is
   __syncthreads();   // the kept indices written above are visible to the workgroup
 
-  // ---- copies: chunks of kFusedRows new slots, resolved to (source, destination) rows in
-  // LDS, then moved in 16-byte pieces (K plane, then V plane)
-  int64_t* src_row = reinterpret_cast<int64_t*>(lds_keys);
-  int64_t* dst_row = src_row + kFusedRows;
+  // ---- copies: chunks of kFusedRows new slots, resolved to (source, destination) element
+  // offsets of the K plane in LDS (only the slots with both, packed in slot order), then
+  // moved in 16-byte pieces (K rows, then V rows).  Whole batches of kFusedBatch pieces per
+  // thread carry no condition, so their loads are in flight together (a condition per piece
+  // made the compiler wait for every outstanding access before each load and store).
+  int64_t* src_off = reinterpret_cast<int64_t*>(lds_keys);
+  int64_t* dst_off = src_off + kFusedRows;
   const int CH = D / 8;
   const int64_t plane = dp.num_pages * kPageSize * Hkv * (int64_t)D;   // K -> V, elements
   const int32_t* bt_row = bt + (int64_t)r * dp.bt_stride;
+  constexpr int kStep = kSelectThreads * kFusedBatch;
 #pragma unroll 1
   for (int j0 = 0; j0 < k; j0 += kFusedRows) {
     const int nj = k - j0 < kFusedRows ? k - j0 : kFusedRows;
+    int64_t src = -1, dst = -1;
     if (tid < nj) {
       const int j = j0 + tid;
       const int t = kout[j];
-      int64_t src = -1, dst = -1;
       if (t >= 0 && t < pl.L) {
         const int64_t page = bt_row[t / kPageSize];
         // pages outside the pool are never dereferenced (the slot is left unwritten)
-        if (page >= 0 && page < dp.num_pages) src = (page * kPageSize + t % kPageSize) * Hkv + h;
+        if (page >= 0 && page < dp.num_pages)
+          src = ((page * kPageSize + t % kPageSize) * Hkv + h) * (int64_t)D;
       }
       const int64_t dpg = free_pages[pl.fresh_off + j / kPageSize];
-      if (dpg >= 0 && dpg < dp.num_pages) dst = (dpg * kPageSize + j % kPageSize) * Hkv + h;
-      src_row[tid] = dst >= 0 ? src : -1;
-      dst_row[tid] = dst;
+      if (dpg >= 0 && dpg < dp.num_pages) dst = ((dpg * kPageSize + j % kPageSize) * Hkv + h) * (int64_t)D;
+    }
+    uint32_t nvalid;
+    const bool valid = src >= 0 && dst >= 0;
+    const uint32_t at = block_excl_count(valid, mm_tmp, &nvalid);
+    if (valid) {
+      src_off[at] = src;
+      dst_off[at] = dst;
     }
     __syncthreads();
-    const int items = 2 * nj * CH;
+    const int half = (int)nvalid * CH, items = 2 * half;
+    auto piece = [&](int it, int64_t* from, int64_t* to) {
+      const bool v_plane = it >= half;
+      const int i = v_plane ? it - half : it;
+      const int64_t add = (v_plane ? plane : 0) + (i % CH) * 8;
+      *from = src_off[i / CH] + add;
+      *to = dst_off[i / CH] + add;
+    };
+    const int full = items / kStep * kStep;
 #pragma unroll 1
-    for (int base = 0; base < items; base += kSelectThreads * kFusedBatch) {
+    for (int base = 0; base < full; base += kStep) {
       u32x4 v[kFusedBatch];
       int64_t to[kFusedBatch];
 #pragma unroll
       for (int u = 0; u < kFusedBatch; ++u) {
-        to[u] = -1;
-        const int it = base + u * kSelectThreads + tid;
-        if (it >= items) continue;
-        const int ch = it % CH, rest = it / CH;
-        const int jj = rest % nj, which = rest / nj;
-        const int64_t sr = src_row[jj];
-        if (sr < 0) continue;
-        to[u] = which * plane + dst_row[jj] * D + ch * 8;
-        v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kv + which * plane + sr * D + ch * 8));
+        int64_t from;
+        piece(base + u * kSelectThreads + tid, &from, &to[u]);
+        v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kv + from));
       }
 #pragma unroll
       for (int u = 0; u < kFusedBatch; ++u)
-        if (to[u] >= 0) __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(kv + to[u]));
+        __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(kv + to[u]));
+    }
+    if (full < items) {
+      u32x4 v[kFusedBatch];
+      int64_t to[kFusedBatch];
+#pragma unroll
+      for (int u = 0; u < kFusedBatch; ++u) {
+        const int it = full + u * kSelectThreads + tid;
+        if (it < items) {
+          int64_t from;
+          piece(it, &from, &to[u]);
+          v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kv + from));
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kFusedBatch; ++u)
+        if (full + u * kSelectThreads + tid < items)
+          __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(kv + to[u]));
     }
     __syncthreads();   // the tables are rewritten by the next chunk
   }
