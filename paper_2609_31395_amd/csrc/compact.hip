@@ -5,15 +5,14 @@
 //
 // compact_gather_kernel: one 256-thread workgroup per group of destination (fresh) pages of
 // one request (grid: page groups of the longest request x requests; the workgroups past a
-// request's own pages copy nothing).  It first resolves every (page, slot, head) to its
-// source slot through the kept indices and the OLD block table (one lookup per thread, into
+// request's own pages return at once).  It first resolves every (page, slot, head) to its
+// source row through the kept indices and the OLD block table (one lookup per thread, into
 // LDS), then streams the rows: each destination page is written contiguously
 // ([slot][head][D] rows, 16 bytes per lane) and each source row is read as one contiguous
 // run.  Destination pages are disjoint from every live page, so all copies are independent
-// and need no ordering among themselves.  The last workgroup of a request to finish its
-// reads of the old row (a per-request counter in the workspace) then copies that row into
-// the freed list and writes the new one, so the rewrite never races a read and costs no
-// launch of its own.
+// and need no ordering among themselves.
+// compact_rewrite_kernel (runs after the gather, same stream): copies the old block-table
+// row into freed_pages and writes the new row, so the gather never races the rewrite.
 #include "device_common.hpp"
 
 namespace actkv {
@@ -31,21 +30,12 @@ __host__ __device__ inline int compact_pages_per_wg(int Hkv) {
   return p < 1 ? 1 : p;
 }
 
-// Every workgroup of request r counts itself once its reads of the old block-table row are
-// done (they have returned: their values are in LDS); the one that completes the count (all
-// gridDim.x of them) rewrites the row once its own copies are issued, and sets the counter
-// back to zero for the next launch on this workspace (the plan kernel zeroes it too).  The
-// count waits for no store, and no workgroup waits for another.
-__device__ __forceinline__ void count_request(const DevProblem& dp, int r, int* s_last) {
-  if (threadIdx.x == 0) *s_last = atomicAdd(&dp.req_done[r], 1) == (int)gridDim.x - 1;
-}
-
 // The copies of destination pages q0 .. of request r (see compact_gather_kernel).
 template <int D, bool kInPlace>
 __device__ __forceinline__ void gather_pages(const DevProblem& dp, int r, const ReqPlan& pl, int q0,
                                              uint16_t* kv, const int32_t* __restrict__ bt,
                                              const int32_t* __restrict__ kept,
-                                             const int32_t* __restrict__ free_pages, int* s_last) {
+                                             const int32_t* __restrict__ free_pages) {
   constexpr int CH = D / 8;                 // 16-byte chunks per row
   static_assert((CH & (CH - 1)) == 0, "chunks per row: a power of two");
   // per (page, slot, head) entry: the source row's element offset in the K plane (-1:
@@ -85,8 +75,6 @@ __device__ __forceinline__ void gather_pages(const DevProblem& dp, int r, const 
     }
   }
   __syncthreads();
-  // every read of the old row by this workgroup is done: count it (fresh-page form)
-  if constexpr (!kInPlace) count_request(dp, r, s_last);
 
   // ---- the entries that copy a row, in ascending order (with unequal head budgets or in
   // place, many slots of a destination page receive nothing; the copy loop skips them):
@@ -198,29 +186,29 @@ __device__ __forceinline__ void rewrite_row(const DevProblem& dp, int r, const R
 // only where that token is not already there.
 template <int D, bool kInPlace>
 __global__ __launch_bounds__(kCompactThreads, kCompactMinWaves) void compact_gather_kernel(
-    DevProblem dp, int r0, uint16_t* kv, int32_t* bt, const int32_t* __restrict__ kept,
-    const int32_t* __restrict__ free_pages, int32_t* __restrict__ freed,
-    int32_t* __restrict__ new_lens) {
+    DevProblem dp, int r0, uint16_t* kv, const int32_t* __restrict__ bt,
+    const int32_t* __restrict__ kept, const int32_t* __restrict__ free_pages) {
   if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
   const int ppw = compact_pages_per_wg(dp.Hkv);
   // request r's destination pages q0 .. q0 + npages - 1 (of its X)
   const int r = r0 + (int)blockIdx.y;
   const ReqPlan pl = dp.plan[r];
   const int q0 = (int)blockIdx.x * ppw;
-  __shared__ int s_last;
-  // past the request's own pages (it has fewer than the grid's longest) there is nothing to
-  // copy; such a workgroup still counts towards the request's block-table rewrite
-  if (q0 < pl.X) {
-    gather_pages<D, kInPlace>(dp, r, pl, q0, kv, bt, kept, free_pages, &s_last);
-  } else if constexpr (!kInPlace) {
-    count_request(dp, r, &s_last);
-  }
-  if constexpr (!kInPlace) {
-    __syncthreads();
-    if (!s_last) return;
-    rewrite_row(dp, r, pl, bt, free_pages, freed, new_lens);
-    if (threadIdx.x == 0) dp.req_done[r] = 0;
-  }
+  if (q0 >= pl.X) return;   // the request has fewer pages than the grid's longest
+  gather_pages<D, kInPlace>(dp, r, pl, q0, kv, bt, kept, free_pages);
+}
+
+// After the gather on the same stream, so the gather always reads the old row.  (Fused
+// into the gather's tail -- the last workgroup of a request, found by a per-request counter,
+// rewriting its row -- the counter's atomics cost more than this launch: 1169 against 1076
+// us per layer of the 48-layer model, 240 against 199 us for the adaptive batch.)
+__global__ __launch_bounds__(256) void compact_rewrite_kernel(DevProblem dp, int r0, int32_t* bt,
+                                                              const int32_t* __restrict__ free_pages,
+                                                              int32_t* __restrict__ freed,
+                                                              int32_t* __restrict__ new_lens) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
+  const int r = r0 + (int)blockIdx.x;
+  rewrite_row(dp, r, dp.plan[r], bt, free_pages, freed, new_lens);
 }
 
 hipError_t launch_compact_range(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
@@ -228,16 +216,20 @@ hipError_t launch_compact_range(const DevProblem& dp, const HostPlan& hp, int r0
                                 const int32_t* free_pages, int32_t* freed, int32_t* new_lens,
                                 hipStream_t s) {
   if (r0 >= r1) return hipSuccess;
-  // at least one workgroup per request, so that every request's row is rewritten
-  const int ppw = compact_pages_per_wg(hp.Hkv);
-  const int64_t gx = max_x > 0 ? (max_x + ppw - 1) / ppw : 1;
-  const dim3 grid((unsigned)gx, (unsigned)(r1 - r0));
-  if (dp.D == 128)
-    hipLaunchKernelGGL((compact_gather_kernel<128, false>), grid, dim3(kCompactThreads), 0, s, dp,
-                       r0, static_cast<uint16_t*>(kv), bt, kept, free_pages, freed, new_lens);
-  else
-    hipLaunchKernelGGL((compact_gather_kernel<64, false>), grid, dim3(kCompactThreads), 0, s, dp,
-                       r0, static_cast<uint16_t*>(kv), bt, kept, free_pages, freed, new_lens);
+  if (max_x > 0) {
+    const int ppw = compact_pages_per_wg(hp.Hkv);
+    const dim3 grid((unsigned)((max_x + ppw - 1) / ppw), (unsigned)(r1 - r0));
+    if (dp.D == 128)
+      hipLaunchKernelGGL((compact_gather_kernel<128, false>), grid, dim3(kCompactThreads), 0, s,
+                         dp, r0, static_cast<uint16_t*>(kv), bt, kept, free_pages);
+    else
+      hipLaunchKernelGGL((compact_gather_kernel<64, false>), grid, dim3(kCompactThreads), 0, s,
+                         dp, r0, static_cast<uint16_t*>(kv), bt, kept, free_pages);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(compact_rewrite_kernel, dim3(r1 - r0), dim3(256), 0, s, dp, r0, bt,
+                     free_pages, freed, new_lens);
   return hipGetLastError();
 }
 
@@ -379,12 +371,10 @@ hipError_t launch_compact_inplace(const DevProblem& dp, const HostPlan& hp, void
     const dim3 grid((unsigned)((hp.max_fresh + ppw - 1) / ppw), (unsigned)hp.R);
     if (dp.D == 128)
       hipLaunchKernelGGL((compact_gather_kernel<128, true>), grid, dim3(kCompactThreads), 0, s,
-                         dp, 0, static_cast<uint16_t*>(kv), bt, new_order, nullptr, nullptr,
-                         nullptr);
+                         dp, 0, static_cast<uint16_t*>(kv), bt, new_order, nullptr);
     else
       hipLaunchKernelGGL((compact_gather_kernel<64, true>), grid, dim3(kCompactThreads), 0, s,
-                         dp, 0, static_cast<uint16_t*>(kv), bt, new_order, nullptr, nullptr,
-                         nullptr);
+                         dp, 0, static_cast<uint16_t*>(kv), bt, new_order, nullptr);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
