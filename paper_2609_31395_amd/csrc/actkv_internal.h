@@ -16,18 +16,22 @@ constexpr int kKeyTile = 64;         // keys per scoring / LSE pipeline step (4 
 // Scoring cost of one 64-key tile of a row chunk, in units of 32 query rows: the scoring
 // kernel adds rows in steps of kScoreRowStep (one 16-row tile in each of its 8 waves), so a
 // chunk of `rows` rows costs its rows rounded up to that step, plus a fixed share per tile
-// (the K gather, the barrier, the per-key finish) worth seven units.  Workgroups split the
-// scoring by this cost.  (Measured on the ragged 32-request batch: rounding to 128-row steps
-// instead of 32 took the scoring from 646 to 602 us; fixed shares of 7 and 10 were equal, 4
-// was slower.)
+// (the K gather, the barrier, the per-key finish) worth five units.  A chunk of at most half
+// a step leaves every other wave idle, one busy wave per SIMD, and costs half a step.
+// Workgroups split the scoring by this cost.  (Measured per workgroup on the ragged batches,
+// a tile of <= 64, 128, 256, 384 and 512 rows takes 0.33, 0.44, 0.62, 0.79 and 1 times the
+// time of a full one, which these costs, 7/21, 9/21, 13/21, 17/21 and 21/21, follow; rounding
+// every chunk to 64-row steps instead was slower.)
 constexpr int kScoreRowStep = 128;
-constexpr int kTileCostFixed = 7;
+constexpr int kTileCostFixed = 5;
 __host__ __device__ constexpr int64_t score_tile_cost(int64_t units) { return units + kTileCostFixed; }
 // 32-row units of one key tile of a row chunk holding `rows` query rows (a chunk with no
 // row costs what one row costs)
 __host__ __device__ constexpr int64_t chunk_units(int64_t rows) {
-  return ((rows <= 0 ? 1 : rows < kRowsPerChunk ? rows : kRowsPerChunk) + kScoreRowStep - 1) /
-         kScoreRowStep * (kScoreRowStep / 32);
+  return rows <= kScoreRowStep / 2
+             ? kScoreRowStep / 64
+             : ((rows < kRowsPerChunk ? rows : kRowsPerChunk) + kScoreRowStep - 1) /
+                   kScoreRowStep * (kScoreRowStep / 32);
 }
 constexpr int kLseKeysPerBlock = 2048;  // keys one LSE workgroup reduces (32 key tiles)
 constexpr int kMaxPoolWindow = 63;
