@@ -203,9 +203,10 @@ hipError_t launch_select_range(const DevProblem& dp, const HostPlan& hp, int r0,
 hipError_t launch_select_side(const DevProblem& dp, const HostPlan& hp, int r0, int r1,
                               const float* scores, float* pooled, int32_t* kept,
                               hipStream_t s);
-// Selection and fresh-page compaction of every request in one kernel (one workgroup per
-// segment; the rewrite of a request by its last workgroup): the results of launch_select
-// then launch_compact.
+// Selection and fresh-page compaction of every request in one kernel (select_compact_splits
+// workgroups per segment, each selecting it and copying a share of its rows; the rewrite of
+// a request by its last workgroup): the results of launch_select then launch_compact.
+int select_compact_splits(const HostPlan& hp, int head_dim);
 hipError_t launch_select_compact(const DevProblem& dp, const HostPlan& hp, const float* scores,
                                  float* pooled, int32_t* kept, void* kv, int32_t* bt,
                                  const int32_t* free_pages, int32_t* freed, int32_t* new_lens,

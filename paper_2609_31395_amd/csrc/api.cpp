@@ -204,12 +204,16 @@ hipError_t run_select(const Ctx& cx, const actkv_problem* p, const float* scores
   return actkv::launch_select(cx.dp, cx.hp, scores, pooled, kept, s);
 }
 
-// Selection and fresh-page compaction fused into one kernel (launch_select_compact) for
-// at most this many segments keeping at most this many entries each: one workgroup per
-// segment then copies its own rows, which only beats the separate selection, gather and
-// rewrite launches when there is little to copy.  Measured on MI355X (Hkv = 8, d = 128):
-// 31-33 against 36 us at 8 and 32 segments of 512 kept entries; 49 against 36 us at 8
-// segments of 1,536, 45 against 42 us at 128 segments of 512.
+// Selection and fresh-page compaction fused into one kernel (launch_select_compact), for
+// batches whose copies are small: with several workgroups per segment when the segments fit
+// its LDS form and the kept rows are few (select_compact_splits > 1), else, for at most this
+// many segments keeping at most this many entries each, with one workgroup per segment that
+// copies its own rows.  Measured on MI355X (Table 1 shapes: Hkv = 8, d = 128, GPU time): one
+// request kept 512 of 1,024 entries in 20 against 26 us (one workgroup per segment), 1,536
+// of 2,048 in 23 against 24 us and 4,096 of 6,144 in 28 against 32 us (selection, gather and
+// rewrite kernels); four requests, 512 of 1,024: 25 against 34 us.  Earlier, with one
+// workgroup per segment: 49 against 36 us at 8 segments of 1,536, 45 against 42 us at 128
+// segments of 512.
 constexpr int64_t kFusedMaxSegments = 32;
 constexpr int64_t kFusedMaxKeptPerSegment = 512;
 
@@ -218,8 +222,9 @@ actkv_status run_select_compact(const Ctx& cx, const actkv_problem* p, const flo
                                 float* pooled, int32_t* kept, void* kv_cache,
                                 int32_t* block_table, const int32_t* free_pages,
                                 int32_t* freed_pages, int32_t* new_lens, hipStream_t s) {
-  if (!(p->flags & ACTKV_FLAG_SMALL_SELECT) && (int64_t)cx.hp.R * cx.hp.Hkv <= kFusedMaxSegments &&
-      cx.hp.max_k <= kFusedMaxKeptPerSegment)
+  const bool small = (int64_t)cx.hp.R * cx.hp.Hkv <= kFusedMaxSegments &&
+                     cx.hp.max_k <= kFusedMaxKeptPerSegment;
+  if (!(p->flags & ACTKV_FLAG_SMALL_SELECT) && (small || actkv::select_compact_splits(cx.hp, cx.dp.D) > 1))
     return hip_status(actkv::launch_select_compact(cx.dp, cx.hp, scores, pooled, kept, kv_cache,
                                                    block_table, free_pages, freed_pages,
                                                    new_lens, s));

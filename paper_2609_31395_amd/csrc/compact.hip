@@ -140,23 +140,21 @@ __device__ __forceinline__ void gather_pages(const DevProblem& dp, int r, const 
     for (int u = 0; u < kBatch; ++u)
       __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(kv + dst[u]));
   }
-  // the last, partial batch
+  // the last, partial batch: items past the end repeat the last one (the same bytes to the
+  // same place), so this batch carries no condition either
   if (full < items) {
     u32x4 v[kBatch];
     int64_t dst[kBatch];
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const int it = full + kCompactThreads * u + (int)threadIdx.x;
-      if (it < items) {
-        int64_t src;
-        chunk_of(it, &src, &dst[u]);
-        v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kv + src));
-      }
+      int64_t src;
+      chunk_of(it < items ? it : items - 1, &src, &dst[u]);
+      v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kv + src));
     }
 #pragma unroll
     for (int u = 0; u < kBatch; ++u)
-      if (full + kCompactThreads * u + (int)threadIdx.x < items)
-        __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(kv + dst[u]));
+      __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(kv + dst[u]));
   }
 }
 

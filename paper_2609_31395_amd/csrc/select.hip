@@ -387,7 +387,8 @@ __device__ __forceinline__ void radix_tau_by(Visit visit, int k, uint32_t lo, ui
 // Kept entries: every key > tau, then the first `need` keys == tau, in index order.  The
 // run's greater / equal flags are kept as bit masks; one workgroup prefix sum of both counts
 // places each thread's kept indices, which are staged in LDS (`idx`, kSelectLdsKeys entries
-// at a time) and written out coalesced.  When vout is given, vout[j] = vsrc[kept[j]] (vsrc in
+// at a time) and written out coalesced (not written when kout is null: k <= kSelectLdsKeys
+// then leaves them all in idx).  When vout is given, vout[j] = vsrc[kept[j]] (vsrc in
 // global memory).  Every read of the keys is done before idx is written: idx may overlay
 // them.
 template <typename Visit>
@@ -420,21 +421,23 @@ __device__ __forceinline__ void emit_kept_by(Visit visit, RunGeom g, uint32_t ta
     for (int pos = pos0; m; ++pos, m &= m - 1)
       if (pos >= b && pos < b + nc) idx[pos - b] = g.t0 + __builtin_ctzll(m);
     __syncthreads();
-    copy_out_u32(nc, reinterpret_cast<const uint32_t*>(idx), kout + b, AsIs());
+    if (kout) copy_out_u32(nc, reinterpret_cast<const uint32_t*>(idx), kout + b, AsIs());
     if (vout) gather_out_f32(nc, idx, vsrc, vout + b);
     __syncthreads();
   }
 }
 
-// TopK of the segment in LDS (0 <= k): indices to kout and, when vout is given, the kept
-// values (vsrc holds the values the keys stand for, in global memory).
+// TopK of the segment in LDS (0 <= k): indices to kout (when given; for 0 < k < L they are
+// also left in LDS, over the keys) and, when vout is given, the kept values (vsrc holds the
+// values the keys stand for, in global memory).
 __device__ __forceinline__ void topk_lds(int L, int k, RunGeom g, uint32_t* keys, uint32_t* hist,
                                          int64_t* scan_tmp, uint32_t* mm_tmp, int* s_bin,
                                          uint32_t* s_above, int32_t* __restrict__ kout,
                                          const float* vsrc, float* __restrict__ vout) {
   if (k <= 0) return;
   if (k >= L) {
-    for (int t = threadIdx.x; t < L; t += kSelectThreads) kout[t] = t;
+    if (kout)
+      for (int t = threadIdx.x; t < L; t += kSelectThreads) kout[t] = t;
     if (vout) copy_out_u32(L, keys, vout, KeyToFloatBits());
     return;
   }
@@ -629,7 +632,8 @@ __device__ __forceinline__ void select_global(int L, int k, int hw, const float*
   }
 }
 
-// The selection of segment (r, h): pooled scores and kept indices.  Returns k.
+// The selection of segment (r, h): pooled scores and kept indices.  Returns k.  For a
+// segment held in LDS (L <= kSelectLdsKeys) either output may be null (not written).
 __device__ __forceinline__ int select_segment(const DevProblem& dp, const ReqPlan& pl, int r,
                                               int h, const float* __restrict__ scores,
                                               float* pooled, int32_t* __restrict__ kout,
@@ -640,7 +644,7 @@ __device__ __forceinline__ int select_segment(const DevProblem& dp, const ReqPla
   const int b = dp.budgets[r * dp.Hkv + h];
   const int k = b < L ? b : L;
   const float* in = scores + pl.seg_off + (int64_t)h * L;
-  float* pout = pooled + pl.seg_off + (int64_t)h * L;
+  float* pout = pooled ? pooled + pl.seg_off + (int64_t)h * L : nullptr;
   const int hw = dp.pool_window / 2;
   if (L <= kSelectLdsKeys)
     select_lds(L, k, hw, in, pout, kout, lds_keys, hist, scan_tmp, mm_tmp, s_bin, s_above);
@@ -673,23 +677,79 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(DevProblem dp, i
 
 // ---- selection and fresh-page compaction in one kernel (small problems) ------------------
 //
-// One 1024-thread workgroup per (request, KV head) selects the segment as select_kernel does,
-// then copies its own head's kept K and V rows to their fresh slots (new slot j of head h is
-// row (j % 16, h) of fresh page j / 16: the heads of a page are disjoint rows, so the
-// workgroups of a request never write the same bytes), and writes the head's new length.
-// The block-table rewrite of a request must follow every read of its old row, so it falls to
-// the request's last workgroup to finish: each workgroup counts itself in a per-request
-// counter once its reads are done, and the one that completes the count rewrites the row
-// and the freed list and sets the counter back to zero for the next launch (the plan kernel
-// zeroes the counters too).  Nothing waits on another workgroup.  Results equal
-// select_kernel then the fresh-page compaction, bit for bit; used where the whole
-// compaction is small enough that a single workgroup per segment copies it faster than the
-// separate launches would (one launch instead of three).
+// Two forms, with results equal to select_kernel then the fresh-page compaction, bit for bit.
+// New slot j of head h is row (j % 16, h) of fresh page j / 16: the heads of a page are
+// disjoint rows, so workgroups of different heads never write the same bytes.
+//
+// select_compact_kernel: one 1024-thread workgroup per (request, KV head) selects the
+// segment as select_kernel does, then copies its own head's kept K and V rows to their fresh
+// slots and writes the head's new length.  The block-table rewrite of a request must follow
+// every read of its old row, so it falls to the request's last workgroup to finish: each
+// workgroup counts itself in a per-request counter once its reads are done, and the one that
+// completes the count rewrites the row and the freed list and sets the counter back to zero
+// for the next launch (the plan kernel zeroes the counters too).  Nothing waits on another
+// workgroup.
+//
+// select_compact_split_kernel: `splits` workgroups per (request, KV head), for batches whose
+// rows are few enough that a copy by whole pages (the separate gather) does not pay for its
+// extra launches.  Each part first copies the request's old block-table row and its own
+// fresh page ids into LDS and counts itself at once (its last read of the row is done), then
+// selects the segment (the same steps on the same scores, so the same entries: selecting it
+// more than once costs nothing the otherwise idle CUs would do), and copies the slots
+// [k p / splits, k (p + 1) / splits) of part p.  Part 0 writes the pooled scores, the kept
+// indices and the new length; every part reads the kept indices from its own LDS, where the
+// selection leaves them.  The counter's round trip and the page-id reads thus overlap the
+// selection, and the copy phase touches global memory only for the rows themselves.
 constexpr int kFusedRows = kSelectThreads;   // destination slots resolved per chunk
 constexpr int kFusedBatch = 8;               // 16-byte loads of a thread in flight together
-// LDS the copy tables overlay on the selection's dynamic LDS: source and destination row
-// of every slot of a chunk.
+// LDS of the copy tables: source and destination row of every slot of a chunk.
 constexpr size_t kFusedLdsBytes = 2 * sizeof(int64_t) * kFusedRows;
+// The split form: segments up to this length (keys, tables and page ids share LDS), at most
+// this many bytes of kept K and V rows in the whole batch, workgroups aimed for (one per
+// CU), at most this many parts, at least this many slots per part.
+constexpr int kSplitMaxKeys = 28672;
+constexpr int64_t kSplitMaxBytes = 32ll << 20;
+constexpr int kSplitTargetGroups = 256;
+constexpr int kMaxSplits = 16;
+constexpr int kSplitMinSlots = 128;
+constexpr int kStaticSelectLds = kMaxBins * 4 + 17 * 8 + 32 * 4 + 16;   // the kernels' own LDS
+static_assert(kSplitMaxKeys <= kSelectLdsKeys, "split segments are selected in LDS");
+
+// Rows n of the chunk tables (src_off[i] -> dst_off[i], element offsets in the K plane) move
+// in 16-byte pieces, K rows then V rows.  Whole batches of kFusedBatch pieces per thread
+// carry no condition, so their loads are in flight together (a condition per piece made the
+// compiler wait for every outstanding access before each load and store); pieces past the
+// end of the last batch repeat the last piece (the same bytes to the same place).
+__device__ __forceinline__ void copy_table_rows(uint16_t* kv, const int64_t* src_off,
+                                                const int64_t* dst_off, int n, int CH,
+                                                int64_t plane) {
+  const int tid = threadIdx.x, half = n * CH, items = 2 * half;
+  auto piece = [&](int it, int64_t* from, int64_t* to) {
+    const bool v_plane = it >= half;
+    const int i = v_plane ? it - half : it;
+    const int64_t add = (v_plane ? plane : 0) + (i % CH) * 8;
+    *from = src_off[i / CH] + add;
+    *to = dst_off[i / CH] + add;
+  };
+  constexpr int kStep = kSelectThreads * kFusedBatch;
+  const int full = items / kStep * kStep;
+#pragma unroll 1
+  for (int base = 0; base < items; base += kStep) {
+    const bool whole = base < full;   // uniform
+    u32x4 v[kFusedBatch];
+    int64_t to[kFusedBatch];
+#pragma unroll
+    for (int u = 0; u < kFusedBatch; ++u) {
+      const int it = base + u * kSelectThreads + tid;
+      int64_t from;
+      piece(whole || it < items ? it : items - 1, &from, &to[u]);
+      v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kv + from));
+    }
+#pragma unroll
+    for (int u = 0; u < kFusedBatch; ++u)
+      __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(kv + to[u]));
+  }
+}
 
 __global__ __launch_bounds__(kSelectThreads) void select_compact_kernel(
     DevProblem dp, const float* __restrict__ scores, float* pooled, int32_t* __restrict__ kept,
@@ -715,16 +775,12 @@ __global__ __launch_bounds__(kSelectThreads) void select_compact_kernel(
   __syncthreads();   // the kept indices written above are visible to the workgroup
 
   // ---- copies: chunks of kFusedRows new slots, resolved to (source, destination) element
-  // offsets of the K plane in LDS (only the slots with both, packed in slot order), then
-  // moved in 16-byte pieces (K rows, then V rows).  Whole batches of kFusedBatch pieces per
-  // thread carry no condition, so their loads are in flight together (a condition per piece
-  // made the compiler wait for every outstanding access before each load and store).
+  // offsets of the K plane in LDS (only the slots with both, packed in slot order; the
+  // tables overlay the selection's keys)
   int64_t* src_off = reinterpret_cast<int64_t*>(lds_keys);
   int64_t* dst_off = src_off + kFusedRows;
-  const int CH = D / 8;
   const int64_t plane = dp.num_pages * kPageSize * Hkv * (int64_t)D;   // K -> V, elements
   const int32_t* bt_row = bt + (int64_t)r * dp.bt_stride;
-  constexpr int kStep = kSelectThreads * kFusedBatch;
 #pragma unroll 1
   for (int j0 = 0; j0 < k; j0 += kFusedRows) {
     const int nj = k - j0 < kFusedRows ? k - j0 : kFusedRows;
@@ -749,46 +805,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_compact_kernel(
       dst_off[at] = dst;
     }
     __syncthreads();
-    const int half = (int)nvalid * CH, items = 2 * half;
-    auto piece = [&](int it, int64_t* from, int64_t* to) {
-      const bool v_plane = it >= half;
-      const int i = v_plane ? it - half : it;
-      const int64_t add = (v_plane ? plane : 0) + (i % CH) * 8;
-      *from = src_off[i / CH] + add;
-      *to = dst_off[i / CH] + add;
-    };
-    const int full = items / kStep * kStep;
-#pragma unroll 1
-    for (int base = 0; base < full; base += kStep) {
-      u32x4 v[kFusedBatch];
-      int64_t to[kFusedBatch];
-#pragma unroll
-      for (int u = 0; u < kFusedBatch; ++u) {
-        int64_t from;
-        piece(base + u * kSelectThreads + tid, &from, &to[u]);
-        v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kv + from));
-      }
-#pragma unroll
-      for (int u = 0; u < kFusedBatch; ++u)
-        __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(kv + to[u]));
-    }
-    if (full < items) {
-      u32x4 v[kFusedBatch];
-      int64_t to[kFusedBatch];
-#pragma unroll
-      for (int u = 0; u < kFusedBatch; ++u) {
-        const int it = full + u * kSelectThreads + tid;
-        if (it < items) {
-          int64_t from;
-          piece(it, &from, &to[u]);
-          v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kv + from));
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kFusedBatch; ++u)
-        if (full + u * kSelectThreads + tid < items)
-          __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(kv + to[u]));
-    }
+    copy_table_rows(kv, src_off, dst_off, (int)nvalid, D / 8, plane);
     __syncthreads();   // the tables are rewritten by the next chunk
   }
 
@@ -804,6 +821,123 @@ __global__ __launch_bounds__(kSelectThreads) void select_compact_kernel(
   for (int i = tid; i < pl.Y; i += kSelectThreads) {
     const int32_t old = row[i];
     freed[pl.freed_off + i] = old;
+    row[i] = i < pl.X ? free_pages[pl.fresh_off + i] : -1;
+  }
+  if (tid == 0) dp.req_done[r] = 0;   // ready for the next launch on this workspace
+}
+
+// LDS of the split form, in 32-bit words from the start of the dynamic LDS: the selection's
+// keys (then the kept indices), the copy tables, the old block-table row, the part's fresh
+// page ids.
+struct SplitLds {
+  int table_off, row_off, fresh_off, words;
+};
+
+__host__ __device__ inline SplitLds split_lds(int64_t max_L, int64_t max_k, int splits) {
+  SplitLds o;
+  o.table_off = (int)((max_L + kLdsPad + 1) / 2 * 2);   // 8-byte aligned
+  o.row_off = o.table_off + (int)(kFusedLdsBytes / sizeof(uint32_t));
+  o.fresh_off = o.row_off + (int)((max_L + kPageSize - 1) / kPageSize);
+  const int64_t part_slots = (max_k + splits - 1) / splits;
+  o.words = o.fresh_off + (int)((part_slots + kPageSize - 1) / kPageSize) + 1;
+  return o;
+}
+
+__global__ __launch_bounds__(kSelectThreads) void select_compact_split_kernel(
+    DevProblem dp, const float* __restrict__ scores, float* pooled, int32_t* __restrict__ kept,
+    uint16_t* kv, int32_t* bt, const int32_t* __restrict__ free_pages,
+    int32_t* __restrict__ freed, int32_t* __restrict__ new_lens, int splits, SplitLds lay) {
+  if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
+  extern __shared__ uint32_t lds_keys[];
+  __shared__ uint32_t hist[kMaxBins];
+  __shared__ int64_t scan_tmp[17];
+  __shared__ uint32_t mm_tmp[32];
+  __shared__ int s_bin;
+  __shared__ uint32_t s_above;
+  __shared__ int s_last;
+
+  const int tid = threadIdx.x;
+  const int h = (int)blockIdx.x / splits, part = (int)blockIdx.x - h * splits;
+  const int r = blockIdx.y, Hkv = dp.Hkv, D = dp.D;
+  const bool lead = part == 0;
+  const ReqPlan pl = dp.plan[r];
+  int32_t* kout = kept + dp.kept_off[r * Hkv + h];
+  if (pl.skip) {   // every head keeps everything: the request is left as it is
+    if (!lead) return;
+    select_segment(dp, pl, r, h, scores, pooled, kout, lds_keys, hist, scan_tmp, mm_tmp,
+                   &s_bin, &s_above);
+    if (tid == 0) new_lens[r * Hkv + h] = pl.L;
+    return;
+  }
+  // this part's new slots (k as select_segment takes it)
+  const int b = dp.budgets[r * Hkv + h];
+  const int kk = b < pl.L ? b : pl.L;
+  const int j_lo = (int)((int64_t)kk * part / splits);
+  const int j_hi = (int)((int64_t)kk * (part + 1) / splits);
+  const int pg_lo = j_lo / kPageSize;
+  const int pg_n = j_hi > j_lo ? (j_hi - 1) / kPageSize - pg_lo + 1 : 0;
+
+  // ---- page ids into LDS, then this workgroup counts itself: its reads of the old row are
+  // done, so the request's last workgroup to count may rewrite the row at any time after
+  int32_t* row_lds = reinterpret_cast<int32_t*>(lds_keys + lay.row_off);
+  int32_t* fresh_lds = reinterpret_cast<int32_t*>(lds_keys + lay.fresh_off);
+  const int32_t* bt_row = bt + (int64_t)r * dp.bt_stride;
+  for (int i = tid; i < pl.Y; i += kSelectThreads) row_lds[i] = bt_row[i];
+  for (int i = tid; i < pg_n; i += kSelectThreads) fresh_lds[i] = free_pages[pl.fresh_off + pg_lo + i];
+  __syncthreads();   // every thread's row reads have returned
+  int ticket = 0;    // thread 0: this workgroup's place in the request's count
+  if (tid == 0) {
+    __threadfence();
+    ticket = atomicAdd(&dp.req_done[r], 1);
+  }
+
+  const int k = select_segment(dp, pl, r, h, scores, lead ? pooled : nullptr,
+                               lead ? kout : nullptr, lds_keys, hist, scan_tmp, mm_tmp, &s_bin,
+                               &s_above);
+  if (lead && tid == 0) new_lens[r * Hkv + h] = k;
+  __syncthreads();   // the kept indices in LDS are complete
+
+  // ---- copies: chunks of kFusedRows new slots of this part, resolved from LDS alone
+  const int32_t* kidx = reinterpret_cast<const int32_t*>(lds_keys);   // for 0 < k < L
+  int64_t* src_off = reinterpret_cast<int64_t*>(lds_keys + lay.table_off);
+  int64_t* dst_off = src_off + kFusedRows;
+  const int64_t plane = dp.num_pages * kPageSize * Hkv * (int64_t)D;   // K -> V, elements
+#pragma unroll 1
+  for (int j0 = j_lo; j0 < j_hi; j0 += kFusedRows) {
+    const int nj = j_hi - j0 < kFusedRows ? j_hi - j0 : kFusedRows;
+    int64_t src = -1, dst = -1;
+    if (tid < nj) {
+      const int j = j0 + tid;
+      const int t = k >= pl.L ? j : kidx[j];
+      if (t >= 0 && t < pl.L) {
+        const int64_t page = row_lds[t / kPageSize];
+        // pages outside the pool are never dereferenced (the slot is left unwritten)
+        if (page >= 0 && page < dp.num_pages)
+          src = ((page * kPageSize + t % kPageSize) * Hkv + h) * (int64_t)D;
+      }
+      const int64_t dpg = fresh_lds[j / kPageSize - pg_lo];
+      if (dpg >= 0 && dpg < dp.num_pages) dst = ((dpg * kPageSize + j % kPageSize) * Hkv + h) * (int64_t)D;
+    }
+    uint32_t nvalid;
+    const bool valid = src >= 0 && dst >= 0;
+    const uint32_t at = block_excl_count(valid, mm_tmp, &nvalid);
+    if (valid) {
+      src_off[at] = src;
+      dst_off[at] = dst;
+    }
+    __syncthreads();
+    copy_table_rows(kv, src_off, dst_off, (int)nvalid, D / 8, plane);
+    __syncthreads();   // the tables are rewritten by the next chunk
+  }
+
+  // ---- the request's last workgroup to count rewrites its row and freed list (the old row
+  // from LDS; every other workgroup read it before counting)
+  if (tid == 0) s_last = ticket == Hkv * splits - 1;
+  __syncthreads();
+  if (!s_last) return;
+  int32_t* row = bt + (int64_t)r * dp.bt_stride;
+  for (int i = tid; i < pl.Y; i += kSelectThreads) {
+    freed[pl.freed_off + i] = row_lds[i];
     row[i] = i < pl.X ? free_pages[pl.fresh_off + i] : -1;
   }
   if (tid == 0) dp.req_done[r] = 0;   // ready for the next launch on this workspace
@@ -1355,11 +1489,37 @@ hipError_t launch_select(const DevProblem& dp, const HostPlan& hp, const float* 
   return launch_select_range(dp, hp, 0, hp.R, scores, pooled, kept, s);
 }
 
+int select_compact_splits(const HostPlan& hp, int head_dim) {
+  const int64_t segs = (int64_t)hp.R * hp.Hkv;
+  if (segs <= 0 || hp.max_L > kSplitMaxKeys || hp.num_kept * 4 * head_dim > kSplitMaxBytes)
+    return 1;
+  int64_t s = kSplitTargetGroups / segs;
+  const int64_t by_slots = (hp.max_k + kSplitMinSlots - 1) / kSplitMinSlots;
+  s = s < by_slots ? s : by_slots;
+  s = s < kMaxSplits ? s : kMaxSplits;
+  return s < 1 ? 1 : (int)s;
+}
+
 hipError_t launch_select_compact(const DevProblem& dp, const HostPlan& hp, const float* scores,
                                  float* pooled, int32_t* kept, void* kv, int32_t* bt,
                                  const int32_t* free_pages, int32_t* freed, int32_t* new_lens,
                                  hipStream_t s) {
   if (hp.R == 0) return hipSuccess;
+  const int splits = select_compact_splits(hp, dp.D);
+  if (splits > 1) {
+    const SplitLds lay = split_lds(hp.max_L, hp.max_k, splits);
+    const size_t lds = (size_t)lay.words * sizeof(uint32_t);
+    if (lds + kStaticSelectLds > 160 * 1024) return hipErrorInvalidValue;   // by the limits above: never
+    if (lds > 64 * 1024) {
+      hipError_t e = hipFuncSetAttribute((const void*)select_compact_split_kernel,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(select_compact_split_kernel, dim3(hp.Hkv * splits, hp.R),
+                       dim3(kSelectThreads), lds, s, dp, scores, pooled, kept,
+                       static_cast<uint16_t*>(kv), bt, free_pages, freed, new_lens, splits, lay);
+    return hipGetLastError();
+  }
   const int64_t keys = hp.max_L < kSelectLdsKeys ? hp.max_L : kSelectLdsKeys;
   size_t lds = (size_t)(keys + kLdsPad) * sizeof(uint32_t);
   if (lds < kFusedLdsBytes) lds = kFusedLdsBytes;

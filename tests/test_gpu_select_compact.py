@@ -1,10 +1,13 @@
 """actkv_select_compact (selection then fresh-page compaction in one call) against
-actkv_select followed by actkv_compact: every output bit-identical, both for problems small
-enough to take the single fused kernel (at most 32 segments keeping at most 512 entries each:
-one workgroup per segment, the block-table rewrite by each request's last workgroup) and for
-larger ones (separate kernels); repeated calls on one planned workspace (the per-request
-counters are left at zero); and the fused path against the oracle's compaction of its own
-selection."""
+actkv_select followed by actkv_compact: every output bit-identical, both for problems that
+take the fused kernel and for larger ones (separate kernels); repeated calls on one planned
+workspace (the per-request counters are left at zero); and the fused path against the
+oracle's compaction of its own selection.  The fused kernel runs with one workgroup per
+segment (at most 32 segments keeping at most 512 entries each), or with several workgroups
+per segment that each select it and copy a share of its rows (segments up to 28,672 entries,
+at most 32 MiB of kept K and V rows, as many parts as keep the batch near one workgroup per
+CU, at least 128 slots per part, at most 16); the block-table rewrite falls to each
+request's last workgroup."""
 import numpy as np
 import pytest
 import torch
@@ -16,7 +19,9 @@ from paper_2609_31395_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-FUSED_MAX_SEGMENTS, FUSED_MAX_K = 32, 512   # the fused kernel's limits
+FUSED_MAX_SEGMENTS, FUSED_MAX_K = 32, 512   # the one-part fused kernel's limits
+SPLIT_MAX_KEYS, SPLIT_MAX_BYTES = 28672, 32 << 20
+SPLIT_GROUPS, SPLIT_MAX, SPLIT_MIN_SLOTS = 256, 16, 128
 
 
 def custom(**kw):
@@ -37,8 +42,18 @@ CASES = {
                                                budgets=[500, 512, 0, 333]),
     "fused_hkv8_32_segments": lambda: custom(seq_lens=[1024] * 4, q_lens=[1] * 4,
                                              num_q_heads=32, num_kv_heads=8, budgets=512),
-    "hkv8_table1_like": lambda: custom(seq_lens=[2048, 2048], q_lens=[1, 1], num_q_heads=32,
-                                       num_kv_heads=8, budgets=1536),
+    "fused_hkv8_table1_like": lambda: custom(seq_lens=[2048, 2048], q_lens=[1, 1],
+                                             num_q_heads=32, num_kv_heads=8, budgets=1536),
+    "fused_one_part": lambda: custom(seq_lens=[900, 37, 2500, 640], q_lens=[7, 1, 20, 3],
+                                     budgets=[30, 50, 10, 37, 128, 1, 120, 100]),
+    "fused_split_keep_all_head": lambda: custom(seq_lens=[300, 700, 129], q_lens=[2, 5, 1],
+                                                budgets=[300, 150, 700, 5, 129, 200]),
+    "fused_split_max_len": lambda: custom(seq_lens=[28672, 1000], q_lens=[2, 1],
+                                          budgets=[8000, 28671, 999, 1000]),
+    "fused_one_part_past_the_split_length": lambda: custom(
+        seq_lens=[28673, 500], q_lens=[1, 1], budgets=[500, 100, 300, 400]),
+    "past_the_split_bytes": lambda: custom(seq_lens=[8192] * 4, q_lens=[1] * 4,
+                                           num_q_heads=32, num_kv_heads=8, budgets=4096),
     "past_the_segment_limit": lambda: custom(seq_lens=[300] * 17, q_lens=[1] * 17,
                                              budgets=100),
     "large": lambda: custom(seq_lens=[35000] * 4, q_lens=[1] * 4, num_q_heads=8,
@@ -46,9 +61,23 @@ CASES = {
 }
 
 
+def _splits(pb):
+    """Workgroups per segment of the fused kernel (1 where it does not split)."""
+    k = np.minimum(pb.budgets.reshape(len(pb.seq_lens), -1), pb.seq_lens[:, None])
+    if int(pb.seq_lens.max()) > SPLIT_MAX_KEYS or int(k.sum()) * 4 * pb.head_dim > SPLIT_MAX_BYTES:
+        return 1
+    s = min(SPLIT_GROUPS // k.size, -(-int(k.max()) // SPLIT_MIN_SLOTS), SPLIT_MAX)
+    return max(s, 1)
+
+
 def _fused(pb):
     k = np.minimum(pb.budgets.reshape(len(pb.seq_lens), -1), pb.seq_lens[:, None])
-    return k.size <= FUSED_MAX_SEGMENTS and int(k.max()) <= FUSED_MAX_K
+    return (k.size <= FUSED_MAX_SEGMENTS and int(k.max()) <= FUSED_MAX_K) or _splits(pb) > 1
+
+
+def test_the_cases_cover_both_fused_forms():
+    fused = [CASES[c]() for c in CASES if c.startswith("fused_")]
+    assert any(_splits(pb) == 1 for pb in fused) and any(_splits(pb) >= 8 for pb in fused)
 
 
 @pytest.fixture(scope="module", autouse=True)
