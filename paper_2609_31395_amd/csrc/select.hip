@@ -351,10 +351,11 @@ __device__ __forceinline__ void seg_key_range(RunGeom g, const uint32_t* keys,
   key_range_by([&](auto f) { visit_run(g, keys, f); }, mm_tmp, lo, hi);
 }
 
-// Radix select over the segment, keys in [lo, hi]: tau, the order key of the k-th largest
-// (0 < k < L), and `need`, how many keys equal to tau are taken.  Digits of up to 11 bits
-// over d = key - lo, within the bit width of the key range, so concentrated values still
-// spread over the whole first histogram.
+// Radix select over the segment, keys in [lo, hi]: tau and `need` such that the kept entries
+// are every key > tau and the first `need` keys equal to tau (0 < k < L): tau is the order
+// key of the k-th largest, or, when a pass finds that its whole bin is kept, the key just
+// below that bin (need 0).  Digits of up to 11 bits over d = key - lo, within the bit width
+// of the key range, so concentrated values still spread over the whole first histogram.
 template <typename Visit>
 __device__ __forceinline__ void radix_tau_by(Visit visit, int k, uint32_t lo, uint32_t hi,
                                              uint32_t* hist, int64_t* scan_tmp, int* s_bin,
@@ -379,6 +380,14 @@ __device__ __forceinline__ void radix_tau_by(Visit visit, int k, uint32_t lo, ui
     need -= *s_above;
     prefix = (prefix << bits) | (uint32_t)*s_bin;
     rem = sh;
+    // every key of the chosen bin is taken: the kept set is then every key from the bin's
+    // lowest possible key up, whatever the digits below, and the passes end early.  (That
+    // key is above lo: otherwise all L keys would be kept, and 0 < k < L here.)
+    if (rem > 0 && hist[*s_bin] == need) {
+      *tau_out = lo + (prefix << rem) - 1u;   // keys > tau: exactly those from the bin up
+      *need_out = 0;
+      return;
+    }
   }
   *tau_out = lo + prefix;
   *need_out = need;
