@@ -830,9 +830,9 @@ def _leg(name, fn, *args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the compression step shards by request and KV head with no exchange, "
-              "see the design notes.", file=sys.stderr)
+        print(f"bench.py: the benchmark runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the compression step would shard by request and KV head with no exchange "
+              "between GPUs.", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2609_31395_amd import actkv

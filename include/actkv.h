@@ -59,7 +59,7 @@ extern "C" {
 typedef enum actkv_status {
   ACTKV_OK = 0,
   ACTKV_ERR_INVALID_ARGUMENT = -1,    /* shapes, lengths, flags or pointers out of contract */
-  ACTKV_ERR_UNSUPPORTED = -2,         /* valid request this build does not handle          */
+  ACTKV_ERR_UNSUPPORTED = -2,         /* valid request the library does not handle         */
   ACTKV_ERR_WORKSPACE_TOO_SMALL = -3, /* workspace_bytes below actkv_query's figure        */
   ACTKV_ERR_OUT_OF_PAGES = -4,        /* free list shorter than the fresh pages needed     */
   ACTKV_ERR_HIP = -5                  /* a HIP launch or runtime call failed               */

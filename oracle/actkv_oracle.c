@@ -31,7 +31,7 @@
  * rounded once to float at the end; pooling and selection then act on those float values,
  * which is also the precision the selection is decided in on the GPU.
  *
- * Readings where the paper is silent (each also listed in the design notes):
+ * Readings where the paper is silent:
  *   - logits are sm_scale * q.k (the paper writes q.k^T with no scale);
  *   - action query j of a request with L cached tokens and n action queries sits at
  *     position L - n + j and, when causal, sees keys t <= L - n + j (itself included);
