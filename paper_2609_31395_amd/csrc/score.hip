@@ -38,6 +38,10 @@ constexpr int kStages = 3;   // K tiles resident in LDS for the LSE pass
 constexpr int kLseThreads = 512;
 constexpr int kLseWaves = kLseThreads / 64;
 constexpr int kLseTilesPerWave = kRowsPerChunk / 32 / kLseWaves;
+// A tile's 16 terms against a shift below the running max are summed as they come while the
+// sum stays at or under this (each term then under 2^64; a 2048-key block adds at most 64
+// such sums per row, far from the fp32 range).
+constexpr float kLseLazyLimit = 18446744073709551616.0f;   // 2^64
 
 // Geometry of one K tile (kKeyTile keys of one KV head) in LDS.  Rows are not padded;
 // instead the 16-byte chunk c of row r sits in slot c ^ (r % kChunks), which keeps both
@@ -962,27 +966,36 @@ __global__ __launch_bounds__(kLseThreads, 1) void lse_partial_kernel(
           f32x16 x = {};
 #pragma unroll
           for (int ks = 0; ks < Gm::kSteps; ++ks) x = mfma32(kreg[ks], qreg[ti][ks], x);
-          // the running max on the raw dot products (alpha > 0 keeps the order), then
-          // 2^(alpha x - m) with the scale and the shift in one FMA
-          float mx = -__builtin_inff();
           if (masked) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
               const int key = keybase + 8 * (v / 4) + (v % 4);
               x[v] = key <= pos[ti] ? x[v] : -__builtin_inff();
-              mx = fmaxf(mx, x[v]);
             }
-          } else {
+          }
+          // 2^(alpha x - m) with the scale and the shift in one FMA, first against the
+          // running shift m0 as it stands: while no term of the tile exceeds 2^64 the
+          // (shift, sum) pair stays exact to rounding whether or not m0 is the running max,
+          // so the max is taken (on the raw dot products: alpha > 0 keeps the order) only
+          // for a row's first tile and when a larger value arrives
+          const float m0 = rm[ti];
+          float sum = 0.f;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) sum += fast_exp2(__builtin_fmaf(x[v], alpha, -m0));
+          if (sum <= kLseLazyLimit) {
+            rs[ti] += sum;
+          } else {   // also the first tile (m0 = -inf gives inf or NaN terms)
+            float mx = -__builtin_inff();
 #pragma unroll
             for (int v = 0; v < 16; ++v) mx = fmaxf(mx, x[v]);
-          }
-          const float m = fmaxf(rm[ti], mx * alpha);
-          if (m != -__builtin_inff()) {
-            float sum = rs[ti] * fast_exp2(rm[ti] - m);
+            const float m = fmaxf(m0, mx * alpha);
+            if (m != -__builtin_inff()) {
+              float s2 = rs[ti] * fast_exp2(m0 - m);
 #pragma unroll
-            for (int v = 0; v < 16; ++v) sum += fast_exp2(__builtin_fmaf(x[v], alpha, -m));
-            rs[ti] = sum;
-            rm[ti] = m;
+              for (int v = 0; v < 16; ++v) s2 += fast_exp2(__builtin_fmaf(x[v], alpha, -m));
+              rs[ti] = s2;
+              rm[ti] = m;
+            }
           }
         }
       }
