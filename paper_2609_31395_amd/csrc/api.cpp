@@ -224,7 +224,8 @@ actkv_status run_select_compact(const Ctx& cx, const actkv_problem* p, const flo
                                 int32_t* freed_pages, int32_t* new_lens, hipStream_t s) {
   const bool small = (int64_t)cx.hp.R * cx.hp.Hkv <= kFusedMaxSegments &&
                      cx.hp.max_k <= kFusedMaxKeptPerSegment;
-  if (!(p->flags & ACTKV_FLAG_SMALL_SELECT) && (small || actkv::select_compact_splits(cx.hp, cx.dp.D) > 1))
+  const bool split = actkv::select_compact_splits(cx.hp, cx.dp.D) > 1;
+  if (!(p->flags & ACTKV_FLAG_SMALL_SELECT) && (small || split))
     return hip_status(actkv::launch_select_compact(cx.dp, cx.hp, scores, pooled, kept, kv_cache,
                                                    block_table, free_pages, freed_pages,
                                                    new_lens, s));
