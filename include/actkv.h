@@ -29,10 +29,14 @@
  *    concatenated in (r, h) order; segment (r, h) holds k_rh = min(budget_rh, L_r)
  *    entries.
  *  - Ownership: the caller owns every buffer, including the workspace whose size
- *    actkv_query reports.  The library allocates and frees nothing and keeps no pointer
- *    after a call returns.  Its only process-wide state is a cache of per-kernel occupancy
- *    figures (written once per kernel, with atomics; the same for every gfx950 device), so
- *    concurrent calls are safe as long as their buffers do not overlap.
+ *    actkv_query reports.  The library allocates no device memory and keeps no pointer to
+ *    a caller's buffer after a call returns.  Its process-wide state: caches of the CU count
+ *    per device and of per-kernel occupancy figures (written once, with atomics), the
+ *    kernels' dynamic-LDS limits (set before a launch that needs more than 64 KiB), the
+ *    overlap setting of actkv_set_overlap, a second stream and its events per device
+ *    (created the first time a step is pipelined), and actkv_step_noalloc's static device
+ *    array.  Concurrent calls are safe as long as their buffers do not overlap (calls of
+ *    actkv_step_noalloc on one device share its array: see there).
  *  - Asynchrony: each call validates its arguments on the host, then enqueues kernels on
  *    `stream` (a hipStream_t; NULL is the default stream) and returns without
  *    synchronising.  Outputs are valid once the stream reaches that point.
