@@ -87,7 +87,7 @@ __device__ __forceinline__ uint32_t wave_kth_key(uint32_t key, int need) {
 #pragma unroll
   for (int b = 31; b >= 0; --b) {
     const uint32_t t = p | (1u << b);
-    if (__popcll(__ballot(key >= t)) >= need) p = t;
+    if ((int)__popcll(__ballot(key >= t)) >= need) p = t;
   }
   return p;
 }

@@ -136,7 +136,7 @@ struct RunGeom {
 
 __device__ __forceinline__ RunGeom run_geom(int L) {
   const int per = ((L + kSelectThreads - 1) / kSelectThreads) | 1;
-  const int t0 = threadIdx.x * per < L ? threadIdx.x * per : L;
+  const int t0 = (int)threadIdx.x * per < L ? (int)threadIdx.x * per : L;
   const int t1 = t0 + per < L ? t0 + per : L;
   return RunGeom{t0, t1 - t0};
 }
@@ -343,12 +343,6 @@ __device__ __forceinline__ void key_range_by(Visit visit, uint32_t* mm_tmp, uint
     kmax = max(kmax, kk);
   });
   block_min_max(kmin, kmax, mm_tmp, lo, hi);
-}
-
-// Smallest and largest order key of the segment in LDS.
-__device__ __forceinline__ void seg_key_range(RunGeom g, const uint32_t* keys,
-                                              uint32_t* mm_tmp, uint32_t* lo, uint32_t* hi) {
-  key_range_by([&](auto f) { visit_run(g, keys, f); }, mm_tmp, lo, hi);
 }
 
 // Radix select over the segment, keys in [lo, hi]: tau and `need` such that the kept entries
@@ -974,7 +968,6 @@ __global__ __launch_bounds__(kSelectThreads) void select_compact_split_kernel(
 namespace {
 
 constexpr int kSideThreads = 512;
-constexpr int kSideWaves = kSideThreads / 64;
 constexpr int kSidePer = 8;                            // entries per thread and tile
 constexpr int kSideTile = kSideThreads * kSidePer;     // 4096
 constexpr int kSideHalo = kMaxPoolWindow / 2;          // widest pooling half-window
