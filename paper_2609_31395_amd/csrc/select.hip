@@ -836,15 +836,18 @@ struct SplitLds {
   int table_off, row_off, fresh_off, words;
 };
 
-__host__ __device__ inline SplitLds split_lds(int64_t max_L, int64_t max_k, int splits) {
-  SplitLds o;
-  o.table_off = (int)((max_L + kLdsPad + 1) / 2 * 2);   // 8-byte aligned
-  o.row_off = o.table_off + (int)(kFusedLdsBytes / sizeof(uint32_t));
-  o.fresh_off = o.row_off + (int)((max_L + kPageSize - 1) / kPageSize);
+__host__ __device__ constexpr SplitLds split_lds(int64_t max_L, int64_t max_k, int splits) {
+  const int table_off = (int)((max_L + kLdsPad + 1) / 2 * 2);   // 8-byte aligned
+  const int row_off = table_off + (int)(kFusedLdsBytes / sizeof(uint32_t));
+  const int fresh_off = row_off + (int)((max_L + kPageSize - 1) / kPageSize);
   const int64_t part_slots = (max_k + splits - 1) / splits;
-  o.words = o.fresh_off + (int)((part_slots + kPageSize - 1) / kPageSize) + 1;
-  return o;
+  return SplitLds{table_off, row_off, fresh_off,
+                  fresh_off + (int)((part_slots + kPageSize - 1) / kPageSize) + 1};
 }
+// the largest layout (two parts of the longest segment, everything kept) fits one CU's LDS
+static_assert(split_lds(kSplitMaxKeys, kSplitMaxKeys, 2).words * sizeof(uint32_t) +
+                  kStaticSelectLds <= 160 * 1024,
+              "the split form's LDS fits a workgroup");
 
 __global__ __launch_bounds__(kSelectThreads) void select_compact_split_kernel(
     DevProblem dp, const float* __restrict__ scores, float* pooled, int32_t* __restrict__ kept,
