@@ -1,6 +1,8 @@
-"""Layers back to back with layer l's compaction on a second stream, beside layer l+1's
-plan, scoring and selection (the schedule the benchmark's full-model leg also times):
-every output equals the one-stream sequence of actkv_step calls, bit for bit.
+"""Layers back to back on two streams, every output equal to the one-stream sequence of
+actkv_step calls, bit for bit, for two schedules: layer l's selection and compaction on the
+second stream beside layer l+1's plan and scoring (the schedule the benchmark's full-model
+leg times), and layer l's compaction alone there, beside layer l+1's plan, scoring and
+selection.
 
 Four layers of the full-model workload (32 requests of 16K-64K tokens, per-layer
 Dirichlet budgets) over one page pool; every layer takes its fresh pages from the pool's
@@ -28,7 +30,8 @@ def _binding(dp, dev):
                          causal=dp.causal).to_device(dev)
 
 
-def test_layer_pipeline_matches_sequential_steps():
+@pytest.mark.parametrize("side_work", ["select_and_compact", "compact"])
+def test_layer_pipeline_matches_sequential_steps(side_work):
     dev = torch.device("cuda:0")
     layers = W.make_device_model("model48x32", device=dev, num_layers=LAYERS)
     kv = layers[0].kv
@@ -63,16 +66,19 @@ def test_layer_pipeline_matches_sequential_steps():
     kv_ref = kv.clone()
     kv.copy_(kv0)
 
-    # two streams: compaction of layer l beside layer l+1
+    # two streams: layer l's tail on the second stream beside layer l+1
     main = torch.cuda.current_stream()
-    side = torch.cuda.Stream(device=dev)
+    side = torch.cuda.Stream(device=dev)   # default priority
     got = [buffers(c) for c in ctx]
     side.wait_stream(main)
     for c, b in zip(ctx, got):
         pp = c["bp"].planned()
         actkv.plan(c["bp"], c["ws"], stream=main)
         actkv.score(pp, c["q"], kv, b["bt"], lse=c["lse"], out=b["sc"], ws=c["ws"], stream=main)
-        actkv.select(pp, b["sc"], pooled=b["po"], kept=b["kept"], ws=c["ws"], stream=main)
+        sel_stream = side if side_work == "select_and_compact" else main
+        if side_work == "select_and_compact":
+            side.wait_stream(main)
+        actkv.select(pp, b["sc"], pooled=b["po"], kept=b["kept"], ws=c["ws"], stream=sel_stream)
         side.wait_stream(main)
         actkv.compact(pp, kv, b["bt"], b["kept"], spare, freed=b["freed"], new_lens=b["lens"],
                       ws=c["ws"], stream=side)
