@@ -22,6 +22,7 @@ constexpr int kCompactThreads = 256;
 constexpr int kCompactMinWaves = 7;
 constexpr int kCompactTable = 1024;   // (page, slot, head) source entries per workgroup
 constexpr int kCompactBatch = 8;      // 16-byte loads of a thread in flight together
+constexpr int kRewriteBatch = 8;      // block-table entries a rewrite thread reads together
 
 // Fresh pages handled by one workgroup: enough (page, slot, head) rows to give every
 // thread one source lookup, at least one page.
@@ -169,12 +170,33 @@ __device__ __forceinline__ void rewrite_row(const DevProblem& dp, int r, const R
     const int b = dp.budgets[r * Hkv + h];
     new_lens[r * Hkv + h] = pl.skip ? pl.L : (b < pl.L ? b : pl.L);
   }
-  if (pl.skip) return;
+  if (pl.skip || pl.Y <= 0) return;
+  // batches of kRewriteBatch entries per thread: every load of a batch is issued before its
+  // stores (an entry is read and written by the same thread only), and the loads carry no
+  // condition (indices past the row re-read its last entry, values unused), so they are in
+  // flight together instead of one round trip per entry
   int32_t* row = bt + (int64_t)r * dp.bt_stride;
-  for (int i = threadIdx.x; i < pl.Y; i += blockDim.x) {
-    const int32_t old = row[i];
-    freed[pl.freed_off + i] = old;
-    row[i] = i < pl.X ? free_pages[pl.fresh_off + i] : -1;
+  const int last = pl.Y - 1;
+  // the fresh page ids (a request that takes none, every head keeping nothing, reads its own
+  // row instead and writes -1)
+  const int32_t* fresh = pl.X > 0 ? free_pages + pl.fresh_off : row;
+  const int fresh_last = pl.X > 0 ? pl.X - 1 : last;
+  for (int i0 = threadIdx.x; i0 < pl.Y; i0 += kRewriteBatch * (int)blockDim.x) {
+    int32_t old[kRewriteBatch], now[kRewriteBatch];
+#pragma unroll
+    for (int u = 0; u < kRewriteBatch; ++u) {
+      const int i = i0 + u * (int)blockDim.x;
+      old[u] = row[i < last ? i : last];
+      now[u] = fresh[i < fresh_last ? i : fresh_last];
+    }
+#pragma unroll
+    for (int u = 0; u < kRewriteBatch; ++u) {
+      const int i = i0 + u * (int)blockDim.x;
+      if (i < pl.Y) {
+        freed[pl.freed_off + i] = old[u];
+        row[i] = i < pl.X ? now[u] : -1;
+      }
+    }
   }
 }
 
