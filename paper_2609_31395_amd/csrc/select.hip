@@ -1052,7 +1052,7 @@ __device__ __forceinline__ void side_append(bool take, uint32_t key, uint32_t* l
 
 }  // namespace
 
-__global__ __launch_bounds__(kSideThreads, 7) void select_side_kernel(
+__global__ __launch_bounds__(kSideThreads, 6) void select_side_kernel(
     DevProblem dp, int r0, const float* __restrict__ scores, float* pooled,
     int32_t* __restrict__ kept) {
   if (!plan_ok(dp)) return;   // the workspace holds another problem's plan
